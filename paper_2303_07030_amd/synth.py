@@ -1,0 +1,261 @@
+"""Seeded synthetic inputs shaped like the paper's sparse workloads.
+
+This module only *draws inputs*: sparsity patterns, values and dense operands.
+It holds none of the gradient arithmetic, so the oracle and the HIP path can
+both be fed from it without sharing any of the method.
+
+The paper evaluates on SuiteSparse matrices and on random matrices of varying
+density and dimension (Section "Experimental Results", Table of real-world
+matrices and the synthetic sweeps).  Those matrices are not available here, so
+every workload is synthetic, at the shapes below:
+
+  spmv  1,000 x 1,000 CSR, 10,000 uniform-random positions, values N(0,1);
+        dense x (1,000) N(0,1).
+  spmm  100,000 x 100,000 CSR, 1M nnz, row lengths from a Zipf(s=1.1) profile
+        capped at 5,000, uniform columns, values N(0,1); dense B 100,000 x 64.
+  mf    1,000,000 x 500,000 COO, 50M unique (row, col) pairs drawn i.i.d. from
+        truncated Zipf(1.1) on each axis, values U(1,5); U, V with 128 columns
+        ~ N(0, 0.1^2).
+  cp    10,000^3 COO 3-tensor, 20M unique uniform coordinates, values N(0,1);
+        three 10,000 x 32 factors ~ N(0, 0.1^2).
+  gnn   2,400,000-node power-law graph, 60M edges (out-degree Zipf profile
+        s=1.05), weights U[0,1); H and G 2,400,000 x 256 ~ N(0,1).
+
+Seeds: numpy PCG64 streams from SeedSequence(entropy=230307030,
+spawn_key=(workload id, replicate)); each workload spawns five child streams
+used in a fixed order: pattern, values, dense 1, dense 2, dense 3.
+
+Zipf readings (the workload text only says "Zipf(s)"):
+  * row-length profiles: l_r = min(cap, floor(c * r^-s)) over ranks
+    r = 1..nrows with c found by bisection so that the lengths sum to nnz;
+    the remainder goes +1 to the uncapped ranks with the largest fractional
+    part; ranks map to row ids through a seeded permutation.
+  * per-entry indices (mf): i.i.d. draws from the truncated discrete Zipf on
+    ranks 1..N by inverse CDF, with a seeded rank -> id permutation per axis;
+    pairs are deduplicated by first occurrence.
+  * N(0, 0.1) means standard deviation 0.1.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+ENTROPY = 230307030
+WORKLOAD_IDS = {"spmv": 1, "spmm": 2, "mf": 3, "cp": 4, "gnn": 5}
+
+# Full-size workloads and smaller variants of the same recipes that the
+# oracle finishes in seconds (they still span many tiles and ragged tails).
+PRESETS = {
+    "spmv": {"full": dict(nrows=1000, ncols=1000, nnz=10_000)},
+    "spmm": {
+        "full": dict(n=100_000, nnz=1_000_000, s=1.1, cap=5000, k=64),
+        "small": dict(n=3000, nnz=30_000, s=1.1, cap=600, k=64),
+    },
+    "mf": {
+        "full": dict(nrows=1_000_000, ncols=500_000, nnz=50_000_000, s=1.1, k=128),
+        "small": dict(nrows=4000, ncols=2500, nnz=60_000, s=1.1, k=128),
+    },
+    "cp": {
+        "full": dict(dim=10_000, nnz=20_000_000, rank=32),
+        "small": dict(dim=60, nnz=25_000, rank=32),
+    },
+    "gnn": {
+        "full": dict(n=2_400_000, nnz=60_000_000, s=1.05, k=256),
+        "small": dict(n=5000, nnz=70_000, s=1.05, k=256),
+    },
+}
+
+
+def streams(workload: str, replicate: int = 0):
+    """Five independent generators: pattern, values, dense1, dense2, dense3."""
+    ss = np.random.SeedSequence(entropy=ENTROPY,
+                                spawn_key=(WORKLOAD_IDS[workload], replicate))
+    return [np.random.Generator(np.random.PCG64(c)) for c in ss.spawn(5)]
+
+
+def zipf_lengths(nrows: int, nnz: int, s: float, cap: int) -> np.ndarray:
+    """Row-length profile by rank: min(cap, floor(c r^-s)) summing to nnz."""
+    if cap * nrows < nnz:
+        raise ValueError("cap * nrows < nnz")
+    w = np.arange(1, nrows + 1, dtype=np.float64) ** (-s)
+
+    def total(c):
+        return np.minimum(cap, c * w).sum()
+
+    lo, hi = 0.0, cap / w[-1]
+    for _ in range(200):
+        mid = 0.5 * (lo + hi)
+        if total(mid) <= nnz:
+            lo = mid
+        else:
+            hi = mid
+    real = np.minimum(cap, lo * w)
+    lens = np.floor(real).astype(np.int64)
+    rem = nnz - int(lens.sum())
+    uncapped = np.nonzero(real < cap)[0]
+    frac = real[uncapped] - lens[uncapped]
+    order = np.lexsort((uncapped, -frac))  # largest fraction first, then rank
+    lens[uncapped[order[:rem]]] += 1
+    assert int(lens.sum()) == nnz and lens.max() <= cap
+    return lens
+
+
+def _rows_without_replacement(rng, lengths: np.ndarray, ncols: int):
+    """Sorted, distinct uniform columns for each row; returns rowptr, colind."""
+    nrows = lengths.shape[0]
+    rowptr = np.zeros(nrows + 1, dtype=np.int64)
+    np.cumsum(lengths, out=rowptr[1:])
+    colind = np.empty(int(rowptr[-1]), dtype=np.int32)
+    big = min(4096, max(1, ncols // 8))
+    small_rows = np.nonzero((lengths > 0) & (lengths <= big))[0]
+    big_rows = np.nonzero(lengths > big)[0]
+    # short rows: all at once, redraw collisions until every row is distinct
+    ls = lengths[small_rows]
+    rows_rep = np.repeat(small_rows.astype(np.int64), ls)
+    cols = rng.integers(0, ncols, size=rows_rep.shape[0], dtype=np.int64)
+    while True:
+        key = rows_rep * ncols + cols
+        order = np.argsort(key, kind="stable")
+        ks = key[order]
+        dup = np.zeros(key.shape[0], dtype=bool)
+        dup[order[1:][ks[1:] == ks[:-1]]] = True
+        ndup = int(dup.sum())
+        if ndup == 0:
+            break
+        cols[dup] = rng.integers(0, ncols, size=ndup, dtype=np.int64)
+    key = rows_rep * ncols + cols
+    cols_sorted = (np.sort(key) % ncols).astype(np.int32)
+    starts = np.zeros(small_rows.shape[0], dtype=np.int64)
+    if ls.shape[0] > 1:
+        np.cumsum(ls[:-1], out=starts[1:])
+    offs = np.arange(rows_rep.shape[0], dtype=np.int64) - np.repeat(starts, ls)
+    pos = np.repeat(rowptr[small_rows], ls) + offs
+    colind[pos] = cols_sorted
+    # long rows one by one (numpy picks a set-based or permutation method)
+    for r in big_rows:
+        c = rng.choice(ncols, size=int(lengths[r]), replace=False)
+        c.sort()
+        colind[rowptr[r]:rowptr[r + 1]] = c
+    return rowptr.astype(np.int32), colind
+
+
+def _power_law_csr(rng, n: int, nnz: int, s: float, cap: int):
+    lens_by_rank = zipf_lengths(n, nnz, s, cap)
+    row_of_rank = rng.permutation(n)
+    lengths = np.empty(n, dtype=np.int64)
+    lengths[row_of_rank] = lens_by_rank
+    return _rows_without_replacement(rng, lengths, n)
+
+
+def _normal(rng, shape, std=1.0):
+    x = rng.standard_normal(size=shape, dtype=np.float32)
+    if std != 1.0:
+        x *= np.float32(std)
+    return x
+
+
+def _zipf_ids(rng, u_count: int, N: int, s: float, rank_to_id: np.ndarray):
+    cdf = np.cumsum(np.arange(1, N + 1, dtype=np.float64) ** (-s))
+    cdf /= cdf[-1]
+    u = rng.random(u_count)
+    rank = np.minimum(np.searchsorted(cdf, u, side="right"), N - 1)
+    return rank_to_id[rank]
+
+
+def _dedupe_first(draw_batch, nnz: int):
+    """Keep the first nnz distinct int64 keys in first-occurrence order."""
+    seen = np.empty(0, dtype=np.int64)
+    out = []
+    count = 0
+    while count < nnz:
+        keys = draw_batch()
+        uk, first = np.unique(keys, return_index=True)
+        if seen.shape[0]:
+            pos = np.minimum(np.searchsorted(seen, uk), seen.shape[0] - 1)
+            new = seen[pos] != uk
+            uk, first = uk[new], first[new]
+        take = min(uk.shape[0], nnz - count)
+        order = np.argsort(first, kind="stable")[:take]
+        out.append(uk[order])
+        count += take
+        if count < nnz:
+            seen = np.sort(np.concatenate([seen, uk[order]]), kind="stable")
+    return np.concatenate(out)
+
+
+# ---------------------------------------------------------------- workloads
+
+def make_spmv(nrows=1000, ncols=1000, nnz=10_000, replicate=0):
+    g_pat, g_val, g_d1, _, _ = streams("spmv", replicate)
+    keys = np.sort(g_pat.choice(nrows * ncols, size=nnz, replace=False))
+    row = (keys // ncols).astype(np.int32)
+    colind = (keys % ncols).astype(np.int32)
+    rowptr = np.zeros(nrows + 1, dtype=np.int32)
+    np.cumsum(np.bincount(row, minlength=nrows), out=rowptr[1:])
+    return dict(workload="spmv", nrows=nrows, ncols=ncols, rowptr=rowptr,
+                colind=colind, val=_normal(g_val, nnz), x=_normal(g_d1, ncols))
+
+
+def make_spmm(n=100_000, nnz=1_000_000, s=1.1, cap=5000, k=64, replicate=0):
+    g_pat, g_val, g_d1, _, _ = streams("spmm", replicate)
+    rowptr, colind = _power_law_csr(g_pat, n, nnz, s, cap)
+    return dict(workload="spmm", nrows=n, ncols=n, rowptr=rowptr, colind=colind,
+                val=_normal(g_val, nnz), B=_normal(g_d1, (n, k)), k=k)
+
+
+def make_mf(nrows=1_000_000, ncols=500_000, nnz=50_000_000, s=1.1, k=128,
+            replicate=0, batch=20_000_000):
+    g_pat, g_val, g_d1, g_d2, _ = streams("mf", replicate)
+    row_ids = g_pat.permutation(nrows)
+    col_ids = g_pat.permutation(ncols)
+    batch = min(batch, max(4 * nnz, 1024))
+
+    def draw():
+        r = _zipf_ids(g_pat, batch, nrows, s, row_ids).astype(np.int64)
+        c = _zipf_ids(g_pat, batch, ncols, s, col_ids).astype(np.int64)
+        return r * ncols + c
+
+    keys = _dedupe_first(draw, nnz)
+    val = (np.float32(1.0) + np.float32(4.0) * g_val.random(nnz, dtype=np.float32))
+    return dict(workload="mf", nrows=nrows, ncols=ncols,
+                row=(keys // ncols).astype(np.int32),
+                col=(keys % ncols).astype(np.int32), val=val,
+                U=_normal(g_d1, (nrows, k), 0.1), V=_normal(g_d2, (ncols, k), 0.1),
+                k=k)
+
+
+def make_cp(dim=10_000, nnz=20_000_000, rank=32, replicate=0):
+    g_pat, g_val, g_d1, g_d2, g_d3 = streams("cp", replicate)
+    draws = nnz + nnz // 20 + 64
+
+    def draw():
+        i = g_pat.integers(0, dim, size=draws, dtype=np.int64)
+        j = g_pat.integers(0, dim, size=draws, dtype=np.int64)
+        kk = g_pat.integers(0, dim, size=draws, dtype=np.int64)
+        return (i * dim + j) * dim + kk
+
+    keys = _dedupe_first(draw, nnz)
+    return dict(workload="cp", dims=(dim, dim, dim),
+                i=(keys // (dim * dim)).astype(np.int32),
+                j=((keys // dim) % dim).astype(np.int32),
+                k=(keys % dim).astype(np.int32),
+                val=_normal(g_val, nnz),
+                F1=_normal(g_d1, (dim, rank), 0.1), F2=_normal(g_d2, (dim, rank), 0.1),
+                F3=_normal(g_d3, (dim, rank), 0.1), rank=rank)
+
+
+def make_gnn(n=2_400_000, nnz=60_000_000, s=1.05, k=256, replicate=0):
+    g_pat, g_val, g_d1, g_d2, _ = streams("gnn", replicate)
+    rowptr, colind = _power_law_csr(g_pat, n, nnz, s, n)
+    return dict(workload="gnn", nrows=n, ncols=n, rowptr=rowptr, colind=colind,
+                val=g_val.random(nnz, dtype=np.float32),
+                H=_normal(g_d1, (n, k)), G=_normal(g_d2, (n, k)), k=k)
+
+
+MAKERS = {"spmv": make_spmv, "spmm": make_spmm, "mf": make_mf, "cp": make_cp,
+          "gnn": make_gnn}
+
+
+def make(workload: str, size: str = "full", replicate: int = 0, **over):
+    params = dict(PRESETS[workload][size])
+    params.update(over)
+    return MAKERS[workload](replicate=replicate, **params)
