@@ -1,0 +1,234 @@
+/*
+ * nsd.h -- C ABI of libnsd, sparse tensor expressions and their gradients on
+ * AMD MI355X (gfx950), keeping sparsity.
+ *
+ * The problem statement follows the paper's `gradient e x` (Section 4.3, the
+ * gradient API figure): a sparse tensor, dense operands and an upstream
+ * gradient go in; the loss and the gradients come out.  The gradient with
+ * respect to a sparse operand lives only on that operand's stored keys,
+ * because `onehot` iterates the stored keys alone; it is returned as a value
+ * array aligned 1:1 with the operand's own storage order, so its pattern is
+ * the input pattern by construction.  Gradients with respect to dense operands
+ * are transposed sparse x dense products.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Pointers.  Every array argument is a DEVICE pointer unless the comment says
+ *   "host".  The caller owns all memory; the library never allocates, never
+ *   frees, and keeps no pointer after the call returns.
+ * Outputs.  Destination-passing style (Section 5.5): outputs are caller
+ *   buffers that are fully overwritten.  An output element that receives no
+ *   contribution (an empty row or column, nnz = 0) is written as 0, the value
+ *   of an empty sum.
+ * Formats (the physical storage of Section 5.3).  Indices are int32, values
+ *   fp32, dense operands row-major with leading dimension equal to their
+ *   width k (element (i, c) at i * k + c).  A CSR holds unique keys sorted by
+ *   (row, col); its `rowidx` is the row of every stored entry (the COO row
+ *   array of the same order), produced by nsd_csr_expand_rows or
+ *   nsd_coo_to_csr.  A CSC is the stable column order of a CSR plus `perm`,
+ *   the CSR slot of every CSC slot.
+ * Streams.  `stream` is a hipStream_t passed as void* (NULL: the default
+ *   stream).  Hot-path calls are asynchronous on it.  Builders and validators
+ *   synchronise it before returning, because they report counts or errors.
+ * Workspace.  Calls that need scratch take `ws` (device, 256-byte aligned) and
+ *   `ws_bytes`; the size queries say how much.  Contents need no initial value.
+ * Errors.  The status is the return value; nothing is thrown across the ABI.
+ *   Argument errors are detected before any launch and leave outputs
+ *   untouched.  Malformed formats are detected only by the validators and
+ *   builders; passing a malformed CSR/CSC to a hot-path call is undefined.
+ *   nsd_last_error() gives a thread-local message for the last failure.
+ * Determinism.  Every entry point is bitwise reproducible run to run: no
+ *   floating-point atomics; every reduction has a fixed order.
+ * Limits.  nnz and every dimension are < 2^31; dense offsets use 64-bit
+ *   arithmetic.  Any k >= 1 works; k in {1, 32, 64, 128, 256} and other
+ *   multiples of 4 up to 256 take the vector paths.
+ */
+#ifndef NSD_H
+#define NSD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum nsd_status {
+    NSD_OK = 0,
+    NSD_ERR_INVALID_ARG = 1, /* null pointer, negative size, k < 1, ... */
+    NSD_ERR_BAD_FORMAT = 2,  /* validator/builder: malformed indices */
+    NSD_ERR_DUPLICATE = 3,   /* builder: duplicate coordinate under NSD_DUP_ERROR */
+    NSD_ERR_TOO_LARGE = 4,   /* a size at or above 2^31 */
+    NSD_ERR_WORKSPACE = 5,   /* ws_bytes below the queried size */
+    NSD_ERR_UNSUPPORTED = 6,
+    NSD_ERR_HIP = 7          /* a HIP runtime error; see nsd_last_error() */
+} nsd_status;
+
+/* Duplicate coordinates in a COO input: summed (the "+=" of a singleton
+ * inserted inside a sum, Section 5.5) or rejected (the `unique` annotation of
+ * the storage formats, Section 5.3). */
+typedef enum nsd_dup_policy { NSD_DUP_SUM = 0, NSD_DUP_ERROR = 1 } nsd_dup_policy;
+
+/* Matrix CSR (Section 5.3, the matrix CSR storage `(len,pos,idx,val)`). */
+typedef struct nsd_csr {
+    int32_t nrows, ncols, nnz;
+    const int32_t *rowptr; /* [nrows+1], rowptr[0] = 0, rowptr[nrows] = nnz */
+    const int32_t *rowidx; /* [nnz], row of every entry, non-decreasing */
+    const int32_t *colind; /* [nnz], strictly increasing within a row */
+    const float *val;      /* [nnz] */
+} nsd_csr;
+
+/* Matrix CSC of the same matrix (Section 5.3: expressed like CSR). */
+typedef struct nsd_csc {
+    int32_t nrows, ncols, nnz;
+    const int32_t *colptr; /* [ncols+1] */
+    const int32_t *colidx; /* [nnz], column of every CSC slot, non-decreasing */
+    const int32_t *rowind; /* [nnz], strictly increasing within a column */
+    const int32_t *perm;   /* [nnz], CSR slot holding the same entry */
+} nsd_csc;
+
+/* ----------------------------------------------------------------- info */
+
+/* Static string naming a status code. */
+const char *nsd_status_string(int status);
+/* Thread-local detail message of this thread's last failing call ("" if none). */
+const char *nsd_last_error(void);
+/* Library ABI version (major * 10000 + minor * 100 + patch). */
+int nsd_version(void);
+
+/* ------------------------------------------------------------ workspace */
+
+/* Bytes of `ws` that any hot-path entry point below needs for a sparse
+ * operand with `nnz` stored entries, at most `nseg` rows or columns on its
+ * reduced side, and dense width k.  Writes *bytes (host). */
+nsd_status nsd_workspace_size(int32_t nnz, int32_t nseg, int32_t k, size_t *bytes);
+
+/* Bytes of `ws` that the builders need to sort n entries whose keys are below
+ * max_key (max_key >= 1).  Writes *bytes (host). */
+nsd_status nsd_build_workspace_size(int32_t n, int32_t max_key, size_t *bytes);
+
+/* ------------------------------------------------------------- builders */
+
+/* rowidx[p] = the row r with rowptr[r] <= p < rowptr[r+1].  Async. */
+nsd_status nsd_csr_expand_rows(int32_t nrows, int32_t nnz, const int32_t *rowptr,
+                               int32_t *rowidx, void *stream);
+
+/*
+ * COO -> CSR (Section 5.3: vector/matrix COO and CSR storage; the CSR keeps
+ * unique keys).  Entries are stably sorted by (row, col); a coordinate given
+ * several times is merged under NSD_DUP_SUM (values added in input order, the
+ * semi-ring "+=") or rejected with NSD_ERR_DUPLICATE under NSD_DUP_ERROR.
+ * Inputs row/col/val: [nnz].  Outputs (each sized for nnz, the first
+ * *nnz_out entries are written): rowptr [nrows+1], rowidx, colind, val_out,
+ * perm (input position of the first occurrence of each output entry).
+ * *nnz_out is a host int32.  Index outputs are bit-exact; a merged value is
+ * the fp32 sum of its duplicates in input order.  Coordinates out of range
+ * give NSD_ERR_BAD_FORMAT.  Synchronous.  ws: nsd_build_workspace_size(nnz,
+ * max(nrows, ncols)).
+ */
+nsd_status nsd_coo_to_csr(int32_t nrows, int32_t ncols, int32_t nnz, const int32_t *row,
+                          const int32_t *col, const float *val, int policy,
+                          int32_t *rowptr, int32_t *rowidx, int32_t *colind,
+                          float *val_out, int32_t *perm, int32_t *nnz_out,
+                          void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * CSR -> CSC by a stable counting sort on the column index (Section 5.3, CSC
+ * "expressed similarly" to CSR).  Outputs: colptr [ncols+1]; colidx, rowind,
+ * perm [nnz] with perm[q] the CSR slot of CSC slot q; rows ascend within every
+ * column.  Bit-exact.  Synchronous.  ws: nsd_build_workspace_size(nnz, ncols).
+ */
+nsd_status nsd_csr_to_csc(const nsd_csr *A, int32_t *colptr, int32_t *colidx,
+                          int32_t *rowind, int32_t *perm, void *ws, size_t ws_bytes,
+                          void *stream);
+
+/*
+ * Mode index of a COO 3-tensor (or any int32 key array): a stable counting
+ * sort of positions 0..nnz-1 by key[p] in [0, dim).  Outputs: segptr [dim+1],
+ * segidx [nnz] (sorted keys), perm [nnz] (input position of sorted slot q).
+ * Bit-exact.  Synchronous.  ws: nsd_build_workspace_size(nnz, dim).
+ */
+nsd_status nsd_coo_mode_index(int32_t nnz, int32_t dim, const int32_t *key,
+                              int32_t *segptr, int32_t *segidx, int32_t *perm,
+                              void *ws, size_t ws_bytes, void *stream);
+
+/* dst[q] = src[perm[q]] for q < n: an exact fp32 copy (values into CSC or
+ * mode order).  Async. */
+nsd_status nsd_gather_f32(int32_t n, const int32_t *perm, const float *src, float *dst,
+                          void *stream);
+
+/* Checks a CSR: rowptr[0] = 0, non-decreasing, rowptr[nrows] = nnz; colind in
+ * [0, ncols) and, when check_sorted, strictly increasing within each row;
+ * rowidx (if not NULL) consistent with rowptr.  NSD_OK or NSD_ERR_BAD_FORMAT.
+ * Synchronous.  ws: at least 256 bytes. */
+nsd_status nsd_validate_csr(const nsd_csr *A, int check_sorted, void *ws, size_t ws_bytes,
+                            void *stream);
+
+/* ------------------------------------------------------------- forward */
+
+/* y = A x (SpMV).  x [ncols], y [nrows].  Async. */
+nsd_status nsd_spmv(const nsd_csr *A, const float *x, float *y, void *ws, size_t ws_bytes,
+                    void *stream);
+
+/* C = A B (SpMM; the matrix-matrix product of Logical SDQLite, Section 3).
+ * B [ncols x k], C [nrows x k].  Async. */
+nsd_status nsd_spmm(const nsd_csr *A, const float *B, int32_t k, float *C, void *ws,
+                    size_t ws_bytes, void *stream);
+
+/* ---------------------------------------------------- VJP primitives */
+
+/*
+ * SDDMM on A's pattern, the gradient w.r.t. a sparse operand:
+ *   out[p] = alpha * <X[rowidx[p], :], Y[colind[p], :]>   for p < nnz,
+ * aligned with A's CSR order (A's values are not read).  X [nrows x k]
+ * (NULL: all ones), Y [ncols x k], out [nnz].  Async.
+ */
+nsd_status nsd_sddmm(const nsd_csr *A, const float *X, const float *Y, int32_t k,
+                     float alpha, float *out, void *stream);
+
+/*
+ * Transposed product, the gradient w.r.t. a dense right operand:
+ *   out[j, :] = alpha * sum over stored (i, j) of A(i, j) * G[i, :]
+ * read through the CSC At of A (values taken from A->val via At->perm).
+ * G [nrows x k] (NULL: all ones, e.g. column sums for k = 1), out [ncols x k].
+ * Async.
+ */
+nsd_status nsd_spmm_t(const nsd_csr *A, const nsd_csc *At, const float *G, int32_t k,
+                      float alpha, float *out, void *ws, size_t ws_bytes, void *stream);
+
+/* -------------------------------------------------------- fused losses */
+/* `seed` is the upstream gradient dL_out/dL (1 for plain training); it scales
+ * every gradient and never the loss.  `loss` is one device double. */
+
+/*
+ * L = sum(A x) (SMVM of the experiments section).
+ * dA[p] = seed * x[colind[p]] on A's pattern; dx = seed * A^T 1.
+ * x [ncols]; dA [nnz]; dx [ncols].  Async.
+ */
+nsd_status nsd_loss_sum_spmv(const nsd_csr *A, const nsd_csc *At, const float *x, float seed,
+                             double *loss, float *dA, float *dx, void *ws, size_t ws_bytes,
+                             void *stream);
+
+/*
+ * L = 1/2 ||A B||_F^2.  C = A B (written to C [nrows x k]);
+ * dA[p] = seed * <C[i,:], B[j,:]> on A's pattern (SDDMM);
+ * dB = seed * A^T C.  B, dB [ncols x k]; dA [nnz].  Async.
+ */
+nsd_status nsd_loss_frob_spmm(const nsd_csr *A, const nsd_csc *At, const float *B, int32_t k,
+                              float seed, float *C, double *loss, float *dA, float *dB,
+                              void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * GNN layer: L = sum((A H) o G) = sum over stored (i, j) of A(i,j) <G[i,:], H[j,:]>.
+ * dA[p] = seed * <G[i,:], H[j,:]> on A's pattern (SDDMM); dH = seed * A^T G.
+ * H, dH [ncols x k]; G [nrows x k]; dA [nnz].  Async.
+ */
+nsd_status nsd_loss_bilinear(const nsd_csr *A, const nsd_csc *At, const float *H,
+                             const float *G, int32_t k, float seed, double *loss, float *dA,
+                             float *dH, void *ws, size_t ws_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NSD_H */

@@ -1,0 +1,542 @@
+// Format builders: COO -> CSR, CSR -> CSC, mode index of a COO tensor, row
+// expansion, value permutation and CSR validation.
+//
+// Every ordering is a stable sort by key, done as least-significant-digit
+// radix sort: a sequence of stable counting sorts on 8-bit digits (histogram
+// per tile, one device-wide exclusive scan over [digit][tile], stable scatter
+// with wave-level match masks).  Ties keep their input order, so the results
+// are bit-exact and equal to a sequential stable sort.
+#include <algorithm>
+
+#include "nsd_internal.hpp"
+
+namespace nsd {
+
+// ------------------------------------------------------------------ scan
+
+constexpr int kScanThreads = 256;
+constexpr int kScanItems = 8;
+constexpr int kScanTile = kScanThreads * kScanItems;
+
+// Exclusive scan of one value per thread across the block; returns the
+// block total through *total.
+__device__ int block_exclusive_scan(int v, int *total) {
+    __shared__ int wave_tot[kScanThreads / kWave];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    int inc = v;
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        int t = __shfl_up(inc, d, kWave);
+        if (lane >= d) inc += t;
+    }
+    if (lane == kWave - 1) wave_tot[wave] = inc;
+    __syncthreads();
+    int base = 0, all = 0;
+#pragma unroll
+    for (int w = 0; w < kScanThreads / kWave; ++w) {
+        if (w < wave) base += wave_tot[w];
+        all += wave_tot[w];
+    }
+    __syncthreads();
+    *total = all;
+    return base + inc - v;
+}
+
+__global__ __launch_bounds__(kScanThreads) void scan_reduce_kernel(const int32_t *in, int64_t n,
+                                                                   int32_t *sums) {
+    const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
+    int s = 0;
+#pragma unroll
+    for (int i = 0; i < kScanItems; ++i)
+        if (base + i < n) s += in[base + i];
+    int total;
+    block_exclusive_scan(s, &total);
+    if (threadIdx.x == 0) sums[blockIdx.x] = total;
+}
+
+__global__ __launch_bounds__(kScanThreads) void scan_tile_kernel(const int32_t *in, int32_t *out,
+                                                                 int64_t n, const int32_t *offs,
+                                                                 int32_t *total_dev) {
+    const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
+    int v[kScanItems];
+    int s = 0;
+#pragma unroll
+    for (int i = 0; i < kScanItems; ++i) {
+        v[i] = base + i < n ? in[base + i] : 0;
+        s += v[i];
+    }
+    int total;
+    int run = block_exclusive_scan(s, &total) + (offs ? offs[blockIdx.x] : 0);
+#pragma unroll
+    for (int i = 0; i < kScanItems; ++i) {
+        if (base + i < n) out[base + i] = run;
+        run += v[i];
+    }
+    if (total_dev && blockIdx.x == gridDim.x - 1 && threadIdx.x == 0)
+        *total_dev = (offs ? offs[blockIdx.x] : 0) + total;
+}
+
+size_t scan_ws_bytes(int64_t n) {
+    Carver c(nullptr);
+    int64_t m = ceil_div(n, kScanTile);
+    while (m > 1) {
+        c.take<int32_t>(m);
+        m = ceil_div(m, kScanTile);
+    }
+    return c.bytes();
+}
+
+static nsd_status scan_level(const int32_t *in, int32_t *out, int64_t n, int32_t *total_dev,
+                             Carver &c, hipStream_t st) {
+    const int64_t tiles = ceil_div(n, kScanTile);
+    if (tiles <= 1) {
+        scan_tile_kernel<<<1, kScanThreads, 0, st>>>(in, out, n, nullptr, total_dev);
+        return check_launch("scan_tile_kernel");
+    }
+    int32_t *sums = c.take<int32_t>(tiles);
+    scan_reduce_kernel<<<tiles, kScanThreads, 0, st>>>(in, n, sums);
+    NSD_TRY(check_launch("scan_reduce_kernel"));
+    NSD_TRY(scan_level(sums, sums, tiles, nullptr, c, st));
+    scan_tile_kernel<<<tiles, kScanThreads, 0, st>>>(in, out, n, sums, total_dev);
+    return check_launch("scan_tile_kernel");
+}
+
+nsd_status scan_exclusive(const int32_t *in, int32_t *out, int64_t n, int32_t *total_dev,
+                          void *ws, hipStream_t st) {
+    if (n <= 0) {
+        if (total_dev) NSD_HIP(hipMemsetAsync(total_dev, 0, sizeof(int32_t), st));
+        return NSD_OK;
+    }
+    Carver c(ws);
+    return scan_level(in, out, n, total_dev, c, st);
+}
+
+// ------------------------------------------------------------ radix sort
+
+constexpr int kSortThreads = 256;
+constexpr int kSortRounds = 8;  // 64-element rounds per wave
+constexpr int kSortTile = kSortThreads * kSortRounds;
+constexpr int kBins = 256;
+constexpr int kSortWaves = kSortThreads / kWave;
+
+__global__ __launch_bounds__(kSortThreads) void radix_hist_kernel(const int32_t *keys, int64_t n,
+                                                                  int shift, int64_t ntiles,
+                                                                  int32_t *hist) {
+    __shared__ int cnt[kBins];
+    cnt[threadIdx.x] = 0;
+    __syncthreads();
+    const int64_t base = (int64_t)blockIdx.x * kSortTile;
+#pragma unroll
+    for (int i = 0; i < kSortRounds; ++i) {
+        const int64_t q = base + (int64_t)i * kSortThreads + threadIdx.x;
+        if (q < n) atomicAdd(&cnt[((uint32_t)keys[q] >> shift) & (kBins - 1)], 1);
+    }
+    __syncthreads();
+    hist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = cnt[threadIdx.x];
+}
+
+// Stable scatter of one tile.  Wave w owns the tile's elements
+// [w * 512, (w + 1) * 512) and walks them in 8 rounds of 64 consecutive
+// elements, so (wave, round, lane) order is input order.  Inside a round the
+// lanes holding the same digit are found with 8 ballots; a lane's rank is the
+// count of such lanes below it plus what earlier rounds of its wave placed.
+__global__ __launch_bounds__(kSortThreads) void radix_scatter_kernel(
+    const int32_t *kin, const int32_t *vin, int32_t *kout, int32_t *vout, int64_t n, int shift,
+    int64_t ntiles, const int32_t *offs) {
+    __shared__ int wcnt[kSortWaves][kBins];
+    __shared__ int tile_off[kBins];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    for (int w = 0; w < kSortWaves; ++w) wcnt[w][threadIdx.x] = 0;
+    tile_off[threadIdx.x] = offs[(int64_t)threadIdx.x * ntiles + blockIdx.x];
+    __syncthreads();
+
+    const int64_t base = (int64_t)blockIdx.x * kSortTile + (int64_t)wave * (kSortRounds * kWave);
+    int key[kSortRounds], val[kSortRounds], rank[kSortRounds], dig[kSortRounds];
+#pragma unroll
+    for (int i = 0; i < kSortRounds; ++i) {
+        const int64_t q = base + (int64_t)i * kWave + lane;
+        const bool valid = q < n;
+        key[i] = valid ? kin[q] : 0;
+        val[i] = valid ? (vin ? vin[q] : (int32_t)q) : 0;
+        const int d = ((uint32_t)key[i] >> shift) & (kBins - 1);
+        dig[i] = d;
+        uint64_t same = __ballot(valid);
+#pragma unroll
+        for (int b = 0; b < 8; ++b) {
+            const bool bit = (d >> b) & 1;
+            const uint64_t m = __ballot(bit);
+            same &= bit ? m : ~m;
+        }
+        const int below = __popcll(same & __lanemask_lt());
+        const int prev = valid ? wcnt[wave][d] : 0;
+        rank[i] = prev + below;
+        if (valid && below == 0) wcnt[wave][d] = prev + __popcll(same);
+        __builtin_amdgcn_wave_barrier();
+    }
+    __syncthreads();
+    if (threadIdx.x < kBins) {
+        int s = 0;
+        for (int w = 0; w < kSortWaves; ++w) {
+            const int c = wcnt[w][threadIdx.x];
+            wcnt[w][threadIdx.x] = s;
+            s += c;
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kSortRounds; ++i) {
+        const int64_t q = base + (int64_t)i * kWave + lane;
+        if (q < n) {
+            const int64_t pos = (int64_t)tile_off[dig[i]] + wcnt[wave][dig[i]] + rank[i];
+            kout[pos] = key[i];
+            vout[pos] = val[i];
+        }
+    }
+}
+
+static int key_passes(int32_t max_key) {
+    uint32_t top = max_key > 0 ? (uint32_t)(max_key - 1) : 0u;
+    int bits = 0;
+    while (top) {
+        ++bits;
+        top >>= 1;
+    }
+    return bits == 0 ? 1 : (bits + 7) / 8;
+}
+
+size_t sort_ws_bytes(int64_t n, int32_t max_key) {
+    Carver c(nullptr);
+    const int64_t ntiles = ceil_div(n, kSortTile);
+    c.take<int32_t>(n);  // ping keys
+    c.take<int32_t>(n);  // ping payload
+    c.take<int32_t>(n);  // pong keys
+    c.take<int32_t>(n);  // pong payload
+    c.take<int32_t>(ntiles * kBins);
+    const size_t scan = scan_ws_bytes(ntiles * kBins);
+    return c.bytes() + scan;
+}
+
+nsd_status radix_sort_pairs(int64_t n, int32_t max_key, const int32_t *key_in,
+                            const int32_t *payload_in, int32_t *key_out, int32_t *payload_out,
+                            void *ws, hipStream_t st) {
+    if (n <= 0) return NSD_OK;
+    Carver c(ws);
+    const int64_t ntiles = ceil_div(n, kSortTile);
+    int32_t *kbuf[2] = {c.take<int32_t>(n), c.take<int32_t>(n)};
+    int32_t *vbuf[2] = {c.take<int32_t>(n), c.take<int32_t>(n)};
+    int32_t *hist = c.take<int32_t>(ntiles * kBins);
+    void *scan_ws = c.base + c.bytes();
+    const int passes = key_passes(max_key);
+    const int32_t *ksrc = key_in;
+    const int32_t *vsrc = payload_in;
+    for (int p = 0; p < passes; ++p) {
+        const bool last = p == passes - 1;
+        int32_t *kdst = last ? key_out : kbuf[p & 1];
+        int32_t *vdst = last ? payload_out : vbuf[p & 1];
+        radix_hist_kernel<<<ntiles, kSortThreads, 0, st>>>(ksrc, n, 8 * p, ntiles, hist);
+        NSD_TRY(check_launch("radix_hist_kernel"));
+        NSD_TRY(scan_exclusive(hist, hist, ntiles * kBins, nullptr, scan_ws, st));
+        radix_scatter_kernel<<<ntiles, kSortThreads, 0, st>>>(ksrc, vsrc, kdst, vdst, n, 8 * p,
+                                                              ntiles, hist);
+        NSD_TRY(check_launch("radix_scatter_kernel"));
+        ksrc = kdst;
+        vsrc = vdst;
+    }
+    return NSD_OK;
+}
+
+// ------------------------------------------------------- small kernels
+
+constexpr int kThreads = 256;
+
+static int64_t grid_for(int64_t n) { return ceil_div(n > 0 ? n : 1, kThreads); }
+
+__global__ void segptr_kernel(int64_t n, int32_t nseg, const int32_t *key, int32_t *segptr) {
+    const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (q > n) return;
+    // keys outside [0, nseg) (a malformed input) never write out of range
+    const int32_t prev = q == 0 ? -1 : min(key[q - 1], nseg);
+    const int32_t cur = q == n ? nseg : min(key[q], nseg);
+    for (int32_t r = max(prev + 1, 0); r <= cur; ++r) segptr[r] = (int32_t)q;
+}
+
+nsd_status segptr_from_sorted(int64_t n, int32_t nseg, const int32_t *sorted_key,
+                              int32_t *segptr, hipStream_t st) {
+    segptr_kernel<<<grid_for(n + 1), kThreads, 0, st>>>(n, nseg, sorted_key, segptr);
+    return check_launch("segptr_kernel");
+}
+
+__global__ void expand_rows_kernel(int32_t nrows, int32_t nnz, const int32_t *rowptr,
+                                   int32_t *rowidx) {
+    const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (p >= nnz) return;
+    // last r with rowptr[r] <= p
+    int32_t lo = 0, hi = nrows;
+    while (hi - lo > 1) {
+        const int32_t mid = lo + (hi - lo) / 2;
+        if (rowptr[mid] <= p) lo = mid;
+        else hi = mid;
+    }
+    rowidx[p] = lo;
+}
+
+template <class T>
+__global__ void gather_kernel(int64_t n, const int32_t *perm, const T *src, T *dst) {
+    const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (q < n) dst[q] = src[perm[q]];
+}
+
+__global__ void coo_range_kernel(int64_t n, int32_t nrows, int32_t ncols, const int32_t *row,
+                                 const int32_t *col, int32_t *flag) {
+    const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (p >= n) return;
+    if (row[p] < 0 || row[p] >= nrows || col[p] < 0 || col[p] >= ncols) atomicOr(flag, 1);
+}
+
+__global__ void key_range_kernel(int64_t n, int32_t dim, const int32_t *key, int32_t *flag) {
+    const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (p < n && (key[p] < 0 || key[p] >= dim)) atomicOr(flag, 1);
+}
+
+__global__ void run_heads_kernel(int64_t n, const int32_t *row_s, const int32_t *col_s,
+                                 int32_t *head) {
+    const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (q >= n) return;
+    head[q] = (q == 0 || row_s[q] != row_s[q - 1] || col_s[q] != col_s[q - 1]) ? 1 : 0;
+}
+
+// One thread per run of equal (row, col): the first occurrence names the
+// output slot; duplicate values are added in input order.
+__global__ void emit_runs_kernel(int64_t n, const int32_t *head, const int32_t *pos,
+                                 const int32_t *row_s, const int32_t *col_s, const int32_t *perm,
+                                 const float *val, int32_t *rowidx, int32_t *colind,
+                                 float *val_out, int32_t *perm_out) {
+    const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (q >= n || !head[q]) return;
+    const int32_t o = pos[q];
+    float s = val[perm[q]];
+    for (int64_t t = q + 1; t < n && !head[t]; ++t) s += val[perm[t]];
+    rowidx[o] = row_s[q];
+    colind[o] = col_s[q];
+    perm_out[o] = perm[q];
+    val_out[o] = s;
+}
+
+// One thread per row: rowptr monotone, columns in range (and strictly
+// increasing when asked), rowidx consistent.  Bit 0: rowptr, bit 1: column
+// range, bit 2: order, bit 3: rowidx.
+__global__ void validate_csr_kernel(int32_t nrows, int32_t ncols, int32_t nnz,
+                                    const int32_t *rowptr, const int32_t *rowidx,
+                                    const int32_t *colind, int check_sorted, int32_t *flag) {
+    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (r == 0 && (rowptr[0] != 0 || rowptr[nrows] != nnz)) atomicOr(flag, 1);
+    if (r >= nrows) return;
+    const int32_t b = rowptr[r], e = rowptr[r + 1];
+    if (b > e || b < 0 || e > nnz) {
+        atomicOr(flag, 1);
+        return;
+    }
+    int32_t last = -1;
+    for (int32_t p = b; p < e; ++p) {
+        const int32_t c = colind[p];
+        if (c < 0 || c >= ncols) atomicOr(flag, 2);
+        if (check_sorted && c <= last) atomicOr(flag, 4);
+        if (rowidx && rowidx[p] != r) atomicOr(flag, 8);
+        last = c;
+    }
+}
+
+static nsd_status read_flag(int32_t *flag_dev, int32_t *flag_host, hipStream_t st) {
+    NSD_HIP(hipMemcpyAsync(flag_host, flag_dev, sizeof(int32_t), hipMemcpyDeviceToHost, st));
+    NSD_HIP(hipStreamSynchronize(st));
+    return NSD_OK;
+}
+
+static bool too_large(int64_t v) { return v < 0 || v >= (int64_t(1) << 31); }
+
+}  // namespace nsd
+
+using namespace nsd;
+
+extern "C" {
+
+nsd_status nsd_build_workspace_size(int32_t n, int32_t max_key, size_t *bytes) {
+    NSD_REQUIRE(bytes != nullptr, "bytes is NULL");
+    NSD_REQUIRE(n >= 0 && max_key >= 1, "n must be >= 0 and max_key >= 1");
+    Carver c(nullptr);
+    for (int i = 0; i < 8; ++i) c.take<int32_t>(n > 0 ? n : 1);
+    c.take<int32_t>(64);
+    *bytes = c.bytes() + sort_ws_bytes(n, max_key) + scan_ws_bytes(n);
+    return NSD_OK;
+}
+
+nsd_status nsd_csr_expand_rows(int32_t nrows, int32_t nnz, const int32_t *rowptr,
+                               int32_t *rowidx, void *stream) {
+    NSD_REQUIRE(nrows >= 0 && nnz >= 0, "negative size");
+    NSD_REQUIRE(rowptr != nullptr && (nnz == 0 || rowidx != nullptr), "null pointer");
+    if (nnz == 0) return NSD_OK;
+    NSD_REQUIRE(nrows > 0, "nnz > 0 needs nrows > 0");
+    expand_rows_kernel<<<grid_for(nnz), kThreads, 0, as_stream(stream)>>>(nrows, nnz, rowptr,
+                                                                           rowidx);
+    return check_launch("expand_rows_kernel");
+}
+
+nsd_status nsd_gather_f32(int32_t n, const int32_t *perm, const float *src, float *dst,
+                          void *stream) {
+    NSD_REQUIRE(n >= 0, "negative size");
+    if (n == 0) return NSD_OK;
+    NSD_REQUIRE(perm && src && dst, "null pointer");
+    gather_kernel<float><<<grid_for(n), kThreads, 0, as_stream(stream)>>>(n, perm, src, dst);
+    return check_launch("gather_kernel");
+}
+
+nsd_status nsd_coo_to_csr(int32_t nrows, int32_t ncols, int32_t nnz, const int32_t *row,
+                          const int32_t *col, const float *val, int policy, int32_t *rowptr,
+                          int32_t *rowidx, int32_t *colind, float *val_out, int32_t *perm,
+                          int32_t *nnz_out, void *ws, size_t ws_bytes, void *stream) {
+    NSD_REQUIRE(nrows >= 0 && ncols >= 0 && nnz >= 0, "negative size");
+    NSD_REQUIRE(policy == NSD_DUP_SUM || policy == NSD_DUP_ERROR, "unknown duplicate policy %d",
+                policy);
+    NSD_REQUIRE(rowptr && nnz_out, "null pointer");
+    NSD_REQUIRE(nnz == 0 || (row && col && val && rowidx && colind && val_out && perm && ws),
+                "null pointer");
+    const int32_t max_key = std::max(std::max(nrows, ncols), 1);
+    size_t need;
+    NSD_TRY(nsd_build_workspace_size(nnz, max_key, &need));
+    if (nnz > 0 && ws_bytes < need)
+        return fail(NSD_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, need);
+    hipStream_t st = as_stream(stream);
+    if (nnz == 0) {
+        NSD_HIP(hipMemsetAsync(rowptr, 0, sizeof(int32_t) * (nrows + 1), st));
+        NSD_HIP(hipStreamSynchronize(st));
+        *nnz_out = 0;
+        return NSD_OK;
+    }
+    NSD_REQUIRE(nrows > 0 && ncols > 0, "nnz > 0 needs a non-empty shape");
+    Carver c(ws);
+    int32_t *kcol = c.take<int32_t>(nnz);
+    int32_t *perm1 = c.take<int32_t>(nnz);
+    int32_t *rkey = c.take<int32_t>(nnz);
+    int32_t *row_s = c.take<int32_t>(nnz);
+    int32_t *pm = c.take<int32_t>(nnz);
+    int32_t *col_s = c.take<int32_t>(nnz);
+    int32_t *head = c.take<int32_t>(nnz);
+    int32_t *pos = c.take<int32_t>(nnz);
+    int32_t *flag = c.take<int32_t>(64);
+    void *sort_ws = c.base + c.bytes();
+    void *scan_ws = static_cast<char *>(sort_ws) + sort_ws_bytes(nnz, max_key);
+
+    int32_t h = 0;
+    NSD_HIP(hipMemsetAsync(flag, 0, sizeof(int32_t), st));
+    coo_range_kernel<<<grid_for(nnz), kThreads, 0, st>>>(nnz, nrows, ncols, row, col, flag);
+    NSD_TRY(check_launch("coo_range_kernel"));
+    NSD_TRY(read_flag(flag, &h, st));
+    if (h) return fail(NSD_ERR_BAD_FORMAT, "COO coordinate out of range");
+
+    // stable sort by column, then stably by row: (row, col) order, ties in
+    // input order
+    NSD_TRY(radix_sort_pairs(nnz, ncols, col, nullptr, kcol, perm1, sort_ws, st));
+    gather_kernel<int32_t><<<grid_for(nnz), kThreads, 0, st>>>(nnz, perm1, row, rkey);
+    NSD_TRY(check_launch("gather_kernel"));
+    NSD_TRY(radix_sort_pairs(nnz, nrows, rkey, perm1, row_s, pm, sort_ws, st));
+    gather_kernel<int32_t><<<grid_for(nnz), kThreads, 0, st>>>(nnz, pm, col, col_s);
+    NSD_TRY(check_launch("gather_kernel"));
+    run_heads_kernel<<<grid_for(nnz), kThreads, 0, st>>>(nnz, row_s, col_s, head);
+    NSD_TRY(check_launch("run_heads_kernel"));
+    NSD_TRY(scan_exclusive(head, pos, nnz, flag + 1, scan_ws, st));
+    int32_t nuniq = 0;
+    NSD_TRY(read_flag(flag + 1, &nuniq, st));
+    if (policy == NSD_DUP_ERROR && nuniq != nnz)
+        return fail(NSD_ERR_DUPLICATE, "%d duplicate coordinates", nnz - nuniq);
+    emit_runs_kernel<<<grid_for(nnz), kThreads, 0, st>>>(nnz, head, pos, row_s, col_s, pm, val,
+                                                         rowidx, colind, val_out, perm);
+    NSD_TRY(check_launch("emit_runs_kernel"));
+    NSD_TRY(segptr_from_sorted(nuniq, nrows, rowidx, rowptr, st));
+    NSD_HIP(hipStreamSynchronize(st));
+    *nnz_out = nuniq;
+    return NSD_OK;
+}
+
+nsd_status nsd_csr_to_csc(const nsd_csr *A, int32_t *colptr, int32_t *colidx, int32_t *rowind,
+                          int32_t *perm, void *ws, size_t ws_bytes, void *stream) {
+    NSD_REQUIRE(A != nullptr && colptr != nullptr, "null pointer");
+    NSD_REQUIRE(A->nrows >= 0 && A->ncols >= 0 && A->nnz >= 0, "negative size");
+    hipStream_t st = as_stream(stream);
+    const int32_t nnz = A->nnz;
+    if (nnz > 0) {
+        NSD_REQUIRE(A->rowidx && A->colind && colidx && rowind && perm && ws, "null pointer");
+        size_t need;
+        NSD_TRY(nsd_build_workspace_size(nnz, std::max(A->ncols, 1), &need));
+        if (ws_bytes < need) return fail(NSD_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, need);
+        Carver c(ws);
+        for (int i = 0; i < 8; ++i) c.take<int32_t>(nnz);
+        int32_t *flag = c.take<int32_t>(64);
+        void *sort_ws = c.base + c.bytes();
+        int32_t h = 0;
+        NSD_HIP(hipMemsetAsync(flag, 0, sizeof(int32_t), st));
+        key_range_kernel<<<grid_for(nnz), kThreads, 0, st>>>(nnz, A->ncols, A->colind, flag);
+        NSD_TRY(check_launch("key_range_kernel"));
+        NSD_TRY(read_flag(flag, &h, st));
+        if (h) return fail(NSD_ERR_BAD_FORMAT, "column index out of range [0, %d)", A->ncols);
+        NSD_TRY(radix_sort_pairs(nnz, A->ncols, A->colind, nullptr, colidx, perm, sort_ws, st));
+        gather_kernel<int32_t><<<grid_for(nnz), kThreads, 0, st>>>(nnz, perm, A->rowidx, rowind);
+        NSD_TRY(check_launch("gather_kernel"));
+    }
+    NSD_TRY(segptr_from_sorted(nnz, A->ncols, colidx, colptr, st));
+    NSD_HIP(hipStreamSynchronize(st));
+    return NSD_OK;
+}
+
+nsd_status nsd_coo_mode_index(int32_t nnz, int32_t dim, const int32_t *key, int32_t *segptr,
+                              int32_t *segidx, int32_t *perm, void *ws, size_t ws_bytes,
+                              void *stream) {
+    NSD_REQUIRE(nnz >= 0 && dim >= 1, "need nnz >= 0 and dim >= 1");
+    NSD_REQUIRE(segptr != nullptr, "null pointer");
+    hipStream_t st = as_stream(stream);
+    if (nnz > 0) {
+        NSD_REQUIRE(key && segidx && perm && ws, "null pointer");
+        size_t need;
+        NSD_TRY(nsd_build_workspace_size(nnz, dim, &need));
+        if (ws_bytes < need) return fail(NSD_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, need);
+        Carver c(ws);
+        for (int i = 0; i < 8; ++i) c.take<int32_t>(nnz);
+        int32_t *flag = c.take<int32_t>(64);
+        void *sort_ws = c.base + c.bytes();
+        int32_t h = 0;
+        NSD_HIP(hipMemsetAsync(flag, 0, sizeof(int32_t), st));
+        key_range_kernel<<<grid_for(nnz), kThreads, 0, st>>>(nnz, dim, key, flag);
+        NSD_TRY(check_launch("key_range_kernel"));
+        NSD_TRY(read_flag(flag, &h, st));
+        if (h) return fail(NSD_ERR_BAD_FORMAT, "key out of range [0, %d)", dim);
+        NSD_TRY(radix_sort_pairs(nnz, dim, key, nullptr, segidx, perm, sort_ws, st));
+    }
+    NSD_TRY(segptr_from_sorted(nnz, dim, segidx, segptr, st));
+    NSD_HIP(hipStreamSynchronize(st));
+    return NSD_OK;
+}
+
+nsd_status nsd_validate_csr(const nsd_csr *A, int check_sorted, void *ws, size_t ws_bytes,
+                            void *stream) {
+    NSD_REQUIRE(A != nullptr && A->rowptr != nullptr, "null pointer");
+    NSD_REQUIRE(A->nrows >= 0 && A->ncols >= 0 && A->nnz >= 0, "negative size");
+    NSD_REQUIRE(A->nnz == 0 || A->colind != nullptr, "null colind");
+    NSD_REQUIRE(ws != nullptr && ws_bytes >= 256, "validation needs 256 bytes of workspace");
+    hipStream_t st = as_stream(stream);
+    int32_t *flag = static_cast<int32_t *>(ws);
+    NSD_HIP(hipMemsetAsync(flag, 0, sizeof(int32_t), st));
+    validate_csr_kernel<<<grid_for(A->nrows + 1), kThreads, 0, st>>>(
+        A->nrows, A->ncols, A->nnz, A->rowptr, A->rowidx, A->colind, check_sorted, flag);
+    NSD_TRY(check_launch("validate_csr_kernel"));
+    int32_t h = 0;
+    NSD_TRY(read_flag(flag, &h, st));
+    if (h) {
+        return fail(NSD_ERR_BAD_FORMAT, "malformed CSR:%s%s%s%s", (h & 1) ? " rowptr" : "",
+                    (h & 2) ? " column-range" : "", (h & 4) ? " column-order" : "",
+                    (h & 8) ? " rowidx" : "");
+    }
+    return NSD_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,231 @@
+"""ctypes binding of libnsd (include/nsd.h), argument marshalling only.
+
+Every function has the name of the C entry point it calls and takes torch
+tensors (device memory owned by the caller), which are passed as raw
+pointers; `None` passes NULL.  A status other than NSD_OK raises NsdError.
+No arithmetic of the method happens here: every step runs in the HIP
+library, and importing this module fails loudly when the library is missing.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import torch  # noqa: F401  (loads the HIP runtime libnsd links against)
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libnsd.so")
+
+NSD_OK = 0
+NSD_ERR_INVALID_ARG = 1
+NSD_ERR_BAD_FORMAT = 2
+NSD_ERR_DUPLICATE = 3
+NSD_ERR_TOO_LARGE = 4
+NSD_ERR_WORKSPACE = 5
+NSD_ERR_UNSUPPORTED = 6
+NSD_ERR_HIP = 7
+NSD_DUP_SUM = 0
+NSD_DUP_ERROR = 1
+
+
+class NsdError(RuntimeError):
+    def __init__(self, status: int, func: str, msg: str):
+        super().__init__(f"{func}: {status_name(status)}: {msg}")
+        self.status = status
+
+
+class nsd_csr(C.Structure):
+    _fields_ = [("nrows", C.c_int32), ("ncols", C.c_int32), ("nnz", C.c_int32),
+                ("rowptr", C.c_void_p), ("rowidx", C.c_void_p), ("colind", C.c_void_p),
+                ("val", C.c_void_p)]
+
+
+class nsd_csc(C.Structure):
+    _fields_ = [("nrows", C.c_int32), ("ncols", C.c_int32), ("nnz", C.c_int32),
+                ("colptr", C.c_void_p), ("colidx", C.c_void_p), ("rowind", C.c_void_p),
+                ("perm", C.c_void_p)]
+
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"libnsd.so is not built ({LIB_PATH}); run "
+                      "`python -m paper_2303_07030_amd.build` first")
+_lib = C.CDLL(LIB_PATH)
+
+_P = C.c_void_p
+_I = C.c_int32
+_SZ = C.c_size_t
+_CSR = C.POINTER(nsd_csr)
+_CSC = C.POINTER(nsd_csc)
+
+_SIGS = {
+    "nsd_status_string": (C.c_char_p, [C.c_int]),
+    "nsd_last_error": (C.c_char_p, []),
+    "nsd_version": (C.c_int, []),
+    "nsd_workspace_size": (C.c_int, [_I, _I, _I, C.POINTER(_SZ)]),
+    "nsd_build_workspace_size": (C.c_int, [_I, _I, C.POINTER(_SZ)]),
+    "nsd_csr_expand_rows": (C.c_int, [_I, _I, _P, _P, _P]),
+    "nsd_coo_to_csr": (C.c_int, [_I, _I, _I, _P, _P, _P, C.c_int, _P, _P, _P, _P, _P,
+                                 C.POINTER(_I), _P, _SZ, _P]),
+    "nsd_csr_to_csc": (C.c_int, [_CSR, _P, _P, _P, _P, _P, _SZ, _P]),
+    "nsd_coo_mode_index": (C.c_int, [_I, _I, _P, _P, _P, _P, _P, _SZ, _P]),
+    "nsd_gather_f32": (C.c_int, [_I, _P, _P, _P, _P]),
+    "nsd_validate_csr": (C.c_int, [_CSR, C.c_int, _P, _SZ, _P]),
+    "nsd_spmv": (C.c_int, [_CSR, _P, _P, _P, _SZ, _P]),
+    "nsd_spmm": (C.c_int, [_CSR, _P, _I, _P, _P, _SZ, _P]),
+    "nsd_sddmm": (C.c_int, [_CSR, _P, _P, _I, C.c_float, _P, _P]),
+    "nsd_spmm_t": (C.c_int, [_CSR, _CSC, _P, _I, C.c_float, _P, _P, _SZ, _P]),
+    "nsd_loss_sum_spmv": (C.c_int, [_CSR, _CSC, _P, C.c_float, _P, _P, _P, _P, _SZ, _P]),
+    "nsd_loss_frob_spmm": (C.c_int, [_CSR, _CSC, _P, _I, C.c_float, _P, _P, _P, _P, _P, _SZ,
+                                     _P]),
+    "nsd_loss_bilinear": (C.c_int, [_CSR, _CSC, _P, _P, _I, C.c_float, _P, _P, _P, _P, _SZ,
+                                    _P]),
+}
+for _name, (_res, _args) in _SIGS.items():
+    _f = getattr(_lib, _name)
+    _f.restype = _res
+    _f.argtypes = _args
+
+EXPORTED = tuple(_SIGS)
+
+
+def status_name(status: int) -> str:
+    return _lib.nsd_status_string(status).decode()
+
+
+def _p(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _nbytes(t):
+    return 0 if t is None else t.numel() * t.element_size()
+
+
+def _stream(s):
+    if s is None:
+        return torch.cuda.current_stream().cuda_stream if torch.cuda.is_available() else None
+    return s if isinstance(s, int) else s.cuda_stream
+
+
+def _check(status: int, func: str):
+    if status != NSD_OK:
+        raise NsdError(status, func, _lib.nsd_last_error().decode())
+
+
+# ------------------------------------------------------------------ info
+
+def nsd_status_string(status: int) -> str:
+    return status_name(status)
+
+
+def nsd_last_error() -> str:
+    return _lib.nsd_last_error().decode()
+
+
+def nsd_version() -> int:
+    return _lib.nsd_version()
+
+
+def nsd_workspace_size(nnz: int, nseg: int, k: int) -> int:
+    b = _SZ(0)
+    _check(_lib.nsd_workspace_size(nnz, nseg, k, C.byref(b)), "nsd_workspace_size")
+    return b.value
+
+
+def nsd_build_workspace_size(n: int, max_key: int) -> int:
+    b = _SZ(0)
+    _check(_lib.nsd_build_workspace_size(n, max_key, C.byref(b)), "nsd_build_workspace_size")
+    return b.value
+
+
+# ------------------------------------------------------------ descriptors
+
+def csr_desc(nrows, ncols, rowptr, rowidx, colind, val) -> nsd_csr:
+    nnz = 0 if colind is None else colind.numel()
+    d = nsd_csr(nrows, ncols, nnz, _p(rowptr), _p(rowidx), _p(colind), _p(val))
+    d._keep = (rowptr, rowidx, colind, val)
+    return d
+
+
+def csc_desc(nrows, ncols, colptr, colidx, rowind, perm) -> nsd_csc:
+    nnz = 0 if rowind is None else rowind.numel()
+    d = nsd_csc(nrows, ncols, nnz, _p(colptr), _p(colidx), _p(rowind), _p(perm))
+    d._keep = (colptr, colidx, rowind, perm)
+    return d
+
+
+# -------------------------------------------------------------- builders
+
+def nsd_csr_expand_rows(nrows, nnz, rowptr, rowidx, stream=None):
+    _check(_lib.nsd_csr_expand_rows(nrows, nnz, _p(rowptr), _p(rowidx), _stream(stream)),
+           "nsd_csr_expand_rows")
+
+
+def nsd_coo_to_csr(nrows, ncols, nnz, row, col, val, policy, rowptr, rowidx, colind, val_out,
+                   perm, ws, stream=None) -> int:
+    out = _I(0)
+    _check(_lib.nsd_coo_to_csr(nrows, ncols, nnz, _p(row), _p(col), _p(val), policy, _p(rowptr),
+                               _p(rowidx), _p(colind), _p(val_out), _p(perm), C.byref(out),
+                               _p(ws), _nbytes(ws), _stream(stream)), "nsd_coo_to_csr")
+    return out.value
+
+
+def nsd_csr_to_csc(A: nsd_csr, colptr, colidx, rowind, perm, ws, stream=None):
+    _check(_lib.nsd_csr_to_csc(C.byref(A), _p(colptr), _p(colidx), _p(rowind), _p(perm), _p(ws),
+                               _nbytes(ws), _stream(stream)), "nsd_csr_to_csc")
+
+
+def nsd_coo_mode_index(nnz, dim, key, segptr, segidx, perm, ws, stream=None):
+    _check(_lib.nsd_coo_mode_index(nnz, dim, _p(key), _p(segptr), _p(segidx), _p(perm), _p(ws),
+                                   _nbytes(ws), _stream(stream)), "nsd_coo_mode_index")
+
+
+def nsd_gather_f32(n, perm, src, dst, stream=None):
+    _check(_lib.nsd_gather_f32(n, _p(perm), _p(src), _p(dst), _stream(stream)), "nsd_gather_f32")
+
+
+def nsd_validate_csr(A: nsd_csr, check_sorted, ws, stream=None):
+    _check(_lib.nsd_validate_csr(C.byref(A), int(check_sorted), _p(ws), _nbytes(ws),
+                                 _stream(stream)), "nsd_validate_csr")
+
+
+# --------------------------------------------------------------- compute
+
+def nsd_spmv(A: nsd_csr, x, y, ws, stream=None):
+    _check(_lib.nsd_spmv(C.byref(A), _p(x), _p(y), _p(ws), _nbytes(ws), _stream(stream)),
+           "nsd_spmv")
+
+
+def nsd_spmm(A: nsd_csr, B, k, Cout, ws, stream=None):
+    _check(_lib.nsd_spmm(C.byref(A), _p(B), k, _p(Cout), _p(ws), _nbytes(ws), _stream(stream)),
+           "nsd_spmm")
+
+
+def nsd_sddmm(A: nsd_csr, X, Y, k, alpha, out, stream=None):
+    _check(_lib.nsd_sddmm(C.byref(A), _p(X), _p(Y), k, alpha, _p(out), _stream(stream)),
+           "nsd_sddmm")
+
+
+def nsd_spmm_t(A: nsd_csr, At: nsd_csc, G, k, alpha, out, ws, stream=None):
+    _check(_lib.nsd_spmm_t(C.byref(A), C.byref(At), _p(G), k, alpha, _p(out), _p(ws), _nbytes(ws),
+                           _stream(stream)), "nsd_spmm_t")
+
+
+def nsd_loss_sum_spmv(A: nsd_csr, At: nsd_csc, x, seed, loss, dA, dx, ws, stream=None):
+    _check(_lib.nsd_loss_sum_spmv(C.byref(A), C.byref(At), _p(x), seed, _p(loss), _p(dA), _p(dx),
+                                  _p(ws), _nbytes(ws), _stream(stream)), "nsd_loss_sum_spmv")
+
+
+def nsd_loss_frob_spmm(A: nsd_csr, At: nsd_csc, B, k, seed, Cout, loss, dA, dB, ws, stream=None):
+    _check(_lib.nsd_loss_frob_spmm(C.byref(A), C.byref(At), _p(B), k, seed, _p(Cout), _p(loss),
+                                   _p(dA), _p(dB), _p(ws), _nbytes(ws), _stream(stream)),
+           "nsd_loss_frob_spmm")
+
+
+def nsd_loss_bilinear(A: nsd_csr, At: nsd_csc, H, G, k, seed, loss, dA, dH, ws, stream=None):
+    _check(_lib.nsd_loss_bilinear(C.byref(A), C.byref(At), _p(H), _p(G), k, seed, _p(loss),
+                                  _p(dA), _p(dH), _p(ws), _nbytes(ws), _stream(stream)),
+           "nsd_loss_bilinear")

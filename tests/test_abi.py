@@ -1,0 +1,109 @@
+"""The C ABI: the library loads, exports every declared entry point, answers
+size queries and rejects bad arguments on the host before any launch."""
+import ctypes
+import os
+import shutil
+import subprocess
+import sys
+
+import pytest
+
+from helpers import header_functions, ROOT
+
+LIB = os.path.join(ROOT, "paper_2303_07030_amd", "libnsd.so")
+
+
+@pytest.fixture(scope="module")
+def nsd():
+    if not os.path.exists(LIB):
+        pytest.fail("libnsd.so is not built; run __graft_entry__.build()")
+    from paper_2303_07030_amd import nsd as m
+    return m
+
+
+def test_header_declares_entry_points():
+    names = header_functions()
+    assert "nsd_loss_frob_spmm" in names and "nsd_csr_to_csc" in names
+    assert len(names) >= 15
+
+
+def test_every_declared_symbol_is_exported(nsd):
+    lib = ctypes.CDLL(LIB)
+    missing = [n for n in header_functions() if not hasattr(lib, n)]
+    assert not missing, f"declared but not exported: {missing}"
+
+
+def test_binding_covers_every_declared_symbol(nsd):
+    assert sorted(nsd.EXPORTED) == header_functions()
+    for n in header_functions():
+        assert callable(getattr(nsd, n)), n
+
+
+def test_exports_are_c_symbols():
+    out = subprocess.run(["nm", "-D", "--defined-only", LIB], capture_output=True, text=True).stdout
+    syms = {line.split()[-1] for line in out.splitlines() if line.strip()}
+    for n in header_functions():
+        assert n in syms, f"{n} missing or mangled"
+
+
+def test_status_strings_and_version(nsd):
+    assert nsd.nsd_status_string(0) == "NSD_OK"
+    assert nsd.nsd_status_string(5) == "NSD_ERR_WORKSPACE"
+    assert nsd.nsd_status_string(99) == "NSD_ERR_UNKNOWN"
+    assert nsd.nsd_version() >= 100
+
+
+def test_workspace_queries(nsd):
+    small = nsd.nsd_workspace_size(1000, 100, 64)
+    big = nsd.nsd_workspace_size(1_000_000, 100_000, 64)
+    assert 0 < small < big and big % 256 == 0
+    assert nsd.nsd_build_workspace_size(0, 1) > 0
+    with pytest.raises(nsd.NsdError) as e:
+        nsd.nsd_workspace_size(10, 10, 0)
+    assert e.value.status == nsd.NSD_ERR_INVALID_ARG
+
+
+def _desc(nsd, nrows=4, ncols=4, nnz=3, ptr=0x1000):
+    d = nsd.nsd_csr(nrows, ncols, nnz, ptr, ptr, ptr, ptr)
+    return d
+
+
+def test_host_argument_errors_before_launch(nsd):
+    # every call below must be rejected on the host: no pointer is ever read
+    with pytest.raises(nsd.NsdError) as e:
+        nsd._check(nsd._lib.nsd_spmm(None, None, 64, None, None, 0, None), "nsd_spmm")
+    assert e.value.status == nsd.NSD_ERR_INVALID_ARG
+    A = _desc(nsd)
+    with pytest.raises(nsd.NsdError) as e:
+        nsd.nsd_spmm(A, 0x1000, 0, 0x1000, None)            # k < 1
+    assert e.value.status == nsd.NSD_ERR_INVALID_ARG
+    with pytest.raises(nsd.NsdError) as e:
+        nsd.nsd_spmm(A, 0x1000, 8, 0x1000, None)            # no workspace
+    assert e.value.status == nsd.NSD_ERR_WORKSPACE
+    bad = nsd.nsd_csr(-1, 4, 3, 0x1000, 0x1000, 0x1000, 0x1000)
+    with pytest.raises(nsd.NsdError) as e:
+        nsd.nsd_sddmm(bad, None, 0x1000, 4, 1.0, 0x1000)
+    assert e.value.status == nsd.NSD_ERR_INVALID_ARG
+    At = nsd.nsd_csc(4, 5, 3, 0x1000, 0x1000, 0x1000, 0x1000)  # shape mismatch
+    with pytest.raises(nsd.NsdError) as e:
+        nsd.nsd_spmm_t(A, At, None, 1, 1.0, 0x1000, None)
+    assert e.value.status == nsd.NSD_ERR_INVALID_ARG
+    with pytest.raises(nsd.NsdError) as e:
+        nsd.nsd_coo_to_csr(4, 4, 3, 0x1000, 0x1000, 0x1000, 7, 0x1000, 0x1000, 0x1000, 0x1000,
+                           0x1000, None)                      # unknown policy
+    assert e.value.status == nsd.NSD_ERR_INVALID_ARG
+    with pytest.raises(nsd.NsdError) as e:
+        nsd.nsd_coo_mode_index(3, 0, 0x1000, 0x1000, 0x1000, 0x1000, None)   # dim < 1
+    assert e.value.status == nsd.NSD_ERR_INVALID_ARG
+    assert "dim" in nsd.nsd_last_error()
+
+
+def test_binding_fails_loudly_without_library(tmp_path):
+    # a copy of the binding next to no library must refuse to import
+    pkg = tmp_path / "paper_2303_07030_amd"
+    pkg.mkdir()
+    shutil.copy(os.path.join(ROOT, "paper_2303_07030_amd", "nsd.py"), pkg / "nsd.py")
+    (pkg / "__init__.py").write_text("")
+    r = subprocess.run([sys.executable, "-c", "import paper_2303_07030_amd.nsd"], cwd=tmp_path,
+                       capture_output=True, text=True)
+    assert r.returncode != 0 and "libnsd.so is not built" in r.stderr

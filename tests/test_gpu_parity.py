@@ -1,0 +1,416 @@
+"""Parity of the HIP path with the fp64 oracle, called through the C ABI.
+
+Index and pattern outputs must equal the oracle bit for bit; floating-point
+outputs must satisfy |got - ref| <= 1e-4 * mag (mag: the oracle's evaluation
+on absolute values), with exact zeros where mag is 0.
+"""
+import numpy as np
+import pytest
+import torch
+
+from helpers import assert_mag_close
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def nsd():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2303_07030_amd import nsd as m
+    return m
+
+
+@pytest.fixture(scope="module")
+def operand(nsd):
+    from paper_2303_07030_amd.operand import DeviceCsr
+    return DeviceCsr
+
+
+def dev(a, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(a))
+    if dtype is not None:
+        t = t.to(dtype)
+    return t.cuda()
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def make_csr(rng, nrows, ncols, lengths, hot_col=None):
+    """Sorted unique columns per row; hot_col (if given) joins every other row."""
+    rowptr = np.zeros(nrows + 1, np.int64)
+    cols = []
+    for r in range(nrows):
+        L = int(lengths[r])
+        c = rng.choice(ncols, size=L, replace=False) if L else np.empty(0, np.int64)
+        if hot_col is not None and r % 2 == 0 and L and hot_col not in c:
+            c[0] = hot_col
+        c = np.sort(c)
+        cols.append(c)
+        rowptr[r + 1] = rowptr[r] + L
+    colind = np.concatenate(cols).astype(np.int32) if cols else np.empty(0, np.int32)
+    val = rng.standard_normal(colind.shape[0]).astype(np.float32)
+    return rowptr.astype(np.int32), colind, val
+
+
+def edge_pattern(seed=0, nrows=700, ncols=900):
+    """Power-law rows, empty rows at the start, middle and end, one row of
+    850 entries spanning many slots, and a column present in half the rows."""
+    rng = np.random.default_rng(seed)
+    lengths = np.minimum((40 * rng.pareto(1.2, nrows)).astype(np.int64), 300)
+    lengths[[0, 1, 350, 351, nrows - 3, nrows - 2, nrows - 1]] = 0
+    lengths[123] = 850
+    return nrows, ncols, *make_csr(rng, nrows, ncols, lengths, hot_col=5)
+
+
+def oracle_dok(orc, nrows, ncols, rowptr, colind, val):
+    return orc.Dok.from_csr(nrows, ncols, rowptr, colind, val)
+
+
+# ------------------------------------------------------------------ builders
+
+def test_expand_rows_bit_exact(nsd, operand):
+    nrows, ncols, rowptr, colind, val = edge_pattern(1)
+    A = operand(nrows, ncols, rowptr, colind, val, build_csc=False)
+    ref = np.repeat(np.arange(nrows, dtype=np.int32), np.diff(rowptr))
+    assert np.array_equal(host(A.rowidx), ref)
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_csr_to_csc_bit_exact(nsd, operand, orc, seed):
+    nrows, ncols, rowptr, colind, val = edge_pattern(seed)
+    A = operand(nrows, ncols, rowptr, colind, val)
+    segptr, skey, perm = orc.stable_sort_by_key(colind, ncols)
+    rows = np.repeat(np.arange(nrows, dtype=np.int32), np.diff(rowptr))
+    assert np.array_equal(host(A.colptr), segptr)
+    assert np.array_equal(host(A.colidx), skey)
+    assert np.array_equal(host(A.perm), perm)
+    assert np.array_equal(host(A.rowind), rows[perm])
+
+
+def test_csr_to_csc_full_size_spmm_workload(nsd, operand, orc):
+    from paper_2303_07030_amd import synth
+    d = synth.make("spmm")
+    A = operand(d["nrows"], d["ncols"], d["rowptr"], d["colind"], d["val"])
+    segptr, skey, perm = orc.stable_sort_by_key(d["colind"], d["ncols"])
+    assert np.array_equal(host(A.colptr), segptr)
+    assert np.array_equal(host(A.perm), perm)
+    assert np.array_equal(host(A.colidx), skey)
+
+
+@pytest.mark.parametrize("seed", [0, 3])
+def test_coo_to_csr_sums_duplicates(nsd, orc, seed):
+    rng = np.random.default_rng(seed)
+    nr, nc, n = 300, 517, 20000
+    keys = rng.choice(nr * nc, size=n - 3000, replace=False)
+    keys = np.concatenate([keys, rng.choice(keys, size=3000)])
+    rng.shuffle(keys)
+    row, col = (keys // nc).astype(np.int32), (keys % nc).astype(np.int32)
+    val = rng.standard_normal(n).astype(np.float32)
+    ws = torch.empty(nsd.nsd_build_workspace_size(n, max(nr, nc)), dtype=torch.uint8, device="cuda")
+    out = [torch.empty(m, dtype=t, device="cuda") for m, t in
+           [(nr + 1, torch.int32), (n, torch.int32), (n, torch.int32), (n, torch.float32),
+            (n, torch.int32)]]
+    nuniq = nsd.nsd_coo_to_csr(nr, nc, n, dev(row), dev(col), dev(val), nsd.NSD_DUP_SUM, *out, ws)
+    rowptr_r, colind_r, val_r, first_r = orc.coo_to_csr(orc.Dok((nr, nc), (row, col), val))
+    assert nuniq == len(colind_r)
+    rowptr, rowidx, colind, vout, perm = [host(t) for t in out]
+    assert np.array_equal(rowptr, rowptr_r)
+    assert np.array_equal(colind[:nuniq], colind_r)
+    assert np.array_equal(perm[:nuniq], first_r)
+    assert np.array_equal(rowidx[:nuniq], np.repeat(np.arange(nr), np.diff(rowptr_r)))
+    # values: the fp32 sum of the duplicates; bit-exact where there is only one
+    counts = np.bincount(np.searchsorted(np.unique(keys), keys), minlength=nuniq)
+    single = counts == 1
+    assert np.array_equal(vout[:nuniq][single], val[first_r[single]])
+    mag = np.zeros(nuniq)
+    np.add.at(mag, np.searchsorted(np.unique(keys), keys), np.abs(val.astype(np.float64)))
+    assert_mag_close(vout[:nuniq], val_r, mag, what="merged values")
+
+
+def test_coo_to_csr_errors(nsd):
+    row = dev(np.array([0, 1, 1, 2], np.int32))
+    col = dev(np.array([0, 2, 2, 1], np.int32))
+    val = dev(np.ones(4, np.float32))
+    ws = torch.empty(nsd.nsd_build_workspace_size(4, 3), dtype=torch.uint8, device="cuda")
+    outs = [torch.empty(m, dtype=t, device="cuda") for m, t in
+            [(4, torch.int32), (4, torch.int32), (4, torch.int32), (4, torch.float32),
+             (4, torch.int32)]]
+    with pytest.raises(nsd.NsdError) as e:
+        nsd.nsd_coo_to_csr(3, 3, 4, row, col, val, nsd.NSD_DUP_ERROR, *outs, ws)
+    assert e.value.status == nsd.NSD_ERR_DUPLICATE
+    bad = dev(np.array([0, 1, 5, 2], np.int32))
+    with pytest.raises(nsd.NsdError) as e:
+        nsd.nsd_coo_to_csr(3, 3, 4, row, bad, val, nsd.NSD_DUP_SUM, *outs, ws)
+    assert e.value.status == nsd.NSD_ERR_BAD_FORMAT
+    assert nsd.nsd_coo_to_csr(3, 3, 4, row, col, val, nsd.NSD_DUP_SUM, *outs, ws) == 3
+
+
+def test_mode_index_bit_exact(nsd, orc):
+    from paper_2303_07030_amd import synth
+    d = synth.make("cp", "small")
+    n = len(d["val"])
+    ws = torch.empty(nsd.nsd_build_workspace_size(n, d["dims"][0]), dtype=torch.uint8,
+                     device="cuda")
+    for key in (d["i"], d["j"], d["k"]):
+        segptr = torch.empty(d["dims"][0] + 1, dtype=torch.int32, device="cuda")
+        segidx = torch.empty(n, dtype=torch.int32, device="cuda")
+        perm = torch.empty(n, dtype=torch.int32, device="cuda")
+        nsd.nsd_coo_mode_index(n, d["dims"][0], dev(key), segptr, segidx, perm, ws)
+        rs, rk, rp = orc.stable_sort_by_key(key, d["dims"][0])
+        assert np.array_equal(host(segptr), rs)
+        assert np.array_equal(host(segidx), rk)
+        assert np.array_equal(host(perm), rp)
+
+
+def test_gather_is_exact_copy(nsd):
+    rng = np.random.default_rng(2)
+    src = rng.standard_normal(5000).astype(np.float32)
+    perm = rng.permutation(5000).astype(np.int32)
+    dst = torch.empty(5000, dtype=torch.float32, device="cuda")
+    nsd.nsd_gather_f32(5000, dev(perm), dev(src), dst)
+    assert np.array_equal(host(dst), src[perm])
+
+
+def test_validate_csr(nsd, operand):
+    nrows, ncols, rowptr, colind, val = edge_pattern(4)
+    A = operand(nrows, ncols, rowptr, colind, val, build_csc=False)
+    ws = torch.empty(256, dtype=torch.uint8, device="cuda")
+    nsd.nsd_validate_csr(A.desc, 1, ws)
+    bad = colind.copy()
+    r = 123
+    bad[rowptr[r]], bad[rowptr[r] + 1] = bad[rowptr[r] + 1], bad[rowptr[r]]
+    B = operand(nrows, ncols, rowptr, bad, val, build_csc=False)
+    nsd.nsd_validate_csr(B.desc, 0, ws)  # order not checked
+    with pytest.raises(nsd.NsdError) as e:
+        nsd.nsd_validate_csr(B.desc, 1, ws)
+    assert e.value.status == nsd.NSD_ERR_BAD_FORMAT and "order" in str(e.value)
+    bad2 = colind.copy()
+    bad2[10] = ncols + 3
+    Cm = operand(nrows, ncols, rowptr, bad2, val, build_csc=False)
+    with pytest.raises(nsd.NsdError) as e:
+        nsd.nsd_validate_csr(Cm.desc, 0, ws)
+    assert "column-range" in str(e.value)
+
+
+# ---------------------------------------------------------------- primitives
+
+KS = [1, 3, 4, 8, 16, 32, 64, 100, 128, 256, 264]
+
+
+@pytest.fixture(scope="module")
+def edge_A(operand, orc):
+    nrows, ncols, rowptr, colind, val = edge_pattern(7)
+    A = operand(nrows, ncols, rowptr, colind, val)
+    D = oracle_dok(orc, nrows, ncols, rowptr, colind, val)
+    rows = np.repeat(np.arange(nrows, dtype=np.int32), np.diff(rowptr))
+    return A, D, rows, colind
+
+
+@pytest.mark.parametrize("k", KS)
+def test_spmm(nsd, orc, edge_A, k):
+    A, D, _, _ = edge_A
+    rng = np.random.default_rng(k)
+    B = rng.standard_normal((A.ncols, k)).astype(np.float32)
+    Cg = torch.full((A.nrows, k), np.nan, dtype=torch.float32, device="cuda")
+    nsd.nsd_spmm(A.desc, dev(B), k, Cg, A.workspace(k))
+    ref, mag = orc.spmm(D, B, k)
+    assert_mag_close(host(Cg), ref, mag, what=f"spmm k={k}")
+
+
+def test_spmv(nsd, orc, edge_A):
+    A, D, _, _ = edge_A
+    x = np.random.default_rng(0).standard_normal(A.ncols).astype(np.float32)
+    y = torch.full((A.nrows,), np.nan, dtype=torch.float32, device="cuda")
+    nsd.nsd_spmv(A.desc, dev(x), y, A.workspace(1))
+    ref, mag = orc.spmm(D, x.reshape(-1, 1), 1)
+    assert_mag_close(host(y), ref[:, 0], mag[:, 0], what="spmv")
+
+
+@pytest.mark.parametrize("k", KS)
+def test_sddmm(nsd, orc, edge_A, k):
+    A, D, rows, cols = edge_A
+    rng = np.random.default_rng(100 + k)
+    X = rng.standard_normal((A.nrows, k)).astype(np.float32)
+    Y = rng.standard_normal((A.ncols, k)).astype(np.float32)
+    out = torch.full((A.nnz,), np.nan, dtype=torch.float32, device="cuda")
+    nsd.nsd_sddmm(A.desc, dev(X), dev(Y), k, -0.75, out)
+    ref, mag = orc.sddmm(D, X, Y, k, rows, cols, alpha=-0.75)
+    assert_mag_close(host(out), ref, mag, what=f"sddmm k={k}")
+
+
+@pytest.mark.parametrize("k", KS)
+def test_spmm_t(nsd, orc, edge_A, k):
+    A, D, _, _ = edge_A
+    rng = np.random.default_rng(200 + k)
+    G = rng.standard_normal((A.nrows, k)).astype(np.float32)
+    out = torch.full((A.ncols, k), np.nan, dtype=torch.float32, device="cuda")
+    nsd.nsd_spmm_t(A.desc, A.csc, dev(G), k, 1.5, out, A.workspace(k))
+    ref, mag = orc.spmm_t(D, G, k, alpha=1.5)
+    assert_mag_close(host(out), ref, mag, what=f"spmm_t k={k}")
+
+
+def test_spmm_t_ones_is_column_sums(nsd, orc, edge_A):
+    A, D, _, _ = edge_A
+    out = torch.full((A.ncols, 1), np.nan, dtype=torch.float32, device="cuda")
+    nsd.nsd_spmm_t(A.desc, A.csc, None, 1, 1.0, out, A.workspace(1))
+    ref, mag = orc.spmm_t(D, None, 1)
+    assert_mag_close(host(out), ref, mag, what="column sums")
+
+
+# ------------------------------------------------------------ fused losses
+
+def run_frob(nsd, A, B, k, seed=1.0):
+    Cg = torch.empty((A.nrows, k), dtype=torch.float32, device="cuda")
+    loss = torch.empty(1, dtype=torch.float64, device="cuda")
+    dA = torch.empty(A.nnz, dtype=torch.float32, device="cuda")
+    dB = torch.empty((A.ncols, k), dtype=torch.float32, device="cuda")
+    nsd.nsd_loss_frob_spmm(A.desc, A.csc, dev(B), k, seed, Cg, loss, dA, dB, A.workspace(k))
+    return host(Cg), host(loss)[0], host(dA), host(dB)
+
+
+def check_frob(orc, nrows, ncols, rowptr, colind, val, B, k, got, seed=1.0):
+    D = oracle_dok(orc, nrows, ncols, rowptr, colind, val)
+    rows = np.repeat(np.arange(nrows, dtype=np.int32), np.diff(rowptr))
+    Cref, Cmag = orc.spmm(D, B, k)
+    L, Lmag = orc.loss_half_sq(Cref, Cmag)
+    dA, dAm = orc.sddmm(D, Cref, B, k, rows, colind, alpha=seed, Xmag=Cmag)
+    dB, dBm = orc.spmm_t(D, Cref, k, alpha=seed, Gmag=Cmag)
+    Cg, Lg, dAg, dBg = got
+    assert_mag_close(Cg, Cref, Cmag, what="C")
+    assert_mag_close(Lg, L, Lmag, what="loss")
+    assert_mag_close(dAg, dA, dAm, what="dA")
+    assert_mag_close(dBg, dB, dBm, what="dB")
+
+
+def test_loss_sum_spmv_full_workload(nsd, operand, orc):
+    from paper_2303_07030_amd import synth
+    d = synth.make("spmv")
+    A = operand(d["nrows"], d["ncols"], d["rowptr"], d["colind"], d["val"])
+    loss = torch.empty(1, dtype=torch.float64, device="cuda")
+    dA = torch.empty(A.nnz, dtype=torch.float32, device="cuda")
+    dx = torch.empty(A.ncols, dtype=torch.float32, device="cuda")
+    nsd.nsd_loss_sum_spmv(A.desc, A.csc, dev(d["x"]), 1.0, loss, dA, dx, A.workspace(1))
+    D = oracle_dok(orc, d["nrows"], d["ncols"], d["rowptr"], d["colind"], d["val"])
+    L, Lm = orc.loss_sum_spmv(D, d["x"])
+    assert_mag_close(host(loss)[0], L, Lm, what="loss")
+    # closed forms: dA = x[col] exactly, dx = column sums
+    assert np.array_equal(host(dA), d["x"][d["colind"]])
+    ref, mag = orc.spmm_t(D, None, 1)
+    assert_mag_close(host(dx), ref[:, 0], mag[:, 0], what="dx")
+
+
+@pytest.mark.parametrize("size", ["small", "full"])
+def test_loss_frob_spmm_workload(nsd, operand, orc, size):
+    from paper_2303_07030_amd import synth
+    d = synth.make("spmm", size)
+    A = operand(d["nrows"], d["ncols"], d["rowptr"], d["colind"], d["val"])
+    got = run_frob(nsd, A, d["B"], d["k"])
+    check_frob(orc, d["nrows"], d["ncols"], d["rowptr"], d["colind"], d["val"], d["B"], d["k"], got)
+
+
+@pytest.mark.parametrize("k", [1, 12, 64, 128])
+def test_loss_frob_spmm_edge(nsd, operand, orc, k):
+    nrows, ncols, rowptr, colind, val = edge_pattern(11)
+    A = operand(nrows, ncols, rowptr, colind, val)
+    B = np.random.default_rng(k).standard_normal((ncols, k)).astype(np.float32)
+    got = run_frob(nsd, A, B, k, seed=0.5)
+    check_frob(orc, nrows, ncols, rowptr, colind, val, B, k, got, seed=0.5)
+
+
+def run_bilinear(nsd, A, H, G, k, seed=1.0):
+    loss = torch.empty(1, dtype=torch.float64, device="cuda")
+    dA = torch.empty(A.nnz, dtype=torch.float32, device="cuda")
+    dH = torch.empty((A.ncols, k), dtype=torch.float32, device="cuda")
+    nsd.nsd_loss_bilinear(A.desc, A.csc, dev(H), dev(G), k, seed, loss, dA, dH, A.workspace(k))
+    return host(loss)[0], host(dA), host(dH)
+
+
+def test_loss_bilinear_small_workload(nsd, operand, orc):
+    from paper_2303_07030_amd import synth
+    d = synth.make("gnn", "small")
+    A = operand(d["nrows"], d["ncols"], d["rowptr"], d["colind"], d["val"])
+    Lg, dAg, dHg = run_bilinear(nsd, A, d["H"], d["G"], d["k"])
+    D = oracle_dok(orc, d["nrows"], d["ncols"], d["rowptr"], d["colind"], d["val"])
+    rows = np.repeat(np.arange(d["nrows"], dtype=np.int32), np.diff(d["rowptr"]))
+    L, Lm = orc.loss_bilinear(D, d["G"], d["H"], d["k"])
+    dA, dAm = orc.sddmm(D, d["G"], d["H"], d["k"], rows, d["colind"])
+    dH, dHm = orc.spmm_t(D, d["G"], d["k"])
+    assert_mag_close(Lg, L, Lm, what="loss")
+    assert_mag_close(dAg, dA, dAm, what="dA")
+    assert_mag_close(dHg, dH, dHm, what="dH")
+
+
+# ------------------------------------------------------- edge cases
+
+def test_empty_matrix_writes_zeros(nsd, operand):
+    nrows, ncols, k = 50, 40, 64
+    A = operand(nrows, ncols, np.zeros(nrows + 1, np.int32), np.empty(0, np.int32),
+                np.empty(0, np.float32))
+    B = np.ones((ncols, k), np.float32)
+    Cg, Lg, dAg, dBg = run_frob(nsd, A, B, k)
+    assert Lg == 0.0 and dAg.size == 0
+    assert np.all(Cg == 0) and np.all(dBg == 0)
+    Lb, _, dH = run_bilinear(nsd, A, B, np.ones((nrows, k), np.float32), k)
+    assert Lb == 0.0 and np.all(dH == 0)
+
+
+def test_single_entry_and_single_dense_row(nsd, operand, orc):
+    for nrows, ncols, lengths in [(3, 4, [0, 1, 0]), (5, 3000, [0, 0, 3000, 0, 0])]:
+        rng = np.random.default_rng(nrows)
+        rowptr, colind, val = make_csr(rng, nrows, ncols, lengths)
+        A = operand(nrows, ncols, rowptr, colind, val)
+        B = rng.standard_normal((ncols, 64)).astype(np.float32)
+        got = run_frob(nsd, A, B, 64)
+        check_frob(orc, nrows, ncols, rowptr, colind, val, B, 64, got)
+
+
+def test_single_dense_column(nsd, operand, orc):
+    nrows, ncols = 4000, 6
+    rowptr = np.arange(nrows + 1, dtype=np.int32)
+    colind = np.full(nrows, 2, np.int32)
+    val = np.random.default_rng(9).standard_normal(nrows).astype(np.float32)
+    A = operand(nrows, ncols, rowptr, colind, val)
+    G = np.random.default_rng(10).standard_normal((nrows, 32)).astype(np.float32)
+    out = torch.empty((ncols, 32), dtype=torch.float32, device="cuda")
+    nsd.nsd_spmm_t(A.desc, A.csc, dev(G), 32, 1.0, out, A.workspace(32))
+    D = oracle_dok(orc, nrows, ncols, rowptr, colind, val)
+    ref, mag = orc.spmm_t(D, G, 32)
+    assert_mag_close(host(out), ref, mag, what="dense column")
+
+
+# ---------------------------------------------------------- invariants
+
+def test_bitwise_deterministic(nsd, operand):
+    from paper_2303_07030_amd import synth
+    d = synth.make("spmm", "small")
+    A = operand(d["nrows"], d["ncols"], d["rowptr"], d["colind"], d["val"])
+    a = run_frob(nsd, A, d["B"], d["k"])
+    b = run_frob(nsd, A, d["B"], d["k"])
+    for x, y in zip(a, b):
+        assert np.array_equal(np.asarray(x), np.asarray(y))
+
+
+def test_seed_scales_gradients_exactly(nsd, operand):
+    from paper_2303_07030_amd import synth
+    d = synth.make("spmm", "small")
+    A = operand(d["nrows"], d["ncols"], d["rowptr"], d["colind"], d["val"])
+    C1, L1, dA1, dB1 = run_frob(nsd, A, d["B"], d["k"], seed=1.0)
+    C2, L2, dA2, dB2 = run_frob(nsd, A, d["B"], d["k"], seed=4.0)
+    assert L1 == L2 and np.array_equal(C1, C2)
+    assert np.array_equal(dA2, 4 * dA1) and np.array_equal(dB2, 4 * dB1)
+
+
+def test_bilinear_dA_ignores_values_and_dH_ignores_H(nsd, operand):
+    from paper_2303_07030_amd import synth
+    d = synth.make("gnn", "small")
+    A = operand(d["nrows"], d["ncols"], d["rowptr"], d["colind"], d["val"])
+    A2 = operand(d["nrows"], d["ncols"], d["rowptr"], d["colind"], 2 * d["val"] + 1)
+    _, dA1, dH1 = run_bilinear(nsd, A, d["H"], d["G"], d["k"])
+    _, dA2, _ = run_bilinear(nsd, A2, d["H"], d["G"], d["k"])
+    _, _, dH3 = run_bilinear(nsd, A, 3 * d["H"] - 1, d["G"], d["k"])
+    assert np.array_equal(dA1, dA2)   # the gradient on the pattern does not read A's values
+    assert np.array_equal(dH1, dH3)   # a linear loss: dH does not depend on H
