@@ -69,6 +69,27 @@ typedef enum nsd_status {
  * the storage formats, Section 5.3). */
 typedef enum nsd_dup_policy { NSD_DUP_SUM = 0, NSD_DUP_ERROR = 1 } nsd_dup_policy;
 
+/*
+ * Work plan of a sorted sparse operand (the rows of a CSR or the columns of a
+ * CSC), built once per sparsity pattern by nsd_plan_build.  Entries are cut
+ * into work items of about item_len entries: a segment of at most item_len
+ * entries is never split (consecutive ones are packed into one item), a longer
+ * segment is cut into chunks of item_len entries whose partial sums are added
+ * in chunk order afterwards, and empty segments are listed for a zero fill.
+ * It balances power-law segment lengths without atomics.  A long segment with
+ * more than 64 chunks is "huge": its chunks are combined by a whole workgroup.
+ */
+typedef struct nsd_plan {
+    int32_t item_len;          /* L: entries per chunk; segments above L are long */
+    int32_t nitems, nlong, nhuge, nchunks, nempty;
+    const int32_t *item_ptr;   /* [nitems+1] first entry of every item; [nitems] = nnz */
+    const int32_t *long_seg;   /* [nlong] segment id of every long segment */
+    const int32_t *long_first; /* [nlong] first item of every long segment */
+    const int32_t *huge_idx;   /* [nhuge] positions in the long lists of huge segments */
+    const int32_t *chunk_item; /* [nchunks] every item that is a chunk of a long segment */
+    const int32_t *empty_seg;  /* [nempty] segments without entries */
+} nsd_plan;
+
 /* Matrix CSR (Section 5.3, the matrix CSR storage `(len,pos,idx,val)`). */
 typedef struct nsd_csr {
     int32_t nrows, ncols, nnz;
@@ -76,6 +97,7 @@ typedef struct nsd_csr {
     const int32_t *rowidx; /* [nnz], row of every entry, non-decreasing */
     const int32_t *colind; /* [nnz], strictly increasing within a row */
     const float *val;      /* [nnz] */
+    nsd_plan plan;         /* plan over the rows (for reductions into rows) */
 } nsd_csr;
 
 /* Matrix CSC of the same matrix (Section 5.3: expressed like CSR). */
@@ -85,6 +107,7 @@ typedef struct nsd_csc {
     const int32_t *colidx; /* [nnz], column of every CSC slot, non-decreasing */
     const int32_t *rowind; /* [nnz], strictly increasing within a column */
     const int32_t *perm;   /* [nnz], CSR slot holding the same entry */
+    nsd_plan plan;         /* plan over the columns (for reductions into columns) */
 } nsd_csc;
 
 /* ----------------------------------------------------------------- info */
@@ -98,16 +121,37 @@ int nsd_version(void);
 
 /* ------------------------------------------------------------ workspace */
 
-/* Bytes of `ws` that any hot-path entry point below needs for a sparse
- * operand with `nnz` stored entries, at most `nseg` rows or columns on its
- * reduced side, and dense width k.  Writes *bytes (host). */
-nsd_status nsd_workspace_size(int32_t nnz, int32_t nseg, int32_t k, size_t *bytes);
+/* Bytes of `ws` that any hot-path entry point below needs for the operand A
+ * (with its row plan), its CSC At (with its column plan; may be NULL when only
+ * row-side calls are made) and dense width k.  Writes *bytes (host). */
+nsd_status nsd_workspace_size(const nsd_csr *A, const nsd_csc *At, int32_t k, size_t *bytes);
 
 /* Bytes of `ws` that the builders need to sort n entries whose keys are below
  * max_key (max_key >= 1).  Writes *bytes (host). */
 nsd_status nsd_build_workspace_size(int32_t n, int32_t max_key, size_t *bytes);
 
 /* ------------------------------------------------------------- builders */
+
+/* Suggested item length L for a plan of an operand with nnz entries used at
+ * dense width k (enough items to fill the GPU; 16 <= L <= 256). */
+nsd_status nsd_plan_item_len(int32_t nnz, int32_t k, int32_t *item_len);
+
+/* Array sizes for nsd_plan_build: item_ptr needs *max_items + 1 entries,
+ * long_seg, long_first and huge_idx *max_long each, chunk_item *max_chunks,
+ * empty_seg nseg; *ws_bytes of workspace.  Host outputs.
+ * NSD_ERR_TOO_LARGE when 2 nnz + nseg >= 2^31. */
+nsd_status nsd_plan_bounds(int32_t nseg, int32_t nnz, int32_t item_len, int32_t *max_items,
+                           int32_t *max_long, int32_t *max_chunks, size_t *ws_bytes);
+
+/*
+ * Builds the work plan of a segment pointer array segptr [nseg+1] (a CSR
+ * rowptr or a CSC colptr) into the caller's arrays and fills *plan (host):
+ * counts and device pointers.  Deterministic.  Synchronous.
+ */
+nsd_status nsd_plan_build(int32_t nseg, int32_t nnz, const int32_t *segptr, int32_t item_len,
+                          int32_t *item_ptr, int32_t *long_seg, int32_t *long_first,
+                          int32_t *huge_idx, int32_t *chunk_item, int32_t *empty_seg,
+                          nsd_plan *plan, void *ws, size_t ws_bytes, void *stream);
 
 /* rowidx[p] = the row r with rowptr[r] <= p < rowptr[r+1].  Async. */
 nsd_status nsd_csr_expand_rows(int32_t nrows, int32_t nnz, const int32_t *rowptr,

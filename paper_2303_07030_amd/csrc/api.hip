@@ -8,7 +8,17 @@
 
 namespace nsd {
 
-static nsd_status check_csr(const nsd_csr *A, bool need_val) {
+static nsd_status check_plan(const nsd_plan &pl, int32_t nnz, const char *what) {
+    if (nnz == 0) return NSD_OK;
+    NSD_REQUIRE(pl.item_ptr && pl.nitems >= 1 && pl.nlong >= 0 && pl.nempty >= 0 &&
+                    pl.item_len >= 1,
+                "%s plan is not built (nsd_plan_build)", what);
+    NSD_REQUIRE(pl.nlong == 0 || pl.long_first, "%s plan long_first is NULL", what);
+    NSD_REQUIRE(pl.nempty == 0 || pl.empty_seg, "%s plan empty_seg is NULL", what);
+    return NSD_OK;
+}
+
+static nsd_status check_csr(const nsd_csr *A, bool need_val, bool need_plan) {
     NSD_REQUIRE(A != nullptr, "CSR descriptor is NULL");
     NSD_REQUIRE(A->nrows >= 0 && A->ncols >= 0 && A->nnz >= 0, "negative CSR size");
     NSD_REQUIRE(A->rowptr != nullptr, "CSR rowptr is NULL");
@@ -17,6 +27,7 @@ static nsd_status check_csr(const nsd_csr *A, bool need_val) {
         NSD_REQUIRE(A->rowidx && A->colind, "CSR rowidx/colind is NULL");
         NSD_REQUIRE(!need_val || A->val, "CSR val is NULL");
     }
+    if (need_plan) NSD_TRY(check_plan(A->plan, A->nnz, "row"));
     return NSD_OK;
 }
 
@@ -27,52 +38,58 @@ static nsd_status check_csc(const nsd_csc *At, const nsd_csr *A) {
                 At->nnz, A->nrows, A->ncols, A->nnz);
     NSD_REQUIRE(At->colptr != nullptr, "CSC colptr is NULL");
     if (At->nnz > 0) NSD_REQUIRE(At->colidx && At->rowind && At->perm, "CSC array is NULL");
-    return NSD_OK;
+    return check_plan(At->plan, At->nnz, "column");
 }
 
-// Workspace: one gather-reduce carry region (reused by every reduction of a
-// call, which run in stream order) followed by the loss partials.
-static size_t sgr_region_bytes(int64_t nnz, int k) {
-    size_t best = 0;
-    for (int kk : {k, 1}) {
-        Carver c(nullptr);
-        sgr_carve(c, nnz, kk, nullptr);
-        best = std::max(best, c.bytes());
-    }
-    return best;
+// Workspace: the chunk partials of the larger plan (reused by every reduction
+// of a call, which run in stream order) followed by the loss partials.
+static size_t part_region_bytes(const nsd_csr *A, const nsd_csc *At, int k) {
+    size_t b = sgr_part_bytes(A->plan, std::max(k, 1));
+    if (At) b = std::max(b, sgr_part_bytes(At->plan, std::max(k, 1)));
+    return (b + 255) & ~size_t(255);
 }
 
-static size_t part_count(int64_t nnz, int k) {
-    int64_t m = 1;
+static size_t loss_part_count(const nsd_csr *A, int k) {
+    int64_t m = std::max<int64_t>(1, frob_row_blocks(A->plan, k));
     for (int kk : {k, 1})
-        for (bool v : {true, false}) m = std::max(m, sddmm_shape(nnz, kk, v).nblocks);
+        for (bool v : {true, false}) m = std::max(m, sddmm_shape(A->nnz, kk, v).nblocks);
     return (size_t)m;
 }
 
-static size_t compute_ws_bytes(int64_t nnz, int k) {
-    return sgr_region_bytes(nnz, k) + ((part_count(nnz, k) * sizeof(double) + 255) & ~size_t(255));
+static size_t round256(size_t b) { return (b + 255) & ~size_t(255); }
+
+static size_t compute_ws_bytes(const nsd_csr *A, const nsd_csc *At, int k) {
+    return part_region_bytes(A, At, k) + round256(loss_part_count(A, k) * sizeof(double)) +
+           round256(std::max<size_t>(A->plan.nlong, 1) * sizeof(double));
 }
 
 struct ComputeWs {
-    void *sgr;
-    double *part;
+    float *part;
+    double *loss_part;
+    double *seg_loss;
 };
 
-static nsd_status carve_compute(void *ws, size_t ws_bytes, int64_t nnz, int k, ComputeWs *out) {
-    const size_t need = compute_ws_bytes(nnz, k);
+static nsd_status carve_compute(void *ws, size_t ws_bytes, const nsd_csr *A, const nsd_csc *At,
+                                int k, ComputeWs *out) {
+    const size_t need = compute_ws_bytes(A, At, k);
     if (ws == nullptr || ws_bytes < need)
         return fail(NSD_ERR_WORKSPACE, "workspace %zu bytes at %p, need %zu", ws_bytes, ws, need);
-    out->sgr = ws;
-    out->part = reinterpret_cast<double *>(static_cast<char *>(ws) + sgr_region_bytes(nnz, k));
+    char *b = static_cast<char *>(ws);
+    out->part = reinterpret_cast<float *>(b);
+    b += part_region_bytes(A, At, k);
+    out->loss_part = reinterpret_cast<double *>(b);
+    b += round256(loss_part_count(A, k) * sizeof(double));
+    out->seg_loss = reinterpret_cast<double *>(b);
     return NSD_OK;
 }
 
 static SgrParams rows_params(const nsd_csr *A, const float *X, int k, float alpha, float *out,
-                             void *region) {
+                             float *part) {
     SgrParams p;
     p.nseg = A->nrows;
     p.nnz = A->nnz;
     p.k = k;
+    p.plan = A->plan;
     p.segptr = A->rowptr;
     p.segidx = A->rowidx;
     p.idx = A->colind;
@@ -80,17 +97,17 @@ static SgrParams rows_params(const nsd_csr *A, const float *X, int k, float alph
     p.X = X;
     p.alpha = alpha;
     p.out = out;
-    Carver c(region);
-    sgr_carve(c, A->nnz, k, &p);
+    p.part = part;
     return p;
 }
 
 static SgrParams cols_params(const nsd_csr *A, const nsd_csc *At, const float *G, int k,
-                             float alpha, float *out, void *region) {
+                             float alpha, float *out, float *part) {
     SgrParams p;
     p.nseg = A->ncols;
     p.nnz = A->nnz;
     p.k = k;
+    p.plan = At->plan;
     p.segptr = At->colptr;
     p.segidx = At->colidx;
     p.idx = At->rowind;
@@ -99,8 +116,7 @@ static SgrParams cols_params(const nsd_csr *A, const nsd_csc *At, const float *G
     p.X = G;
     p.alpha = alpha;
     p.out = out;
-    Carver c(region);
-    sgr_carve(c, A->nnz, k, &p);
+    p.part = part;
     return p;
 }
 
@@ -130,37 +146,39 @@ using namespace nsd;
 
 extern "C" {
 
-nsd_status nsd_workspace_size(int32_t nnz, int32_t nseg, int32_t k, size_t *bytes) {
+nsd_status nsd_workspace_size(const nsd_csr *A, const nsd_csc *At, int32_t k, size_t *bytes) {
     NSD_REQUIRE(bytes != nullptr, "bytes is NULL");
-    NSD_REQUIRE(nnz >= 0 && nseg >= 0 && k >= 1, "need nnz >= 0, nseg >= 0, k >= 1");
-    *bytes = compute_ws_bytes(nnz, k);
+    NSD_REQUIRE(k >= 1, "k = %d < 1", k);
+    NSD_TRY(check_csr(A, false, false));
+    if (At) NSD_TRY(check_csc(At, A));
+    *bytes = compute_ws_bytes(A, At, k);
     return NSD_OK;
 }
 
 nsd_status nsd_spmv(const nsd_csr *A, const float *x, float *y, void *ws, size_t ws_bytes,
                     void *stream) {
-    NSD_TRY(check_csr(A, true));
+    NSD_TRY(check_csr(A, true, true));
     NSD_REQUIRE(A->nrows == 0 || y != nullptr, "y is NULL");
     NSD_REQUIRE(A->nnz == 0 || x != nullptr, "x is NULL");
     ComputeWs w;
-    NSD_TRY(carve_compute(ws, ws_bytes, A->nnz, 1, &w));
-    return segreduce(rows_params(A, x, 1, 1.f, y, w.sgr), as_stream(stream));
+    NSD_TRY(carve_compute(ws, ws_bytes, A, nullptr, 1, &w));
+    return segreduce(rows_params(A, x, 1, 1.f, y, w.part), as_stream(stream));
 }
 
 nsd_status nsd_spmm(const nsd_csr *A, const float *B, int32_t k, float *C, void *ws,
                     size_t ws_bytes, void *stream) {
-    NSD_TRY(check_csr(A, true));
+    NSD_TRY(check_csr(A, true, true));
     NSD_REQUIRE(k >= 1, "k = %d < 1", k);
     NSD_REQUIRE(A->nrows == 0 || C != nullptr, "C is NULL");
     NSD_REQUIRE(A->nnz == 0 || B != nullptr, "B is NULL");
     ComputeWs w;
-    NSD_TRY(carve_compute(ws, ws_bytes, A->nnz, k, &w));
-    return segreduce(rows_params(A, B, k, 1.f, C, w.sgr), as_stream(stream));
+    NSD_TRY(carve_compute(ws, ws_bytes, A, nullptr, k, &w));
+    return segreduce(rows_params(A, B, k, 1.f, C, w.part), as_stream(stream));
 }
 
 nsd_status nsd_sddmm(const nsd_csr *A, const float *X, const float *Y, int32_t k, float alpha,
                      float *out, void *stream) {
-    NSD_TRY(check_csr(A, false));
+    NSD_TRY(check_csr(A, false, false));
     NSD_REQUIRE(k >= 1, "k = %d < 1", k);
     NSD_REQUIRE(A->nnz == 0 || (Y != nullptr && out != nullptr), "Y/out is NULL");
     return sddmm(sddmm_params(A, X, Y, k, alpha, out), as_stream(stream));
@@ -168,41 +186,41 @@ nsd_status nsd_sddmm(const nsd_csr *A, const float *X, const float *Y, int32_t k
 
 nsd_status nsd_spmm_t(const nsd_csr *A, const nsd_csc *At, const float *G, int32_t k,
                       float alpha, float *out, void *ws, size_t ws_bytes, void *stream) {
-    NSD_TRY(check_csr(A, true));
+    NSD_TRY(check_csr(A, true, false));
     NSD_TRY(check_csc(At, A));
     NSD_REQUIRE(k >= 1, "k = %d < 1", k);
     NSD_REQUIRE(A->ncols == 0 || out != nullptr, "out is NULL");
     ComputeWs w;
-    NSD_TRY(carve_compute(ws, ws_bytes, A->nnz, k, &w));
-    return segreduce(cols_params(A, At, G, k, alpha, out, w.sgr), as_stream(stream));
+    NSD_TRY(carve_compute(ws, ws_bytes, A, At, k, &w));
+    return segreduce(cols_params(A, At, G, k, alpha, out, w.part), as_stream(stream));
 }
 
 nsd_status nsd_loss_sum_spmv(const nsd_csr *A, const nsd_csc *At, const float *x, float seed,
                              double *loss, float *dA, float *dx, void *ws, size_t ws_bytes,
                              void *stream) {
-    NSD_TRY(check_csr(A, true));
+    NSD_TRY(check_csr(A, true, false));
     NSD_TRY(check_csc(At, A));
     NSD_REQUIRE(loss != nullptr, "loss is NULL");
     NSD_REQUIRE(A->nnz == 0 || (x && dA), "x/dA is NULL");
     NSD_REQUIRE(A->ncols == 0 || dx != nullptr, "dx is NULL");
     ComputeWs w;
-    NSD_TRY(carve_compute(ws, ws_bytes, A->nnz, 1, &w));
+    NSD_TRY(carve_compute(ws, ws_bytes, A, At, 1, &w));
     hipStream_t st = as_stream(stream);
     // dA[p] = seed * x[col]; loss = sum_p A_p * x[col]
     SddmmParams sp = sddmm_params(A, nullptr, x, 1, seed, dA);
     sp.w = A->val;
     sp.beta = 1.0;
-    sp.part = w.part;
+    sp.part = w.loss_part;
     NSD_TRY(sddmm(sp, st));
     NSD_TRY(finish_loss(sp, loss, st));
     // dx = seed * A^T 1
-    return segreduce(cols_params(A, At, nullptr, 1, seed, dx, w.sgr), st);
+    return segreduce(cols_params(A, At, nullptr, 1, seed, dx, w.part), st);
 }
 
 nsd_status nsd_loss_frob_spmm(const nsd_csr *A, const nsd_csc *At, const float *B, int32_t k,
                               float seed, float *C, double *loss, float *dA, float *dB,
                               void *ws, size_t ws_bytes, void *stream) {
-    NSD_TRY(check_csr(A, true));
+    NSD_TRY(check_csr(A, true, true));
     NSD_TRY(check_csc(At, A));
     NSD_REQUIRE(k >= 1, "k = %d < 1", k);
     NSD_REQUIRE(loss != nullptr, "loss is NULL");
@@ -210,42 +228,54 @@ nsd_status nsd_loss_frob_spmm(const nsd_csr *A, const nsd_csc *At, const float *
     NSD_REQUIRE(A->ncols == 0 || dB != nullptr, "dB is NULL");
     NSD_REQUIRE(A->nnz == 0 || (B && dA), "B/dA is NULL");
     ComputeWs w;
-    NSD_TRY(carve_compute(ws, ws_bytes, A->nnz, k, &w));
+    NSD_TRY(carve_compute(ws, ws_bytes, A, At, k, &w));
     hipStream_t st = as_stream(stream);
+    if (A->nnz > 0 && frob_fused_ok(k, B, C, dB)) {
+        // row pass (C, loss, dA on short rows), long-row combine, column pass
+        // (dB and dA on long rows), long-column combine, loss total
+        FrobParams f;
+        f.rows = rows_params(A, B, k, 1.f, C, w.part);
+        f.cols = cols_params(A, At, C, k, seed, dB, w.part);
+        f.sdd = sddmm_params(A, C, B, k, seed, dA);
+        f.loss_part = w.loss_part;
+        f.seg_loss = w.seg_loss;
+        f.loss = loss;
+        return frob_fused(f, st);
+    }
     // forward: C = A B
-    NSD_TRY(segreduce(rows_params(A, B, k, 1.f, C, w.sgr), st));
+    NSD_TRY(segreduce(rows_params(A, B, k, 1.f, C, w.part), st));
     // dA = seed * <C_i, B_j> on the pattern; loss = 1/2 sum_p A_p <C_i, B_j> = 1/2 ||C||^2
     SddmmParams sp = sddmm_params(A, C, B, k, seed, dA);
     sp.w = A->val;
     sp.beta = 0.5;
-    sp.part = w.part;
+    sp.part = w.loss_part;
     NSD_TRY(sddmm(sp, st));
     NSD_TRY(finish_loss(sp, loss, st));
     // dB = seed * A^T C
-    return segreduce(cols_params(A, At, C, k, seed, dB, w.sgr), st);
+    return segreduce(cols_params(A, At, C, k, seed, dB, w.part), st);
 }
 
 nsd_status nsd_loss_bilinear(const nsd_csr *A, const nsd_csc *At, const float *H,
                              const float *G, int32_t k, float seed, double *loss, float *dA,
                              float *dH, void *ws, size_t ws_bytes, void *stream) {
-    NSD_TRY(check_csr(A, true));
+    NSD_TRY(check_csr(A, true, false));
     NSD_TRY(check_csc(At, A));
     NSD_REQUIRE(k >= 1, "k = %d < 1", k);
     NSD_REQUIRE(loss != nullptr, "loss is NULL");
     NSD_REQUIRE(A->ncols == 0 || dH != nullptr, "dH is NULL");
     NSD_REQUIRE(A->nnz == 0 || (H && G && dA), "H/G/dA is NULL");
     ComputeWs w;
-    NSD_TRY(carve_compute(ws, ws_bytes, A->nnz, k, &w));
+    NSD_TRY(carve_compute(ws, ws_bytes, A, At, k, &w));
     hipStream_t st = as_stream(stream);
     // dA = seed * <G_i, H_j>; loss = sum_p A_p <G_i, H_j>
     SddmmParams sp = sddmm_params(A, G, H, k, seed, dA);
     sp.w = A->val;
     sp.beta = 1.0;
-    sp.part = w.part;
+    sp.part = w.loss_part;
     NSD_TRY(sddmm(sp, st));
     NSD_TRY(finish_loss(sp, loss, st));
     // dH = seed * A^T G
-    return segreduce(cols_params(A, At, G, k, seed, dH, w.sgr), st);
+    return segreduce(cols_params(A, At, G, k, seed, dH, w.part), st);
 }
 
 }  // extern "C"

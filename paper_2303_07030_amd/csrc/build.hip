@@ -18,8 +18,18 @@ constexpr int kScanThreads = 256;
 constexpr int kScanItems = 8;
 constexpr int kScanTile = kScanThreads * kScanItems;
 
+struct OpSum {
+    static constexpr int kIdentity = 0;
+    __device__ static int apply(int a, int b) { return a + b; }
+};
+struct OpMax {
+    static constexpr int kIdentity = INT32_MIN;
+    __device__ static int apply(int a, int b) { return a > b ? a : b; }
+};
+
 // Exclusive scan of one value per thread across the block; returns the
 // block total through *total.
+template <class Op>
 __device__ int block_exclusive_scan(int v, int *total) {
     __shared__ int wave_tot[kScanThreads / kWave];
     const int lane = threadIdx.x & (kWave - 1);
@@ -28,53 +38,58 @@ __device__ int block_exclusive_scan(int v, int *total) {
 #pragma unroll
     for (int d = 1; d < kWave; d <<= 1) {
         int t = __shfl_up(inc, d, kWave);
-        if (lane >= d) inc += t;
+        if (lane >= d) inc = Op::apply(t, inc);
     }
+    int exc = __shfl_up(inc, 1, kWave);
+    if (lane == 0) exc = Op::kIdentity;
     if (lane == kWave - 1) wave_tot[wave] = inc;
     __syncthreads();
-    int base = 0, all = 0;
+    int base = Op::kIdentity, all = Op::kIdentity;
 #pragma unroll
     for (int w = 0; w < kScanThreads / kWave; ++w) {
-        if (w < wave) base += wave_tot[w];
-        all += wave_tot[w];
+        if (w < wave) base = Op::apply(base, wave_tot[w]);
+        all = Op::apply(all, wave_tot[w]);
     }
     __syncthreads();
     *total = all;
-    return base + inc - v;
+    return Op::apply(base, exc);
 }
 
+template <class Op>
 __global__ __launch_bounds__(kScanThreads) void scan_reduce_kernel(const int32_t *in, int64_t n,
                                                                    int32_t *sums) {
     const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
-    int s = 0;
+    int s = Op::kIdentity;
 #pragma unroll
     for (int i = 0; i < kScanItems; ++i)
-        if (base + i < n) s += in[base + i];
+        if (base + i < n) s = Op::apply(s, in[base + i]);
     int total;
-    block_exclusive_scan(s, &total);
+    block_exclusive_scan<Op>(s, &total);
     if (threadIdx.x == 0) sums[blockIdx.x] = total;
 }
 
+template <class Op>
 __global__ __launch_bounds__(kScanThreads) void scan_tile_kernel(const int32_t *in, int32_t *out,
                                                                  int64_t n, const int32_t *offs,
                                                                  int32_t *total_dev) {
     const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
     int v[kScanItems];
-    int s = 0;
+    int s = Op::kIdentity;
 #pragma unroll
     for (int i = 0; i < kScanItems; ++i) {
-        v[i] = base + i < n ? in[base + i] : 0;
-        s += v[i];
+        v[i] = base + i < n ? in[base + i] : Op::kIdentity;
+        s = Op::apply(s, v[i]);
     }
     int total;
-    int run = block_exclusive_scan(s, &total) + (offs ? offs[blockIdx.x] : 0);
+    const int pre = offs ? offs[blockIdx.x] : Op::kIdentity;
+    int run = Op::apply(pre, block_exclusive_scan<Op>(s, &total));
 #pragma unroll
     for (int i = 0; i < kScanItems; ++i) {
         if (base + i < n) out[base + i] = run;
-        run += v[i];
+        run = Op::apply(run, v[i]);
     }
     if (total_dev && blockIdx.x == gridDim.x - 1 && threadIdx.x == 0)
-        *total_dev = (offs ? offs[blockIdx.x] : 0) + total;
+        *total_dev = Op::apply(pre, total);
 }
 
 size_t scan_ws_bytes(int64_t n) {
@@ -87,29 +102,33 @@ size_t scan_ws_bytes(int64_t n) {
     return c.bytes();
 }
 
+template <class Op>
 static nsd_status scan_level(const int32_t *in, int32_t *out, int64_t n, int32_t *total_dev,
                              Carver &c, hipStream_t st) {
     const int64_t tiles = ceil_div(n, kScanTile);
     if (tiles <= 1) {
-        scan_tile_kernel<<<1, kScanThreads, 0, st>>>(in, out, n, nullptr, total_dev);
+        scan_tile_kernel<Op><<<1, kScanThreads, 0, st>>>(in, out, n, nullptr, total_dev);
         return check_launch("scan_tile_kernel");
     }
     int32_t *sums = c.take<int32_t>(tiles);
-    scan_reduce_kernel<<<tiles, kScanThreads, 0, st>>>(in, n, sums);
+    scan_reduce_kernel<Op><<<tiles, kScanThreads, 0, st>>>(in, n, sums);
     NSD_TRY(check_launch("scan_reduce_kernel"));
-    NSD_TRY(scan_level(sums, sums, tiles, nullptr, c, st));
-    scan_tile_kernel<<<tiles, kScanThreads, 0, st>>>(in, out, n, sums, total_dev);
+    NSD_TRY(scan_level<Op>(sums, sums, tiles, nullptr, c, st));
+    scan_tile_kernel<Op><<<tiles, kScanThreads, 0, st>>>(in, out, n, sums, total_dev);
     return check_launch("scan_tile_kernel");
 }
 
+// n == 0 is not allowed here (the callers handle empty inputs themselves).
 nsd_status scan_exclusive(const int32_t *in, int32_t *out, int64_t n, int32_t *total_dev,
                           void *ws, hipStream_t st) {
-    if (n <= 0) {
-        if (total_dev) NSD_HIP(hipMemsetAsync(total_dev, 0, sizeof(int32_t), st));
-        return NSD_OK;
-    }
     Carver c(ws);
-    return scan_level(in, out, n, total_dev, c, st);
+    return scan_level<OpSum>(in, out, n, total_dev, c, st);
+}
+
+nsd_status scan_exclusive_max(const int32_t *in, int32_t *out, int64_t n, void *ws,
+                              hipStream_t st) {
+    Carver c(ws);
+    return scan_level<OpMax>(in, out, n, nullptr, c, st);
 }
 
 // ------------------------------------------------------------ radix sort

@@ -146,6 +146,9 @@ inline WidthPlan width_plan(int k, bool vec_ok) {
 size_t scan_ws_bytes(int64_t n);
 nsd_status scan_exclusive(const int32_t *in, int32_t *out, int64_t n, int32_t *total_dev,
                           void *ws, hipStream_t st);
+// Exclusive max-scan (identity INT32_MIN), same workspace as scan_exclusive.
+nsd_status scan_exclusive_max(const int32_t *in, int32_t *out, int64_t n, void *ws,
+                              hipStream_t st);
 
 // Stable LSD radix sort of (key, payload) by key in [0, max_key); payload_in
 // NULL means the identity 0..n-1.  Results land in key_out / payload_out.

@@ -1,26 +1,27 @@
-// Segmented gather-reduce and sampled dense-dense products.
+// Segmented gather-reduce, sampled dense-dense products and the fused row
+// pass of the SpMM gradient.
 //
 // Gather-reduce computes, for every segment s of a sorted sparse operand
 // (a row of a CSR, or a column of its CSC),
 //     out[s, :] = alpha * sum_{p in s} w_p * X[idx_p, :]
 // which is SpMV / SpMM (segments = rows, idx = colind, w = val) and the
 // transposed product A^T G (segments = columns, idx = rowind, w = val[perm]).
-// It is the `sum(<j, a> in row) a * X(j)` of the paper's matrix product with
-// the singleton insert "+=" of its code generation (Section 5.5), done so that
-// every output is written once, with no atomics.
+// It is the `sum(<j, a> in row) a * X(j)` of the matrix product in Logical
+// SDQLite (Section 3) with the singleton "+=" of the paper's code generation
+// (Section 5.5), arranged so that every output is written once, without
+// atomics.
 //
-// Load balance: the nnz are cut into equal slots of L entries, independent of
-// where rows begin (nnz-split).  A slot is G lanes holding VEC floats of a
-// dense row each (VEC * G = up to 256 columns per pass).  Inside a slot the
-// entries are walked in order with U gathers in flight; a row that starts and
-// ends inside the slot is written directly (alpha applied), and the partial
-// sums of rows that cross a slot boundary go to per-slot carries.  A second
-// kernel adds, for every row that spans slots, its owner's partial and the
-// following slots' partials in slot order.  Power-law rows therefore cost the
-// same per nnz as short ones, and results are bitwise deterministic.
-//
-// Empty rows are written as zeros by the slot that holds the entry just
-// before them (slot 0 for leading empty rows, the last slot for trailing ones).
+// Load balance comes from the operand's work plan (nsd_plan): every work item
+// is either a run of whole short segments or one chunk of a long segment.  A
+// slot of G lanes (VEC floats of a dense row each; VEC * G up to 256 columns
+// per pass) walks its item in batches of U entries.  The entry metadata
+// (segment, gathered row, weight) of the next batch is loaded while the
+// current batch's dense rows are in flight, so one memory round trip is paid
+// per batch.  A segment that ends inside the item is written directly; a
+// chunk of a long segment leaves one partial sum, and a second kernel adds a
+// long segment's chunk partials in chunk order, one wave per segment (one
+// workgroup for huge segments).  Empty segments are zero-filled by extra
+// blocks of the first launch.  Results are bitwise reproducible.
 #include <algorithm>
 
 #include "nsd_internal.hpp"
@@ -29,159 +30,212 @@
 namespace nsd {
 
 constexpr int kBlock = 256;
+constexpr int kBlockWaves = kBlock / kWave;
+constexpr int kHugeChunks = 64;  // matches the plan builder
+
+// --------------------------------------------------------- entry metadata
+
+template <int U>
+struct Meta {
+    int r[U], c[U];
+    float w[U];
+};
+
+// Metadata of entries [p, p + U) of an item ending at b0; entries past the
+// end become padding: same segment as the item's last entry (no flush), its
+// gathered row (a valid address) and weight 0.
+template <int U>
+__device__ __forceinline__ void load_meta(const SgrParams &a, int64_t p, int64_t b0, int last_r,
+                                          int last_c, Meta<U> &m) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int64_t q = p + u;
+        if (q < b0) {
+            m.r[u] = a.segidx[q];
+            m.c[u] = a.idx[q];
+            m.w[u] = a.w ? (a.wperm ? a.w[a.wperm[q]] : a.w[q]) : 1.f;
+        } else {
+            m.r[u] = last_r;
+            m.c[u] = last_c;
+            m.w[u] = 0.f;
+        }
+    }
+}
+
+// One slot's walk over item s (entries [a0, b0)).  Complete segments are
+// written as alpha * sum; a segment cut by the item's end or start goes to
+// part[s].  `seg_done(segment, unscaled sum)` is called for every segment
+// completed inside the item.
+template <int VEC, int G, int U, class SegDone>
+__device__ __forceinline__ void sgr_walk(const SgrParams &a, int64_t s, int col, bool on,
+                                         SegDone seg_done) {
+    const int64_t k = a.k;
+    const int64_t a0 = a.plan.item_ptr[s];
+    const int64_t b0 = a.plan.item_ptr[s + 1];
+    const int last_r = a.segidx[b0 - 1];
+    const int last_c = a.idx[b0 - 1];
+    int row = a.segidx[a0];
+    bool carry = a0 > 0 && a.segidx[a0 - 1] == row;  // a chunk after the first one
+
+    Vec<VEC> acc;
+    acc.zero();
+    auto flush = [&]() {
+        if (carry) {
+            if (on) acc.store(a.part + s * k + col);
+        } else {
+            seg_done(row, acc);
+            if (on) {
+                Vec<VEC> t = acc;
+                t.scale(a.alpha);
+                t.store(a.out + (int64_t)row * k + col);
+            }
+        }
+    };
+
+    Meta<U> cur, nxt;
+    load_meta(a, a0, b0, last_r, last_c, cur);
+    for (int64_t p = a0; p < b0; p += U) {
+        if (p + U < b0) load_meta(a, p + U, b0, last_r, last_c, nxt);
+        Vec<VEC> xv[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (a.X && on) xv[u].load(a.X + (int64_t)cur.c[u] * k + col);
+            else xv[u].ones();
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (cur.r[u] != row) {
+                flush();
+                row = cur.r[u];
+                carry = false;
+                acc.zero();
+            }
+            acc.fma(cur.w[u], xv[u]);
+        }
+        cur = nxt;
+    }
+    if (b0 == a.nnz || a.segidx[b0] != row) {
+        flush();
+    } else if (on) {
+        acc.store(a.part + s * k + col);  // the first chunk of a long segment
+    }
+}
+
+template <int VEC>
+__device__ __forceinline__ void zero_segment(const SgrParams &a, int64_t e, int col, bool on) {
+    if (e < a.plan.nempty && on) {
+        Vec<VEC> z;
+        z.zero();
+        z.store(a.out + (int64_t)a.plan.empty_seg[e] * a.k + col);
+    }
+}
+
+struct NoSegDone {
+    template <int VEC>
+    __device__ void operator()(int, const Vec<VEC> &) const {}
+};
 
 template <int VEC, int G, int U>
 __global__ __launch_bounds__(kBlock) void sgr_main_kernel(SgrParams a) {
     constexpr int kSlots = kBlock / G;
     const int g = threadIdx.x % G;
-    const int64_t s = (int64_t)blockIdx.x * kSlots + threadIdx.x / G;
-    if (s >= a.nslots) return;
     const int col = blockIdx.y * (G * VEC) + g * VEC;
     const bool on = col < a.k;
-    const int64_t k = a.k;
-    const int64_t a0 = s * a.L;
-    const int64_t b0 = min(a0 + (int64_t)a.L, (int64_t)a.nnz);
-
-    int row = a.segidx[a0];
-    bool carry = a0 > 0 && a.segidx[a0 - 1] == row;
-
-    Vec<VEC> zero;
-    zero.zero();
-    auto zero_rows = [&](int r0, int r1) {
-        if (on)
-            for (int r = r0; r < r1; ++r) zero.store(a.out + (int64_t)r * k + col);
-    };
-    Vec<VEC> acc;
-    acc.zero();
-    auto flush = [&]() {
-        if (!on) return;
-        if (carry) {
-            acc.store(a.pfirst + s * k + col);
-        } else {
-            Vec<VEC> t = acc;
-            t.scale(a.alpha);
-            t.store(a.out + (int64_t)row * k + col);
-        }
-    };
-    auto weight = [&](int64_t p) -> float {
-        if (!a.w) return 1.f;
-        return a.wperm ? a.w[a.wperm[p]] : a.w[p];
-    };
-
-    if (s == 0) zero_rows(0, row);
-
-    int64_t p = a0;
-    for (; p + U <= b0; p += U) {
-        int r[U], c[U];
-        float wt[U];
-        Vec<VEC> xv[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            r[u] = a.segidx[p + u];
-            c[u] = a.idx[p + u];
-            wt[u] = weight(p + u);
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            if (a.X && on) xv[u].load(a.X + (int64_t)c[u] * k + col);
-            else xv[u].ones();
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            if (r[u] != row) {
-                flush();
-                zero_rows(row + 1, r[u]);
-                row = r[u];
-                carry = false;
-                acc.zero();
-            }
-            acc.fma(wt[u], xv[u]);
-        }
+    if ((int)blockIdx.x >= a.item_blocks) {
+        zero_segment<VEC>(a, (int64_t)(blockIdx.x - a.item_blocks) * kSlots + threadIdx.x / G,
+                          col, on);
+        return;
     }
-    for (; p < b0; ++p) {
-        const int r = a.segidx[p];
-        const int c = a.idx[p];
-        const float wt = weight(p);
-        Vec<VEC> xv;
-        if (a.X && on) xv.load(a.X + (int64_t)c * k + col);
-        else xv.ones();
-        if (r != row) {
-            flush();
-            zero_rows(row + 1, r);
-            row = r;
-            carry = false;
-            acc.zero();
-        }
-        acc.fma(wt, xv);
-    }
-
-    const bool ends = b0 == a.nnz || a.segidx[b0] != row;
-    const bool lead = g == 0 && blockIdx.y == 0;
-    if (ends) {
-        flush();
-        zero_rows(row + 1, b0 == a.nnz ? a.nseg : a.segidx[b0]);
-        if (lead) a.span[s] = -1;
-    } else if (carry) {
-        if (on) acc.store(a.pfirst + s * k + col);
-        if (lead) a.span[s] = -1;
-    } else {
-        if (on) acc.store(a.plast + s * k + col);
-        if (lead) a.span[s] = row;
-    }
+    const int64_t s = (int64_t)blockIdx.x * kSlots + threadIdx.x / G;
+    if (s >= a.plan.nitems) return;
+    sgr_walk<VEC, G, U>(a, s, col, on, NoSegDone{});
 }
 
-// One block per slot.  For a slot that owns a row continuing past its end,
-// out[row] = alpha * (plast[s] + sum_{t = s+1..t_end} pfirst[t]); the four
-// waves take interleaved t and are added in a fixed order.
-template <int VEC>
-__global__ __launch_bounds__(kBlock) void sgr_fix_kernel(SgrParams a) {
-    const int64_t s = blockIdx.x;
-    const int r = a.span[s];
-    if (r < 0) return;
-    const int64_t k = a.k;
-    const int64_t t_end = ((int64_t)a.segptr[r + 1] - 1) / a.L;
+// ----------------------------------------------------------- long segments
+
+// out[seg] = alpha * sum of the segment's chunk partials, in chunk order per
+// row group, the groups then combined by a fixed butterfly.  Blocks below
+// wave_blocks give one wave to each non-huge long segment; the blocks after
+// them give a whole block to each huge segment.  When seg_loss is given,
+// beta * ||out[seg]||^2 is stored for every long segment.
+template <int VEC, int G>
+__global__ __launch_bounds__(kBlock) void sgr_fix_kernel(SgrParams a, int wave_blocks,
+                                                         double *seg_loss, double beta) {
+    constexpr int RG = kWave / G;  // row groups per wave
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-    __shared__ float part[kBlock / kWave][kWave * VEC];
-    for (int c0 = 0; c0 < a.k; c0 += kWave * VEC) {
-        const int col = c0 + lane * VEC;
+    const int q = lane / G, g = lane % G;
+    const int64_t k = a.k;
+    const int L = a.plan.item_len;
+    __shared__ float red[kBlockWaves][G * VEC];
+    const bool huge = (int)blockIdx.x >= wave_blocks;
+    int64_t i;
+    int nsum, qq;  // number of groups sharing the chunks, this lane's group
+    if (!huge) {
+        i = (int64_t)blockIdx.x * kBlockWaves + wave;
+        if (i >= a.plan.nlong) return;
+        nsum = RG;
+        qq = q;
+    } else {
+        i = a.plan.huge_idx[blockIdx.x - wave_blocks];
+        nsum = RG * kBlockWaves;
+        qq = wave * RG + q;
+    }
+    const int seg = a.plan.long_seg[i];
+    const int64_t s0 = a.plan.long_first[i];
+    const int64_t n = ((int64_t)a.segptr[seg + 1] - a.segptr[seg] + L - 1) / L;
+    if (!huge && n > kHugeChunks) return;
+    double lsq = 0.0;
+    for (int c0 = 0; c0 < a.k; c0 += G * VEC) {
+        const int col = c0 + g * VEC;
         const bool on = col < a.k;
-        Vec<VEC> acc[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) acc[i].zero();
+        Vec<VEC> acc[2];
+        acc[0].zero();
+        acc[1].zero();
         if (on) {
-            int64_t t = s + 1 + wave;
-            for (; t + 12 <= t_end; t += 16) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    Vec<VEC> x;
-                    x.load(a.pfirst + (t + 4 * i) * k + col);
-                    acc[i].add(x);
-                }
+            int64_t t = qq;
+            for (; t + nsum < n; t += 2 * nsum) {
+                Vec<VEC> x0, x1;
+                x0.load(a.part + (s0 + t) * k + col);
+                x1.load(a.part + (s0 + t + nsum) * k + col);
+                acc[0].add(x0);
+                acc[1].add(x1);
             }
-            for (int i = 0; t <= t_end; t += 4, ++i) {
+            if (t < n) {
                 Vec<VEC> x;
-                x.load(a.pfirst + t * k + col);
-                acc[i & 3].add(x);
+                x.load(a.part + (s0 + t) * k + col);
+                acc[0].add(x);
             }
         }
         acc[0].add(acc[1]);
-        acc[2].add(acc[3]);
-        acc[0].add(acc[2]);
 #pragma unroll
-        for (int i = 0; i < VEC; ++i) part[wave][lane * VEC + i] = acc[0].v[i];
-        __syncthreads();
-        if (wave == 0 && on) {
-            Vec<VEC> tot;
-            tot.load(a.plast + s * k + col);
+        for (int m = G; m < kWave; m <<= 1)
 #pragma unroll
-            for (int i = 0; i < VEC; ++i) {
-                const int e = lane * VEC + i;
-                tot.v[i] += (part[0][e] + part[1][e]) + (part[2][e] + part[3][e]);
+            for (int e = 0; e < VEC; ++e) acc[0].v[e] += shfl_xor(acc[0].v[e], m);
+        if (huge) {
+            if (q == 0)
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) red[wave][g * VEC + e] = acc[0].v[e];
+            __syncthreads();
+            if (wave == 0) {
+#pragma unroll
+                for (int e = 0; e < VEC; ++e)
+                    acc[0].v[e] = (red[0][g * VEC + e] + red[1][g * VEC + e]) +
+                                  (red[2][g * VEC + e] + red[3][g * VEC + e]);
             }
-            tot.scale(a.alpha);
-            tot.store(a.out + (int64_t)r * k + col);
+            __syncthreads();
         }
-        __syncthreads();
+        if ((!huge || wave == 0) && q == 0 && on) {
+            acc[0].scale(a.alpha);
+            acc[0].store(a.out + (int64_t)seg * k + col);
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) lsq += (double)acc[0].v[e] * acc[0].v[e];
+        }
+    }
+    if (seg_loss) {
+        // only the lanes of group 0 (of wave 0 for a huge segment) hold squares
+#pragma unroll
+        for (int m = 1; m < kWave; m <<= 1) lsq += __shfl_xor(lsq, m, kWave);
+        if (lane == 0 && (!huge || wave == 0)) seg_loss[i] = beta * lsq;
     }
 }
 
@@ -191,61 +245,68 @@ __global__ void fill_zero_kernel(float *out, int64_t n) {
     if (i < n) out[i] = 0.f;
 }
 
-int choose_slot_len(int64_t nnz, int slots_per_wave) {
-    // aim for ~8192 waves (8 per SIMD on 256 CUs); 16 <= L <= 256
-    const int64_t target = 8192LL * slots_per_wave;
-    int L = 16;
-    while (L < 256 && (int64_t)L * 2 * target <= nnz) L <<= 1;
-    return L;
-}
-
-SgrShape sgr_shape(int64_t nnz, int k) {
-    SgrShape sh;
-    sh.wp = width_plan(k, true);
-    sh.L = choose_slot_len(nnz, kWave / sh.wp.g);
-    sh.nslots = nnz > 0 ? ceil_div(nnz, sh.L) : 0;
-    return sh;
-}
-
-void sgr_carve(Carver &c, int64_t nnz, int k, SgrParams *p) {
-    const SgrShape sh = sgr_shape(nnz, k);
-    // sized for the smallest slot length either lane layout can choose
-    const SgrShape sh1 = sgr_shape_vec1(nnz, k);
-    const int64_t ns = std::max<int64_t>({sh.nslots, sh1.nslots, 1});
-    float *pf = c.take<float>(ns * k);
-    float *pl = c.take<float>(ns * k);
-    int32_t *sp = c.take<int32_t>(ns);
-    if (p) {
-        p->pfirst = pf;
-        p->plast = pl;
-        p->span = sp;
-    }
-}
-
-// Slot length and count for the lane layout segreduce will launch.
-static void sgr_finalize_shape(SgrParams &a, const WidthPlan &wp) {
-    a.L = choose_slot_len(a.nnz, kWave / wp.g);
-    a.nslots = (int32_t)ceil_div(a.nnz, a.L);
-}
-
-template <int VEC, int G>
-static void launch_sgr_vg(const SgrParams &a, hipStream_t st) {
-    constexpr int U = G >= 16 ? 4 : 8;
-    constexpr int kSlots = kBlock / G;
-    dim3 grid((unsigned)ceil_div(a.nslots, kSlots), (unsigned)ceil_div(a.k, G * VEC));
-    sgr_main_kernel<VEC, G, U><<<grid, kBlock, 0, st>>>(a);
-    sgr_fix_kernel<VEC><<<(unsigned)a.nslots, kBlock, 0, st>>>(a);
-}
-
-SgrShape sgr_shape_vec1(int64_t nnz, int k) {
-    SgrShape sh;
-    sh.wp = width_plan(k, false);
-    sh.L = choose_slot_len(nnz, kWave / sh.wp.g);
-    sh.nslots = nnz > 0 ? ceil_div(nnz, sh.L) : 0;
-    return sh;
+size_t sgr_part_bytes(const nsd_plan &plan, int k) {
+    return (size_t)std::max<int64_t>(plan.nitems, 1) * (size_t)k * sizeof(float);
 }
 
 static bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+template <int G>
+constexpr int sgr_unroll() {
+    return G >= 16 ? 4 : 8;
+}
+
+template <int VEC, int G>
+static nsd_status launch_fix(const SgrParams &a, double *seg_loss, double beta, hipStream_t st) {
+    if (a.plan.nlong == 0) return NSD_OK;
+    const int wave_blocks = (int)ceil_div(a.plan.nlong, kBlockWaves);
+    sgr_fix_kernel<VEC, G><<<wave_blocks + a.plan.nhuge, kBlock, 0, st>>>(a, wave_blocks, seg_loss,
+                                                                         beta);
+    return check_launch("sgr_fix_kernel");
+}
+
+template <int VEC, int G>
+static nsd_status launch_sgr_vg(SgrParams a, hipStream_t st) {
+    constexpr int kSlots = kBlock / G;
+    a.item_blocks = (int32_t)ceil_div(a.plan.nitems, kSlots);
+    const int64_t empty_blocks = ceil_div(a.plan.nempty, kSlots);
+    dim3 grid((unsigned)(a.item_blocks + empty_blocks), (unsigned)ceil_div(a.k, G * VEC));
+    sgr_main_kernel<VEC, G, sgr_unroll<G>()><<<grid, kBlock, 0, st>>>(a);
+    NSD_TRY(check_launch("sgr_main_kernel"));
+    return launch_fix<VEC, G>(a, nullptr, 0.0, st);
+}
+
+// Calls f.template operator()<VEC, G>() for the lane layout wp.
+template <class F>
+static nsd_status dispatch_width(const WidthPlan &wp, F &f) {
+    if (wp.vec == 4) {
+        switch (wp.g) {
+            case 1: return f.template operator()<4, 1>();
+            case 2: return f.template operator()<4, 2>();
+            case 4: return f.template operator()<4, 4>();
+            case 8: return f.template operator()<4, 8>();
+            case 16: return f.template operator()<4, 16>();
+            case 32: return f.template operator()<4, 32>();
+            default: return f.template operator()<4, 64>();
+        }
+    }
+    switch (wp.g) {
+        case 1: return f.template operator()<1, 1>();
+        case 2: return f.template operator()<1, 2>();
+        case 4: return f.template operator()<1, 4>();
+        case 8: return f.template operator()<1, 8>();
+        case 16: return f.template operator()<1, 16>();
+        case 32: return f.template operator()<1, 32>();
+        default: return f.template operator()<1, 64>();
+    }
+}
+
+struct SgrLauncher {
+    SgrParams a;
+    hipStream_t st;
+    template <int VEC, int G>
+    nsd_status operator()() { return launch_sgr_vg<VEC, G>(a, st); }
+};
 
 nsd_status segreduce(SgrParams a, hipStream_t st) {
     const int64_t total = (int64_t)a.nseg * a.k;
@@ -255,29 +316,8 @@ nsd_status segreduce(SgrParams a, hipStream_t st) {
     }
     // float4 lanes need 16-byte aligned dense rows; otherwise use scalar lanes
     const WidthPlan wp = width_plan(a.k, aligned16(a.out) && (!a.X || aligned16(a.X)));
-    sgr_finalize_shape(a, wp);
-    if (wp.vec == 4) {
-        switch (wp.g) {
-            case 1: launch_sgr_vg<4, 1>(a, st); break;
-            case 2: launch_sgr_vg<4, 2>(a, st); break;
-            case 4: launch_sgr_vg<4, 4>(a, st); break;
-            case 8: launch_sgr_vg<4, 8>(a, st); break;
-            case 16: launch_sgr_vg<4, 16>(a, st); break;
-            case 32: launch_sgr_vg<4, 32>(a, st); break;
-            default: launch_sgr_vg<4, 64>(a, st); break;
-        }
-    } else {
-        switch (wp.g) {
-            case 1: launch_sgr_vg<1, 1>(a, st); break;
-            case 2: launch_sgr_vg<1, 2>(a, st); break;
-            case 4: launch_sgr_vg<1, 4>(a, st); break;
-            case 8: launch_sgr_vg<1, 8>(a, st); break;
-            case 16: launch_sgr_vg<1, 16>(a, st); break;
-            case 32: launch_sgr_vg<1, 32>(a, st); break;
-            default: launch_sgr_vg<1, 64>(a, st); break;
-        }
-    }
-    return check_launch("segreduce");
+    SgrLauncher f{a, st};
+    return dispatch_width(wp, f);
 }
 
 // ------------------------------------------------------------------ SDDMM
@@ -310,74 +350,108 @@ __device__ __forceinline__ float transpose_reduce(float (&v)[U], int lane) {
     return v[0];
 }
 
-template <int VEC, int G, int U>
-__global__ __launch_bounds__(kBlock) void sddmm_kernel(SddmmParams a) {
-    constexpr int kSlots = kBlock / G;
-    const int lane = threadIdx.x % kWave;
-    const int g = threadIdx.x % G;
-    const int64_t s = (int64_t)blockIdx.x * kSlots + threadIdx.x / G;
-    const int64_t k = a.k;
-    double lsum = 0.0;
-    if (s < a.nslots) {
-        const int64_t a0 = s * a.L;
-        const int64_t b0 = min(a0 + (int64_t)a.L, (int64_t)a.nnz);
-        for (int64_t p = a0; p < b0; p += U) {
-            int rr[U], cc[U];
-            float part[U];
+// Block total of per-lane fp64 values, in a fixed order.
+__device__ __forceinline__ double block_sum(double v) {
+    __shared__ double wsum[kBlockWaves];
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const bool valid = p + u < b0;
-                rr[u] = valid ? a.rowidx[p + u] : 0;
-                cc[u] = valid ? a.colind[p + u] : 0;
-                part[u] = 0.f;
-            }
-            for (int c0 = 0; c0 < a.k; c0 += G * VEC) {
-                const int col = c0 + g * VEC;
-                const bool on = col < a.k;
+    for (int m = kWave / 2; m >= 1; m >>= 1) v += __shfl_xor(v, m, kWave);
+    if (threadIdx.x % kWave == 0) wsum[threadIdx.x / kWave] = v;
+    __syncthreads();
+    const double t = (wsum[0] + wsum[1]) + (wsum[2] + wsum[3]);
+    __syncthreads();
+    return t;
+}
+
+// SDDMM of entries [a0, b0) by one slot:
+//   out[p] = alpha * <X[rowidx[p]], Y[colind[p]]>, lsum += w[p] * <...>.
+template <int VEC, int G, int U>
+__device__ __forceinline__ void sddmm_range(const SddmmParams &a, int64_t a0, int64_t b0,
+                                            int lane, double &lsum) {
+    const int g = lane % G;
+    const int64_t k = a.k;
+    const int last_r = a.rowidx[b0 - 1], last_c = a.colind[b0 - 1];
+    int rr[U], cc[U], nr[U], nc[U];
+    auto load = [&](int64_t p, int (&r)[U], int (&c)[U]) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const bool valid = p + u < b0;
+            r[u] = valid ? a.rowidx[p + u] : last_r;
+            c[u] = valid ? a.colind[p + u] : last_c;
+        }
+    };
+    load(a0, rr, cc);
+    for (int64_t p = a0; p < b0; p += U) {
+        if (p + U < b0) load(p + U, nr, nc);
+        float part[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) part[u] = 0.f;
+        for (int c0 = 0; c0 < a.k; c0 += G * VEC) {
+            const int col = c0 + g * VEC;
+            if (col < a.k) {
                 Vec<VEC> xv[U], yv[U];
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
-                    if (on && p + u < b0) {
-                        if (a.X) xv[u].load(a.X + (int64_t)rr[u] * k + col);
-                        else xv[u].ones();
-                        yv[u].load(a.Y + (int64_t)cc[u] * k + col);
-                    } else {
-                        xv[u].zero();
-                        yv[u].zero();
-                    }
+                    if (a.X) xv[u].load(a.X + (int64_t)rr[u] * k + col);
+                    else xv[u].ones();
+                    yv[u].load(a.Y + (int64_t)cc[u] * k + col);
                 }
 #pragma unroll
                 for (int u = 0; u < U; ++u) part[u] += xv[u].dot(yv[u]);
             }
-            if constexpr (G == 1) {
+        }
+        if constexpr (G == 1) {
 #pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    if (p + u < b0) {
-                        a.out[p + u] = a.alpha * part[u];
-                        if (a.w) lsum += (double)a.w[p + u] * (double)part[u];
-                    }
-                }
-            } else {
-                const float tot = transpose_reduce<G, U>(part, lane);
-                constexpr int kRep = G / U;
-                const int64_t q = p + g / kRep;
-                if (g % kRep == 0 && q < b0) {
-                    a.out[q] = a.alpha * tot;
-                    if (a.w) lsum += (double)a.w[q] * (double)tot;
+            for (int u = 0; u < U; ++u) {
+                if (p + u < b0) {
+                    a.out[p + u] = a.alpha * part[u];
+                    if (a.w) lsum += (double)a.w[p + u] * (double)part[u];
                 }
             }
+        } else {
+            const float tot = transpose_reduce<G, U>(part, lane);
+            constexpr int kRep = G / U;
+            const int64_t q = p + g / kRep;
+            if (g % kRep == 0 && q < b0) {
+                a.out[q] = a.alpha * tot;
+                if (a.w) lsum += (double)a.w[q] * (double)tot;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            rr[u] = nr[u];
+            cc[u] = nc[u];
         }
     }
-    if (a.part) {
-        // block total of the fused loss, fixed order
-        __shared__ double wsum[kBlock / kWave];
-#pragma unroll
-        for (int m = kWave / 2; m >= 1; m >>= 1) lsum += __shfl_xor(lsum, m, kWave);
-        if (lane == 0) wsum[threadIdx.x / kWave] = lsum;
-        __syncthreads();
-        if (threadIdx.x == 0)
-            a.part[blockIdx.x] = a.beta * ((wsum[0] + wsum[1]) + (wsum[2] + wsum[3]));
+}
+
+template <int G>
+constexpr int sddmm_unroll() {
+    return G >= 4 ? 4 : (G == 1 ? 4 : G);
+}
+
+// Slots over equal entry ranges (nnz-split): no segment structure needed.
+template <int VEC, int G, int U>
+__global__ __launch_bounds__(kBlock) void sddmm_kernel(SddmmParams a) {
+    constexpr int kSlots = kBlock / G;
+    const int lane = threadIdx.x % kWave;
+    const int64_t s = (int64_t)blockIdx.x * kSlots + threadIdx.x / G;
+    double lsum = 0.0;
+    if (s < a.nslots) {
+        const int64_t a0 = s * a.L;
+        sddmm_range<VEC, G, U>(a, a0, min(a0 + (int64_t)a.L, (int64_t)a.nnz), lane, lsum);
     }
+    if (a.part) {
+        const double t = block_sum(lsum);
+        if (threadIdx.x == 0) a.part[blockIdx.x] = a.beta * t;
+    }
+}
+
+int choose_slot_len(int64_t nnz, int slots_per_wave) {
+    // aim for ~8192 waves (8 per SIMD on 256 CUs); 16 <= L <= 256
+    const int64_t target = 8192LL * slots_per_wave;
+    int L = 16;
+    while (L < 256 && (int64_t)L * 2 * target <= nnz) L <<= 1;
+    return L;
 }
 
 SddmmShape sddmm_shape(int64_t nnz, int k, bool vec_ok) {
@@ -392,50 +466,46 @@ SddmmShape sddmm_shape(int64_t nnz, int k, bool vec_ok) {
 
 bool sddmm_vec_ok(const SddmmParams &a) { return (!a.X || aligned16(a.X)) && aligned16(a.Y); }
 
-template <int VEC, int G>
-static void launch_sddmm_vg(const SddmmParams &a, int64_t nblocks, hipStream_t st) {
-    constexpr int U = G >= 8 ? 8 : (G == 1 ? 4 : G);
-    sddmm_kernel<VEC, G, U><<<(unsigned)nblocks, kBlock, 0, st>>>(a);
-}
+struct SddmmLauncher {
+    SddmmParams a;
+    int64_t nb;
+    hipStream_t st;
+    template <int VEC, int G>
+    nsd_status operator()() {
+        sddmm_kernel<VEC, G, sddmm_unroll<G>()><<<(unsigned)nb, kBlock, 0, st>>>(a);
+        return check_launch("sddmm_kernel");
+    }
+};
 
 nsd_status sddmm(SddmmParams a, hipStream_t st) {
     const SddmmShape sh = sddmm_shape(a.nnz, a.k, sddmm_vec_ok(a));
     a.L = sh.L;
     a.nslots = (int32_t)sh.nslots;
     if (sh.nblocks == 0) return NSD_OK;
-    if (sh.wp.vec == 4) {
-        switch (sh.wp.g) {
-            case 1: launch_sddmm_vg<4, 1>(a, sh.nblocks, st); break;
-            case 2: launch_sddmm_vg<4, 2>(a, sh.nblocks, st); break;
-            case 4: launch_sddmm_vg<4, 4>(a, sh.nblocks, st); break;
-            case 8: launch_sddmm_vg<4, 8>(a, sh.nblocks, st); break;
-            case 16: launch_sddmm_vg<4, 16>(a, sh.nblocks, st); break;
-            case 32: launch_sddmm_vg<4, 32>(a, sh.nblocks, st); break;
-            default: launch_sddmm_vg<4, 64>(a, sh.nblocks, st); break;
-        }
-    } else {
-        switch (sh.wp.g) {
-            case 1: launch_sddmm_vg<1, 1>(a, sh.nblocks, st); break;
-            case 2: launch_sddmm_vg<1, 2>(a, sh.nblocks, st); break;
-            case 4: launch_sddmm_vg<1, 4>(a, sh.nblocks, st); break;
-            case 8: launch_sddmm_vg<1, 8>(a, sh.nblocks, st); break;
-            case 16: launch_sddmm_vg<1, 16>(a, sh.nblocks, st); break;
-            case 32: launch_sddmm_vg<1, 32>(a, sh.nblocks, st); break;
-            default: launch_sddmm_vg<1, 64>(a, sh.nblocks, st); break;
-        }
-    }
-    return check_launch("sddmm_kernel");
+    SddmmLauncher f{a, sh.nblocks, st};
+    return dispatch_width(sh.wp, f);
 }
 
 // ------------------------------------------------------------ loss total
 
-// One block: strided partial sums per thread, then a fixed tree.
-__global__ __launch_bounds__(kBlock) void loss_finalize_kernel(const double *part, int64_t n,
+// One block: strided partial sums per thread (four independent chains so the
+// loads overlap), then a fixed tree.  Sums part1[0, n1) and part2[0, n2).
+__device__ __forceinline__ double strided_sum(const double *p, int64_t n) {
+    double s[4] = {0.0, 0.0, 0.0, 0.0};
+    int64_t i = threadIdx.x;
+    for (; i + 3 * kBlock < n; i += 4 * kBlock) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) s[j] += p[i + j * kBlock];
+    }
+    for (int j = 0; i < n; i += kBlock, ++j) s[j & 3] += p[i];
+    return (s[0] + s[1]) + (s[2] + s[3]);
+}
+
+__global__ __launch_bounds__(kBlock) void loss_finalize_kernel(const double *part1, int64_t n1,
+                                                               const double *part2, int64_t n2,
                                                                double *loss) {
     __shared__ double sh[kBlock];
-    double s = 0.0;
-    for (int64_t i = threadIdx.x; i < n; i += kBlock) s += part[i];
-    sh[threadIdx.x] = s;
+    sh[threadIdx.x] = strided_sum(part1, n1) + strided_sum(part2, n2);
     __syncthreads();
     for (int w = kBlock / 2; w >= 1; w >>= 1) {
         if ((int)threadIdx.x < w) sh[threadIdx.x] += sh[threadIdx.x + w];
@@ -445,8 +515,120 @@ __global__ __launch_bounds__(kBlock) void loss_finalize_kernel(const double *par
 }
 
 nsd_status loss_finalize(const double *part, int64_t n, double *loss, hipStream_t st) {
-    loss_finalize_kernel<<<1, kBlock, 0, st>>>(part, n, loss);
+    loss_finalize_kernel<<<1, kBlock, 0, st>>>(part, n, nullptr, 0, loss);
     return check_launch("loss_finalize_kernel");
+}
+
+// ------------------------------------------ fused pass of the SpMM gradient
+
+// Row pass of L = 1/2 ||A B||^2 over A's row plan, one slot per item:
+//   phase 1: C rows of the item (gather-reduce), ||C_i||^2 into the block's
+//            loss partial; a long row's chunk leaves a partial instead;
+//   phase 2: for items of whole rows, dA[p] = seed * <C_i, B_j> on the
+//            item's entries, reading back the C rows this slot just wrote.
+// Blocks past the items zero the C rows of empty rows.
+template <int VEC, int G, int U>
+__global__ __launch_bounds__(kBlock) void frob_row_kernel(FrobParams f) {
+    constexpr int kSlots = kBlock / G;
+    const SgrParams &a = f.rows;
+    const int lane = threadIdx.x % kWave;
+    const int g = threadIdx.x % G;
+    const int col = g * VEC;  // k <= G * VEC on this path
+    const bool on = col < a.k;
+    double lsq = 0.0;
+    if ((int)blockIdx.x >= a.item_blocks) {
+        zero_segment<VEC>(a, (int64_t)(blockIdx.x - a.item_blocks) * kSlots + threadIdx.x / G, col,
+                          on);
+    } else {
+        const int64_t s = (int64_t)blockIdx.x * kSlots + threadIdx.x / G;
+        if (s < a.plan.nitems) {
+            sgr_walk<VEC, G, U>(a, s, col, on, [&](int, const Vec<VEC> &c) {
+                if (on)
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) lsq += (double)c.v[e] * c.v[e];
+            });
+            const int64_t a0 = a.plan.item_ptr[s], b0 = a.plan.item_ptr[s + 1];
+            const bool chunk = (a0 > 0 && a.segidx[a0 - 1] == a.segidx[a0]) ||
+                               (b0 < a.nnz && a.segidx[b0] == a.segidx[b0 - 1]);
+            if (!chunk) {
+                double unused = 0.0;
+                sddmm_range<VEC, G, sddmm_unroll<G>()>(f.sdd, a0, b0, lane, unused);
+            }
+        }
+    }
+    const double t = block_sum(lsq);
+    if (threadIdx.x == 0) f.loss_part[blockIdx.x] = 0.5 * t;
+}
+
+// Column pass of the SpMM gradient: dB = seed * A^T C over the column plan,
+// and in the blocks after it the SDDMM of the long rows' chunks.
+template <int VEC, int G, int U>
+__global__ __launch_bounds__(kBlock) void frob_col_kernel(FrobParams f) {
+    constexpr int kSlots = kBlock / G;
+    const SgrParams &a = f.cols;
+    const int lane = threadIdx.x % kWave;
+    const int g = threadIdx.x % G;
+    const int col = g * VEC;
+    const bool on = col < a.k;
+    const int col_blocks = a.item_blocks + f.col_empty_blocks;
+    if ((int)blockIdx.x < a.item_blocks) {
+        const int64_t s = (int64_t)blockIdx.x * kSlots + threadIdx.x / G;
+        if (s < a.plan.nitems) sgr_walk<VEC, G, U>(a, s, col, on, NoSegDone{});
+    } else if ((int)blockIdx.x < col_blocks) {
+        zero_segment<VEC>(a, (int64_t)(blockIdx.x - a.item_blocks) * kSlots + threadIdx.x / G, col,
+                          on);
+    } else {
+        const int64_t j = (int64_t)(blockIdx.x - col_blocks) * kSlots + threadIdx.x / G;
+        if (j < f.rows.plan.nchunks) {
+            const int it = f.rows.plan.chunk_item[j];
+            double unused = 0.0;
+            sddmm_range<VEC, G, sddmm_unroll<G>()>(f.sdd, f.rows.plan.item_ptr[it],
+                                                   f.rows.plan.item_ptr[it + 1], lane, unused);
+        }
+    }
+}
+
+template <int VEC, int G>
+static nsd_status launch_frob(FrobParams f, hipStream_t st) {
+    constexpr int kSlots = kBlock / G;
+    constexpr int U = sgr_unroll<G>();
+    f.rows.item_blocks = (int32_t)ceil_div(f.rows.plan.nitems, kSlots);
+    const int row_blocks = f.rows.item_blocks + (int)ceil_div(f.rows.plan.nempty, kSlots);
+    frob_row_kernel<VEC, G, U><<<row_blocks, kBlock, 0, st>>>(f);
+    NSD_TRY(check_launch("frob_row_kernel"));
+    NSD_TRY((launch_fix<VEC, G>(f.rows, f.seg_loss, 0.5, st)));
+    f.cols.item_blocks = (int32_t)ceil_div(f.cols.plan.nitems, kSlots);
+    f.col_empty_blocks = (int32_t)ceil_div(f.cols.plan.nempty, kSlots);
+    const int col_blocks = f.cols.item_blocks + f.col_empty_blocks +
+                           (int)ceil_div(f.rows.plan.nchunks, kSlots);
+    frob_col_kernel<VEC, G, U><<<col_blocks, kBlock, 0, st>>>(f);
+    NSD_TRY(check_launch("frob_col_kernel"));
+    NSD_TRY((launch_fix<VEC, G>(f.cols, nullptr, 0.0, st)));
+    loss_finalize_kernel<<<1, kBlock, 0, st>>>(f.loss_part, row_blocks, f.seg_loss,
+                                               f.rows.plan.nlong, f.loss);
+    return check_launch("loss_finalize_kernel");
+}
+
+int64_t frob_row_blocks(const nsd_plan &rows, int k) {
+    const WidthPlan wp = width_plan(k, true);
+    const int slots = kBlock / wp.g;
+    return ceil_div(rows.nitems, slots) + ceil_div(rows.nempty, slots);
+}
+
+bool frob_fused_ok(int k, const void *B, const void *C, const void *dB) {
+    return k <= 256 && k % 4 == 0 && aligned16(B) && aligned16(C) && aligned16(dB);
+}
+
+struct FrobLauncher {
+    FrobParams f;
+    hipStream_t st;
+    template <int VEC, int G>
+    nsd_status operator()() { return launch_frob<VEC, G>(f, st); }
+};
+
+nsd_status frob_fused(FrobParams f, hipStream_t st) {
+    FrobLauncher fn{f, st};
+    return dispatch_width(width_plan(f.rows.k, true), fn);
 }
 
 }  // namespace nsd

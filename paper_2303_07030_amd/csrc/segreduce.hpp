@@ -6,7 +6,8 @@
 namespace nsd {
 
 struct SgrParams {
-    int32_t nseg = 0, nnz = 0, k = 0, L = 0, nslots = 0;
+    int32_t nseg = 0, nnz = 0, k = 0;
+    nsd_plan plan{};                  // work items over the segments
     const int32_t *segptr = nullptr;  // [nseg+1]
     const int32_t *segidx = nullptr;  // [nnz] segment of each entry, sorted
     const int32_t *idx = nullptr;     // [nnz] row of X gathered by each entry
@@ -15,15 +16,8 @@ struct SgrParams {
     const float *X = nullptr;         // gathered dense operand (NULL: ones)
     float alpha = 1.f;
     float *out = nullptr;             // [nseg x k]
-    float *pfirst = nullptr;          // [nslots x k] carry-in partials
-    float *plast = nullptr;           // [nslots x k] carry-out partials
-    int32_t *span = nullptr;          // [nslots] row continuing past the slot, or -1
-};
-
-struct SgrShape {
-    WidthPlan wp;
-    int L;
-    int64_t nslots;
+    float *part = nullptr;            // [plan.nitems x k] chunk partials
+    int32_t item_blocks = 0;          // set by the launcher
 };
 
 struct SddmmParams {
@@ -46,10 +40,24 @@ struct SddmmShape {
 };
 
 int choose_slot_len(int64_t nnz, int slots_per_wave);
-SgrShape sgr_shape(int64_t nnz, int k);
-SgrShape sgr_shape_vec1(int64_t nnz, int k);
-void sgr_carve(Carver &c, int64_t nnz, int k, SgrParams *p);
+size_t sgr_part_bytes(const nsd_plan &plan, int k);
 nsd_status segreduce(SgrParams a, hipStream_t st);
+
+// Fused SpMM-gradient passes (L = 1/2 ||A B||^2): rows = C = A B over the
+// row plan, sdd = dA = seed <C_i, B_j>, cols = dB = seed A^T C over the
+// column plan.
+struct FrobParams {
+    SgrParams rows, cols;
+    SddmmParams sdd;
+    double *loss_part = nullptr;  // [frob_row_blocks] row-pass block partials
+    double *seg_loss = nullptr;   // [rows.plan.nlong] long-row partials
+    double *loss = nullptr;
+    int32_t col_empty_blocks = 0; // set by the launcher
+};
+
+int64_t frob_row_blocks(const nsd_plan &rows, int k);
+bool frob_fused_ok(int k, const void *B, const void *C, const void *dB);
+nsd_status frob_fused(FrobParams f, hipStream_t st);
 
 SddmmShape sddmm_shape(int64_t nnz, int k, bool vec_ok);
 bool sddmm_vec_ok(const SddmmParams &a);

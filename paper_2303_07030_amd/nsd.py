@@ -34,16 +34,23 @@ class NsdError(RuntimeError):
         self.status = status
 
 
+class nsd_plan(C.Structure):
+    _fields_ = [("item_len", C.c_int32), ("nitems", C.c_int32), ("nlong", C.c_int32),
+                ("nhuge", C.c_int32), ("nchunks", C.c_int32), ("nempty", C.c_int32),
+                ("item_ptr", C.c_void_p), ("long_seg", C.c_void_p), ("long_first", C.c_void_p),
+                ("huge_idx", C.c_void_p), ("chunk_item", C.c_void_p), ("empty_seg", C.c_void_p)]
+
+
 class nsd_csr(C.Structure):
     _fields_ = [("nrows", C.c_int32), ("ncols", C.c_int32), ("nnz", C.c_int32),
                 ("rowptr", C.c_void_p), ("rowidx", C.c_void_p), ("colind", C.c_void_p),
-                ("val", C.c_void_p)]
+                ("val", C.c_void_p), ("plan", nsd_plan)]
 
 
 class nsd_csc(C.Structure):
     _fields_ = [("nrows", C.c_int32), ("ncols", C.c_int32), ("nnz", C.c_int32),
                 ("colptr", C.c_void_p), ("colidx", C.c_void_p), ("rowind", C.c_void_p),
-                ("perm", C.c_void_p)]
+                ("perm", C.c_void_p), ("plan", nsd_plan)]
 
 
 if not os.path.exists(LIB_PATH):
@@ -61,7 +68,12 @@ _SIGS = {
     "nsd_status_string": (C.c_char_p, [C.c_int]),
     "nsd_last_error": (C.c_char_p, []),
     "nsd_version": (C.c_int, []),
-    "nsd_workspace_size": (C.c_int, [_I, _I, _I, C.POINTER(_SZ)]),
+    "nsd_workspace_size": (C.c_int, [_CSR, _CSC, _I, C.POINTER(_SZ)]),
+    "nsd_plan_item_len": (C.c_int, [_I, _I, C.POINTER(_I)]),
+    "nsd_plan_bounds": (C.c_int, [_I, _I, _I, C.POINTER(_I), C.POINTER(_I), C.POINTER(_I),
+                                  C.POINTER(_SZ)]),
+    "nsd_plan_build": (C.c_int, [_I, _I, _P, _I, _P, _P, _P, _P, _P, _P, C.POINTER(nsd_plan), _P,
+                                 _SZ, _P]),
     "nsd_build_workspace_size": (C.c_int, [_I, _I, C.POINTER(_SZ)]),
     "nsd_csr_expand_rows": (C.c_int, [_I, _I, _P, _P, _P]),
     "nsd_coo_to_csr": (C.c_int, [_I, _I, _I, _P, _P, _P, C.c_int, _P, _P, _P, _P, _P,
@@ -129,10 +141,37 @@ def nsd_version() -> int:
     return _lib.nsd_version()
 
 
-def nsd_workspace_size(nnz: int, nseg: int, k: int) -> int:
+def nsd_workspace_size(A: nsd_csr, At, k: int) -> int:
     b = _SZ(0)
-    _check(_lib.nsd_workspace_size(nnz, nseg, k, C.byref(b)), "nsd_workspace_size")
+    _check(_lib.nsd_workspace_size(C.byref(A), None if At is None else C.byref(At), k,
+                                   C.byref(b)), "nsd_workspace_size")
     return b.value
+
+
+def nsd_plan_item_len(nnz: int, k: int) -> int:
+    L = _I(0)
+    _check(_lib.nsd_plan_item_len(nnz, k, C.byref(L)), "nsd_plan_item_len")
+    return L.value
+
+
+def nsd_plan_bounds(nseg: int, nnz: int, item_len: int):
+    """(max_items, max_long, max_chunks, workspace bytes) for nsd_plan_build."""
+    mi, ml, mc, wb = _I(0), _I(0), _I(0), _SZ(0)
+    _check(_lib.nsd_plan_bounds(nseg, nnz, item_len, C.byref(mi), C.byref(ml), C.byref(mc),
+                                C.byref(wb)), "nsd_plan_bounds")
+    return mi.value, ml.value, mc.value, wb.value
+
+
+def nsd_plan_build(nseg, nnz, segptr, item_len, item_ptr, long_seg, long_first, huge_idx,
+                   chunk_item, empty_seg, ws, stream=None) -> nsd_plan:
+    plan = nsd_plan()
+    _check(_lib.nsd_plan_build(nseg, nnz, _p(segptr), item_len, _p(item_ptr), _p(long_seg),
+                               _p(long_first), _p(huge_idx), _p(chunk_item), _p(empty_seg),
+                               C.byref(plan), _p(ws), _nbytes(ws), _stream(stream)),
+           "nsd_plan_build")
+    plan._keep = dict(item_ptr=item_ptr, long_seg=long_seg, long_first=long_first,
+                      huge_idx=huge_idx, chunk_item=chunk_item, empty_seg=empty_seg)
+    return plan
 
 
 def nsd_build_workspace_size(n: int, max_key: int) -> int:

@@ -1,10 +1,10 @@
 """Device-resident sparse operands for the hot path.
 
 A DeviceCsr holds a CSR in HBM together with the arrays the gradient
-kernels read: rowidx (the row of every stored entry) and the CSC of the same
-matrix (colptr, colidx, rowind, perm).  All of them are produced by the
-library's own builders; this module only allocates torch tensors and calls
-the binding.
+kernels read: rowidx (the row of every stored entry), the work plan over the
+rows, and the CSC of the same matrix (colptr, colidx, rowind, perm) with its
+plan over the columns.  All of them are produced by the library's own
+builders; this module only allocates torch tensors and calls the binding.
 """
 from __future__ import annotations
 
@@ -18,9 +18,21 @@ def _dev(a, dtype, device):
     return torch.from_numpy(np.ascontiguousarray(a)).to(device=device, dtype=dtype)
 
 
+def build_plan(nseg, nnz, segptr, item_len, device, stream=None):
+    """Work plan of a segment pointer array (device tensors kept alive on it)."""
+    max_items, max_long, max_chunks, wsb = nsd.nsd_plan_bounds(nseg, nnz, item_len)
+
+    def arr(n):
+        return torch.empty(max(n, 1), dtype=torch.int32, device=device)
+
+    ws = torch.empty(max(wsb, 256), dtype=torch.uint8, device=device)
+    return nsd.nsd_plan_build(nseg, nnz, segptr, item_len, arr(max_items + 1), arr(max_long),
+                              arr(max_long), arr(max_long), arr(max_chunks), arr(nseg), ws, stream)
+
+
 class DeviceCsr:
     def __init__(self, nrows: int, ncols: int, rowptr, colind, val, device="cuda",
-                 build_csc: bool = True, stream=None):
+                 build_csc: bool = True, stream=None, k_hint: int = 64, item_len=None):
         self.nrows, self.ncols = int(nrows), int(ncols)
         self.rowptr = _dev(rowptr, torch.int32, device)
         self.colind = _dev(colind, torch.int32, device)
@@ -30,6 +42,10 @@ class DeviceCsr:
         nsd.nsd_csr_expand_rows(self.nrows, self.nnz, self.rowptr, self.rowidx, stream)
         self.desc = nsd.csr_desc(self.nrows, self.ncols, self.rowptr, self.rowidx, self.colind,
                                  self.val)
+        self.item_len = item_len or nsd.nsd_plan_item_len(self.nnz, k_hint)
+        self.row_plan = build_plan(self.nrows, self.nnz, self.rowptr, self.item_len, device,
+                                   stream)
+        self.desc.plan = self.row_plan
         self.csc = None
         if build_csc:
             self.build_csc(stream)
@@ -45,8 +61,10 @@ class DeviceCsr:
         nsd.nsd_csr_to_csc(self.desc, self.colptr, self.colidx, self.rowind, self.perm, ws, stream)
         self.csc = nsd.csc_desc(self.nrows, self.ncols, self.colptr, self.colidx, self.rowind,
                                 self.perm)
+        self.col_plan = build_plan(self.ncols, self.nnz, self.colptr, self.item_len, dev, stream)
+        self.csc.plan = self.col_plan
         return self.csc
 
     def workspace(self, k: int):
-        n = nsd.nsd_workspace_size(self.nnz, max(self.nrows, self.ncols), k)
+        n = nsd.nsd_workspace_size(self.desc, self.csc, k)
         return torch.empty(max(n, 256), dtype=torch.uint8, device=self.rowptr.device)

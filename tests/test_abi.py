@@ -53,19 +53,27 @@ def test_status_strings_and_version(nsd):
     assert nsd.nsd_version() >= 100
 
 
+def _desc(nsd, nrows=4, ncols=4, nnz=3, ptr=0x1000, nitems=1):
+    d = nsd.nsd_csr(nrows, ncols, nnz, ptr, ptr, ptr, ptr)
+    d.plan = nsd.nsd_plan(16, nitems, 0, 0, 0, 0, ptr, 0, 0, 0, 0, 0)
+    return d
+
+
 def test_workspace_queries(nsd):
-    small = nsd.nsd_workspace_size(1000, 100, 64)
-    big = nsd.nsd_workspace_size(1_000_000, 100_000, 64)
+    # descriptors with plans of 100 and 10,000 items: sizes only, nothing is read
+    small = nsd.nsd_workspace_size(_desc(nsd, 1000, 1000, 5000, nitems=100), None, 64)
+    big = nsd.nsd_workspace_size(_desc(nsd, 1000, 1000, 5000, nitems=10_000), None, 64)
     assert 0 < small < big and big % 256 == 0
     assert nsd.nsd_build_workspace_size(0, 1) > 0
     with pytest.raises(nsd.NsdError) as e:
-        nsd.nsd_workspace_size(10, 10, 0)
+        nsd.nsd_workspace_size(_desc(nsd), None, 0)
     assert e.value.status == nsd.NSD_ERR_INVALID_ARG
-
-
-def _desc(nsd, nrows=4, ncols=4, nnz=3, ptr=0x1000):
-    d = nsd.nsd_csr(nrows, ncols, nnz, ptr, ptr, ptr, ptr)
-    return d
+    mi, ml, mc, wb = nsd.nsd_plan_bounds(100_000, 1_000_000, 32)
+    assert mi >= 100_000 and ml >= 1 and mc >= 2 * 1_000_000 // 32 and wb > 0
+    assert 16 <= nsd.nsd_plan_item_len(1_000_000, 64) <= 256
+    with pytest.raises(nsd.NsdError) as e:
+        nsd.nsd_plan_bounds(10, 2**30, 16)
+    assert e.value.status == nsd.NSD_ERR_TOO_LARGE
 
 
 def test_host_argument_errors_before_launch(nsd):
@@ -80,6 +88,10 @@ def test_host_argument_errors_before_launch(nsd):
     with pytest.raises(nsd.NsdError) as e:
         nsd.nsd_spmm(A, 0x1000, 8, 0x1000, None)            # no workspace
     assert e.value.status == nsd.NSD_ERR_WORKSPACE
+    noplan = nsd.nsd_csr(4, 4, 3, 0x1000, 0x1000, 0x1000, 0x1000)
+    with pytest.raises(nsd.NsdError) as e:
+        nsd.nsd_spmm(noplan, 0x1000, 8, 0x1000, None)       # plan never built
+    assert e.value.status == nsd.NSD_ERR_INVALID_ARG and "plan" in str(e.value)
     bad = nsd.nsd_csr(-1, 4, 3, 0x1000, 0x1000, 0x1000, 0x1000)
     with pytest.raises(nsd.NsdError) as e:
         nsd.nsd_sddmm(bad, None, 0x1000, 4, 1.0, 0x1000)

@@ -196,6 +196,47 @@ def test_validate_csr(nsd, operand):
     assert "column-range" in str(e.value)
 
 
+@pytest.mark.parametrize("L", [4, 16, 64, 256])
+def test_plan_invariants(nsd, L):
+    # a plan is an implementation device, checked by its defining properties:
+    # items tile the entries of the non-empty segments in order, never split a
+    # short segment, cut long ones into chunks of L, and list empty segments
+    from paper_2303_07030_amd.operand import build_plan
+    nrows, ncols, rowptr, colind, val = edge_pattern(5)
+    lens = np.diff(rowptr)
+    plan = build_plan(nrows, len(colind), dev(rowptr), L, "cuda")
+    n_it, n_long, n_empty = plan.nitems, plan.nlong, plan.nempty
+    kp = plan._keep
+    item_ptr = host(kp["item_ptr"])[: n_it + 1]
+    long_first = host(kp["long_first"])[:n_long]
+    long_seg = host(kp["long_seg"])[:n_long]
+    huge = host(kp["huge_idx"])[: plan.nhuge]
+    chunks = host(kp["chunk_item"])[: plan.nchunks]
+    empty = host(kp["empty_seg"])[:n_empty]
+    assert item_ptr[0] == 0 and item_ptr[-1] == len(colind)
+    assert np.all(np.diff(item_ptr) > 0)
+    assert np.array_equal(empty, np.nonzero(lens == 0)[0])
+    long_rows = np.nonzero(lens > L)[0]
+    assert n_long == len(long_rows) and np.array_equal(long_seg, long_rows)
+    nch_all = -(-lens[long_rows] // L)
+    assert np.array_equal(huge, np.nonzero(nch_all > 64)[0])
+    assert plan.nchunks == nch_all.sum()
+    assert np.array_equal(chunks, np.concatenate(
+        [long_first[i] + np.arange(nch_all[i]) for i in range(n_long)]) if n_long else chunks)
+    starts = set(item_ptr[:-1].tolist())
+    for r in np.nonzero((lens > 0) & (lens <= L))[0]:
+        # a short row lies inside one item: no item starts strictly inside it
+        inner = [q for q in range(rowptr[r] + 1, rowptr[r + 1]) if q in starts]
+        assert not inner
+    for i, r in enumerate(long_rows):
+        s0 = long_first[i]
+        nch = -(-lens[r] // L)
+        assert np.array_equal(item_ptr[s0:s0 + nch + 1][:-1], rowptr[r] + L * np.arange(nch))
+        assert item_ptr[s0 + nch] == rowptr[r + 1]
+    # bounded work: an item of short rows holds at most 2L + 1 entries
+    assert np.diff(item_ptr).max() <= 2 * L + 1
+
+
 # ---------------------------------------------------------------- primitives
 
 KS = [1, 3, 4, 8, 16, 32, 64, 100, 128, 256, 264]
