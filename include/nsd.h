@@ -271,6 +271,20 @@ nsd_status nsd_loss_bilinear(const nsd_csr *A, const nsd_csc *At, const float *H
                              const float *G, int32_t k, float seed, double *loss, float *dA,
                              float *dH, void *ws, size_t ws_bytes, void *stream);
 
+/*
+ * Sparse matrix factorisation:
+ *   L = sum over stored (i, j) of r_ij^2,  r_ij = A(i,j) - <U[i,:], V[j,:]>
+ *   dU[i,:] = -2 seed sum_j r_ij V[j,:];  dV[j,:] = -2 seed sum_i r_ij U[i,:]
+ * A's CSR gives the row pass (values A->val), its CSC the column pass with
+ * the values in CSC order valT [nnz] (nsd_gather_f32 of A->val by At->perm,
+ * made once when A is data; NULL: read A->val through At->perm each call).
+ * U, dU [nrows x k]; V, dV [ncols x k].  k <= 256 (multiple of 4, 16-byte
+ * aligned rows), otherwise k <= 64; larger k gives NSD_ERR_UNSUPPORTED.  Async.
+ */
+nsd_status nsd_loss_mf(const nsd_csr *A, const nsd_csc *At, const float *valT, const float *U,
+                       const float *V, int32_t k, float seed, double *loss, float *dU, float *dV,
+                       void *ws, size_t ws_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -41,30 +41,38 @@ static nsd_status check_csc(const nsd_csc *At, const nsd_csr *A) {
     return check_plan(At->plan, At->nnz, "column");
 }
 
-// Workspace: the chunk partials of the larger plan (reused by every reduction
-// of a call, which run in stream order) followed by the loss partials.
-static size_t part_region_bytes(const nsd_csr *A, const nsd_csc *At, int k) {
-    size_t b = sgr_part_bytes(A->plan, std::max(k, 1));
-    if (At) b = std::max(b, sgr_part_bytes(At->plan, std::max(k, 1)));
-    return (b + 255) & ~size_t(255);
+static size_t round256(size_t b) { return (b + 255) & ~size_t(255); }
+
+// Workspace: the chunk partials of the row plan, then of the column plan
+// (passes that run in one launch need both), then the loss partials and the
+// long-row loss partials.
+static size_t row_part_bytes(const nsd_csr *A, int k) {
+    return round256(sgr_part_bytes(A->plan, std::max(k, 1)));
 }
 
-static size_t loss_part_count(const nsd_csr *A, int k) {
+static size_t part_region_bytes(const nsd_csr *A, const nsd_csc *At, int k) {
+    size_t b = row_part_bytes(A, k);
+    if (At) b += round256(sgr_part_bytes(At->plan, std::max(k, 1)));
+    return b;
+}
+
+static size_t loss_part_count(const nsd_csr *A, const nsd_csc *At, int k) {
     int64_t m = std::max<int64_t>(1, frob_row_blocks(A->plan, k));
     for (int kk : {k, 1})
         for (bool v : {true, false}) m = std::max(m, sddmm_shape(A->nnz, kk, v).nblocks);
+    if (At)
+        for (bool v : {true, false}) m = std::max(m, mf_blocks(A->plan, At->plan, k, v));
     return (size_t)m;
 }
 
-static size_t round256(size_t b) { return (b + 255) & ~size_t(255); }
-
 static size_t compute_ws_bytes(const nsd_csr *A, const nsd_csc *At, int k) {
-    return part_region_bytes(A, At, k) + round256(loss_part_count(A, k) * sizeof(double)) +
+    return part_region_bytes(A, At, k) + round256(loss_part_count(A, At, k) * sizeof(double)) +
            round256(std::max<size_t>(A->plan.nlong, 1) * sizeof(double));
 }
 
 struct ComputeWs {
-    float *part;
+    float *part;      // row-plan partials (also used alone by single passes)
+    float *part_col;  // column-plan partials for passes sharing a launch
     double *loss_part;
     double *seg_loss;
 };
@@ -76,9 +84,10 @@ static nsd_status carve_compute(void *ws, size_t ws_bytes, const nsd_csr *A, con
         return fail(NSD_ERR_WORKSPACE, "workspace %zu bytes at %p, need %zu", ws_bytes, ws, need);
     char *b = static_cast<char *>(ws);
     out->part = reinterpret_cast<float *>(b);
+    out->part_col = reinterpret_cast<float *>(b + row_part_bytes(A, k));
     b += part_region_bytes(A, At, k);
     out->loss_part = reinterpret_cast<double *>(b);
-    b += round256(loss_part_count(A, k) * sizeof(double));
+    b += round256(loss_part_count(A, At, k) * sizeof(double));
     out->seg_loss = reinterpret_cast<double *>(b);
     return NSD_OK;
 }
@@ -192,7 +201,7 @@ nsd_status nsd_spmm_t(const nsd_csr *A, const nsd_csc *At, const float *G, int32
     NSD_REQUIRE(A->ncols == 0 || out != nullptr, "out is NULL");
     ComputeWs w;
     NSD_TRY(carve_compute(ws, ws_bytes, A, At, k, &w));
-    return segreduce(cols_params(A, At, G, k, alpha, out, w.part), as_stream(stream));
+    return segreduce(cols_params(A, At, G, k, alpha, out, w.part_col), as_stream(stream));
 }
 
 nsd_status nsd_loss_sum_spmv(const nsd_csr *A, const nsd_csc *At, const float *x, float seed,
@@ -214,7 +223,7 @@ nsd_status nsd_loss_sum_spmv(const nsd_csr *A, const nsd_csc *At, const float *x
     NSD_TRY(sddmm(sp, st));
     NSD_TRY(finish_loss(sp, loss, st));
     // dx = seed * A^T 1
-    return segreduce(cols_params(A, At, nullptr, 1, seed, dx, w.part), st);
+    return segreduce(cols_params(A, At, nullptr, 1, seed, dx, w.part_col), st);
 }
 
 nsd_status nsd_loss_frob_spmm(const nsd_csr *A, const nsd_csc *At, const float *B, int32_t k,
@@ -235,7 +244,7 @@ nsd_status nsd_loss_frob_spmm(const nsd_csr *A, const nsd_csc *At, const float *
         // (dB and dA on long rows), long-column combine, loss total
         FrobParams f;
         f.rows = rows_params(A, B, k, 1.f, C, w.part);
-        f.cols = cols_params(A, At, C, k, seed, dB, w.part);
+        f.cols = cols_params(A, At, C, k, seed, dB, w.part_col);
         f.sdd = sddmm_params(A, C, B, k, seed, dA);
         f.loss_part = w.loss_part;
         f.seg_loss = w.seg_loss;
@@ -252,7 +261,7 @@ nsd_status nsd_loss_frob_spmm(const nsd_csr *A, const nsd_csc *At, const float *
     NSD_TRY(sddmm(sp, st));
     NSD_TRY(finish_loss(sp, loss, st));
     // dB = seed * A^T C
-    return segreduce(cols_params(A, At, C, k, seed, dB, w.part), st);
+    return segreduce(cols_params(A, At, C, k, seed, dB, w.part_col), st);
 }
 
 nsd_status nsd_loss_bilinear(const nsd_csr *A, const nsd_csc *At, const float *H,
@@ -275,7 +284,36 @@ nsd_status nsd_loss_bilinear(const nsd_csr *A, const nsd_csc *At, const float *H
     NSD_TRY(sddmm(sp, st));
     NSD_TRY(finish_loss(sp, loss, st));
     // dH = seed * A^T G
-    return segreduce(cols_params(A, At, G, k, seed, dH, w.part), st);
+    return segreduce(cols_params(A, At, G, k, seed, dH, w.part_col), st);
+}
+
+nsd_status nsd_loss_mf(const nsd_csr *A, const nsd_csc *At, const float *valT, const float *U,
+                       const float *V, int32_t k, float seed, double *loss, float *dU, float *dV,
+                       void *ws, size_t ws_bytes, void *stream) {
+    NSD_TRY(check_csr(A, true, true));
+    NSD_TRY(check_csc(At, A));
+    NSD_REQUIRE(k >= 1, "k = %d < 1", k);
+    NSD_REQUIRE(loss != nullptr, "loss is NULL");
+    NSD_REQUIRE(A->nrows == 0 || dU != nullptr, "dU is NULL");
+    NSD_REQUIRE(A->ncols == 0 || dV != nullptr, "dV is NULL");
+    NSD_REQUIRE(A->nnz == 0 || (U && V), "U/V is NULL");
+    const bool vec = mf_vec_ok(k, U, V, dU, dV);
+    if (vec ? k > 256 : k > 64)
+        return fail(NSD_ERR_UNSUPPORTED, "factor width k = %d (at most 256, multiple of 4 and "
+                                         "16-byte aligned rows; otherwise at most 64)", k);
+    ComputeWs w;
+    NSD_TRY(carve_compute(ws, ws_bytes, A, At, k, &w));
+    MfParams f;
+    f.rows.s = rows_params(A, V, k, -2.f * seed, dU, w.part);
+    f.rows.own = U;
+    f.cols.s = cols_params(A, At, U, k, -2.f * seed, dV, w.part_col);
+    if (valT) {
+        f.cols.s.w = valT;
+        f.cols.s.wperm = nullptr;
+    }
+    f.cols.own = V;
+    f.loss_part = w.loss_part;
+    return mf_fused(f, loss, as_stream(stream));
 }
 
 }  // extern "C"

@@ -55,6 +55,24 @@ struct FrobParams {
     int32_t col_empty_blocks = 0; // set by the launcher
 };
 
+// Factorisation passes: s is the gather-reduce (X = the gathered factor,
+// w = A's values in this pass's order, out = its gradient, alpha = -2 seed),
+// own = the segment's own factor.
+struct MfPass {
+    SgrParams s;
+    const float *own = nullptr;
+    int32_t item_blocks = 0, empty_blocks = 0;  // set by the launcher
+};
+
+struct MfParams {
+    MfPass rows, cols;
+    double *loss_part = nullptr;  // [mf_blocks] block partials (row pass only)
+};
+
+int64_t mf_blocks(const nsd_plan &rows, const nsd_plan &cols, int k, bool vec);
+bool mf_vec_ok(int k, const void *U, const void *V, const void *dU, const void *dV);
+nsd_status mf_fused(MfParams f, double *loss, hipStream_t st);
+
 int64_t frob_row_blocks(const nsd_plan &rows, int k);
 bool frob_fused_ok(int k, const void *B, const void *C, const void *dB);
 nsd_status frob_fused(FrobParams f, hipStream_t st);

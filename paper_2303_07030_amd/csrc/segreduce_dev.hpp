@@ -1,0 +1,295 @@
+// Device building blocks shared by the gather-reduce, SDDMM, factorisation
+// and CP kernels: the pipelined per-entry metadata, the walk of one work
+// item, the long-segment combine, lane reductions and the lane-layout
+// dispatch.  Included by several translation units; everything here is a
+// template or inline.
+#pragma once
+
+#include <algorithm>
+
+#include "nsd_internal.hpp"
+#include "segreduce.hpp"
+
+namespace nsd {
+
+constexpr int kBlock = 256;
+constexpr int kBlockWaves = kBlock / kWave;
+constexpr int kHugeChunks = 64;  // matches the plan builder
+
+// --------------------------------------------------------- entry metadata
+
+template <int U>
+struct Meta {
+    int r[U], c[U];
+    float w[U];
+};
+
+// Metadata of entries [p, p + U) of an item ending at b0; entries past the
+// end become padding: same segment as the item's last entry (no flush), its
+// gathered row (a valid address) and weight 0.
+template <int U>
+__device__ __forceinline__ void load_meta(const SgrParams &a, int64_t p, int64_t b0, int last_r,
+                                          int last_c, Meta<U> &m) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int64_t q = p + u;
+        if (q < b0) {
+            m.r[u] = a.segidx[q];
+            m.c[u] = a.idx[q];
+            m.w[u] = a.w ? (a.wperm ? a.w[a.wperm[q]] : a.w[q]) : 1.f;
+        } else {
+            m.r[u] = last_r;
+            m.c[u] = last_c;
+            m.w[u] = 0.f;
+        }
+    }
+}
+
+// One slot's walk over item s (entries [a0, b0)).  Complete segments are
+// written as alpha * sum; a segment cut by the item's end or start goes to
+// part[s].  `seg_done(segment, unscaled sum)` is called for every segment
+// completed inside the item.
+template <int VEC, int G, int U, class SegDone>
+__device__ __forceinline__ void sgr_walk(const SgrParams &a, int64_t s, int col, bool on,
+                                         SegDone seg_done) {
+    const int64_t k = a.k;
+    const int64_t a0 = a.plan.item_ptr[s];
+    const int64_t b0 = a.plan.item_ptr[s + 1];
+    const int last_r = a.segidx[b0 - 1];
+    const int last_c = a.idx[b0 - 1];
+    int row = a.segidx[a0];
+    bool carry = a0 > 0 && a.segidx[a0 - 1] == row;  // a chunk after the first one
+
+    Vec<VEC> acc;
+    acc.zero();
+    auto flush = [&]() {
+        if (carry) {
+            if (on) acc.store(a.part + s * k + col);
+        } else {
+            seg_done(row, acc);
+            if (on) {
+                Vec<VEC> t = acc;
+                t.scale(a.alpha);
+                t.store(a.out + (int64_t)row * k + col);
+            }
+        }
+    };
+
+    Meta<U> cur, nxt;
+    load_meta(a, a0, b0, last_r, last_c, cur);
+    for (int64_t p = a0; p < b0; p += U) {
+        if (p + U < b0) load_meta(a, p + U, b0, last_r, last_c, nxt);
+        Vec<VEC> xv[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (a.X && on) xv[u].load(a.X + (int64_t)cur.c[u] * k + col);
+            else xv[u].ones();
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (cur.r[u] != row) {
+                flush();
+                row = cur.r[u];
+                carry = false;
+                acc.zero();
+            }
+            acc.fma(cur.w[u], xv[u]);
+        }
+        cur = nxt;
+    }
+    if (b0 == a.nnz || a.segidx[b0] != row) {
+        flush();
+    } else if (on) {
+        acc.store(a.part + s * k + col);  // the first chunk of a long segment
+    }
+}
+
+template <int VEC>
+__device__ __forceinline__ void zero_segment(const SgrParams &a, int64_t e, int col, bool on) {
+    if (e < a.plan.nempty && on) {
+        Vec<VEC> z;
+        z.zero();
+        z.store(a.out + (int64_t)a.plan.empty_seg[e] * a.k + col);
+    }
+}
+
+struct NoSegDone {
+    template <int VEC>
+    __device__ void operator()(int, const Vec<VEC> &) const {}
+};
+
+// ----------------------------------------------------------- long segments
+
+// out[seg] = alpha * sum of the segment's chunk partials, in chunk order per
+// row group, the groups then combined by a fixed butterfly.  Blocks below
+// wave_blocks give one wave to each non-huge long segment; the blocks after
+// them give a whole block to each huge segment.  When seg_loss is given,
+// beta * ||out[seg]||^2 is stored for every long segment.
+template <int VEC, int G>
+__global__ __launch_bounds__(kBlock) void sgr_fix_kernel(SgrParams a, int wave_blocks,
+                                                         double *seg_loss, double beta) {
+    constexpr int RG = kWave / G;  // row groups per wave
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int q = lane / G, g = lane % G;
+    const int64_t k = a.k;
+    const int L = a.plan.item_len;
+    __shared__ float red[kBlockWaves][G * VEC];
+    const bool huge = (int)blockIdx.x >= wave_blocks;
+    int64_t i;
+    int nsum, qq;  // number of groups sharing the chunks, this lane's group
+    if (!huge) {
+        i = (int64_t)blockIdx.x * kBlockWaves + wave;
+        if (i >= a.plan.nlong) return;
+        nsum = RG;
+        qq = q;
+    } else {
+        i = a.plan.huge_idx[blockIdx.x - wave_blocks];
+        nsum = RG * kBlockWaves;
+        qq = wave * RG + q;
+    }
+    const int seg = a.plan.long_seg[i];
+    const int64_t s0 = a.plan.long_first[i];
+    const int64_t n = ((int64_t)a.segptr[seg + 1] - a.segptr[seg] + L - 1) / L;
+    if (!huge && n > kHugeChunks) return;
+    double lsq = 0.0;
+    for (int c0 = 0; c0 < a.k; c0 += G * VEC) {
+        const int col = c0 + g * VEC;
+        const bool on = col < a.k;
+        Vec<VEC> acc[2];
+        acc[0].zero();
+        acc[1].zero();
+        if (on) {
+            int64_t t = qq;
+            for (; t + nsum < n; t += 2 * nsum) {
+                Vec<VEC> x0, x1;
+                x0.load(a.part + (s0 + t) * k + col);
+                x1.load(a.part + (s0 + t + nsum) * k + col);
+                acc[0].add(x0);
+                acc[1].add(x1);
+            }
+            if (t < n) {
+                Vec<VEC> x;
+                x.load(a.part + (s0 + t) * k + col);
+                acc[0].add(x);
+            }
+        }
+        acc[0].add(acc[1]);
+#pragma unroll
+        for (int m = G; m < kWave; m <<= 1)
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) acc[0].v[e] += shfl_xor(acc[0].v[e], m);
+        if (huge) {
+            if (q == 0)
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) red[wave][g * VEC + e] = acc[0].v[e];
+            __syncthreads();
+            if (wave == 0) {
+#pragma unroll
+                for (int e = 0; e < VEC; ++e)
+                    acc[0].v[e] = (red[0][g * VEC + e] + red[1][g * VEC + e]) +
+                                  (red[2][g * VEC + e] + red[3][g * VEC + e]);
+            }
+            __syncthreads();
+        }
+        if ((!huge || wave == 0) && q == 0 && on) {
+            acc[0].scale(a.alpha);
+            acc[0].store(a.out + (int64_t)seg * k + col);
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) lsq += (double)acc[0].v[e] * acc[0].v[e];
+        }
+    }
+    if (seg_loss) {
+        // only the lanes of group 0 (of wave 0 for a huge segment) hold squares
+#pragma unroll
+        for (int m = 1; m < kWave; m <<= 1) lsq += __shfl_xor(lsq, m, kWave);
+        if (lane == 0 && (!huge || wave == 0)) seg_loss[i] = beta * lsq;
+    }
+}
+
+inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+template <int G>
+constexpr int sgr_unroll() {
+    return G >= 16 ? 4 : 8;
+}
+
+template <int G>
+constexpr int sddmm_unroll() {
+    return G >= 4 ? 4 : (G == 1 ? 4 : G);
+}
+
+template <int VEC, int G>
+inline nsd_status launch_fix(const SgrParams &a, double *seg_loss, double beta, hipStream_t st) {
+    if (a.plan.nlong == 0) return NSD_OK;
+    const int wave_blocks = (int)ceil_div(a.plan.nlong, kBlockWaves);
+    sgr_fix_kernel<VEC, G><<<wave_blocks + a.plan.nhuge, kBlock, 0, st>>>(a, wave_blocks, seg_loss,
+                                                                         beta);
+    return check_launch("sgr_fix_kernel");
+}
+
+// Calls f.template operator()<VEC, G>() for the lane layout wp.
+template <class F>
+inline nsd_status dispatch_width(const WidthPlan &wp, F &f) {
+    if (wp.vec == 4) {
+        switch (wp.g) {
+            case 1: return f.template operator()<4, 1>();
+            case 2: return f.template operator()<4, 2>();
+            case 4: return f.template operator()<4, 4>();
+            case 8: return f.template operator()<4, 8>();
+            case 16: return f.template operator()<4, 16>();
+            case 32: return f.template operator()<4, 32>();
+            default: return f.template operator()<4, 64>();
+        }
+    }
+    switch (wp.g) {
+        case 1: return f.template operator()<1, 1>();
+        case 2: return f.template operator()<1, 2>();
+        case 4: return f.template operator()<1, 4>();
+        case 8: return f.template operator()<1, 8>();
+        case 16: return f.template operator()<1, 16>();
+        case 32: return f.template operator()<1, 32>();
+        default: return f.template operator()<1, 64>();
+    }
+}
+
+// Reduces U partial dot products across the G lanes of a slot with a
+// transposing butterfly: at each step a lane keeps half of its values and
+// receives the partner's matching half, so U values cost U - 1 exchanges
+// plus log2(G / U) for the last one.  Lane g ends with the total of value
+// number g / (G / U).
+template <int G, int U>
+__device__ __forceinline__ float transpose_reduce(float (&v)[U], int lane) {
+    int c = U;
+#pragma unroll
+    for (int m = G / 2; m >= 1; m >>= 1) {
+        if (c > 1) {
+            const bool upper = (lane & m) != 0;
+#pragma unroll
+            for (int i = 0; i < U / 2; ++i) {
+                if (i < c / 2) {
+                    const float send = upper ? v[i] : v[i + c / 2];
+                    const float keep = upper ? v[i + c / 2] : v[i];
+                    v[i] = keep + shfl_xor(send, m);
+                }
+            }
+            c >>= 1;
+        } else {
+            v[0] += shfl_xor(v[0], m);
+        }
+    }
+    return v[0];
+}
+
+// Block total of per-lane fp64 values, in a fixed order.
+__device__ __forceinline__ double block_sum(double v) {
+    __shared__ double wsum[kBlockWaves];
+#pragma unroll
+    for (int m = kWave / 2; m >= 1; m >>= 1) v += __shfl_xor(v, m, kWave);
+    if (threadIdx.x % kWave == 0) wsum[threadIdx.x / kWave] = v;
+    __syncthreads();
+    const double t = (wsum[0] + wsum[1]) + (wsum[2] + wsum[3]);
+    __syncthreads();
+    return t;
+}
+
+}  // namespace nsd

@@ -91,6 +91,7 @@ _SIGS = {
                                      _P]),
     "nsd_loss_bilinear": (C.c_int, [_CSR, _CSC, _P, _P, _I, C.c_float, _P, _P, _P, _P, _SZ,
                                     _P]),
+    "nsd_loss_mf": (C.c_int, [_CSR, _CSC, _P, _P, _P, _I, C.c_float, _P, _P, _P, _P, _SZ, _P]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _f = getattr(_lib, _name)
@@ -268,3 +269,8 @@ def nsd_loss_bilinear(A: nsd_csr, At: nsd_csc, H, G, k, seed, loss, dA, dH, ws, 
     _check(_lib.nsd_loss_bilinear(C.byref(A), C.byref(At), _p(H), _p(G), k, seed, _p(loss),
                                   _p(dA), _p(dH), _p(ws), _nbytes(ws), _stream(stream)),
            "nsd_loss_bilinear")
+
+
+def nsd_loss_mf(A: nsd_csr, At: nsd_csc, valT, U, V, k, seed, loss, dU, dV, ws, stream=None):
+    _check(_lib.nsd_loss_mf(C.byref(A), C.byref(At), _p(valT), _p(U), _p(V), k, seed, _p(loss),
+                            _p(dU), _p(dV), _p(ws), _nbytes(ws), _stream(stream)), "nsd_loss_mf")

@@ -15,6 +15,8 @@ from . import nsd
 
 
 def _dev(a, dtype, device):
+    if isinstance(a, torch.Tensor):
+        return a.to(device=device, dtype=dtype)
     return torch.from_numpy(np.ascontiguousarray(a)).to(device=device, dtype=dtype)
 
 
@@ -32,14 +34,18 @@ def build_plan(nseg, nnz, segptr, item_len, device, stream=None):
 
 class DeviceCsr:
     def __init__(self, nrows: int, ncols: int, rowptr, colind, val, device="cuda",
-                 build_csc: bool = True, stream=None, k_hint: int = 64, item_len=None):
+                 build_csc: bool = True, stream=None, k_hint: int = 64, item_len=None,
+                 rowidx=None):
         self.nrows, self.ncols = int(nrows), int(ncols)
         self.rowptr = _dev(rowptr, torch.int32, device)
         self.colind = _dev(colind, torch.int32, device)
         self.val = _dev(val, torch.float32, device)
         self.nnz = int(self.colind.numel())
-        self.rowidx = torch.empty(self.nnz, dtype=torch.int32, device=device)
-        nsd.nsd_csr_expand_rows(self.nrows, self.nnz, self.rowptr, self.rowidx, stream)
+        if rowidx is None:
+            self.rowidx = torch.empty(self.nnz, dtype=torch.int32, device=device)
+            nsd.nsd_csr_expand_rows(self.nrows, self.nnz, self.rowptr, self.rowidx, stream)
+        else:
+            self.rowidx = rowidx
         self.desc = nsd.csr_desc(self.nrows, self.ncols, self.rowptr, self.rowidx, self.colind,
                                  self.val)
         self.item_len = item_len or nsd.nsd_plan_item_len(self.nnz, k_hint)
@@ -68,3 +74,31 @@ class DeviceCsr:
     def workspace(self, k: int):
         n = nsd.nsd_workspace_size(self.desc, self.csc, k)
         return torch.empty(max(n, 256), dtype=torch.uint8, device=self.rowptr.device)
+
+    @classmethod
+    def from_coo(cls, nrows, ncols, row, col, val, device="cuda", policy=None, **kw):
+        """CSR of a COO input built on the GPU by nsd_coo_to_csr; `coo_perm`
+        maps every CSR slot to the input position of its first occurrence."""
+        row = _dev(row, torch.int32, device)
+        col = _dev(col, torch.int32, device)
+        v = _dev(val, torch.float32, device)
+        n = int(row.numel())
+        rowptr = torch.empty(nrows + 1, dtype=torch.int32, device=device)
+        rowidx = torch.empty(max(n, 1), dtype=torch.int32, device=device)
+        colind = torch.empty(max(n, 1), dtype=torch.int32, device=device)
+        vout = torch.empty(max(n, 1), dtype=torch.float32, device=device)
+        perm = torch.empty(max(n, 1), dtype=torch.int32, device=device)
+        ws = torch.empty(nsd.nsd_build_workspace_size(n, max(nrows, ncols, 1)), dtype=torch.uint8,
+                         device=device)
+        pol = nsd.NSD_DUP_SUM if policy is None else policy
+        m = nsd.nsd_coo_to_csr(nrows, ncols, n, row, col, v, pol, rowptr, rowidx, colind, vout,
+                               perm, ws)
+        A = cls(nrows, ncols, rowptr, colind[:m], vout[:m], device=device, rowidx=rowidx[:m], **kw)
+        A.coo_perm = perm[:m]
+        return A
+
+    def values_in_csc_order(self, stream=None):
+        """A's values permuted into CSC order (an exact copy, nsd_gather_f32)."""
+        valT = torch.empty(max(self.nnz, 1), dtype=torch.float32, device=self.val.device)
+        nsd.nsd_gather_f32(self.nnz, self.perm, self.val, valT, stream)
+        return valT[: self.nnz]

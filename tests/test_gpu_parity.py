@@ -385,6 +385,59 @@ def test_loss_bilinear_small_workload(nsd, operand, orc):
     assert_mag_close(dHg, dH, dHm, what="dH")
 
 
+def run_mf(nsd, A, U, V, k, seed=1.0, with_valT=True):
+    loss = torch.empty(1, dtype=torch.float64, device="cuda")
+    dU = torch.full((A.nrows, k), np.nan, dtype=torch.float32, device="cuda")
+    dV = torch.full((A.ncols, k), np.nan, dtype=torch.float32, device="cuda")
+    valT = A.values_in_csc_order() if with_valT else None
+    nsd.nsd_loss_mf(A.desc, A.csc, valT, dev(U), dev(V), k, seed, loss, dU, dV, A.workspace(k))
+    return host(loss)[0], host(dU), host(dV)
+
+
+def check_mf(orc, D, U, V, k, got, seed=1.0):
+    L, Lm = orc.mf_loss(D, U, V, k)
+    dU, dUm = orc.mf_grad(D, U, V, k, 0)
+    dV, dVm = orc.mf_grad(D, U, V, k, 1)
+    Lg, dUg, dVg = got
+    assert_mag_close(Lg, L, Lm, what="loss")
+    assert_mag_close(dUg, seed * dU, abs(seed) * dUm, what="dU")
+    assert_mag_close(dVg, seed * dV, abs(seed) * dVm, what="dV")
+
+
+def test_loss_mf_small_workload_from_coo(nsd, operand, orc):
+    from paper_2303_07030_amd import synth
+    d = synth.make("mf", "small")
+    A = operand.from_coo(d["nrows"], d["ncols"], d["row"], d["col"], d["val"], k_hint=d["k"])
+    got = run_mf(nsd, A, d["U"], d["V"], d["k"])
+    D = orc.Dok((d["nrows"], d["ncols"]), (d["row"], d["col"]), d["val"])
+    check_mf(orc, D, d["U"], d["V"], d["k"], got)
+    # the column pass reading values through perm gives the same bits
+    got2 = run_mf(nsd, A, d["U"], d["V"], d["k"], with_valT=False)
+    for x, y in zip(got, got2):
+        assert np.array_equal(np.asarray(x), np.asarray(y))
+
+
+@pytest.mark.parametrize("k", [1, 5, 12, 64, 128, 256])
+def test_loss_mf_edge(nsd, operand, orc, k):
+    nrows, ncols, rowptr, colind, val = edge_pattern(13)
+    val = (1 + 4 * np.abs(val)).astype(np.float32)
+    A = operand(nrows, ncols, rowptr, colind, val, k_hint=k)
+    rng = np.random.default_rng(k)
+    U = (0.1 * rng.standard_normal((nrows, k))).astype(np.float32)
+    V = (0.1 * rng.standard_normal((ncols, k))).astype(np.float32)
+    got = run_mf(nsd, A, U, V, k, seed=0.5)
+    D = oracle_dok(orc, nrows, ncols, rowptr, colind, val)
+    check_mf(orc, D, U, V, k, got, seed=0.5)
+
+
+def test_loss_mf_rejects_wide_factors(nsd, operand):
+    nrows, ncols, rowptr, colind, val = edge_pattern(14)
+    A = operand(nrows, ncols, rowptr, colind, val)
+    with pytest.raises(nsd.NsdError) as e:
+        run_mf(nsd, A, np.zeros((nrows, 260), np.float32), np.zeros((ncols, 260), np.float32), 260)
+    assert e.value.status == nsd.NSD_ERR_UNSUPPORTED
+
+
 # ------------------------------------------------------- edge cases
 
 def test_empty_matrix_writes_zeros(nsd, operand):
