@@ -110,6 +110,29 @@ typedef struct nsd_csc {
     nsd_plan plan;         /* plan over the columns (for reductions into columns) */
 } nsd_csc;
 
+/*
+ * A COO 3-tensor seen through one mode n: its entries stably sorted by the
+ * mode-n coordinate (nsd_coo_mode_index), with the other coordinates and the
+ * values gathered into that order, and the work plan over the mode-n slices.
+ */
+typedef struct nsd_coo3_mode {
+    int32_t mode;          /* n in {0, 1, 2} */
+    const int32_t *segptr; /* [dims[n]+1] */
+    const int32_t *segidx; /* [nnz] mode-n coordinate, non-decreasing */
+    const int32_t *idx_a;  /* [nnz] coordinate of mode (n+1) % 3 */
+    const int32_t *idx_b;  /* [nnz] coordinate of mode (n+2) % 3 */
+    const float *val;      /* [nnz] values in this order */
+    const int32_t *perm;   /* [nnz] input position of every sorted entry */
+    nsd_plan plan;         /* plan over the mode-n slices */
+} nsd_coo3_mode;
+
+/* Sparse 3-tensor (the order-3 `tensor` of Section 3) in its three mode orders. */
+typedef struct nsd_coo3 {
+    int32_t dims[3];
+    int32_t nnz;
+    nsd_coo3_mode mode[3];
+} nsd_coo3;
+
 /* ----------------------------------------------------------------- info */
 
 /* Static string naming a status code. */
@@ -201,6 +224,10 @@ nsd_status nsd_coo_mode_index(int32_t nnz, int32_t dim, const int32_t *key,
 nsd_status nsd_gather_f32(int32_t n, const int32_t *perm, const float *src, float *dst,
                           void *stream);
 
+/* dst[q] = src[perm[q]] for q < n, int32 (coordinates into mode order).  Async. */
+nsd_status nsd_gather_i32(int32_t n, const int32_t *perm, const int32_t *src, int32_t *dst,
+                          void *stream);
+
 /* Checks a CSR: rowptr[0] = 0, non-decreasing, rowptr[nrows] = nnz; colind in
  * [0, ncols) and, when check_sorted, strictly increasing within each row;
  * rowidx (if not NULL) consistent with rowptr.  NSD_OK or NSD_ERR_BAD_FORMAT.
@@ -284,6 +311,24 @@ nsd_status nsd_loss_bilinear(const nsd_csr *A, const nsd_csc *At, const float *H
 nsd_status nsd_loss_mf(const nsd_csr *A, const nsd_csc *At, const float *valT, const float *U,
                        const float *V, int32_t k, float seed, double *loss, float *dU, float *dV,
                        void *ws, size_t ws_bytes, void *stream);
+
+/* Bytes of `ws` nsd_loss_cp needs for X (with its three plans) at the given
+ * rank.  Writes *bytes (host). */
+nsd_status nsd_cp_workspace_size(const nsd_coo3 *X, int32_t rank, size_t *bytes);
+
+/*
+ * CP decomposition of a sparse 3-tensor X with factors F1 [dims[0] x rank],
+ * F2 [dims[1] x rank], F3 [dims[2] x rank]:
+ *   R = X - m on X's keys, m_ijl = sum_r F1[i,r] F2[j,r] F3[l,r]
+ *   L = 1/2 sum R^2
+ *   dX [nnz] = seed * R, aligned with X's input order (X->mode[n].perm)
+ *   dF1[i,:] = -seed sum R_ijl (F2[j,:] o F3[l,:]), cyclically dF2, dF3
+ *   (the negated mode-n MTTKRPs of R).
+ * rank <= 256 (multiple of 4, 16-byte aligned rows), otherwise <= 64.  Async.
+ */
+nsd_status nsd_loss_cp(const nsd_coo3 *X, const float *F1, const float *F2, const float *F3,
+                       int32_t rank, float seed, double *loss, float *dX, float *dF1,
+                       float *dF2, float *dF3, void *ws, size_t ws_bytes, void *stream);
 
 #ifdef __cplusplus
 }

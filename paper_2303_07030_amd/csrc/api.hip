@@ -316,4 +316,92 @@ nsd_status nsd_loss_mf(const nsd_csr *A, const nsd_csc *At, const float *valT, c
     return mf_fused(f, loss, as_stream(stream));
 }
 
+static nsd_status check_coo3(const nsd_coo3 *X) {
+    NSD_REQUIRE(X != nullptr, "COO3 descriptor is NULL");
+    NSD_REQUIRE(X->nnz >= 0 && X->dims[0] >= 0 && X->dims[1] >= 0 && X->dims[2] >= 0,
+                "negative COO3 size");
+    for (int n = 0; n < 3; ++n) {
+        const nsd_coo3_mode &m = X->mode[n];
+        NSD_REQUIRE(m.mode == n, "mode[%d] holds mode %d", n, m.mode);
+        NSD_REQUIRE(m.segptr != nullptr, "mode %d segptr is NULL", n);
+        if (X->nnz > 0) {
+            NSD_REQUIRE(X->dims[0] > 0 && X->dims[1] > 0 && X->dims[2] > 0,
+                        "nnz > 0 in an empty shape");
+            NSD_REQUIRE(m.segidx && m.idx_a && m.idx_b && m.val && m.perm,
+                        "mode %d array is NULL", n);
+        }
+        NSD_TRY(check_plan(m.plan, X->nnz, "mode"));
+    }
+    return NSD_OK;
+}
+
+static size_t cp_ws_bytes(const nsd_coo3 *X, int rank) {
+    size_t b = 0;
+    nsd_plan plans[3];
+    for (int n = 0; n < 3; ++n) {
+        b += round256(sgr_part_bytes(X->mode[n].plan, std::max(rank, 1)));
+        plans[n] = X->mode[n].plan;
+    }
+    const int64_t blocks = std::max(cp_blocks(plans, rank, true), cp_blocks(plans, rank, false));
+    return b + round256(std::max<int64_t>(blocks, 1) * sizeof(double));
+}
+
+nsd_status nsd_cp_workspace_size(const nsd_coo3 *X, int32_t rank, size_t *bytes) {
+    NSD_REQUIRE(bytes != nullptr, "bytes is NULL");
+    NSD_REQUIRE(rank >= 1, "rank = %d < 1", rank);
+    NSD_TRY(check_coo3(X));
+    *bytes = cp_ws_bytes(X, rank);
+    return NSD_OK;
+}
+
+nsd_status nsd_loss_cp(const nsd_coo3 *X, const float *F1, const float *F2, const float *F3,
+                       int32_t rank, float seed, double *loss, float *dX, float *dF1,
+                       float *dF2, float *dF3, void *ws, size_t ws_bytes, void *stream) {
+    NSD_TRY(check_coo3(X));
+    NSD_REQUIRE(rank >= 1, "rank = %d < 1", rank);
+    NSD_REQUIRE(loss != nullptr, "loss is NULL");
+    const float *F[3] = {F1, F2, F3};
+    float *dF[3] = {dF1, dF2, dF3};
+    for (int n = 0; n < 3; ++n) {
+        NSD_REQUIRE(X->dims[n] == 0 || dF[n] != nullptr, "dF%d is NULL", n + 1);
+        NSD_REQUIRE(X->nnz == 0 || F[n] != nullptr, "F%d is NULL", n + 1);
+    }
+    NSD_REQUIRE(X->nnz == 0 || dX != nullptr, "dX is NULL");
+    bool vec = rank % 4 == 0;
+    for (int n = 0; n < 3; ++n) vec = vec && aligned16(F[n]) && aligned16(dF[n]);
+    if (vec ? rank > 256 : rank > 64)
+        return fail(NSD_ERR_UNSUPPORTED, "rank %d (at most 256, multiple of 4 and 16-byte "
+                                         "aligned rows; otherwise at most 64)", rank);
+    const size_t need = cp_ws_bytes(X, rank);
+    if (ws == nullptr || ws_bytes < need)
+        return fail(NSD_ERR_WORKSPACE, "workspace %zu bytes at %p, need %zu", ws_bytes, ws, need);
+    char *b = static_cast<char *>(ws);
+    CpParams f;
+    for (int n = 0; n < 3; ++n) {
+        const nsd_coo3_mode &md = X->mode[n];
+        CpMode &m = f.m[n];
+        m.s.nseg = X->dims[n];
+        m.s.nnz = X->nnz;
+        m.s.k = rank;
+        m.s.plan = md.plan;
+        m.s.segptr = md.segptr;
+        m.s.segidx = md.segidx;
+        m.s.idx = md.idx_a;
+        m.s.w = md.val;
+        m.s.alpha = -seed;
+        m.s.out = dF[n];
+        m.s.part = reinterpret_cast<float *>(b);
+        b += round256(sgr_part_bytes(md.plan, rank));
+        m.idx_b = md.idx_b;
+        m.own = F[n];
+        m.fa = F[(n + 1) % 3];
+        m.fb = F[(n + 2) % 3];
+        m.perm = md.perm;
+        m.resid = dX;
+        m.seed = seed;
+    }
+    f.loss_part = reinterpret_cast<double *>(b);
+    return cp_fused(f, vec, loss, as_stream(stream));
+}
+
 }  // extern "C"

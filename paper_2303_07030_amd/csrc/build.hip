@@ -411,6 +411,15 @@ nsd_status nsd_gather_f32(int32_t n, const int32_t *perm, const float *src, floa
     return check_launch("gather_kernel");
 }
 
+nsd_status nsd_gather_i32(int32_t n, const int32_t *perm, const int32_t *src, int32_t *dst,
+                          void *stream) {
+    NSD_REQUIRE(n >= 0, "negative size");
+    if (n == 0) return NSD_OK;
+    NSD_REQUIRE(perm && src && dst, "null pointer");
+    gather_kernel<int32_t><<<grid_for(n), kThreads, 0, as_stream(stream)>>>(n, perm, src, dst);
+    return check_launch("gather_kernel");
+}
+
 nsd_status nsd_coo_to_csr(int32_t nrows, int32_t ncols, int32_t nnz, const int32_t *row,
                           const int32_t *col, const float *val, int policy, int32_t *rowptr,
                           int32_t *rowidx, int32_t *colind, float *val_out, int32_t *perm,

@@ -73,6 +73,28 @@ int64_t mf_blocks(const nsd_plan &rows, const nsd_plan &cols, int k, bool vec);
 bool mf_vec_ok(int k, const void *U, const void *V, const void *dU, const void *dV);
 nsd_status mf_fused(MfParams f, double *loss, hipStream_t st);
 
+// One mode pass of the CP gradient: s is the gather-reduce over the mode's
+// plan (segidx = mode coordinate, idx = coordinate of mode n+1, w = values,
+// out = dF_n, alpha = -seed, k = rank); own = F_n, fa / fb = the factors of
+// modes n+1 / n+2.  The first pass also writes the residual through perm.
+struct CpMode {
+    SgrParams s;
+    const int32_t *idx_b = nullptr;
+    const float *own = nullptr, *fa = nullptr, *fb = nullptr;
+    const int32_t *perm = nullptr;
+    float *resid = nullptr;
+    float seed = 1.f;
+    int32_t item_blocks = 0, empty_blocks = 0;  // set by the launcher
+};
+
+struct CpParams {
+    CpMode m[3];
+    double *loss_part = nullptr;
+};
+
+int64_t cp_blocks(const nsd_plan *plans, int rank, bool vec);
+nsd_status cp_fused(CpParams f, bool vec, double *loss, hipStream_t st);
+
 int64_t frob_row_blocks(const nsd_plan &rows, int k);
 bool frob_fused_ok(int k, const void *B, const void *C, const void *dB);
 nsd_status frob_fused(FrobParams f, hipStream_t st);

@@ -206,7 +206,6 @@ __global__ __launch_bounds__(kBlock) void sgr_fix_kernel(SgrParams a, int wave_b
     }
 }
 
-inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
 template <int G>
 constexpr int sgr_unroll() {

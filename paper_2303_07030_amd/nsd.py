@@ -53,6 +53,16 @@ class nsd_csc(C.Structure):
                 ("perm", C.c_void_p), ("plan", nsd_plan)]
 
 
+class nsd_coo3_mode(C.Structure):
+    _fields_ = [("mode", C.c_int32), ("segptr", C.c_void_p), ("segidx", C.c_void_p),
+                ("idx_a", C.c_void_p), ("idx_b", C.c_void_p), ("val", C.c_void_p),
+                ("perm", C.c_void_p), ("plan", nsd_plan)]
+
+
+class nsd_coo3(C.Structure):
+    _fields_ = [("dims", C.c_int32 * 3), ("nnz", C.c_int32), ("mode", nsd_coo3_mode * 3)]
+
+
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"libnsd.so is not built ({LIB_PATH}); run "
                       "`python -m paper_2303_07030_amd.build` first")
@@ -63,6 +73,7 @@ _I = C.c_int32
 _SZ = C.c_size_t
 _CSR = C.POINTER(nsd_csr)
 _CSC = C.POINTER(nsd_csc)
+_COO3 = C.POINTER(nsd_coo3)
 
 _SIGS = {
     "nsd_status_string": (C.c_char_p, [C.c_int]),
@@ -81,6 +92,7 @@ _SIGS = {
     "nsd_csr_to_csc": (C.c_int, [_CSR, _P, _P, _P, _P, _P, _SZ, _P]),
     "nsd_coo_mode_index": (C.c_int, [_I, _I, _P, _P, _P, _P, _P, _SZ, _P]),
     "nsd_gather_f32": (C.c_int, [_I, _P, _P, _P, _P]),
+    "nsd_gather_i32": (C.c_int, [_I, _P, _P, _P, _P]),
     "nsd_validate_csr": (C.c_int, [_CSR, C.c_int, _P, _SZ, _P]),
     "nsd_spmv": (C.c_int, [_CSR, _P, _P, _P, _SZ, _P]),
     "nsd_spmm": (C.c_int, [_CSR, _P, _I, _P, _P, _SZ, _P]),
@@ -92,6 +104,9 @@ _SIGS = {
     "nsd_loss_bilinear": (C.c_int, [_CSR, _CSC, _P, _P, _I, C.c_float, _P, _P, _P, _P, _SZ,
                                     _P]),
     "nsd_loss_mf": (C.c_int, [_CSR, _CSC, _P, _P, _P, _I, C.c_float, _P, _P, _P, _P, _SZ, _P]),
+    "nsd_cp_workspace_size": (C.c_int, [_COO3, _I, C.POINTER(_SZ)]),
+    "nsd_loss_cp": (C.c_int, [_COO3, _P, _P, _P, _I, C.c_float, _P, _P, _P, _P, _P, _P, _SZ,
+                              _P]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _f = getattr(_lib, _name)
@@ -227,6 +242,10 @@ def nsd_gather_f32(n, perm, src, dst, stream=None):
     _check(_lib.nsd_gather_f32(n, _p(perm), _p(src), _p(dst), _stream(stream)), "nsd_gather_f32")
 
 
+def nsd_gather_i32(n, perm, src, dst, stream=None):
+    _check(_lib.nsd_gather_i32(n, _p(perm), _p(src), _p(dst), _stream(stream)), "nsd_gather_i32")
+
+
 def nsd_validate_csr(A: nsd_csr, check_sorted, ws, stream=None):
     _check(_lib.nsd_validate_csr(C.byref(A), int(check_sorted), _p(ws), _nbytes(ws),
                                  _stream(stream)), "nsd_validate_csr")
@@ -274,3 +293,15 @@ def nsd_loss_bilinear(A: nsd_csr, At: nsd_csc, H, G, k, seed, loss, dA, dH, ws, 
 def nsd_loss_mf(A: nsd_csr, At: nsd_csc, valT, U, V, k, seed, loss, dU, dV, ws, stream=None):
     _check(_lib.nsd_loss_mf(C.byref(A), C.byref(At), _p(valT), _p(U), _p(V), k, seed, _p(loss),
                             _p(dU), _p(dV), _p(ws), _nbytes(ws), _stream(stream)), "nsd_loss_mf")
+
+
+def nsd_cp_workspace_size(X: nsd_coo3, rank: int) -> int:
+    b = _SZ(0)
+    _check(_lib.nsd_cp_workspace_size(C.byref(X), rank, C.byref(b)), "nsd_cp_workspace_size")
+    return b.value
+
+
+def nsd_loss_cp(X: nsd_coo3, F1, F2, F3, rank, seed, loss, dX, dF1, dF2, dF3, ws, stream=None):
+    _check(_lib.nsd_loss_cp(C.byref(X), _p(F1), _p(F2), _p(F3), rank, seed, _p(loss), _p(dX),
+                            _p(dF1), _p(dF2), _p(dF3), _p(ws), _nbytes(ws), _stream(stream)),
+           "nsd_loss_cp")

@@ -102,3 +102,49 @@ class DeviceCsr:
         valT = torch.empty(max(self.nnz, 1), dtype=torch.float32, device=self.val.device)
         nsd.nsd_gather_f32(self.nnz, self.perm, self.val, valT, stream)
         return valT[: self.nnz]
+
+
+class DeviceCoo3:
+    """A COO 3-tensor in HBM in its three mode orders: for every mode n the
+    library's mode index (stable sort by the mode-n coordinate), the other
+    two coordinates and the values gathered into that order, and the work
+    plan over the mode-n slices."""
+
+    def __init__(self, dims, i, j, l, val, device="cuda", rank_hint=32, item_len=None,
+                 stream=None):
+        self.dims = tuple(int(d) for d in dims)
+        coords = [_dev(c, torch.int32, device) for c in (i, j, l)]
+        self.val = _dev(val, torch.float32, device)
+        self.nnz = int(self.val.numel())
+        self.item_len = item_len or nsd.nsd_plan_item_len(self.nnz, rank_hint)
+        self.desc = nsd.nsd_coo3()
+        self.desc.dims[:] = self.dims
+        self.desc.nnz = self.nnz
+        self._keep = []
+        ws = torch.empty(nsd.nsd_build_workspace_size(self.nnz, max(max(self.dims), 1)),
+                         dtype=torch.uint8, device=device)
+        n = max(self.nnz, 1)
+        for m in range(3):
+            segptr = torch.empty(self.dims[m] + 1, dtype=torch.int32, device=device)
+            segidx = torch.empty(n, dtype=torch.int32, device=device)
+            perm = torch.empty(n, dtype=torch.int32, device=device)
+            nsd.nsd_coo_mode_index(self.nnz, self.dims[m], coords[m], segptr, segidx, perm, ws,
+                                   stream)
+            ia = torch.empty(n, dtype=torch.int32, device=device)
+            ib = torch.empty(n, dtype=torch.int32, device=device)
+            v = torch.empty(n, dtype=torch.float32, device=device)
+            nsd.nsd_gather_i32(self.nnz, perm, coords[(m + 1) % 3], ia, stream)
+            nsd.nsd_gather_i32(self.nnz, perm, coords[(m + 2) % 3], ib, stream)
+            nsd.nsd_gather_f32(self.nnz, perm, self.val, v, stream)
+            plan = build_plan(self.dims[m], self.nnz, segptr, self.item_len, device, stream)
+            md = self.desc.mode[m]
+            md.mode = m
+            md.segptr, md.segidx, md.idx_a, md.idx_b = (segptr.data_ptr(), segidx.data_ptr(),
+                                                        ia.data_ptr(), ib.data_ptr())
+            md.val, md.perm = v.data_ptr(), perm.data_ptr()
+            md.plan = plan
+            self._keep += [segptr, segidx, perm, ia, ib, v, plan]
+
+    def workspace(self, rank: int):
+        n = nsd.nsd_cp_workspace_size(self.desc, rank)
+        return torch.empty(max(n, 256), dtype=torch.uint8, device=self.val.device)

@@ -438,6 +438,58 @@ def test_loss_mf_rejects_wide_factors(nsd, operand):
     assert e.value.status == nsd.NSD_ERR_UNSUPPORTED
 
 
+def run_cp(nsd, X, F, rank, seed=1.0):
+    from paper_2303_07030_amd.operand import DeviceCoo3  # noqa: F401
+    loss = torch.empty(1, dtype=torch.float64, device="cuda")
+    dX = torch.full((X.nnz,), np.nan, dtype=torch.float32, device="cuda")
+    dF = [torch.full((X.dims[m], rank), np.nan, dtype=torch.float32, device="cuda")
+          for m in range(3)]
+    nsd.nsd_loss_cp(X.desc, *[dev(f) for f in F], rank, seed, loss, dX, *dF, X.workspace(rank))
+    return host(loss)[0], host(dX), [host(t) for t in dF]
+
+
+def check_cp(orc, dims, i, j, l, val, F, rank, got, seed=1.0):
+    D = orc.Dok(dims, (i, j, l), val)
+    L, Lm = orc.cp_loss(D, *F, rank)
+    R, Rm = orc.cp_resid(D, *F, rank, i, j, l)
+    Lg, dXg, dFg = got
+    assert_mag_close(Lg, L, Lm, what="loss")
+    assert_mag_close(dXg, seed * R, abs(seed) * Rm, what="residual")
+    for m in range(3):
+        g, gm = orc.cp_grad(D, *F, rank, m)
+        assert_mag_close(dFg[m], seed * g, abs(seed) * gm, what=f"dF{m + 1}")
+
+
+def test_loss_cp_small_workload(nsd, orc):
+    from paper_2303_07030_amd import synth
+    from paper_2303_07030_amd.operand import DeviceCoo3
+    d = synth.make("cp", "small")
+    X = DeviceCoo3(d["dims"], d["i"], d["j"], d["k"], d["val"], rank_hint=d["rank"])
+    F = [d["F1"], d["F2"], d["F3"]]
+    got = run_cp(nsd, X, F, d["rank"])
+    check_cp(orc, d["dims"], d["i"], d["j"], d["k"], d["val"], F, d["rank"], got)
+
+
+@pytest.mark.parametrize("rank,dims", [(32, (7, 300, 45)), (8, (50, 3, 200)), (5, (20, 20, 20)),
+                                       (64, (1, 40, 40))])
+def test_loss_cp_shapes(nsd, orc, rank, dims):
+    # skewed mode sizes: long slices (a mode of size 1 or 3), short ones, and
+    # empty slices; odd rank takes the scalar lane layout
+    from paper_2303_07030_amd.operand import DeviceCoo3
+    rng = np.random.default_rng(rank)
+    total = dims[0] * dims[1] * dims[2]
+    nnz = min(4000, total // 2)
+    keys = rng.choice(total, size=nnz, replace=False)
+    i = (keys // (dims[1] * dims[2])).astype(np.int32)
+    j = ((keys // dims[2]) % dims[1]).astype(np.int32)
+    l = (keys % dims[2]).astype(np.int32)
+    val = rng.standard_normal(nnz).astype(np.float32)
+    F = [(0.3 * rng.standard_normal((dims[m], rank))).astype(np.float32) for m in range(3)]
+    X = DeviceCoo3(dims, i, j, l, val, rank_hint=rank, item_len=16)
+    got = run_cp(nsd, X, F, rank, seed=2.0)
+    check_cp(orc, dims, i, j, l, val, F, rank, got, seed=2.0)
+
+
 # ------------------------------------------------------- edge cases
 
 def test_empty_matrix_writes_zeros(nsd, operand):
