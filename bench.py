@@ -1,18 +1,20 @@
 #!/usr/bin/env python3
 """Benchmark of the sparse-gradient hot path on one MI355X.
 
-A step is one pass of the whole path over the workload's inputs, already
-resident in HBM: for the default SpMM-gradient workload (CSR A 100,000 x
-100,000 with 1M power-law nnz, B 100,000 x 64) that is the forward product
-C = A B, the SDDMM gradient dA on A's pattern with the fused loss
-1/2 ||C||^2, and the transposed product dB = A^T C (nsd_loss_frob_spmm).
-The pattern-only preprocessing (row expansion, CSR -> CSC) is timed
-separately.
+A step is one pass of the whole path over one batch of inputs already
+resident in HBM.  The default workload is the SpMM gradient (CSR A 100,000 x
+100,000 with 1M power-law nnz, B 100,000 x 64): forward C = A B, the SDDMM
+gradient dA on A's pattern with the loss 1/2 ||C||^2, and dB = A^T C, through
+nsd_loss_frob_spmm.  --workload selects the other paths (gnn: bilinear GNN
+layer; mf: sparse factorisation; cp: CP decomposition; spmv: SMVM).
+Pattern-only preprocessing (row expansion, CSR -> CSC, work plans, mode
+indexes) is timed separately and is not part of a step.
 
-Prints one JSON line with the metric (gradient nonzeros per second), the
-roofline of the dominant kernel (algorithmic bytes / its average launch
-duration from HIP events, against 8 TB/s), and the fp64 oracle timed on the
-host as a reported CPU baseline.
+Prints one JSON line: the metric (gradient nonzeros per second), the roofline
+of the step's dominant kernel (its algorithmic bytes over its average launch
+duration, from HIP events recorded around every launch of that kernel during
+the timed steps, against 8 TB/s), and the fp64 oracle timed on this host on
+a bounded sample of the workload, as a reported baseline.
 """
 import argparse
 import hashlib
@@ -28,6 +30,13 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+WORKLOAD_NAMES = {
+    "spmm": "spmm_grad_100k_1M_zipf1.1_k64",
+    "gnn": "gnn_bilinear_2.4M_60M_zipf1.05_k256",
+    "mf": "mf_1M_500k_50M_zipf1.1_k128",
+    "cp": "cp_10k3_20M_rank32",
+    "spmv": "spmv_sum_1k_10k",
+}
 
 
 def parse():
@@ -35,26 +44,30 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="spmm", choices=["spmm", "gnn", "spmv"])
+    ap.add_argument("--workload", default="spmm", choices=list(WORKLOAD_NAMES))
     ap.add_argument("--size", default="full")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--profile-only", action="store_true",
-                    help="run warmup + steps only (for rocprofv3), no JSON line")
+                    help="warmup + steps only (for rocprofv3), no JSON line")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
+                    help="with --profile-only: also copy a buffer of BYTES once (a plain copy "
+                         "kernel of known size, to scale the HBM counters)")
     return ap.parse_args()
 
 
 def source_digest():
     h = hashlib.sha256()
-    for f in sorted(os.listdir(os.path.join(ROOT, "paper_2303_07030_amd", "csrc"))):
-        with open(os.path.join(ROOT, "paper_2303_07030_amd", "csrc", f), "rb") as fh:
+    d = os.path.join(ROOT, "paper_2303_07030_amd", "csrc")
+    for f in sorted(os.listdir(d)):
+        with open(os.path.join(d, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
 def committed_traffic(kernel, workload):
     """HBM bytes per launch from the committed counter summary, if it was
-    taken on the current kernel sources."""
+    taken on the current kernel sources (else None)."""
     path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_counters.md")
     if not os.path.exists(path):
         return None
@@ -66,188 +79,335 @@ def committed_traffic(kernel, workload):
     return float(m.group(1))
 
 
-class Events:
-    def __init__(self, torch):
-        self.torch = torch
+# ----------------------------------------------------------------- setups
 
-    def time(self, fn, reps):
-        t = self.torch
-        s, e = t.cuda.Event(enable_timing=True), t.cuda.Event(enable_timing=True)
-        s.record()
-        for _ in range(reps):
-            fn()
+class Setup:
+    """Operands in HBM, one step function and the kernels worth a roofline:
+    name -> (kernel id, algorithmic bytes per launch)."""
+
+
+def setup_spmm(d, dev, torch, nsd, ops):
+    A = ops.DeviceCsr(d["nrows"], d["ncols"], d["rowptr"], d["colind"], d["val"], device=dev,
+                      k_hint=d["k"])
+    k, nnz, nr, nc = d["k"], A.nnz, A.nrows, A.ncols
+    B = torch.from_numpy(d["B"]).to(dev)
+    C = torch.empty((nr, k), dtype=torch.float32, device=dev)
+    dB = torch.empty((nc, k), dtype=torch.float32, device=dev)
+    dA = torch.empty(nnz, dtype=torch.float32, device=dev)
+    loss = torch.empty(1, dtype=torch.float64, device=dev)
+    ws = A.workspace(k)
+    S = Setup()
+    S.A, S.nnz, S.k = A, nnz, k
+    S.step = lambda: nsd.nsd_loss_frob_spmm(A.desc, A.csc, B, k, 1.0, C, loss, dA, dB, ws)
+    long_nnz = int(sum(np.diff(d["rowptr"])[np.diff(d["rowptr"]) > A.item_len]))
+    S.kernels = {
+        # rowidx, colind, val in; dA out; B read and C written once
+        "frob_row": (4 * 4 * nnz + 4 * k * (nr + nc)),
+        # colidx, rowind, perm, val (via perm) in; C read, dB written once;
+        # SDDMM of the long rows' entries (indices in, dA out)
+        "frob_col": (4 * 4 * nnz + 4 * k * (nr + nc) + 3 * 4 * long_nnz),
+    }
+    return S
+
+
+def setup_gnn(d, dev, torch, nsd, ops):
+    A = ops.DeviceCsr(d["nrows"], d["ncols"], d["rowptr"], d["colind"], d["val"], device=dev,
+                      k_hint=d["k"])
+    k, nnz, nr, nc = d["k"], A.nnz, A.nrows, A.ncols
+    H = torch.from_numpy(d["H"]).to(dev)
+    G = torch.from_numpy(d["G"]).to(dev)
+    dH = torch.empty((nc, k), dtype=torch.float32, device=dev)
+    dA = torch.empty(nnz, dtype=torch.float32, device=dev)
+    loss = torch.empty(1, dtype=torch.float64, device=dev)
+    ws = A.workspace(k)
+    S = Setup()
+    S.A, S.nnz, S.k = A, nnz, k
+    S.step = lambda: nsd.nsd_loss_bilinear(A.desc, A.csc, H, G, k, 1.0, loss, dA, dH, ws)
+    S.kernels = {
+        # rowidx, colind, val in, dA out; G and H read once
+        "sddmm": 4 * 4 * nnz + 4 * k * (nr + nc),
+        # colidx, rowind, perm, val (via perm) in; G read once, dH written once
+        "sgr_main": 4 * 4 * nnz + 4 * k * (nr + nc),
+    }
+    return S
+
+
+def setup_mf(d, dev, torch, nsd, ops):
+    A = ops.DeviceCsr.from_coo(d["nrows"], d["ncols"], d["row"], d["col"], d["val"], device=dev,
+                               k_hint=d["k"])
+    valT = A.values_in_csc_order()
+    k, nnz, nr, nc = d["k"], A.nnz, A.nrows, A.ncols
+    U = torch.from_numpy(d["U"]).to(dev)
+    V = torch.from_numpy(d["V"]).to(dev)
+    dU = torch.empty((nr, k), dtype=torch.float32, device=dev)
+    dV = torch.empty((nc, k), dtype=torch.float32, device=dev)
+    loss = torch.empty(1, dtype=torch.float64, device=dev)
+    ws = A.workspace(k)
+    S = Setup()
+    S.A, S.nnz, S.k = A, nnz, k
+    S.step = lambda: nsd.nsd_loss_mf(A.desc, A.csc, valT, U, V, k, 1.0, loss, dU, dV, ws)
+    S.kernels = {
+        # both passes: (segment, gathered index, value) in per entry per pass;
+        # U and V read once, dU and dV written once
+        "mf": 2 * 3 * 4 * nnz + 2 * 4 * k * (nr + nc),
+    }
+    return S
+
+
+def setup_cp(d, dev, torch, nsd, ops):
+    X = ops.DeviceCoo3(d["dims"], d["i"], d["j"], d["k"], d["val"], device=dev,
+                       rank_hint=d["rank"])
+    R, nnz = d["rank"], X.nnz
+    F = [torch.from_numpy(d[f]).to(dev) for f in ("F1", "F2", "F3")]
+    dF = [torch.empty((X.dims[m], R), dtype=torch.float32, device=dev) for m in range(3)]
+    dX = torch.empty(nnz, dtype=torch.float32, device=dev)
+    loss = torch.empty(1, dtype=torch.float64, device=dev)
+    ws = X.workspace(R)
+    S = Setup()
+    S.A, S.nnz, S.k = X, nnz, R
+    S.step = lambda: nsd.nsd_loss_cp(X.desc, *F, R, 1.0, loss, dX, *dF, ws)
+    fac = 4 * R * sum(X.dims)
+    S.kernels = {
+        # three passes of (mode coordinate, two coordinates, value); the
+        # first also reads perm and writes the residual; factors read and
+        # gradients written once
+        "cp": 3 * 4 * 4 * nnz + 2 * 4 * nnz + 2 * fac,
+    }
+    return S
+
+
+def setup_spmv(d, dev, torch, nsd, ops):
+    A = ops.DeviceCsr(d["nrows"], d["ncols"], d["rowptr"], d["colind"], d["val"], device=dev,
+                      k_hint=1)
+    nnz, nr, nc = A.nnz, A.nrows, A.ncols
+    x = torch.from_numpy(d["x"]).to(dev)
+    dx = torch.empty(nc, dtype=torch.float32, device=dev)
+    dA = torch.empty(nnz, dtype=torch.float32, device=dev)
+    loss = torch.empty(1, dtype=torch.float64, device=dev)
+    ws = A.workspace(1)
+    S = Setup()
+    S.A, S.nnz, S.k = A, nnz, 1
+    S.step = lambda: nsd.nsd_loss_sum_spmv(A.desc, A.csc, x, 1.0, loss, dA, dx, ws)
+    S.kernels = {
+        "sddmm": 4 * 4 * nnz + 4 * nc,
+        "sgr_main": 4 * 4 * nnz + 4 * nc,
+    }
+    return S
+
+
+SETUPS = {"spmm": setup_spmm, "gnn": setup_gnn, "mf": setup_mf, "cp": setup_cp,
+          "spmv": setup_spmv}
+
+
+# ------------------------------------------------------------ measurement
+
+def probe_durations(torch, nsd, kernel, step, n_steps):
+    """Average duration (ms) of every launch of `kernel` over n_steps steps,
+    from HIP events the library records around those launches."""
+    # events are created lazily by torch: record once before handing them over
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(n_steps)]
+    stops = [torch.cuda.Event(enable_timing=True) for _ in range(n_steps)]
+    for e in starts + stops:
         e.record()
-        e.synchronize()
-        return s.elapsed_time(e) / reps
+    torch.cuda.synchronize()
+    nsd.nsd_probe_set(nsd.KERNEL_IDS[kernel], [e.cuda_event for e in starts],
+                      [e.cuda_event for e in stops])
+    return starts, stops
+
+
+def collect(torch, nsd, starts, stops):
+    torch.cuda.synchronize()
+    n = nsd.nsd_probe_count()
+    nsd.nsd_probe_clear()
+    m = min(n, len(starts))
+    if m == 0:
+        return None, 0
+    return float(np.mean([starts[i].elapsed_time(stops[i]) for i in range(m)])), n
 
 
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU "
-              "design is described, not built", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): this build measures "
+              "one GPU's share; the multi-GPU layout is a design, not a runnable path",
+              file=sys.stderr)
         sys.exit(2)
 
     import torch
     from paper_2303_07030_amd import nsd, synth
-    from paper_2303_07030_amd.operand import DeviceCsr
+    from paper_2303_07030_amd import operand as ops
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    ev = Events(torch)
 
+    t0 = time.perf_counter()
     d = synth.make(args.workload, args.size)
-    nrows, ncols = d["nrows"], d["ncols"]
-    nnz = len(d["colind"])
-    k = d.get("k", 1)
-
-    # ---- preprocessing (pattern only), timed separately
+    gen_s = time.perf_counter() - t0
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    A = DeviceCsr(nrows, ncols, d["rowptr"], d["colind"], d["val"], device=dev)
+    S = SETUPS[args.workload](d, dev, torch, nsd, ops)
     torch.cuda.synchronize()
-    prep_ms_incl_upload = (time.perf_counter() - t0) * 1e3
-    csc_ms = ev.time(lambda: A.build_csc(), 3)
-
-    ws = A.workspace(k)
-    loss = torch.empty(1, dtype=torch.float64, device=dev)
-    dA = torch.empty(nnz, dtype=torch.float32, device=dev)
-    if args.workload == "spmm":
-        B = torch.from_numpy(d["B"]).to(dev)
-        C = torch.empty((nrows, k), dtype=torch.float32, device=dev)
-        dB = torch.empty((ncols, k), dtype=torch.float32, device=dev)
-
-        def step():
-            nsd.nsd_loss_frob_spmm(A.desc, A.csc, B, k, 1.0, C, loss, dA, dB, ws)
-
-        kernels = {
-            "spmm_forward": (lambda: nsd.nsd_spmm(A.desc, B, k, C, ws),
-                             4 * (3 * nnz) + 4 * (nrows + ncols) * k),
-            "sddmm_grad": (lambda: nsd.nsd_sddmm(A.desc, C, B, k, 1.0, dA),
-                           4 * (2 * nnz + nnz) + 4 * (nrows + ncols) * k),
-            "spmm_t_grad": (lambda: nsd.nsd_spmm_t(A.desc, A.csc, C, k, 1.0, dB, ws),
-                            4 * (3 * nnz + nnz) + 4 * (nrows + ncols) * k),
-        }
-    elif args.workload == "gnn":
-        H = torch.from_numpy(d["H"]).to(dev)
-        G = torch.from_numpy(d["G"]).to(dev)
-        dH = torch.empty((ncols, k), dtype=torch.float32, device=dev)
-
-        def step():
-            nsd.nsd_loss_bilinear(A.desc, A.csc, H, G, k, 1.0, loss, dA, dH, ws)
-
-        kernels = {
-            "sddmm_grad": (lambda: nsd.nsd_sddmm(A.desc, G, H, k, 1.0, dA),
-                           4 * (3 * nnz) + 4 * (nrows + ncols) * k),
-            "spmm_t_grad": (lambda: nsd.nsd_spmm_t(A.desc, A.csc, G, k, 1.0, dH, ws),
-                            4 * (4 * nnz) + 4 * (nrows + ncols) * k),
-        }
-    else:
-        x = torch.from_numpy(d["x"]).to(dev)
-        dx = torch.empty(ncols, dtype=torch.float32, device=dev)
-
-        def step():
-            nsd.nsd_loss_sum_spmv(A.desc, A.csc, x, 1.0, loss, dA, dx, ws)
-
-        kernels = {
-            "spmm_t_grad": (lambda: nsd.nsd_spmm_t(A.desc, A.csc, None, 1, 1.0, dx, ws),
-                            4 * (4 * nnz) + 4 * ncols),
-        }
+    prep_ms = (time.perf_counter() - t0) * 1e3
 
     for _ in range(args.warmup):
-        step()
+        S.step()
     torch.cuda.synchronize()
     if args.profile_only:
+        if args.calibrate_copy:
+            n = args.calibrate_copy // 4
+            src = torch.ones(n, dtype=torch.float32, device=dev)
+            dst = torch.empty_like(src)
+            torch.cuda.synchronize()
+            dst.copy_(src)
+            torch.cuda.synchronize()
+            del src, dst
         for _ in range(args.steps):
-            step()
+            S.step()
         torch.cuda.synchronize()
         return
 
-    # ---- timed region: exactly K steps
-    torch.cuda.synchronize()
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    start.record()
-    for _ in range(args.steps):
-        step()
-    end.record()
-    torch.cuda.synchronize()
-    ms_per_step = start.elapsed_time(end) / args.steps
-
-    # ---- per-kernel durations (HIP events on the launching stream)
+    # which kernel dominates a step: probe each candidate over a few steps
     per_kernel = {}
-    for name, (fn, algo_bytes) in kernels.items():
-        fn()
-        ms = ev.time(fn, max(args.steps, 20))
-        per_kernel[name] = {"ms": round(ms, 5), "algo_bytes": int(algo_bytes),
-                            "GBps": round(algo_bytes / (ms * 1e-3) / 1e9, 1)}
-    dom = max(per_kernel, key=lambda n: per_kernel[n]["ms"])
-    dk = per_kernel[dom]
-    traffic = committed_traffic(dom, args.workload)
-    roofline = {
-        "bound": "hbm", "kernel": dom,
-        "achieved": dk["GBps"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-        "frac": round(dk["GBps"] / HBM_PEAK_GBS, 4),
-        "traffic": traffic,
-    }
+    for name in S.kernels:
+        starts, stops = probe_durations(torch, nsd, name, S.step, 8)
+        for _ in range(4):
+            S.step()
+        ms, _ = collect(torch, nsd, starts, stops)
+        per_kernel[name] = ms
+    dom = max(per_kernel, key=lambda n: per_kernel[n] or 0.0)
 
-    # ---- the oracle on the host, a reported baseline
+    # timed region: exactly K steps; the library records events around every
+    # launch of the dominant kernel
+    starts, stops = probe_durations(torch, nsd, dom, S.step, args.steps)
+    torch.cuda.synchronize()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    t_start.record()
+    for _ in range(args.steps):
+        S.step()
+    t_end.record()
+    torch.cuda.synchronize()
+    ms_per_step = t_start.elapsed_time(t_end) / args.steps
+    dom_ms, dom_launches = collect(torch, nsd, starts, stops)
+
+    algo = S.kernels[dom]
+    achieved = algo / (dom_ms * 1e-3) / 1e9
+    roofline = {
+        "bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+        "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+        "traffic": committed_traffic(dom, args.workload),
+        "algo_bytes_per_launch": int(algo), "avg_launch_ms": round(dom_ms, 5),
+        "launches_timed": dom_launches,
+    }
+    kernels = {n: {"ms": None if v is None else round(v, 5), "algo_bytes": int(S.kernels[n]),
+                   "GBps": None if not v else round(S.kernels[n] / (v * 1e-3) / 1e9, 1)}
+               for n, v in per_kernel.items()}
+
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(args, d, nnz)
+        cpu = cpu_baseline(args, d)
 
     out = {
         "metric": "gradient nonzeros/sec (forward+backward)",
-        "value": round(nnz / (ms_per_step * 1e-3), 1),
+        "value": round(S.nnz / (ms_per_step * 1e-3), 1),
         "unit": "nnz/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f32", "data": "synthetic",
-        "config": {"workload": workload_name(args.workload, d), "nnz": nnz, "k": k,
-                   "nrows": nrows, "ncols": ncols},
+        "config": {"workload": WORKLOAD_NAMES[args.workload] if args.size == "full"
+                   else f"{args.workload}_{args.size}", "nnz": S.nnz, "k": S.k},
         "roofline": roofline,
-        "kernels": per_kernel,
-        "preprocess_ms": {"csr_to_csc": round(csc_ms, 4),
-                          "upload_expand_csc": round(prep_ms_incl_upload, 2)},
+        "kernels": kernels,
+        "preprocess_ms": round(prep_ms, 2), "generate_s": round(gen_s, 1),
         "cpu_baseline": cpu,
         "source_digest": source_digest(),
     }
     print(json.dumps(out))
 
 
-def workload_name(w, d):
-    if w == "spmm":
-        return "spmm_grad_100k_1M_zipf1.1_k64"
+# ------------------------------------------------------------ CPU baseline
+
+def _sample(args, d):
+    """A bounded sample of the workload for the oracle: the whole input when
+    it is small, else a prefix (leading rows / entries) of it."""
+    w = args.workload
+    if w in ("spmm", "spmv"):
+        return d, "the full workload"
     if w == "gnn":
-        return "gnn_bilinear_2.4M_60M_zipf1.05_k256"
-    return "spmv_sum_1k_10k"
+        # leading rows; the columns they touch are renumbered so that only
+        # the needed rows of H and of dH are formed
+        rp = d["rowptr"]
+        nr = int(np.searchsorted(rp, 150_000, side="right")) - 1
+        e = int(rp[nr])
+        cols, colind = np.unique(d["colind"][:e], return_inverse=True)
+        s = dict(d, nrows=nr, ncols=len(cols), rowptr=rp[: nr + 1],
+                 colind=colind.astype(np.int32), val=d["val"][:e], G=d["G"][:nr],
+                 H=d["H"][cols])
+        return s, f"rows 0..{nr - 1} ({e} nnz) of the workload with the {len(cols)} columns they use"
+    if w == "mf":
+        e = 400_000
+        rows, row = np.unique(d["row"][:e], return_inverse=True)
+        cols, col = np.unique(d["col"][:e], return_inverse=True)
+        s = dict(d, nrows=len(rows), ncols=len(cols), row=row.astype(np.int32),
+                 col=col.astype(np.int32), val=d["val"][:e], U=d["U"][rows], V=d["V"][cols])
+        return s, f"the first {e} COO entries of the workload with their rows of U and V"
+    e = 1_000_000
+    return dict(d, i=d["i"][:e], j=d["j"][:e], k=d["k"][:e], val=d["val"][:e]), \
+        f"the first {e} COO entries of the workload, full factors"
 
 
-def cpu_baseline(args, d, nnz):
-    """The fp64 oracle, unchanged, on this host: whole passes of the same
-    workload (DOK build + every output) repeated for about cpu_seconds."""
+def cpu_baseline(args, d):
+    """The fp64 oracle, unchanged, single-threaded, on a bounded sample of the
+    workload: whole passes (DOK build + every output) repeated for about
+    cpu_seconds."""
     import oracle
-    nrows, ncols = d["nrows"], d["ncols"]
-    rows = np.repeat(np.arange(nrows, dtype=np.int32), np.diff(d["rowptr"]))
-    k = d.get("k", 1)
+    oracle.set_threads(1)
+    s, what = _sample(args, d)
+    w = args.workload
+
+    if w in ("spmm", "spmv", "gnn"):
+        nrows, ncols = s["nrows"], s["ncols"]
+        rows = np.repeat(np.arange(nrows, dtype=np.int32), np.diff(s["rowptr"]))
+        nnz = len(s["colind"])
+    elif w == "mf":
+        nnz = len(s["row"])
+    else:
+        nnz = len(s["i"])
 
     def one_pass():
-        D = oracle.Dok((nrows, ncols), (rows, d["colind"]), d["val"])
-        if args.workload == "spmm":
-            Cr, Cm = oracle.spmm(D, d["B"], k)
+        if w == "spmm":
+            D = oracle.Dok((nrows, ncols), (rows, s["colind"]), s["val"])
+            k = s["k"]
+            Cr, Cm = oracle.spmm(D, s["B"], k)
             oracle.loss_half_sq(Cr, Cm)
-            oracle.sddmm(D, Cr, d["B"], k, rows, d["colind"], Xmag=Cm)
+            oracle.sddmm(D, Cr, s["B"], k, rows, s["colind"], Xmag=Cm)
             oracle.spmm_t(D, Cr, k, Gmag=Cm)
-        elif args.workload == "gnn":
-            oracle.loss_bilinear(D, d["G"], d["H"], k)
-            oracle.sddmm(D, d["G"], d["H"], k, rows, d["colind"])
-            oracle.spmm_t(D, d["G"], k)
-        else:
-            oracle.loss_sum_spmv(D, d["x"])
-            oracle.sddmm(D, None, d["x"].reshape(-1, 1), 1, rows, d["colind"])
+        elif w == "spmv":
+            D = oracle.Dok((nrows, ncols), (rows, s["colind"]), s["val"])
+            oracle.loss_sum_spmv(D, s["x"])
+            oracle.sddmm(D, None, s["x"].reshape(-1, 1), 1, rows, s["colind"])
             oracle.spmm_t(D, None, 1)
+        elif w == "gnn":
+            D = oracle.Dok((nrows, ncols), (rows, s["colind"]), s["val"])
+            k = s["k"]
+            oracle.loss_bilinear(D, s["G"], s["H"], k)
+            oracle.sddmm(D, s["G"], s["H"], k, rows, s["colind"])
+            oracle.spmm_t(D, s["G"], k)
+        elif w == "mf":
+            D = oracle.Dok((s["nrows"], s["ncols"]), (s["row"], s["col"]), s["val"])
+            k = s["k"]
+            oracle.mf_loss(D, s["U"], s["V"], k)
+            oracle.mf_grad(D, s["U"], s["V"], k, 0)
+            oracle.mf_grad(D, s["U"], s["V"], k, 1)
+        else:
+            D = oracle.Dok(s["dims"], (s["i"], s["j"], s["k"]), s["val"])
+            F = (s["F1"], s["F2"], s["F3"])
+            oracle.cp_loss(D, *F, s["rank"])
+            oracle.cp_resid(D, *F, s["rank"], s["i"], s["j"], s["k"])
+            for m in range(3):
+                oracle.cp_grad(D, *F, s["rank"], m)
 
     passes, t0 = 0, time.perf_counter()
     while True:
@@ -256,10 +416,9 @@ def cpu_baseline(args, d, nnz):
         el = time.perf_counter() - t0
         if el >= args.cpu_seconds or passes >= 1000:
             break
-    per_pass = el / passes
-    return {"value": round(nnz / per_pass, 1), "unit": "nnz/s", "cores": 1, "kind": "oracle",
-            "sample": f"{passes} full pass(es) of the {args.workload} workload "
-                      f"({nnz} nnz; DOK build + all outputs), {el:.1f} s single-threaded",
+    return {"value": round(nnz * passes / el, 1), "unit": "nnz/s", "cores": 1, "kind": "oracle",
+            "sample": f"{what}: {passes} pass(es) of DOK build + loss + all gradients, "
+                      f"{el:.1f} s on one thread",
             "host_cpus_visible": len(os.sched_getaffinity(0))}
 
 

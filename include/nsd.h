@@ -133,6 +133,29 @@ typedef struct nsd_coo3 {
     nsd_coo3_mode mode[3];
 } nsd_coo3;
 
+/*
+ * Tensor-times-vector along the third mode of a sparse 3-tensor X (see
+ * nsd_ttv): X's entries in (i, j) order with the distinct projected keys
+ * numbered, and in l order, each view with its work plan.  Built by
+ * nsd_ttv_build; the two plans by nsd_plan_build on yptr and lptr.
+ */
+typedef struct nsd_ttv_plan {
+    int32_t dims[3];
+    int32_t nnz, ny;       /* entries of X; distinct (i, j) keys of Y */
+    const int32_t *yi;     /* [ny] key rows, (i, j) order */
+    const int32_t *yj;     /* [ny] key columns */
+    const int32_t *yptr;   /* [ny+1] entries of every key in the (i, j)-sorted order */
+    const int32_t *yseg;   /* [nnz] key of every (i, j)-sorted entry */
+    const int32_t *yperm;  /* [nnz] input position of every (i, j)-sorted entry */
+    const int32_t *ykidx;  /* [nnz] l of every (i, j)-sorted entry */
+    nsd_plan yplan;        /* plan over the keys */
+    const int32_t *lptr;   /* [dims[2]+1] entries of every l in the l-sorted order */
+    const int32_t *lseg;   /* [nnz] l of every l-sorted entry, non-decreasing */
+    const int32_t *lperm;  /* [nnz] input position of every l-sorted entry */
+    const int32_t *lpair;  /* [nnz] key of every l-sorted entry */
+    nsd_plan lplan;        /* plan over l */
+} nsd_ttv_plan;
+
 /* ----------------------------------------------------------------- info */
 
 /* Static string naming a status code. */
@@ -141,6 +164,37 @@ const char *nsd_status_string(int status);
 const char *nsd_last_error(void);
 /* Library ABI version (major * 10000 + minor * 100 + patch). */
 int nsd_version(void);
+
+/* ------------------------------------------------------- timing probe */
+
+/* Kernels that a timing probe can bracket. */
+typedef enum nsd_kernel_id {
+    NSD_KERNEL_NONE = 0,
+    NSD_KERNEL_SGR_MAIN = 1,   /* gather-reduce over a plan (SpMV/SpMM/A^T G) */
+    NSD_KERNEL_SGR_FIX = 2,    /* long-segment combine */
+    NSD_KERNEL_SDDMM = 3,      /* SDDMM over equal entry ranges */
+    NSD_KERNEL_FROB_ROW = 4,   /* SpMM-gradient row pass */
+    NSD_KERNEL_FROB_COL = 5,   /* SpMM-gradient column pass */
+    NSD_KERNEL_MF = 6,         /* factorisation row + column passes */
+    NSD_KERNEL_CP = 7,         /* CP three mode passes */
+    NSD_KERNEL_LOSS = 8,       /* loss total */
+    NSD_KERNEL_TTV = 9         /* TTV entry kernels */
+} nsd_kernel_id;
+
+/*
+ * Instrumentation for callers that measure kernel durations (benchmarks).
+ * While a probe is set on the calling thread, the library records the
+ * caller's hipEvent_t start[i % n] on the launching stream right before the
+ * i-th launch of the given kernel and stop[i % n] right after it, so that
+ * hipEventElapsedTime(start[i], stop[i]) is that launch's duration.  The
+ * probe keeps the n event handles (host arrays copied at the call) until
+ * nsd_probe_clear; the events themselves stay owned by the caller.
+ */
+nsd_status nsd_probe_set(int kernel_id, void *const *start_events, void *const *stop_events,
+                         int32_t n);
+/* Launches recorded since nsd_probe_set (host output). */
+nsd_status nsd_probe_count(int32_t *count);
+nsd_status nsd_probe_clear(void);
 
 /* ------------------------------------------------------------ workspace */
 
@@ -329,6 +383,41 @@ nsd_status nsd_cp_workspace_size(const nsd_coo3 *X, int32_t rank, size_t *bytes)
 nsd_status nsd_loss_cp(const nsd_coo3 *X, const float *F1, const float *F2, const float *F3,
                        int32_t rank, float seed, double *loss, float *dX, float *dF1,
                        float *dF2, float *dF3, void *ws, size_t ws_bytes, void *stream);
+
+/* Bytes of workspace nsd_ttv_build needs; dims is a host array of 3. */
+nsd_status nsd_ttv_build_workspace_size(int32_t nnz, const int32_t *dims, size_t *bytes);
+
+/*
+ * Projection of a COO 3-tensor (coordinates i, j, l [nnz], dims host[3]) onto
+ * its (i, j) keys: stable sort by (i, j), distinct keys numbered in (i, j)
+ * order (yi, yj [<= nnz]; yptr [nnz+1]), and the l-sorted view (lptr
+ * [dims[2]+1]).  *ny (host) = number of distinct keys.  Arrays yseg, yperm,
+ * ykidx, lseg, lperm, lpair are [nnz].  Bit-exact.  Synchronous.
+ */
+nsd_status nsd_ttv_build(int32_t nnz, const int32_t *dims, const int32_t *i, const int32_t *j,
+                         const int32_t *l, int32_t *yi, int32_t *yj, int32_t *yptr,
+                         int32_t *yseg, int32_t *yperm, int32_t *ykidx, int32_t *lptr,
+                         int32_t *lseg, int32_t *lperm, int32_t *lpair, int32_t *ny,
+                         void *ws, size_t ws_bytes, void *stream);
+
+/* Bytes of `ws` for nsd_ttv and nsd_ttv_vjp.  Writes *bytes (host). */
+nsd_status nsd_ttv_workspace_size(const nsd_ttv_plan *T, size_t *bytes);
+
+/*
+ * y[s] = sum over stored (i, j, l) with key s = (yi[s], yj[s]) of x * v(l):
+ * Y = X x_3 v on the projected keys.  x [nnz] in X's input order, v
+ * [dims[2]], y [ny].  Async.
+ */
+nsd_status nsd_ttv(const nsd_ttv_plan *T, const float *x, const float *v, float *y, void *ws,
+                   size_t ws_bytes, void *stream);
+
+/*
+ * Vector-Jacobian product of nsd_ttv for the upstream gy [ny]:
+ * dx[p] = gy[key(p)] * v(l_p) on X's keys (input order, [nnz]);
+ * dv(l) = sum over stored (i, j, l) of x * gy[key]  (dv [dims[2]]).  Async.
+ */
+nsd_status nsd_ttv_vjp(const nsd_ttv_plan *T, const float *x, const float *v, const float *gy,
+                       float *dx, float *dv, void *ws, size_t ws_bytes, void *stream);
 
 #ifdef __cplusplus
 }

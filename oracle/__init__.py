@@ -54,6 +54,8 @@ def _load():
         "orc_cp_grad": (None, [_p, _p, _p, _p, _i64, C.c_int, _i64, _p, _p, _p]),
         "orc_ttv": (_i64, [_p, _p, _p, _p, _p, _p]),
         "orc_ttv_vjp": (None, [_p, _p, _p, _i64, _p, _p, _p, _p, _p, _p, _p]),
+        "orc_set_threads": (None, [C.c_int]),
+        "orc_max_threads": (C.c_int, []),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -61,6 +63,15 @@ def _load():
         f.argtypes = args
     _lib = lib
     return lib
+
+
+def set_threads(n: int):
+    """Threads for the oracle's OpenMP loss scans on the calling thread."""
+    _load().orc_set_threads(n)
+
+
+def max_threads() -> int:
+    return _load().orc_max_threads()
 
 
 def _ptr(a):

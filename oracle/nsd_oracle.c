@@ -38,6 +38,25 @@
 #include <omp.h>
 #endif
 
+/* threads used by the OpenMP loss scans (the rest is single-threaded) */
+void orc_set_threads(int n)
+{
+#ifdef _OPENMP
+    omp_set_num_threads(n > 0 ? n : 1);
+#else
+    (void)n;
+#endif
+}
+
+int orc_max_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
 /* ------------------------------------------------------------------ DOK */
 
 typedef struct orc_dok {

@@ -189,7 +189,9 @@ static nsd_status launch_cp(CpParams f, double *loss, hipStream_t st) {
         grid += f.m[i].item_blocks + f.m[i].empty_blocks;
     }
     if (grid == 0) return loss_finalize(f.loss_part, 0, loss, st);
+    probe_begin(NSD_KERNEL_CP, st);
     cp_kernel<VEC, G, cp_unroll<G>()><<<grid, kBlock, 0, st>>>(f);
+    probe_end(NSD_KERNEL_CP, st);
     NSD_TRY(check_launch("cp_kernel"));
     for (int i = 0; i < 3; ++i) NSD_TRY((launch_fix<VEC, G>(f.m[i].s, nullptr, 0.0, st)));
     return loss_finalize(f.loss_part, grid, loss, st);

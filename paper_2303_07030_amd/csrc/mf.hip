@@ -147,7 +147,9 @@ static nsd_status launch_mf(MfParams f, double *loss, hipStream_t st) {
     const int grid = f.rows.item_blocks + f.rows.empty_blocks + f.cols.item_blocks +
                      f.cols.empty_blocks;
     if (grid == 0) return loss_finalize(f.loss_part, 0, loss, st);
+    probe_begin(NSD_KERNEL_MF, st);
     mf_kernel<VEC, G, mf_unroll_c<G>()><<<grid, kBlock, 0, st>>>(f);
+    probe_end(NSD_KERNEL_MF, st);
     NSD_TRY(check_launch("mf_kernel"));
     NSD_TRY((launch_fix<VEC, G>(f.rows.s, nullptr, 0.0, st)));
     NSD_TRY((launch_fix<VEC, G>(f.cols.s, nullptr, 0.0, st)));

@@ -25,6 +25,11 @@ nsd_status check_launch(const char *what);
 
 inline hipStream_t as_stream(void *s) { return reinterpret_cast<hipStream_t>(s); }
 
+// Timing probe hooks around a kernel launch (no-ops unless a probe is set
+// on this thread for that kernel id).
+void probe_begin(int kernel_id, hipStream_t st);
+void probe_end(int kernel_id, hipStream_t st);
+
 #define NSD_REQUIRE(cond, ...)                                   \
     do {                                                         \
         if (!(cond)) return ::nsd::fail(NSD_ERR_INVALID_ARG, __VA_ARGS__); \

@@ -63,7 +63,9 @@ static nsd_status launch_sgr_vg(SgrParams a, hipStream_t st) {
     a.item_blocks = (int32_t)ceil_div(a.plan.nitems, kSlots);
     const int64_t empty_blocks = ceil_div(a.plan.nempty, kSlots);
     dim3 grid((unsigned)(a.item_blocks + empty_blocks), (unsigned)ceil_div(a.k, G * VEC));
+    probe_begin(NSD_KERNEL_SGR_MAIN, st);
     sgr_main_kernel<VEC, G, sgr_unroll<G>()><<<grid, kBlock, 0, st>>>(a);
+    probe_end(NSD_KERNEL_SGR_MAIN, st);
     NSD_TRY(check_launch("sgr_main_kernel"));
     return launch_fix<VEC, G>(a, nullptr, 0.0, st);
 }
@@ -194,7 +196,9 @@ struct SddmmLauncher {
     hipStream_t st;
     template <int VEC, int G>
     nsd_status operator()() {
+        probe_begin(NSD_KERNEL_SDDMM, st);
         sddmm_kernel<VEC, G, sddmm_unroll<G>()><<<(unsigned)nb, kBlock, 0, st>>>(a);
+        probe_end(NSD_KERNEL_SDDMM, st);
         return check_launch("sddmm_kernel");
     }
 };
@@ -237,7 +241,9 @@ __global__ __launch_bounds__(kBlock) void loss_finalize_kernel(const double *par
 }
 
 nsd_status loss_finalize(const double *part, int64_t n, double *loss, hipStream_t st) {
+    probe_begin(NSD_KERNEL_LOSS, st);
     loss_finalize_kernel<<<1, kBlock, 0, st>>>(part, n, nullptr, 0, loss);
+    probe_end(NSD_KERNEL_LOSS, st);
     return check_launch("loss_finalize_kernel");
 }
 
@@ -316,18 +322,24 @@ static nsd_status launch_frob(FrobParams f, hipStream_t st) {
     constexpr int U = sgr_unroll<G>();
     f.rows.item_blocks = (int32_t)ceil_div(f.rows.plan.nitems, kSlots);
     const int row_blocks = f.rows.item_blocks + (int)ceil_div(f.rows.plan.nempty, kSlots);
+    probe_begin(NSD_KERNEL_FROB_ROW, st);
     frob_row_kernel<VEC, G, U><<<row_blocks, kBlock, 0, st>>>(f);
+    probe_end(NSD_KERNEL_FROB_ROW, st);
     NSD_TRY(check_launch("frob_row_kernel"));
     NSD_TRY((launch_fix<VEC, G>(f.rows, f.seg_loss, 0.5, st)));
     f.cols.item_blocks = (int32_t)ceil_div(f.cols.plan.nitems, kSlots);
     f.col_empty_blocks = (int32_t)ceil_div(f.cols.plan.nempty, kSlots);
     const int col_blocks = f.cols.item_blocks + f.col_empty_blocks +
                            (int)ceil_div(f.rows.plan.nchunks, kSlots);
+    probe_begin(NSD_KERNEL_FROB_COL, st);
     frob_col_kernel<VEC, G, U><<<col_blocks, kBlock, 0, st>>>(f);
+    probe_end(NSD_KERNEL_FROB_COL, st);
     NSD_TRY(check_launch("frob_col_kernel"));
     NSD_TRY((launch_fix<VEC, G>(f.cols, nullptr, 0.0, st)));
+    probe_begin(NSD_KERNEL_LOSS, st);
     loss_finalize_kernel<<<1, kBlock, 0, st>>>(f.loss_part, row_blocks, f.seg_loss,
                                                f.rows.plan.nlong, f.loss);
+    probe_end(NSD_KERNEL_LOSS, st);
     return check_launch("loss_finalize_kernel");
 }
 

@@ -221,8 +221,10 @@ template <int VEC, int G>
 inline nsd_status launch_fix(const SgrParams &a, double *seg_loss, double beta, hipStream_t st) {
     if (a.plan.nlong == 0) return NSD_OK;
     const int wave_blocks = (int)ceil_div(a.plan.nlong, kBlockWaves);
+    probe_begin(NSD_KERNEL_SGR_FIX, st);
     sgr_fix_kernel<VEC, G><<<wave_blocks + a.plan.nhuge, kBlock, 0, st>>>(a, wave_blocks, seg_loss,
                                                                          beta);
+    probe_end(NSD_KERNEL_SGR_FIX, st);
     return check_launch("sgr_fix_kernel");
 }
 

@@ -26,6 +26,8 @@ NSD_ERR_UNSUPPORTED = 6
 NSD_ERR_HIP = 7
 NSD_DUP_SUM = 0
 NSD_DUP_ERROR = 1
+KERNEL_IDS = {"sgr_main": 1, "sgr_fix": 2, "sddmm": 3, "frob_row": 4, "frob_col": 5, "mf": 6,
+              "cp": 7, "loss": 8, "ttv": 9}
 
 
 class NsdError(RuntimeError):
@@ -63,6 +65,14 @@ class nsd_coo3(C.Structure):
     _fields_ = [("dims", C.c_int32 * 3), ("nnz", C.c_int32), ("mode", nsd_coo3_mode * 3)]
 
 
+class nsd_ttv_plan(C.Structure):
+    _fields_ = [("dims", C.c_int32 * 3), ("nnz", C.c_int32), ("ny", C.c_int32),
+                ("yi", C.c_void_p), ("yj", C.c_void_p), ("yptr", C.c_void_p),
+                ("yseg", C.c_void_p), ("yperm", C.c_void_p), ("ykidx", C.c_void_p),
+                ("yplan", nsd_plan), ("lptr", C.c_void_p), ("lseg", C.c_void_p),
+                ("lperm", C.c_void_p), ("lpair", C.c_void_p), ("lplan", nsd_plan)]
+
+
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"libnsd.so is not built ({LIB_PATH}); run "
                       "`python -m paper_2303_07030_amd.build` first")
@@ -74,11 +84,15 @@ _SZ = C.c_size_t
 _CSR = C.POINTER(nsd_csr)
 _CSC = C.POINTER(nsd_csc)
 _COO3 = C.POINTER(nsd_coo3)
+_TTV = C.POINTER(nsd_ttv_plan)
 
 _SIGS = {
     "nsd_status_string": (C.c_char_p, [C.c_int]),
     "nsd_last_error": (C.c_char_p, []),
     "nsd_version": (C.c_int, []),
+    "nsd_probe_set": (C.c_int, [C.c_int, C.POINTER(_P), C.POINTER(_P), _I]),
+    "nsd_probe_count": (C.c_int, [C.POINTER(_I)]),
+    "nsd_probe_clear": (C.c_int, []),
     "nsd_workspace_size": (C.c_int, [_CSR, _CSC, _I, C.POINTER(_SZ)]),
     "nsd_plan_item_len": (C.c_int, [_I, _I, C.POINTER(_I)]),
     "nsd_plan_bounds": (C.c_int, [_I, _I, _I, C.POINTER(_I), C.POINTER(_I), C.POINTER(_I),
@@ -105,6 +119,12 @@ _SIGS = {
                                     _P]),
     "nsd_loss_mf": (C.c_int, [_CSR, _CSC, _P, _P, _P, _I, C.c_float, _P, _P, _P, _P, _SZ, _P]),
     "nsd_cp_workspace_size": (C.c_int, [_COO3, _I, C.POINTER(_SZ)]),
+    "nsd_ttv_build_workspace_size": (C.c_int, [_I, C.POINTER(_I), C.POINTER(_SZ)]),
+    "nsd_ttv_build": (C.c_int, [_I, C.POINTER(_I), _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                _P, C.POINTER(_I), _P, _SZ, _P]),
+    "nsd_ttv_workspace_size": (C.c_int, [_TTV, C.POINTER(_SZ)]),
+    "nsd_ttv": (C.c_int, [_TTV, _P, _P, _P, _P, _SZ, _P]),
+    "nsd_ttv_vjp": (C.c_int, [_TTV, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "nsd_loss_cp": (C.c_int, [_COO3, _P, _P, _P, _I, C.c_float, _P, _P, _P, _P, _P, _P, _SZ,
                               _P]),
 }
@@ -155,6 +175,24 @@ def nsd_last_error() -> str:
 
 def nsd_version() -> int:
     return _lib.nsd_version()
+
+
+def nsd_probe_set(kernel_id: int, start_events, stop_events):
+    """start_events / stop_events: raw hipEvent_t handles (ints)."""
+    n = len(start_events)
+    sa = (_P * n)(*start_events)
+    so = (_P * n)(*stop_events)
+    _check(_lib.nsd_probe_set(kernel_id, sa, so, n), "nsd_probe_set")
+
+
+def nsd_probe_count() -> int:
+    c = _I(0)
+    _check(_lib.nsd_probe_count(C.byref(c)), "nsd_probe_count")
+    return c.value
+
+
+def nsd_probe_clear():
+    _check(_lib.nsd_probe_clear(), "nsd_probe_clear")
 
 
 def nsd_workspace_size(A: nsd_csr, At, k: int) -> int:
@@ -305,3 +343,40 @@ def nsd_loss_cp(X: nsd_coo3, F1, F2, F3, rank, seed, loss, dX, dF1, dF2, dF3, ws
     _check(_lib.nsd_loss_cp(C.byref(X), _p(F1), _p(F2), _p(F3), rank, seed, _p(loss), _p(dX),
                             _p(dF1), _p(dF2), _p(dF3), _p(ws), _nbytes(ws), _stream(stream)),
            "nsd_loss_cp")
+
+
+def _dims3(dims):
+    return (_I * 3)(*[int(x) for x in dims])
+
+
+def nsd_ttv_build_workspace_size(nnz, dims) -> int:
+    b = _SZ(0)
+    _check(_lib.nsd_ttv_build_workspace_size(nnz, _dims3(dims), C.byref(b)),
+           "nsd_ttv_build_workspace_size")
+    return b.value
+
+
+def nsd_ttv_build(nnz, dims, i, j, l, yi, yj, yptr, yseg, yperm, ykidx, lptr, lseg, lperm, lpair,
+                  ws, stream=None) -> int:
+    ny = _I(0)
+    _check(_lib.nsd_ttv_build(nnz, _dims3(dims), _p(i), _p(j), _p(l), _p(yi), _p(yj), _p(yptr),
+                              _p(yseg), _p(yperm), _p(ykidx), _p(lptr), _p(lseg), _p(lperm),
+                              _p(lpair), C.byref(ny), _p(ws), _nbytes(ws), _stream(stream)),
+           "nsd_ttv_build")
+    return ny.value
+
+
+def nsd_ttv_workspace_size(T: nsd_ttv_plan) -> int:
+    b = _SZ(0)
+    _check(_lib.nsd_ttv_workspace_size(C.byref(T), C.byref(b)), "nsd_ttv_workspace_size")
+    return b.value
+
+
+def nsd_ttv(T: nsd_ttv_plan, x, v, y, ws, stream=None):
+    _check(_lib.nsd_ttv(C.byref(T), _p(x), _p(v), _p(y), _p(ws), _nbytes(ws), _stream(stream)),
+           "nsd_ttv")
+
+
+def nsd_ttv_vjp(T: nsd_ttv_plan, x, v, gy, dx, dv, ws, stream=None):
+    _check(_lib.nsd_ttv_vjp(C.byref(T), _p(x), _p(v), _p(gy), _p(dx), _p(dv), _p(ws), _nbytes(ws),
+                            _stream(stream)), "nsd_ttv_vjp")

@@ -148,3 +148,41 @@ class DeviceCoo3:
     def workspace(self, rank: int):
         n = nsd.nsd_cp_workspace_size(self.desc, rank)
         return torch.empty(max(n, 256), dtype=torch.uint8, device=self.val.device)
+
+
+class DeviceTtv:
+    """The TTV projection of a COO 3-tensor onto its (i, j) keys, built by
+    nsd_ttv_build, with work plans over the keys and over l."""
+
+    def __init__(self, dims, i, j, l, device="cuda", item_len=16, stream=None):
+        self.dims = tuple(int(d) for d in dims)
+        i, j, l = (_dev(c, torch.int32, device) for c in (i, j, l))
+        nnz = int(i.numel())
+        n = max(nnz, 1)
+
+        def arr(m):
+            return torch.empty(max(m, 1), dtype=torch.int32, device=device)
+
+        self.yi, self.yj, self.yptr = arr(n), arr(n), arr(nnz + 1)
+        self.yseg, self.yperm, self.ykidx = arr(n), arr(n), arr(n)
+        self.lptr, self.lseg, self.lperm, self.lpair = (arr(self.dims[2] + 1), arr(n), arr(n),
+                                                        arr(n))
+        ws = torch.empty(max(nsd.nsd_ttv_build_workspace_size(nnz, self.dims), 256),
+                         dtype=torch.uint8, device=device)
+        self.ny = nsd.nsd_ttv_build(nnz, self.dims, i, j, l, self.yi, self.yj, self.yptr,
+                                    self.yseg, self.yperm, self.ykidx, self.lptr, self.lseg,
+                                    self.lperm, self.lpair, ws, stream)
+        self.nnz = nnz
+        self.yplan = build_plan(self.ny, nnz, self.yptr, item_len, device, stream)
+        self.lplan = build_plan(self.dims[2], nnz, self.lptr, item_len, device, stream)
+        T = nsd.nsd_ttv_plan()
+        T.dims[:] = self.dims
+        T.nnz, T.ny = nnz, self.ny
+        for f in ("yi", "yj", "yptr", "yseg", "yperm", "ykidx", "lptr", "lseg", "lperm", "lpair"):
+            setattr(T, f, getattr(self, f).data_ptr())
+        T.yplan, T.lplan = self.yplan, self.lplan
+        self.desc = T
+
+    def workspace(self):
+        n = nsd.nsd_ttv_workspace_size(self.desc)
+        return torch.empty(max(n, 256), dtype=torch.uint8, device=self.yptr.device)

@@ -108,20 +108,26 @@ def _rows_without_replacement(rng, lengths: np.ndarray, ncols: int):
     big = min(4096, max(1, ncols // 8))
     small_rows = np.nonzero((lengths > 0) & (lengths <= big))[0]
     big_rows = np.nonzero(lengths > big)[0]
-    # short rows: all at once, redraw collisions until every row is distinct
+    # short rows: all at once, redraw collisions until every row is distinct;
+    # after the first round only the rows that had a collision are re-checked
     ls = lengths[small_rows]
     rows_rep = np.repeat(small_rows.astype(np.int64), ls)
     cols = rng.integers(0, ncols, size=rows_rep.shape[0], dtype=np.int64)
-    while True:
-        key = rows_rep * ncols + cols
+    active = np.arange(rows_rep.shape[0], dtype=np.int64)
+    while active.shape[0]:
+        key = rows_rep[active] * ncols + cols[active]
         order = np.argsort(key, kind="stable")
         ks = key[order]
-        dup = np.zeros(key.shape[0], dtype=bool)
+        dup = np.zeros(active.shape[0], dtype=bool)
         dup[order[1:][ks[1:] == ks[:-1]]] = True
         ndup = int(dup.sum())
         if ndup == 0:
             break
-        cols[dup] = rng.integers(0, ncols, size=ndup, dtype=np.int64)
+        pos = active[dup]
+        cols[pos] = rng.integers(0, ncols, size=ndup, dtype=np.int64)
+        bad = np.zeros(nrows, dtype=bool)
+        bad[rows_rep[pos]] = True
+        active = np.nonzero(bad[rows_rep])[0]
     key = rows_rep * ncols + cols
     cols_sorted = (np.sort(key) % ncols).astype(np.int32)
     starts = np.zeros(small_rows.shape[0], dtype=np.int64)

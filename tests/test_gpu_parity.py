@@ -490,6 +490,36 @@ def test_loss_cp_shapes(nsd, orc, rank, dims):
     check_cp(orc, dims, i, j, l, val, F, rank, got, seed=2.0)
 
 
+@pytest.mark.parametrize("dims,nnz", [((60, 60, 60), 25_000), ((5, 7, 300), 2_000),
+                                       ((40, 30, 1), 500)])
+def test_ttv_and_vjp(nsd, orc, dims, nnz):
+    from paper_2303_07030_amd.operand import DeviceTtv
+    rng = np.random.default_rng(nnz)
+    keys = rng.choice(dims[0] * dims[1] * dims[2], size=nnz, replace=False)
+    i = (keys // (dims[1] * dims[2])).astype(np.int32)
+    j = ((keys // dims[2]) % dims[1]).astype(np.int32)
+    l = (keys % dims[2]).astype(np.int32)
+    x = rng.standard_normal(nnz).astype(np.float32)
+    v = rng.standard_normal(dims[2]).astype(np.float32)
+    T = DeviceTtv(dims, i, j, l)
+    D = orc.Dok(dims, (i, j, l), x)
+    yi, yj, y, ym = orc.ttv(D, v)
+    assert T.ny == len(yi)
+    assert np.array_equal(host(T.yi)[:T.ny], yi) and np.array_equal(host(T.yj)[:T.ny], yj)
+    ws = T.workspace()
+    yg = torch.full((T.ny,), np.nan, dtype=torch.float32, device="cuda")
+    nsd.nsd_ttv(T.desc, dev(x), dev(v), yg, ws)
+    assert_mag_close(host(yg), y, ym, what="Y")
+    gy = rng.standard_normal(T.ny).astype(np.float32)
+    dx = torch.full((nnz,), np.nan, dtype=torch.float32, device="cuda")
+    dv = torch.full((dims[2],), np.nan, dtype=torch.float32, device="cuda")
+    nsd.nsd_ttv_vjp(T.desc, dev(x), dev(v), dev(gy), dx, dv, ws)
+    gY = orc.Dok((dims[0], dims[1]), (yi, yj), gy)
+    rdx, rdxm, rdv, rdvm = orc.ttv_vjp(D, v, gY, i, j, l)
+    assert_mag_close(host(dx), rdx, rdxm, what="dX")
+    assert_mag_close(host(dv), rdv, rdvm, what="dv")
+
+
 # ------------------------------------------------------- edge cases
 
 def test_empty_matrix_writes_zeros(nsd, operand):
