@@ -241,6 +241,7 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
 
+    synth.VERBOSE = True  # progress lines on stderr while the inputs are drawn
     t0 = time.perf_counter()
     d = synth.make(args.workload, args.size)
     gen_s = time.perf_counter() - t0

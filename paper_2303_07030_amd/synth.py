@@ -37,9 +37,18 @@ Zipf readings (the workload text only says "Zipf(s)"):
 """
 from __future__ import annotations
 
+import sys
+import time
+
 import numpy as np
 
 ENTROPY = 230307030
+VERBOSE = False  # progress lines on stderr for the multi-minute workloads
+
+
+def _say(msg):
+    if VERBOSE:
+        print(f"[synth {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
 WORKLOAD_IDS = {"spmv": 1, "spmm": 2, "mf": 3, "cp": 4, "gnn": 5}
 
 # Full-size workloads and smaller variants of the same recipes that the
@@ -136,6 +145,7 @@ def _rows_without_replacement(rng, lengths: np.ndarray, ncols: int):
     offs = np.arange(rows_rep.shape[0], dtype=np.int64) - np.repeat(starts, ls)
     pos = np.repeat(rowptr[small_rows], ls) + offs
     colind[pos] = cols_sorted
+    _say(f"short rows placed; {len(big_rows)} long rows to draw")
     # long rows one by one (numpy picks a set-based or permutation method)
     for r in big_rows:
         c = rng.choice(ncols, size=int(lengths[r]), replace=False)
@@ -159,12 +169,52 @@ def _normal(rng, shape, std=1.0):
     return x
 
 
-def _zipf_ids(rng, u_count: int, N: int, s: float, rank_to_id: np.ndarray):
+def _zipf_cdf(N: int, s: float):
+    """Truncated Zipf CDF over ranks 1..N plus a guide table for inversion."""
     cdf = np.cumsum(np.arange(1, N + 1, dtype=np.float64) ** (-s))
     cdf /= cdf[-1]
+    # guide[b] = first rank index whose CDF exceeds b / M (M a power of two,
+    # so u * M and b / M are exact and the bracket below is exact)
+    M = 1 << 22
+    guide = np.searchsorted(cdf, np.arange(M + 1, dtype=np.float64) / M, side="right")
+    return cdf, guide
+
+
+def _zipf_ids(rng, u_count: int, table, rank_to_id: np.ndarray):
+    """Inverse-CDF draws: the first rank whose CDF exceeds u (bracketed by
+    the guide table, then bisected), mapped through rank_to_id."""
+    cdf, guide = table
+    N = cdf.shape[0]
+    M = guide.shape[0] - 1
     u = rng.random(u_count)
-    rank = np.minimum(np.searchsorted(cdf, u, side="right"), N - 1)
-    return rank_to_id[rank]
+    b = (u * M).astype(np.int64)
+    lo, hi = guide[b], guide[b + 1]
+    act = np.nonzero(lo < hi)[0]
+    while act.shape[0]:
+        l, h = lo[act], hi[act]
+        mid = (l + h) >> 1
+        right = cdf[mid] <= u[act]
+        lo[act] = np.where(right, mid + 1, l)
+        hi[act] = np.where(right, h, mid)
+        act = act[lo[act] < hi[act]]
+    return rank_to_id[np.minimum(lo, N - 1)]
+
+
+def _first_unique(keys: np.ndarray):
+    """np.unique(keys, return_index=True) (sorted distinct keys and the index
+    of each one's first occurrence) via one sort of (key, index) packed into
+    a uint64 when both fit."""
+    n = keys.shape[0]
+    ib = max(1, int(n - 1).bit_length())
+    if n == 0 or int(keys.min()) < 0 or int(keys.max()).bit_length() + ib > 64:
+        return np.unique(keys, return_index=True)
+    c = (keys.astype(np.uint64) << np.uint64(ib)) | np.arange(n, dtype=np.uint64)
+    c.sort()
+    k = (c >> np.uint64(ib)).astype(np.int64)
+    head = np.ones(n, dtype=bool)
+    head[1:] = k[1:] != k[:-1]
+    first = (c[head] & np.uint64((1 << ib) - 1)).astype(np.int64)
+    return k[head], first
 
 
 def _dedupe_first(draw_batch, nnz: int):
@@ -173,8 +223,9 @@ def _dedupe_first(draw_batch, nnz: int):
     out = []
     count = 0
     while count < nnz:
+        _say(f"distinct keys {count}/{nnz}")
         keys = draw_batch()
-        uk, first = np.unique(keys, return_index=True)
+        uk, first = _first_unique(keys)
         if seen.shape[0]:
             pos = np.minimum(np.searchsorted(seen, uk), seen.shape[0] - 1)
             new = seen[pos] != uk
@@ -215,9 +266,11 @@ def make_mf(nrows=1_000_000, ncols=500_000, nnz=50_000_000, s=1.1, k=128,
     col_ids = g_pat.permutation(ncols)
     batch = min(batch, max(4 * nnz, 1024))
 
+    cdf_r, cdf_c = _zipf_cdf(nrows, s), _zipf_cdf(ncols, s)
+
     def draw():
-        r = _zipf_ids(g_pat, batch, nrows, s, row_ids).astype(np.int64)
-        c = _zipf_ids(g_pat, batch, ncols, s, col_ids).astype(np.int64)
+        r = _zipf_ids(g_pat, batch, cdf_r, row_ids).astype(np.int64)
+        c = _zipf_ids(g_pat, batch, cdf_c, col_ids).astype(np.int64)
         return r * ncols + c
 
     keys = _dedupe_first(draw, nnz)
@@ -264,4 +317,7 @@ MAKERS = {"spmv": make_spmv, "spmm": make_spmm, "mf": make_mf, "cp": make_cp,
 def make(workload: str, size: str = "full", replicate: int = 0, **over):
     params = dict(PRESETS[workload][size])
     params.update(over)
-    return MAKERS[workload](replicate=replicate, **params)
+    _say(f"generating {workload} ({size})")
+    d = MAKERS[workload](replicate=replicate, **params)
+    _say(f"generated {workload} ({size})")
+    return d
