@@ -99,13 +99,12 @@ def setup_spmm(d, dev, torch, nsd, ops):
     S = Setup()
     S.A, S.nnz, S.k = A, nnz, k
     S.step = lambda: nsd.nsd_loss_frob_spmm(A.desc, A.csc, B, k, 1.0, C, loss, dA, dB, ws)
-    long_nnz = int(sum(np.diff(d["rowptr"])[np.diff(d["rowptr"]) > A.item_len]))
     S.kernels = {
-        # rowidx, colind, val in; dA out; B read and C written once
-        "frob_row": (4 * 4 * nnz + 4 * k * (nr + nc)),
-        # colidx, rowind, perm, val (via perm) in; C read, dB written once;
-        # SDDMM of the long rows' entries (indices in, dA out)
-        "frob_col": (4 * 4 * nnz + 4 * k * (nr + nc) + 3 * 4 * long_nnz),
+        # rowidx, colind, val in; B read once, C written once
+        "frob_row": 3 * 4 * nnz + 4 * k * (nr + nc),
+        # colidx, rowind, perm, val (through perm) in, dA out; C and B read
+        # once, dB written once
+        "frob_col": 5 * 4 * nnz + 4 * k * (nr + 2 * nc),
     }
     return S
 
@@ -124,10 +123,9 @@ def setup_gnn(d, dev, torch, nsd, ops):
     S.A, S.nnz, S.k = A, nnz, k
     S.step = lambda: nsd.nsd_loss_bilinear(A.desc, A.csc, H, G, k, 1.0, loss, dA, dH, ws)
     S.kernels = {
-        # rowidx, colind, val in, dA out; G and H read once
-        "sddmm": 4 * 4 * nnz + 4 * k * (nr + nc),
-        # colidx, rowind, perm, val (via perm) in; G read once, dH written once
-        "sgr_main": 4 * 4 * nnz + 4 * k * (nr + nc),
+        # one column pass: colidx, rowind, perm, val (through perm) in, dA
+        # out; G and H read once, dH written once
+        "dual": 5 * 4 * nnz + 4 * k * (nr + 2 * nc),
     }
     return S
 
@@ -189,8 +187,9 @@ def setup_spmv(d, dev, torch, nsd, ops):
     S.A, S.nnz, S.k = A, nnz, 1
     S.step = lambda: nsd.nsd_loss_sum_spmv(A.desc, A.csc, x, 1.0, loss, dA, dx, ws)
     S.kernels = {
-        "sddmm": 4 * 4 * nnz + 4 * nc,
-        "sgr_main": 4 * 4 * nnz + 4 * nc,
+        # one column pass: colidx, rowind, perm, val (through perm) in, dA
+        # out; x read once, dx written once
+        "dual": 5 * 4 * nnz + 2 * 4 * nc,
     }
     return S
 

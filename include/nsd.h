@@ -178,7 +178,9 @@ typedef enum nsd_kernel_id {
     NSD_KERNEL_MF = 6,         /* factorisation row + column passes */
     NSD_KERNEL_CP = 7,         /* CP three mode passes */
     NSD_KERNEL_LOSS = 8,       /* loss total */
-    NSD_KERNEL_TTV = 9         /* TTV entry kernels */
+    NSD_KERNEL_TTV = 9,        /* TTV entry kernels */
+    NSD_KERNEL_DUAL = 10       /* one column pass giving dA, A^T G and the loss
+                                  (bilinear and SMVM losses) */
 } nsd_kernel_id;
 
 /*

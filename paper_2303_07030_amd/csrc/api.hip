@@ -60,8 +60,10 @@ static size_t loss_part_count(const nsd_csr *A, const nsd_csc *At, int k) {
     int64_t m = std::max<int64_t>(1, frob_row_blocks(A->plan, k));
     for (int kk : {k, 1})
         for (bool v : {true, false}) m = std::max(m, sddmm_shape(A->nnz, kk, v).nblocks);
-    if (At)
-        for (bool v : {true, false}) m = std::max(m, mf_blocks(A->plan, At->plan, k, v));
+    if (At) {
+        const nsd_plan *both[2] = {&A->plan, &At->plan};
+        for (bool v : {true, false}) m = std::max(m, dual_blocks(both, 2, k, v));
+    }
     return (size_t)m;
 }
 
@@ -143,6 +145,39 @@ static SddmmParams sddmm_params(const nsd_csr *A, const float *X, const float *Y
     return p;
 }
 
+// Linear dual pass over A's columns: own row O[j], gathered row X[i] (NULL:
+// ones), w = A's values through perm;  out = alpha * A^T X,
+// sdd[p] = sdd_alpha * <X_i, O_j> at A's storage position p.
+static DualPass col_dual(const nsd_csr *A, const nsd_csc *At, const float *X, const float *O,
+                         int k, float alpha, float *out, float *part, float *sdd,
+                         float sdd_alpha, bool count_loss) {
+    DualPass d;
+    d.s = cols_params(A, At, X, k, alpha, out, part);
+    d.own = O;
+    d.sdd = sdd;
+    d.sdd_alpha = sdd_alpha;
+    d.count_loss = count_loss ? 1 : 0;
+    return d;
+}
+
+// One linear dual pass over the columns with its loss, then the loss total.
+static nsd_status col_dual_loss(const DualPass &pass, double *loss_part, double *loss,
+                                hipStream_t st) {
+    DualParams f;
+    f.pass[0] = pass;
+    f.npass = 1;
+    f.loss_part = loss_part;
+    int64_t grid = 0;
+    NSD_TRY(dual_fused(kDualLin, f, NSD_KERNEL_DUAL, &grid, st));
+    return loss_finalize(loss_part, grid, loss, st);
+}
+
+static bool col_dual_ok(const DualPass &pass) {
+    DualParams f;
+    f.pass[0] = pass;
+    return dual_supported(pass.s.k, dual_vec_ok(f));
+}
+
 // The loss partial count of a fused SDDMM; with nnz == 0 the loss is 0.
 static nsd_status finish_loss(const SddmmParams &p, double *loss, hipStream_t st) {
     // with nnz == 0 there are no partials and the finaliser writes 0
@@ -215,6 +250,12 @@ nsd_status nsd_loss_sum_spmv(const nsd_csr *A, const nsd_csc *At, const float *x
     ComputeWs w;
     NSD_TRY(carve_compute(ws, ws_bytes, A, At, 1, &w));
     hipStream_t st = as_stream(stream);
+    if (A->nnz > 0) {
+        // one pass over the columns: own row x[j], gathered row 1:
+        // dA[p] = seed * x[j], loss = sum_p A_p x[j], dx = seed * A^T 1
+        return col_dual_loss(col_dual(A, At, nullptr, x, 1, seed, dx, w.part_col, dA, seed, true),
+                             w.loss_part, loss, st);
+    }
     // dA[p] = seed * x[col]; loss = sum_p A_p * x[col]
     SddmmParams sp = sddmm_params(A, nullptr, x, 1, seed, dA);
     sp.w = A->val;
@@ -240,12 +281,11 @@ nsd_status nsd_loss_frob_spmm(const nsd_csr *A, const nsd_csc *At, const float *
     NSD_TRY(carve_compute(ws, ws_bytes, A, At, k, &w));
     hipStream_t st = as_stream(stream);
     if (A->nnz > 0 && frob_fused_ok(k, B, C, dB)) {
-        // row pass (C, loss, dA on short rows), long-row combine, column pass
-        // (dB and dA on long rows), long-column combine, loss total
+        // row pass (C and the loss), long-row combine, one column pass (dB
+        // and dA, with B_j the column's own row), long-column combine, total
         FrobParams f;
         f.rows = rows_params(A, B, k, 1.f, C, w.part);
-        f.cols = cols_params(A, At, C, k, seed, dB, w.part_col);
-        f.sdd = sddmm_params(A, C, B, k, seed, dA);
+        f.cols = col_dual(A, At, C, B, k, seed, dB, w.part_col, dA, seed, false);
         f.loss_part = w.loss_part;
         f.seg_loss = w.seg_loss;
         f.loss = loss;
@@ -276,6 +316,12 @@ nsd_status nsd_loss_bilinear(const nsd_csr *A, const nsd_csc *At, const float *H
     ComputeWs w;
     NSD_TRY(carve_compute(ws, ws_bytes, A, At, k, &w));
     hipStream_t st = as_stream(stream);
+    if (A->nnz > 0) {
+        // one pass over the columns: own row H_j, gathered row G_i:
+        // dA[p] = seed <G_i, H_j>, loss = sum_p A_p <G_i, H_j>, dH = seed A^T G
+        const DualPass pass = col_dual(A, At, G, H, k, seed, dH, w.part_col, dA, seed, true);
+        if (col_dual_ok(pass)) return col_dual_loss(pass, w.loss_part, loss, st);
+    }
     // dA = seed * <G_i, H_j>; loss = sum_p A_p <G_i, H_j>
     SddmmParams sp = sddmm_params(A, G, H, k, seed, dA);
     sp.w = A->val;
@@ -297,23 +343,30 @@ nsd_status nsd_loss_mf(const nsd_csr *A, const nsd_csc *At, const float *valT, c
     NSD_REQUIRE(A->nrows == 0 || dU != nullptr, "dU is NULL");
     NSD_REQUIRE(A->ncols == 0 || dV != nullptr, "dV is NULL");
     NSD_REQUIRE(A->nnz == 0 || (U && V), "U/V is NULL");
-    const bool vec = mf_vec_ok(k, U, V, dU, dV);
-    if (vec ? k > 256 : k > 64)
+    const bool vec = k % 4 == 0 && aligned16(U) && aligned16(V) && aligned16(dU) && aligned16(dV);
+    if (!dual_supported(k, vec))
         return fail(NSD_ERR_UNSUPPORTED, "factor width k = %d (at most 256, multiple of 4 and "
                                          "16-byte aligned rows; otherwise at most 64)", k);
     ComputeWs w;
     NSD_TRY(carve_compute(ws, ws_bytes, A, At, k, &w));
-    MfParams f;
-    f.rows.s = rows_params(A, V, k, -2.f * seed, dU, w.part);
-    f.rows.own = U;
-    f.cols.s = cols_params(A, At, U, k, -2.f * seed, dV, w.part_col);
+    // row pass: dU = -2 seed sum_j r_ij V_j with the loss; column pass:
+    // dV = -2 seed sum_i r_ij U_i, r recomputed; both in one launch
+    DualParams f;
+    f.npass = 2;
+    f.pass[0].s = rows_params(A, V, k, -2.f * seed, dU, w.part);
+    f.pass[0].own = U;
+    f.pass[0].count_loss = 1;
+    f.pass[1].s = cols_params(A, At, U, k, -2.f * seed, dV, w.part_col);
     if (valT) {
-        f.cols.s.w = valT;
-        f.cols.s.wperm = nullptr;
+        f.pass[1].s.w = valT;
+        f.pass[1].s.wperm = nullptr;
     }
-    f.cols.own = V;
+    f.pass[1].own = V;
     f.loss_part = w.loss_part;
-    return mf_fused(f, loss, as_stream(stream));
+    hipStream_t st = as_stream(stream);
+    int64_t grid = 0;
+    NSD_TRY(dual_fused(kDualMf, f, NSD_KERNEL_MF, &grid, st));
+    return loss_finalize(w.loss_part, grid, loss, st);
 }
 
 static nsd_status check_coo3(const nsd_coo3 *X) {

@@ -1,0 +1,292 @@
+// Segment passes that use the segment's own dense row: one gather per entry
+// serves both a sampled dot product and a gather-reduce.
+//
+// A pass walks a sorted sparse operand over its work plan (segments = the
+// rows of a CSR, or the columns of its CSC).  For entry p of segment s, with
+// gathered row X[idx_p] and the segment's own row O[s]:
+//     d_p = <O[s], X[idx_p]>                  (reduced across the slot's lanes)
+//     out[s] = alpha * sum_{p in s} c_p X[idx_p]
+// where the coefficient c_p depends on the kind of pass:
+//   linear (kDualLin):   c_p = w_p; optionally sdd[pos_p] = sdd_alpha * d_p
+//                        and loss += w_p d_p.  With O = B, X = C = A B over
+//                        A's columns this is dB = A^T C together with
+//                        dA = <C_i, B_j> of L = 1/2 ||A B||^2; with O = H,
+//                        X = G it is the whole bilinear layer
+//                        L = sum (A H) o G: dA = <G_i, H_j>, dH = A^T G.
+//   residual (kDualMf):  c_p = r_p = w_p - d_p, loss += r_p^2: the row and
+//                        column passes of sparse matrix factorisation.
+// These are the paper's sums over the stored keys of A with the dense rows
+// looked up by key (Logical SDQLite, Section 3); the sampled product keeps
+// the gradient of A on A's keys (Section 4.2), the `+=` of the code
+// generation (Section 5.5) becomes a fixed-order segmented sum.
+//
+// pos_p is the entry's position in the sparse operand's storage order
+// (perm[p] for a CSC pass), so the sampled product is written aligned with
+// A's own pattern.  Up to two passes share one launch on disjoint block
+// ranges; long segments leave chunk partials combined by the shared kernel.
+#include "nsd_internal.hpp"
+#include "segreduce.hpp"
+#include "segreduce_dev.hpp"
+
+namespace nsd {
+
+template <int U>
+struct DualMeta {
+    int r[U], c[U], pos[U];
+    float w[U];
+};
+
+// Storage positions of entries [p, p + U): wperm[q], or q itself.  They are
+// loaded one batch before the rest of the metadata, so that the weight
+// gather w[pos] never waits on them inside a batch.
+template <int U>
+__device__ __forceinline__ void dual_pos(const SgrParams &a, int64_t p, int64_t b0, int (&pos)[U]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int64_t q = p + u;
+        pos[u] = q < b0 ? (a.wperm ? a.wperm[q] : (int)q) : 0;
+    }
+}
+
+// The rest of the metadata of entries [p, p + U), positions already in
+// m.pos; padding entries repeat the item's last segment and gathered row
+// (valid addresses) with weight 0.
+template <int U>
+__device__ __forceinline__ void dual_rest(const SgrParams &a, int64_t p, int64_t b0, int last_r,
+                                          int last_c, DualMeta<U> &m) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int64_t q = p + u;
+        if (q < b0) {
+            m.r[u] = a.segidx[q];
+            m.c[u] = a.idx[q];
+            m.w[u] = a.w ? a.w[m.pos[u]] : 1.f;
+        } else {
+            m.r[u] = last_r;
+            m.c[u] = last_c;
+            m.w[u] = 0.f;
+        }
+    }
+}
+
+template <int KIND, int VEC, int G, int U>
+__device__ __forceinline__ void dual_walk(const DualPass &m, int64_t s, int lane, double &lsum) {
+    const SgrParams &a = m.s;
+    const int g = lane % G;
+    const int col = g * VEC;  // k <= G * VEC on this path
+    const bool on = col < a.k;
+    const int64_t k = a.k;
+    const int64_t a0 = a.plan.item_ptr[s];
+    const int64_t b0 = a.plan.item_ptr[s + 1];
+    const int last_r = a.segidx[b0 - 1];
+    const int last_c = a.idx[b0 - 1];
+    int row = a.segidx[a0];
+    bool carry = a0 > 0 && a.segidx[a0 - 1] == row;
+
+    Vec<VEC> acc;
+    acc.zero();
+    auto flush = [&]() {
+        if (!on) return;
+        if (carry) {
+            acc.store(a.part + s * k + col);
+        } else {
+            Vec<VEC> t = acc;
+            t.scale(a.alpha);
+            t.store(a.out + (int64_t)row * k + col);
+        }
+    };
+
+    // three-stage metadata pipeline: positions two batches ahead, the rest
+    // one batch ahead, the dense rows of the current batch
+    DualMeta<U> cur, nxt;
+    int pnext[U];
+    dual_pos(a, a0, b0, cur.pos);
+    dual_rest(a, a0, b0, last_r, last_c, cur);
+    dual_pos(a, a0 + U, b0, pnext);
+    for (int64_t p = a0; p < b0; p += U) {
+        if (p + U < b0) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) nxt.pos[u] = pnext[u];
+            dual_rest(a, p + U, b0, last_r, last_c, nxt);
+            if (p + 2 * U < b0) dual_pos(a, p + 2 * U, b0, pnext);
+        }
+        Vec<VEC> xv[U], ov[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (on) {
+                if (a.X) xv[u].load(a.X + (int64_t)cur.c[u] * k + col);
+                else xv[u].ones();
+                ov[u].load(m.own + (int64_t)cur.r[u] * k + col);
+            } else {
+                xv[u].zero();
+                ov[u].zero();
+            }
+        }
+        float d[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) d[u] = ov[u].dot(xv[u]);
+        float coef[U];
+        if constexpr (KIND == kDualMf) {
+            if constexpr (G == 1) {
+#pragma unroll
+                for (int u = 0; u < U; ++u) coef[u] = p + u < b0 ? cur.w[u] - d[u] : 0.f;
+            } else {
+                const float tot = transpose_reduce<G, U>(d, lane);
+                constexpr int kRep = G / U;
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const float t = __shfl(tot, u * kRep, G);
+                    coef[u] = p + u < b0 ? cur.w[u] - t : 0.f;
+                }
+            }
+            if (m.count_loss && g == 0)
+#pragma unroll
+                for (int u = 0; u < U; ++u) lsum += (double)coef[u] * coef[u];
+        } else {
+#pragma unroll
+            for (int u = 0; u < U; ++u) coef[u] = cur.w[u];  // 0 on padding
+            if constexpr (G == 1) {
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    if (p + u < b0) {
+                        if (m.sdd) m.sdd[cur.pos[u]] = m.sdd_alpha * d[u];
+                        if (m.count_loss) lsum += (double)cur.w[u] * d[u];
+                    }
+                }
+            } else {
+                const float tot = transpose_reduce<G, U>(d, lane);
+                constexpr int kRep = G / U;
+                const int us = g / kRep;  // the entry whose total this lane holds
+                int pos = cur.pos[0];
+                float w = cur.w[0];
+#pragma unroll
+                for (int u = 1; u < U; ++u) {
+                    if (us == u) {
+                        pos = cur.pos[u];
+                        w = cur.w[u];
+                    }
+                }
+                if (g % kRep == 0 && p + us < b0) {
+                    if (m.sdd) m.sdd[pos] = m.sdd_alpha * tot;
+                    if (m.count_loss) lsum += (double)w * tot;
+                }
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (cur.r[u] != row) {
+                flush();
+                row = cur.r[u];
+                carry = false;
+                acc.zero();
+            }
+            acc.fma(coef[u], xv[u]);
+        }
+        cur = nxt;
+    }
+    if (b0 == a.nnz || a.segidx[b0] != row) {
+        flush();
+    } else if (on) {
+        acc.store(a.part + s * k + col);
+    }
+}
+
+template <int KIND, int VEC, int G, int U>
+__device__ __forceinline__ void dual_block(const DualPass &m, int b, double &lsum) {
+    constexpr int kSlots = kBlock / G;
+    const int lane = threadIdx.x % kWave;
+    const int g = threadIdx.x % G;
+    if (b < m.item_blocks) {
+        const int64_t s = (int64_t)b * kSlots + threadIdx.x / G;
+        if (s < m.s.plan.nitems) dual_walk<KIND, VEC, G, U>(m, s, lane, lsum);
+    } else {
+        zero_segment<VEC>(m.s, (int64_t)(b - m.item_blocks) * kSlots + threadIdx.x / G, g * VEC,
+                          g * VEC < m.s.k);
+    }
+}
+
+template <int KIND, int VEC, int G, int U>
+__global__ __launch_bounds__(kBlock) void dual_kernel(DualParams f) {
+    const int first = f.pass[0].item_blocks + f.pass[0].empty_blocks;
+    double lsum = 0.0;
+    if ((int)blockIdx.x < first) dual_block<KIND, VEC, G, U>(f.pass[0], blockIdx.x, lsum);
+    else dual_block<KIND, VEC, G, U>(f.pass[1], (int)blockIdx.x - first, lsum);
+    if (f.loss_part) {
+        const double t = block_sum(lsum);
+        if (threadIdx.x == 0) f.loss_part[blockIdx.x] = f.loss_beta * t;
+    }
+}
+
+template <int G>
+constexpr int dual_unroll() {
+    return G >= 4 ? 4 : (G == 1 ? 4 : G);
+}
+
+int64_t dual_blocks(const nsd_plan *const *plans, int npass, int k, bool vec) {
+    const WidthPlan wp = width_plan(k, vec);
+    const int slots = kBlock / wp.g;
+    int64_t n = 0;
+    for (int i = 0; i < npass; ++i)
+        n += ceil_div(plans[i]->nitems, slots) + ceil_div(plans[i]->nempty, slots);
+    return n;
+}
+
+template <int KIND, int VEC, int G>
+static nsd_status launch_dual(DualParams f, int probe_id, int64_t *grid_out, hipStream_t st) {
+    constexpr int kSlots = kBlock / G;
+    int64_t grid = 0;
+    for (int i = 0; i < 2; ++i) {
+        DualPass &m = f.pass[i];
+        if (i >= f.npass) {
+            m.item_blocks = m.empty_blocks = 0;
+            continue;
+        }
+        m.item_blocks = (int32_t)ceil_div(m.s.plan.nitems, kSlots);
+        m.empty_blocks = (int32_t)ceil_div(m.s.plan.nempty, kSlots);
+        grid += m.item_blocks + m.empty_blocks;
+    }
+    *grid_out = grid;
+    if (grid == 0) return NSD_OK;
+    probe_begin(probe_id, st);
+    dual_kernel<KIND, VEC, G, dual_unroll<G>()><<<(unsigned)grid, kBlock, 0, st>>>(f);
+    probe_end(probe_id, st);
+    NSD_TRY(check_launch("dual_kernel"));
+    for (int i = 0; i < f.npass; ++i) NSD_TRY((launch_fix<VEC, G>(f.pass[i].s, nullptr, 0.0, st)));
+    return NSD_OK;
+}
+
+template <int KIND>
+struct DualLauncher {
+    DualParams f;
+    int probe_id;
+    int64_t *grid;
+    hipStream_t st;
+    template <int VEC, int G>
+    nsd_status operator()() { return launch_dual<KIND, VEC, G>(f, probe_id, grid, st); }
+};
+
+bool dual_vec_ok(const DualParams &f) {
+    bool ok = f.pass[0].s.k % 4 == 0;
+    for (int i = 0; i < f.npass; ++i) {
+        const DualPass &m = f.pass[i];
+        ok = ok && aligned16(m.own) && aligned16(m.s.out) && (!m.s.X || aligned16(m.s.X));
+    }
+    return ok;
+}
+
+bool dual_supported(int k, bool vec) { return vec ? k <= 256 : k <= 64; }
+
+nsd_status dual_fused(int kind, DualParams f, int probe_id, int64_t *grid, hipStream_t st) {
+    const bool vec = dual_vec_ok(f);
+    const WidthPlan wp = width_plan(f.pass[0].s.k, vec);
+    if (!dual_supported(f.pass[0].s.k, vec))
+        return fail(NSD_ERR_UNSUPPORTED, "dense width k = %d on a fused pass", f.pass[0].s.k);
+    if (kind == kDualMf) {
+        DualLauncher<kDualMf> fn{f, probe_id, grid, st};
+        return dispatch_width(wp, fn);
+    }
+    DualLauncher<kDualLin> fn{f, probe_id, grid, st};
+    return dispatch_width(wp, fn);
+}
+
+}  // namespace nsd

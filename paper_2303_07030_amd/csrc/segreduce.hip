@@ -1,5 +1,5 @@
-// Segmented gather-reduce, sampled dense-dense products and the fused row
-// pass of the SpMM gradient.
+// Segmented gather-reduce, sampled dense-dense products and the row pass of
+// the SpMM gradient.
 //
 // Gather-reduce computes, for every segment s of a sorted sparse operand
 // (a row of a CSR, or a column of its CSC),
@@ -249,17 +249,14 @@ nsd_status loss_finalize(const double *part, int64_t n, double *loss, hipStream_
 
 // ------------------------------------------ fused pass of the SpMM gradient
 
-// Row pass of L = 1/2 ||A B||^2 over A's row plan, one slot per item:
-//   phase 1: C rows of the item (gather-reduce), ||C_i||^2 into the block's
-//            loss partial; a long row's chunk leaves a partial instead;
-//   phase 2: for items of whole rows, dA[p] = seed * <C_i, B_j> on the
-//            item's entries, reading back the C rows this slot just wrote.
+// Row pass of L = 1/2 ||A B||^2 over A's row plan, one slot per item: the C
+// rows of the item (gather-reduce) and ||C_i||^2 of the rows completed in it
+// into the block's loss partial; a long row's chunk leaves a partial instead.
 // Blocks past the items zero the C rows of empty rows.
 template <int VEC, int G, int U>
 __global__ __launch_bounds__(kBlock) void frob_row_kernel(FrobParams f) {
     constexpr int kSlots = kBlock / G;
     const SgrParams &a = f.rows;
-    const int lane = threadIdx.x % kWave;
     const int g = threadIdx.x % G;
     const int col = g * VEC;  // k <= G * VEC on this path
     const bool on = col < a.k;
@@ -275,47 +272,15 @@ __global__ __launch_bounds__(kBlock) void frob_row_kernel(FrobParams f) {
 #pragma unroll
                     for (int e = 0; e < VEC; ++e) lsq += (double)c.v[e] * c.v[e];
             });
-            const int64_t a0 = a.plan.item_ptr[s], b0 = a.plan.item_ptr[s + 1];
-            const bool chunk = (a0 > 0 && a.segidx[a0 - 1] == a.segidx[a0]) ||
-                               (b0 < a.nnz && a.segidx[b0] == a.segidx[b0 - 1]);
-            if (!chunk) {
-                double unused = 0.0;
-                sddmm_range<VEC, G, sddmm_unroll<G>()>(f.sdd, a0, b0, lane, unused);
-            }
         }
     }
     const double t = block_sum(lsq);
     if (threadIdx.x == 0) f.loss_part[blockIdx.x] = 0.5 * t;
 }
 
-// Column pass of the SpMM gradient: dB = seed * A^T C over the column plan,
-// and in the blocks after it the SDDMM of the long rows' chunks.
-template <int VEC, int G, int U>
-__global__ __launch_bounds__(kBlock) void frob_col_kernel(FrobParams f) {
-    constexpr int kSlots = kBlock / G;
-    const SgrParams &a = f.cols;
-    const int lane = threadIdx.x % kWave;
-    const int g = threadIdx.x % G;
-    const int col = g * VEC;
-    const bool on = col < a.k;
-    const int col_blocks = a.item_blocks + f.col_empty_blocks;
-    if ((int)blockIdx.x < a.item_blocks) {
-        const int64_t s = (int64_t)blockIdx.x * kSlots + threadIdx.x / G;
-        if (s < a.plan.nitems) sgr_walk<VEC, G, U>(a, s, col, on, NoSegDone{});
-    } else if ((int)blockIdx.x < col_blocks) {
-        zero_segment<VEC>(a, (int64_t)(blockIdx.x - a.item_blocks) * kSlots + threadIdx.x / G, col,
-                          on);
-    } else {
-        const int64_t j = (int64_t)(blockIdx.x - col_blocks) * kSlots + threadIdx.x / G;
-        if (j < f.rows.plan.nchunks) {
-            const int it = f.rows.plan.chunk_item[j];
-            double unused = 0.0;
-            sddmm_range<VEC, G, sddmm_unroll<G>()>(f.sdd, f.rows.plan.item_ptr[it],
-                                                   f.rows.plan.item_ptr[it + 1], lane, unused);
-        }
-    }
-}
-
+// C = A B with the loss (row pass, long-row combine with their ||C_i||^2),
+// then dB and dA in one linear dual pass over the columns (own row B_j,
+// gathered row C_i), then the loss total.
 template <int VEC, int G>
 static nsd_status launch_frob(FrobParams f, hipStream_t st) {
     constexpr int kSlots = kBlock / G;
@@ -327,15 +292,11 @@ static nsd_status launch_frob(FrobParams f, hipStream_t st) {
     probe_end(NSD_KERNEL_FROB_ROW, st);
     NSD_TRY(check_launch("frob_row_kernel"));
     NSD_TRY((launch_fix<VEC, G>(f.rows, f.seg_loss, 0.5, st)));
-    f.cols.item_blocks = (int32_t)ceil_div(f.cols.plan.nitems, kSlots);
-    f.col_empty_blocks = (int32_t)ceil_div(f.cols.plan.nempty, kSlots);
-    const int col_blocks = f.cols.item_blocks + f.col_empty_blocks +
-                           (int)ceil_div(f.rows.plan.nchunks, kSlots);
-    probe_begin(NSD_KERNEL_FROB_COL, st);
-    frob_col_kernel<VEC, G, U><<<col_blocks, kBlock, 0, st>>>(f);
-    probe_end(NSD_KERNEL_FROB_COL, st);
-    NSD_TRY(check_launch("frob_col_kernel"));
-    NSD_TRY((launch_fix<VEC, G>(f.cols, nullptr, 0.0, st)));
+    DualParams d;
+    d.pass[0] = f.cols;
+    d.npass = 1;
+    int64_t unused = 0;
+    NSD_TRY(dual_fused(kDualLin, d, NSD_KERNEL_FROB_COL, &unused, st));
     probe_begin(NSD_KERNEL_LOSS, st);
     loss_finalize_kernel<<<1, kBlock, 0, st>>>(f.loss_part, row_blocks, f.seg_loss,
                                                f.rows.plan.nlong, f.loss);

@@ -43,35 +43,49 @@ int choose_slot_len(int64_t nnz, int slots_per_wave);
 size_t sgr_part_bytes(const nsd_plan &plan, int k);
 nsd_status segreduce(SgrParams a, hipStream_t st);
 
-// Fused SpMM-gradient passes (L = 1/2 ||A B||^2): rows = C = A B over the
-// row plan, sdd = dA = seed <C_i, B_j>, cols = dB = seed A^T C over the
-// column plan.
-struct FrobParams {
-    SgrParams rows, cols;
-    SddmmParams sdd;
-    double *loss_part = nullptr;  // [frob_row_blocks] row-pass block partials
-    double *seg_loss = nullptr;   // [rows.plan.nlong] long-row partials
-    double *loss = nullptr;
-    int32_t col_empty_blocks = 0; // set by the launcher
-};
+// A pass over a segmented sparse operand that also uses each segment's own
+// dense row `own` (see dual.hip):
+//   d_p = <own[seg_p], X[idx_p]>,  out[seg] = alpha * sum_p c_p X[idx_p],
+// with c_p = w_p (kDualLin; then sdd[pos_p] = sdd_alpha * d_p when sdd is
+// set, and loss += w_p d_p when count_loss) or c_p = w_p - d_p (kDualMf;
+// loss += c_p^2 when count_loss).  pos_p = wperm[p] when the weights are
+// permuted, else p.
+constexpr int kDualLin = 0;
+constexpr int kDualMf = 1;
 
-// Factorisation passes: s is the gather-reduce (X = the gathered factor,
-// w = A's values in this pass's order, out = its gradient, alpha = -2 seed),
-// own = the segment's own factor.
-struct MfPass {
+struct DualPass {
     SgrParams s;
-    const float *own = nullptr;
+    const float *own = nullptr;  // [nseg x k]
+    float *sdd = nullptr;        // [nnz] sampled products at pos_p (kDualLin)
+    float sdd_alpha = 1.f;
+    int32_t count_loss = 0;
     int32_t item_blocks = 0, empty_blocks = 0;  // set by the launcher
 };
 
-struct MfParams {
-    MfPass rows, cols;
-    double *loss_part = nullptr;  // [mf_blocks] block partials (row pass only)
+struct DualParams {
+    DualPass pass[2];
+    int32_t npass = 1;
+    double *loss_part = nullptr;  // [dual_blocks] block partials (NULL: no loss)
+    double loss_beta = 1.0;       // scale of every block partial
 };
 
-int64_t mf_blocks(const nsd_plan &rows, const nsd_plan &cols, int k, bool vec);
-bool mf_vec_ok(int k, const void *U, const void *V, const void *dU, const void *dV);
-nsd_status mf_fused(MfParams f, double *loss, hipStream_t st);
+int64_t dual_blocks(const nsd_plan *const *plans, int npass, int k, bool vec);
+bool dual_vec_ok(const DualParams &f);
+bool dual_supported(int k, bool vec);
+// Launches the passes and their long-segment combines; *grid = the number of
+// loss partials written.
+nsd_status dual_fused(int kind, DualParams f, int probe_id, int64_t *grid, hipStream_t st);
+
+// Fused SpMM-gradient passes (L = 1/2 ||A B||^2): rows = C = A B over the
+// row plan with the loss; cols = a linear dual pass over the column plan
+// (own = B, X = C): dB = seed A^T C and dA = seed <C_i, B_j>.
+struct FrobParams {
+    SgrParams rows;
+    DualPass cols;
+    double *loss_part = nullptr;  // [frob_row_blocks] row-pass block partials
+    double *seg_loss = nullptr;   // [rows.plan.nlong] long-row partials
+    double *loss = nullptr;
+};
 
 // One mode pass of the CP gradient: s is the gather-reduce over the mode's
 // plan (segidx = mode coordinate, idx = coordinate of mode n+1, w = values,

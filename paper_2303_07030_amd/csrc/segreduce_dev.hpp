@@ -20,13 +20,24 @@ constexpr int kHugeChunks = 64;  // matches the plan builder
 
 template <int U>
 struct Meta {
-    int r[U], c[U];
+    int r[U], c[U], pos[U];
     float w[U];
 };
 
-// Metadata of entries [p, p + U) of an item ending at b0; entries past the
-// end become padding: same segment as the item's last entry (no flush), its
-// gathered row (a valid address) and weight 0.
+// Positions of the weights of entries [p, p + U) (wperm[q], or q); loaded
+// one batch ahead of the rest so that w[pos] never waits on them.
+template <int U>
+__device__ __forceinline__ void load_pos(const SgrParams &a, int64_t p, int64_t b0, int (&pos)[U]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int64_t q = p + u;
+        pos[u] = q < b0 ? (a.wperm ? a.wperm[q] : (int)q) : 0;
+    }
+}
+
+// Metadata of entries [p, p + U) of an item ending at b0, positions already
+// in m.pos; entries past the end become padding: same segment as the item's
+// last entry (no flush), its gathered row (a valid address) and weight 0.
 template <int U>
 __device__ __forceinline__ void load_meta(const SgrParams &a, int64_t p, int64_t b0, int last_r,
                                           int last_c, Meta<U> &m) {
@@ -36,7 +47,7 @@ __device__ __forceinline__ void load_meta(const SgrParams &a, int64_t p, int64_t
         if (q < b0) {
             m.r[u] = a.segidx[q];
             m.c[u] = a.idx[q];
-            m.w[u] = a.w ? (a.wperm ? a.w[a.wperm[q]] : a.w[q]) : 1.f;
+            m.w[u] = a.w ? a.w[m.pos[u]] : 1.f;
         } else {
             m.r[u] = last_r;
             m.c[u] = last_c;
@@ -76,9 +87,17 @@ __device__ __forceinline__ void sgr_walk(const SgrParams &a, int64_t s, int col,
     };
 
     Meta<U> cur, nxt;
+    int pnext[U];
+    load_pos(a, a0, b0, cur.pos);
     load_meta(a, a0, b0, last_r, last_c, cur);
+    load_pos(a, a0 + U, b0, pnext);
     for (int64_t p = a0; p < b0; p += U) {
-        if (p + U < b0) load_meta(a, p + U, b0, last_r, last_c, nxt);
+        if (p + U < b0) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) nxt.pos[u] = pnext[u];
+            load_meta(a, p + U, b0, last_r, last_c, nxt);
+            if (p + 2 * U < b0) load_pos(a, p + 2 * U, b0, pnext);
+        }
         Vec<VEC> xv[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {

@@ -119,3 +119,21 @@ def test_binding_fails_loudly_without_library(tmp_path):
     r = subprocess.run([sys.executable, "-c", "import paper_2303_07030_amd.nsd"], cwd=tmp_path,
                        capture_output=True, text=True)
     assert r.returncode != 0 and "libnsd.so is not built" in r.stderr
+
+
+def test_probe_accepts_every_kernel_id():
+    """Every kernel id the header declares is known to the binding and is
+    accepted by nsd_probe_set (fake handles: no kernel runs, so they are
+    never recorded), and an unknown one is refused."""
+    import re
+    from paper_2303_07030_amd import nsd
+    text = open(os.path.join(ROOT, "include", "nsd.h")).read()
+    ids = {m.group(1).lower(): int(m.group(2))
+           for m in re.finditer(r"NSD_KERNEL_(\w+)\s*=\s*(\d+)", text) if m.group(1) != "NONE"}
+    assert ids == nsd.KERNEL_IDS
+    for kid in ids.values():
+        nsd.nsd_probe_set(kid, [1], [1])
+        assert nsd.nsd_probe_count() == 0
+        nsd.nsd_probe_clear()
+    with pytest.raises(nsd.NsdError):
+        nsd.nsd_probe_set(max(ids.values()) + 1, [1], [1])
