@@ -30,6 +30,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+ITEM_LEN = None  # work-plan item length; None = the library's choice
 WORKLOAD_NAMES = {
     "spmm": "spmm_grad_100k_1M_zipf1.1_k64",
     "gnn": "gnn_bilinear_2.4M_60M_zipf1.05_k256",
@@ -47,6 +48,8 @@ def parse():
     ap.add_argument("--workload", default="spmm", choices=list(WORKLOAD_NAMES))
     ap.add_argument("--size", default="full")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--item-len", type=int, default=None,
+                    help="work-plan item length (default: the library's choice)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--profile-only", action="store_true",
                     help="warmup + steps only (for rocprofv3), no JSON line")
@@ -88,7 +91,7 @@ class Setup:
 
 def setup_spmm(d, dev, torch, nsd, ops):
     A = ops.DeviceCsr(d["nrows"], d["ncols"], d["rowptr"], d["colind"], d["val"], device=dev,
-                      k_hint=d["k"])
+                      k_hint=d["k"], item_len=ITEM_LEN)
     k, nnz, nr, nc = d["k"], A.nnz, A.nrows, A.ncols
     B = torch.from_numpy(d["B"]).to(dev)
     C = torch.empty((nr, k), dtype=torch.float32, device=dev)
@@ -111,7 +114,7 @@ def setup_spmm(d, dev, torch, nsd, ops):
 
 def setup_gnn(d, dev, torch, nsd, ops):
     A = ops.DeviceCsr(d["nrows"], d["ncols"], d["rowptr"], d["colind"], d["val"], device=dev,
-                      k_hint=d["k"])
+                      k_hint=d["k"], item_len=ITEM_LEN)
     k, nnz, nr, nc = d["k"], A.nnz, A.nrows, A.ncols
     H = torch.from_numpy(d["H"]).to(dev)
     G = torch.from_numpy(d["G"]).to(dev)
@@ -132,7 +135,7 @@ def setup_gnn(d, dev, torch, nsd, ops):
 
 def setup_mf(d, dev, torch, nsd, ops):
     A = ops.DeviceCsr.from_coo(d["nrows"], d["ncols"], d["row"], d["col"], d["val"], device=dev,
-                               k_hint=d["k"])
+                               k_hint=d["k"], item_len=ITEM_LEN)
     valT = A.values_in_csc_order()
     k, nnz, nr, nc = d["k"], A.nnz, A.nrows, A.ncols
     U = torch.from_numpy(d["U"]).to(dev)
@@ -154,7 +157,7 @@ def setup_mf(d, dev, torch, nsd, ops):
 
 def setup_cp(d, dev, torch, nsd, ops):
     X = ops.DeviceCoo3(d["dims"], d["i"], d["j"], d["k"], d["val"], device=dev,
-                       rank_hint=d["rank"])
+                       rank_hint=d["rank"], item_len=ITEM_LEN)
     R, nnz = d["rank"], X.nnz
     F = [torch.from_numpy(d[f]).to(dev) for f in ("F1", "F2", "F3")]
     dF = [torch.empty((X.dims[m], R), dtype=torch.float32, device=dev) for m in range(3)]
@@ -176,7 +179,7 @@ def setup_cp(d, dev, torch, nsd, ops):
 
 def setup_spmv(d, dev, torch, nsd, ops):
     A = ops.DeviceCsr(d["nrows"], d["ncols"], d["rowptr"], d["colind"], d["val"], device=dev,
-                      k_hint=1)
+                      k_hint=1, item_len=ITEM_LEN)
     nnz, nr, nc = A.nnz, A.nrows, A.ncols
     x = torch.from_numpy(d["x"]).to(dev)
     dx = torch.empty(nc, dtype=torch.float32, device=dev)
@@ -226,6 +229,8 @@ def collect(torch, nsd, starts, stops):
 
 def main():
     args = parse()
+    global ITEM_LEN
+    ITEM_LEN = args.item_len
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): this build measures "
               "one GPU's share; the multi-GPU layout is a design, not a runnable path",
@@ -317,7 +322,8 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f32", "data": "synthetic",
         "config": {"workload": WORKLOAD_NAMES[args.workload] if args.size == "full"
-                   else f"{args.workload}_{args.size}", "nnz": S.nnz, "k": S.k},
+                   else f"{args.workload}_{args.size}", "nnz": S.nnz, "k": S.k,
+                   "item_len": S.A.item_len},
         "roofline": roofline,
         "kernels": kernels,
         "preprocess_ms": round(prep_ms, 2), "generate_s": round(gen_s, 1),

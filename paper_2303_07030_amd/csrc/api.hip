@@ -167,9 +167,9 @@ static nsd_status col_dual_loss(const DualPass &pass, double *loss_part, double 
     f.pass[0] = pass;
     f.npass = 1;
     f.loss_part = loss_part;
-    int64_t grid = 0;
-    NSD_TRY(dual_fused(kDualLin, f, NSD_KERNEL_DUAL, &grid, st));
-    return loss_finalize(loss_part, grid, loss, st);
+    LossJob job;
+    job.loss = loss;  // sums the dual kernel's own block partials
+    return dual_fused(kDualLin, f, NSD_KERNEL_DUAL, job, st);
 }
 
 static bool col_dual_ok(const DualPass &pass) {
@@ -364,9 +364,9 @@ nsd_status nsd_loss_mf(const nsd_csr *A, const nsd_csc *At, const float *valT, c
     f.pass[1].own = V;
     f.loss_part = w.loss_part;
     hipStream_t st = as_stream(stream);
-    int64_t grid = 0;
-    NSD_TRY(dual_fused(kDualMf, f, NSD_KERNEL_MF, &grid, st));
-    return loss_finalize(w.loss_part, grid, loss, st);
+    LossJob job;
+    job.loss = loss;  // sums the dual kernel's own block partials
+    return dual_fused(kDualMf, f, NSD_KERNEL_MF, job, st);
 }
 
 static nsd_status check_coo3(const nsd_coo3 *X) {

@@ -168,7 +168,11 @@ __global__ __launch_bounds__(kBlock) void cp_kernel(CpParams f) {
 
 template <int G>
 constexpr int cp_unroll() {
-    return G >= 4 ? 4 : (G == 1 ? 4 : G);
+#ifdef NSD_CP_UNROLL
+    return reduce_unroll<G, NSD_CP_UNROLL>();
+#else
+    return reduce_unroll<G, 4>();
+#endif
 }
 
 int64_t cp_blocks(const nsd_plan *plans, int rank, bool vec) {
@@ -193,8 +197,14 @@ static nsd_status launch_cp(CpParams f, double *loss, hipStream_t st) {
     cp_kernel<VEC, G, cp_unroll<G>()><<<grid, kBlock, 0, st>>>(f);
     probe_end(NSD_KERNEL_CP, st);
     NSD_TRY(check_launch("cp_kernel"));
-    for (int i = 0; i < 3; ++i) NSD_TRY((launch_fix<VEC, G>(f.m[i].s, nullptr, 0.0, st)));
-    return loss_finalize(f.loss_part, grid, loss, st);
+    // the loss total rides on the last combine launch
+    LossJob job;
+    job.p1 = f.loss_part;
+    job.n1 = grid;
+    job.loss = loss;
+    for (int i = 0; i < 3; ++i)
+        NSD_TRY((launch_fix<VEC, G>(f.m[i].s, nullptr, 0.0, st, i == 2 ? job : LossJob{})));
+    return NSD_OK;
 }
 
 struct CpLauncher {

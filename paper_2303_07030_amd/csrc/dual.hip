@@ -219,7 +219,13 @@ __global__ __launch_bounds__(kBlock) void dual_kernel(DualParams f) {
 
 template <int G>
 constexpr int dual_unroll() {
-    return G >= 4 ? 4 : (G == 1 ? 4 : G);
+#ifdef NSD_DUAL_UNROLL
+    return reduce_unroll<G, NSD_DUAL_UNROLL>();
+#else
+    // measured on MI355X: two entries per batch up to 32-lane slots, four
+    // for full-wave slots (k > 128)
+    return reduce_unroll<G, (G >= 64 || G == 1) ? 4 : 2>();
+#endif
 }
 
 int64_t dual_blocks(const nsd_plan *const *plans, int npass, int k, bool vec) {
@@ -232,7 +238,7 @@ int64_t dual_blocks(const nsd_plan *const *plans, int npass, int k, bool vec) {
 }
 
 template <int KIND, int VEC, int G>
-static nsd_status launch_dual(DualParams f, int probe_id, int64_t *grid_out, hipStream_t st) {
+static nsd_status launch_dual(DualParams f, int probe_id, LossJob job, hipStream_t st) {
     constexpr int kSlots = kBlock / G;
     int64_t grid = 0;
     for (int i = 0; i < 2; ++i) {
@@ -245,13 +251,19 @@ static nsd_status launch_dual(DualParams f, int probe_id, int64_t *grid_out, hip
         m.empty_blocks = (int32_t)ceil_div(m.s.plan.nempty, kSlots);
         grid += m.item_blocks + m.empty_blocks;
     }
-    *grid_out = grid;
-    if (grid == 0) return NSD_OK;
-    probe_begin(probe_id, st);
-    dual_kernel<KIND, VEC, G, dual_unroll<G>()><<<(unsigned)grid, kBlock, 0, st>>>(f);
-    probe_end(probe_id, st);
-    NSD_TRY(check_launch("dual_kernel"));
-    for (int i = 0; i < f.npass; ++i) NSD_TRY((launch_fix<VEC, G>(f.pass[i].s, nullptr, 0.0, st)));
+    if (job.loss && !job.p1) {
+        job.p1 = f.loss_part;
+        job.n1 = grid;
+    }
+    if (grid > 0) {
+        probe_begin(probe_id, st);
+        dual_kernel<KIND, VEC, G, dual_unroll<G>()><<<(unsigned)grid, kBlock, 0, st>>>(f);
+        probe_end(probe_id, st);
+        NSD_TRY(check_launch("dual_kernel"));
+    }
+    for (int i = 0; i < f.npass; ++i)
+        NSD_TRY((launch_fix<VEC, G>(f.pass[i].s, nullptr, 0.0, st,
+                                    i == f.npass - 1 ? job : LossJob{})));
     return NSD_OK;
 }
 
@@ -259,10 +271,10 @@ template <int KIND>
 struct DualLauncher {
     DualParams f;
     int probe_id;
-    int64_t *grid;
+    LossJob job;
     hipStream_t st;
     template <int VEC, int G>
-    nsd_status operator()() { return launch_dual<KIND, VEC, G>(f, probe_id, grid, st); }
+    nsd_status operator()() { return launch_dual<KIND, VEC, G>(f, probe_id, job, st); }
 };
 
 bool dual_vec_ok(const DualParams &f) {
@@ -276,16 +288,16 @@ bool dual_vec_ok(const DualParams &f) {
 
 bool dual_supported(int k, bool vec) { return vec ? k <= 256 : k <= 64; }
 
-nsd_status dual_fused(int kind, DualParams f, int probe_id, int64_t *grid, hipStream_t st) {
+nsd_status dual_fused(int kind, DualParams f, int probe_id, LossJob job, hipStream_t st) {
     const bool vec = dual_vec_ok(f);
     const WidthPlan wp = width_plan(f.pass[0].s.k, vec);
     if (!dual_supported(f.pass[0].s.k, vec))
         return fail(NSD_ERR_UNSUPPORTED, "dense width k = %d on a fused pass", f.pass[0].s.k);
     if (kind == kDualMf) {
-        DualLauncher<kDualMf> fn{f, probe_id, grid, st};
+        DualLauncher<kDualMf> fn{f, probe_id, job, st};
         return dispatch_width(wp, fn);
     }
-    DualLauncher<kDualLin> fn{f, probe_id, grid, st};
+    DualLauncher<kDualLin> fn{f, probe_id, job, st};
     return dispatch_width(wp, fn);
 }
 

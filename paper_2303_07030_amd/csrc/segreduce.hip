@@ -214,30 +214,17 @@ nsd_status sddmm(SddmmParams a, hipStream_t st) {
 
 // ------------------------------------------------------------ loss total
 
-// One block: strided partial sums per thread (four independent chains so the
-// loads overlap), then a fixed tree.  Sums part1[0, n1) and part2[0, n2).
-__device__ __forceinline__ double strided_sum(const double *p, int64_t n) {
-    double s[4] = {0.0, 0.0, 0.0, 0.0};
-    int64_t i = threadIdx.x;
-    for (; i + 3 * kBlock < n; i += 4 * kBlock) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) s[j] += p[i + j * kBlock];
-    }
-    for (int j = 0; i < n; i += kBlock, ++j) s[j & 3] += p[i];
-    return (s[0] + s[1]) + (s[2] + s[3]);
-}
-
+// One block: the loss total of part1[0, n1) and part2[0, n2).
 __global__ __launch_bounds__(kBlock) void loss_finalize_kernel(const double *part1, int64_t n1,
                                                                const double *part2, int64_t n2,
                                                                double *loss) {
-    __shared__ double sh[kBlock];
-    sh[threadIdx.x] = strided_sum(part1, n1) + strided_sum(part2, n2);
-    __syncthreads();
-    for (int w = kBlock / 2; w >= 1; w >>= 1) {
-        if ((int)threadIdx.x < w) sh[threadIdx.x] += sh[threadIdx.x + w];
-        __syncthreads();
-    }
-    if (threadIdx.x == 0) *loss = sh[0];
+    LossJob job;
+    job.p1 = part1;
+    job.n1 = n1;
+    job.p2 = part2;
+    job.n2 = n2;
+    job.loss = loss;
+    loss_total_block(job);
 }
 
 nsd_status loss_finalize(const double *part, int64_t n, double *loss, hipStream_t st) {
@@ -280,7 +267,7 @@ __global__ __launch_bounds__(kBlock) void frob_row_kernel(FrobParams f) {
 
 // C = A B with the loss (row pass, long-row combine with their ||C_i||^2),
 // then dB and dA in one linear dual pass over the columns (own row B_j,
-// gathered row C_i), then the loss total.
+// gathered row C_i), its long-column combine running the loss total.
 template <int VEC, int G>
 static nsd_status launch_frob(FrobParams f, hipStream_t st) {
     constexpr int kSlots = kBlock / G;
@@ -295,13 +282,15 @@ static nsd_status launch_frob(FrobParams f, hipStream_t st) {
     DualParams d;
     d.pass[0] = f.cols;
     d.npass = 1;
-    int64_t unused = 0;
-    NSD_TRY(dual_fused(kDualLin, d, NSD_KERNEL_FROB_COL, &unused, st));
-    probe_begin(NSD_KERNEL_LOSS, st);
-    loss_finalize_kernel<<<1, kBlock, 0, st>>>(f.loss_part, row_blocks, f.seg_loss,
-                                               f.rows.plan.nlong, f.loss);
-    probe_end(NSD_KERNEL_LOSS, st);
-    return check_launch("loss_finalize_kernel");
+    // the loss total (row partials and long-row partials) rides on the
+    // column pass's last launch
+    LossJob job;
+    job.p1 = f.loss_part;
+    job.n1 = row_blocks;
+    job.p2 = f.seg_loss;
+    job.n2 = f.rows.plan.nlong;
+    job.loss = f.loss;
+    return dual_fused(kDualLin, d, NSD_KERNEL_FROB_COL, job, st);
 }
 
 int64_t frob_row_blocks(const nsd_plan &rows, int k) {

@@ -69,12 +69,23 @@ struct DualParams {
     double loss_beta = 1.0;       // scale of every block partial
 };
 
+// The loss total, run by one extra block of the last kernel of a call:
+// *loss = sum of p1[0, n1) + sum of p2[0, n2) in a fixed order.
+struct LossJob {
+    const double *p1 = nullptr;
+    int64_t n1 = 0;
+    const double *p2 = nullptr;
+    int64_t n2 = 0;
+    double *loss = nullptr;  // NULL: no job
+};
+
 int64_t dual_blocks(const nsd_plan *const *plans, int npass, int k, bool vec);
 bool dual_vec_ok(const DualParams &f);
 bool dual_supported(int k, bool vec);
-// Launches the passes and their long-segment combines; *grid = the number of
-// loss partials written.
-nsd_status dual_fused(int kind, DualParams f, int probe_id, int64_t *grid, hipStream_t st);
+// Launches the passes and their long-segment combines, the last of which
+// also runs `job` (when job.loss is set); a job without p1 sums the block
+// partials of the dual kernel itself (f.loss_part).
+nsd_status dual_fused(int kind, DualParams f, int probe_id, LossJob job, hipStream_t st);
 
 // Fused SpMM-gradient passes (L = 1/2 ||A B||^2): rows = C = A B over the
 // row plan with the loss; cols = a linear dual pass over the column plan

@@ -137,6 +137,33 @@ struct NoSegDone {
     __device__ void operator()(int, const Vec<VEC> &) const {}
 };
 
+// ------------------------------------------------------------- loss total
+
+// Strided partial sums of one thread over p[0, n) (four independent chains so
+// the loads overlap).
+__device__ __forceinline__ double strided_sum(const double *p, int64_t n) {
+    double s[4] = {0.0, 0.0, 0.0, 0.0};
+    int64_t i = threadIdx.x;
+    for (; i + 3 * kBlock < n; i += 4 * kBlock) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) s[j] += p[i + j * kBlock];
+    }
+    for (int j = 0; i < n; i += kBlock, ++j) s[j & 3] += p[i];
+    return (s[0] + s[1]) + (s[2] + s[3]);
+}
+
+// One whole block: the loss total of a job, in a fixed order.
+__device__ __forceinline__ void loss_total_block(const LossJob &job) {
+    __shared__ double sh[kBlock];
+    sh[threadIdx.x] = strided_sum(job.p1, job.n1) + strided_sum(job.p2, job.n2);
+    __syncthreads();
+    for (int w = kBlock / 2; w >= 1; w >>= 1) {
+        if ((int)threadIdx.x < w) sh[threadIdx.x] += sh[threadIdx.x + w];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) *job.loss = sh[0];
+}
+
 // ----------------------------------------------------------- long segments
 
 // out[seg] = alpha * sum of the segment's chunk partials, in chunk order per
@@ -144,9 +171,17 @@ struct NoSegDone {
 // wave_blocks give one wave to each non-huge long segment; the blocks after
 // them give a whole block to each huge segment.  When seg_loss is given,
 // beta * ||out[seg]||^2 is stored for every long segment.
+//
+// With a loss job, the grid's last block computes the call's loss total
+// instead (every partial it sums was written by earlier launches).
 template <int VEC, int G>
 __global__ __launch_bounds__(kBlock) void sgr_fix_kernel(SgrParams a, int wave_blocks,
-                                                         double *seg_loss, double beta) {
+                                                         double *seg_loss, double beta,
+                                                         LossJob job) {
+    if (job.loss && blockIdx.x == gridDim.x - 1) {
+        loss_total_block(job);
+        return;
+    }
     constexpr int RG = kWave / G;  // row groups per wave
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int q = lane / G, g = lane % G;
@@ -226,23 +261,47 @@ __global__ __launch_bounds__(kBlock) void sgr_fix_kernel(SgrParams a, int wave_b
 }
 
 
+// Entries per batch (rows in flight per lane).  The defaults can be changed
+// at build time (-DNSD_SGR_UNROLL=..., and likewise for the other kernel
+// families) for tuning.  Where a batch's dot products are reduced with
+// transpose_reduce the batch may not exceed the slot width G (G = 1 aside).
+template <int G, int U>
+constexpr int reduce_unroll() {
+    return G == 1 ? U : (U < G ? U : G);
+}
+
 template <int G>
 constexpr int sgr_unroll() {
-    return G >= 16 ? 4 : 8;
+#ifdef NSD_SGR_UNROLL
+    return NSD_SGR_UNROLL;
+#else
+    // measured on MI355X: two rows in flight per lane for 16- and 32-lane
+    // slots (more resident waves beat deeper batches), four for full-wave
+    // slots, eight for the narrow slots of small widths
+    return G >= 64 ? 4 : (G >= 16 ? 2 : 8);
+#endif
 }
 
 template <int G>
 constexpr int sddmm_unroll() {
-    return G >= 4 ? 4 : (G == 1 ? 4 : G);
+#ifdef NSD_SDDMM_UNROLL
+    return reduce_unroll<G, NSD_SDDMM_UNROLL>();
+#else
+    return reduce_unroll<G, 4>();
+#endif
 }
 
+// Combines the long segments of a pass (when it has any) and runs the loss
+// job (when given) in the same launch.
 template <int VEC, int G>
-inline nsd_status launch_fix(const SgrParams &a, double *seg_loss, double beta, hipStream_t st) {
-    if (a.plan.nlong == 0) return NSD_OK;
+inline nsd_status launch_fix(const SgrParams &a, double *seg_loss, double beta, hipStream_t st,
+                             LossJob job = LossJob{}) {
     const int wave_blocks = (int)ceil_div(a.plan.nlong, kBlockWaves);
+    const int grid = a.plan.nlong > 0 ? wave_blocks + a.plan.nhuge : 0;
+    if (grid == 0 && !job.loss) return NSD_OK;
     probe_begin(NSD_KERNEL_SGR_FIX, st);
-    sgr_fix_kernel<VEC, G><<<wave_blocks + a.plan.nhuge, kBlock, 0, st>>>(a, wave_blocks, seg_loss,
-                                                                         beta);
+    sgr_fix_kernel<VEC, G><<<grid + (job.loss ? 1 : 0), kBlock, 0, st>>>(a, wave_blocks,
+                                                                        seg_loss, beta, job);
     probe_end(NSD_KERNEL_SGR_FIX, st);
     return check_launch("sgr_fix_kernel");
 }
