@@ -30,93 +30,57 @@
 
 namespace nsd {
 
-template <int U>
-struct DualMeta {
-    int r[U], c[U], pos[U];
-    float w[U];
-};
-
-// Storage positions of entries [p, p + U): wperm[q], or q itself.  They are
-// loaded one batch before the rest of the metadata, so that the weight
-// gather w[pos] never waits on them inside a batch.
-template <int U>
-__device__ __forceinline__ void dual_pos(const SgrParams &a, int64_t p, int64_t b0, int (&pos)[U]) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-        const int64_t q = p + u;
-        pos[u] = q < b0 ? (a.wperm ? a.wperm[q] : (int)q) : 0;
-    }
-}
-
-// The rest of the metadata of entries [p, p + U), positions already in
-// m.pos; padding entries repeat the item's last segment and gathered row
-// (valid addresses) with weight 0.
-template <int U>
-__device__ __forceinline__ void dual_rest(const SgrParams &a, int64_t p, int64_t b0, int last_r,
-                                          int last_c, DualMeta<U> &m) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-        const int64_t q = p + u;
-        if (q < b0) {
-            m.r[u] = a.segidx[q];
-            m.c[u] = a.idx[q];
-            m.w[u] = a.w ? a.w[m.pos[u]] : 1.f;
-        } else {
-            m.r[u] = last_r;
-            m.c[u] = last_c;
-            m.w[u] = 0.f;
-        }
-    }
-}
-
+// State of one slot walking one work item: the open segment, its sum, and
+// the per-batch arithmetic shared by both ways of fetching entry metadata.
 template <int KIND, int VEC, int G, int U>
-__device__ __forceinline__ void dual_walk(const DualPass &m, int64_t s, int lane, double &lsum) {
-    const SgrParams &a = m.s;
-    const int g = lane % G;
-    const int col = g * VEC;  // k <= G * VEC on this path
-    const bool on = col < a.k;
-    const int64_t k = a.k;
-    const int64_t a0 = a.plan.item_ptr[s];
-    const int64_t b0 = a.plan.item_ptr[s + 1];
-    const int last_r = a.segidx[b0 - 1];
-    const int last_c = a.idx[b0 - 1];
-    int row = a.segidx[a0];
-    bool carry = a0 > 0 && a.segidx[a0 - 1] == row;
-
+struct DualSlot {
+    const DualPass &m;
+    int64_t s, k, b0;
+    int lane, g, col;
+    bool on;
+    int row;
+    bool carry;  // the open segment started before this item (a later chunk)
     Vec<VEC> acc;
-    acc.zero();
-    auto flush = [&]() {
+    double &lsum;
+
+    __device__ __forceinline__ DualSlot(const DualPass &m_, int64_t s_, int lane_, double &ls)
+        : m(m_), s(s_), k(m_.s.k), lane(lane_), g(lane_ % G), col((lane_ % G) * VEC), lsum(ls) {
+        const SgrParams &a = m.s;
+        on = col < a.k;  // k <= G * VEC on this path
+        const int64_t a0 = a.plan.item_ptr[s];
+        b0 = a.plan.item_ptr[s + 1];
+        row = a.segidx[a0];
+        carry = a0 > 0 && a.segidx[a0 - 1] == row;
+        acc.zero();
+    }
+
+    __device__ __forceinline__ void flush() {
         if (!on) return;
         if (carry) {
-            acc.store(a.part + s * k + col);
+            acc.store(m.s.part + s * k + col);
         } else {
             Vec<VEC> t = acc;
-            t.scale(a.alpha);
-            t.store(a.out + (int64_t)row * k + col);
+            t.scale(m.s.alpha);
+            t.store(m.s.out + (int64_t)row * k + col);
         }
-    };
+    }
 
-    // three-stage metadata pipeline: positions two batches ahead, the rest
-    // one batch ahead, the dense rows of the current batch
-    DualMeta<U> cur, nxt;
-    int pnext[U];
-    dual_pos(a, a0, b0, cur.pos);
-    dual_rest(a, a0, b0, last_r, last_c, cur);
-    dual_pos(a, a0 + U, b0, pnext);
-    for (int64_t p = a0; p < b0; p += U) {
-        if (p + U < b0) {
-#pragma unroll
-            for (int u = 0; u < U; ++u) nxt.pos[u] = pnext[u];
-            dual_rest(a, p + U, b0, last_r, last_c, nxt);
-            if (p + 2 * U < b0) dual_pos(a, p + 2 * U, b0, pnext);
-        }
+    // Entries [p, p + U) with metadata r, c, pos, w (padding past b0 has
+    // weight 0, the last entry's segment and gathered row).
+    // For a linear pass with G > 1, ps / ws are the position and weight of
+    // entry g / (G / U) of the batch, the one whose dot product this lane
+    // ends up holding.
+    __device__ __forceinline__ void batch(int64_t p, const int (&r)[U], const int (&c)[U],
+                                          const int (&pos)[U], const float (&w)[U], int ps,
+                                          float ws) {
+        const SgrParams &a = m.s;
         Vec<VEC> xv[U], ov[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             if (on) {
-                if (a.X) xv[u].load(a.X + (int64_t)cur.c[u] * k + col);
+                if (a.X) xv[u].load(a.X + (int64_t)c[u] * k + col);
                 else xv[u].ones();
-                ov[u].load(m.own + (int64_t)cur.r[u] * k + col);
+                ov[u].load(m.own + (int64_t)r[u] * k + col);
             } else {
                 xv[u].zero();
                 ov[u].zero();
@@ -129,14 +93,14 @@ __device__ __forceinline__ void dual_walk(const DualPass &m, int64_t s, int lane
         if constexpr (KIND == kDualMf) {
             if constexpr (G == 1) {
 #pragma unroll
-                for (int u = 0; u < U; ++u) coef[u] = p + u < b0 ? cur.w[u] - d[u] : 0.f;
+                for (int u = 0; u < U; ++u) coef[u] = p + u < b0 ? w[u] - d[u] : 0.f;
             } else {
                 const float tot = transpose_reduce<G, U>(d, lane);
                 constexpr int kRep = G / U;
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
                     const float t = __shfl(tot, u * kRep, G);
-                    coef[u] = p + u < b0 ? cur.w[u] - t : 0.f;
+                    coef[u] = p + u < b0 ? w[u] - t : 0.f;
                 }
             }
             if (m.count_loss && g == 0)
@@ -144,51 +108,52 @@ __device__ __forceinline__ void dual_walk(const DualPass &m, int64_t s, int lane
                 for (int u = 0; u < U; ++u) lsum += (double)coef[u] * coef[u];
         } else {
 #pragma unroll
-            for (int u = 0; u < U; ++u) coef[u] = cur.w[u];  // 0 on padding
+            for (int u = 0; u < U; ++u) coef[u] = w[u];  // 0 on padding
             if constexpr (G == 1) {
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
                     if (p + u < b0) {
-                        if (m.sdd) m.sdd[cur.pos[u]] = m.sdd_alpha * d[u];
-                        if (m.count_loss) lsum += (double)cur.w[u] * d[u];
+                        if (m.sdd) m.sdd[pos[u]] = m.sdd_alpha * d[u];
+                        if (m.count_loss) lsum += (double)w[u] * d[u];
                     }
                 }
             } else {
                 const float tot = transpose_reduce<G, U>(d, lane);
                 constexpr int kRep = G / U;
                 const int us = g / kRep;  // the entry whose total this lane holds
-                int pos = cur.pos[0];
-                float w = cur.w[0];
-#pragma unroll
-                for (int u = 1; u < U; ++u) {
-                    if (us == u) {
-                        pos = cur.pos[u];
-                        w = cur.w[u];
-                    }
-                }
                 if (g % kRep == 0 && p + us < b0) {
-                    if (m.sdd) m.sdd[pos] = m.sdd_alpha * tot;
-                    if (m.count_loss) lsum += (double)w * tot;
+                    if (m.sdd) m.sdd[ps] = m.sdd_alpha * tot;
+                    if (m.count_loss) lsum += (double)ws * tot;
                 }
             }
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            if (cur.r[u] != row) {
+            if (r[u] != row) {
                 flush();
-                row = cur.r[u];
+                row = r[u];
                 carry = false;
                 acc.zero();
             }
             acc.fma(coef[u], xv[u]);
         }
-        cur = nxt;
     }
-    if (b0 == a.nnz || a.segidx[b0] != row) {
-        flush();
-    } else if (on) {
-        acc.store(a.part + s * k + col);
+
+    __device__ __forceinline__ void finish() {
+        const SgrParams &a = m.s;
+        if (b0 == a.nnz || a.segidx[b0] != row) {
+            flush();
+        } else if (on) {
+            acc.store(a.part + s * k + col);  // the first chunk of a long segment
+        }
     }
+};
+
+template <int KIND, int VEC, int G, int U>
+__device__ __forceinline__ void dual_walk(const DualPass &m, int64_t s, int lane, double &lsum) {
+    DualSlot<KIND, VEC, G, U> st(m, s, lane, lsum);
+    walk_item<G, U>(m.s, m.s.plan.item_ptr[s], st.b0, st.g, st);
+    st.finish();
 }
 
 template <int KIND, int VEC, int G, int U>

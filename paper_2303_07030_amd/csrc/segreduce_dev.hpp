@@ -18,62 +18,156 @@ constexpr int kHugeChunks = 64;  // matches the plan builder
 
 // --------------------------------------------------------- entry metadata
 
-template <int U>
-struct Meta {
-    int r[U], c[U], pos[U];
-    float w[U];
-};
-
-// Positions of the weights of entries [p, p + U) (wperm[q], or q); loaded
-// one batch ahead of the rest so that w[pos] never waits on them.
-template <int U>
-__device__ __forceinline__ void load_pos(const SgrParams &a, int64_t p, int64_t b0, int (&pos)[U]) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-        const int64_t q = p + u;
-        pos[u] = q < b0 ? (a.wperm ? a.wperm[q] : (int)q) : 0;
-    }
+// The value held by lane `src` of this lane's slot of G lanes (src uniform
+// over the slot): a lane read into a scalar register for full-wave slots, a
+// cross-lane shuffle otherwise.  Every lane of the slot must be active.
+template <int G>
+__device__ __forceinline__ int slot_bcast(int v, int src) {
+    if constexpr (G == 64) return __builtin_amdgcn_readlane(v, src);
+    else return __shfl(v, src, G);
 }
 
-// Metadata of entries [p, p + U) of an item ending at b0, positions already
-// in m.pos; entries past the end become padding: same segment as the item's
-// last entry (no flush), its gathered row (a valid address) and weight 0.
-template <int U>
-__device__ __forceinline__ void load_meta(const SgrParams &a, int64_t p, int64_t b0, int last_r,
-                                          int last_c, Meta<U> &m) {
+template <int G>
+__device__ __forceinline__ float slot_bcast(float v, int src) {
+    return __int_as_float(slot_bcast<G>(__float_as_int(v), src));
+}
+
+// Feeds the entries [a0, b0) of one work item, in order, to
+//   st.batch(p, r, c, pos, w, ps, ws)
+// in batches of U entries p .. p + U - 1: segment r, gathered row c, weight
+// position pos (wperm[q], or q) and weight w (1 without weights).  Entries
+// past b0 are padding: the item's last segment and gathered row (valid
+// addresses), position 0, weight 0.  ps / ws are the position and weight of
+// entry g / (G / U) of the batch when G >= U (else those of the first).
+//
+// Slots of 8 or more lanes read the item in tiles of G entries: lane g
+// loads the metadata of entry g of a tile, one coalesced load per field,
+// and each batch takes its entries' fields from their lanes by broadcast.
+// Narrow slots load every entry's metadata in every lane.  Either way the
+// weight positions run one stage ahead of the weights they index, and the
+// rest of the metadata one stage ahead of the batch that uses it.
+template <int G, int U, class Slot>
+__device__ __forceinline__ void walk_item(const SgrParams &a, int64_t a0, int64_t b0, int g,
+                                          Slot &st) {
+    const int last_r = a.segidx[b0 - 1], last_c = a.idx[b0 - 1];
+    if constexpr (G >= 8) {
+        static_assert(G % U == 0, "a tile holds whole batches");
+        auto position = [&](int64_t t) -> int {
+            const int64_t q = t + g;
+            return q < b0 ? (a.wperm ? a.wperm[q] : (int)q) : 0;
+        };
+        auto rest = [&](int64_t t, int pos, int &r, int &c, float &w) {
+            const int64_t q = t + g;
+            r = q < b0 ? a.segidx[q] : last_r;
+            c = q < b0 ? a.idx[q] : last_c;
+            w = q < b0 ? (a.w ? a.w[pos] : 1.f) : 0.f;
+        };
+        int tr, tc, tpos, nr = 0, nc = 0, npos = 0, ppos = 0;
+        float tw, nw = 0.f;
+        tpos = position(a0);
+        rest(a0, tpos, tr, tc, tw);
+        if (a0 + G < b0) ppos = position(a0 + G);
+        for (int64_t t = a0; t < b0; t += G) {
+            if (t + G < b0) {
+                npos = ppos;
+                rest(t + G, npos, nr, nc, nw);
+                if (t + 2 * G < b0) ppos = position(t + 2 * G);
+            }
+            for (int base = 0; base < G && t + base < b0; base += U) {
+                int r[U], c[U], pos[U];
+                float w[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-        const int64_t q = p + u;
-        if (q < b0) {
-            m.r[u] = a.segidx[q];
-            m.c[u] = a.idx[q];
-            m.w[u] = a.w ? a.w[m.pos[u]] : 1.f;
-        } else {
-            m.r[u] = last_r;
-            m.c[u] = last_c;
-            m.w[u] = 0.f;
+                for (int u = 0; u < U; ++u) {
+                    r[u] = slot_bcast<G>(tr, base + u);
+                    c[u] = slot_bcast<G>(tc, base + u);
+                    pos[u] = slot_bcast<G>(tpos, base + u);
+                    w[u] = slot_bcast<G>(tw, base + u);
+                }
+                const int src = base + g / (G / U);
+                st.batch(t + base, r, c, pos, w, __shfl(tpos, src, G), __shfl(tw, src, G));
+            }
+            tr = nr;
+            tc = nc;
+            tpos = npos;
+            tw = nw;
+        }
+    } else {
+        auto positions = [&](int64_t p, int (&pos)[U]) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int64_t q = p + u;
+                pos[u] = q < b0 ? (a.wperm ? a.wperm[q] : (int)q) : 0;
+            }
+        };
+        auto rest = [&](int64_t p, const int (&pos)[U], int (&r)[U], int (&c)[U], float (&w)[U]) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int64_t q = p + u;
+                r[u] = q < b0 ? a.segidx[q] : last_r;
+                c[u] = q < b0 ? a.idx[q] : last_c;
+                w[u] = q < b0 ? (a.w ? a.w[pos[u]] : 1.f) : 0.f;
+            }
+        };
+        int r[U], c[U], pos[U], nr[U], nc[U], npos[U], ppos[U];
+        float w[U], nw[U];
+        positions(a0, pos);
+        rest(a0, pos, r, c, w);
+        positions(a0 + U, ppos);
+        for (int64_t p = a0; p < b0; p += U) {
+            if (p + U < b0) {
+#pragma unroll
+                for (int u = 0; u < U; ++u) npos[u] = ppos[u];
+                rest(p + U, npos, nr, nc, nw);
+                if (p + 2 * U < b0) positions(p + 2 * U, ppos);
+            }
+            int ps = pos[0];
+            float ws = w[0];
+            if constexpr (G > 1 && G >= U) {
+                const int us = g / (G / U);
+#pragma unroll
+                for (int u = 1; u < U; ++u) {
+                    if (us == u) {
+                        ps = pos[u];
+                        ws = w[u];
+                    }
+                }
+            }
+            st.batch(p, r, c, pos, w, ps, ws);
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                r[u] = nr[u];
+                c[u] = nc[u];
+                pos[u] = npos[u];
+                w[u] = nw[u];
+            }
         }
     }
 }
 
-// One slot's walk over item s (entries [a0, b0)).  Complete segments are
-// written as alpha * sum; a segment cut by the item's end or start goes to
-// part[s].  `seg_done(segment, unscaled sum)` is called for every segment
-// completed inside the item.
+// One slot's gather-reduce over item s (entries [a0, b0)).  Complete
+// segments are written as alpha * sum; a segment cut by the item's end or
+// start goes to part[s].  `seg_done(segment, unscaled sum)` is called for
+// every segment completed inside the item.
 template <int VEC, int G, int U, class SegDone>
-__device__ __forceinline__ void sgr_walk(const SgrParams &a, int64_t s, int col, bool on,
-                                         SegDone seg_done) {
-    const int64_t k = a.k;
-    const int64_t a0 = a.plan.item_ptr[s];
-    const int64_t b0 = a.plan.item_ptr[s + 1];
-    const int last_r = a.segidx[b0 - 1];
-    const int last_c = a.idx[b0 - 1];
-    int row = a.segidx[a0];
-    bool carry = a0 > 0 && a.segidx[a0 - 1] == row;  // a chunk after the first one
-
+struct SgrSlot {
+    const SgrParams &a;
+    int64_t s, k;
+    int col;
+    bool on;
+    int row;
+    bool carry;  // the open segment started before this item (a later chunk)
     Vec<VEC> acc;
-    acc.zero();
-    auto flush = [&]() {
+    SegDone &seg_done;
+
+    __device__ __forceinline__ SgrSlot(const SgrParams &a_, int64_t s_, int col_, bool on_,
+                                       int64_t a0, SegDone &sd)
+        : a(a_), s(s_), k(a_.k), col(col_), on(on_), seg_done(sd) {
+        row = a.segidx[a0];
+        carry = a0 > 0 && a.segidx[a0 - 1] == row;
+        acc.zero();
+    }
+
+    __device__ __forceinline__ void flush() {
         if (carry) {
             if (on) acc.store(a.part + s * k + col);
         } else {
@@ -84,43 +178,45 @@ __device__ __forceinline__ void sgr_walk(const SgrParams &a, int64_t s, int col,
                 t.store(a.out + (int64_t)row * k + col);
             }
         }
-    };
+    }
 
-    Meta<U> cur, nxt;
-    int pnext[U];
-    load_pos(a, a0, b0, cur.pos);
-    load_meta(a, a0, b0, last_r, last_c, cur);
-    load_pos(a, a0 + U, b0, pnext);
-    for (int64_t p = a0; p < b0; p += U) {
-        if (p + U < b0) {
-#pragma unroll
-            for (int u = 0; u < U; ++u) nxt.pos[u] = pnext[u];
-            load_meta(a, p + U, b0, last_r, last_c, nxt);
-            if (p + 2 * U < b0) load_pos(a, p + 2 * U, b0, pnext);
-        }
+    __device__ __forceinline__ void batch(int64_t, const int (&r)[U], const int (&c)[U],
+                                          const int (&)[U], const float (&w)[U], int, float) {
         Vec<VEC> xv[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            if (a.X && on) xv[u].load(a.X + (int64_t)cur.c[u] * k + col);
+            if (a.X && on) xv[u].load(a.X + (int64_t)c[u] * k + col);
             else xv[u].ones();
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            if (cur.r[u] != row) {
+            if (r[u] != row) {
                 flush();
-                row = cur.r[u];
+                row = r[u];
                 carry = false;
                 acc.zero();
             }
-            acc.fma(cur.w[u], xv[u]);
+            acc.fma(w[u], xv[u]);
         }
-        cur = nxt;
     }
-    if (b0 == a.nnz || a.segidx[b0] != row) {
-        flush();
-    } else if (on) {
-        acc.store(a.part + s * k + col);  // the first chunk of a long segment
+
+    __device__ __forceinline__ void finish(int64_t b0) {
+        if (b0 == a.nnz || a.segidx[b0] != row) {
+            flush();
+        } else if (on) {
+            acc.store(a.part + s * k + col);  // the first chunk of a long segment
+        }
     }
+};
+
+template <int VEC, int G, int U, class SegDone>
+__device__ __forceinline__ void sgr_walk(const SgrParams &a, int64_t s, int col, bool on,
+                                         SegDone seg_done) {
+    const int64_t a0 = a.plan.item_ptr[s];
+    const int64_t b0 = a.plan.item_ptr[s + 1];
+    SgrSlot<VEC, G, U, SegDone> st(a, s, col, on, a0, seg_done);
+    walk_item<G, U>(a, a0, b0, (int)(threadIdx.x % G), st);
+    st.finish(b0);
 }
 
 template <int VEC>
