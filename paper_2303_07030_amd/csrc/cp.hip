@@ -22,122 +22,184 @@
 
 namespace nsd {
 
-template <int U>
-struct CpMeta {
-    int r[U], ca[U], cb[U], pp[U];
-    float x[U];
-};
-
-template <int U>
-__device__ __forceinline__ void cp_meta(const CpMode &m, int64_t p, int64_t b0, int last_r,
-                                        int last_a, int last_b, bool with_perm, CpMeta<U> &t) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-        const int64_t q = p + u;
-        if (q < b0) {
-            t.r[u] = m.s.segidx[q];
-            t.ca[u] = m.s.idx[q];
-            t.cb[u] = m.idx_b[q];
-            t.x[u] = m.s.w[q];
-            t.pp[u] = with_perm ? m.perm[q] : 0;
-        } else {
-            t.r[u] = last_r;
-            t.ca[u] = last_a;
-            t.cb[u] = last_b;
-            t.x[u] = 0.f;
-            t.pp[u] = 0;
-        }
-    }
-}
-
+// State of one slot walking one work item of a mode pass.
 template <int VEC, int G, int U>
-__device__ __forceinline__ void cp_walk(const CpMode &m, int64_t s, int lane, bool first_mode,
-                                        double &lsum) {
-    const SgrParams &a = m.s;
-    const int g = lane % G;
-    const int col = g * VEC;  // rank <= G * VEC
-    const bool on = col < a.k;
-    const int64_t k = a.k;
-    const int64_t a0 = a.plan.item_ptr[s];
-    const int64_t b0 = a.plan.item_ptr[s + 1];
-    const int last_r = a.segidx[b0 - 1], last_a = a.idx[b0 - 1], last_b = m.idx_b[b0 - 1];
-    int row = a.segidx[a0];
-    bool carry = a0 > 0 && a.segidx[a0 - 1] == row;
+struct CpSlot {
+    const CpMode &m;
+    int64_t s, k, b0;
+    int lane, g, col;
+    bool on, first_mode;
+    int row;
+    bool carry;     // the open segment started before this item (a later chunk)
+    Vec<VEC> acc;   // sum of R * (fa o fb) over the open segment
+    Vec<VEC> ownv;  // own[row]: the open segment's own factor row
+    double &lsum;
 
-    Vec<VEC> acc;
-    acc.zero();
-    auto flush = [&]() {
+    __device__ __forceinline__ CpSlot(const CpMode &m_, int64_t s_, int lane_, bool fm,
+                                      double &ls)
+        : m(m_), s(s_), k(m_.s.k), lane(lane_), g(lane_ % G), col((lane_ % G) * VEC),
+          first_mode(fm), lsum(ls) {
+        const SgrParams &a = m.s;
+        on = col < a.k;  // rank <= G * VEC
+        const int64_t a0 = a.plan.item_ptr[s];
+        b0 = a.plan.item_ptr[s + 1];
+        row = a.segidx[a0];
+        carry = a0 > 0 && a.segidx[a0 - 1] == row;
+        acc.zero();
+        if (on) ownv.load(m.own + (int64_t)row * k + col);
+        else ownv.zero();
+    }
+
+    __device__ __forceinline__ void flush() {
         if (!on) return;
         if (carry) {
-            acc.store(a.part + s * k + col);
+            acc.store(m.s.part + s * k + col);
         } else {
             Vec<VEC> t = acc;
-            t.scale(a.alpha);
-            t.store(a.out + (int64_t)row * k + col);
+            t.scale(m.s.alpha);
+            t.store(m.s.out + (int64_t)row * k + col);
         }
-    };
+    }
 
-    CpMeta<U> cur, nxt;
-    cp_meta(m, a0, b0, last_r, last_a, last_b, first_mode, cur);
-    for (int64_t p = a0; p < b0; p += U) {
-        if (p + U < b0) cp_meta(m, p + U, b0, last_r, last_a, last_b, first_mode, nxt);
+    // Entries [p, p + U): segment r, coordinates ca / cb of the two other
+    // modes, value x, input position pp (padding past b0: value 0).
+    __device__ __forceinline__ void batch(int64_t p, const int (&r)[U], const int (&ca)[U],
+                                          const int (&cb)[U], const float (&x)[U],
+                                          const int (&pp)[U]) {
+        // segments are long in most tensors: the own row is reused while the
+        // whole batch stays in the open segment, else loaded per entry
+        bool same = true;
+#pragma unroll
+        for (int u = 0; u < U; ++u) same = same && r[u] == row;
         Vec<VEC> t[U], ow[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             if (on) {
                 Vec<VEC> fb;
-                t[u].load(m.fa + (int64_t)cur.ca[u] * k + col);
-                fb.load(m.fb + (int64_t)cur.cb[u] * k + col);
-                ow[u].load(m.own + (int64_t)cur.r[u] * k + col);
+                t[u].load(m.fa + (int64_t)ca[u] * k + col);
+                fb.load(m.fb + (int64_t)cb[u] * k + col);
+                if (!same) ow[u].load(m.own + (int64_t)r[u] * k + col);
 #pragma unroll
                 for (int e = 0; e < VEC; ++e) t[u].v[e] *= fb.v[e];
             } else {
                 t[u].zero();
-                ow[u].zero();
             }
         }
         float d[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) d[u] = ow[u].dot(t[u]);
+        for (int u = 0; u < U; ++u) d[u] = (same || !on) ? ownv.dot(t[u]) : ow[u].dot(t[u]);
         float res[U];
         if constexpr (G == 1) {
 #pragma unroll
-            for (int u = 0; u < U; ++u) res[u] = p + u < b0 ? cur.x[u] - d[u] : 0.f;
+            for (int u = 0; u < U; ++u) res[u] = p + u < b0 ? x[u] - d[u] : 0.f;
         } else {
             const float tot = transpose_reduce<G, U>(d, lane);
             constexpr int kRep = G / U;
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const float mv = __shfl(tot, u * kRep, G);
-                res[u] = p + u < b0 ? cur.x[u] - mv : 0.f;
+                res[u] = p + u < b0 ? x[u] - mv : 0.f;
             }
         }
         if (first_mode && g == 0) {
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 if (p + u < b0) {
-                    m.resid[cur.pp[u]] = m.seed * res[u];
+                    m.resid[pp[u]] = m.seed * res[u];
                     lsum += 0.5 * (double)res[u] * res[u];
                 }
             }
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            if (cur.r[u] != row) {
+            if (r[u] != row) {
                 flush();
-                row = cur.r[u];
+                row = r[u];
                 carry = false;
                 acc.zero();
             }
             acc.fma(res[u], t[u]);
         }
-        cur = nxt;
+        if (!same && on) ownv = ow[U - 1];  // own row of the segment now open
     }
-    if (b0 == a.nnz || a.segidx[b0] != row) {
-        flush();
-    } else if (on) {
-        acc.store(a.part + s * k + col);
+
+    __device__ __forceinline__ void finish() {
+        const SgrParams &a = m.s;
+        if (b0 == a.nnz || a.segidx[b0] != row) {
+            flush();
+        } else if (on) {
+            acc.store(a.part + s * k + col);  // the first chunk of a long segment
+        }
     }
+};
+
+// One slot's walk over item s of a mode pass.  Slots of 8 or more lanes read
+// the entries' metadata in tiles of G (lane g loads entry g of a tile, each
+// batch takes its fields by broadcast); narrow slots load them per entry.
+// The next tile's (batch's) metadata is in flight under the current one.
+template <int VEC, int G, int U>
+__device__ __forceinline__ void cp_walk(const CpMode &m, int64_t s, int lane, bool first_mode,
+                                        double &lsum) {
+    const SgrParams &a = m.s;
+    CpSlot<VEC, G, U> st(m, s, lane, first_mode, lsum);
+    const int64_t a0 = a.plan.item_ptr[s], b0 = st.b0;
+    const int last_r = a.segidx[b0 - 1], last_a = a.idx[b0 - 1], last_b = m.idx_b[b0 - 1];
+    auto fields = [&](int64_t q, int &r, int &ca, int &cb, float &x, int &pp) {
+        const bool in = q < b0;
+        r = in ? a.segidx[q] : last_r;
+        ca = in ? a.idx[q] : last_a;
+        cb = in ? m.idx_b[q] : last_b;
+        x = in ? a.w[q] : 0.f;
+        pp = (in && first_mode) ? m.perm[q] : 0;
+    };
+    if constexpr (G >= 8) {
+        static_assert(G % U == 0, "a tile holds whole batches");
+        const int g = st.g;
+        int tr, ta, tb, tp, nr = 0, na = 0, nb = 0, np = 0;
+        float tx, nx = 0.f;
+        fields(a0 + g, tr, ta, tb, tx, tp);
+        for (int64_t t = a0; t < b0; t += G) {
+            if (t + G < b0) fields(t + G + g, nr, na, nb, nx, np);
+            for (int base = 0; base < G && t + base < b0; base += U) {
+                int r[U], ca[U], cb[U], pp[U];
+                float x[U];
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    r[u] = slot_bcast<G>(tr, base + u);
+                    ca[u] = slot_bcast<G>(ta, base + u);
+                    cb[u] = slot_bcast<G>(tb, base + u);
+                    x[u] = slot_bcast<G>(tx, base + u);
+                    pp[u] = first_mode ? slot_bcast<G>(tp, base + u) : 0;
+                }
+                st.batch(t + base, r, ca, cb, x, pp);
+            }
+            tr = nr;
+            ta = na;
+            tb = nb;
+            tx = nx;
+            tp = np;
+        }
+    } else {
+        int r[U], ca[U], cb[U], pp[U], nr[U], na[U], nb[U], np[U];
+        float x[U], nx[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) fields(a0 + u, r[u], ca[u], cb[u], x[u], pp[u]);
+        for (int64_t p = a0; p < b0; p += U) {
+            if (p + U < b0)
+#pragma unroll
+                for (int u = 0; u < U; ++u) fields(p + U + u, nr[u], na[u], nb[u], nx[u], np[u]);
+            st.batch(p, r, ca, cb, x, pp);
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                r[u] = nr[u];
+                ca[u] = na[u];
+                cb[u] = nb[u];
+                x[u] = nx[u];
+                pp[u] = np[u];
+            }
+        }
+    }
+    st.finish();
 }
 
 template <int VEC, int G, int U>
@@ -171,7 +233,8 @@ constexpr int cp_unroll() {
 #ifdef NSD_CP_UNROLL
     return reduce_unroll<G, NSD_CP_UNROLL>();
 #else
-    return reduce_unroll<G, 4>();
+    // measured on MI355X (rank 32): two entries per batch beat four and eight
+    return reduce_unroll<G, (G >= 64 || G == 1) ? 4 : 2>();
 #endif
 }
 
