@@ -72,15 +72,17 @@ typedef enum nsd_dup_policy { NSD_DUP_SUM = 0, NSD_DUP_ERROR = 1 } nsd_dup_polic
 /*
  * Work plan of a sorted sparse operand (the rows of a CSR or the columns of a
  * CSC), built once per sparsity pattern by nsd_plan_build.  Entries are cut
- * into work items of about item_len entries: a segment of at most item_len
- * entries is never split (consecutive ones are packed into one item), a longer
- * segment is cut into chunks of item_len entries whose partial sums are added
- * in chunk order afterwards, and empty segments are listed for a zero fill.
+ * into work items of about item_len (L) entries: a segment of at most
+ * S = L + min(L, 32) entries is never split (consecutive ones are packed into
+ * one item, at most L + S entries), a longer segment is cut into chunks of L
+ * entries whose partial sums are added in chunk order afterwards, and empty
+ * segments are listed for a zero fill.
  * It balances power-law segment lengths without atomics.  A long segment with
  * more than 64 chunks is "huge": its chunks are combined by a whole workgroup.
  */
 typedef struct nsd_plan {
-    int32_t item_len;          /* L: entries per chunk; segments above L are long */
+    int32_t item_len;          /* L: entries per chunk; segments above
+                                  L + min(L, 32) are long */
     int32_t nitems, nlong, nhuge, nchunks, nempty;
     const int32_t *item_ptr;   /* [nitems+1] first entry of every item; [nitems] = nnz */
     const int32_t *long_seg;   /* [nlong] segment id of every long segment */

@@ -39,9 +39,16 @@ struct DualSlot {
     int lane, g, col;
     bool on;
     int row;
-    bool carry;  // the open segment started before this item (a later chunk)
+    bool carry;    // the open segment started before this item (a later chunk)
     Vec<VEC> acc;
+    Vec<VEC> ownv; // own[row] when kKeepOwn: the open segment's own dense row
     double &lsum;
+
+    // Keeping the open segment's own row pays where a slot is a whole wave
+    // (the branches on segment boundaries are then uniform); with several
+    // slots per wave they diverge, and per-entry loads (L1 hits) measured
+    // faster.
+    static constexpr bool kKeepOwn = G == 64;
 
     __device__ __forceinline__ DualSlot(const DualPass &m_, int64_t s_, int lane_, double &ls)
         : m(m_), s(s_), k(m_.s.k), lane(lane_), g(lane_ % G), col((lane_ % G) * VEC), lsum(ls) {
@@ -52,6 +59,8 @@ struct DualSlot {
         row = a.segidx[a0];
         carry = a0 > 0 && a.segidx[a0 - 1] == row;
         acc.zero();
+        if (kKeepOwn && on) ownv.load(m.own + (int64_t)row * k + col);
+        else ownv.zero();
     }
 
     __device__ __forceinline__ void flush() {
@@ -74,21 +83,48 @@ struct DualSlot {
                                           const int (&pos)[U], const float (&w)[U], int ps,
                                           float ws) {
         const SgrParams &a = m.s;
-        Vec<VEC> xv[U], ov[U];
+        Vec<VEC> xv[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             if (on) {
                 if (a.X) xv[u].load(a.X + (int64_t)c[u] * k + col);
                 else xv[u].ones();
-                ov[u].load(m.own + (int64_t)r[u] * k + col);
             } else {
                 xv[u].zero();
-                ov[u].zero();
             }
         }
         float d[U];
+        if constexpr (kKeepOwn) {
+            // the open segment's own row is kept; a batch that ends in
+            // another segment loads that one (ownn); an entry in neither (a
+            // segment that starts and ends inside the batch) loads its own
+            const bool same = r[U - 1] == row;  // segments are sorted in an item
+            Vec<VEC> ownn = ownv;
+            if (!same && on) ownn.load(m.own + (int64_t)r[U - 1] * k + col);
 #pragma unroll
-        for (int u = 0; u < U; ++u) d[u] = ov[u].dot(xv[u]);
+            for (int u = 0; u < U; ++u) {
+                if (!on) {
+                    d[u] = 0.f;
+                } else if (r[u] == row) {
+                    d[u] = ownv.dot(xv[u]);
+                } else if (r[u] == r[U - 1]) {
+                    d[u] = ownn.dot(xv[u]);
+                } else {
+                    Vec<VEC> o;
+                    o.load(m.own + (int64_t)r[u] * k + col);
+                    d[u] = o.dot(xv[u]);
+                }
+            }
+            ownv = ownn;  // own row of the last entry's segment
+        } else {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                Vec<VEC> o;
+                if (on) o.load(m.own + (int64_t)r[u] * k + col);
+                else o.zero();
+                d[u] = o.dot(xv[u]);
+            }
+        }
         float coef[U];
         if constexpr (KIND == kDualMf) {
             if constexpr (G == 1) {
@@ -172,6 +208,10 @@ __device__ __forceinline__ void dual_block(const DualPass &m, int b, double &lsu
 
 template <int KIND, int VEC, int G, int U>
 __global__ __launch_bounds__(kBlock) void dual_kernel(DualParams f) {
+    if (f.early.loss && blockIdx.x == gridDim.x - 1) {
+        loss_total_block(f.early);
+        return;
+    }
     const int first = f.pass[0].item_blocks + f.pass[0].empty_blocks;
     double lsum = 0.0;
     if ((int)blockIdx.x < first) dual_block<KIND, VEC, G, U>(f.pass[0], blockIdx.x, lsum);
@@ -220,9 +260,10 @@ static nsd_status launch_dual(DualParams f, int probe_id, LossJob job, hipStream
         job.p1 = f.loss_part;
         job.n1 = grid;
     }
-    if (grid > 0) {
+    const int64_t launch = grid + (f.early.loss ? 1 : 0);
+    if (launch > 0) {
         probe_begin(probe_id, st);
-        dual_kernel<KIND, VEC, G, dual_unroll<G>()><<<(unsigned)grid, kBlock, 0, st>>>(f);
+        dual_kernel<KIND, VEC, G, dual_unroll<G>()><<<(unsigned)launch, kBlock, 0, st>>>(f);
         probe_end(probe_id, st);
         NSD_TRY(check_launch("dual_kernel"));
     }

@@ -2,13 +2,13 @@
 //
 // A plan cuts the entries of a sorted sparse operand (the rows of a CSR or
 // the columns of a CSC) into work items of about L entries:
-//   * a short segment (1 <= length <= L) is never split; consecutive short
-//     segments are packed into one item while their merged cost (entries +
-//     one per segment) stays inside the same window of L;
-//   * a long segment (length > L) is cut into chunks of L entries, one item
+//   * a short segment (1 <= length <= S = L + min(L, 32)) is never split;
+//     consecutive short segments are packed into one item while their merged
+//     cost (entries + one per segment) starts inside the same window of L;
+//   * a long segment (length > S) is cut into chunks of L entries, one item
 //     each, whose partial sums are combined afterwards in chunk order;
 //   * empty segments get no item; they are listed for a zero fill.
-// Work per item is therefore bounded by about 2L entries whatever the length
+// Work per item is therefore bounded by L + S entries whatever the length
 // distribution, and only long segments ever need a second pass.
 //
 // Construction (all on the GPU, with device-wide scans):
@@ -32,6 +32,14 @@ namespace nsd {
 constexpr int kPlanThreads = 256;
 constexpr int kHugeChunks = 64;
 
+// A segment is long (chunked) above L + min(L, 32) entries: keeping slightly
+// longer segments whole spares the combine pass to most moderate lengths at
+// small L, while items stay near L entries at large L (measured on MI355X).
+__host__ __device__ __forceinline__ int64_t short_max(int32_t L) {
+    return (int64_t)L + (L < 32 ? L : 32);
+}
+__device__ __forceinline__ bool seg_long(int32_t len, int32_t L) { return len > short_max(L); }
+
 static int64_t plan_grid(int64_t n) { return ceil_div(n > 0 ? n : 1, kPlanThreads); }
 
 __global__ void plan_cost_kernel(int32_t nseg, const int32_t *segptr, int32_t L, int32_t *cost,
@@ -39,8 +47,9 @@ __global__ void plan_cost_kernel(int32_t nseg, const int32_t *segptr, int32_t L,
     const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (r >= nseg) return;
     const int32_t len = segptr[r + 1] - segptr[r];
-    cost[r] = len == 0 ? 0 : (len > L ? L : len + 1);
-    is_long[r] = len > L;
+    const bool lg = seg_long(len, L);
+    cost[r] = len == 0 ? 0 : (lg ? L : len + 1);
+    is_long[r] = lg;
     is_empty[r] = len == 0;
 }
 
@@ -49,7 +58,7 @@ __global__ void plan_window_kernel(int32_t nseg, const int32_t *segptr, int32_t 
     const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (r >= nseg) return;
     const int32_t len = segptr[r + 1] - segptr[r];
-    win[r] = (len >= 1 && len <= L) ? pos[r] / L : INT32_MIN;
+    win[r] = (len >= 1 && !seg_long(len, L)) ? pos[r] / L : INT32_MIN;
 }
 
 __global__ void plan_count_kernel(int32_t nseg, const int32_t *segptr, int32_t L,
@@ -58,15 +67,16 @@ __global__ void plan_count_kernel(int32_t nseg, const int32_t *segptr, int32_t L
     const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (r >= nseg) return;
     const int32_t len = segptr[r + 1] - segptr[r];
-    if (len > L) {
+    const bool lg = seg_long(len, L);
+    if (lg) {
         nitem[r] = (len + L - 1) / L;
     } else if (len >= 1) {
         nitem[r] = prev_win[r] != pos[r] / L ? 1 : 0;
     } else {
         nitem[r] = 0;
     }
-    nchunk[r] = len > L ? nitem[r] : 0;
-    is_huge[r] = len > L && nitem[r] > kHugeChunks;
+    nchunk[r] = lg ? nitem[r] : 0;
+    is_huge[r] = lg && nitem[r] > kHugeChunks;
 }
 
 struct PlanScans {
@@ -83,7 +93,7 @@ __global__ void plan_fill_kernel(int32_t nseg, int32_t nnz, const int32_t *segpt
     const int32_t *ipos = sc.ipos;
     const int32_t b = segptr[r], len = segptr[r + 1] - b;
     const int32_t first = ipos[r];
-    if (len > L) {
+    if (seg_long(len, L)) {
         for (int32_t c = 0; c < nitem[r]; ++c) {
             item_ptr[first + c] = b + c * L;
             chunk_item[sc.cpos[r] + c] = first + c;

@@ -267,7 +267,8 @@ __global__ __launch_bounds__(kBlock) void frob_row_kernel(FrobParams f) {
 
 // C = A B with the loss (row pass, long-row combine with their ||C_i||^2),
 // then dB and dA in one linear dual pass over the columns (own row B_j,
-// gathered row C_i), its long-column combine running the loss total.
+// gathered row C_i) with the loss total in one extra block, then the
+// long-column combine when there are long columns.
 template <int VEC, int G>
 static nsd_status launch_frob(FrobParams f, hipStream_t st) {
     constexpr int kSlots = kBlock / G;
@@ -282,15 +283,14 @@ static nsd_status launch_frob(FrobParams f, hipStream_t st) {
     DualParams d;
     d.pass[0] = f.cols;
     d.npass = 1;
-    // the loss total (row partials and long-row partials) rides on the
-    // column pass's last launch
-    LossJob job;
-    job.p1 = f.loss_part;
-    job.n1 = row_blocks;
-    job.p2 = f.seg_loss;
-    job.n2 = f.rows.plan.nlong;
-    job.loss = f.loss;
-    return dual_fused(kDualLin, d, NSD_KERNEL_FROB_COL, job, st);
+    // the loss total (row partials and long-row partials, complete before
+    // the column pass starts) is one extra block of the column pass
+    d.early.p1 = f.loss_part;
+    d.early.n1 = row_blocks;
+    d.early.p2 = f.seg_loss;
+    d.early.n2 = f.rows.plan.nlong;
+    d.early.loss = f.loss;
+    return dual_fused(kDualLin, d, NSD_KERNEL_FROB_COL, LossJob{}, st);
 }
 
 int64_t frob_row_blocks(const nsd_plan &rows, int k) {

@@ -43,6 +43,16 @@ int choose_slot_len(int64_t nnz, int slots_per_wave);
 size_t sgr_part_bytes(const nsd_plan &plan, int k);
 nsd_status segreduce(SgrParams a, hipStream_t st);
 
+// The loss total, run by one extra block of the last kernel of a call:
+// *loss = sum of p1[0, n1) + sum of p2[0, n2) in a fixed order.
+struct LossJob {
+    const double *p1 = nullptr;
+    int64_t n1 = 0;
+    const double *p2 = nullptr;
+    int64_t n2 = 0;
+    double *loss = nullptr;  // NULL: no job
+};
+
 // A pass over a segmented sparse operand that also uses each segment's own
 // dense row `own` (see dual.hip):
 //   d_p = <own[seg_p], X[idx_p]>,  out[seg] = alpha * sum_p c_p X[idx_p],
@@ -67,16 +77,8 @@ struct DualParams {
     int32_t npass = 1;
     double *loss_part = nullptr;  // [dual_blocks] block partials (NULL: no loss)
     double loss_beta = 1.0;       // scale of every block partial
-};
-
-// The loss total, run by one extra block of the last kernel of a call:
-// *loss = sum of p1[0, n1) + sum of p2[0, n2) in a fixed order.
-struct LossJob {
-    const double *p1 = nullptr;
-    int64_t n1 = 0;
-    const double *p2 = nullptr;
-    int64_t n2 = 0;
-    double *loss = nullptr;  // NULL: no job
+    LossJob early;                // a loss total over partials of earlier launches,
+                                  // run by one extra block (when early.loss is set)
 };
 
 int64_t dual_blocks(const nsd_plan *const *plans, int npass, int k, bool vec);

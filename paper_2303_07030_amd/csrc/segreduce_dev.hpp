@@ -305,25 +305,31 @@ __global__ __launch_bounds__(kBlock) void sgr_fix_kernel(SgrParams a, int wave_b
     for (int c0 = 0; c0 < a.k; c0 += G * VEC) {
         const int col = c0 + g * VEC;
         const bool on = col < a.k;
-        Vec<VEC> acc[2];
-        acc[0].zero();
-        acc[1].zero();
+        // four chunk partials in flight per lane, four running sums
+        Vec<VEC> acc[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[j].zero();
         if (on) {
             int64_t t = qq;
-            for (; t + nsum < n; t += 2 * nsum) {
-                Vec<VEC> x0, x1;
-                x0.load(a.part + (s0 + t) * k + col);
-                x1.load(a.part + (s0 + t + nsum) * k + col);
-                acc[0].add(x0);
-                acc[1].add(x1);
+            for (; t + 3 * nsum < n; t += 4 * nsum) {
+                Vec<VEC> x[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) x[j].load(a.part + (s0 + t + j * nsum) * k + col);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[j].add(x[j]);
             }
-            if (t < n) {
-                Vec<VEC> x;
-                x.load(a.part + (s0 + t) * k + col);
-                acc[0].add(x);
+#pragma unroll
+            for (int j = 0; j < 3; ++j) {  // at most three left
+                if (t + j * nsum < n) {
+                    Vec<VEC> x;
+                    x.load(a.part + (s0 + t + j * nsum) * k + col);
+                    acc[j].add(x);
+                }
             }
         }
         acc[0].add(acc[1]);
+        acc[2].add(acc[3]);
+        acc[0].add(acc[2]);
 #pragma unroll
         for (int m = G; m < kWave; m <<= 1)
 #pragma unroll

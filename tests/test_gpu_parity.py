@@ -200,7 +200,8 @@ def test_validate_csr(nsd, operand):
 def test_plan_invariants(nsd, L):
     # a plan is an implementation device, checked by its defining properties:
     # items tile the entries of the non-empty segments in order, never split a
-    # short segment, cut long ones into chunks of L, and list empty segments
+    # short segment (at most S = L + min(L, 32) entries), cut long ones into
+    # chunks of L, and list empty segments
     from paper_2303_07030_amd.operand import build_plan
     nrows, ncols, rowptr, colind, val = edge_pattern(5)
     lens = np.diff(rowptr)
@@ -216,7 +217,8 @@ def test_plan_invariants(nsd, L):
     assert item_ptr[0] == 0 and item_ptr[-1] == len(colind)
     assert np.all(np.diff(item_ptr) > 0)
     assert np.array_equal(empty, np.nonzero(lens == 0)[0])
-    long_rows = np.nonzero(lens > L)[0]
+    S = L + min(L, 32)
+    long_rows = np.nonzero(lens > S)[0]
     assert n_long == len(long_rows) and np.array_equal(long_seg, long_rows)
     nch_all = -(-lens[long_rows] // L)
     assert np.array_equal(huge, np.nonzero(nch_all > 64)[0])
@@ -224,7 +226,7 @@ def test_plan_invariants(nsd, L):
     assert np.array_equal(chunks, np.concatenate(
         [long_first[i] + np.arange(nch_all[i]) for i in range(n_long)]) if n_long else chunks)
     starts = set(item_ptr[:-1].tolist())
-    for r in np.nonzero((lens > 0) & (lens <= L))[0]:
+    for r in np.nonzero((lens > 0) & (lens <= S))[0]:
         # a short row lies inside one item: no item starts strictly inside it
         inner = [q for q in range(rowptr[r] + 1, rowptr[r + 1]) if q in starts]
         assert not inner
@@ -233,8 +235,8 @@ def test_plan_invariants(nsd, L):
         nch = -(-lens[r] // L)
         assert np.array_equal(item_ptr[s0:s0 + nch + 1][:-1], rowptr[r] + L * np.arange(nch))
         assert item_ptr[s0 + nch] == rowptr[r + 1]
-    # bounded work: an item of short rows holds at most 2L + 1 entries
-    assert np.diff(item_ptr).max() <= 2 * L + 1
+    # bounded work: an item of short rows holds at most L + S entries
+    assert np.diff(item_ptr).max() <= L + S
 
 
 # ---------------------------------------------------------------- primitives
