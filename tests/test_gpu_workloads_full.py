@@ -1,0 +1,203 @@
+"""Parity at the full workload sizes, in the launch configuration bench.py
+times (default work plans, the same entry points).
+
+The oracle cannot take whole passes over 20M-60M entries in test time, so:
+  * sampled outputs are compared with the oracle run on a sub-problem that
+    holds every stored entry the sampled outputs depend on (all entries of
+    the sampled rows or columns), indices compacted;
+  * the global losses of the factorisation and CP workloads are the oracle's
+    losses summed over disjoint chunks of the stored entries (the loss is a
+    sum over stored entries, so the split is exact in fp64), chunks built in
+    parallel;
+  * the bilinear layer's loss is checked through identities that hold at any
+    size: L = sum_p A_p dA_p = <H, dH> (seed 1).
+Tolerance as everywhere: |got - ref| <= 1e-4 * mag, exact zero where mag = 0.
+"""
+import concurrent.futures as cf
+
+import numpy as np
+import pytest
+import torch
+
+from helpers import TOL, assert_mag_close
+
+pytestmark = [pytest.mark.gpu, pytest.mark.timeout(600)]
+
+
+@pytest.fixture(scope="module")
+def nsd():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2303_07030_amd import nsd as m
+    return m
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def compact(idx):
+    """Unique ids and the compacted index of every element."""
+    u, inv = np.unique(idx, return_inverse=True)
+    return u, inv.astype(np.int32)
+
+
+def chunked_loss(orc, n, build_and_loss, nchunks=8):
+    """Sum of (loss, mag) of the oracle over disjoint entry chunks, one
+    single-threaded oracle per chunk, chunks in parallel threads."""
+    bounds = np.linspace(0, n, nchunks + 1).astype(np.int64)
+
+    def one(c):
+        orc.set_threads(1)  # OpenMP thread count is per calling thread
+        return build_and_loss(bounds[c], bounds[c + 1])
+
+    with cf.ThreadPoolExecutor(max_workers=nchunks) as ex:
+        parts = list(ex.map(one, range(nchunks)))
+    return sum(p[0] for p in parts), sum(p[1] for p in parts)
+
+
+# ------------------------------------------------------------ bilinear layer
+
+def test_bilinear_full_workload(nsd, orc):
+    from paper_2303_07030_amd import synth
+    from paper_2303_07030_amd.operand import DeviceCsr
+    d = synth.make("gnn")
+    n, k = d["nrows"], d["k"]
+    rowptr, colind, val, H, G = d["rowptr"], d["colind"], d["val"], d["H"], d["G"]
+    A = DeviceCsr(n, n, rowptr, colind, val, k_hint=k)
+    loss = torch.empty(1, dtype=torch.float64, device="cuda")
+    dA = torch.empty(A.nnz, dtype=torch.float32, device="cuda")
+    dH = torch.empty((n, k), dtype=torch.float32, device="cuda")
+    nsd.nsd_loss_bilinear(A.desc, A.csc, dev(H), dev(G), k, 1.0, loss, dA, dH, A.workspace(k))
+    Lg, dAg, dHg = host(loss)[0], host(dA), host(dH)
+    del A, dA, dH
+    rows = np.repeat(np.arange(n, dtype=np.int32), np.diff(rowptr))
+    rng = np.random.default_rng(5)
+
+    # dA on sampled entries (and every entry of the longest row)
+    r0 = int(np.argmax(np.diff(rowptr)))
+    P = np.concatenate([rng.choice(len(colind), 4096, replace=False),
+                        rowptr[r0] + rng.choice(rowptr[r0 + 1] - rowptr[r0], 1024, replace=False)])
+    ru, ri = compact(rows[P])
+    cu, ci = compact(colind[P])
+    D = orc.Dok((len(ru), len(cu)), (ri, ci), val[P])
+    ref, mag = orc.sddmm(D, G[ru], H[cu], k, ri, ci)
+    assert_mag_close(dAg[P], ref, mag, what="dA (sampled)")
+
+    # dH on sampled columns, the most referenced one included: every entry
+    # of those columns forms the sub-problem
+    indeg = np.bincount(colind, minlength=n)
+    J = np.unique(np.concatenate([rng.choice(n, 24, replace=False), [np.argmax(indeg)],
+                                  np.nonzero(indeg == 0)[0][:4]]))
+    sel = np.isin(colind, J)
+    ru, ri = compact(rows[sel])
+    cj = np.searchsorted(J, colind[sel]).astype(np.int32)
+    D = orc.Dok((len(ru), len(J)), (ri, cj), val[sel])
+    ref, mag = orc.spmm_t(D, G[ru], k)
+    assert_mag_close(dHg[J], ref, mag, what="dH (sampled columns)")
+
+    # loss through identities of the exact values: sum_p A_p dA_p and <H, dH>
+    a64 = val.astype(np.float64)
+    s1 = float(np.dot(a64, dAg.astype(np.float64)))
+    m1 = float(np.dot(np.abs(a64), np.abs(dAg.astype(np.float64))))
+    s2 = m2 = 0.0
+    for b in range(0, n, 200_000):
+        h, g = H[b:b + 200_000].astype(np.float64), dHg[b:b + 200_000].astype(np.float64)
+        s2 += float(np.sum(h * g))
+        m2 += float(np.sum(np.abs(h) * np.abs(g)))
+    assert abs(Lg - s1) <= TOL * m1, (Lg, s1, m1)
+    assert abs(Lg - s2) <= TOL * m2, (Lg, s2, m2)
+
+
+# ----------------------------------------------------- matrix factorisation
+
+def test_mf_full_workload(nsd, orc):
+    from paper_2303_07030_amd import synth
+    from paper_2303_07030_amd.operand import DeviceCsr
+    d = synth.make("mf")
+    nr, nc, k = d["nrows"], d["ncols"], d["k"]
+    row, col, val, U, V = d["row"], d["col"], d["val"], d["U"], d["V"]
+    A = DeviceCsr.from_coo(nr, nc, row, col, val, k_hint=k)
+    valT = A.values_in_csc_order()
+    loss = torch.empty(1, dtype=torch.float64, device="cuda")
+    dU = torch.empty((nr, k), dtype=torch.float32, device="cuda")
+    dV = torch.empty((nc, k), dtype=torch.float32, device="cuda")
+    nsd.nsd_loss_mf(A.desc, A.csc, valT, dev(U), dev(V), k, 1.0, loss, dU, dV, A.workspace(k))
+    Lg, dUg, dVg = host(loss)[0], host(dU), host(dV)
+    del A, valT, dU, dV
+    rng = np.random.default_rng(6)
+
+    # sampled rows (the two longest included) with all their entries
+    rlen = np.bincount(row, minlength=nr)
+    I = np.unique(np.concatenate([rng.choice(np.nonzero(rlen)[0], 12, replace=False),
+                                  np.argsort(rlen)[-2:], np.nonzero(rlen == 0)[0][:4]]))
+    sel = np.isin(row, I)
+    cu, ci = compact(col[sel])
+    D = orc.Dok((len(I), len(cu)), (np.searchsorted(I, row[sel]).astype(np.int32), ci), val[sel])
+    ref, mag = orc.mf_grad(D, U[I], V[cu], k, 0)
+    assert_mag_close(dUg[I], ref, mag, what="dU (sampled rows)")
+
+    clen = np.bincount(col, minlength=nc)
+    J = np.unique(np.concatenate([rng.choice(np.nonzero(clen)[0], 12, replace=False),
+                                  np.argsort(clen)[-2:], np.nonzero(clen == 0)[0][:4]]))
+    sel = np.isin(col, J)
+    ru, ri = compact(row[sel])
+    D = orc.Dok((len(ru), len(J)), (ri, np.searchsorted(J, col[sel]).astype(np.int32)), val[sel])
+    ref, mag = orc.mf_grad(D, U[ru], V[J], k, 1)
+    assert_mag_close(dVg[J], ref, mag, what="dV (sampled columns)")
+
+    # the loss over all 50M entries, as a sum of per-chunk oracle losses
+    def part(b, e):
+        ru, ri = compact(row[b:e])
+        cu, ci = compact(col[b:e])
+        D = orc.Dok((len(ru), len(cu)), (ri, ci), val[b:e])
+        return orc.mf_loss(D, U[ru], V[cu], k)
+
+    L, Lm = chunked_loss(orc, len(row), part)
+    assert_mag_close(Lg, L, Lm, what="loss")
+
+
+# --------------------------------------------------------- CP decomposition
+
+def test_cp_full_workload(nsd, orc):
+    from paper_2303_07030_amd import synth
+    from paper_2303_07030_amd.operand import DeviceCoo3
+    d = synth.make("cp")
+    dims, R = d["dims"], d["rank"]
+    i, j, l, val = d["i"], d["j"], d["k"], d["val"]
+    F = [d["F1"], d["F2"], d["F3"]]
+    X = DeviceCoo3(dims, i, j, l, val, rank_hint=R)
+    loss = torch.empty(1, dtype=torch.float64, device="cuda")
+    dX = torch.empty(X.nnz, dtype=torch.float32, device="cuda")
+    dF = [torch.empty((dims[m], R), dtype=torch.float32, device="cuda") for m in range(3)]
+    nsd.nsd_loss_cp(X.desc, *[dev(f) for f in F], R, 1.0, loss, dX, *dF, X.workspace(R))
+    Lg, dXg, dFg = host(loss)[0], host(dX), [host(t) for t in dF]
+    del X, dX, dF
+    rng = np.random.default_rng(7)
+    coords = (i, j, l)
+
+    # residual at sampled entries (in the input order)
+    P = rng.choice(len(val), 8192, replace=False)
+    D = orc.Dok(dims, (i[P], j[P], l[P]), val[P])
+    ref, mag = orc.cp_resid(D, *F, R, i[P], j[P], l[P])
+    assert_mag_close(dXg[P], ref, mag, what="residual (sampled)")
+
+    # every mode's gradient on sampled slices, with all their entries
+    for m in range(3):
+        S = np.unique(rng.choice(dims[m], 6, replace=False))
+        sel = np.isin(coords[m], S)
+        D = orc.Dok(dims, (i[sel], j[sel], l[sel]), val[sel])
+        ref, mag = orc.cp_grad(D, *F, R, m, sel=S.astype(np.int32))
+        assert_mag_close(dFg[m][S], ref, mag, what=f"dF{m + 1} (sampled slices)")
+
+    def part(b, e):
+        D = orc.Dok(dims, (i[b:e], j[b:e], l[b:e]), val[b:e])
+        return orc.cp_loss(D, *F, R)
+
+    L, Lm = chunked_loss(orc, len(val), part)
+    assert_mag_close(Lg, L, Lm, what="loss")
