@@ -232,8 +232,8 @@ def main():
     global ITEM_LEN
     ITEM_LEN = args.item_len
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): this build measures "
-              "one GPU's share; the multi-GPU layout is a design, not a runnable path",
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): the library measures "
+              "one GPU's share; a multi-GPU layout is described, not implemented",
               file=sys.stderr)
         sys.exit(2)
 
