@@ -37,6 +37,7 @@ WORKLOAD_NAMES = {
     "mf": "mf_1M_500k_50M_zipf1.1_k128",
     "cp": "cp_10k3_20M_rank32",
     "spmv": "spmv_sum_1k_10k",
+    "build": "build_coo_to_csr_csc_1M_500k_50M",
 }
 
 
@@ -197,8 +198,50 @@ def setup_spmv(d, dev, torch, nsd, ops):
     return S
 
 
+def _sort_passes(max_key):
+    """8-bit digit passes of the library's radix sort for keys < max_key."""
+    bits = max(max_key - 1, 0).bit_length()
+    return 1 if bits == 0 else (bits + 7) // 8
+
+
+def setup_build(d, dev, torch, nsd, ops):
+    """Pattern preparation of the factorisation input (50M unsorted COO
+    entries): COO -> CSR (a1), CSR -> CSC (a2) and the value permute (a3)."""
+    nr, nc = d["nrows"], d["ncols"]
+    row, col = (torch.from_numpy(d[x]).to(dev) for x in ("row", "col"))
+    val = torch.from_numpy(d["val"]).to(dev)
+    n = int(row.numel())
+
+    def i32(m):
+        return torch.empty(max(m, 1), dtype=torch.int32, device=dev)
+
+    rowptr, rowidx, colind, perm = i32(nr + 1), i32(n), i32(n), i32(n)
+    colptr, colidx, rowind, permc = i32(nc + 1), i32(n), i32(n), i32(n)
+    vout = torch.empty(n, dtype=torch.float32, device=dev)
+    valT = torch.empty(n, dtype=torch.float32, device=dev)
+    ws = torch.empty(max(nsd.nsd_build_workspace_size(n, max(nr, nc)),
+                         nsd.nsd_build_workspace_size(n, nc)), dtype=torch.uint8, device=dev)
+
+    def step():
+        m = nsd.nsd_coo_to_csr(nr, nc, n, row, col, val, nsd.NSD_DUP_ERROR, rowptr, rowidx,
+                               colind, vout, perm, ws)
+        A = nsd.csr_desc(nr, nc, rowptr, rowidx[:m], colind[:m], vout[:m])
+        nsd.nsd_csr_to_csc(A, colptr, colidx, rowind, permc, ws)
+        nsd.nsd_gather_f32(m, permc, vout, valT)
+
+    S = Setup()
+    S.A, S.nnz, S.k, S.step = None, n, 0, step
+    # scatter passes: by column (COO -> CSR), by row, by column (CSR -> CSC);
+    # each reads and writes a key and a payload (16 B per entry), except the
+    # first pass of a sort, whose payload is the entry's own index (12 B)
+    pc, pr = _sort_passes(nc), _sort_passes(nr)
+    launches = 2 * pc + pr
+    S.kernels = {"sort": (16 * n * launches - 2 * 4 * n) / launches}
+    return S
+
+
 SETUPS = {"spmm": setup_spmm, "gnn": setup_gnn, "mf": setup_mf, "cp": setup_cp,
-          "spmv": setup_spmv}
+          "spmv": setup_spmv, "build": setup_build}
 
 
 # ------------------------------------------------------------ measurement
@@ -247,7 +290,7 @@ def main():
 
     synth.VERBOSE = True  # progress lines on stderr while the inputs are drawn
     t0 = time.perf_counter()
-    d = synth.make(args.workload, args.size)
+    d = synth.make("mf" if args.workload == "build" else args.workload, args.size)
     gen_s = time.perf_counter() - t0
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -313,17 +356,19 @@ def main():
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(args, d)
 
+    build = args.workload == "build"
     out = {
-        "metric": "gradient nonzeros/sec (forward+backward)",
+        "metric": ("pattern entries/sec (COO->CSR, CSR->CSC, value permute)" if build
+                   else "gradient nonzeros/sec (forward+backward)"),
         "value": round(S.nnz / (ms_per_step * 1e-3), 1),
-        "unit": "nnz/s",
+        "unit": "entries/s" if build else "nnz/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f32", "data": "synthetic",
         "config": {"workload": WORKLOAD_NAMES[args.workload] if args.size == "full"
                    else f"{args.workload}_{args.size}", "nnz": S.nnz, "k": S.k,
-                   "item_len": S.A.item_len},
+                   "item_len": S.A.item_len if S.A is not None else None},
         "roofline": roofline,
         "kernels": kernels,
         "preprocess_ms": round(prep_ms, 2), "generate_s": round(gen_s, 1),
@@ -352,6 +397,10 @@ def _sample(args, d):
                  colind=colind.astype(np.int32), val=d["val"][:e], G=d["G"][:nr],
                  H=d["H"][cols])
         return s, f"rows 0..{nr - 1} ({e} nnz) of the workload with the {len(cols)} columns they use"
+    if w == "build":
+        e = 4_000_000
+        return dict(d, row=d["row"][:e], col=d["col"][:e], val=d["val"][:e]), \
+            f"the first {e} COO entries of the workload"
     if w == "mf":
         e = 400_000
         rows, row = np.unique(d["row"][:e], return_inverse=True)
@@ -377,7 +426,7 @@ def cpu_baseline(args, d):
         nrows, ncols = s["nrows"], s["ncols"]
         rows = np.repeat(np.arange(nrows, dtype=np.int32), np.diff(s["rowptr"]))
         nnz = len(s["colind"])
-    elif w == "mf":
+    elif w in ("mf", "build"):
         nnz = len(s["row"])
     else:
         nnz = len(s["i"])
@@ -401,6 +450,10 @@ def cpu_baseline(args, d):
             oracle.loss_bilinear(D, s["G"], s["H"], k)
             oracle.sddmm(D, s["G"], s["H"], k, rows, s["colind"])
             oracle.spmm_t(D, s["G"], k)
+        elif w == "build":
+            D = oracle.Dok((s["nrows"], s["ncols"]), (s["row"], s["col"]), s["val"])
+            _, ci, _, _ = oracle.coo_to_csr(D)
+            oracle.stable_sort_by_key(ci, s["ncols"])
         elif w == "mf":
             D = oracle.Dok((s["nrows"], s["ncols"]), (s["row"], s["col"]), s["val"])
             k = s["k"]
@@ -422,9 +475,11 @@ def cpu_baseline(args, d):
         el = time.perf_counter() - t0
         if el >= args.cpu_seconds or passes >= 1000:
             break
-    return {"value": round(nnz * passes / el, 1), "unit": "nnz/s", "cores": 1, "kind": "oracle",
-            "sample": f"{what}: {passes} pass(es) of DOK build + loss + all gradients, "
-                      f"{el:.1f} s on one thread",
+    done = ("DOK build + CSR emission + stable column sort" if w == "build"
+            else "DOK build + loss + all gradients")
+    return {"value": round(nnz * passes / el, 1), "unit": "entries/s" if w == "build" else "nnz/s",
+            "cores": 1, "kind": "oracle",
+            "sample": f"{what}: {passes} pass(es) of {done}, {el:.1f} s on one thread",
             "host_cpus_visible": len(os.sched_getaffinity(0))}
 
 

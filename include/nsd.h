@@ -181,8 +181,9 @@ typedef enum nsd_kernel_id {
     NSD_KERNEL_CP = 7,         /* CP three mode passes */
     NSD_KERNEL_LOSS = 8,       /* loss total */
     NSD_KERNEL_TTV = 9,        /* TTV entry kernels */
-    NSD_KERNEL_DUAL = 10       /* one column pass giving dA, A^T G and the loss
+    NSD_KERNEL_DUAL = 10,      /* one column pass giving dA, A^T G and the loss
                                   (bilinear and SMVM losses) */
+    NSD_KERNEL_SORT = 11       /* radix-sort scatter pass of the builders */
 } nsd_kernel_id;
 
 /*

@@ -257,8 +257,10 @@ nsd_status radix_sort_pairs(int64_t n, int32_t max_key, const int32_t *key_in,
         radix_hist_kernel<<<ntiles, kSortThreads, 0, st>>>(ksrc, n, 8 * p, ntiles, hist);
         NSD_TRY(check_launch("radix_hist_kernel"));
         NSD_TRY(scan_exclusive(hist, hist, ntiles * kBins, nullptr, scan_ws, st));
+        probe_begin(NSD_KERNEL_SORT, st);
         radix_scatter_kernel<<<ntiles, kSortThreads, 0, st>>>(ksrc, vsrc, kdst, vdst, n, 8 * p,
                                                               ntiles, hist);
+        probe_end(NSD_KERNEL_SORT, st);
         NSD_TRY(check_launch("radix_scatter_kernel"));
         ksrc = kdst;
         vsrc = vdst;

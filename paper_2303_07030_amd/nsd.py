@@ -27,7 +27,7 @@ NSD_ERR_HIP = 7
 NSD_DUP_SUM = 0
 NSD_DUP_ERROR = 1
 KERNEL_IDS = {"sgr_main": 1, "sgr_fix": 2, "sddmm": 3, "frob_row": 4, "frob_col": 5, "mf": 6,
-              "cp": 7, "loss": 8, "ttv": 9, "dual": 10}
+              "cp": 7, "loss": 8, "ttv": 9, "dual": 10, "sort": 11}
 
 
 class NsdError(RuntimeError):
