@@ -54,6 +54,7 @@ def _load():
         "orc_cp_grad": (None, [_p, _p, _p, _p, _i64, C.c_int, _i64, _p, _p, _p]),
         "orc_ttv": (_i64, [_p, _p, _p, _p, _p, _p]),
         "orc_ttv_vjp": (None, [_p, _p, _p, _i64, _p, _p, _p, _p, _p, _p, _p]),
+        "orc_batax_jacobian": (_i64, [_p, _f64, _i64, _p, _p, _p, _p]),
         "orc_set_threads": (None, [C.c_int]),
         "orc_max_threads": (C.c_int, []),
     }
@@ -283,3 +284,19 @@ def ttv_vjp(X: Dok, v, gY: Dok, qi, qj, ql):
     _load().orc_ttv_vjp(X.h, _ptr(v), gY.h, len(qi), _ptr(qi), _ptr(qj), _ptr(ql), _ptr(dX),
                         _ptr(dXm), _ptr(dv), _ptr(dvm))
     return dX, dXm, dv, dvm
+
+
+def batax_jacobian(A: Dok, beta):
+    """J = beta A^T A of the BATAX kernel as an n x n CSR (rowptr, colind,
+    val, mag), n = columns of A; keys are the pairs of stored keys sharing a
+    row of A."""
+    rowptr_a, _, _, _ = coo_to_csr(A)
+    cap = int(np.sum(np.diff(rowptr_a).astype(np.int64) ** 2))
+    n = A.dims[1]
+    rowptr = np.empty(n + 1, dtype=np.int32)
+    colind = np.empty(max(cap, 1), dtype=np.int32)
+    val, mag = np.empty(max(cap, 1)), np.empty(max(cap, 1))
+    nk = _load().orc_batax_jacobian(A.h, float(beta), cap, _ptr(rowptr), _ptr(colind), _ptr(val),
+                                    _ptr(mag))
+    assert nk <= cap
+    return rowptr, colind[:nk], val[:nk], mag[:nk]

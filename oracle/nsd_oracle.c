@@ -656,3 +656,60 @@ void orc_ttv_vjp(const orc_dok *X, const double *v, const orc_dok *gY, int64_t n
         dvmag[l] += fabs(X->val[s] * g);
     }
 }
+
+/* ---------------------------------------------------- BATAX Jacobian */
+
+/*
+ * Jacobian of the BATAX kernel f(j) = sum_{i,k} beta A(i,j) A(i,k) x(k) with
+ * respect to x (Example 5; the matrix-kernel benchmarks of Section 7):
+ *   J(j, k) = beta sum_i A(i, j) A(i, k)
+ * taken the way the differentiated, normalised program of Example 5 runs:
+ * for every stored row r of A, the outer product r x r is inserted into the
+ * result with the semi-ring += (Section 5.4, destination-passing code of
+ * Section 5.5).  A key of J exists for every pair of stored keys of A that
+ * share a row, also when the product is 0 (stored zeros keep their keys).
+ * Emitted as an n x n CSR (n = columns of A) in (row, col) order, with mag =
+ * the sum of |terms| of every value.  cap must hold the number of keys
+ * (sum over rows of length^2 suffices).  Returns the number of keys.
+ */
+int64_t orc_batax_jacobian(const orc_dok *A, double beta, int64_t cap, int32_t *rowptr,
+                           int32_t *colind, double *val, double *mag)
+{
+    int64_t m = A->dims[0], n = A->dims[1], nnz = A->n;
+    int32_t *arp = (int32_t *)malloc(sizeof(int32_t) * (m + 1));
+    int32_t *aci = (int32_t *)malloc(sizeof(int32_t) * (nnz ? nnz : 1));
+    double *av = (double *)malloc(sizeof(double) * (nnz ? nnz : 1));
+    int64_t *afirst = (int64_t *)malloc(sizeof(int64_t) * (nnz ? nnz : 1));
+    orc_coo_to_csr(A, arp, aci, av, afirst);
+    int64_t pairs = 0;
+    for (int64_t i = 0; i < m; ++i) {
+        int64_t len = arp[i + 1] - arp[i];
+        pairs += len * len;
+    }
+    int64_t dims[3] = {n, n, 1};
+    orc_dok *J = dok_new(2, dims, pairs);
+    orc_dok *Jm = dok_new(2, dims, pairs);
+    int64_t tag = 0;
+    for (int64_t i = 0; i < m; ++i)               /* every stored row r ...     */
+        for (int32_t p = arp[i]; p < arp[i + 1]; ++p)      /* ... r x r into J */
+            for (int32_t q = arp[i]; q < arp[i + 1]; ++q) {
+                int64_t key = (int64_t)aci[p] * n + aci[q];
+                double t = beta * av[p] * av[q];
+                dok_add(J, key, t, tag);
+                dok_add(Jm, key, fabs(t), tag);
+                ++tag;
+            }
+    int64_t nk = J->n;
+    if (nk <= cap) {
+        int64_t *first = (int64_t *)malloc(sizeof(int64_t) * (nk ? nk : 1));
+        orc_coo_to_csr(J, rowptr, colind, val, first);
+        for (int64_t r = 0; r < n; ++r)
+            for (int32_t p = rowptr[r]; p < rowptr[r + 1]; ++p)
+                mag[p] = dok_get(Jm, r * n + colind[p], NULL);
+        free(first);
+    }
+    orc_dok_free(J);
+    orc_dok_free(Jm);
+    free(arp); free(aci); free(av); free(afirst);
+    return nk;
+}

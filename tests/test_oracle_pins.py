@@ -389,3 +389,64 @@ def test_golden_trace_gradient(orc):
     eye = np.eye(n)
     grad, _ = orc.sddmm(M, eye, eye, n, row, col)
     assert grad.tolist() == g["expected_gradient_on_keys"]
+
+
+# ------------------------------------------------------- BATAX Jacobian
+
+def _batax_case(rng, nr=9, nc=7, nnz=24):
+    row, col, val = rand_coo(rng, nr, nc, nnz)
+    val[3] = 0.0  # a stored zero keeps its keys
+    return row, col, val
+
+
+def test_batax_jacobian_matches_autograd_and_dense(orc):
+    """J of f(x) = beta A^T (A x) by PyTorch fp64 autograd on the dense A;
+    keys = pairs of stored keys that share a row (structural, stored zeros
+    included); values = beta A^T A, 0 off the keys."""
+    rng = np.random.default_rng(21)
+    nr, nc, beta = 9, 7, 1.75
+    row, col, val = _batax_case(rng, nr, nc)
+    D = orc.Dok((nr, nc), (row, col), val)
+    rowptr, colind, jv, jm = orc.batax_jacobian(D, beta)
+    A = torch.tensor(dense_of(nr, nc, row, col, val))
+    x0 = torch.tensor(rng.standard_normal(nc))
+    Jt = torch.autograd.functional.jacobian(lambda x: beta * (A.T @ (A @ x)), x0).numpy()
+    J = np.zeros((nc, nc))
+    rows = np.repeat(np.arange(nc), np.diff(rowptr))
+    J[rows, colind] = jv
+    assert np.allclose(J, Jt, rtol=0, atol=1e-12)
+    S = dense_of(nr, nc, row, col, np.ones_like(val)) > 0
+    keys = (S.T.astype(int) @ S.astype(int)) > 0
+    got = np.zeros((nc, nc), bool)
+    got[rows, colind] = True
+    assert np.array_equal(got, keys)
+    assert np.all(jm >= np.abs(jv) - 1e-15)
+    # sorted CSR emission, symmetric result
+    for r in range(nc):
+        assert np.all(np.diff(colind[rowptr[r]:rowptr[r + 1]]) > 0)
+    assert np.allclose(J, J.T, atol=0)
+
+
+def test_batax_jacobian_matrix_free_identity(orc):
+    """J x = beta A^T (A x) with scipy products on a larger random matrix."""
+    rng = np.random.default_rng(22)
+    nr, nc, beta = 300, 200, -0.5
+    row, col, val = rand_coo(rng, nr, nc, 2500)
+    D = orc.Dok((nr, nc), (row, col), val)
+    rowptr, colind, jv, _ = orc.batax_jacobian(D, beta)
+    J = sp.csr_matrix((jv, colind, rowptr), shape=(nc, nc))
+    A = sp.csr_matrix((val.astype(np.float64), (row, col)), shape=(nr, nc))
+    x = rng.standard_normal(nc)
+    assert np.allclose(J @ x, beta * (A.T @ (A @ x)), rtol=1e-12, atol=1e-12)
+
+
+def test_batax_jacobian_row_outer_products(orc):
+    """A single stored row r gives exactly beta r r^T on r's keys."""
+    D = orc.Dok((1, 5), (np.array([0, 0, 0], np.int32), np.array([0, 2, 4], np.int32)),
+                np.array([1.0, -2.0, 3.0], np.float32))
+    rowptr, colind, jv, jm = orc.batax_jacobian(D, 2.0)
+    r = np.array([1.0, 0.0, -2.0, 0.0, 3.0])
+    J = np.zeros((5, 5))
+    J[np.repeat(np.arange(5), np.diff(rowptr)), colind] = jv
+    assert np.array_equal(J, 2.0 * np.outer(r, r))
+    assert len(colind) == 9 and np.array_equal(jm, np.abs(jv))
