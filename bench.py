@@ -38,6 +38,7 @@ WORKLOAD_NAMES = {
     "cp": "cp_10k3_20M_rank32",
     "spmv": "spmv_sum_1k_10k",
     "build": "build_coo_to_csr_csc_1M_500k_50M",
+    "batax": "batax_jacobian_100k_1M_uniform",
 }
 
 
@@ -240,8 +241,33 @@ def setup_build(d, dev, torch, nsd, ops):
     return S
 
 
+def setup_batax(d, dev, torch, nsd, ops):
+    """Jacobian of the BATAX kernel, J = beta A^T A (an output pattern that
+    is not an input's): expand the products of every row, two stable radix
+    sorts, runs, and fixed-order run sums."""
+    A = ops.DeviceCsr(d["nrows"], d["ncols"], d["rowptr"], d["colind"], d["val"], device=dev,
+                      build_csc=False)
+    ws0 = torch.empty(256, dtype=torch.uint8, device=dev)
+    P = nsd.nsd_batax_pairs(A.desc, ws0)  # depends on the pattern only
+    ws = torch.empty(nsd.nsd_batax_workspace_size(A.desc, P), dtype=torch.uint8, device=dev)
+    n = A.ncols
+    jrowptr = torch.empty(n + 1, dtype=torch.int32, device=dev)
+    jcol = torch.empty(max(P, 1), dtype=torch.int32, device=dev)
+    jval = torch.empty(max(P, 1), dtype=torch.float32, device=dev)
+    S = Setup()
+    nk = nsd.nsd_batax_jacobian(A.desc, d["beta"], P, jrowptr, jcol, jval, ws)
+    S.A, S.nnz, S.k = A, nk, 0
+    S.step = lambda: nsd.nsd_batax_jacobian(A.desc, d["beta"], P, jrowptr, jcol, jval, ws)
+    S.pairs = P
+    # scatter passes over the P products: by k, then by j (with payload)
+    p = _sort_passes(n)
+    launches = 2 * p
+    S.kernels = {"sort": (16 * P * launches - 4 * P) / launches}
+    return S
+
+
 SETUPS = {"spmm": setup_spmm, "gnn": setup_gnn, "mf": setup_mf, "cp": setup_cp,
-          "spmv": setup_spmv, "build": setup_build}
+          "spmv": setup_spmv, "build": setup_build, "batax": setup_batax}
 
 
 # ------------------------------------------------------------ measurement
@@ -357,9 +383,11 @@ def main():
         cpu = cpu_baseline(args, d)
 
     build = args.workload == "build"
+    metric = {"build": "pattern entries/sec (COO->CSR, CSR->CSC, value permute)",
+              "batax": "Jacobian nonzeros/sec (BATAX, beta A^T A)"}.get(
+                  args.workload, "gradient nonzeros/sec (forward+backward)")
     out = {
-        "metric": ("pattern entries/sec (COO->CSR, CSR->CSC, value permute)" if build
-                   else "gradient nonzeros/sec (forward+backward)"),
+        "metric": metric,
         "value": round(S.nnz / (ms_per_step * 1e-3), 1),
         "unit": "entries/s" if build else "nnz/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
@@ -397,6 +425,12 @@ def _sample(args, d):
                  colind=colind.astype(np.int32), val=d["val"][:e], G=d["G"][:nr],
                  H=d["H"][cols])
         return s, f"rows 0..{nr - 1} ({e} nnz) of the workload with the {len(cols)} columns they use"
+    if w == "batax":
+        rp = d["rowptr"]
+        nr = 12_000
+        e = int(rp[nr])
+        return dict(d, nrows=nr, rowptr=rp[: nr + 1], colind=d["colind"][:e], val=d["val"][:e]), \
+            f"rows 0..{nr - 1} ({e} entries) of the workload"
     if w == "build":
         e = 4_000_000
         return dict(d, row=d["row"][:e], col=d["col"][:e], val=d["val"][:e]), \
@@ -422,7 +456,7 @@ def cpu_baseline(args, d):
     s, what = _sample(args, d)
     w = args.workload
 
-    if w in ("spmm", "spmv", "gnn"):
+    if w in ("spmm", "spmv", "gnn", "batax"):
         nrows, ncols = s["nrows"], s["ncols"]
         rows = np.repeat(np.arange(nrows, dtype=np.int32), np.diff(s["rowptr"]))
         nnz = len(s["colind"])
@@ -450,6 +484,9 @@ def cpu_baseline(args, d):
             oracle.loss_bilinear(D, s["G"], s["H"], k)
             oracle.sddmm(D, s["G"], s["H"], k, rows, s["colind"])
             oracle.spmm_t(D, s["G"], k)
+        elif w == "batax":
+            D = oracle.Dok((nrows, ncols), (rows, s["colind"]), s["val"])
+            one_pass.nk = len(oracle.batax_jacobian(D, s["beta"])[1])
         elif w == "build":
             D = oracle.Dok((s["nrows"], s["ncols"]), (s["row"], s["col"]), s["val"])
             _, ci, _, _ = oracle.coo_to_csr(D)
@@ -475,8 +512,11 @@ def cpu_baseline(args, d):
         el = time.perf_counter() - t0
         if el >= args.cpu_seconds or passes >= 1000:
             break
-    done = ("DOK build + CSR emission + stable column sort" if w == "build"
-            else "DOK build + loss + all gradients")
+    done = {"build": "DOK build + CSR emission + stable column sort",
+            "batax": "DOK build + the Jacobian's outer products + CSR emission"}.get(
+                w, "DOK build + loss + all gradients")
+    if w == "batax":
+        nnz = one_pass.nk  # the metric counts the Jacobian's keys
     return {"value": round(nnz * passes / el, 1), "unit": "entries/s" if w == "build" else "nnz/s",
             "cores": 1, "kind": "oracle",
             "sample": f"{what}: {passes} pass(es) of {done}, {el:.1f} s on one thread",

@@ -424,6 +424,38 @@ nsd_status nsd_ttv(const nsd_ttv_plan *T, const float *x, const float *v, float 
 nsd_status nsd_ttv_vjp(const nsd_ttv_plan *T, const float *x, const float *v, const float *gy,
                        float *dx, float *dv, void *ws, size_t ws_bytes, void *stream);
 
+/* ---------------------------------------------------------------------------
+ * Jacobian of the BATAX kernel f(j) = sum_{i,k} beta A(i,j) A(i,k) x(k) with
+ * respect to x (Example 5; the matrix kernels of Section 7):
+ *     J = beta A^T A,  J(j, k) = beta sum_i A(i, j) A(i, k),
+ * an ncols x ncols sparse matrix whose pattern is not an input's: a key
+ * (j, k) for every pair of stored entries of A that share a row (the
+ * normalised program of Example 5 inserts the outer product of every row
+ * with itself).  Keys are structural: a pair whose product is 0 keeps its
+ * key.  A is a CSR (rowptr, colind, val; sorted unique columns per row; no
+ * plan or rowidx needed).
+ *
+ * Three calls:
+ *   nsd_batax_pairs          *npairs (host) = sum over rows of length^2, the
+ *                            number of products and an upper bound on the
+ *                            keys of J.  `ws`: at least 256 device bytes.
+ *                            Synchronous.
+ *   nsd_batax_workspace_size bytes of `ws` for nsd_batax_jacobian.
+ *   nsd_batax_jacobian       J as a CSR: jrowptr [ncols + 1], jcolind / jval
+ *                            [npairs capacity]; *nnz_out (host) = its keys,
+ *                            in (row, col) order.  Values are the sums of
+ *                            the products in row order of A (fixed-order
+ *                            segmented sums, reproducible).  Synchronous.
+ * Errors: NSD_ERR_TOO_LARGE when npairs >= 2^30; NSD_ERR_INVALID_ARG when
+ * npairs differs from A's (nothing is written then but workspace).
+ */
+nsd_status nsd_batax_pairs(const nsd_csr *A, int64_t *npairs, void *ws, size_t ws_bytes,
+                           void *stream);
+nsd_status nsd_batax_workspace_size(const nsd_csr *A, int64_t npairs, size_t *bytes);
+nsd_status nsd_batax_jacobian(const nsd_csr *A, float beta, int64_t npairs, int32_t *jrowptr,
+                              int32_t *jcolind, float *jval, int32_t *nnz_out, void *ws,
+                              size_t ws_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

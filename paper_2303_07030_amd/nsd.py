@@ -125,6 +125,10 @@ _SIGS = {
     "nsd_ttv_workspace_size": (C.c_int, [_TTV, C.POINTER(_SZ)]),
     "nsd_ttv": (C.c_int, [_TTV, _P, _P, _P, _P, _SZ, _P]),
     "nsd_ttv_vjp": (C.c_int, [_TTV, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "nsd_batax_pairs": (C.c_int, [_CSR, C.POINTER(C.c_int64), _P, _SZ, _P]),
+    "nsd_batax_workspace_size": (C.c_int, [_CSR, C.c_int64, C.POINTER(_SZ)]),
+    "nsd_batax_jacobian": (C.c_int, [_CSR, C.c_float, C.c_int64, _P, _P, _P, C.POINTER(_I), _P,
+                                     _SZ, _P]),
     "nsd_loss_cp": (C.c_int, [_COO3, _P, _P, _P, _I, C.c_float, _P, _P, _P, _P, _P, _P, _SZ,
                               _P]),
 }
@@ -380,3 +384,27 @@ def nsd_ttv(T: nsd_ttv_plan, x, v, y, ws, stream=None):
 def nsd_ttv_vjp(T: nsd_ttv_plan, x, v, gy, dx, dv, ws, stream=None):
     _check(_lib.nsd_ttv_vjp(C.byref(T), _p(x), _p(v), _p(gy), _p(dx), _p(dv), _p(ws), _nbytes(ws),
                             _stream(stream)), "nsd_ttv_vjp")
+
+
+# ------------------------------------------------------------ BATAX Jacobian
+
+def nsd_batax_pairs(A: nsd_csr, ws, stream=None) -> int:
+    n = C.c_int64(0)
+    _check(_lib.nsd_batax_pairs(C.byref(A), C.byref(n), _p(ws), _nbytes(ws), _stream(stream)),
+           "nsd_batax_pairs")
+    return n.value
+
+
+def nsd_batax_workspace_size(A: nsd_csr, npairs: int) -> int:
+    b = _SZ(0)
+    _check(_lib.nsd_batax_workspace_size(C.byref(A), npairs, C.byref(b)),
+           "nsd_batax_workspace_size")
+    return b.value
+
+
+def nsd_batax_jacobian(A: nsd_csr, beta, npairs, jrowptr, jcolind, jval, ws, stream=None) -> int:
+    out = _I(0)
+    _check(_lib.nsd_batax_jacobian(C.byref(A), beta, npairs, _p(jrowptr), _p(jcolind), _p(jval),
+                                   C.byref(out), _p(ws), _nbytes(ws), _stream(stream)),
+           "nsd_batax_jacobian")
+    return out.value

@@ -20,6 +20,9 @@ every workload is synthetic, at the shapes below:
         three 10,000 x 32 factors ~ N(0, 0.1^2).
   gnn   2,400,000-node power-law graph, 60M edges (out-degree Zipf profile
         s=1.05), weights U[0,1); H and G 2,400,000 x 256 ~ N(0,1).
+  batax 100,000 x 100,000 CSR, 1M entries at uniform random positions
+        (multinomial row lengths, distinct uniform columns), values N(0,1),
+        beta = 1.5 (the Jacobian beta A^T A of Example 5's kernel).
 
 Seeds: numpy PCG64 streams from SeedSequence(entropy=230307030,
 spawn_key=(workload id, replicate)); each workload spawns five child streams
@@ -49,7 +52,7 @@ VERBOSE = False  # progress lines on stderr for the multi-minute workloads
 def _say(msg):
     if VERBOSE:
         print(f"[synth {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
-WORKLOAD_IDS = {"spmv": 1, "spmm": 2, "mf": 3, "cp": 4, "gnn": 5}
+WORKLOAD_IDS = {"spmv": 1, "spmm": 2, "mf": 3, "cp": 4, "gnn": 5, "batax": 6}
 
 # Full-size workloads and smaller variants of the same recipes that the
 # oracle finishes in seconds (they still span many tiles and ragged tails).
@@ -70,6 +73,10 @@ PRESETS = {
     "gnn": {
         "full": dict(n=2_400_000, nnz=60_000_000, s=1.05, k=256),
         "small": dict(n=5000, nnz=70_000, s=1.05, k=256),
+    },
+    "batax": {
+        "full": dict(n=100_000, nnz=1_000_000, beta=1.5),
+        "small": dict(n=2000, nnz=20_000, beta=1.5),
     },
 }
 
@@ -310,8 +317,18 @@ def make_gnn(n=2_400_000, nnz=60_000_000, s=1.05, k=256, replicate=0):
                 H=_normal(g_d1, (n, k)), G=_normal(g_d2, (n, k)), k=k)
 
 
+def make_batax(n=100_000, nnz=1_000_000, beta=1.5, replicate=0):
+    """A square CSR with entries at uniform random positions (each entry's
+    row uniform, distinct uniform columns per row), values N(0,1)."""
+    g_pat, g_val, g_d1, _, _ = streams("batax", replicate)
+    lengths = g_pat.multinomial(nnz, np.full(n, 1.0 / n))
+    rowptr, colind = _rows_without_replacement(g_pat, lengths.astype(np.int64), n)
+    return dict(workload="batax", nrows=n, ncols=n, rowptr=rowptr, colind=colind,
+                val=_normal(g_val, nnz), x=_normal(g_d1, n), beta=beta)
+
+
 MAKERS = {"spmv": make_spmv, "spmm": make_spmm, "mf": make_mf, "cp": make_cp,
-          "gnn": make_gnn}
+          "gnn": make_gnn, "batax": make_batax}
 
 
 def make(workload: str, size: str = "full", replicate: int = 0, **over):

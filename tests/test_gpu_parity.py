@@ -592,3 +592,88 @@ def test_bilinear_dA_ignores_values_and_dH_ignores_H(nsd, operand):
     _, _, dH3 = run_bilinear(nsd, A, 3 * d["H"] - 1, d["G"], d["k"])
     assert np.array_equal(dA1, dA2)   # the gradient on the pattern does not read A's values
     assert np.array_equal(dH1, dH3)   # a linear loss: dH does not depend on H
+
+
+# ---------------------------------------------------------- BATAX Jacobian
+
+def run_batax(nsd, A, beta):
+    """J = beta A^T A through the C ABI: (rowptr, colind, val) on the host."""
+    ws0 = torch.empty(256, dtype=torch.uint8, device="cuda")
+    P = nsd.nsd_batax_pairs(A.desc, ws0)
+    ws = torch.empty(nsd.nsd_batax_workspace_size(A.desc, P), dtype=torch.uint8, device="cuda")
+    jrowptr = torch.full((A.ncols + 1,), -1, dtype=torch.int32, device="cuda")
+    jcol = torch.full((max(P, 1),), -1, dtype=torch.int32, device="cuda")
+    jval = torch.full((max(P, 1),), np.nan, dtype=torch.float32, device="cuda")
+    nk = nsd.nsd_batax_jacobian(A.desc, beta, P, jrowptr, jcol, jval, ws)
+    return host(jrowptr), host(jcol)[:nk], host(jval)[:nk]
+
+
+def check_batax(orc, nrows, ncols, rowptr, colind, val, beta, got):
+    D = oracle_dok(orc, nrows, ncols, rowptr, colind, val)
+    rp, ci, v, m = orc.batax_jacobian(D, beta)
+    grp, gci, gv = got
+    assert np.array_equal(grp, rp), "J row pointers"
+    assert np.array_equal(gci, ci), "J columns"
+    assert_mag_close(gv, v, m, what="J values")
+
+
+def test_batax_jacobian_edge(nsd, operand, orc):
+    # power-law rows (one of 850 entries: 722K products), empty rows, a hot
+    # column shared by half the rows, and a stored zero
+    nrows, ncols, rowptr, colind, val = edge_pattern(17)
+    val[10] = 0.0
+    A = operand(nrows, ncols, rowptr, colind, val, build_csc=False)
+    check_batax(orc, nrows, ncols, rowptr, colind, val, 0.75,
+                run_batax(nsd, A, 0.75))
+
+
+def test_batax_jacobian_small_workload(nsd, operand, orc):
+    from paper_2303_07030_amd import synth
+    d = synth.make("batax", "small")
+    A = operand(d["nrows"], d["ncols"], d["rowptr"], d["colind"], d["val"], build_csc=False)
+    got = run_batax(nsd, A, d["beta"])
+    check_batax(orc, d["nrows"], d["ncols"], d["rowptr"], d["colind"], d["val"], d["beta"], got)
+    again = run_batax(nsd, A, d["beta"])  # bitwise reproducible
+    for x, y in zip(got, again):
+        assert np.array_equal(x, y)
+
+
+@pytest.mark.parametrize("case", ["empty", "no_entries", "single", "dense_row"])
+def test_batax_jacobian_degenerate(nsd, operand, orc, case):
+    rng = np.random.default_rng(3)
+    if case == "empty":
+        nrows, ncols = 0, 0
+        rowptr, colind, val = np.zeros(1, np.int32), np.empty(0, np.int32), np.empty(0, np.float32)
+    elif case == "no_entries":
+        nrows, ncols = 5, 4
+        rowptr, colind, val = np.zeros(6, np.int32), np.empty(0, np.int32), np.empty(0, np.float32)
+    elif case == "single":
+        nrows, ncols = 3, 5
+        rowptr = np.array([0, 0, 1, 1], np.int32)
+        colind, val = np.array([4], np.int32), np.array([-2.5], np.float32)
+    else:
+        nrows, ncols = 4, 300
+        lengths = np.array([0, 300, 3, 0])
+        rowptr, colind, val = make_csr(rng, nrows, ncols, lengths)
+    A = operand(nrows, ncols, rowptr, colind, val, build_csc=False)
+    got = run_batax(nsd, A, 2.0)
+    if nrows == 0:
+        assert np.array_equal(got[0], np.zeros(1, np.int32)) and len(got[1]) == 0
+        return
+    check_batax(orc, nrows, ncols, rowptr, colind, val, 2.0, got)
+
+
+def test_batax_jacobian_rejects_wrong_pair_count(nsd, operand):
+    nrows, ncols, rowptr, colind, val = edge_pattern(18)
+    A = operand(nrows, ncols, rowptr, colind, val, build_csc=False)
+    ws0 = torch.empty(256, dtype=torch.uint8, device="cuda")
+    P = nsd.nsd_batax_pairs(A.desc, ws0)
+    assert P == int(np.sum(np.diff(rowptr).astype(np.int64) ** 2))
+    ws = torch.empty(nsd.nsd_batax_workspace_size(A.desc, P + 1), dtype=torch.uint8,
+                     device="cuda")
+    jr = torch.empty(ncols + 1, dtype=torch.int32, device="cuda")
+    jc = torch.empty(P + 1, dtype=torch.int32, device="cuda")
+    jv = torch.empty(P + 1, dtype=torch.float32, device="cuda")
+    with pytest.raises(nsd.NsdError) as e:
+        nsd.nsd_batax_jacobian(A.desc, 1.0, P + 1, jr, jc, jv, ws)
+    assert e.value.status == nsd.NSD_ERR_INVALID_ARG
