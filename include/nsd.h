@@ -444,8 +444,9 @@ nsd_status nsd_ttv_vjp(const nsd_ttv_plan *T, const float *x, const float *v, co
  *   nsd_batax_jacobian       J as a CSR: jrowptr [ncols + 1], jcolind / jval
  *                            [npairs capacity]; *nnz_out (host) = its keys,
  *                            in (row, col) order.  Values are the sums of
- *                            the products in row order of A (fixed-order
- *                            segmented sums, reproducible).  Synchronous.
+ *                            the products in row order of A, accumulated in
+ *                            fp64 and rounded once (reproducible).
+ *                            Synchronous.
  * Errors: NSD_ERR_TOO_LARGE when npairs >= 2^30; NSD_ERR_INVALID_ARG when
  * npairs differs from A's (nothing is written then but workspace).
  */

@@ -12,20 +12,21 @@
 //      so a run of equal (j, k) keeps its terms in row order;
 //   3. runs become the keys of J (run heads, a scan); J's row pointers come
 //      from the runs' j, its columns from their k;
-//   4. the values are the run sums, a segmented reduction over the runs with
-//      the library's work plan (fixed order, long runs chunked): no float
-//      atomics, bitwise reproducible.
+//   4. the values are the run sums, one thread per run adding its terms in
+//      row order in fp64 and rounding once: no float atomics, bitwise
+//      reproducible.  (A run is as long as the number of rows two columns
+//      share, at most a column's length; a pathologically dense column makes
+//      its diagonal run a serial tail, which the fixed order accepts.)
 // Keys are structural: a pair whose product is 0 keeps its key, as the
 // dictionary insert of the paper's program does.
 #include <algorithm>
 
 #include "nsd_internal.hpp"
-#include "segreduce.hpp"
 
 namespace nsd {
 
 constexpr int kBataxThreads = 256;
-constexpr int64_t kBataxMaxPairs = 1LL << 30;  // positions and plan costs stay in int32
+constexpr int64_t kBataxMaxPairs = 1LL << 30;  // positions stay in int32
 
 static int64_t bgrid(int64_t n) { return ceil_div(n > 0 ? n : 1, kBataxThreads); }
 
@@ -98,15 +99,24 @@ __global__ void runs_kernel(int64_t n, const int32_t *head, const int32_t *pos,
     }
 }
 
+// jval[r] = sum of the terms of run r (sorted positions runptr[r] ..
+// runptr[r+1], terms reached through perm), in order, in fp64.
+__global__ void run_sums_kernel(int32_t nruns, const int32_t *runptr, const int32_t *perm,
+                                const float *term, float *jval) {
+    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= nruns) return;
+    double s = 0.0;
+    for (int32_t t = runptr[r]; t < runptr[r + 1]; ++t) s += (double)term[perm[t]];
+    jval[r] = (float)s;
+}
+
 // Workspace layout shared by the size query and the call.
 struct BataxWs {
     int32_t *sq, *off, *tot;
     int32_t *key_j, *key_k, *kperm, *jg, *js, *perm2, *ks, *head, *pos, *run, *runptr, *run_j;
     float *term;
-    int32_t *item_ptr, *long_seg, *long_first, *huge_idx, *chunk_item, *empty_seg;
-    float *part;
-    void *sort_ws, *scan_ws, *plan_ws;
-    size_t sort_bytes, scan_bytes, plan_bytes;
+    void *sort_ws, *scan_ws;
+    size_t sort_bytes, scan_bytes;
 };
 
 static nsd_status batax_carve(void *ws, int32_t nrows, int32_t n, int64_t P, BataxWs *w,
@@ -129,27 +139,11 @@ static nsd_status batax_carve(void *ws, int32_t nrows, int32_t n, int64_t P, Bat
     w->run = c.take<int32_t>(Q);
     w->runptr = c.take<int32_t>(Q + 1);
     w->run_j = c.take<int32_t>(Q);
-    // a plan over at most P runs of P terms in all, bounded for the shortest
-    // item length (16) so that any longer one fits
-    const int32_t L = 16;
-    int32_t max_items = 0, max_long = 0, max_chunks = 0;
-    size_t plan_ws = 0;
-    NSD_TRY(nsd_plan_bounds((int32_t)Q, (int32_t)Q, L, &max_items, &max_long, &max_chunks,
-                            &plan_ws));
-    w->item_ptr = c.take<int32_t>((int64_t)max_items + 1);
-    w->long_seg = c.take<int32_t>(max_long);
-    w->long_first = c.take<int32_t>(max_long);
-    w->huge_idx = c.take<int32_t>(max_long);
-    w->chunk_item = c.take<int32_t>(max_chunks);
-    w->empty_seg = c.take<int32_t>(Q);
-    w->part = c.take<float>((int64_t)max_items + 1);
     w->sort_bytes = sort_ws_bytes(Q, std::max(n, 1));
     w->scan_bytes = scan_ws_bytes(std::max<int64_t>(Q, nrows));
-    w->plan_bytes = plan_ws;
-    // the sort, scan and plan scratch are used one after another
-    const size_t scratch = std::max(std::max(w->sort_bytes, w->scan_bytes), w->plan_bytes);
-    char *s = c.take<char>((int64_t)scratch);
-    w->sort_ws = w->scan_ws = w->plan_ws = s;
+    // the sort and scan scratch are used one after another
+    char *s = c.take<char>((int64_t)std::max(w->sort_bytes, w->scan_bytes));
+    w->sort_ws = w->scan_ws = s;
     *total = c.bytes();
     return NSD_OK;
 }
@@ -257,29 +251,9 @@ nsd_status nsd_batax_jacobian(const nsd_csr *A, float beta, int64_t npairs, int3
     NSD_HIP(hipStreamSynchronize(st));
     NSD_TRY(segptr_from_sorted(P, nk, w.run, w.runptr, st));
     NSD_TRY(segptr_from_sorted(nk, n, w.run_j, jrowptr, st));
-    // 4. run sums over a plan of the runs (terms reached through perm2)
-    nsd_plan plan;
-    int32_t L = 16;
-    NSD_TRY(nsd_plan_item_len((int32_t)P, 1, &L));
-    L = std::max(L, 16);
-    NSD_TRY(nsd_plan_build(nk, (int32_t)P, w.runptr, L, w.item_ptr, w.long_seg, w.long_first,
-                           w.huge_idx, w.chunk_item, w.empty_seg, &plan, w.plan_ws,
-                           w.plan_bytes, st));
-    SgrParams sp;
-    sp.nseg = nk;
-    sp.nnz = (int32_t)P;
-    sp.k = 1;
-    sp.plan = plan;
-    sp.segptr = w.runptr;
-    sp.segidx = w.run;
-    sp.idx = w.run;  // no dense operand is gathered (X = NULL: ones)
-    sp.w = w.term;
-    sp.wperm = w.perm2;
-    sp.X = nullptr;
-    sp.alpha = 1.f;
-    sp.out = jval;
-    sp.part = w.part;
-    NSD_TRY(segreduce(sp, st));
+    // 4. run sums (terms reached through perm2)
+    run_sums_kernel<<<bgrid(nk), kBataxThreads, 0, st>>>(nk, w.runptr, w.perm2, w.term, jval);
+    NSD_TRY(check_launch("run_sums_kernel"));
     NSD_HIP(hipStreamSynchronize(st));
     *nnz_out = nk;
     return NSD_OK;

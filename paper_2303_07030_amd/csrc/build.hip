@@ -92,6 +92,41 @@ __global__ __launch_bounds__(kScanThreads) void scan_tile_kernel(const int32_t *
         *total_dev = Op::apply(pre, total);
 }
 
+// A tile scan whose block first forms its own prefix from the tile sums of
+// the blocks before it (at most kScanTile of them): one level and one launch
+// fewer than scanning the sums separately.
+template <class Op>
+__global__ __launch_bounds__(kScanThreads) void scan_tile_prefix_kernel(const int32_t *in,
+                                                                        int32_t *out, int64_t n,
+                                                                        const int32_t *sums,
+                                                                        int32_t *total_dev) {
+    int s = Op::kIdentity;
+#pragma unroll
+    for (int i = 0; i < kScanItems; ++i) {
+        const int j = threadIdx.x * kScanItems + i;  // tiles before this block, in order
+        if (j < (int)blockIdx.x) s = Op::apply(s, sums[j]);
+    }
+    int pre;
+    block_exclusive_scan<Op>(s, &pre);  // pre = the sum over all of them
+    const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
+    int v[kScanItems];
+    int t = Op::kIdentity;
+#pragma unroll
+    for (int i = 0; i < kScanItems; ++i) {
+        v[i] = base + i < n ? in[base + i] : Op::kIdentity;
+        t = Op::apply(t, v[i]);
+    }
+    int total;
+    int run = Op::apply(pre, block_exclusive_scan<Op>(t, &total));
+#pragma unroll
+    for (int i = 0; i < kScanItems; ++i) {
+        if (base + i < n) out[base + i] = run;
+        run = Op::apply(run, v[i]);
+    }
+    if (total_dev && blockIdx.x == gridDim.x - 1 && threadIdx.x == 0)
+        *total_dev = Op::apply(pre, total);
+}
+
 size_t scan_ws_bytes(int64_t n) {
     Carver c(nullptr);
     int64_t m = ceil_div(n, kScanTile);
@@ -113,6 +148,10 @@ static nsd_status scan_level(const int32_t *in, int32_t *out, int64_t n, int32_t
     int32_t *sums = c.take<int32_t>(tiles);
     scan_reduce_kernel<Op><<<tiles, kScanThreads, 0, st>>>(in, n, sums);
     NSD_TRY(check_launch("scan_reduce_kernel"));
+    if (tiles <= kScanTile) {
+        scan_tile_prefix_kernel<Op><<<tiles, kScanThreads, 0, st>>>(in, out, n, sums, total_dev);
+        return check_launch("scan_tile_prefix_kernel");
+    }
     NSD_TRY(scan_level<Op>(sums, sums, tiles, nullptr, c, st));
     scan_tile_kernel<Op><<<tiles, kScanThreads, 0, st>>>(in, out, n, sums, total_dev);
     return check_launch("scan_tile_kernel");
