@@ -61,11 +61,23 @@ def parse():
     return ap.parse_args()
 
 
-def source_digest():
+# The source file that holds each probed kernel; a kernel's digest covers
+# that file, every shared header and the public header.
+KERNEL_SOURCE = {"frob_row": "segreduce.hip", "sgr_main": "segreduce.hip",
+                 "sddmm": "segreduce.hip", "frob_col": "dual.hip", "dual": "dual.hip",
+                 "mf": "dual.hip", "cp": "cp.hip", "sort": "build.hip"}
+
+
+def source_digest(kernel=None):
+    """Digest of the sources a kernel is built from (all sources if None)."""
     h = hashlib.sha256()
     d = os.path.join(ROOT, "paper_2303_07030_amd", "csrc")
-    for f in sorted(os.listdir(d)):
-        with open(os.path.join(d, f), "rb") as fh:
+    files = sorted(os.listdir(d))
+    if kernel is not None:
+        files = [f for f in files if f.endswith(".hpp") or f == KERNEL_SOURCE[kernel]]
+    paths = [os.path.join(d, f) for f in files] + [os.path.join(ROOT, "include", "nsd.h")]
+    for path in paths:
+        with open(path, "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
@@ -79,7 +91,7 @@ def committed_traffic(kernel, workload):
     text = open(path).read()
     m = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
     s = re.search(r"source_digest:\s*([0-9a-f]+)", text)
-    if not m or not s or s.group(1) != source_digest():
+    if not m or not s or s.group(1) != source_digest(kernel):
         return None
     return float(m.group(1))
 
