@@ -55,6 +55,7 @@ def _load():
         "orc_ttv": (_i64, [_p, _p, _p, _p, _p, _p]),
         "orc_ttv_vjp": (None, [_p, _p, _p, _i64, _p, _p, _p, _p, _p, _p, _p]),
         "orc_batax_jacobian": (_i64, [_p, _f64, _i64, _p, _p, _p, _p]),
+        "orc_spmm_jvp": (None, [_p, _p, _p, _p, _i64, _p, _p, _p, _p]),
         "orc_set_threads": (None, [C.c_int]),
         "orc_max_threads": (C.c_int, []),
     }
@@ -300,3 +301,12 @@ def batax_jacobian(A: Dok, beta):
                                     _ptr(mag))
     assert nk <= cap
     return rowptr, colind[:nk], val[:nk], mag[:nk]
+
+
+def spmm_jvp(A: Dok, dA: Dok, B, dB, k):
+    """(C, Cmag, dC, dCmag) of C = A B with tangents dA (on A's keys) and dB."""
+    B, dB = _f64a(B), _f64a(dB)
+    m = A.dims[0]
+    C, Cm, dC, dCm = (np.empty((m, k)) for _ in range(4))
+    _load().orc_spmm_jvp(A.h, dA.h, _ptr(B), _ptr(dB), k, _ptr(C), _ptr(Cm), _ptr(dC), _ptr(dCm))
+    return C, Cm, dC, dCm

@@ -713,3 +713,38 @@ int64_t orc_batax_jacobian(const orc_dok *A, double beta, int64_t cap, int32_t *
     free(arp); free(aci); free(av); free(afirst);
     return nk;
 }
+
+/* ------------------------------------------------- forward-mode tangent */
+
+/*
+ * Forward-mode tangent of the matrix product C = A B (the forward-mode rules
+ * of Section 4.1 applied to the product's sum over A's stored keys, Section
+ * 3), for a tangent dA that lives on A's keys and a dense tangent dB:
+ *   C(i,:)  = sum over stored (i,j) of A(i,j) B(j,:)
+ *   dC(i,:) = sum over stored (i,j) of dA(i,j) B(j,:) + A(i,j) dB(j,:)
+ * dA is read from its own dictionary by key (an absent key is 0).  B, dB are
+ * row-major [ncols x k]; C, dC and their mags [nrows x k].
+ */
+void orc_spmm_jvp(const orc_dok *A, const orc_dok *dA, const double *B, const double *dB,
+                  int64_t k, double *C, double *Cmag, double *dC, double *dCmag)
+{
+    int64_t nr = A->dims[0];
+    memset(C, 0, sizeof(double) * nr * k);
+    memset(Cmag, 0, sizeof(double) * nr * k);
+    memset(dC, 0, sizeof(double) * nr * k);
+    memset(dCmag, 0, sizeof(double) * nr * k);
+    for (int64_t s = 0; s < A->cap; ++s) {
+        if (A->key[s] == -1) continue;
+        int64_t i, j;
+        unpack2(A, A->key[s], &i, &j);
+        double a = A->val[s];
+        double da = dok_get(dA, A->key[s], NULL);
+        for (int64_t c = 0; c < k; ++c) {
+            double b = B[j * k + c], db = dB[j * k + c];
+            C[i * k + c] += a * b;
+            Cmag[i * k + c] += fabs(a * b);
+            dC[i * k + c] += da * b + a * db;
+            dCmag[i * k + c] += fabs(da * b) + fabs(a * db);
+        }
+    }
+}

@@ -450,3 +450,47 @@ def test_batax_jacobian_row_outer_products(orc):
     J[np.repeat(np.arange(5), np.diff(rowptr)), colind] = jv
     assert np.array_equal(J, 2.0 * np.outer(r, r))
     assert len(colind) == 9 and np.array_equal(jm, np.abs(jv))
+
+
+# ------------------------------------------------- forward-mode tangent
+
+def test_spmm_jvp_matches_torch_forward_mode(orc):
+    """dC of C = A B by PyTorch's forward-mode jvp on the dense operands, the
+    tangent of A masked to A's keys; C equals the dense product."""
+    from torch.func import jvp
+    rng = np.random.default_rng(31)
+    nr, nc, k = 8, 6, 5
+    row, col, val = rand_coo(rng, nr, nc, 20)
+    dval = rng.standard_normal(len(val)).astype(np.float32)
+    A = orc.Dok((nr, nc), (row, col), val)
+    dA = orc.Dok((nr, nc), (row, col), dval)
+    B = rng.standard_normal((nc, k)).astype(np.float32)
+    dB = rng.standard_normal((nc, k)).astype(np.float32)
+    C, Cm, dC, dCm = orc.spmm_jvp(A, dA, B, dB, k)
+    Ad = torch.tensor(dense_of(nr, nc, row, col, val))
+    dAd = torch.tensor(dense_of(nr, nc, row, col, dval))
+    Ct, dCt = jvp(lambda a, b: a @ b, (Ad, torch.tensor(B, dtype=torch.float64)),
+                  (dAd, torch.tensor(dB, dtype=torch.float64)))
+    assert np.allclose(C, Ct.numpy(), rtol=0, atol=1e-12)
+    assert np.allclose(dC, dCt.numpy(), rtol=0, atol=1e-12)
+    assert np.all(Cm >= np.abs(C) - 1e-15) and np.all(dCm >= np.abs(dC) - 1e-15)
+
+
+def test_spmm_jvp_linear_in_the_tangent(orc):
+    """Zero tangents give dC = 0; dB alone gives A dB; dA alone gives dA B."""
+    rng = np.random.default_rng(32)
+    nr, nc, k = 30, 20, 3
+    row, col, val = rand_coo(rng, nr, nc, 90)
+    A = orc.Dok((nr, nc), (row, col), val)
+    zero = orc.Dok((nr, nc), (row, col), np.zeros_like(val))
+    B = rng.standard_normal((nc, k)).astype(np.float32)
+    dB = rng.standard_normal((nc, k)).astype(np.float32)
+    _, _, d0, m0 = orc.spmm_jvp(A, zero, B, np.zeros_like(B), k)
+    assert np.array_equal(d0, np.zeros_like(d0)) and np.array_equal(m0, np.zeros_like(m0))
+    _, _, d1, _ = orc.spmm_jvp(A, zero, B, dB, k)
+    As = sp.csr_matrix((val.astype(np.float64), (row, col)), shape=(nr, nc))
+    assert np.allclose(d1, As @ dB.astype(np.float64), rtol=1e-12, atol=1e-12)
+    dval = rng.standard_normal(len(val)).astype(np.float32)
+    _, _, d2, _ = orc.spmm_jvp(A, orc.Dok((nr, nc), (row, col), dval), B, np.zeros_like(B), k)
+    dAs = sp.csr_matrix((dval.astype(np.float64), (row, col)), shape=(nr, nc))
+    assert np.allclose(d2, dAs @ B.astype(np.float64), rtol=1e-12, atol=1e-12)
