@@ -39,6 +39,7 @@ WORKLOAD_NAMES = {
     "spmv": "spmv_sum_1k_10k",
     "build": "build_coo_to_csr_csc_1M_500k_50M",
     "batax": "batax_jacobian_100k_1M_uniform",
+    "jvp": "spmm_jvp_100k_1M_zipf1.1_k64",
 }
 
 
@@ -278,8 +279,29 @@ def setup_batax(d, dev, torch, nsd, ops):
     return S
 
 
+def setup_jvp(d, dev, torch, nsd, ops):
+    """Forward-mode tangent of C = A B on the SpMM workload: C and
+    dC = dA B + A dB in one pass (tangents dA on A's keys and dB ~ N(0,1),
+    drawn from the workload's fourth stream)."""
+    A = ops.DeviceCsr(d["nrows"], d["ncols"], d["rowptr"], d["colind"], d["val"], device=dev,
+                      k_hint=d["k"], item_len=ITEM_LEN, build_csc=False)
+    k, nnz, nr, nc = d["k"], A.nnz, A.nrows, A.ncols
+    B = torch.from_numpy(d["B"]).to(dev)
+    dA = torch.from_numpy(d["dval"]).to(dev)
+    dB = torch.from_numpy(d["dB"]).to(dev)
+    C = torch.empty((nr, k), dtype=torch.float32, device=dev)
+    dC = torch.empty((nr, k), dtype=torch.float32, device=dev)
+    ws = A.workspace(2 * k)
+    S = Setup()
+    S.A, S.nnz, S.k = A, nnz, k
+    S.step = lambda: nsd.nsd_spmm_jvp(A.desc, dA, B, dB, k, C, dC, ws)
+    # rowidx, colind, val, dA in; B and dB read once, C and dC written once
+    S.kernels = {"jvp": 4 * 4 * nnz + 2 * 4 * k * (nr + nc)}
+    return S
+
+
 SETUPS = {"spmm": setup_spmm, "gnn": setup_gnn, "mf": setup_mf, "cp": setup_cp,
-          "spmv": setup_spmv, "build": setup_build, "batax": setup_batax}
+          "spmv": setup_spmv, "build": setup_build, "batax": setup_batax, "jvp": setup_jvp}
 
 
 # ------------------------------------------------------------ measurement
@@ -328,7 +350,11 @@ def main():
 
     synth.VERBOSE = True  # progress lines on stderr while the inputs are drawn
     t0 = time.perf_counter()
-    d = synth.make("mf" if args.workload == "build" else args.workload, args.size)
+    d = synth.make({"build": "mf", "jvp": "spmm"}.get(args.workload, args.workload), args.size)
+    if args.workload == "jvp":
+        g = synth.streams("spmm")[3]  # the fourth stream: the tangents
+        d["dval"] = g.standard_normal(len(d["val"]), dtype=np.float32)
+        d["dB"] = g.standard_normal(d["B"].shape, dtype=np.float32)
     gen_s = time.perf_counter() - t0
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -398,6 +424,8 @@ def main():
     metric = {"build": "pattern entries/sec (COO->CSR, CSR->CSC, value permute)",
               "batax": "Jacobian nonzeros/sec (BATAX, beta A^T A)"}.get(
                   args.workload, "gradient nonzeros/sec (forward+backward)")
+    if args.workload == "jvp":
+        metric = "tangent nonzeros/sec (forward-mode dC = dA B + A dB)"
     out = {
         "metric": metric,
         "value": round(S.nnz / (ms_per_step * 1e-3), 1),
@@ -424,7 +452,7 @@ def _sample(args, d):
     """A bounded sample of the workload for the oracle: the whole input when
     it is small, else a prefix (leading rows / entries) of it."""
     w = args.workload
-    if w in ("spmm", "spmv"):
+    if w in ("spmm", "spmv", "jvp"):
         return d, "the full workload"
     if w == "gnn":
         # leading rows; the columns they touch are renumbered so that only
@@ -468,7 +496,7 @@ def cpu_baseline(args, d):
     s, what = _sample(args, d)
     w = args.workload
 
-    if w in ("spmm", "spmv", "gnn", "batax"):
+    if w in ("spmm", "spmv", "gnn", "batax", "jvp"):
         nrows, ncols = s["nrows"], s["ncols"]
         rows = np.repeat(np.arange(nrows, dtype=np.int32), np.diff(s["rowptr"]))
         nnz = len(s["colind"])
@@ -496,6 +524,10 @@ def cpu_baseline(args, d):
             oracle.loss_bilinear(D, s["G"], s["H"], k)
             oracle.sddmm(D, s["G"], s["H"], k, rows, s["colind"])
             oracle.spmm_t(D, s["G"], k)
+        elif w == "jvp":
+            D = oracle.Dok((nrows, ncols), (rows, s["colind"]), s["val"])
+            dD = oracle.Dok((nrows, ncols), (rows, s["colind"]), s["dval"])
+            oracle.spmm_jvp(D, dD, s["B"], s["dB"], s["k"])
         elif w == "batax":
             D = oracle.Dok((nrows, ncols), (rows, s["colind"]), s["val"])
             one_pass.nk = len(oracle.batax_jacobian(D, s["beta"])[1])
@@ -525,6 +557,7 @@ def cpu_baseline(args, d):
         if el >= args.cpu_seconds or passes >= 1000:
             break
     done = {"build": "DOK build + CSR emission + stable column sort",
+            "jvp": "DOK builds + C and its tangent",
             "batax": "DOK build + the Jacobian's outer products + CSR emission"}.get(
                 w, "DOK build + loss + all gradients")
     if w == "batax":

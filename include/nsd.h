@@ -183,7 +183,8 @@ typedef enum nsd_kernel_id {
     NSD_KERNEL_TTV = 9,        /* TTV entry kernels */
     NSD_KERNEL_DUAL = 10,      /* one column pass giving dA, A^T G and the loss
                                   (bilinear and SMVM losses) */
-    NSD_KERNEL_SORT = 11       /* radix-sort scatter pass of the builders */
+    NSD_KERNEL_SORT = 11,      /* radix-sort scatter pass of the builders */
+    NSD_KERNEL_JVP = 12        /* forward-mode tangent of the matrix product */
 } nsd_kernel_id;
 
 /*
@@ -423,6 +424,20 @@ nsd_status nsd_ttv(const nsd_ttv_plan *T, const float *x, const float *v, float 
  */
 nsd_status nsd_ttv_vjp(const nsd_ttv_plan *T, const float *x, const float *v, const float *gy,
                        float *dx, float *dv, void *ws, size_t ws_bytes, void *stream);
+
+/* ---------------------------------------------------------------------------
+ * Forward-mode tangent of C = A B, the paper's mode of differentiation
+ * (Section 4.1: values carried with their tangents; Section 4.2: tensors of
+ * tangents): for a tangent dA on A's stored keys and a dense tangent dB,
+ *     C  = A B,     dC = dA B + A dB.
+ * A: CSR with rowidx and the row plan.  dAval [nnz]: the tangent of A's
+ * values in A's storage order.  B, dB [ncols x k], C, dC [nrows x k],
+ * row-major, fully overwritten (0 for empty rows).  Any k >= 1.
+ * Workspace: at least nsd_workspace_size(A, NULL, 2k, ...) bytes.  Async.
+ */
+nsd_status nsd_spmm_jvp(const nsd_csr *A, const float *dAval, const float *B, const float *dB,
+                        int32_t k, float *C, float *dC, void *ws, size_t ws_bytes,
+                        void *stream);
 
 /* ---------------------------------------------------------------------------
  * Jacobian of the BATAX kernel f(j) = sum_{i,k} beta A(i,j) A(i,k) x(k) with

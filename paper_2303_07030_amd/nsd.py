@@ -27,7 +27,7 @@ NSD_ERR_HIP = 7
 NSD_DUP_SUM = 0
 NSD_DUP_ERROR = 1
 KERNEL_IDS = {"sgr_main": 1, "sgr_fix": 2, "sddmm": 3, "frob_row": 4, "frob_col": 5, "mf": 6,
-              "cp": 7, "loss": 8, "ttv": 9, "dual": 10, "sort": 11}
+              "cp": 7, "loss": 8, "ttv": 9, "dual": 10, "sort": 11, "jvp": 12}
 
 
 class NsdError(RuntimeError):
@@ -125,6 +125,7 @@ _SIGS = {
     "nsd_ttv_workspace_size": (C.c_int, [_TTV, C.POINTER(_SZ)]),
     "nsd_ttv": (C.c_int, [_TTV, _P, _P, _P, _P, _SZ, _P]),
     "nsd_ttv_vjp": (C.c_int, [_TTV, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "nsd_spmm_jvp": (C.c_int, [_CSR, _P, _P, _P, _I, _P, _P, _P, _SZ, _P]),
     "nsd_batax_pairs": (C.c_int, [_CSR, C.POINTER(C.c_int64), _P, _SZ, _P]),
     "nsd_batax_workspace_size": (C.c_int, [_CSR, C.c_int64, C.POINTER(_SZ)]),
     "nsd_batax_jacobian": (C.c_int, [_CSR, C.c_float, C.c_int64, _P, _P, _P, C.POINTER(_I), _P,
@@ -408,3 +409,10 @@ def nsd_batax_jacobian(A: nsd_csr, beta, npairs, jrowptr, jcolind, jval, ws, str
                                    C.byref(out), _p(ws), _nbytes(ws), _stream(stream)),
            "nsd_batax_jacobian")
     return out.value
+
+
+# ------------------------------------------------------ forward-mode tangent
+
+def nsd_spmm_jvp(A: nsd_csr, dAval, B, dB, k, C_out, dC, ws, stream=None):
+    _check(_lib.nsd_spmm_jvp(C.byref(A), _p(dAval), _p(B), _p(dB), k, _p(C_out), _p(dC), _p(ws),
+                             _nbytes(ws), _stream(stream)), "nsd_spmm_jvp")

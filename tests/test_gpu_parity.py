@@ -677,3 +677,44 @@ def test_batax_jacobian_rejects_wrong_pair_count(nsd, operand):
     with pytest.raises(nsd.NsdError) as e:
         nsd.nsd_batax_jacobian(A.desc, 1.0, P + 1, jr, jc, jv, ws)
     assert e.value.status == nsd.NSD_ERR_INVALID_ARG
+
+
+# ------------------------------------------------- forward-mode tangent
+
+def run_spmm_jvp(nsd, A, dAval, B, dB, k):
+    C = torch.full((A.nrows, k), np.nan, dtype=torch.float32, device="cuda")
+    dC = torch.full((A.nrows, k), np.nan, dtype=torch.float32, device="cuda")
+    nsd.nsd_spmm_jvp(A.desc, dev(dAval), dev(B), dev(dB), k, C, dC, A.workspace(2 * k))
+    return host(C), host(dC)
+
+
+@pytest.mark.parametrize("k", [1, 3, 16, 64, 128, 256, 264])
+def test_spmm_jvp(nsd, orc, edge_A, k):
+    A, D, rows, colind = edge_A
+    rng = np.random.default_rng(100 + k)
+    dval = rng.standard_normal(A.nnz).astype(np.float32)
+    B = rng.standard_normal((A.ncols, k)).astype(np.float32)
+    dB = rng.standard_normal((A.ncols, k)).astype(np.float32)
+    Cg, dCg = run_spmm_jvp(nsd, A, dval, B, dB, k)
+    dD = orc.Dok((A.nrows, A.ncols), (rows, colind), dval)
+    C, Cm, dC, dCm = orc.spmm_jvp(D, dD, B, dB, k)
+    assert_mag_close(Cg, C, Cm, what="C")
+    assert_mag_close(dCg, dC, dCm, what="dC")
+
+
+def test_spmm_jvp_full_workload(nsd, operand, orc):
+    from paper_2303_07030_amd import synth
+    d = synth.make("spmm")
+    k = d["k"]
+    A = operand(d["nrows"], d["ncols"], d["rowptr"], d["colind"], d["val"], build_csc=False,
+                k_hint=k)
+    rng = np.random.default_rng(7)
+    dval = rng.standard_normal(A.nnz).astype(np.float32)
+    dB = rng.standard_normal(d["B"].shape).astype(np.float32)
+    Cg, dCg = run_spmm_jvp(nsd, A, dval, d["B"], dB, k)
+    rows = np.repeat(np.arange(d["nrows"], dtype=np.int32), np.diff(d["rowptr"]))
+    D = orc.Dok((d["nrows"], d["ncols"]), (rows, d["colind"]), d["val"])
+    dD = orc.Dok((d["nrows"], d["ncols"]), (rows, d["colind"]), dval)
+    C, Cm, dC, dCm = orc.spmm_jvp(D, dD, d["B"], dB, k)
+    assert_mag_close(Cg, C, Cm, what="C")
+    assert_mag_close(dCg, dC, dCm, what="dC")
