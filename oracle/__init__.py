@@ -56,6 +56,10 @@ def _load():
         "orc_ttv_vjp": (None, [_p, _p, _p, _i64, _p, _p, _p, _p, _p, _p, _p]),
         "orc_batax_jacobian": (_i64, [_p, _f64, _i64, _p, _p, _p, _p]),
         "orc_spmm_jvp": (None, [_p, _p, _p, _p, _i64, _p, _p, _p, _p]),
+        "orc_dok_buildn": (_p, [C.c_int32, _p, _i64, _p, _p]),
+        "orc_cpn_loss": (None, [_p, _p, _i64, _p, _p]),
+        "orc_cpn_resid": (None, [_p, _p, _i64, _i64, _p, _p, _p]),
+        "orc_cpn_grad": (None, [_p, _p, _i64, C.c_int, _i64, _p, _p, _p]),
         "orc_set_threads": (None, [C.c_int]),
         "orc_max_threads": (C.c_int, []),
     }
@@ -93,7 +97,7 @@ def _sel(sel):
 
 
 class Dok:
-    """A sparse matrix (order 2) or 3-tensor (order 3) held as a DOK.
+    """A sparse matrix (order 2) or tensor (order 3 to 6) held as a DOK.
 
     Duplicate coordinates are summed on insert (semi-ring insert)."""
 
@@ -106,9 +110,13 @@ class Dok:
         if len(self.dims) == 2:
             self.h = lib.orc_dok_build2(self.dims[0], self.dims[1], n,
                                         _ptr(self._keep[0]), _ptr(self._keep[1]), _ptr(v))
-        else:
+        elif len(self.dims) == 3:
             self.h = lib.orc_dok_build3(self.dims[0], self.dims[1], self.dims[2], n,
                                         *[_ptr(c) for c in self._keep], _ptr(v))
+        else:
+            dims = np.asarray(self.dims, dtype=np.int64)
+            ptrs = (C.c_void_p * len(self.dims))(*[_ptr(c) for c in self._keep])
+            self.h = lib.orc_dok_buildn(len(self.dims), _ptr(dims), n, ptrs, _ptr(v))
         self._keep = None
 
     @classmethod
@@ -310,3 +318,37 @@ def spmm_jvp(A: Dok, dA: Dok, B, dB, k):
     C, Cm, dC, dCm = (np.empty((m, k)) for _ in range(4))
     _load().orc_spmm_jvp(A.h, dA.h, _ptr(B), _ptr(dB), k, _ptr(C), _ptr(Cm), _ptr(dC), _ptr(dCm))
     return C, Cm, dC, dCm
+
+
+def _fptrs(F):
+    Fs = [_f64a(f) for f in F]
+    return Fs, (C.c_void_p * len(Fs))(*[_ptr(f) for f in Fs])
+
+
+def cpn_loss(X: Dok, F, R):
+    """Order-N CP loss 1/2 sum (x - m)^2 (and its mag); F = [F_1 .. F_N]."""
+    Fs, fp = _fptrs(F)
+    L, M = _two()
+    _load().orc_cpn_loss(X.h, fp, R, C.byref(L), C.byref(M))
+    return L.value, M.value
+
+
+def cpn_resid(X: Dok, F, R, coords):
+    """Residual x - m at the queried keys (coords: N arrays)."""
+    Fs, fp = _fptrs(F)
+    qs = [_i32(c) for c in coords]
+    qp = (C.c_void_p * len(qs))(*[_ptr(c) for c in qs])
+    n = len(qs[0])
+    r, m = np.empty(n), np.empty(n)
+    _load().orc_cpn_resid(X.h, fp, R, n, qp, _ptr(r), _ptr(m))
+    return r, m
+
+
+def cpn_grad(X: Dok, F, R, mode, sel=None):
+    """dF_mode, the negated mode MTTKRP of the residual (selected rows)."""
+    Fs, fp = _fptrs(F)
+    nsel, s = _sel(sel)
+    m = nsel if sel is not None else X.dims[mode]
+    out, mag = np.empty((m, R)), np.empty((m, R))
+    _load().orc_cpn_grad(X.h, fp, R, mode, nsel, _ptr(s), _ptr(out), _ptr(mag))
+    return out, mag

@@ -65,9 +65,11 @@ typedef struct orc_dok {
     int64_t *key;    /* packed coordinate, -1 marks an empty slot */
     double *val;     /* value stored under the key */
     int64_t *first;  /* index of the insertion that created the key */
-    int32_t order;   /* 2 (matrix) or 3 (3-tensor) */
-    int64_t dims[3];
+    int32_t order;   /* 2 (matrix) to ORC_MAX_ORDER */
+    int64_t dims[6];
 } orc_dok;
+
+#define ORC_MAX_ORDER 6
 
 static uint64_t orc_hash(uint64_t x)
 {   /* splitmix64 finaliser */
@@ -93,7 +95,7 @@ static orc_dok *dok_new(int32_t order, const int64_t *dims, int64_t expected)
     while (cap < 2 * expected + 16) cap <<= 1;
     d->cap = cap;
     d->order = order;
-    for (int i = 0; i < 3; ++i) d->dims[i] = i < order ? dims[i] : 1;
+    for (int i = 0; i < ORC_MAX_ORDER; ++i) d->dims[i] = i < order ? dims[i] : 1;
     d->key = (int64_t *)malloc(sizeof(int64_t) * cap);
     d->val = (double *)malloc(sizeof(double) * cap);
     d->first = (int64_t *)malloc(sizeof(int64_t) * cap);
@@ -747,4 +749,114 @@ void orc_spmm_jvp(const orc_dok *A, const orc_dok *dA, const double *B, const do
             dCmag[i * k + c] += fabs(da * b) + fabs(a * db);
         }
     }
+}
+
+
+/* ------------------------------------------------ order-N CP gradient */
+
+/* coordinates of a packed key of an order-N DOK (mixed radix, mode 0 most
+ * significant) */
+static void unpackn(const orc_dok *d, int64_t k, int64_t *c)
+{
+    for (int n = d->order - 1; n >= 0; --n) {
+        c[n] = k % d->dims[n];
+        k /= d->dims[n];
+    }
+}
+
+orc_dok *orc_dok_buildn(int32_t order, const int64_t *dims, int64_t nnz,
+                        const int32_t *const *coords, const float *val)
+{
+    orc_dok *d = dok_new(order, dims, nnz);
+    for (int64_t p = 0; p < nnz; ++p) {
+        int64_t key = 0;
+        for (int n = 0; n < order; ++n) key = key * dims[n] + coords[n][p];
+        dok_add(d, key, val ? (double)val[p] : 1.0, p);
+    }
+    return d;
+}
+
+/* m = sum_r prod_n F_n(c_n, r) at one key, R = x - m; *rmag = |x| + sum |terms| */
+static double cpn_resid(const orc_dok *X, const double *const *F, int64_t R, const int64_t *c,
+                        double x, double *rmag)
+{
+    double m = 0.0, mm = 0.0;
+    for (int64_t r = 0; r < R; ++r) {
+        double t = 1.0;
+        for (int n = 0; n < X->order; ++n) t *= F[n][c[n] * R + r];
+        m += t;
+        mm += fabs(t);
+    }
+    *rmag = fabs(x) + mm;
+    return x - m;
+}
+
+/*
+ * Rank-R CP model of an order-N sparse tensor X (the order-3 case of
+ * Section 3's nested dictionaries, with N nested levels):
+ *   L = 1/2 sum over stored keys of (x - m)^2,  m = sum_r prod_n F_n(c_n, r)
+ */
+void orc_cpn_loss(const orc_dok *X, const double *const *F, int64_t R, double *loss,
+                  double *mag)
+{
+    double L = 0.0, M = 0.0;
+    int64_t c[ORC_MAX_ORDER];
+    for (int64_t s = 0; s < X->cap; ++s) {
+        if (X->key[s] == -1) continue;
+        unpackn(X, X->key[s], c);
+        double rm, r = cpn_resid(X, F, R, c, X->val[s], &rm);
+        L += r * r;
+        M += rm * rm;
+    }
+    *loss = 0.5 * L;
+    *mag = 0.5 * M;
+}
+
+/* residual (the gradient w.r.t. the stored values) at queried keys;
+ * q[n][p] is coordinate n of query p */
+void orc_cpn_resid(const orc_dok *X, const double *const *F, int64_t R, int64_t nq,
+                   const int32_t *const *q, double *res, double *resmag)
+{
+    int64_t c[ORC_MAX_ORDER];
+    for (int64_t p = 0; p < nq; ++p) {
+        int64_t key = 0;
+        for (int n = 0; n < X->order; ++n) {
+            c[n] = q[n][p];
+            key = key * X->dims[n] + c[n];
+        }
+        int pr;
+        double x = dok_get(X, key, &pr);
+        if (!pr) { res[p] = 0.0; resmag[p] = 0.0; continue; }
+        res[p] = cpn_resid(X, F, R, c, x, &resmag[p]);
+    }
+}
+
+/*
+ * Factor gradient of mode n, the negated mode-n MTTKRP of the residual:
+ *   dF_n(c_n, :) = -sum over stored keys of R * (o_{m != n} F_m(c_m, :))
+ */
+void orc_cpn_grad(const orc_dok *X, const double *const *F, int64_t R, int mode, int64_t nsel,
+                  const int32_t *sel, double *out, double *outmag)
+{
+    int64_t rows_all = X->dims[mode];
+    int64_t *map = select_map(rows_all, nsel, sel);
+    int64_t rows = sel ? nsel : rows_all;
+    memset(out, 0, sizeof(double) * rows * R);
+    memset(outmag, 0, sizeof(double) * rows * R);
+    int64_t c[ORC_MAX_ORDER];
+    for (int64_t s = 0; s < X->cap; ++s) {
+        if (X->key[s] == -1) continue;
+        unpackn(X, X->key[s], c);
+        int64_t o = map[c[mode]];
+        if (o < 0) continue;
+        double rm, r = cpn_resid(X, F, R, c, X->val[s], &rm);
+        for (int64_t t = 0; t < R; ++t) {
+            double h = 1.0;
+            for (int n = 0; n < X->order; ++n)
+                if (n != mode) h *= F[n][c[n] * R + t];
+            out[o * R + t] += -r * h;
+            outmag[o * R + t] += rm * fabs(h);
+        }
+    }
+    free(map);
 }

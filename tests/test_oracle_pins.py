@@ -494,3 +494,54 @@ def test_spmm_jvp_linear_in_the_tangent(orc):
     _, _, d2, _ = orc.spmm_jvp(A, orc.Dok((nr, nc), (row, col), dval), B, np.zeros_like(B), k)
     dAs = sp.csr_matrix((dval.astype(np.float64), (row, col)), shape=(nr, nc))
     assert np.allclose(d2, dAs @ B.astype(np.float64), rtol=1e-12, atol=1e-12)
+
+
+# ----------------------------------------------------- order-N CP gradient
+
+@pytest.mark.parametrize("dims", [(4, 5, 3, 6), (3, 4, 3, 2, 5)])
+def test_cpn_matches_autograd(orc, dims):
+    """Order-4 and order-5 CP: loss, residual and every factor gradient by
+    PyTorch fp64 autograd of 1/2 sum over the stored keys of (x - m)^2 with
+    m from a dense einsum."""
+    rng = np.random.default_rng(sum(dims))
+    N, R = len(dims), 3
+    size = int(np.prod(dims))
+    keys = rng.choice(size, size=size // 3, replace=False)
+    coords = np.unravel_index(keys, dims)
+    coords = [c.astype(np.int32) for c in coords]
+    val = rng.standard_normal(len(keys)).astype(np.float32)
+    F = [rng.standard_normal((d, R)).astype(np.float32) for d in dims]
+    X = orc.Dok(dims, coords, val)
+    L, Lm = orc.cpn_loss(X, F, R)
+    Ft = [torch.tensor(f, dtype=torch.float64, requires_grad=True) for f in F]
+    letters = "abcdef"[:N]
+    m = torch.einsum(",".join(f"{l}r" for l in letters) + "->" + letters, *Ft)
+    x = torch.tensor(val, dtype=torch.float64)
+    res = x - m[tuple(torch.tensor(c, dtype=torch.long) for c in coords)]
+    Lt = 0.5 * (res ** 2).sum()
+    Lt.backward()
+    assert abs(L - Lt.item()) <= 1e-12 * max(1.0, Lm)
+    r, rm = orc.cpn_resid(X, F, R, coords)
+    assert np.allclose(r, res.detach().numpy(), rtol=0, atol=1e-12)
+    for n in range(N):
+        g, gm = orc.cpn_grad(X, F, R, n)
+        assert np.allclose(g, Ft[n].grad.numpy(), rtol=0, atol=1e-12)
+        assert np.all(gm >= np.abs(g) - 1e-12)
+    # a selection gives the same rows
+    sel = np.array([dims[0] - 1, 0], np.int32)
+    g0, _ = orc.cpn_grad(X, F, R, 0, sel=sel)
+    assert np.array_equal(g0, orc.cpn_grad(X, F, R, 0)[0][sel])
+
+
+def test_cpn_order3_equals_the_order3_oracle(orc):
+    rng = np.random.default_rng(41)
+    dims, R = (7, 6, 5), 4
+    keys = rng.choice(210, size=60, replace=False)
+    i, j, l = (c.astype(np.int32) for c in np.unravel_index(keys, dims))
+    val = rng.standard_normal(60).astype(np.float32)
+    F = [rng.standard_normal((d, R)).astype(np.float32) for d in dims]
+    X3 = orc.Dok(dims, (i, j, l), val)
+    assert np.isclose(orc.cpn_loss(X3, F, R)[0], orc.cp_loss(X3, *F, R)[0], rtol=1e-14)
+    for n in range(3):
+        assert np.allclose(orc.cpn_grad(X3, F, R, n)[0], orc.cp_grad(X3, *F, R, n)[0],
+                           rtol=1e-13, atol=1e-13)
