@@ -40,6 +40,7 @@ WORKLOAD_NAMES = {
     "build": "build_coo_to_csr_csc_1M_500k_50M",
     "batax": "batax_jacobian_100k_1M_uniform",
     "jvp": "spmm_jvp_100k_1M_zipf1.1_k64",
+    "cp4": "cp_order4_1000^4_20M_rank32",
 }
 
 
@@ -300,8 +301,29 @@ def setup_jvp(d, dev, torch, nsd, ops):
     return S
 
 
+def setup_cp4(d, dev, torch, nsd, ops):
+    """CP gradient of an order-4 tensor through the order-N entry point."""
+    X = ops.DeviceCooN(d["dims"], d["coords"], d["val"], device=dev, rank_hint=d["rank"],
+                       item_len=ITEM_LEN)
+    R, nnz, N = d["rank"], X.nnz, len(d["dims"])
+    F = [torch.from_numpy(f).to(dev) for f in d["F"]]
+    dF = [torch.empty((X.dims[m], R), dtype=torch.float32, device=dev) for m in range(N)]
+    dX = torch.empty(nnz, dtype=torch.float32, device=dev)
+    loss = torch.empty(1, dtype=torch.float64, device=dev)
+    ws = X.workspace(R)
+    S = Setup()
+    S.A, S.nnz, S.k = X, nnz, R
+    S.step = lambda: nsd.nsd_loss_cpn(X.desc, F, R, 1.0, loss, dX, dF, ws)
+    # N passes of (mode coordinate, N-1 coordinates, value); the first also
+    # reads perm and writes the residual; factors read and gradients
+    # written once
+    S.kernels = {"cpn": N * (N + 1) * 4 * nnz + 2 * 4 * nnz + 2 * 4 * R * sum(X.dims)}
+    return S
+
+
 SETUPS = {"spmm": setup_spmm, "gnn": setup_gnn, "mf": setup_mf, "cp": setup_cp,
-          "spmv": setup_spmv, "build": setup_build, "batax": setup_batax, "jvp": setup_jvp}
+          "spmv": setup_spmv, "build": setup_build, "batax": setup_batax, "jvp": setup_jvp,
+          "cp4": setup_cp4}
 
 
 # ------------------------------------------------------------ measurement
@@ -465,6 +487,10 @@ def _sample(args, d):
                  colind=colind.astype(np.int32), val=d["val"][:e], G=d["G"][:nr],
                  H=d["H"][cols])
         return s, f"rows 0..{nr - 1} ({e} nnz) of the workload with the {len(cols)} columns they use"
+    if w == "cp4":
+        e = 1_000_000
+        return dict(d, coords=[c[:e] for c in d["coords"]], val=d["val"][:e]), \
+            f"the first {e} COO entries of the workload, full factors"
     if w == "batax":
         rp = d["rowptr"]
         nr = 12_000
@@ -502,6 +528,8 @@ def cpu_baseline(args, d):
         nnz = len(s["colind"])
     elif w in ("mf", "build"):
         nnz = len(s["row"])
+    elif w == "cp4":
+        nnz = len(s["val"])
     else:
         nnz = len(s["i"])
 
@@ -524,6 +552,12 @@ def cpu_baseline(args, d):
             oracle.loss_bilinear(D, s["G"], s["H"], k)
             oracle.sddmm(D, s["G"], s["H"], k, rows, s["colind"])
             oracle.spmm_t(D, s["G"], k)
+        elif w == "cp4":
+            D = oracle.Dok(s["dims"], s["coords"], s["val"])
+            oracle.cpn_loss(D, s["F"], s["rank"])
+            oracle.cpn_resid(D, s["F"], s["rank"], s["coords"])
+            for m in range(len(s["dims"])):
+                oracle.cpn_grad(D, s["F"], s["rank"], m)
         elif w == "jvp":
             D = oracle.Dok((nrows, ncols), (rows, s["colind"]), s["val"])
             dD = oracle.Dok((nrows, ncols), (rows, s["colind"]), s["dval"])

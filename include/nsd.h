@@ -184,7 +184,8 @@ typedef enum nsd_kernel_id {
     NSD_KERNEL_DUAL = 10,      /* one column pass giving dA, A^T G and the loss
                                   (bilinear and SMVM losses) */
     NSD_KERNEL_SORT = 11,      /* radix-sort scatter pass of the builders */
-    NSD_KERNEL_JVP = 12        /* forward-mode tangent of the matrix product */
+    NSD_KERNEL_JVP = 12,       /* forward-mode tangent of the matrix product */
+    NSD_KERNEL_CPN = 13        /* order-N CP mode passes */
 } nsd_kernel_id;
 
 /*
@@ -424,6 +425,52 @@ nsd_status nsd_ttv(const nsd_ttv_plan *T, const float *x, const float *v, float 
  */
 nsd_status nsd_ttv_vjp(const nsd_ttv_plan *T, const float *x, const float *v, const float *gy,
                        float *dx, float *dv, void *ws, size_t ws_bytes, void *stream);
+
+/* ---------------------------------------------------------------------------
+ * Order-N sparse tensors and the CP gradient for orders 3 to NSD_MAX_ORDER
+ * (the order-N form of the nested-dictionary tensor of Section 3).
+ *
+ * nsd_coon holds one mode index per mode n: the stored entries sorted
+ * stably by coordinate n (nsd_coo_mode_index), segptr / segidx over the
+ * mode's slices, idx[o] = the coordinate of mode (n + 1 + o) mod order of
+ * every entry in that order (o = 0 .. order - 2), val in that order, perm =
+ * input position of every slot, and the slices' work plan.
+ */
+#define NSD_MAX_ORDER 6
+
+typedef struct nsd_coon_mode {
+    int32_t mode;
+    const int32_t *segptr;                  /* [dims[mode] + 1] */
+    const int32_t *segidx;                  /* [nnz] */
+    const int32_t *idx[NSD_MAX_ORDER - 1];  /* [order - 1][nnz] other coordinates */
+    const float *val;                       /* [nnz] */
+    const int32_t *perm;                    /* [nnz] */
+    nsd_plan plan;
+} nsd_coon_mode;
+
+typedef struct nsd_coon {
+    int32_t order;                  /* 3 .. NSD_MAX_ORDER */
+    int32_t dims[NSD_MAX_ORDER];
+    int32_t nnz;
+    nsd_coon_mode mode[NSD_MAX_ORDER];
+} nsd_coon;
+
+/* Bytes of `ws` for nsd_loss_cpn.  Writes *bytes (host). */
+nsd_status nsd_cpn_workspace_size(const nsd_coon *X, int32_t rank, size_t *bytes);
+
+/*
+ * Rank-R CP model of an order-N sparse tensor X:
+ *   m = sum_r prod_n F_n(c_n, r),  R = x - m on X's keys,  L = 1/2 sum R^2,
+ *   dX = seed * R on X's keys (X's input order, [nnz]),
+ *   dF_n(c_n, :) = -seed sum R * (o_{m != n} F_m(c_m, :))  (negated MTTKRPs).
+ * F and dF are HOST arrays of `order` device pointers to [dims[n] x rank]
+ * row-major factors.  *loss (device fp64) is not scaled by seed.  rank <= 256
+ * (multiple of 4, 16-byte aligned rows) or <= 64 otherwise, else
+ * NSD_ERR_UNSUPPORTED.  Async.
+ */
+nsd_status nsd_loss_cpn(const nsd_coon *X, const float *const *F, int32_t rank, float seed,
+                        double *loss, float *dX, float *const *dF, void *ws, size_t ws_bytes,
+                        void *stream);
 
 /* ---------------------------------------------------------------------------
  * Forward-mode tangent of C = A B, the paper's mode of differentiation

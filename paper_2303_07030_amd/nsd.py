@@ -27,7 +27,7 @@ NSD_ERR_HIP = 7
 NSD_DUP_SUM = 0
 NSD_DUP_ERROR = 1
 KERNEL_IDS = {"sgr_main": 1, "sgr_fix": 2, "sddmm": 3, "frob_row": 4, "frob_col": 5, "mf": 6,
-              "cp": 7, "loss": 8, "ttv": 9, "dual": 10, "sort": 11, "jvp": 12}
+              "cp": 7, "loss": 8, "ttv": 9, "dual": 10, "sort": 11, "jvp": 12, "cpn": 13}
 
 
 class NsdError(RuntimeError):
@@ -63,6 +63,20 @@ class nsd_coo3_mode(C.Structure):
 
 class nsd_coo3(C.Structure):
     _fields_ = [("dims", C.c_int32 * 3), ("nnz", C.c_int32), ("mode", nsd_coo3_mode * 3)]
+
+
+MAX_ORDER = 6
+
+
+class nsd_coon_mode(C.Structure):
+    _fields_ = [("mode", C.c_int32), ("segptr", C.c_void_p), ("segidx", C.c_void_p),
+                ("idx", C.c_void_p * (MAX_ORDER - 1)), ("val", C.c_void_p),
+                ("perm", C.c_void_p), ("plan", nsd_plan)]
+
+
+class nsd_coon(C.Structure):
+    _fields_ = [("order", C.c_int32), ("dims", C.c_int32 * MAX_ORDER), ("nnz", C.c_int32),
+                ("mode", nsd_coon_mode * MAX_ORDER)]
 
 
 class nsd_ttv_plan(C.Structure):
@@ -125,6 +139,9 @@ _SIGS = {
     "nsd_ttv_workspace_size": (C.c_int, [_TTV, C.POINTER(_SZ)]),
     "nsd_ttv": (C.c_int, [_TTV, _P, _P, _P, _P, _SZ, _P]),
     "nsd_ttv_vjp": (C.c_int, [_TTV, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "nsd_cpn_workspace_size": (C.c_int, [C.POINTER(nsd_coon), _I, C.POINTER(_SZ)]),
+    "nsd_loss_cpn": (C.c_int, [C.POINTER(nsd_coon), C.POINTER(_P), _I, C.c_float, _P, _P,
+                               C.POINTER(_P), _P, _SZ, _P]),
     "nsd_spmm_jvp": (C.c_int, [_CSR, _P, _P, _P, _I, _P, _P, _P, _SZ, _P]),
     "nsd_batax_pairs": (C.c_int, [_CSR, C.POINTER(C.c_int64), _P, _SZ, _P]),
     "nsd_batax_workspace_size": (C.c_int, [_CSR, C.c_int64, C.POINTER(_SZ)]),
@@ -416,3 +433,20 @@ def nsd_batax_jacobian(A: nsd_csr, beta, npairs, jrowptr, jcolind, jval, ws, str
 def nsd_spmm_jvp(A: nsd_csr, dAval, B, dB, k, C_out, dC, ws, stream=None):
     _check(_lib.nsd_spmm_jvp(C.byref(A), _p(dAval), _p(B), _p(dB), k, _p(C_out), _p(dC), _p(ws),
                              _nbytes(ws), _stream(stream)), "nsd_spmm_jvp")
+
+
+# --------------------------------------------------- order-N CP gradient
+
+def nsd_cpn_workspace_size(X: nsd_coon, rank: int) -> int:
+    b = _SZ(0)
+    _check(_lib.nsd_cpn_workspace_size(C.byref(X), rank, C.byref(b)), "nsd_cpn_workspace_size")
+    return b.value
+
+
+def nsd_loss_cpn(X: nsd_coon, F, rank, seed, loss, dX, dF, ws, stream=None):
+    """F, dF: sequences of `order` device tensors (passed as a host array of
+    device pointers)."""
+    fp = (_P * len(F))(*[_p(f) for f in F])
+    dp = (_P * len(dF))(*[_p(t) for t in dF])
+    _check(_lib.nsd_loss_cpn(C.byref(X), fp, rank, seed, _p(loss), _p(dX), dp, _p(ws),
+                             _nbytes(ws), _stream(stream)), "nsd_loss_cpn")

@@ -150,6 +150,59 @@ class DeviceCoo3:
         return torch.empty(max(n, 256), dtype=torch.uint8, device=self.val.device)
 
 
+class DeviceCooN:
+    """A COO tensor of order 3 to 6 in HBM in all its mode orders: for every
+    mode n the library's mode index (stable sort by coordinate n), the other
+    coordinates (modes n+1, n+2, ... mod order) and the values gathered into
+    that order, and the work plan over the mode-n slices."""
+
+    def __init__(self, dims, coords, val, device="cuda", rank_hint=32, item_len=None,
+                 stream=None):
+        self.dims = tuple(int(d) for d in dims)
+        N = self.order = len(self.dims)
+        if not 3 <= N <= nsd.MAX_ORDER:
+            raise ValueError(f"order {N} outside [3, {nsd.MAX_ORDER}]")
+        coords = [_dev(c, torch.int32, device) for c in coords]
+        self.val = _dev(val, torch.float32, device)
+        self.nnz = int(self.val.numel())
+        self.item_len = item_len or nsd.nsd_plan_item_len(self.nnz, rank_hint)
+        self.desc = nsd.nsd_coon()
+        self.desc.order = N
+        for m in range(N):
+            self.desc.dims[m] = self.dims[m]
+        self.desc.nnz = self.nnz
+        self._keep = []
+        ws = torch.empty(nsd.nsd_build_workspace_size(self.nnz, max(max(self.dims), 1)),
+                         dtype=torch.uint8, device=device)
+        n = max(self.nnz, 1)
+        for m in range(N):
+            segptr = torch.empty(self.dims[m] + 1, dtype=torch.int32, device=device)
+            segidx = torch.empty(n, dtype=torch.int32, device=device)
+            perm = torch.empty(n, dtype=torch.int32, device=device)
+            nsd.nsd_coo_mode_index(self.nnz, self.dims[m], coords[m], segptr, segidx, perm, ws,
+                                   stream)
+            others = []
+            for o in range(N - 1):
+                t = torch.empty(n, dtype=torch.int32, device=device)
+                nsd.nsd_gather_i32(self.nnz, perm, coords[(m + 1 + o) % N], t, stream)
+                others.append(t)
+            v = torch.empty(n, dtype=torch.float32, device=device)
+            nsd.nsd_gather_f32(self.nnz, perm, self.val, v, stream)
+            plan = build_plan(self.dims[m], self.nnz, segptr, self.item_len, device, stream)
+            md = self.desc.mode[m]
+            md.mode = m
+            md.segptr, md.segidx = segptr.data_ptr(), segidx.data_ptr()
+            for o, t in enumerate(others):
+                md.idx[o] = t.data_ptr()
+            md.val, md.perm = v.data_ptr(), perm.data_ptr()
+            md.plan = plan
+            self._keep += [segptr, segidx, perm, v, plan] + others
+
+    def workspace(self, rank: int):
+        n = nsd.nsd_cpn_workspace_size(self.desc, rank)
+        return torch.empty(max(n, 256), dtype=torch.uint8, device=self.val.device)
+
+
 class DeviceTtv:
     """The TTV projection of a COO 3-tensor onto its (i, j) keys, built by
     nsd_ttv_build, with work plans over the keys and over l."""

@@ -20,6 +20,9 @@ every workload is synthetic, at the shapes below:
         three 10,000 x 32 factors ~ N(0, 0.1^2).
   gnn   2,400,000-node power-law graph, 60M edges (out-degree Zipf profile
         s=1.05), weights U[0,1); H and G 2,400,000 x 256 ~ N(0,1).
+  cp4   1,000^4 COO 4-tensor, 20M distinct uniform coordinates, values
+        N(0,1); four 1,000 x 32 factors ~ N(0, 0.1^2) (the CP workload at
+        order 4).
   batax 100,000 x 100,000 CSR, 1M entries at uniform random positions
         (multinomial row lengths, distinct uniform columns), values N(0,1),
         beta = 1.5 (the Jacobian beta A^T A of Example 5's kernel).
@@ -52,7 +55,7 @@ VERBOSE = False  # progress lines on stderr for the multi-minute workloads
 def _say(msg):
     if VERBOSE:
         print(f"[synth {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
-WORKLOAD_IDS = {"spmv": 1, "spmm": 2, "mf": 3, "cp": 4, "gnn": 5, "batax": 6}
+WORKLOAD_IDS = {"spmv": 1, "spmm": 2, "mf": 3, "cp": 4, "gnn": 5, "batax": 6, "cp4": 7}
 
 # Full-size workloads and smaller variants of the same recipes that the
 # oracle finishes in seconds (they still span many tiles and ragged tails).
@@ -77,6 +80,10 @@ PRESETS = {
     "batax": {
         "full": dict(n=100_000, nnz=1_000_000, beta=1.5),
         "small": dict(n=2000, nnz=20_000, beta=1.5),
+    },
+    "cp4": {
+        "full": dict(dims=(1000, 1000, 1000, 1000), nnz=20_000_000, rank=32),
+        "small": dict(dims=(24, 20, 16, 30), nnz=30_000, rank=32),
     },
 }
 
@@ -327,8 +334,37 @@ def make_batax(n=100_000, nnz=1_000_000, beta=1.5, replicate=0):
                 val=_normal(g_val, nnz), x=_normal(g_d1, n), beta=beta)
 
 
+def make_cpn(dims, nnz, rank, workload="cp4", replicate=0):
+    """An order-N tensor with distinct uniform coordinates (first occurrence
+    of uniform draws), values N(0,1), factors N(0, 0.1^2); the order-N form of
+    the CP workload."""
+    g_pat, g_val, g_d1, g_d2, _ = streams(workload, replicate)
+    dims = tuple(int(x) for x in dims)
+    draws = nnz + nnz // 20 + 64
+
+    def draw():
+        key = np.zeros(draws, dtype=np.int64)
+        for d in dims:
+            key = key * d + g_pat.integers(0, d, size=draws, dtype=np.int64)
+        return key
+
+    keys = _dedupe_first(draw, nnz)
+    coords = []
+    for d in reversed(dims):
+        coords.append((keys % d).astype(np.int32))
+        keys = keys // d
+    coords = coords[::-1]
+    F = [_normal(g_d1 if n % 2 == 0 else g_d2, (d, rank), 0.1) for n, d in enumerate(dims)]
+    return dict(workload=workload, dims=dims, coords=coords, val=_normal(g_val, nnz), F=F,
+                rank=rank)
+
+
+def make_cp4(dims=(1000, 1000, 1000, 1000), nnz=20_000_000, rank=32, replicate=0):
+    return make_cpn(dims, nnz, rank, "cp4", replicate)
+
+
 MAKERS = {"spmv": make_spmv, "spmm": make_spmm, "mf": make_mf, "cp": make_cp,
-          "gnn": make_gnn, "batax": make_batax}
+          "gnn": make_gnn, "batax": make_batax, "cp4": make_cp4}
 
 
 def make(workload: str, size: str = "full", replicate: int = 0, **over):

@@ -718,3 +718,70 @@ def test_spmm_jvp_full_workload(nsd, operand, orc):
     C, Cm, dC, dCm = orc.spmm_jvp(D, dD, d["B"], dB, k)
     assert_mag_close(Cg, C, Cm, what="C")
     assert_mag_close(dCg, dC, dCm, what="dC")
+
+
+# --------------------------------------------------- order-N CP gradient
+
+def run_cpn(nsd, X, F, rank, seed=1.0):
+    loss = torch.empty(1, dtype=torch.float64, device="cuda")
+    dX = torch.full((max(X.nnz, 1),), np.nan, dtype=torch.float32, device="cuda")
+    dF = [torch.full((d, rank), np.nan, dtype=torch.float32, device="cuda") for d in X.dims]
+    nsd.nsd_loss_cpn(X.desc, [dev(f) for f in F], rank, seed, loss, dX, dF, X.workspace(rank))
+    return host(loss)[0], host(dX)[: X.nnz], [host(t) for t in dF]
+
+
+def check_cpn(orc, dims, coords, val, F, rank, got, seed=1.0):
+    D = orc.Dok(dims, coords, val)
+    L, Lm = orc.cpn_loss(D, F, rank)
+    R, Rm = orc.cpn_resid(D, F, rank, coords)
+    Lg, dXg, dFg = got
+    assert_mag_close(Lg, L, Lm, what="loss")
+    assert_mag_close(dXg, seed * R, abs(seed) * Rm, what="residual")
+    for m in range(len(dims)):
+        g, gm = orc.cpn_grad(D, F, rank, m)
+        assert_mag_close(dFg[m], seed * g, abs(seed) * gm, what=f"dF{m + 1}")
+
+
+def test_loss_cpn_small_order4_workload(nsd, orc):
+    from paper_2303_07030_amd import synth
+    from paper_2303_07030_amd.operand import DeviceCooN
+    d = synth.make("cp4", "small")
+    X = DeviceCooN(d["dims"], d["coords"], d["val"], rank_hint=d["rank"])
+    got = run_cpn(nsd, X, d["F"], d["rank"])
+    check_cpn(orc, d["dims"], d["coords"], d["val"], d["F"], d["rank"], got)
+
+
+@pytest.mark.parametrize("dims,rank", [((9, 7, 5), 12), ((6, 5, 4, 7, 3), 8),
+                                       ((4, 3, 5, 2, 3, 4), 5), ((40, 3, 2, 50), 64),
+                                       ((30, 2, 2, 2), 256)])
+def test_loss_cpn_orders_and_ranks(nsd, orc, dims, rank):
+    # skewed and tiny modes (long slices, chunked), scalar ranks (5), wide
+    # ranks (256: a full wave per slot), empty slices
+    from paper_2303_07030_amd.operand import DeviceCooN
+    rng = np.random.default_rng(len(dims) * 100 + rank)
+    size = int(np.prod(dims))
+    nnz = min(size // 2, 4000)
+    keys = rng.choice(size, size=nnz, replace=False)
+    coords = [c.astype(np.int32) for c in np.unravel_index(keys, dims)]
+    val = rng.standard_normal(nnz).astype(np.float32)
+    F = [(0.3 * rng.standard_normal((dd, rank))).astype(np.float32) for dd in dims]
+    X = DeviceCooN(dims, coords, val, rank_hint=rank, item_len=16)
+    got = run_cpn(nsd, X, F, rank, seed=0.5)
+    check_cpn(orc, dims, coords, val, F, rank, got, seed=0.5)
+
+
+def test_loss_cpn_order3_equals_cp(nsd, orc):
+    """The order-N path on an order-3 tensor gives the order-3 path's bits
+    where both use the same plans (same summation orders)."""
+    from paper_2303_07030_amd import synth
+    from paper_2303_07030_amd.operand import DeviceCoo3, DeviceCooN
+    d = synth.make("cp", "small")
+    F = [d["F1"], d["F2"], d["F3"]]
+    X3 = DeviceCoo3(d["dims"], d["i"], d["j"], d["k"], d["val"], rank_hint=d["rank"])
+    XN = DeviceCooN(d["dims"], [d["i"], d["j"], d["k"]], d["val"], rank_hint=d["rank"])
+    a = run_cp(nsd, X3, F, d["rank"])
+    b = run_cpn(nsd, XN, F, d["rank"])
+    check_cpn(orc, d["dims"], [d["i"], d["j"], d["k"]], d["val"], F, d["rank"], b)
+    assert np.array_equal(a[1], b[1])
+    for x, y in zip(a[2], b[2]):
+        assert np.array_equal(x, y)
