@@ -201,3 +201,37 @@ def test_cp_full_workload(nsd, orc):
 
     L, Lm = chunked_loss(orc, len(val), part)
     assert_mag_close(Lg, L, Lm, what="loss")
+
+
+# ------------------------------------------------ order-4 CP decomposition
+
+def test_cp4_full_workload(nsd, orc):
+    from paper_2303_07030_amd import synth
+    from paper_2303_07030_amd.operand import DeviceCooN
+    d = synth.make("cp4")
+    dims, R, coords, val, F = d["dims"], d["rank"], d["coords"], d["val"], d["F"]
+    X = DeviceCooN(dims, coords, val, rank_hint=R)
+    loss = torch.empty(1, dtype=torch.float64, device="cuda")
+    dX = torch.empty(X.nnz, dtype=torch.float32, device="cuda")
+    dF = [torch.empty((dd, R), dtype=torch.float32, device="cuda") for dd in dims]
+    nsd.nsd_loss_cpn(X.desc, [dev(f) for f in F], R, 1.0, loss, dX, dF, X.workspace(R))
+    Lg, dXg, dFg = host(loss)[0], host(dX), [host(t) for t in dF]
+    del X, dX, dF
+    rng = np.random.default_rng(8)
+    P = rng.choice(len(val), 8192, replace=False)
+    D = orc.Dok(dims, [c[P] for c in coords], val[P])
+    ref, mag = orc.cpn_resid(D, F, R, [c[P] for c in coords])
+    assert_mag_close(dXg[P], ref, mag, what="residual (sampled)")
+    for m in range(len(dims)):
+        S = np.unique(rng.choice(dims[m], 3, replace=False))
+        sel = np.isin(coords[m], S)
+        D = orc.Dok(dims, [c[sel] for c in coords], val[sel])
+        ref, mag = orc.cpn_grad(D, F, R, m, sel=S.astype(np.int32))
+        assert_mag_close(dFg[m][S], ref, mag, what=f"dF{m + 1} (sampled slices)")
+
+    def part(b, e):
+        D = orc.Dok(dims, [c[b:e] for c in coords], val[b:e])
+        return orc.cpn_loss(D, F, R)
+
+    L, Lm = chunked_loss(orc, len(val), part)
+    assert_mag_close(Lg, L, Lm, what="loss")
