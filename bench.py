@@ -52,6 +52,9 @@ def parse():
     ap.add_argument("--workload", default="spmm", choices=list(WORKLOAD_NAMES))
     ap.add_argument("--size", default="full")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cold-steps", type=int, default=10,
+                    help="steps timed one by one after writing a 512 MiB buffer (no cached "
+                         "operand left in L2 or the 256 MB MALL); 0 to skip")
     ap.add_argument("--item-len", type=int, default=None,
                     help="work-plan item length (default: the library's choice)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
@@ -438,6 +441,8 @@ def main():
                    "GBps": None if not v else round(S.kernels[n] / (v * 1e-3) / 1e9, 1)}
                for n, v in per_kernel.items()}
 
+    cold = cold_steps(torch, dev, S, args) if args.cold_steps else None
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(args, d)
@@ -462,10 +467,31 @@ def main():
         "roofline": roofline,
         "kernels": kernels,
         "preprocess_ms": round(prep_ms, 2), "generate_s": round(gen_s, 1),
+        "cold": cold,
         "cpu_baseline": cpu,
         "source_digest": source_digest(),
     }
     print(json.dumps(out))
+
+
+def cold_steps(torch, dev, S, args):
+    """Steps with cold caches: before each, a 512 MiB buffer is rewritten
+    (untimed), then the step alone is timed between HIP events."""
+    flush = torch.empty(128 << 20, dtype=torch.float32, device=dev)
+    times = []
+    for _ in range(args.cold_steps):
+        flush.fill_(1.0)
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        S.step()
+        b.record()
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(b))
+    del flush
+    ms = float(np.median(times))
+    return {"ms_per_step": round(ms, 5), "value": round(S.nnz / (ms * 1e-3), 1),
+            "steps": args.cold_steps, "note": "median step after a 512 MiB cache flush"}
 
 
 # ------------------------------------------------------------ CPU baseline
