@@ -1,0 +1,235 @@
+"""Pins for the reference interpreter of Logical SDQLite (oracle/sdql.py).
+
+Its values are tied to numpy (dot and matrix products, Examples 1 and 2 and
+the matrix product of Section 3), to the semi-ring dictionary laws of
+Section 2 (absent keys read as zero, insertion adds), and to the fp64 C
+oracle's losses; its forward-mode gradients are tied to closed forms and to
+central finite differences, which share nothing with the dual numbers.
+"""
+import numpy as np
+import pytest
+
+from oracle import sdql as ref
+
+
+def rand_csr(rng, nr, nc, nnz, empty_row=None):
+    cells = np.arange(nr * nc)
+    if empty_row is not None:
+        cells = cells[cells // nc != empty_row]
+    keys = np.sort(rng.choice(cells, size=nnz, replace=False))
+    row, col = keys // nc, keys % nc
+    rowptr = np.zeros(nr + 1, dtype=np.int64)
+    np.add.at(rowptr, row + 1, 1)
+    val = rng.standard_normal(nnz).astype(np.float32).astype(np.float64)
+    return np.cumsum(rowptr), col, val
+
+
+def dense(nr, nc, rowptr, colind, val):
+    D = np.zeros((nr, nc))
+    for i in range(nr):
+        D[i, colind[rowptr[i]:rowptr[i + 1]]] = val[rowptr[i]:rowptr[i + 1]]
+    return D
+
+
+# ----------------------------------------------------------------- syntax
+
+
+@pytest.mark.parametrize("text,want", [
+    ("1 + 2 * 3", 7),
+    ("(1 + 2) * 3", 9),
+    ("-2 * 3 + 1", -5),
+    ("let x = 2 in let y = x * x in y + x", 6),
+    ("let x = 2 in (let x = 5 in x) + x", 7),
+    ("if 1 = 1 then 4", 4),
+    ("if not (1 = 1) then 4 + 0", ref.ZERO),
+    ("{3 -> 2.5}(3)", 2.5),
+])
+def test_expressions(text, want):
+    assert ref.evaluate(text, {}) == want
+
+
+def test_sum_body_extends_to_the_right():
+    V = {0: 1.0, 3: 2.0}
+    assert ref.evaluate("2 * sum(<i,a> in V) a + 1", {"V": V}) == 2 * ((1 + 1) + (2 + 1))
+
+
+# ------------------------------------------------------ dictionary semantics
+
+
+def test_absent_key_reads_zero_and_is_the_identity():
+    V = {0: 1.0, 3: 2.0}
+    assert ref.evaluate("V(1)", {"V": V}) is ref.ZERO
+    assert ref.evaluate("V(1) + 4", {"V": V}) == 4
+    assert ref.evaluate("V(1) * 4", {"V": V}) is ref.ZERO
+    assert ref.evaluate("{} + V", {"V": V}) == V
+    assert ref.evaluate("sum(<i,a> in W) a", {"W": {}}) is ref.ZERO
+
+
+def test_insertion_adds_values_of_equal_keys():
+    V = {0: 1.0, 3: 2.0, 5: 4.0}
+    assert ref.evaluate("sum(<i,a> in V) {0 -> a}", {"V": V}) == {0: 7.0}
+
+
+def test_map_over_values():
+    V = {0: 1.0, 3: 2.0}
+    assert ref.evaluate("sum(<k,v> in V) {k -> 2 * v}", {"V": V}) == {0: 2.0, 3: 4.0}
+
+
+def test_scalar_vector_product_is_scaling():
+    # Example 2: s * V
+    v = np.array([1.0, -2.0, 0.5])
+    out = ref.evaluate("s * V", {"s": 3.0, "V": ref.dense_dict(v)})
+    np.testing.assert_array_equal(ref.to_array(out, (3,)), 3 * v)
+
+
+def test_outer_product_of_vectors():
+    a, b = np.array([1.0, 2.0]), np.array([3.0, -1.0, 5.0])
+    out = ref.evaluate("a * b", {"a": ref.dense_dict(a), "b": ref.dense_dict(b)})
+    np.testing.assert_array_equal(ref.to_array(out, (2, 3)), np.outer(a, b))
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_dot_product_both_variants(seed):
+    # Example 1: iterate either vector; a sparse V1 stores a subset of keys
+    rng = np.random.default_rng(seed)
+    v1 = rng.standard_normal(9)
+    keep = rng.random(9) < 0.5
+    v2 = rng.standard_normal(9)
+    V1 = {i: float(v1[i]) for i in range(9) if keep[i]}
+    env = {"V1": V1, "V2": ref.dense_dict(v2)}
+    want = float(np.dot(np.where(keep, v1, 0.0), v2))
+    assert ref.evaluate("sum(<i, a> in V1) a * V2(i)", env) == pytest.approx(want, rel=1e-14)
+    assert ref.evaluate("sum(<i, a> in V2) V1(i) * a", env) == pytest.approx(want, rel=1e-14)
+
+
+MATMUL = ("sum(<i,row> in M1) { i -> sum(<j, v1> in row) sum(<k, v2> in M2(j)) "
+          "{ k -> v1 * v2 } }")
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_matrix_product(seed):
+    # the matrix product of Section 3, with a sparse M1 that has an empty row
+    rng = np.random.default_rng(seed)
+    rowptr, colind, val = rand_csr(rng, 5, 4, 9, empty_row=2)
+    B = rng.standard_normal((4, 3))
+    out = ref.evaluate(MATMUL, {"M1": ref.csr_dict(rowptr, colind, val),
+                                "M2": ref.dense_dict(B)})
+    assert 2 not in out                      # no stored row, no key
+    np.testing.assert_allclose(ref.to_array(out, (5, 3)), dense(5, 4, rowptr, colind, val) @ B,
+                               rtol=1e-13, atol=1e-14)
+
+
+# ---------------------------------------------------- against the C oracle
+
+
+SMVM = "sum(<i,r> in A) sum(<j,a> in r) a * x(j)"
+FROB = ("let C = sum(<i,row> in A) { i -> sum(<j,a> in row) sum(<c,b> in B(j)) { c -> a * b } }"
+        " in 0.5 * sum(<i,r> in C) sum(<c,v> in r) v * v")
+GNN = "sum(<i,r> in A) sum(<j,a> in r) sum(<c,h> in H(j)) a * h * G(i)(c)"
+MF = ("let R = sum(<i,r> in A) {i -> sum(<j,a> in r) {j -> a + -1 * sum(<c,u> in U(i)) "
+      "u * V(j)(c)}} in sum(<i,r> in R) sum(<j,v> in r) v * v")
+
+
+def test_losses_agree_with_the_c_oracle(orc):
+    rng = np.random.default_rng(4)
+    nr, nc, k = 7, 6, 3
+    rowptr, colind, val = rand_csr(rng, nr, nc, 15, empty_row=3)
+    A = orc.Dok.from_csr(nr, nc, rowptr, colind, val.astype(np.float32))
+    Ad = ref.csr_dict(rowptr, colind, val)
+    x = rng.standard_normal(nc)
+    B, H = rng.standard_normal((nc, k)), rng.standard_normal((nc, k))
+    G, U = rng.standard_normal((nr, k)), rng.standard_normal((nr, k))
+    V = rng.standard_normal((nc, k))
+    dd = ref.dense_dict
+    got = ref.value(SMVM, {"A": Ad, "x": dd(x)})
+    assert got == pytest.approx(orc.loss_sum_spmv(A, x)[0], rel=1e-12)
+    C, Cmag = orc.spmm(A, B, k)
+    got = ref.value(FROB, {"A": Ad, "B": dd(B)})
+    assert got == pytest.approx(orc.loss_half_sq(C, Cmag)[0], rel=1e-12)
+    got = ref.value(GNN, {"A": Ad, "H": dd(H), "G": dd(G)})
+    assert got == pytest.approx(orc.loss_bilinear(A, G, H, k)[0], rel=1e-12)
+    got = ref.value(MF, {"A": Ad, "U": dd(U), "V": dd(V)})
+    assert got == pytest.approx(orc.mf_loss(A, U, V, k)[0], rel=1e-12)
+
+
+# -------------------------------------------------------------- gradients
+
+
+def test_dot_product_gradient_is_the_other_vector():
+    # Example 1 (cont.): d(V1 . V2)/dV2 = V1 on V2's keys
+    v1, v2 = np.array([1.0, 0.0, -2.0, 4.0]), np.array([3.0, 1.0, 2.0, -1.0])
+    env = {"V1": {0: 1.0, 2: -2.0, 3: 4.0}, "V2": ref.dense_dict(v2)}
+    g = ref.gradient("sum(<i, a> in V1) a * V2(i)", env, "V2")
+    assert g == {(0,): 1.0, (1,): 0.0, (2,): -2.0, (3,): 4.0}
+    g = ref.gradient("sum(<i, a> in V1) a * V2(i)", env, "V1")
+    assert g == {(0,): 3.0, (2,): 2.0, (3,): -1.0}
+
+
+def test_trace_gradient_is_one_on_the_diagonal():
+    # Example 3: d trace(M)/dM is 1 on the stored diagonal keys, 0 elsewhere
+    M = {0: {0: 2.0, 2: 1.0}, 1: {0: 5.0}, 2: {2: -1.0, 1: 3.0}}
+    g = ref.gradient("sum(<i,r> in M) r(i)", {"M": M}, "M")
+    assert g == {(0, 0): 1.0, (0, 2): 0.0, (1, 0): 0.0, (2, 1): 0.0, (2, 2): 1.0}
+
+
+def test_gradients_closed_forms():
+    rng = np.random.default_rng(7)
+    nr, nc, k = 6, 5, 3
+    rowptr, colind, val = rand_csr(rng, nr, nc, 12, empty_row=1)
+    D = dense(nr, nc, rowptr, colind, val)
+    mask = dense(nr, nc, rowptr, colind, np.ones_like(val)) > 0
+    Ad = ref.csr_dict(rowptr, colind, val)
+    x, B = rng.standard_normal(nc), rng.standard_normal((nc, k))
+    U, V = rng.standard_normal((nr, k)), rng.standard_normal((nc, k))
+
+    def at_keys(g, shape):
+        out = np.full(shape, np.nan)
+        for key, v in g.items():
+            out[key] = v
+        return out
+
+    env = {"A": Ad, "x": ref.dense_dict(x)}
+    gA = at_keys(ref.gradient(SMVM, env, "A"), (nr, nc))
+    np.testing.assert_allclose(gA[mask], np.broadcast_to(x, (nr, nc))[mask], rtol=1e-14)
+    np.testing.assert_allclose(at_keys(ref.gradient(SMVM, env, "x"), (nc,)), D.sum(0),
+                               rtol=1e-13, atol=1e-15)
+    env = {"A": Ad, "B": ref.dense_dict(B)}
+    C = D @ B
+    np.testing.assert_allclose(at_keys(ref.gradient(FROB, env, "B"), (nc, k)), D.T @ C,
+                               rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(at_keys(ref.gradient(FROB, env, "A"), (nr, nc))[mask],
+                               (C @ B.T)[mask], rtol=1e-12, atol=1e-13)
+    env = {"A": Ad, "U": ref.dense_dict(U), "V": ref.dense_dict(V)}
+    R = np.where(mask, D - U @ V.T, 0.0)
+    np.testing.assert_allclose(at_keys(ref.gradient(MF, env, "U"), (nr, k)), -2 * R @ V,
+                               rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(at_keys(ref.gradient(MF, env, "V"), (nc, k)), -2 * R.T @ U,
+                               rtol=1e-12, atol=1e-13)
+
+
+NONLINEAR = [
+    "sum(<i,a> in V) exp(a) * a",
+    "sum(<i,a> in V) sin(a * W(i)) + W(i) * W(i) * a",
+    "let s = sum(<i,a> in V) a * a in s * s + sum(<j,b> in W) cos(b) * s",
+    "sum(<i,r> in M) sum(<j,a> in r) let t = a * V(j) in sqrt(t * t + 1)",
+]
+
+
+@pytest.mark.parametrize("text", NONLINEAR)
+def test_gradients_match_central_differences(text):
+    rng = np.random.default_rng(11)
+    v, w = rng.standard_normal(4), rng.standard_normal(4)
+    M = {0: {1: 0.5, 3: -1.2}, 2: {0: 2.0}, 3: {2: 0.7, 3: 0.1}}
+    env = {"V": ref.dense_dict(v), "W": ref.dense_dict(w), "M": M}
+    h = 1e-5
+    for wrt in ("V", "W", "M"):
+        g = ref.gradient(text, env, wrt)
+        for key, got in g.items():
+            def shifted(dx):
+                e2 = dict(env)
+                src = env[wrt]
+                e2[wrt] = ref._replace_leaves(src, lambda kk, val: val + dx if kk == key else val)
+                return ref.value(text, e2)
+
+            fd = (shifted(h) - shifted(-h)) / (2 * h)
+            assert got == pytest.approx(fd, rel=1e-6, abs=1e-8), (wrt, key)
