@@ -426,6 +426,26 @@ nsd_status nsd_ttv(const nsd_ttv_plan *T, const float *x, const float *v, float 
 nsd_status nsd_ttv_vjp(const nsd_ttv_plan *T, const float *x, const float *v, const float *gy,
                        float *dx, float *dv, void *ws, size_t ws_bytes, void *stream);
 
+/*
+ * *out = alpha * sum_{i < n} x[i] * y[i] (y NULL: ones), accumulated in fp64
+ * in a fixed order, plus the previous *out when `accumulate` is nonzero: the
+ * full contraction of two dense tensors, or of a sparse operand's values with
+ * a sampled product on its keys (the scalar `sum` of Logical SDQLite,
+ * Section 3).  `out` is one device double.  Workspace: 16 KiB suffice (one
+ * double per block, at most 2048 blocks).  Async.
+ */
+nsd_status nsd_dot(int64_t n, const float *x, const float *y, double alpha, int accumulate,
+                   double *out, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * y = alpha * x + beta * y over n elements (x NULL: ones; beta == 0: y is
+ * overwritten without being read): the sum and scalar product of tensors
+ * that share one layout (Logical SDQLite `+` and real `*`, Section 3).
+ * Async.
+ */
+nsd_status nsd_axpby(int64_t n, float alpha, const float *x, float beta, float *y,
+                     void *stream);
+
 /* ---------------------------------------------------------------------------
  * Order-N sparse tensors and the CP gradient for orders 3 to NSD_MAX_ORDER
  * (the order-N form of the nested-dictionary tensor of Section 3).

@@ -333,6 +333,25 @@ nsd_status nsd_loss_bilinear(const nsd_csr *A, const nsd_csc *At, const float *H
     return segreduce(cols_params(A, At, G, k, seed, dH, w.part_col), st);
 }
 
+nsd_status nsd_dot(int64_t n, const float *x, const float *y, double alpha, int accumulate,
+                   double *out, void *ws, size_t ws_bytes, void *stream) {
+    NSD_REQUIRE(n >= 0, "negative length");
+    NSD_REQUIRE(out != nullptr, "out is NULL");
+    NSD_REQUIRE(n == 0 || x != nullptr, "x is NULL");
+    const size_t need = dot_blocks(n) * sizeof(double);
+    if (ws == nullptr || ws_bytes < need)
+        return fail(NSD_ERR_WORKSPACE, "workspace %zu bytes at %p, need %zu", ws_bytes, ws, need);
+    return dot(n, x, y, alpha, accumulate != 0, static_cast<double *>(ws), out,
+               as_stream(stream));
+}
+
+nsd_status nsd_axpby(int64_t n, float alpha, const float *x, float beta, float *y,
+                     void *stream) {
+    NSD_REQUIRE(n >= 0, "negative length");
+    NSD_REQUIRE(n == 0 || y != nullptr, "y is NULL");
+    return axpby(n, alpha, x, beta, y, as_stream(stream));
+}
+
 nsd_status nsd_loss_mf(const nsd_csr *A, const nsd_csc *At, const float *valT, const float *U,
                        const float *V, int32_t k, float seed, double *loss, float *dU, float *dV,
                        void *ws, size_t ws_bytes, void *stream) {

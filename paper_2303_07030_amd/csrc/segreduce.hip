@@ -227,6 +227,56 @@ __global__ __launch_bounds__(kBlock) void loss_finalize_kernel(const double *par
     loss_total_block(job);
 }
 
+// Block partials of alpha * sum_i x_i * y_i (y NULL: ones) in fp64: block b
+// sums elements b*kDotChunk .. in a fixed strided order.
+constexpr int kDotItems = 8;
+constexpr int64_t kDotChunk = (int64_t)kBlock * kDotItems;
+
+__global__ __launch_bounds__(kBlock) void dot_kernel(int64_t n, const float *x, const float *y,
+                                                     double alpha, int64_t per_block,
+                                                     double *part) {
+    double s = 0.0;
+    const int64_t lo = (int64_t)blockIdx.x * per_block;
+    const int64_t hi = min(n, lo + per_block);
+    for (int64_t i = lo + threadIdx.x; i < hi; i += kBlock)
+        s += y ? (double)x[i] * (double)y[i] : (double)x[i];
+    const double t = block_sum(s);
+    if (threadIdx.x == 0) part[blockIdx.x] = alpha * t;
+}
+
+int64_t dot_blocks(int64_t n) {
+    return std::max<int64_t>(1, std::min<int64_t>(ceil_div(n, kDotChunk), 2048));
+}
+
+nsd_status dot(int64_t n, const float *x, const float *y, double alpha, bool accumulate,
+               double *part, double *out, hipStream_t st) {
+    const int64_t nb = dot_blocks(n);
+    const int64_t per = ceil_div(std::max<int64_t>(n, 1), nb);
+    dot_kernel<<<(unsigned)nb, kBlock, 0, st>>>(n, x, y, alpha, per, part);
+    NSD_TRY(check_launch("dot_kernel"));
+    // accumulate: the old *out is a second partial (read before the one write)
+    loss_finalize_kernel<<<1, kBlock, 0, st>>>(part, nb, accumulate ? out : nullptr,
+                                               accumulate ? 1 : 0, out);
+    return check_launch("loss_finalize_kernel");
+}
+
+// y = alpha x + beta y (x NULL: ones; beta 0: y is not read).
+__global__ __launch_bounds__(kBlock) void axpby_kernel(int64_t n, float alpha, const float *x,
+                                                       float beta, float *y) {
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += stride) {
+        const float ax = alpha * (x ? x[i] : 1.f);
+        y[i] = beta == 0.f ? ax : ax + beta * y[i];
+    }
+}
+
+nsd_status axpby(int64_t n, float alpha, const float *x, float beta, float *y, hipStream_t st) {
+    if (n == 0) return NSD_OK;
+    const int64_t nb = std::min<int64_t>(ceil_div(n, kBlock), 8192);
+    axpby_kernel<<<(unsigned)nb, kBlock, 0, st>>>(n, alpha, x, beta, y);
+    return check_launch("axpby_kernel");
+}
+
 nsd_status loss_finalize(const double *part, int64_t n, double *loss, hipStream_t st) {
     probe_begin(NSD_KERNEL_LOSS, st);
     loss_finalize_kernel<<<1, kBlock, 0, st>>>(part, n, nullptr, 0, loss);

@@ -132,4 +132,13 @@ nsd_status sddmm(SddmmParams a, hipStream_t st);
 
 nsd_status loss_finalize(const double *part, int64_t n, double *loss, hipStream_t st);
 
+// *out = alpha * sum x_i y_i (y NULL: ones) in fp64, fixed order, plus the
+// old *out when accumulating; part holds dot_blocks(n) doubles.
+int64_t dot_blocks(int64_t n);
+nsd_status dot(int64_t n, const float *x, const float *y, double alpha, bool accumulate,
+               double *part, double *out, hipStream_t st);
+
+// y = alpha x + beta y elementwise (x NULL: ones; beta 0: y is not read).
+nsd_status axpby(int64_t n, float alpha, const float *x, float beta, float *y, hipStream_t st);
+
 }  // namespace nsd

@@ -139,6 +139,8 @@ _SIGS = {
     "nsd_ttv_workspace_size": (C.c_int, [_TTV, C.POINTER(_SZ)]),
     "nsd_ttv": (C.c_int, [_TTV, _P, _P, _P, _P, _SZ, _P]),
     "nsd_ttv_vjp": (C.c_int, [_TTV, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "nsd_dot": (C.c_int, [C.c_int64, _P, _P, C.c_double, C.c_int, _P, _P, _SZ, _P]),
+    "nsd_axpby": (C.c_int, [C.c_int64, C.c_float, _P, C.c_float, _P, _P]),
     "nsd_cpn_workspace_size": (C.c_int, [C.POINTER(nsd_coon), _I, C.POINTER(_SZ)]),
     "nsd_loss_cpn": (C.c_int, [C.POINTER(nsd_coon), C.POINTER(_P), _I, C.c_float, _P, _P,
                                C.POINTER(_P), _P, _SZ, _P]),
@@ -450,3 +452,12 @@ def nsd_loss_cpn(X: nsd_coon, F, rank, seed, loss, dX, dF, ws, stream=None):
     dp = (_P * len(dF))(*[_p(t) for t in dF])
     _check(_lib.nsd_loss_cpn(C.byref(X), fp, rank, seed, _p(loss), _p(dX), dp, _p(ws),
                              _nbytes(ws), _stream(stream)), "nsd_loss_cpn")
+
+
+def nsd_dot(n, x, y, alpha, accumulate, out, ws, stream=None):
+    _check(_lib.nsd_dot(n, _p(x), _p(y), alpha, int(bool(accumulate)), _p(out), _p(ws),
+                        _nbytes(ws), _stream(stream)), "nsd_dot")
+
+
+def nsd_axpby(n, alpha, x, beta, y, stream=None):
+    _check(_lib.nsd_axpby(n, alpha, _p(x), beta, _p(y), _stream(stream)), "nsd_axpby")

@@ -1,0 +1,1034 @@
+"""Front end: Logical SDQLite programs over one sparse matrix, differentiated
+and lowered to the library's kernels.
+
+Pipeline (Sections 3-5 of the paper, without equality saturation):
+  1. parse the program (the Logical SDQLite grammar of Section 3);
+  2. normalize it into sums of products of reals: every term is
+     "sum over index variables of coef * product of tensor entries", with
+     tensor-valued products expanded into explicit loops (the multiplication
+     normalization rules of Section 5) and the iteration domain of a sparse
+     loop kept as a mask (the stored keys it runs over);  `let`-bound tensors
+     stay named intermediates, and a `let` of a real inside loops becomes a
+     tensor over the loop indices it depends on (an ANF-style binding,
+     Section 5.1);
+  3. differentiate with the tensorized forward-mode rules (Section 4.2): the
+     tangent of a product is the sum over its factors (product rule), the
+     tangent of a lookup is the lookup of the tangent, a `let` binds its
+     tangent beside it, and the gradient API seeds the input of interest with
+     its one-hot tensor and every other input with zero (Section 4.3);
+  4. propagate sparsity: products with a zero tangent vanish, sums with zero
+     drop it, and equal terms merge (the first group of transformations of
+     Section 5.2);
+  5. lower each remaining term to one kernel of the library: SpMM / SpMV,
+     the transposed product, SDDMM on the matrix's pattern, a dense dot
+     product, or an axpby; the terms of one result accumulate in place.
+
+All arithmetic runs in the library's kernels; this module only builds and
+dispatches the calls.  Programs outside this class (two sparse iterations in
+one term, `if`, `op`, products of tensors laid out differently) raise
+`NotLowerable` with the reason.
+"""
+from __future__ import annotations
+
+import itertools
+import re
+from dataclasses import dataclass, field, replace
+
+# ------------------------------------------------------------------ errors
+
+
+class SdqlError(Exception):
+    """Malformed program (syntax, names, types or shapes)."""
+
+
+class NotLowerable(SdqlError):
+    """Well-formed program that the kernels here do not cover."""
+
+
+# ------------------------------------------------------------ declarations
+
+
+@dataclass(frozen=True)
+class Sparse:
+    """A sparse matrix input (CSR; its stored keys are the iteration domain)."""
+
+    nrows: int
+    ncols: int
+
+    @property
+    def shape(self):
+        return (self.nrows, self.ncols)
+
+
+@dataclass(frozen=True)
+class Dense:
+    """A dense input of order 1 or 2 (row-major)."""
+
+    shape: tuple
+
+    def __init__(self, *shape):
+        object.__setattr__(self, "shape", tuple(int(s) for s in shape))
+
+
+# ------------------------------------------------------------------ syntax
+
+
+@dataclass(frozen=True)
+class Num:
+    value: float
+
+
+@dataclass(frozen=True)
+class Name:
+    name: str
+
+
+@dataclass(frozen=True)
+class SumE:
+    key: str
+    val: str
+    src: object
+    body: object
+
+
+@dataclass(frozen=True)
+class Single:
+    key: object
+    val: object
+
+
+@dataclass(frozen=True)
+class EmptyE:
+    pass
+
+
+@dataclass(frozen=True)
+class Lookup:
+    dict: object
+    key: object
+
+
+@dataclass(frozen=True)
+class LetE:
+    name: str
+    bound: object
+    body: object
+
+
+@dataclass(frozen=True)
+class AddE:
+    left: object
+    right: object
+
+
+@dataclass(frozen=True)
+class MulE:
+    left: object
+    right: object
+
+
+@dataclass(frozen=True)
+class Other:
+    """`if`, `not`, `=`, `true`/`false` and real unary operations: parsed,
+    outside the sum-of-products class."""
+
+    what: str
+    args: tuple
+
+
+_LEX = re.compile(r"\s+|(?P<num>\d*\.\d+(?:[eE][-+]?\d+)?|\d+\.?(?:[eE][-+]?\d+)?)"
+                  r"|(?P<id>[A-Za-z_][\w']*)|(?P<op>->|[-+*=(){}<>,])")
+_RESERVED = ("sum", "in", "let", "if", "then", "not", "true", "false")
+_UNARY_OPS = ("exp", "log", "sin", "cos", "sqrt")
+
+
+def _lex(text):
+    toks, pos = [], 0
+    while pos < len(text):
+        m = _LEX.match(text, pos)
+        if m is None:
+            raise SdqlError(f"unexpected character {text[pos]!r} at offset {pos}")
+        pos = m.end()
+        if m.lastgroup == "num":
+            toks.append(("num", m.group("num")))
+        elif m.lastgroup == "id":
+            w = m.group("id")
+            toks.append((w if w in _RESERVED else "id", w))
+        elif m.lastgroup == "op":
+            toks.append((m.group("op"), m.group("op")))
+    toks.append(("eof", ""))
+    return toks
+
+
+class _Reader:
+    # Binding strength, loosest first: the greedy forms (sum, let, if),
+    # equality, +, *, prefix (not, unary minus), postfix lookup, atoms.
+    def __init__(self, text):
+        self.toks = _lex(text)
+        self.pos = 0
+
+    def kind(self, off=0):
+        return self.toks[self.pos + off][0]
+
+    def eat(self, kind):
+        k, v = self.toks[self.pos]
+        if k != kind:
+            raise SdqlError(f"expected {kind!r} but found {v or k!r} at token {self.pos}")
+        self.pos += 1
+        return v
+
+    def parse(self):
+        e = self.greedy()
+        self.eat("eof")
+        return e
+
+    def greedy(self):
+        k = self.kind()
+        if k == "sum":
+            self.eat("sum")
+            self.eat("(")
+            self.eat("<")
+            key = self.eat("id")
+            self.eat(",")
+            val = self.eat("id")
+            self.eat(">")
+            self.eat("in")
+            src = self.greedy()
+            self.eat(")")
+            return SumE(key, val, src, self.greedy())
+        if k == "let":
+            self.eat("let")
+            name = self.eat("id")
+            self.eat("=")
+            bound = self.greedy()
+            self.eat("in")
+            return LetE(name, bound, self.greedy())
+        if k == "if":
+            self.eat("if")
+            cond = self.greedy()
+            self.eat("then")
+            return Other("if", (cond, self.greedy()))
+        return self.equality()
+
+    def equality(self):
+        e = self.plus()
+        while self.kind() == "=":
+            self.eat("=")
+            e = Other("eq", (e, self.plus()))
+        return e
+
+    def plus(self):
+        e = self.times()
+        while self.kind() == "+":
+            self.eat("+")
+            e = AddE(e, self.times())
+        return e
+
+    def times(self):
+        e = self.prefix()
+        while self.kind() == "*":
+            self.eat("*")
+            e = MulE(e, self.prefix())
+        return e
+
+    def prefix(self):
+        k = self.kind()
+        if k in ("sum", "let", "if"):
+            return self.greedy()
+        if k == "not":
+            self.eat("not")
+            return Other("not", (self.prefix(),))
+        if k == "-":
+            self.eat("-")
+            return MulE(Num(-1.0), self.prefix())
+        return self.postfix()
+
+    def postfix(self):
+        e = self.atom()
+        while self.kind() == "(":
+            self.eat("(")
+            key = self.greedy()
+            self.eat(")")
+            e = Lookup(e, key)
+        return e
+
+    def atom(self):
+        k = self.kind()
+        if k == "num":
+            return Num(float(self.eat("num")))
+        if k in ("true", "false"):
+            self.eat(k)
+            return Other(k, ())
+        if k == "id":
+            name = self.eat("id")
+            if name in _UNARY_OPS and self.kind() == "(":
+                self.eat("(")
+                arg = self.greedy()
+                self.eat(")")
+                return Other(name, (arg,))
+            return Name(name)
+        if k == "(":
+            self.eat("(")
+            e = self.greedy()
+            self.eat(")")
+            return e
+        if k == "{":
+            self.eat("{")
+            if self.kind() == "}":
+                self.eat("}")
+                return EmptyE()
+            key = self.greedy()
+            self.eat("->")
+            val = self.greedy()
+            self.eat("}")
+            return Single(key, val)
+        raise SdqlError(f"unexpected {self.toks[self.pos][1] or k!r} at token {self.pos}")
+
+
+def parse(text: str):
+    """Syntax tree of a Logical SDQLite program."""
+    return _Reader(text).parse()
+
+
+# ----------------------------------------------------------- sum-of-products
+
+
+@dataclass(frozen=True)
+class Fac:
+    """Entry `tensor[idx]` of a named tensor, idx a tuple of index variables."""
+
+    tensor: str
+    idx: tuple
+
+
+@dataclass(frozen=True)
+class Term:
+    """coef * sum over `loops` of the product of `facs`, restricted to the
+    stored keys named by `masks`, as the entry at `keys` (output position p
+    is the index variable keys[p])."""
+
+    coef: float
+    keys: tuple
+    loops: frozenset
+    facs: tuple
+    masks: tuple = ()
+
+    def variables(self):
+        vs = set(self.keys) | set(self.loops)
+        for f in self.facs + self.masks:
+            vs.update(f.idx)
+        return vs
+
+    def rename(self, sub):
+        def r(v):
+            return sub.get(v, v)
+
+        return Term(self.coef, tuple(r(v) for v in self.keys),
+                    frozenset(r(v) for v in self.loops),
+                    tuple(Fac(f.tensor, tuple(r(v) for v in f.idx)) for f in self.facs),
+                    tuple(Fac(m.tensor, tuple(r(v) for v in m.idx)) for m in self.masks))
+
+
+@dataclass
+class Terms:
+    """A tensor of the given order as a sum of terms."""
+
+    order: int | None
+    terms: list
+
+
+@dataclass(frozen=True)
+class Access:
+    """A named tensor looked up at a prefix of its keys."""
+
+    tensor: str
+    idx: tuple
+
+
+@dataclass
+class TensorInfo:
+    name: str
+    kind: str            # "sparse" (input), "dense", "patterned" (on the sparse input's keys), "scalar"
+    shape: tuple
+    pattern: str | None = None
+    definition: Terms | None = None   # intermediates only
+    deps: tuple = ()                  # enclosing loop variables a hoisted let depends on
+
+    @property
+    def order(self):
+        return len(self.shape)
+
+    @property
+    def input(self):
+        return self.definition is None
+
+
+@dataclass
+class _Bind:
+    kind: str            # "index", "access", "terms"
+    value: object
+
+
+class Program:
+    """A compiled program: its value as terms, its intermediates, and the
+    gradients of the gradient API on request."""
+
+    def __init__(self, text: str, decls: dict):
+        self.text = text
+        self.tensors: dict[str, TensorInfo] = {}
+        self.extent: dict[str, int] = {}
+        self._counter = itertools.count()
+        self._tangents: dict = {}
+        sparse = [n for n, d in decls.items() if isinstance(d, Sparse)]
+        if len(sparse) > 1:
+            raise NotLowerable(f"one sparse matrix per program, got {sparse}")
+        for name, d in decls.items():
+            if isinstance(d, Sparse):
+                self.tensors[name] = TensorInfo(name, "sparse", d.shape, pattern=name)
+            elif isinstance(d, Dense):
+                if not 1 <= len(d.shape) <= 2:
+                    raise NotLowerable(f"dense input {name} must have order 1 or 2")
+                self.tensors[name] = TensorInfo(name, "dense", d.shape)
+            else:
+                raise SdqlError(f"declaration of {name} must be Sparse or Dense")
+        self.sparse = sparse[0] if sparse else None
+        self.inputs = dict(decls)
+        env = {n: _Bind("access", Access(n, ())) for n in decls}
+        self.value = self._as_terms(self._extract(parse(text), env, ()))
+        self.value.terms = _simplify(self.value.terms, self.tensors)
+
+    # -- naming
+    def _fresh(self, base):
+        return f"{base}#{next(self._counter)}"
+
+    def _set_extent(self, var, n, where):
+        old = self.extent.get(var)
+        if old is not None and old != n:
+            raise SdqlError(f"index {var.split('#')[0]} ranges over {old} and {n} ({where})")
+        self.extent[var] = n
+
+    def _is_sparse(self, tensor):
+        return self.tensors[tensor].kind in ("sparse", "patterned")
+
+    # -- step 2: normalization into sums of products
+    def _as_terms(self, x):
+        if isinstance(x, Terms):
+            return x
+        info = self.tensors[x.tensor]
+        rest = []
+        for pos in range(len(x.idx), info.order):
+            v = self._fresh("k")
+            self._set_extent(v, info.shape[pos], f"{x.tensor} at position {pos}")
+            rest.append(v)
+        idx = x.idx + tuple(rest)
+        masks = (Fac(info.pattern, idx),) if self._is_sparse(x.tensor) else ()
+        if info.kind == "scalar":
+            return Terms(0, [Term(1.0, (), frozenset(), (Fac(x.tensor, ()),))])
+        return Terms(len(rest), [Term(1.0, tuple(rest), frozenset(), (Fac(x.tensor, idx),),
+                                      masks)])
+
+    def _extract(self, e, env, loops):
+        """Access or Terms for expression e; `loops` lists the enclosing
+        sparse/dense iterations as (variable, tensor, prefix) triples."""
+        if isinstance(e, Num):
+            return Terms(0, [Term(float(e.value), (), frozenset(), ())])
+        if isinstance(e, Name):
+            b = env.get(e.name)
+            if b is None:
+                raise SdqlError(f"unbound name {e.name}")
+            if b.kind == "index":
+                raise NotLowerable(f"index {e.name} used as a real")
+            if b.kind == "access":
+                return b.value
+            return Terms(b.value.order, [_fresh_loops(t, self) for t in b.value.terms])
+        if isinstance(e, Lookup):
+            d = self._extract(e.dict, env, loops)
+            if not isinstance(d, Access):
+                raise NotLowerable("lookup into a computed expression; bind it with let first")
+            info = self.tensors[d.tensor]
+            if len(d.idx) >= info.order:
+                raise SdqlError(f"too many lookups into {d.tensor}")
+            var = self._index(e.key, env)
+            self._set_extent(var, info.shape[len(d.idx)], f"lookup into {d.tensor}")
+            return Access(d.tensor, d.idx + (var,))
+        if isinstance(e, Single):
+            var = self._index(e.key, env)
+            v = self._as_terms(self._extract(e.val, env, loops))
+            return Terms(v.order + 1 if v.order is not None else None,
+                         [replace(t, keys=(var,) + t.keys) for t in v.terms])
+        if isinstance(e, EmptyE):
+            return Terms(None, [])
+        if isinstance(e, AddE):
+            a = self._as_terms(self._extract(e.left, env, loops))
+            b = self._as_terms(self._extract(e.right, env, loops))
+            if a.order is not None and b.order is not None and a.order != b.order:
+                raise SdqlError(f"adding tensors of orders {a.order} and {b.order}")
+            return Terms(a.order if a.order is not None else b.order, a.terms + b.terms)
+        if isinstance(e, MulE):
+            a = self._as_terms(self._extract(e.left, env, loops))
+            b = self._as_terms(self._extract(e.right, env, loops))
+            out = []
+            for s in a.terms:
+                for t in b.terms:
+                    t = _fresh_loops(t, self)
+                    out.append(Term(s.coef * t.coef, s.keys + t.keys, s.loops | t.loops,
+                                    s.facs + t.facs, s.masks + t.masks))
+            order = None if a.order is None or b.order is None else a.order + b.order
+            return Terms(order, out)
+        if isinstance(e, SumE):
+            src = self._extract(e.src, env, loops)
+            if not isinstance(src, Access):
+                raise NotLowerable("sum over a computed expression; bind it with let first")
+            info = self.tensors[src.tensor]
+            level = len(src.idx)
+            if level >= info.order:
+                raise SdqlError(f"sum over a real ({src.tensor} fully looked up)")
+            var = self._fresh(e.key)
+            self._set_extent(var, info.shape[level], f"sum over {src.tensor}")
+            inner = dict(env)
+            inner[e.key] = _Bind("index", var)
+            inner[e.val] = _Bind("access", Access(src.tensor, src.idx + (var,)))
+            body = self._as_terms(self._extract(e.body, inner, loops + ((var, src),)))
+            mask = (Fac(info.pattern, src.idx + (var,)),) if self._is_sparse(src.tensor) else ()
+            out = [Term(t.coef, t.keys, t.loops if var in t.keys else t.loops | {var}, t.facs,
+                        t.masks + mask) for t in body.terms]
+            return Terms(body.order, out)
+        if isinstance(e, LetE):
+            bound = self._extract(e.bound, env, loops)
+            inner = dict(env)
+            if isinstance(bound, Access):
+                inner[e.name] = _Bind("access", bound)
+            elif all(not t.facs and not t.keys and not t.masks and not t.loops
+                     for t in bound.terms):
+                inner[e.name] = _Bind("terms", bound)      # a constant: substituted
+            else:
+                inner[e.name] = _Bind("access", self._hoist(e.name, bound, loops))
+            return self._extract(e.body, inner, loops)
+        if isinstance(e, Other):
+            raise NotLowerable(f"`{e.what}` is outside the sum-of-products class")
+        raise SdqlError(f"unknown expression {e!r}")
+
+    def _index(self, e, env):
+        if not isinstance(e, Name) or e.name not in env or env[e.name].kind != "index":
+            raise NotLowerable("dictionary keys and lookups must be loop indices")
+        return env[e.name].value
+
+    def _hoist(self, name, bound: Terms, loops):
+        """Named intermediate for `let name = bound`: a tensor over the
+        enclosing loop variables the bound expression uses, then its own keys."""
+        used = set()
+        for t in bound.terms:
+            used |= t.variables() - set(t.loops) - set(t.keys)
+        deps = tuple(v for v, _ in loops if v in used)
+        terms = []
+        for t in bound.terms:
+            masks = t.masks
+            # the domain of the enclosing sparse iteration, when the
+            # intermediate spans all of that iteration's keys
+            for v, src in loops:
+                info = self.tensors[src.tensor]
+                full = src.idx + (v,)
+                if (self._is_sparse(src.tensor) and len(full) == info.order
+                        and all(u in deps for u in full)):
+                    masks = masks + (Fac(info.pattern, full),)
+            terms.append(Term(t.coef, deps + t.keys, t.loops, t.facs, masks))
+        keys_order = len(deps) + (bound.order or 0)
+        inter = self._fresh(name).replace("#", "%")
+        shape = tuple(self.extent[v] for v in deps)
+        if bound.terms:
+            shape = shape + tuple(self.extent[v] for v in bound.terms[0].keys)
+        terms = _simplify(terms, self.tensors)
+        kind = "dense"
+        if keys_order == 0:
+            kind = "scalar"
+        elif self.sparse is not None and keys_order == 2 and terms and all(
+                any(m.tensor == self.sparse and m.idx == t.keys for m in t.masks)
+                for t in terms):
+            kind = "patterned"
+        self.tensors[inter] = TensorInfo(inter, kind, shape,
+                                         pattern=self.sparse if kind == "patterned" else None,
+                                         definition=Terms(keys_order, terms), deps=deps)
+        return Access(inter, deps)
+
+    # -- step 3: tensorized forward mode with the gradient API's seeds
+    def depends(self, tensor, x):
+        info = self.tensors[tensor]
+        if tensor == x:
+            return True
+        if info.input:
+            return False
+        return any(self.depends(f.tensor, x) for t in info.definition.terms for f in t.facs)
+
+    def tangent(self, T: Terms, x: str) -> Terms:
+        """Tangent of T when the input x is seeded with its one-hot tensor and
+        every other input with zero: a tensor of order T.order + order(x)."""
+        xinfo = self.tensors[x]
+        out = []
+        for t in T.terms:
+            for p, f in enumerate(t.facs):
+                rest = t.facs[:p] + t.facs[p + 1:]
+                if f.tensor == x:
+                    # x'(idx) is the one-hot tensor: 1 at the key idx, on x's
+                    # stored keys only
+                    masks = t.masks + ((Fac(xinfo.pattern, f.idx),)
+                                       if self._is_sparse(x) else ())
+                    out.append(Term(t.coef, t.keys + f.idx, t.loops - set(f.idx), rest, masks))
+                elif not self.tensors[f.tensor].input and self.depends(f.tensor, x):
+                    info = self.tensors[f.tensor]
+                    dT = self._tangent_of(f.tensor, x)
+                    for s in dT.terms:
+                        s = _fresh_all(s, self)
+                        sub = {}
+                        for kv, iv in zip(s.keys[:info.order], f.idx):
+                            if sub.get(kv, iv) != iv:
+                                raise NotLowerable(f"diagonal use of {info.name}")
+                            sub[kv] = iv
+                        s = s.rename(sub)
+                        gkeys = s.keys[info.order:]
+                        out.append(Term(t.coef * s.coef, t.keys + gkeys,
+                                        (t.loops | s.loops) - set(gkeys), rest + s.facs,
+                                        t.masks + s.masks))
+        order = None if T.order is None else T.order + xinfo.order
+        return Terms(order, _simplify(out, self.tensors))
+
+    def _tangent_of(self, tensor, x):
+        key = (tensor, x)
+        if key not in self._tangents:
+            self._tangents[key] = self.tangent(self.tensors[tensor].definition, x)
+        return self._tangents[key]
+
+    def gradient(self, x: str) -> Terms:
+        """`gradient e x` of the gradient API (Section 4.3): the program's
+        derivative w.r.t. input x, as terms over x's keys."""
+        if x not in self.inputs:
+            raise SdqlError(f"{x} is not an input")
+        return self.tangent(self.value, x)
+
+    # -- step 5: lowering
+    def plan(self, grads=(), value=True):
+        """Kernel calls computing the value (when asked) and the gradients."""
+        return _Lowering(self).run(value, tuple(grads))
+
+    def run(self, inputs: dict, grads=(), value=True, stream=None):
+        """Executes the plan on device tensors: inputs maps each sparse name
+        to a DeviceCsr and each dense name to a float32 tensor of its shape.
+        Returns {"value": ..., "d<name>": ...}."""
+        return self.plan(grads, value).execute(inputs, stream)
+
+
+def compile(text: str, **decls) -> Program:   # noqa: A001 - the natural name
+    """Compiles a program; decls give each input as Sparse(...) or Dense(...)."""
+    return Program(text, decls)
+
+
+def _renamed(t: Term, prog, vs) -> Term:
+    sub = {}
+    for v in sorted(vs):
+        sub[v] = prog._fresh(v.split("#")[0])
+        prog.extent[sub[v]] = prog.extent[v]
+    return t.rename(sub)
+
+
+def _fresh_loops(t: Term, prog) -> Term:
+    return _renamed(t, prog, t.loops)
+
+
+def _fresh_all(t: Term, prog) -> Term:
+    return _renamed(t, prog, t.variables())
+
+
+# -------------------------------------------------- step 4: simplification
+
+
+def _canonical(t: Term, tensors):
+    """Term with masks completed and deduplicated, and a hashable form with
+    its index variables renamed canonically, so that equal terms compare equal."""
+    masks = list(dict.fromkeys(t.masks))
+    for f in t.facs:   # a stored-keys-only factor is zero off its pattern
+        info = tensors.get(f.tensor)
+        if info and info.kind in ("sparse", "patterned") and len(f.idx) == info.order:
+            m = Fac(info.pattern, f.idx)
+            if m not in masks:
+                masks.append(m)
+    full = [m for m in masks if len(m.idx) == tensors[m.tensor].order]
+    masks = [m for m in masks if m in full or not any(
+        f.tensor == m.tensor and f.idx[:len(m.idx)] == m.idx for f in full)]
+    t = Term(t.coef, t.keys, t.loops, t.facs, tuple(masks))
+    names = {}
+    for v in t.keys:
+        names.setdefault(v, f"k{len(names)}")
+
+    def sig(f):
+        return (f.tensor, tuple(names.get(v, "?") for v in f.idx))
+
+    for _ in range(2):
+        for f in sorted(t.facs + t.masks, key=sig):
+            for v in f.idx:
+                names.setdefault(v, f"l{len(names)}")
+    for v in sorted(t.loops):
+        names.setdefault(v, f"l{len(names)}")
+    c = t.rename(names)
+    form = (c.keys, tuple(sorted(c.loops)), tuple(sorted((f.tensor, f.idx) for f in c.facs)),
+            tuple(sorted((m.tensor, m.idx) for m in c.masks)))
+    return t, form
+
+
+def _simplify(terms, tensors):
+    merged = {}
+    for t in terms:
+        if t.coef == 0.0:
+            continue
+        t, form = _canonical(t, tensors)
+        if form in merged:
+            old = merged[form]
+            merged[form] = replace(old, coef=old.coef + t.coef)
+        else:
+            merged[form] = t
+    return [t for t in merged.values() if t.coef != 0.0]
+
+
+# ------------------------------------------------------------------ lowering
+
+
+@dataclass
+class Buf:
+    """A device buffer of the plan: "input" (caller's), "out", "inter" or "temp"."""
+
+    name: str
+    role: str
+    layout: str          # "scalar" (one double), "pattern" (nnz floats), "dense"
+    shape: tuple = ()
+
+
+@dataclass
+class Call:
+    kernel: str
+    args: dict
+    out: str
+
+
+@dataclass
+class Plan:
+    prog: Program
+    bufs: dict = field(default_factory=dict)
+    calls: list = field(default_factory=list)
+    results: dict = field(default_factory=dict)
+
+    def kernels(self):
+        return [c.kernel for c in self.calls]
+
+    def execute(self, inputs: dict, stream=None):
+        return _execute(self, inputs, stream)
+
+
+class _Lowering:
+    def __init__(self, prog: Program):
+        self.p = prog
+        self.plan = Plan(prog)
+        self.done = set()
+        self.ntemp = itertools.count()
+
+    def run(self, value, grads):
+        p = self.p
+        for name, d in p.inputs.items():
+            if isinstance(d, Sparse):
+                self.plan.bufs[name] = Buf(name, "input", "pattern", d.shape)
+            else:
+                self.plan.bufs[name] = Buf(name, "input", "dense", d.shape)
+        if value:
+            self._result("value", p.value, p.value.order or 0, self._value_shape())
+        for x in grads:
+            g = p.gradient(x)
+            info = p.tensors[x]
+            layout = "pattern" if info.kind == "sparse" else "dense"
+            if p.value.order not in (0, None):
+                raise NotLowerable("gradients of tensor-valued programs")
+            self._result("d" + x, g, info.order, info.shape, layout)
+        return self.plan
+
+    def _value_shape(self):
+        ts = self.p.value.terms
+        if not ts or not ts[0].keys:
+            return ()
+        return tuple(self.p.extent[v] for v in ts[0].keys)
+
+    def _result(self, name, T, order, shape, layout=None):
+        if layout is None:
+            layout = "scalar" if order == 0 else "dense"
+        self.plan.bufs[name] = Buf(name, "out", layout, tuple(shape))
+        self._emit_terms(T, name)
+        self.plan.results[name] = name
+
+    def _need(self, tensor):
+        """Computes an intermediate (and what it needs) before its first use."""
+        info = self.p.tensors[tensor]
+        if info.input or tensor in self.done:
+            return
+        if info.kind == "scalar":
+            raise NotLowerable(f"the real {tensor.split('%')[0]} is used as a factor")
+        self.done.add(tensor)
+        layout = "pattern" if info.kind == "patterned" else "dense"
+        self.plan.bufs[tensor] = Buf(tensor, "inter", layout, info.shape)
+        self._emit_terms(info.definition, tensor)
+
+    def _temp(self, like: Buf):
+        name = f"tmp{next(self.ntemp)}"
+        self.plan.bufs[name] = Buf(name, "temp", like.layout, like.shape)
+        return name
+
+    def _emit_terms(self, T: Terms, out):
+        for t in T.terms:
+            for f in t.facs:
+                self._need(f.tensor)
+        if not T.terms:
+            self._zero(out)
+            return
+        for n, t in enumerate(T.terms):
+            self._emit_term(t, out, accumulate=n > 0)
+
+    def _zero(self, out):
+        b = self.plan.bufs[out]
+        if b.layout == "scalar":
+            self.plan.calls.append(Call("dot", dict(x=None, y=None, n=0, alpha=0.0,
+                                                    acc=False), out))
+        else:
+            self.plan.calls.append(Call("axpby", dict(alpha=0.0, x=None, beta=0.0), out))
+
+    def _emit_term(self, t: Term, out, accumulate):
+        p = self.p
+        ob = self.plan.bufs[out]
+        masks = [m for m in t.masks]
+        for m in masks:
+            if len(m.idx) != p.tensors[m.tensor].order:
+                raise NotLowerable("iteration over the rows of a sparse matrix without "
+                                   "their entries")
+        if len(set(masks)) > 1:
+            raise NotLowerable("two sparse iterations in one term")
+        for f in t.facs:
+            if p.tensors[f.tensor].kind == "scalar":
+                raise NotLowerable(f"the real {f.tensor.split('%')[0]} is used as a factor")
+        if masks:
+            self._emit_sparse(t, masks[0], out, ob, accumulate)
+        else:
+            self._emit_dense(t, out, ob, accumulate)
+
+    # terms over the sparse matrix's stored keys (r, c)
+    def _emit_sparse(self, t, mask, out, ob, accumulate):
+        p = self.p
+        r, c = mask.idx
+        if r == c:
+            raise NotLowerable("diagonal keys of the sparse matrix (row index = column index)")
+        W = [f for f in t.facs if p.tensors[f.tensor].kind in ("sparse", "patterned")]
+        D = [f for f in t.facs if p.tensors[f.tensor].kind == "dense"]
+        for f in W:
+            if f.idx != (r, c):
+                raise NotLowerable(f"{f.tensor} is read off the iterated key")
+        keys = t.keys
+        calls = self.plan.calls
+        # the product runs into a temporary when it must be added to `out`
+        dst = self._temp(ob) if accumulate else out
+
+        def finish(scale_done):
+            if accumulate:
+                calls.append(Call("axpby", dict(alpha=1.0 if scale_done else t.coef, x=dst,
+                                                beta=1.0), out))
+            elif not scale_done and t.coef != 1.0:
+                calls.append(Call("axpby", dict(alpha=t.coef, x=out, beta=0.0), out))
+
+        if keys == (r, c):
+            if ob.layout != "pattern":
+                raise NotLowerable("a result on the matrix's keys must have its layout")
+            if not D:
+                if len(W) > 1:
+                    raise NotLowerable("elementwise product of values on the pattern")
+                x = W[0].tensor if W else None
+                calls.append(Call("axpby", dict(alpha=t.coef, x=self._vals(x), beta=1.0
+                                                if accumulate else 0.0), out))
+                return
+            if W:
+                raise NotLowerable("sampled product times values on the pattern")
+            X, Y, k = self._sampled(D, r, c, t.loops)
+            calls.append(Call("sddmm", dict(X=X, Y=Y, k=k, alpha=t.coef), dst))
+            finish(True)
+            return
+        if len(W) > 1 and keys:
+            raise NotLowerable("elementwise product of values on the pattern")
+        vals = self._vals(W[0].tensor) if W else None
+        if vals is None and keys:
+            vals = self._ones_pattern()
+        if keys and keys[0] == r and all(v != c for v in keys):
+            # out[r, z] = sum_c W[r, c] D[c, z]  (SpMM / SpMV)
+            if len(D) > 1 or (D and D[0].idx[0] != c) or (D and D[0].idx[1:] != keys[1:]):
+                raise NotLowerable("row-indexed product outside SpMM")
+            if len(keys) > 2:
+                raise NotLowerable("results of order above 2")
+            if D:
+                dense, k = D[0].tensor, (p.extent[keys[1]] if len(keys) == 2 else 1)
+            else:
+                if len(keys) != 1:
+                    raise NotLowerable("row-indexed product outside SpMM")
+                dense, k = self._ones_dense(p.tensors[p.sparse].shape[1]), 1
+            calls.append(Call("spmm", dict(vals=vals, B=dense, k=k), dst))
+            finish(False)
+            return
+        if keys and keys[0] == c and all(v != r for v in keys):
+            # out[c, z] = sum_r W[r, c] G[r, z]  (transposed product)
+            if len(D) > 1 or (D and D[0].idx[0] != r) or (D and D[0].idx[1:] != keys[1:]):
+                raise NotLowerable("column-indexed product outside the transposed product")
+            if len(keys) > 2 or (not D and len(keys) != 1):
+                raise NotLowerable("column-indexed product outside the transposed product")
+            k = p.extent[keys[1]] if len(keys) == 2 else 1
+            calls.append(Call("spmm_t", dict(vals=vals, G=D[0].tensor if D else None, k=k,
+                                             alpha=t.coef), dst))
+            finish(True)
+            return
+        if not keys:
+            if ob.layout != "scalar":
+                raise NotLowerable("a real result needs a scalar output")
+            if D:
+                if len(W) > 1:
+                    raise NotLowerable("elementwise product of values on the pattern")
+                X, Y, k = self._sampled(D, r, c, t.loops)
+                tmp = self._temp(Buf("", "temp", "pattern", p.tensors[p.sparse].shape))
+                calls.append(Call("sddmm", dict(X=X, Y=Y, k=k, alpha=1.0), tmp))
+                calls.append(Call("dot", dict(x=tmp, y=self._vals(W[0].tensor) if W else None,
+                                              alpha=t.coef, acc=accumulate), out))
+                return
+            x = self._vals(W[0].tensor) if W else self._ones_pattern()
+            y = self._vals(W[1].tensor) if len(W) > 1 else None
+            if len(W) > 2:
+                raise NotLowerable("elementwise product of values on the pattern")
+            calls.append(Call("dot", dict(x=x, y=y, alpha=t.coef, acc=accumulate), out))
+            return
+        raise NotLowerable(f"result keys {keys} over the pattern ({r}, {c})")
+
+    def _sampled(self, D, r, c, loops):
+        """X[r, z], Y[c, z] (or vectors X[r], Y[c]) of an SDDMM."""
+        X = [f for f in D if f.idx and f.idx[0] == r]
+        Y = [f for f in D if f.idx and f.idx[0] == c]
+        if len(X) > 1 or len(Y) != 1 or len(X) + len(Y) != len(D):
+            raise NotLowerable("sampled product outside SDDMM (one factor per side)")
+        zx = X[0].idx[1:] if X else None
+        zy = Y[0].idx[1:]
+        if len(zy) > 1 or (X and zx != zy) or (zy and zy[0] not in loops):
+            raise NotLowerable("sampled product outside SDDMM (one shared summed index)")
+        k = self.p.extent[zy[0]] if zy else 1
+        return (X[0].tensor if X else None), Y[0].tensor, k
+
+    def _vals(self, tensor):
+        if tensor is None:
+            return None
+        self._need(tensor)
+        return tensor
+
+    def _ones_pattern(self):
+        name = "ones_nnz"
+        if name not in self.plan.bufs:
+            self.plan.bufs[name] = Buf(name, "temp", "pattern", self.p.tensors[self.p.sparse].shape)
+            self.plan.calls.append(Call("axpby", dict(alpha=1.0, x=None, beta=0.0), name))
+        return name
+
+    def _ones_dense(self, n):
+        name = f"ones_{n}"
+        if name not in self.plan.bufs:
+            self.plan.bufs[name] = Buf(name, "temp", "dense", (n,))
+            self.plan.calls.append(Call("axpby", dict(alpha=1.0, x=None, beta=0.0), name))
+        return name
+
+    # terms over dense tensors only
+    def _emit_dense(self, t, out, ob, accumulate):
+        calls = self.plan.calls
+        if not t.keys:
+            if ob.layout != "scalar":
+                raise NotLowerable("a real result needs a scalar output")
+            if not t.facs or len(t.facs) > 2 or any(f.idx != t.facs[0].idx for f in t.facs) \
+                    or len(set(t.facs[0].idx)) != len(t.facs[0].idx):
+                raise NotLowerable("dense contraction other than a dot product")
+            shape = self.p.tensors[t.facs[0].tensor].shape
+            for f in t.facs:
+                if self.p.tensors[f.tensor].shape != shape:
+                    raise NotLowerable("dot product of tensors of different shapes")
+            calls.append(Call("dot", dict(x=t.facs[0].tensor,
+                                          y=t.facs[1].tensor if len(t.facs) > 1 else None,
+                                          alpha=t.coef, acc=accumulate), out))
+            return
+        if len(t.facs) == 1 and t.facs[0].idx == t.keys and not t.loops \
+                and len(set(t.keys)) == len(t.keys) and ob.layout == "dense":
+            calls.append(Call("axpby", dict(alpha=t.coef, x=t.facs[0].tensor,
+                                            beta=1.0 if accumulate else 0.0), out))
+            return
+        raise NotLowerable("dense term other than a copy or a dot product")
+
+
+# ------------------------------------------------------------------ execution
+
+
+def _execute(plan: Plan, inputs: dict, stream=None):
+    import torch
+
+    from . import nsd
+
+    prog = plan.prog
+    A = inputs.get(prog.sparse) if prog.sparse else None
+    dev = None
+    for name, d in prog.inputs.items():
+        v = inputs.get(name)
+        if v is None:
+            raise SdqlError(f"missing input {name}")
+        if isinstance(d, Sparse):
+            if (v.nrows, v.ncols) != d.shape:
+                raise SdqlError(f"{name} is {v.nrows}x{v.ncols}, declared {d.shape}")
+            dev = v.val.device
+        else:
+            if tuple(v.shape) != d.shape or v.dtype != torch.float32 or not v.is_contiguous():
+                raise SdqlError(f"{name} must be a contiguous float32 tensor of shape {d.shape}")
+            dev = v.device
+    nnz = A.nnz if A is not None else 0
+    mem = {}
+    for name, b in plan.bufs.items():
+        if b.role == "input":
+            mem[name] = A.val if prog.tensors[name].kind == "sparse" else inputs[name]
+        elif b.layout == "scalar":
+            mem[name] = torch.empty(1, dtype=torch.float64, device=dev)
+        elif b.layout == "pattern":
+            mem[name] = torch.empty(max(nnz, 1), dtype=torch.float32, device=dev)[:nnz]
+        else:
+            mem[name] = torch.empty(b.shape, dtype=torch.float32, device=dev)
+    kmax = max([c.args.get("k", 1) for c in plan.calls] + [1])
+    need = 16384
+    if A is not None:
+        need = max(need, nsd.nsd_workspace_size(A.desc, A.csc, kmax))
+    ws = torch.empty(need, dtype=torch.uint8, device=dev)
+
+    def desc(vals):
+        d = nsd.csr_desc(A.nrows, A.ncols, A.rowptr, A.rowidx, A.colind, mem[vals])
+        d.plan = A.row_plan
+        return d
+
+    def m(name):
+        return None if name is None else mem[name]
+
+    for call in plan.calls:
+        a, out = call.args, mem[call.out]
+        if call.kernel == "axpby":
+            nsd.nsd_axpby(out.numel(), a["alpha"], m(a["x"]), a["beta"], out, stream)
+        elif call.kernel == "dot":
+            x = m(a["x"])
+            n = a.get("n", x.numel() if x is not None else 0)
+            nsd.nsd_dot(n, x, m(a["y"]), a["alpha"], a["acc"], out, ws, stream)
+        elif call.kernel == "sddmm":
+            nsd.nsd_sddmm(A.desc, m(a["X"]), m(a["Y"]), a["k"], a["alpha"], out, stream)
+        elif call.kernel == "spmm":
+            D = desc(a["vals"])
+            if a["k"] == 1:
+                nsd.nsd_spmv(D, m(a["B"]), out, ws, stream)
+            else:
+                nsd.nsd_spmm(D, m(a["B"]), a["k"], out, ws, stream)
+        elif call.kernel == "spmm_t":
+            if A.csc is None:
+                A.build_csc(stream)
+            nsd.nsd_spmm_t(desc(a["vals"]), A.csc, m(a["G"]), a["k"], a["alpha"], out, ws,
+                           stream)
+        else:
+            raise SdqlError(f"unknown kernel {call.kernel}")
+    return {name: mem[name] for name in plan.results}

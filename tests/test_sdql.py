@@ -1,0 +1,292 @@
+"""Front end for Logical SDQLite programs (CPU): parsing, normalization into
+sums of products, the gradient API's derivatives and their lowering.
+
+The derivatives the front end builds symbolically are evaluated here by dense
+brute force (numpy einsum over the terms, masks as 0/1 arrays) and compared
+with the reference interpreter's forward-mode gradient (one evaluation per
+stored key, Sections 4.1 and 4.3) on tiny random inputs.  The interpreter
+itself is pinned in test_sdql_oracle.py.
+"""
+import numpy as np
+import pytest
+
+from oracle import sdql as ref
+from paper_2303_07030_amd import sdql as S
+
+# The programs: the paper's running examples (Example 1, the dot product; the
+# matrix product of Section 3; Example 3, the trace) and the losses of the
+# experiments section written in Logical SDQLite.
+SMVM = "sum(<i,r> in A) sum(<j,a> in r) a * x(j)"
+FROB = ("let C = sum(<i,row> in A) { i -> sum(<j,a> in row) sum(<c,b> in B(j)) { c -> a * b } }"
+        " in 0.5 * sum(<i,r> in C) sum(<c,v> in r) v * v")
+GNN = "sum(<i,r> in A) sum(<j,a> in r) sum(<c,h> in H(j)) a * h * G(i)(c)"
+MF = ("let R = sum(<i,r> in A) {i -> sum(<j,a> in r) {j -> a + -1 * sum(<c,u> in U(i)) "
+      "u * V(j)(c)}} in sum(<i,r> in R) sum(<j,v> in r) v * v")
+MF_INNER = ("sum(<i,r> in A) sum(<j,a> in r) let d = a + -1 * sum(<c,u> in U(i)) u * V(j)(c) "
+            "in d * d")
+QUAD = "sum(<i,r> in A) sum(<j,a> in r) a * x(j) * x(i)"
+DOT1 = "sum(<i, a> in V1) a * V2(i)"
+DOT2 = "sum(<i, a> in V2) V1(i) * a"
+TRACE = "sum(<i,r> in M) r(i)"
+CUBIC = "sum(<i,r> in A) sum(<j,a> in r) 2 * a * a * a * x(j)"
+
+
+def rand_csr(rng, nr, nc, nnz):
+    keys = np.sort(rng.choice(nr * nc, size=nnz, replace=False))
+    row, col = keys // nc, keys % nc
+    rowptr = np.zeros(nr + 1, dtype=np.int64)
+    np.add.at(rowptr, row + 1, 1)
+    return np.cumsum(rowptr), col.astype(np.int64), rng.standard_normal(nnz)
+
+
+def dense_of(nr, nc, rowptr, colind, val):
+    D = np.zeros((nr, nc))
+    for i in range(nr):
+        D[i, colind[rowptr[i]:rowptr[i + 1]]] = val[rowptr[i]:rowptr[i + 1]]
+    return D
+
+
+# ------------------------------------------------- brute-force term evaluator
+
+
+def eval_terms(prog, T, arrays, cache=None):
+    """Dense value of a Terms object: arrays maps input names to dense fp64
+    arrays (sparse inputs with zeros off the pattern) and "#mask:<name>" to
+    their 0/1 patterns."""
+    cache = {} if cache is None else cache
+
+    def tensor(name):
+        if name in arrays:
+            return arrays[name]
+        if name not in cache:
+            info = prog.tensors[name]
+            cache[name] = eval_terms(prog, info.definition, arrays, cache)
+        return cache[name]
+
+    order = T.order or 0
+    shape = None
+    out = None
+    for t in T.terms:
+        tshape = tuple(prog.extent[v] for v in t.keys)
+        if shape is None:
+            shape = tshape
+            out = np.zeros(shape)
+        assert tshape == shape
+        letters = {}
+        for v in sorted(t.variables()):
+            letters[v] = chr(ord("a") + len(letters))
+        ops, subs = [], []
+        for f in t.facs:
+            ops.append(tensor(f.tensor))
+            subs.append("".join(letters[v] for v in f.idx))
+        for m in t.masks:
+            ops.append(arrays["#mask:" + m.tensor])
+            subs.append("".join(letters[v] for v in m.idx))
+        present = set()
+        for f in t.facs + t.masks:
+            present.update(f.idx)
+        keys_present = [v for v in dict.fromkeys(t.keys) if v in present]
+        if ops:
+            res = np.einsum(",".join(subs) + "->" + "".join(letters[v] for v in keys_present),
+                            *ops)
+        else:
+            res = np.asarray(1.0)
+        for v in t.loops:
+            if v not in present:
+                res = res * prog.extent[v]
+        # broadcast over keys that no operand carries, then place repeated
+        # key variables on the diagonal
+        uniq = list(dict.fromkeys(t.keys))
+        full = res
+        for pos, v in enumerate(uniq):
+            if v not in present:
+                full = np.expand_dims(full, pos)
+        full = np.broadcast_to(full, tuple(prog.extent[v] for v in uniq))
+        if len(uniq) == len(t.keys):
+            out = out + t.coef * full
+        else:
+            place = np.zeros(shape)
+            for idx in np.ndindex(*full.shape):
+                val = dict(zip(uniq, idx))
+                place[tuple(val[v] for v in t.keys)] = full[idx]
+            out = out + t.coef * place
+    if out is None:
+        return np.zeros(()) if order == 0 else None
+    return out
+
+
+def setup_inputs(rng, decls, sparse_nnz):
+    arrays, env, csr = {}, {}, {}
+    for name, d in decls.items():
+        if isinstance(d, S.Sparse):
+            rowptr, colind, val = rand_csr(rng, d.nrows, d.ncols, sparse_nnz)
+            D = dense_of(d.nrows, d.ncols, rowptr, colind, val)
+            arrays[name] = D
+            arrays["#mask:" + name] = dense_of(d.nrows, d.ncols, rowptr, colind,
+                                               np.ones_like(val))
+            env[name] = ref.csr_dict(rowptr, colind, val)
+            csr[name] = (rowptr, colind, val)
+        else:
+            a = rng.standard_normal(d.shape)
+            arrays[name] = a
+            env[name] = ref.dense_dict(a)
+    return arrays, env, csr
+
+
+CASES = [
+    ("smvm", SMVM, dict(A=S.Sparse(7, 5), x=S.Dense(5)), ("A", "x")),
+    ("frob", FROB, dict(A=S.Sparse(6, 5), B=S.Dense(5, 3)), ("A", "B")),
+    ("gnn", GNN, dict(A=S.Sparse(6, 5), H=S.Dense(5, 3), G=S.Dense(6, 3)), ("A", "H", "G")),
+    ("mf", MF, dict(A=S.Sparse(6, 5), U=S.Dense(6, 3), V=S.Dense(5, 3)), ("A", "U", "V")),
+    ("mf_inner", MF_INNER, dict(A=S.Sparse(6, 5), U=S.Dense(6, 3), V=S.Dense(5, 3)),
+     ("A", "U", "V")),
+    ("quad", QUAD, dict(A=S.Sparse(6, 6), x=S.Dense(6)), ("A", "x")),
+    ("dot1", DOT1, dict(V1=S.Dense(6), V2=S.Dense(6)), ("V1", "V2")),
+    ("dot2", DOT2, dict(V1=S.Dense(6), V2=S.Dense(6)), ("V1", "V2")),
+    ("trace", TRACE, dict(M=S.Sparse(5, 5)), ("M",)),
+    ("cubic", CUBIC, dict(A=S.Sparse(6, 5), x=S.Dense(5)), ("A", "x")),
+]
+
+
+@pytest.mark.parametrize("name,text,decls,grads", CASES, ids=[c[0] for c in CASES])
+@pytest.mark.parametrize("seed", [0, 1])
+def test_value_and_gradients_match_interpreter(name, text, decls, grads, seed):
+    rng = np.random.default_rng(seed)
+    nnz = 12 if name != "trace" else 14
+    arrays, env, csr = setup_inputs(rng, decls, nnz)
+    prog = S.compile(text, **decls)
+    want = ref.value(text, env)
+    got = eval_terms(prog, prog.value, arrays)
+    np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-12)
+    for x in grads:
+        g = eval_terms(prog, prog.gradient(x), arrays)
+        want = ref.gradient(text, env, x)
+        shape = decls[x].shape
+        if g is None:
+            g = np.zeros(shape)
+        assert g.shape == shape
+        for key, v in want.items():
+            np.testing.assert_allclose(g[key], v, rtol=1e-11, atol=1e-12,
+                                       err_msg=f"d{x} at {key}")
+        if isinstance(decls[x], S.Sparse):
+            off = arrays["#mask:" + x] == 0
+            assert np.all(g[off] == 0), f"d{x} is not confined to the stored keys"
+
+
+# ---------------------------------------------------------------- normalization
+
+
+def test_value_terms_of_the_smvm():
+    prog = S.compile(SMVM, A=S.Sparse(4, 3), x=S.Dense(3))
+    (t,) = prog.value.terms
+    assert t.keys == () and len(t.loops) == 2 and t.coef == 1.0
+    assert sorted(f.tensor for f in t.facs) == ["A", "x"]
+    assert [m.tensor for m in t.masks] == ["A"]
+
+
+def test_product_rule_terms_merge():
+    # d/dB of 1/2 sum C*C: the product rule gives two equal terms, merged
+    prog = S.compile(FROB, A=S.Sparse(4, 3), B=S.Dense(3, 2))
+    (t,) = prog.gradient("B").terms
+    assert t.coef == 1.0
+
+
+def test_let_of_a_real_inside_loops_becomes_a_tensor_on_the_pattern():
+    prog = S.compile(MF_INNER, A=S.Sparse(4, 3), U=S.Dense(4, 2), V=S.Dense(3, 2))
+    inter = [t for t in prog.tensors.values() if not t.input]
+    assert len(inter) == 1 and inter[0].kind == "patterned" and inter[0].shape == (4, 3)
+
+
+def test_zero_tangents_vanish():
+    # the gradient w.r.t. an input the program does not read is zero
+    prog = S.compile(SMVM + " + 0 * sum(<c,y> in z) y", A=S.Sparse(4, 3), x=S.Dense(3),
+                     z=S.Dense(2))
+    assert prog.gradient("z").terms == []
+    plan = prog.plan(("z",))
+    assert plan.kernels()[-1] == "axpby" and plan.calls[-1].args["alpha"] == 0.0
+
+
+# ------------------------------------------------------------------ lowering
+
+
+def plan_of(text, grads, **decls):
+    return S.compile(text, **decls).plan(grads)
+
+
+def test_lowering_smvm():
+    p = plan_of(SMVM, ("A", "x"), A=S.Sparse(5, 4), x=S.Dense(4))
+    assert p.kernels() == ["sddmm", "dot", "sddmm", "spmm_t"]
+    dA = p.calls[2]
+    assert dA.out == "dA" and dA.args["X"] is None and dA.args["Y"] == "x" and dA.args["k"] == 1
+    dx = p.calls[3]
+    assert dx.args["G"] is None and dx.args["vals"] == "A"
+
+
+def test_lowering_frob_computes_C_once():
+    p = plan_of(FROB, ("A", "B"), A=S.Sparse(5, 4), B=S.Dense(4, 3))
+    assert p.kernels() == ["spmm", "dot", "sddmm", "spmm_t"]
+    C = p.calls[0].out
+    assert p.calls[1].args == dict(x=C, y=C, alpha=0.5, acc=False)
+    assert p.calls[2].args["X"] == C and p.calls[2].args["Y"] == "B"
+    assert p.calls[3].args["G"] == C
+
+
+def test_lowering_gnn():
+    p = plan_of(GNN, ("A", "H", "G"), A=S.Sparse(5, 4), H=S.Dense(4, 3), G=S.Dense(5, 3))
+    assert p.kernels() == ["sddmm", "dot", "sddmm", "spmm_t", "spmm"]
+    assert [c.out for c in p.calls[2:]] == ["dA", "dH", "dG"]
+
+
+def test_lowering_mf_residual_and_scaled_gradients():
+    p = plan_of(MF, ("A", "U", "V"), A=S.Sparse(5, 4), U=S.Dense(5, 3), V=S.Dense(4, 3))
+    assert p.kernels() == ["axpby", "sddmm", "axpby", "dot", "axpby", "spmm", "axpby", "spmm_t"]
+    R = p.calls[0].out
+    assert p.calls[1].args["alpha"] == -1.0
+    assert p.calls[4].args == dict(alpha=2.0, x=R, beta=0.0)
+    assert p.calls[6].args["alpha"] == -2.0 and p.calls[7].args["alpha"] == -2.0
+
+
+def test_lowering_accumulates_terms_of_one_result():
+    p = plan_of(QUAD, ("x",), A=S.Sparse(4, 4), x=S.Dense(4))
+    ks = p.kernels()
+    assert ks[-3:] == ["spmm_t", "spmm", "axpby"] and p.calls[-1].args["beta"] == 1.0
+
+
+def test_lowering_dense_dot_product():
+    p = plan_of(DOT1, ("V1", "V2"), V1=S.Dense(6), V2=S.Dense(6))
+    assert p.kernels() == ["dot", "axpby", "axpby"]
+    assert p.calls[1].args["x"] == "V2" and p.calls[2].args["x"] == "V1"
+
+
+@pytest.mark.parametrize("text,decls,grads,msg", [
+    (TRACE, dict(M=S.Sparse(4, 4)), ("M",), "diagonal"),
+    ("sum(<i,r> in A) sum(<j,a> in r) a * a * x(j)", dict(A=S.Sparse(4, 3), x=S.Dense(3)),
+     ("A",), "values on the pattern"),
+    ("sum(<i,a> in x) exp(a)", dict(x=S.Dense(3)), (), "outside"),
+    ("sum(<i,a> in x) if a = 0 then 1", dict(x=S.Dense(3)), (), "outside"),
+    ("sum(<i,r> in A) sum(<j,a> in r) a * B(i)(j)", dict(A=S.Sparse(4, 3), B=S.Dense(4, 3)),
+     (), "SDDMM"),
+])
+def test_outside_the_kernels_raises(text, decls, grads, msg):
+    with pytest.raises(S.NotLowerable, match=msg):
+        S.compile(text, **decls).plan(grads)
+
+
+def test_errors():
+    with pytest.raises(S.SdqlError, match="expected"):
+        S.parse("sum(<i,a> x) a")
+    with pytest.raises(S.SdqlError, match="unbound"):
+        S.compile("sum(<i,a> in x) a * y(i)", x=S.Dense(3))
+    with pytest.raises(S.SdqlError, match="ranges over"):
+        S.compile("sum(<i,a> in x) a * y(i)", x=S.Dense(3), y=S.Dense(4))
+    with pytest.raises(S.NotLowerable, match="one sparse"):
+        S.compile("0", A=S.Sparse(2, 2), B=S.Sparse(2, 2))
+
+
+def test_parser_binding():
+    e = S.parse("2 * sum(<i,a> in V) a + 1")
+    assert isinstance(e, S.MulE) and isinstance(e.right, S.SumE)
+    assert isinstance(e.right.body, S.AddE)       # the sum's body runs to the end
+    e = S.parse("a + b * c(i)(j)")
+    assert isinstance(e, S.AddE) and isinstance(e.right, S.MulE)
+    assert isinstance(e.right.right, S.Lookup) and isinstance(e.right.right.dict, S.Lookup)
