@@ -116,6 +116,10 @@ typedef struct nsd_csc {
  * A COO 3-tensor seen through one mode n: its entries stably sorted by the
  * mode-n coordinate (nsd_coo_mode_index), with the other coordinates and the
  * values gathered into that order, and the work plan over the mode-n slices.
+ * "Input order" is the order of the coordinate arrays the mode indexes were
+ * built from.  Holding the tensor in lexicographic coordinate order (a stable
+ * sort by the last coordinate, then each earlier one) makes mode 0's perm the
+ * identity, so the gradient on X's keys is written sequentially.
  */
 typedef struct nsd_coo3_mode {
     int32_t mode;          /* n in {0, 1, 2} */

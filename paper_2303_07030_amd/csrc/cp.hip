@@ -62,7 +62,8 @@ struct CpSlot {
     }
 
     // Entries [p, p + U): segment r, coordinates ca / cb of the two other
-    // modes, value x, input position pp (padding past b0: value 0).
+    // modes, value x, input position pp (padding past b0 repeats the last
+    // entry; its residual is zeroed here).
     __device__ __forceinline__ void batch(int64_t p, const int (&r)[U], const int (&ca)[U],
                                           const int (&cb)[U], const float (&x)[U],
                                           const int (&pp)[U]) {
@@ -71,19 +72,24 @@ struct CpSlot {
         bool same = true;
 #pragma unroll
         for (int u = 0; u < U; ++u) same = same && r[u] == row;
-        Vec<VEC> t[U], ow[U];
+        // Every load of the batch is issued before any of them is used: the
+        // addresses are always valid (a lane past the rank reads column 0 and
+        // its data is dropped), so no load sits in a branch that must wait.
+        const int cl = on ? col : 0;
+        Vec<VEC> t[U], fb[U], ow[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            if (on) {
-                Vec<VEC> fb;
-                t[u].load(m.fa + (int64_t)ca[u] * k + col);
-                fb.load(m.fb + (int64_t)cb[u] * k + col);
-                if (!same) ow[u].load(m.own + (int64_t)r[u] * k + col);
+            t[u].load(m.fa + (int64_t)ca[u] * k + cl);
+            fb[u].load(m.fb + (int64_t)cb[u] * k + cl);
+        }
+        if (!same) {
 #pragma unroll
-                for (int e = 0; e < VEC; ++e) t[u].v[e] *= fb.v[e];
-            } else {
-                t[u].zero();
-            }
+            for (int u = 0; u < U; ++u) ow[u].load(m.own + (int64_t)r[u] * k + cl);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) t[u].v[e] = on ? t[u].v[e] * fb[u].v[e] : 0.f;
         }
         float d[U];
 #pragma unroll
@@ -143,14 +149,16 @@ __device__ __forceinline__ void cp_walk(const CpMode &m, int64_t s, int lane, bo
     const SgrParams &a = m.s;
     CpSlot<VEC, G, U> st(m, s, lane, first_mode, lsum);
     const int64_t a0 = a.plan.item_ptr[s], b0 = st.b0;
-    const int last_r = a.segidx[b0 - 1], last_a = a.idx[b0 - 1], last_b = m.idx_b[b0 - 1];
+    // Fields of entry q; past the item they are those of its last entry
+    // (every load unconditional, so none is consumed before its batch); the
+    // batch zeroes the padding's residual by position.
     auto fields = [&](int64_t q, int &r, int &ca, int &cb, float &x, int &pp) {
-        const bool in = q < b0;
-        r = in ? a.segidx[q] : last_r;
-        ca = in ? a.idx[q] : last_a;
-        cb = in ? m.idx_b[q] : last_b;
-        x = in ? a.w[q] : 0.f;
-        pp = (in && first_mode) ? m.perm[q] : 0;
+        const int64_t qc = min(q, b0 - 1);
+        r = a.segidx[qc];
+        ca = a.idx[qc];
+        cb = m.idx_b[qc];
+        x = a.w[qc];
+        pp = first_mode ? m.perm[qc] : 0;
     };
     if constexpr (G >= 8) {
         static_assert(G % U == 0, "a tile holds whole batches");
@@ -216,8 +224,15 @@ __device__ __forceinline__ void cp_block(const CpMode &m, int b, bool first_mode
     }
 }
 
+// Occupancy floor (waves per SIMD), a build-time tuning knob.
+#ifdef NSD_CP_WAVES
+#define NSD_CP_OCCUPANCY __attribute__((amdgpu_waves_per_eu(NSD_CP_WAVES, 8)))
+#else
+#define NSD_CP_OCCUPANCY
+#endif
+
 template <int VEC, int G, int U>
-__global__ __launch_bounds__(kBlock) void cp_kernel(CpParams f) {
+__global__ __launch_bounds__(kBlock) NSD_CP_OCCUPANCY void cp_kernel(CpParams f) {
     const int b0 = f.m[0].item_blocks + f.m[0].empty_blocks;
     const int b1 = b0 + f.m[1].item_blocks + f.m[1].empty_blocks;
     double lsum = 0.0;

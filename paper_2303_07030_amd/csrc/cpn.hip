@@ -81,28 +81,35 @@ struct CpnSlot {
     }
 
     // Entries [p, p + U): segment r, other coordinates c[0..N-2], value x,
-    // input position pp (pass 0); padding past b0 has value 0.
+    // input position pp (pass 0); padding past b0 repeats the last entry and
+    // its residual is zeroed here.
     __device__ __forceinline__ void batch(int64_t p, const int (&r)[U], const int (&c)[N - 1][U],
                                           const float (&x)[U], const int (&pp)[U]) {
         bool same = true;
 #pragma unroll
         for (int u = 0; u < U; ++u) same = same && r[u] == row;
-        Vec<VEC> t[U], ow[U];
+        // All gathers of the batch are issued before any is used (a lane past
+        // the rank reads column 0 and drops it), as in the order-3 kernel.
+        const int cl = on ? col : 0;
+        Vec<VEC> t[U], h[N - 2][U], ow[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            if (on) {
-                t[u].load(m.fac[0] + (int64_t)c[0][u] * k + col);
+            t[u].load(m.fac[0] + (int64_t)c[0][u] * k + cl);
 #pragma unroll
-                for (int f = 1; f < N - 1; ++f) {
-                    Vec<VEC> h;
-                    h.load(m.fac[f] + (int64_t)c[f][u] * k + col);
+            for (int f = 1; f < N - 1; ++f) h[f - 1][u].load(m.fac[f] + (int64_t)c[f][u] * k + cl);
+        }
+        if (!same) {
 #pragma unroll
-                    for (int e = 0; e < VEC; ++e) t[u].v[e] *= h.v[e];
-                }
-                if (!same) ow[u].load(m.own + (int64_t)r[u] * k + col);
-            } else {
-                t[u].zero();
+            for (int u = 0; u < U; ++u) ow[u].load(m.own + (int64_t)r[u] * k + cl);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+#pragma unroll
+            for (int f = 0; f < N - 2; ++f) {
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) t[u].v[e] *= h[f][u].v[e];
             }
+            if (!on) t[u].zero();
         }
         float d[U];
 #pragma unroll
@@ -160,17 +167,16 @@ __device__ __forceinline__ void cpn_walk(const CpnMode<N> &m, int64_t s, int lan
     const SgrParams &a = m.s;
     CpnSlot<N, VEC, G, U> st(m, s, lane, first_mode, lsum);
     const int64_t a0 = a.plan.item_ptr[s], b0 = st.b0;
-    int last[N];
-    last[0] = a.segidx[b0 - 1];
-#pragma unroll
-    for (int f = 0; f < N - 1; ++f) last[f + 1] = m.other[f][b0 - 1];
+    // Fields of entry q, past the item those of its last entry (every load
+    // unconditional, so none is consumed before its batch); the batch zeroes
+    // the padding's residual by position.
     auto fields = [&](int64_t q, int &r, int (&c)[N - 1], float &x, int &pp) {
-        const bool in = q < b0;
-        r = in ? a.segidx[q] : last[0];
+        const int64_t qc = min(q, b0 - 1);
+        r = a.segidx[qc];
 #pragma unroll
-        for (int f = 0; f < N - 1; ++f) c[f] = in ? m.other[f][q] : last[f + 1];
-        x = in ? a.w[q] : 0.f;
-        pp = (in && first_mode) ? m.perm[q] : 0;
+        for (int f = 0; f < N - 1; ++f) c[f] = m.other[f][qc];
+        x = a.w[qc];
+        pp = first_mode ? m.perm[qc] : 0;
     };
     if constexpr (G >= 8) {
         static_assert(G % U == 0, "a tile holds whole batches");

@@ -104,18 +104,63 @@ class DeviceCsr:
         return valT[: self.nnz]
 
 
+def lex_order(coords, dims, ws, stream=None):
+    """Permutation q -> input position that sorts COO entries by (c0, c1, ...)
+    lexicographically: stable sorts by the last coordinate first, each one the
+    library's mode index, composed by the library's gather."""
+    n = int(coords[0].numel())
+    dev = coords[0].device
+    m_ = max(n, 1)
+    perm = None
+    for m in reversed(range(len(coords))):
+        key = coords[m]
+        if perm is not None:
+            key = torch.empty(m_, dtype=torch.int32, device=dev)
+            nsd.nsd_gather_i32(n, perm, coords[m], key, stream)
+        segptr = torch.empty(int(dims[m]) + 1, dtype=torch.int32, device=dev)
+        segidx = torch.empty(m_, dtype=torch.int32, device=dev)
+        p = torch.empty(m_, dtype=torch.int32, device=dev)
+        nsd.nsd_coo_mode_index(n, int(dims[m]), key, segptr, segidx, p, ws, stream)
+        if perm is None:
+            perm = p
+        else:
+            composed = torch.empty(m_, dtype=torch.int32, device=dev)
+            nsd.nsd_gather_i32(n, p, perm, composed, stream)
+            perm = composed
+    return perm[:n]
+
+
+def _stored_in_lex_order(coords, val, dims, ws, stream):
+    """(coordinates, values, coo_perm) with the entries in lexicographic
+    coordinate order; coo_perm[q] is the input position of stored entry q."""
+    n = int(val.numel())
+    perm = lex_order(coords, dims, ws, stream)
+    out = []
+    for c in coords:
+        t = torch.empty(max(n, 1), dtype=torch.int32, device=val.device)
+        nsd.nsd_gather_i32(n, perm, c, t, stream)
+        out.append(t[:n])
+    v = torch.empty(max(n, 1), dtype=torch.float32, device=val.device)
+    nsd.nsd_gather_f32(n, perm, val, v, stream)
+    return out, v[:n], perm
+
+
 class DeviceCoo3:
-    """A COO 3-tensor in HBM in its three mode orders: for every mode n the
-    library's mode index (stable sort by the mode-n coordinate), the other
-    two coordinates and the values gathered into that order, and the work
-    plan over the mode-n slices."""
+    """A COO 3-tensor in HBM, stored in lexicographic (i, j, l) order (the
+    order its first mode pass walks, so the residual on X's keys is written
+    sequentially), and in its three mode orders: for every mode n the
+    library's mode index (stable sort by the mode-n coordinate over the
+    stored order), the other two coordinates and the values gathered into
+    that order, and the work plan over the mode-n slices.  `coo_perm[q]` is
+    the input position of stored entry q; gradients on X's keys come out in
+    the stored order (as a CSR's values do)."""
 
     def __init__(self, dims, i, j, l, val, device="cuda", rank_hint=32, item_len=None,
                  stream=None):
         self.dims = tuple(int(d) for d in dims)
         coords = [_dev(c, torch.int32, device) for c in (i, j, l)]
-        self.val = _dev(val, torch.float32, device)
-        self.nnz = int(self.val.numel())
+        val = _dev(val, torch.float32, device)
+        self.nnz = int(val.numel())
         self.item_len = item_len or nsd.nsd_plan_item_len(self.nnz, rank_hint)
         self.desc = nsd.nsd_coo3()
         self.desc.dims[:] = self.dims
@@ -123,6 +168,9 @@ class DeviceCoo3:
         self._keep = []
         ws = torch.empty(nsd.nsd_build_workspace_size(self.nnz, max(max(self.dims), 1)),
                          dtype=torch.uint8, device=device)
+        coords, self.val, self.coo_perm = _stored_in_lex_order(coords, val, self.dims, ws,
+                                                               stream)
+        self.coords = coords
         n = max(self.nnz, 1)
         for m in range(3):
             segptr = torch.empty(self.dims[m] + 1, dtype=torch.int32, device=device)
@@ -151,10 +199,13 @@ class DeviceCoo3:
 
 
 class DeviceCooN:
-    """A COO tensor of order 3 to 6 in HBM in all its mode orders: for every
-    mode n the library's mode index (stable sort by coordinate n), the other
-    coordinates (modes n+1, n+2, ... mod order) and the values gathered into
-    that order, and the work plan over the mode-n slices."""
+    """A COO tensor of order 3 to 6 in HBM, stored in lexicographic
+    coordinate order (`coo_perm[q]` is the input position of stored entry q;
+    gradients on X's keys come out in the stored order), and in all its mode
+    orders: for every mode n the library's mode index (stable sort by
+    coordinate n), the other coordinates (modes n+1, n+2, ... mod order) and
+    the values gathered into that order, and the work plan over the mode-n
+    slices."""
 
     def __init__(self, dims, coords, val, device="cuda", rank_hint=32, item_len=None,
                  stream=None):
@@ -163,8 +214,8 @@ class DeviceCooN:
         if not 3 <= N <= nsd.MAX_ORDER:
             raise ValueError(f"order {N} outside [3, {nsd.MAX_ORDER}]")
         coords = [_dev(c, torch.int32, device) for c in coords]
-        self.val = _dev(val, torch.float32, device)
-        self.nnz = int(self.val.numel())
+        val = _dev(val, torch.float32, device)
+        self.nnz = int(val.numel())
         self.item_len = item_len or nsd.nsd_plan_item_len(self.nnz, rank_hint)
         self.desc = nsd.nsd_coon()
         self.desc.order = N
@@ -174,6 +225,9 @@ class DeviceCooN:
         self._keep = []
         ws = torch.empty(nsd.nsd_build_workspace_size(self.nnz, max(max(self.dims), 1)),
                          dtype=torch.uint8, device=device)
+        coords, self.val, self.coo_perm = _stored_in_lex_order(coords, val, self.dims, ws,
+                                                               stream)
+        self.coords = coords
         n = max(self.nnz, 1)
         for m in range(N):
             segptr = torch.empty(self.dims[m] + 1, dtype=torch.int32, device=device)

@@ -447,7 +447,15 @@ def run_cp(nsd, X, F, rank, seed=1.0):
     dF = [torch.full((X.dims[m], rank), np.nan, dtype=torch.float32, device="cuda")
           for m in range(3)]
     nsd.nsd_loss_cp(X.desc, *[dev(f) for f in F], rank, seed, loss, dX, *dF, X.workspace(rank))
-    return host(loss)[0], host(dX), [host(t) for t in dF]
+    return host(loss)[0], in_input_order(X, host(dX)), [host(t) for t in dF]
+
+
+def in_input_order(X, stored):
+    """A value array on X's keys, from X's stored (lexicographic) order back
+    to the order of the input coordinates."""
+    out = np.full(X.nnz, np.nan, dtype=stored.dtype)
+    out[host(X.coo_perm)] = stored[: X.nnz]
+    return out
 
 
 def check_cp(orc, dims, i, j, l, val, F, rank, got, seed=1.0):
@@ -460,6 +468,24 @@ def check_cp(orc, dims, i, j, l, val, F, rank, got, seed=1.0):
     for m in range(3):
         g, gm = orc.cp_grad(D, *F, rank, m)
         assert_mag_close(dFg[m], seed * g, abs(seed) * gm, what=f"dF{m + 1}")
+
+
+@pytest.mark.parametrize("order", [3, 4, 6])
+def test_coo_stored_in_lexicographic_order(nsd, order):
+    # the operand's storage order is the stable lexicographic sort of the
+    # input coordinates, built by the library's mode index (bit-exact)
+    from paper_2303_07030_amd.operand import DeviceCoo3, DeviceCooN
+    rng = np.random.default_rng(order)
+    dims = (9, 40, 3, 17, 2, 5)[:order]
+    nnz = 3000
+    coords = [rng.integers(0, d, nnz).astype(np.int32) for d in dims]  # duplicates too
+    val = rng.standard_normal(nnz).astype(np.float32)
+    X = DeviceCoo3(dims, *coords, val) if order == 3 else DeviceCooN(dims, coords, val)
+    want = np.lexsort(coords[::-1])
+    assert np.array_equal(host(X.coo_perm), want)
+    for m in range(order):
+        assert np.array_equal(host(X.coords[m]), coords[m][want])
+    assert np.array_equal(host(X.val), val[want])
 
 
 def test_loss_cp_small_workload(nsd, orc):
@@ -727,7 +753,7 @@ def run_cpn(nsd, X, F, rank, seed=1.0):
     dX = torch.full((max(X.nnz, 1),), np.nan, dtype=torch.float32, device="cuda")
     dF = [torch.full((d, rank), np.nan, dtype=torch.float32, device="cuda") for d in X.dims]
     nsd.nsd_loss_cpn(X.desc, [dev(f) for f in F], rank, seed, loss, dX, dF, X.workspace(rank))
-    return host(loss)[0], host(dX)[: X.nnz], [host(t) for t in dF]
+    return host(loss)[0], in_input_order(X, host(dX)), [host(t) for t in dF]
 
 
 def check_cpn(orc, dims, coords, val, F, rank, got, seed=1.0):

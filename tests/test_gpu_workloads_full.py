@@ -176,7 +176,9 @@ def test_cp_full_workload(nsd, orc):
     dX = torch.empty(X.nnz, dtype=torch.float32, device="cuda")
     dF = [torch.empty((dims[m], R), dtype=torch.float32, device="cuda") for m in range(3)]
     nsd.nsd_loss_cp(X.desc, *[dev(f) for f in F], R, 1.0, loss, dX, *dF, X.workspace(R))
-    Lg, dXg, dFg = host(loss)[0], host(dX), [host(t) for t in dF]
+    Lg, dFg = host(loss)[0], [host(t) for t in dF]
+    dXg = np.empty(X.nnz, dtype=np.float32)
+    dXg[host(X.coo_perm)] = host(dX)   # stored order -> input order
     del X, dX, dF
     rng = np.random.default_rng(7)
     coords = (i, j, l)
@@ -215,7 +217,9 @@ def test_cp4_full_workload(nsd, orc):
     dX = torch.empty(X.nnz, dtype=torch.float32, device="cuda")
     dF = [torch.empty((dd, R), dtype=torch.float32, device="cuda") for dd in dims]
     nsd.nsd_loss_cpn(X.desc, [dev(f) for f in F], R, 1.0, loss, dX, dF, X.workspace(R))
-    Lg, dXg, dFg = host(loss)[0], host(dX), [host(t) for t in dF]
+    Lg, dFg = host(loss)[0], [host(t) for t in dF]
+    dXg = np.empty(X.nnz, dtype=np.float32)
+    dXg[host(X.coo_perm)] = host(dX)   # stored order -> input order
     del X, dX, dF
     rng = np.random.default_rng(8)
     P = rng.choice(len(val), 8192, replace=False)
