@@ -70,7 +70,8 @@ def parse():
 # that file, every shared header and the public header.
 KERNEL_SOURCE = {"frob_row": "segreduce.hip", "sgr_main": "segreduce.hip",
                  "sddmm": "segreduce.hip", "frob_col": "dual.hip", "dual": "dual.hip",
-                 "mf": "dual.hip", "cp": "cp.hip", "sort": "build.hip"}
+                 "mf": "dual.hip", "cp": "cp.hip", "sort": "build.hip", "jvp": "jvp.hip",
+                 "cpn": "cpn.hip"}
 
 
 def source_digest(kernel=None):
