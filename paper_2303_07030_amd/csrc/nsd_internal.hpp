@@ -72,6 +72,31 @@ inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 
 
 __device__ __forceinline__ float shfl_xor(float v, int m) { return __shfl_xor(v, m, kWave); }
 
+// v of this lane's partner in a butterfly step of span M: a lane of the
+// other half of its aligned 2M-lane group.  Spans 1 and 2 pair lane i with
+// i ^ M (DPP quad permutation), spans 4 and 8 mirror the group (i with
+// 2M - 1 - i: DPP row half-mirror and row mirror), span 16 pairs i ^ 16
+// (swizzle within 32 lanes), span 32 goes through the LDS crossbar.  A
+// butterfly sum over all lanes is the same with either pairing; the DPP
+// forms are plain VALU moves instead of LDS round trips.
+template <int M>
+__device__ __forceinline__ float lane_xor(float v) {
+    const int x = __float_as_int(v);
+    if constexpr (M == 1) {
+        return __int_as_float(__builtin_amdgcn_mov_dpp(x, 0xB1, 0xF, 0xF, false));
+    } else if constexpr (M == 2) {
+        return __int_as_float(__builtin_amdgcn_mov_dpp(x, 0x4E, 0xF, 0xF, false));
+    } else if constexpr (M == 4) {
+        return __int_as_float(__builtin_amdgcn_mov_dpp(x, 0x141, 0xF, 0xF, false));
+    } else if constexpr (M == 8) {
+        return __int_as_float(__builtin_amdgcn_mov_dpp(x, 0x140, 0xF, 0xF, false));
+    } else if constexpr (M == 16) {
+        return __int_as_float(__builtin_amdgcn_ds_swizzle(x, (16 << 10) | 0x1F));
+    } else {
+        return __shfl_xor(v, M, kWave);
+    }
+}
+
 template <int VEC>
 struct Vec;
 

@@ -438,26 +438,30 @@ inline nsd_status dispatch_width(const WidthPlan &wp, F &f) {
 // receives the partner's matching half, so U values cost U - 1 exchanges
 // plus log2(G / U) for the last one.  Lane g ends with the total of value
 // number g / (G / U).
-template <int G, int U>
-__device__ __forceinline__ float transpose_reduce(float (&v)[U], int lane) {
-    int c = U;
+// Step of span M with C values still held per lane (the partner is the
+// other half of the aligned 2M-lane group, lane_xor<M>).
+template <int M, int C, int U>
+__device__ __forceinline__ void transpose_step(float (&v)[U], int lane) {
+    if constexpr (M >= 1) {
+        if constexpr (C > 1) {
+            const bool upper = (lane & M) != 0;
 #pragma unroll
-    for (int m = G / 2; m >= 1; m >>= 1) {
-        if (c > 1) {
-            const bool upper = (lane & m) != 0;
-#pragma unroll
-            for (int i = 0; i < U / 2; ++i) {
-                if (i < c / 2) {
-                    const float send = upper ? v[i] : v[i + c / 2];
-                    const float keep = upper ? v[i + c / 2] : v[i];
-                    v[i] = keep + shfl_xor(send, m);
-                }
+            for (int i = 0; i < C / 2; ++i) {
+                const float send = upper ? v[i] : v[i + C / 2];
+                const float keep = upper ? v[i + C / 2] : v[i];
+                v[i] = keep + lane_xor<M>(send);
             }
-            c >>= 1;
+            transpose_step<M / 2, C / 2, U>(v, lane);
         } else {
-            v[0] += shfl_xor(v[0], m);
+            v[0] += lane_xor<M>(v[0]);
+            transpose_step<M / 2, 1, U>(v, lane);
         }
     }
+}
+
+template <int G, int U>
+__device__ __forceinline__ float transpose_reduce(float (&v)[U], int lane) {
+    transpose_step<G / 2, U, U>(v, lane);
     return v[0];
 }
 
