@@ -119,13 +119,10 @@ struct CpnSlot {
 #pragma unroll
             for (int u = 0; u < U; ++u) res[u] = p + u < b0 ? x[u] - d[u] : 0.f;
         } else {
-            const float tot = transpose_reduce<G, U>(d, lane);
-            constexpr int kRep = G / U;
+            float mv[U];
+            slot_totals<G, U>(transpose_reduce<G, U>(d, lane), lane, mv);
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const float mv = __shfl(tot, u * kRep, G);
-                res[u] = p + u < b0 ? x[u] - mv : 0.f;
-            }
+            for (int u = 0; u < U; ++u) res[u] = p + u < b0 ? x[u] - mv[u] : 0.f;
         }
         if (first_mode && g == 0) {
 #pragma unroll

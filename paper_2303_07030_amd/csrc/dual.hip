@@ -131,13 +131,10 @@ struct DualSlot {
 #pragma unroll
                 for (int u = 0; u < U; ++u) coef[u] = p + u < b0 ? w[u] - d[u] : 0.f;
             } else {
-                const float tot = transpose_reduce<G, U>(d, lane);
-                constexpr int kRep = G / U;
+                float t[U];
+                slot_totals<G, U>(transpose_reduce<G, U>(d, lane), lane, t);
 #pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    const float t = __shfl(tot, u * kRep, G);
-                    coef[u] = p + u < b0 ? w[u] - t : 0.f;
-                }
+                for (int u = 0; u < U; ++u) coef[u] = p + u < b0 ? w[u] - t[u] : 0.f;
             }
             if (m.count_loss && g == 0)
 #pragma unroll

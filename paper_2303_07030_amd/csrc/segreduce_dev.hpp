@@ -465,6 +465,23 @@ __device__ __forceinline__ float transpose_reduce(float (&v)[U], int lane) {
     return v[0];
 }
 
+// After transpose_reduce (lane g holding the total of value g / (G / U)),
+// every lane's copy of all U totals: with two values one lane move from the
+// other half of the slot, otherwise U broadcasts.
+template <int G, int U>
+__device__ __forceinline__ void slot_totals(float tot, int lane, float (&out)[U]) {
+    if constexpr (U == 2) {
+        const float other = lane_xor<G / 2>(tot);
+        const bool upper = (lane & (G / 2)) != 0;
+        out[0] = upper ? other : tot;
+        out[1] = upper ? tot : other;
+    } else {
+        constexpr int kRep = G / U;
+#pragma unroll
+        for (int u = 0; u < U; ++u) out[u] = __shfl(tot, u * kRep, G);
+    }
+}
+
 // Block total of per-lane fp64 values, in a fixed order.
 __device__ __forceinline__ double block_sum(double v) {
     __shared__ double wsum[kBlockWaves];
