@@ -173,7 +173,7 @@ nsd_status scan_exclusive_max(const int32_t *in, int32_t *out, int64_t n, void *
 // ------------------------------------------------------------ radix sort
 
 constexpr int kSortThreads = 256;
-constexpr int kSortRounds = 8;  // 64-element rounds per wave
+constexpr int kSortRounds = 16;  // 64-element rounds per wave
 constexpr int kSortTile = kSortThreads * kSortRounds;
 constexpr int kBins = 256;
 constexpr int kSortWaves = kSortThreads / kWave;
@@ -195,22 +195,29 @@ __global__ __launch_bounds__(kSortThreads) void radix_hist_kernel(const int32_t 
 }
 
 // Stable scatter of one tile.  Wave w owns the tile's elements
-// [w * 512, (w + 1) * 512) and walks them in 8 rounds of 64 consecutive
+// [w * 1024, (w + 1) * 1024) and walks them in 16 rounds of 64 consecutive
 // elements, so (wave, round, lane) order is input order.  Inside a round the
 // lanes holding the same digit are found with 8 ballots; a lane's rank is the
 // count of such lanes below it plus what earlier rounds of its wave placed.
+// The tile is then staged in LDS in digit order (digit runs in input order)
+// and written back run by run, so consecutive lanes store consecutive
+// addresses of a digit's output range instead of scattering single words.
 __global__ __launch_bounds__(kSortThreads) void radix_scatter_kernel(
     const int32_t *kin, const int32_t *vin, int32_t *kout, int32_t *vout, int64_t n, int shift,
     int64_t ntiles, const int32_t *offs) {
     __shared__ int wcnt[kSortWaves][kBins];
     __shared__ int tile_off[kBins];
+    __shared__ int tile_start[kBins];
+    __shared__ int skey[kSortTile];
+    __shared__ int sval[kSortTile];
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
     for (int w = 0; w < kSortWaves; ++w) wcnt[w][threadIdx.x] = 0;
     tile_off[threadIdx.x] = offs[(int64_t)threadIdx.x * ntiles + blockIdx.x];
     __syncthreads();
 
-    const int64_t base = (int64_t)blockIdx.x * kSortTile + (int64_t)wave * (kSortRounds * kWave);
+    const int64_t tile0 = (int64_t)blockIdx.x * kSortTile;
+    const int64_t base = tile0 + (int64_t)wave * (kSortRounds * kWave);
     int key[kSortRounds], val[kSortRounds], rank[kSortRounds], dig[kSortRounds];
 #pragma unroll
     for (int i = 0; i < kSortRounds; ++i) {
@@ -234,23 +241,44 @@ __global__ __launch_bounds__(kSortThreads) void radix_scatter_kernel(
         __builtin_amdgcn_wave_barrier();
     }
     __syncthreads();
-    if (threadIdx.x < kBins) {
-        int s = 0;
+    // per digit: waves' offsets inside the digit's run, then the run starts
+    // (exclusive scan of the digit totals over the tile)
+    int total = 0;
+    {
+        const int d = threadIdx.x;
         for (int w = 0; w < kSortWaves; ++w) {
-            const int c = wcnt[w][threadIdx.x];
-            wcnt[w][threadIdx.x] = s;
-            s += c;
+            const int c = wcnt[w][d];
+            wcnt[w][d] = total;
+            total += c;
         }
+        tile_start[d] = total;
     }
+    __syncthreads();
+    for (int off = 1; off < kBins; off <<= 1) {
+        const int add = (int)threadIdx.x >= off ? tile_start[threadIdx.x - off] : 0;
+        __syncthreads();
+        tile_start[threadIdx.x] += add;
+        __syncthreads();
+    }
+    tile_start[threadIdx.x] -= total;  // inclusive -> exclusive
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < kSortRounds; ++i) {
         const int64_t q = base + (int64_t)i * kWave + lane;
         if (q < n) {
-            const int64_t pos = (int64_t)tile_off[dig[i]] + wcnt[wave][dig[i]] + rank[i];
-            kout[pos] = key[i];
-            vout[pos] = val[i];
+            const int lp = tile_start[dig[i]] + wcnt[wave][dig[i]] + rank[i];
+            skey[lp] = key[i];
+            sval[lp] = val[i];
         }
+    }
+    __syncthreads();
+    const int tile_n = (int)min<int64_t>(kSortTile, n - tile0);
+    for (int lp = threadIdx.x; lp < tile_n; lp += kSortThreads) {
+        const int k = skey[lp];
+        const int d = ((uint32_t)k >> shift) & (kBins - 1);
+        const int64_t pos = (int64_t)tile_off[d] + (lp - tile_start[d]);
+        kout[pos] = k;
+        vout[pos] = sval[lp];
     }
 }
 
