@@ -300,6 +300,20 @@ nsd_status nsd_gather_i32(int32_t n, const int32_t *perm, const int32_t *src, in
 nsd_status nsd_validate_csr(const nsd_csr *A, int check_sorted, void *ws, size_t ws_bytes,
                             void *stream);
 
+/* Bytes of `ws` for nsd_validate_coo.  dims: host array of `order` sizes. */
+nsd_status nsd_validate_coo_workspace_size(int32_t order, const int32_t *dims, int32_t nnz,
+                                           size_t *bytes);
+
+/* Checks a COO tensor of order 2 to NSD_MAX_ORDER (the dictionary of
+ * Section 2 stores each key once): every coordinate of mode m in
+ * [0, dims[m]) (else NSD_ERR_BAD_FORMAT) and, when check_unique, no key
+ * twice (else NSD_ERR_DUPLICATE; found by sorting the entries
+ * lexicographically).  dims and coords are HOST arrays of `order` sizes /
+ * device pointers to [nnz] int32 coordinates.  Synchronous. */
+nsd_status nsd_validate_coo(int32_t order, const int32_t *dims, int32_t nnz,
+                            const int32_t *const *coords, int check_unique, void *ws,
+                            size_t ws_bytes, void *stream);
+
 /* ------------------------------------------------------------- forward */
 
 /* y = A x (SpMV).  x [ncols], y [nrows].  Async. */
@@ -331,6 +345,23 @@ nsd_status nsd_sddmm(const nsd_csr *A, const float *X, const float *Y, int32_t k
  */
 nsd_status nsd_spmm_t(const nsd_csr *A, const nsd_csc *At, const float *G, int32_t k,
                       float alpha, float *out, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Vector-Jacobian product of C = A X (the reverse-mode result the paper's
+ * tensorized forward mode computes for the matrix product, Sections 4.2
+ * and 6.4) for an upstream gradient G = dL/dC [nrows x k] (NULL: all ones):
+ *   dA[p] = <G[i,:], X[j,:]> on A's pattern (SDDMM, A's storage order),
+ *   dX = A^T G  [ncols x k].
+ * X [ncols x k].  One fused pass over the columns when k fits it (see
+ * nsd_loss_bilinear), else SDDMM then the transposed product.  Workspace:
+ * nsd_workspace_size(A, At, k).  Async.
+ */
+nsd_status nsd_spmm_vjp(const nsd_csr *A, const nsd_csc *At, const float *X, const float *G,
+                        int32_t k, float *dA, float *dX, void *ws, size_t ws_bytes, void *stream);
+
+/* The same for y = A x: gy [nrows] (NULL: ones), dA [nnz], dx [ncols]. */
+nsd_status nsd_spmv_vjp(const nsd_csr *A, const nsd_csc *At, const float *x, const float *gy,
+                        float *dA, float *dx, void *ws, size_t ws_bytes, void *stream);
 
 /* -------------------------------------------------------- fused losses */
 /* `seed` is the upstream gradient dL_out/dL (1 for plain training); it scales

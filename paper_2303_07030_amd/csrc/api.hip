@@ -333,6 +333,37 @@ nsd_status nsd_loss_bilinear(const nsd_csr *A, const nsd_csc *At, const float *H
     return segreduce(cols_params(A, At, G, k, seed, dH, w.part_col), st);
 }
 
+nsd_status nsd_spmm_vjp(const nsd_csr *A, const nsd_csc *At, const float *X, const float *G,
+                        int32_t k, float *dA, float *dX, void *ws, size_t ws_bytes, void *stream) {
+    NSD_TRY(check_csr(A, true, false));
+    NSD_TRY(check_csc(At, A));
+    NSD_REQUIRE(k >= 1, "k = %d < 1", k);
+    NSD_REQUIRE(A->ncols == 0 || dX != nullptr, "dX is NULL");
+    NSD_REQUIRE(A->nnz == 0 || (X && dA), "X/dA is NULL");
+    ComputeWs w;
+    NSD_TRY(carve_compute(ws, ws_bytes, A, At, k, &w));
+    hipStream_t st = as_stream(stream);
+    if (A->nnz > 0) {
+        // one pass over the columns: own row X_j, gathered row G_i (NULL:
+        // ones): dA[p] = <G_i, X_j>, dX = A^T G; no loss
+        const DualPass pass = col_dual(A, At, G, X, k, 1.f, dX, w.part_col, dA, 1.f, false);
+        if (col_dual_ok(pass)) {
+            DualParams f;
+            f.pass[0] = pass;
+            f.npass = 1;
+            f.loss_part = w.loss_part;
+            return dual_fused(kDualLin, f, NSD_KERNEL_DUAL, LossJob{}, st);
+        }
+        NSD_TRY(sddmm(sddmm_params(A, G, X, k, 1.f, dA), st));
+    }
+    return segreduce(cols_params(A, At, G, k, 1.f, dX, w.part_col), st);
+}
+
+nsd_status nsd_spmv_vjp(const nsd_csr *A, const nsd_csc *At, const float *x, const float *gy,
+                        float *dA, float *dx, void *ws, size_t ws_bytes, void *stream) {
+    return nsd_spmm_vjp(A, At, x, gy, 1, dA, dx, ws, ws_bytes, stream);
+}
+
 nsd_status nsd_dot(int64_t n, const float *x, const float *y, double alpha, int accumulate,
                    double *out, void *ws, size_t ws_bytes, void *stream) {
     NSD_REQUIRE(n >= 0, "negative length");

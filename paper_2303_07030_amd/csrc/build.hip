@@ -436,6 +436,30 @@ __global__ void validate_csr_kernel(int32_t nrows, int32_t ncols, int32_t nnz,
     }
 }
 
+// Coordinate arrays of a COO tensor, one per mode.
+struct CoordArrays {
+    const int32_t *p[NSD_MAX_ORDER];
+};
+
+// Flags (bit 2) an entry equal in every coordinate to the entry before it in
+// lexicographic order perm.
+__global__ void adjacent_equal_kernel(int64_t n, int order, CoordArrays c, const int32_t *perm,
+                                      int32_t *flag) {
+    const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (q == 0 || q >= n) return;
+    const int32_t a = perm[q], b = perm[q - 1];
+    bool eq = true;
+    for (int m = 0; m < order; ++m) eq = eq && c.p[m][a] == c.p[m][b];
+    if (eq) atomicOr(flag, 2);
+}
+
+static size_t validate_coo_ws_bytes(int64_t n, int32_t max_dim) {
+    Carver c(nullptr);
+    c.take<int32_t>(64);  // flag
+    for (int i = 0; i < 4; ++i) c.take<int32_t>(n > 0 ? n : 1);
+    return c.bytes() + sort_ws_bytes(n, max_dim);
+}
+
 static nsd_status read_flag(int32_t *flag_dev, int32_t *flag_host, hipStream_t st) {
     NSD_HIP(hipMemcpyAsync(flag_host, flag_dev, sizeof(int32_t), hipMemcpyDeviceToHost, st));
     NSD_HIP(hipStreamSynchronize(st));
@@ -611,6 +635,75 @@ nsd_status nsd_coo_mode_index(int32_t nnz, int32_t dim, const int32_t *key, int3
     }
     NSD_TRY(segptr_from_sorted(nnz, dim, segidx, segptr, st));
     NSD_HIP(hipStreamSynchronize(st));
+    return NSD_OK;
+}
+
+nsd_status nsd_validate_coo_workspace_size(int32_t order, const int32_t *dims, int32_t nnz,
+                                           size_t *bytes) {
+    NSD_REQUIRE(bytes != nullptr && dims != nullptr, "null pointer");
+    NSD_REQUIRE(order >= 2 && order <= NSD_MAX_ORDER, "order %d outside [2, %d]", order,
+                NSD_MAX_ORDER);
+    NSD_REQUIRE(nnz >= 0, "negative nnz");
+    int32_t max_dim = 1;
+    for (int m = 0; m < order; ++m) {
+        NSD_REQUIRE(dims[m] >= 0, "negative dimension");
+        max_dim = std::max(max_dim, dims[m]);
+    }
+    *bytes = validate_coo_ws_bytes(nnz, max_dim);
+    return NSD_OK;
+}
+
+nsd_status nsd_validate_coo(int32_t order, const int32_t *dims, int32_t nnz,
+                            const int32_t *const *coords, int check_unique, void *ws,
+                            size_t ws_bytes, void *stream) {
+    size_t need = 0;
+    NSD_TRY(nsd_validate_coo_workspace_size(order, dims, nnz, &need));
+    if (nnz == 0) return NSD_OK;
+    NSD_REQUIRE(coords != nullptr, "coords is NULL");
+    CoordArrays c;
+    int32_t max_dim = 1;
+    for (int m = 0; m < order; ++m) {
+        NSD_REQUIRE(coords[m] != nullptr, "coordinate array %d is NULL", m);
+        NSD_REQUIRE(dims[m] >= 1, "nnz > 0 needs non-empty dimensions");
+        c.p[m] = coords[m];
+        max_dim = std::max(max_dim, dims[m]);
+    }
+    if (ws == nullptr || ws_bytes < need)
+        return fail(NSD_ERR_WORKSPACE, "workspace %zu bytes at %p, need %zu", ws_bytes, ws, need);
+    hipStream_t st = as_stream(stream);
+    Carver cv(ws);
+    int32_t *flag = cv.take<int32_t>(64);
+    int32_t *key = cv.take<int32_t>(nnz);
+    int32_t *key_sorted = cv.take<int32_t>(nnz);
+    int32_t *perm[2] = {cv.take<int32_t>(nnz), cv.take<int32_t>(nnz)};
+    void *sort_ws = cv.base + cv.bytes();
+    NSD_HIP(hipMemsetAsync(flag, 0, sizeof(int32_t), st));
+    for (int m = 0; m < order; ++m) {
+        key_range_kernel<<<grid_for(nnz), kThreads, 0, st>>>(nnz, dims[m], c.p[m], flag);
+        NSD_TRY(check_launch("key_range_kernel"));
+    }
+    int32_t h = 0;
+    NSD_TRY(read_flag(flag, &h, st));
+    if (h) return fail(NSD_ERR_BAD_FORMAT, "COO coordinate out of range");
+    if (!check_unique || nnz < 2) return NSD_OK;
+    // lexicographic order: stable sorts by the last coordinate first
+    const int32_t *pm = nullptr;
+    int cur = 0;
+    for (int m = order - 1; m >= 0; --m) {
+        const int32_t *k = c.p[m];
+        if (pm) {
+            gather_kernel<int32_t><<<grid_for(nnz), kThreads, 0, st>>>(nnz, pm, c.p[m], key);
+            NSD_TRY(check_launch("gather_kernel"));
+            k = key;
+        }
+        NSD_TRY(radix_sort_pairs(nnz, dims[m], k, pm, key_sorted, perm[cur], sort_ws, st));
+        pm = perm[cur];
+        cur ^= 1;
+    }
+    adjacent_equal_kernel<<<grid_for(nnz), kThreads, 0, st>>>(nnz, order, c, pm, flag);
+    NSD_TRY(check_launch("adjacent_equal_kernel"));
+    NSD_TRY(read_flag(flag, &h, st));
+    if (h) return fail(NSD_ERR_DUPLICATE, "COO coordinates repeat a key");
     return NSD_OK;
 }
 

@@ -140,6 +140,12 @@ _SIGS = {
     "nsd_ttv": (C.c_int, [_TTV, _P, _P, _P, _P, _SZ, _P]),
     "nsd_ttv_vjp": (C.c_int, [_TTV, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "nsd_dot": (C.c_int, [C.c_int64, _P, _P, C.c_double, C.c_int, _P, _P, _SZ, _P]),
+    "nsd_spmm_vjp": (C.c_int, [C.POINTER(nsd_csr), C.POINTER(nsd_csc), _P, _P, _I, _P, _P, _P,
+                               _SZ, _P]),
+    "nsd_spmv_vjp": (C.c_int, [C.POINTER(nsd_csr), C.POINTER(nsd_csc), _P, _P, _P, _P, _P, _SZ,
+                               _P]),
+    "nsd_validate_coo_workspace_size": (C.c_int, [_I, _P, _I, C.POINTER(_SZ)]),
+    "nsd_validate_coo": (C.c_int, [_I, _P, _I, _P, C.c_int, _P, _SZ, _P]),
     "nsd_axpby": (C.c_int, [C.c_int64, C.c_float, _P, C.c_float, _P, _P]),
     "nsd_cpn_workspace_size": (C.c_int, [C.POINTER(nsd_coon), _I, C.POINTER(_SZ)]),
     "nsd_loss_cpn": (C.c_int, [C.POINTER(nsd_coon), C.POINTER(_P), _I, C.c_float, _P, _P,
@@ -461,3 +467,31 @@ def nsd_dot(n, x, y, alpha, accumulate, out, ws, stream=None):
 
 def nsd_axpby(n, alpha, x, beta, y, stream=None):
     _check(_lib.nsd_axpby(n, alpha, _p(x), beta, _p(y), _stream(stream)), "nsd_axpby")
+
+
+def nsd_spmm_vjp(A: nsd_csr, At: nsd_csc, X, G, k, dA, dX, ws, stream=None):
+    _check(_lib.nsd_spmm_vjp(C.byref(A), C.byref(At), _p(X), _p(G), k, _p(dA), _p(dX), _p(ws),
+                             _nbytes(ws), _stream(stream)), "nsd_spmm_vjp")
+
+
+def nsd_spmv_vjp(A: nsd_csr, At: nsd_csc, x, gy, dA, dx, ws, stream=None):
+    _check(_lib.nsd_spmv_vjp(C.byref(A), C.byref(At), _p(x), _p(gy), _p(dA), _p(dx), _p(ws),
+                             _nbytes(ws), _stream(stream)), "nsd_spmv_vjp")
+
+
+def _host_i32(vals):
+    return (C.c_int32 * len(vals))(*[int(v) for v in vals])
+
+
+def nsd_validate_coo_workspace_size(dims, nnz) -> int:
+    out = _SZ(0)
+    _check(_lib.nsd_validate_coo_workspace_size(len(dims), C.cast(_host_i32(dims), _P), nnz,
+                                                C.byref(out)), "nsd_validate_coo_workspace_size")
+    return out.value
+
+
+def nsd_validate_coo(dims, nnz, coords, check_unique, ws, stream=None):
+    ptrs = (C.c_void_p * len(coords))(*[_p(c) for c in coords])
+    _check(_lib.nsd_validate_coo(len(dims), C.cast(_host_i32(dims), _P), nnz, C.cast(ptrs, _P),
+                                 int(bool(check_unique)), _p(ws), _nbytes(ws), _stream(stream)),
+           "nsd_validate_coo")

@@ -811,3 +811,71 @@ def test_loss_cpn_order3_equals_cp(nsd, orc):
     assert np.array_equal(a[1], b[1])
     for x, y in zip(a[2], b[2]):
         assert np.array_equal(x, y)
+
+
+# --------------------------------------------------- VJP of the product
+
+@pytest.mark.parametrize("k,ones", [(1, False), (1, True), (16, False), (64, False),
+                                    (300, False)])
+def test_spmm_vjp(nsd, orc, edge_A, k, ones):
+    # k = 300 is beyond the fused column pass: SDDMM then A^T G
+    A, D, rows, cols = edge_A
+    rng = np.random.default_rng(300 + k)
+    X = rng.standard_normal((A.ncols, k)).astype(np.float32)
+    G = None if ones else rng.standard_normal((A.nrows, k)).astype(np.float32)
+    dA = torch.full((A.nnz,), np.nan, dtype=torch.float32, device="cuda")
+    dX = torch.full((A.ncols, k), np.nan, dtype=torch.float32, device="cuda")
+    nsd.nsd_spmm_vjp(A.desc, A.csc, dev(X), None if G is None else dev(G), k, dA, dX,
+                     A.workspace(k))
+    ref, mag = orc.sddmm(D, G, X, k, rows, cols)
+    assert_mag_close(host(dA), ref, mag, what=f"dA k={k}")
+    ref, mag = orc.spmm_t(D, G, k)
+    assert_mag_close(host(dX), ref, mag, what=f"dX k={k}")
+
+
+def test_spmv_vjp(nsd, orc, edge_A):
+    A, D, rows, cols = edge_A
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal(A.ncols).astype(np.float32)
+    gy = rng.standard_normal(A.nrows).astype(np.float32)
+    dA = torch.full((A.nnz,), np.nan, dtype=torch.float32, device="cuda")
+    dx = torch.full((A.ncols,), np.nan, dtype=torch.float32, device="cuda")
+    nsd.nsd_spmv_vjp(A.desc, A.csc, dev(x), dev(gy), dA, dx, A.workspace(1))
+    ref, mag = orc.sddmm(D, gy.reshape(-1, 1), x.reshape(-1, 1), 1, rows, cols)
+    assert_mag_close(host(dA), ref, mag, what="dA")
+    ref, mag = orc.spmm_t(D, gy.reshape(-1, 1), 1)
+    assert_mag_close(host(dx), ref[:, 0], mag[:, 0], what="dx")
+
+
+# ---------------------------------------------------------- COO validator
+
+@pytest.mark.parametrize("order", [2, 3, 6])
+def test_validate_coo(nsd, order):
+    rng = np.random.default_rng(order)
+    dims = (7, 300, 5, 11, 3, 4)[:order]
+    size = int(np.prod(dims))
+    nnz = min(size // 2, 5000)
+    keys = rng.choice(size, size=nnz, replace=False)
+    coords = [c.astype(np.int32) for c in np.unravel_index(keys, dims)]
+
+    def check(cs, unique=True):
+        ws = torch.empty(nsd.nsd_validate_coo_workspace_size(dims, len(cs[0])),
+                         dtype=torch.uint8, device="cuda")
+        nsd.nsd_validate_coo(dims, len(cs[0]), [dev(c) for c in cs], unique, ws)
+
+    check(coords)                                   # distinct keys in range
+    dup = [np.concatenate([c, c[[17]]]) for c in coords]
+    with pytest.raises(nsd.NsdError) as e:
+        check(dup)
+    assert e.value.status == nsd.NSD_ERR_DUPLICATE
+    check(dup, unique=False)                        # duplicates allowed when not asked
+    bad = [c.copy() for c in coords]
+    bad[order - 1][123] = dims[order - 1]
+    with pytest.raises(nsd.NsdError) as e:
+        check(bad)
+    assert e.value.status == nsd.NSD_ERR_BAD_FORMAT
+    bad[order - 1][123] = -1
+    with pytest.raises(nsd.NsdError) as e:
+        check(bad, unique=False)
+    assert e.value.status == nsd.NSD_ERR_BAD_FORMAT
+    check([c[:1] for c in coords])                  # a single entry
