@@ -83,9 +83,17 @@ def source_digest(kernel=None):
         files = [f for f in files if f.endswith(".hpp") or f == KERNEL_SOURCE[kernel]]
     paths = [os.path.join(d, f) for f in files] + [os.path.join(ROOT, "include", "nsd.h")]
     for path in paths:
-        with open(path, "rb") as fh:
-            h.update(fh.read())
+        with open(path, "r", encoding="utf-8") as fh:
+            h.update(_code_only(fh.read()).encode())
     return h.hexdigest()[:16]
+
+
+def _code_only(text):
+    """Source text without comments and blank space, so that edits to
+    comments alone keep a kernel's digest."""
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
 
 
 def committed_traffic(kernel, workload):
