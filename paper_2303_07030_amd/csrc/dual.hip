@@ -224,9 +224,10 @@ constexpr int dual_unroll() {
 #ifdef NSD_DUAL_UNROLL
     return reduce_unroll<G, NSD_DUAL_UNROLL>();
 #else
-    // measured on MI355X: two entries per batch up to 32-lane slots, four
-    // for full-wave slots (k > 128)
-    return reduce_unroll<G, (G >= 64 || G == 1) ? 4 : 2>();
+    // measured on MI355X: eight entries per batch for full-wave slots
+    // (k > 128), four for 32-lane slots, two for narrower ones, four for
+    // single-lane slots
+    return reduce_unroll<G, G >= 64 ? 8 : (G >= 32 || G == 1 ? 4 : 2)>();
 #endif
 }
 

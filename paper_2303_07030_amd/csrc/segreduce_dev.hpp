@@ -377,10 +377,11 @@ constexpr int sgr_unroll() {
 #ifdef NSD_SGR_UNROLL
     return NSD_SGR_UNROLL;
 #else
-    // measured on MI355X: two rows in flight per lane for 16- and 32-lane
-    // slots (more resident waves beat deeper batches), four for full-wave
-    // slots, eight for the narrow slots of small widths
-    return G >= 64 ? 4 : (G >= 16 ? 2 : 8);
+    // measured on MI355X: eight rows in flight per lane for 16-lane slots
+    // (the SpMM row pass of k = 64, whose short items are latency-bound),
+    // two for 32-lane slots, four for full-wave slots, eight for the narrow
+    // slots of small widths
+    return G >= 64 ? 4 : (G >= 32 ? 2 : 8);
 #endif
 }
 
