@@ -44,11 +44,16 @@ struct DualSlot {
     Vec<VEC> ownv; // own[row] when kKeepOwn: the open segment's own dense row
     double &lsum;
 
-    // Keeping the open segment's own row pays where a slot is a whole wave
-    // (the branches on segment boundaries are then uniform); with several
-    // slots per wave they diverge, and per-entry loads (L1 hits) measured
-    // faster.
-    static constexpr bool kKeepOwn = G == 64;
+    // Keeping the open segment's own row pays for slots of 32 lanes or more
+    // (measured on MI355X: full-wave slots and the 32-lane slots of k = 128);
+    // with four slots per wave the branches on segment boundaries diverge
+    // more, and per-entry loads (L1 hits) measured faster.  Build-time knob:
+    // NSD_KEEP_OWN_MIN.
+#ifdef NSD_KEEP_OWN_MIN
+    static constexpr bool kKeepOwn = G >= NSD_KEEP_OWN_MIN;
+#else
+    static constexpr bool kKeepOwn = G >= 32;
+#endif
 
     __device__ __forceinline__ DualSlot(const DualPass &m_, int64_t s_, int lane_, double &ls)
         : m(m_), s(s_), k(m_.s.k), lane(lane_), g(lane_ % G), col((lane_ % G) * VEC), lsum(ls) {

@@ -116,11 +116,15 @@ __global__ __launch_bounds__(kBlock) void jvp_kernel(JvpParams f) {
     st.finish();
 }
 
-// Entries per batch: two rows are gathered per entry, so narrow slots keep
-// four in flight instead of the plain gather-reduce's eight.
+// Entries per batch (two rows are gathered per entry): four, measured on
+// MI355X for the 16-lane slots of k = 64.
 template <int G>
 constexpr int jvp_unroll() {
-    return G >= 64 ? 4 : (G >= 16 ? 2 : 4);
+#ifdef NSD_JVP_UNROLL
+    return NSD_JVP_UNROLL;
+#else
+    return 4;
+#endif
 }
 
 template <int VEC, int G>
