@@ -803,8 +803,8 @@ def test_loss_cpn_order3_equals_cp(nsd, orc):
     from paper_2303_07030_amd.operand import DeviceCoo3, DeviceCooN
     d = synth.make("cp", "small")
     F = [d["F1"], d["F2"], d["F3"]]
-    X3 = DeviceCoo3(d["dims"], d["i"], d["j"], d["k"], d["val"], rank_hint=d["rank"])
-    XN = DeviceCooN(d["dims"], [d["i"], d["j"], d["k"]], d["val"], rank_hint=d["rank"])
+    X3 = DeviceCoo3(d["dims"], d["i"], d["j"], d["k"], d["val"], item_len=24)
+    XN = DeviceCooN(d["dims"], [d["i"], d["j"], d["k"]], d["val"], item_len=24)
     a = run_cp(nsd, X3, F, d["rank"])
     b = run_cpn(nsd, XN, F, d["rank"])
     check_cpn(orc, d["dims"], [d["i"], d["j"], d["k"]], d["val"], F, d["rank"], b)
