@@ -451,6 +451,8 @@ def main():
                for n, v in per_kernel.items()}
 
     cold = cold_steps(torch, dev, S, args) if args.cold_steps else None
+    stream = stream_copy(torch, dev)
+    stream["frac"] = round(achieved / stream["copy_GBps"], 4)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -477,10 +479,35 @@ def main():
         "kernels": kernels,
         "preprocess_ms": round(prep_ms, 2), "generate_s": round(gen_s, 1),
         "cold": cold,
+        "achievable": stream,
         "cpu_baseline": cpu,
         "source_digest": source_digest(),
     }
     print(json.dumps(out))
+
+
+def stream_copy(torch, dev, nbytes=1 << 30, reps=10):
+    """Achievable streaming rate on this GPU: a plain device-to-device copy
+    of 1 GiB (read + write bytes over time, median of reps), beside which the
+    dominant kernel's algorithmic rate is also given as a fraction."""
+    n = nbytes // 4
+    src = torch.ones(n, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(reps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+    ms = float(np.median(times))
+    del src, dst
+    return {"copy_GBps": round(2 * nbytes / (ms * 1e-3) / 1e9, 1), "copy_bytes": nbytes,
+            "note": "plain device copy, read + write bytes; frac = roofline.achieved / copy"}
 
 
 def cold_steps(torch, dev, S, args):
