@@ -208,8 +208,15 @@ __device__ __forceinline__ void dual_block(const DualPass &m, int b, double &lsu
     }
 }
 
+// Occupancy floor (waves per SIMD), a build-time tuning knob.
+#ifdef NSD_DUAL_WAVES
+#define NSD_DUAL_OCCUPANCY __attribute__((amdgpu_waves_per_eu(NSD_DUAL_WAVES, 8)))
+#else
+#define NSD_DUAL_OCCUPANCY
+#endif
+
 template <int KIND, int VEC, int G, int U>
-__global__ __launch_bounds__(kBlock) void dual_kernel(DualParams f) {
+__global__ __launch_bounds__(kBlock) NSD_DUAL_OCCUPANCY void dual_kernel(DualParams f) {
     if (f.early.loss && blockIdx.x == gridDim.x - 1) {
         loss_total_block(f.early);
         return;

@@ -290,8 +290,15 @@ nsd_status loss_finalize(const double *part, int64_t n, double *loss, hipStream_
 // rows of the item (gather-reduce) and ||C_i||^2 of the rows completed in it
 // into the block's loss partial; a long row's chunk leaves a partial instead.
 // Blocks past the items zero the C rows of empty rows.
+// Occupancy floor (waves per SIMD), a build-time tuning knob.
+#ifdef NSD_FROB_WAVES
+#define NSD_FROB_OCCUPANCY __attribute__((amdgpu_waves_per_eu(NSD_FROB_WAVES, 8)))
+#else
+#define NSD_FROB_OCCUPANCY
+#endif
+
 template <int VEC, int G, int U>
-__global__ __launch_bounds__(kBlock) void frob_row_kernel(FrobParams f) {
+__global__ __launch_bounds__(kBlock) NSD_FROB_OCCUPANCY void frob_row_kernel(FrobParams f) {
     constexpr int kSlots = kBlock / G;
     const SgrParams &a = f.rows;
     const int g = threadIdx.x % G;
