@@ -277,9 +277,10 @@ static nsd_status launch_cp(CpParams f, double *loss, hipStream_t st) {
     job.p1 = f.loss_part;
     job.n1 = grid;
     job.loss = loss;
-    for (int i = 0; i < 3; ++i)
-        NSD_TRY((launch_fix<VEC, G>(f.m[i].s, nullptr, 0.0, st, i == 2 ? job : LossJob{})));
-    return NSD_OK;
+    FixJobs fx;
+    for (int i = 0; i < 3; ++i) add_fix(fx, f.m[i].s);
+    fx.loss = job;
+    return launch_fixes<VEC, G>(fx, st);
 }
 
 struct CpLauncher {

@@ -293,9 +293,10 @@ static nsd_status launch_cpn(CpnParams<N> f, double *loss, hipStream_t st) {
     job.p1 = f.loss_part;
     job.n1 = grid;
     job.loss = loss;
-    for (int i = 0; i < N; ++i)
-        NSD_TRY((launch_fix<VEC, G>(f.m[i].s, nullptr, 0.0, st, i == N - 1 ? job : LossJob{})));
-    return NSD_OK;
+    FixJobs fx;
+    for (int i = 0; i < N; ++i) add_fix(fx, f.m[i].s);
+    fx.loss = job;
+    return launch_fixes<VEC, G>(fx, st);
 }
 
 template <int N>

@@ -277,10 +277,10 @@ static nsd_status launch_dual(DualParams f, int probe_id, LossJob job, hipStream
         probe_end(probe_id, st);
         NSD_TRY(check_launch("dual_kernel"));
     }
-    for (int i = 0; i < f.npass; ++i)
-        NSD_TRY((launch_fix<VEC, G>(f.pass[i].s, nullptr, 0.0, st,
-                                    i == f.npass - 1 ? job : LossJob{})));
-    return NSD_OK;
+    FixJobs fx;
+    for (int i = 0; i < f.npass; ++i) add_fix(fx, f.pass[i].s);
+    fx.loss = job;
+    return launch_fixes<VEC, G>(fx, st);
 }
 
 template <int KIND>

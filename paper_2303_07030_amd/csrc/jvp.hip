@@ -137,8 +137,10 @@ static nsd_status launch_jvp(JvpParams f, hipStream_t st) {
     jvp_kernel<VEC, G, jvp_unroll<G>()><<<grid, kBlock, 0, st>>>(f);
     probe_end(NSD_KERNEL_JVP, st);
     NSD_TRY(check_launch("jvp_kernel"));
-    NSD_TRY((launch_fix<VEC, G>(f.c, nullptr, 0.0, st)));
-    return launch_fix<VEC, G>(f.d, nullptr, 0.0, st);
+    FixJobs fx;
+    add_fix(fx, f.c);
+    add_fix(fx, f.d);
+    return launch_fixes<VEC, G>(fx, st);
 }
 
 struct JvpLauncher {

@@ -263,37 +263,30 @@ __device__ __forceinline__ void loss_total_block(const LossJob &job) {
 // ----------------------------------------------------------- long segments
 
 // out[seg] = alpha * sum of the segment's chunk partials, in chunk order per
-// row group, the groups then combined by a fixed butterfly.  Blocks below
-// wave_blocks give one wave to each non-huge long segment; the blocks after
-// them give a whole block to each huge segment.  When seg_loss is given,
-// beta * ||out[seg]||^2 is stored for every long segment.
-//
-// With a loss job, the grid's last block computes the call's loss total
-// instead (every partial it sums was written by earlier launches).
+// row group, the groups then combined by a fixed butterfly.  Of a pass's
+// blocks, those below wave_blocks give one wave to each non-huge long
+// segment; the blocks after them give a whole block to each huge segment.
+// When seg_loss is given, beta * ||out[seg]||^2 is stored for every long
+// segment.  b is the block's index within the pass.
 template <int VEC, int G>
-__global__ __launch_bounds__(kBlock) void sgr_fix_kernel(SgrParams a, int wave_blocks,
-                                                         double *seg_loss, double beta,
-                                                         LossJob job) {
-    if (job.loss && blockIdx.x == gridDim.x - 1) {
-        loss_total_block(job);
-        return;
-    }
+__device__ __forceinline__ void fix_block(const SgrParams &a, int b, int wave_blocks,
+                                          double *seg_loss, double beta) {
     constexpr int RG = kWave / G;  // row groups per wave
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int q = lane / G, g = lane % G;
     const int64_t k = a.k;
     const int L = a.plan.item_len;
     __shared__ float red[kBlockWaves][G * VEC];
-    const bool huge = (int)blockIdx.x >= wave_blocks;
+    const bool huge = b >= wave_blocks;
     int64_t i;
     int nsum, qq;  // number of groups sharing the chunks, this lane's group
     if (!huge) {
-        i = (int64_t)blockIdx.x * kBlockWaves + wave;
+        i = (int64_t)b * kBlockWaves + wave;
         if (i >= a.plan.nlong) return;
         nsum = RG;
         qq = q;
     } else {
-        i = a.plan.huge_idx[blockIdx.x - wave_blocks];
+        i = a.plan.huge_idx[b - wave_blocks];
         nsum = RG * kBlockWaves;
         qq = wave * RG + q;
     }
@@ -362,6 +355,42 @@ __global__ __launch_bounds__(kBlock) void sgr_fix_kernel(SgrParams a, int wave_b
     }
 }
 
+// Long segments of up to kMaxFixJobs passes, combined in one launch (each
+// pass on its own block range), and the call's loss total.
+constexpr int kMaxFixJobs = NSD_MAX_ORDER;
+
+struct FixJob {
+    SgrParams a;
+    double *seg_loss = nullptr;
+    double beta = 0.0;
+    int wave_blocks = 0, blocks = 0;
+};
+
+struct FixJobs {
+    FixJob job[kMaxFixJobs];
+    int n = 0;
+    LossJob loss;  // with a loss job, the grid's last block computes the
+                   // call's loss total (its partials come from earlier launches)
+};
+
+static_assert(sizeof(FixJobs) <= 4096, "combine jobs fit the kernel argument limit");
+
+template <int VEC, int G>
+__global__ __launch_bounds__(kBlock) void sgr_fix_kernel(FixJobs f) {
+    if (f.loss.loss && blockIdx.x == gridDim.x - 1) {
+        loss_total_block(f.loss);
+        return;
+    }
+    int b = blockIdx.x;
+    for (int t = 0; t < f.n; ++t) {
+        const FixJob &j = f.job[t];
+        if (b < j.blocks) {
+            fix_block<VEC, G>(j.a, b, j.wave_blocks, j.seg_loss, j.beta);
+            return;
+        }
+        b -= j.blocks;
+    }
+}
 
 // Entries per batch (rows in flight per lane).  The defaults can be changed
 // at build time (-DNSD_SGR_UNROLL=..., and likewise for the other kernel
@@ -394,19 +423,38 @@ constexpr int sddmm_unroll() {
 #endif
 }
 
-// Combines the long segments of a pass (when it has any) and runs the loss
-// job (when given) in the same launch.
+// Adds a pass's long segments to a combined launch.
+inline void add_fix(FixJobs &f, const SgrParams &a, double *seg_loss = nullptr,
+                    double beta = 0.0) {
+    FixJob &j = f.job[f.n++];
+    j.a = a;
+    j.seg_loss = seg_loss;
+    j.beta = beta;
+    j.wave_blocks = (int)ceil_div(a.plan.nlong, kBlockWaves);
+    j.blocks = a.plan.nlong > 0 ? j.wave_blocks + a.plan.nhuge : 0;
+}
+
+// Combines the long segments of every pass in f (those that have any) and
+// runs the loss job (when given), all in one launch.
+template <int VEC, int G>
+inline nsd_status launch_fixes(const FixJobs &f, hipStream_t st) {
+    int grid = 0;
+    for (int t = 0; t < f.n; ++t) grid += f.job[t].blocks;
+    if (grid == 0 && !f.loss.loss) return NSD_OK;
+    probe_begin(NSD_KERNEL_SGR_FIX, st);
+    sgr_fix_kernel<VEC, G><<<grid + (f.loss.loss ? 1 : 0), kBlock, 0, st>>>(f);
+    probe_end(NSD_KERNEL_SGR_FIX, st);
+    return check_launch("sgr_fix_kernel");
+}
+
+// One pass's long segments and the loss job, in one launch.
 template <int VEC, int G>
 inline nsd_status launch_fix(const SgrParams &a, double *seg_loss, double beta, hipStream_t st,
                              LossJob job = LossJob{}) {
-    const int wave_blocks = (int)ceil_div(a.plan.nlong, kBlockWaves);
-    const int grid = a.plan.nlong > 0 ? wave_blocks + a.plan.nhuge : 0;
-    if (grid == 0 && !job.loss) return NSD_OK;
-    probe_begin(NSD_KERNEL_SGR_FIX, st);
-    sgr_fix_kernel<VEC, G><<<grid + (job.loss ? 1 : 0), kBlock, 0, st>>>(a, wave_blocks,
-                                                                        seg_loss, beta, job);
-    probe_end(NSD_KERNEL_SGR_FIX, st);
-    return check_launch("sgr_fix_kernel");
+    FixJobs f;
+    add_fix(f, a, seg_loss, beta);
+    f.loss = job;
+    return launch_fixes<VEC, G>(f, st);
 }
 
 // Calls f.template operator()<VEC, G>() for the lane layout wp.
