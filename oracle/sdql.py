@@ -18,11 +18,15 @@ Values (Section 2, semi-ring dictionaries):
   * `e1 * e2` of tensors is the outer product: the left operand's values are
     multiplied by the right operand (Section 2, Example 2; typing rule of `*`);
   * `sum(<k,v> in d) f` folds the semi-ring addition over d's stored pairs.
-Differentiation (Section 4.1, scalar forward mode): every real carries a
-tangent; `gradient` seeds a tangent of 1 on one stored key of the chosen
-input at a time (the one-hot inputs of the gradient API, Section 4.3) and
-reads the result's tangent, so it costs one evaluation per stored key: tiny
-inputs only.
+Differentiation, two independent ways, tiny inputs only:
+  * `gradient` (Section 4.1, scalar forward mode): every real carries a
+    tangent; a tangent of 1 is seeded on one stored key of the chosen input
+    at a time (the one-hot inputs of the gradient API, Section 4.3) and the
+    result's tangent read, one evaluation per stored key;
+  * `gradient_tensorized` (Sections 4.2 and 4.3, literally): the program is
+    transformed by the tensorized forward-mode rules, the free variables are
+    bound to their zero or one-hot tangent tensors, and the transformed
+    program is evaluated once.
 """
 from __future__ import annotations
 
@@ -351,6 +355,13 @@ def evaluate(e, env):
         return a == b
     if tag == "op":
         return apply_op(e[1], evaluate(e[2], env))
+    if tag == "zero":
+        return ZERO
+    if tag == "dop":
+        x = evaluate(e[2], env)
+        return _OPS[e[1]][1](0.0 if x is ZERO else float(_primal(x)))
+    if tag == "tmul":
+        return tensor_mul(evaluate(e[1], env), evaluate(e[2], env), order(evaluate(e[3], env)))
     raise ValueError(f"unknown expression {tag}")
 
 
@@ -436,4 +447,98 @@ def gradient(program, env, wrt):
             out[target] = 0.0
         else:
             raise TypeError("gradient of a program whose value is not a real")
+    return out
+
+
+# ------------------------------------------- tensorized forward mode (literal)
+
+
+def order(v):
+    """Number of dictionary levels of a value (a real, ZERO and {} count 0)."""
+    if isinstance(v, dict):
+        for x in v.values():
+            return 1 + order(x)
+    return 0
+
+
+def tensor_mul(t, e2, m):
+    """The product t *[tau] e2 of the tensorized rules: t has m primal levels
+    followed by tau levels; the result keeps the m primal keys, then e2's
+    keys, then the tau keys (each value v of t at depth m becomes e2 * v)."""
+    if t is ZERO or e2 is ZERO:
+        return ZERO
+    if m == 0:
+        return mul(e2, t)
+    return {k: tensor_mul(v, e2, m - 1) for k, v in t.items()}
+
+
+def tangent(e):
+    """The tensorized forward-mode transformation of an expression (the rule
+    for each construct of Section 4.2, applied to the syntax tree): the
+    tangent of variable x is the variable x', constants and discrete values
+    have a zero tangent, a product takes the product rule with the tau-aware
+    product on its second term, a lookup looks up the tangent, and a sum over
+    a dictionary binds the tangent of the current entry."""
+    tag = e[0]
+    if tag == "sum":
+        _, k, v, src, body = e
+        return ("sum", k, v, src,
+                ("let", k + "'", ("zero",),
+                 ("let", v + "'", ("get", tangent(src), ("var", k)), tangent(body))))
+    if tag == "let":
+        _, x, e1, e2 = e
+        return ("let", x, e1, ("let", x + "'", tangent(e1), tangent(e2)))
+    if tag == "if":
+        return ("if", e[1], tangent(e[2]))
+    if tag == "get":
+        return ("get", tangent(e[1]), e[2])
+    if tag == "single":
+        return ("single", e[1], tangent(e[2]))
+    if tag == "mul":
+        return ("add", ("mul", e[1], tangent(e[2])), ("tmul", tangent(e[1]), e[2], e[1]))
+    if tag == "add":
+        return ("add", tangent(e[1]), tangent(e[2]))
+    if tag == "op":
+        return ("mul", ("dop", e[1], e[2]), tangent(e[2]))
+    if tag == "var":
+        return ("var", e[1] + "'")
+    if tag in ("num", "bool", "empty", "not", "eq", "zero"):
+        return ("zero",)
+    raise ValueError(f"no tangent rule for {tag}")
+
+
+def onehot(x):
+    """The one-hot tensor of the gradient API for input x: for every stored
+    key path p of x, the entry {p -> {p -> 1}} (order twice x's)."""
+    out = {}
+    for path, _ in leaves(x):
+        inner = 1.0
+        for k in reversed(path):
+            inner = {k: inner}
+        outer = inner
+        for k in reversed(path):
+            outer = {k: outer}
+        out = add(out, outer) if out else outer
+    return out if out else ZERO
+
+
+def gradient_tensorized(program, env, wrt):
+    """`gradient e x` of the gradient API evaluated literally: every free
+    variable v gets v' = zero (v != x) or onehot x (v == x), then the
+    tensorized tangent of the program is evaluated once.  For a real-valued
+    program the result is a tensor over x's keys: {key path: value}."""
+    e = parse(program) if isinstance(program, str) else program
+    seeded = dict(env)
+    for name in env:
+        seeded[name + "'"] = onehot(env[name]) if name == wrt else ZERO
+    r = evaluate(tangent(e), seeded)
+    out = {p: 0.0 for p, _ in leaves(env[wrt])}
+    if r is ZERO:
+        return out
+    if not isinstance(r, dict):
+        raise TypeError("gradient of a program whose value is not a real")
+    for p, v in leaves(r):
+        if p not in out:
+            raise KeyError(f"gradient key {p} is not a stored key of {wrt}")
+        out[p] = 0.0 if v is ZERO else float(v)
     return out

@@ -4,8 +4,9 @@ sums of products, the gradient API's derivatives and their lowering.
 The derivatives the front end builds symbolically are evaluated here by dense
 brute force (numpy einsum over the terms, masks as 0/1 arrays) and compared
 with the reference interpreter's forward-mode gradient (one evaluation per
-stored key, Sections 4.1 and 4.3) on tiny random inputs.  The interpreter
-itself is pinned in test_sdql_oracle.py.
+stored key, Sections 4.1 and 4.3) and its literal tensorized evaluation of
+the gradient API (Sections 4.2 and 4.3) on tiny random inputs.  The
+interpreter itself is pinned in test_sdql_oracle.py.
 """
 import numpy as np
 import pytest
@@ -161,6 +162,9 @@ def test_value_and_gradients_match_interpreter(name, text, decls, grads, seed):
     for x in grads:
         g = eval_terms(prog, prog.gradient(x), arrays)
         want = ref.gradient(text, env, x)
+        literal = ref.gradient_tensorized(text, env, x)
+        for key, v in want.items():
+            np.testing.assert_allclose(literal[key], v, rtol=1e-11, atol=1e-12)
         shape = decls[x].shape
         if g is None:
             g = np.zeros(shape)

@@ -233,3 +233,103 @@ def test_gradients_match_central_differences(text):
 
             fd = (shifted(h) - shifted(-h)) / (2 * h)
             assert got == pytest.approx(fd, rel=1e-6, abs=1e-8), (wrt, key)
+
+
+# ----------------------------------- gradient API, evaluated literally
+
+
+TENSORIZED_PROGRAMS = [
+    "sum(<i, a> in V1) a * V2(i)",
+    "sum(<i, a> in V2) V1(i) * a",
+    "sum(<i,r> in M) r(i)",
+    SMVM, FROB, GNN, MF,
+    "sum(<i,r> in A) sum(<j,a> in r) let d = a + -1 * sum(<c,u> in U(i)) u * V(j)(c) in d * d",
+    "sum(<i,a> in V1) exp(a) * a + sin(V2(i)) * a * a",
+]
+
+
+def tiny_env(rng):
+    rowptr, colind, val = rand_csr(rng, 5, 4, 9, empty_row=1)
+    Mp, Mc, Mv = rand_csr(rng, 4, 4, 7)
+    k = 3
+    dd = ref.dense_dict
+    return {
+        "A": ref.csr_dict(rowptr, colind, val), "M": ref.csr_dict(Mp, Mc, Mv),
+        "V1": {0: 0.7, 2: -1.1, 3: 0.4}, "V2": dd(rng.standard_normal(4)),
+        "x": dd(rng.standard_normal(4)), "B": dd(rng.standard_normal((4, k))),
+        "H": dd(rng.standard_normal((4, k))), "G": dd(rng.standard_normal((5, k))),
+        "U": dd(rng.standard_normal((5, k))), "V": dd(rng.standard_normal((4, k))),
+    }, (rowptr, colind, val)
+
+
+@pytest.mark.parametrize("text", TENSORIZED_PROGRAMS)
+def test_tensorized_gradient_equals_scalar_forward_mode(text):
+    # two independent differentiations: the tensorized rules applied to the
+    # program (one evaluation) and dual numbers (one evaluation per key)
+    env, _ = tiny_env(np.random.default_rng(3))
+    used = {n for n in env if n in text.replace("(", " ").replace(")", " ").split()}
+    env = {n: env[n] for n in used}
+    for wrt in sorted(used):
+        a = ref.gradient_tensorized(text, env, wrt)
+        b = ref.gradient(text, env, wrt)
+        assert a.keys() == b.keys()
+        for key in a:
+            assert a[key] == pytest.approx(b[key], rel=1e-12, abs=1e-13), (wrt, key)
+
+
+def test_tensorized_examples_1_and_3():
+    env = {"V1": {0: 1.0, 2: -2.0, 3: 4.0}, "V2": ref.dense_dict([3.0, 1.0, 2.0, -1.0])}
+    assert ref.gradient_tensorized("sum(<i, a> in V1) a * V2(i)", env, "V2") == \
+        {(0,): 1.0, (1,): 0.0, (2,): -2.0, (3,): 4.0}
+    M = {0: {0: 2.0, 2: 1.0}, 1: {0: 5.0}, 2: {2: -1.0, 1: 3.0}}
+    assert ref.gradient_tensorized("sum(<i,r> in M) r(i)", {"M": M}, "M") == \
+        {(0, 0): 1.0, (0, 2): 0.0, (1, 0): 0.0, (2, 1): 0.0, (2, 2): 1.0}
+
+
+def test_tensorized_gradients_equal_the_c_oracle(orc):
+    # the interpreter's `gradient e x` against the fp64 C oracle's
+    # hand-derived gradients: same keys (the stored pattern), same values
+    env, (rowptr, colind, val) = tiny_env(np.random.default_rng(9))
+    nr, nc, k = 5, 4, 3
+    A = orc.Dok.from_csr(nr, nc, rowptr, colind, val.astype(np.float32))
+    rows = np.repeat(np.arange(nr, dtype=np.int32), np.diff(rowptr)).astype(np.int32)
+    cols = np.asarray(colind, dtype=np.int32)
+    arr = {n: ref.to_array(env[n], (4,) if n == "x" else ((5 if n in "GU" else 4), k))
+           for n in ("x", "B", "H", "G", "U", "V")}
+
+    def on_pattern(g):
+        return np.array([g[(int(i), int(j))] for i, j in zip(rows, cols)])
+
+    def dense_grad(g, shape):
+        out = np.zeros(shape)
+        for key, v in g.items():
+            out[key] = v
+        return out
+
+    e = {"A": env["A"], "x": env["x"]}
+    ref_dA, _ = orc.sddmm(A, None, arr["x"].reshape(-1, 1), 1, rows, cols)
+    np.testing.assert_allclose(on_pattern(ref.gradient_tensorized(SMVM, e, "A")), ref_dA,
+                               rtol=1e-12, atol=1e-13)
+    ref_dx, _ = orc.spmm_t(A, None, 1)
+    np.testing.assert_allclose(dense_grad(ref.gradient_tensorized(SMVM, e, "x"), (nc,)),
+                               ref_dx[:, 0], rtol=1e-12, atol=1e-13)
+    e = {"A": env["A"], "B": env["B"]}
+    C, Cm = orc.spmm(A, arr["B"], k)
+    ref_dA, _ = orc.sddmm(A, C, arr["B"], k, rows, cols, Xmag=Cm)
+    np.testing.assert_allclose(on_pattern(ref.gradient_tensorized(FROB, e, "A")), ref_dA,
+                               rtol=1e-11, atol=1e-12)
+    ref_dB, _ = orc.spmm_t(A, C, k, Gmag=Cm)
+    np.testing.assert_allclose(dense_grad(ref.gradient_tensorized(FROB, e, "B"), (nc, k)),
+                               ref_dB, rtol=1e-11, atol=1e-12)
+    e = {"A": env["A"], "U": env["U"], "V": env["V"]}
+    for mode, (w, shape) in enumerate([("U", (nr, k)), ("V", (nc, k))]):
+        g, _ = orc.mf_grad(A, arr["U"], arr["V"], k, mode)
+        np.testing.assert_allclose(dense_grad(ref.gradient_tensorized(MF, e, w), shape), g,
+                                   rtol=1e-11, atol=1e-12)
+    e = {"A": env["A"], "H": env["H"], "G": env["G"]}
+    ref_dA, _ = orc.sddmm(A, arr["G"], arr["H"], k, rows, cols)
+    np.testing.assert_allclose(on_pattern(ref.gradient_tensorized(GNN, e, "A")), ref_dA,
+                               rtol=1e-11, atol=1e-12)
+    ref_dH, _ = orc.spmm_t(A, arr["G"], k)
+    np.testing.assert_allclose(dense_grad(ref.gradient_tensorized(GNN, e, "H"), (nc, k)),
+                               ref_dH, rtol=1e-11, atol=1e-12)
