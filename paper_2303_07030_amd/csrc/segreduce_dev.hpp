@@ -268,6 +268,12 @@ __device__ __forceinline__ void loss_total_block(const LossJob &job) {
 // segment; the blocks after them give a whole block to each huge segment.
 // When seg_loss is given, beta * ||out[seg]||^2 is stored for every long
 // segment.  b is the block's index within the pass.
+#ifdef NSD_FIX_DEPTH
+constexpr int kFixDepth = NSD_FIX_DEPTH;
+#else
+constexpr int kFixDepth = 4;  // chunk partials in flight per lane (a power of two; measured)
+#endif
+
 template <int VEC, int G>
 __device__ __forceinline__ void fix_block(const SgrParams &a, int b, int wave_blocks,
                                           double *seg_loss, double beta) {
@@ -298,21 +304,22 @@ __device__ __forceinline__ void fix_block(const SgrParams &a, int b, int wave_bl
     for (int c0 = 0; c0 < a.k; c0 += G * VEC) {
         const int col = c0 + g * VEC;
         const bool on = col < a.k;
-        // four chunk partials in flight per lane, four running sums
-        Vec<VEC> acc[4];
+        // kFixDepth chunk partials in flight per lane, as many running sums
+        Vec<VEC> acc[kFixDepth];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[j].zero();
+        for (int j = 0; j < kFixDepth; ++j) acc[j].zero();
         if (on) {
             int64_t t = qq;
-            for (; t + 3 * nsum < n; t += 4 * nsum) {
-                Vec<VEC> x[4];
+            for (; t + (kFixDepth - 1) * nsum < n; t += kFixDepth * nsum) {
+                Vec<VEC> x[kFixDepth];
 #pragma unroll
-                for (int j = 0; j < 4; ++j) x[j].load(a.part + (s0 + t + j * nsum) * k + col);
+                for (int j = 0; j < kFixDepth; ++j)
+                    x[j].load(a.part + (s0 + t + j * nsum) * k + col);
 #pragma unroll
-                for (int j = 0; j < 4; ++j) acc[j].add(x[j]);
+                for (int j = 0; j < kFixDepth; ++j) acc[j].add(x[j]);
             }
 #pragma unroll
-            for (int j = 0; j < 3; ++j) {  // at most three left
+            for (int j = 0; j < kFixDepth - 1; ++j) {  // the ones left
                 if (t + j * nsum < n) {
                     Vec<VEC> x;
                     x.load(a.part + (s0 + t + j * nsum) * k + col);
@@ -320,9 +327,10 @@ __device__ __forceinline__ void fix_block(const SgrParams &a, int b, int wave_bl
                 }
             }
         }
-        acc[0].add(acc[1]);
-        acc[2].add(acc[3]);
-        acc[0].add(acc[2]);
+#pragma unroll
+        for (int w = kFixDepth / 2; w >= 1; w >>= 1)
+#pragma unroll
+            for (int j = 0; j < w; ++j) acc[j].add(acc[j + w]);
 #pragma unroll
         for (int m = G; m < kWave; m <<= 1)
 #pragma unroll
