@@ -605,15 +605,21 @@ class Program:
         return self.tangent(self.value, x)
 
     # -- step 5: lowering
-    def plan(self, grads=(), value=True):
-        """Kernel calls computing the value (when asked) and the gradients."""
+    def plan(self, grads=(), value=True, fuse=True):
+        """Kernel calls computing the value (when asked) and the gradients:
+        one fused loss kernel when the whole program is one of the fused
+        losses (and fuse is set), else one kernel per term."""
+        if fuse:
+            fused = _fused_plan(self, tuple(grads), value)
+            if fused is not None:
+                return fused
         return _Lowering(self).run(value, tuple(grads))
 
-    def run(self, inputs: dict, grads=(), value=True, stream=None):
+    def run(self, inputs: dict, grads=(), value=True, stream=None, fuse=True):
         """Executes the plan on device tensors: inputs maps each sparse name
         to a DeviceCsr and each dense name to a float32 tensor of its shape.
         Returns {"value": ..., "d<name>": ...}."""
-        return self.plan(grads, value).execute(inputs, stream)
+        return self.plan(grads, value, fuse).execute(inputs, stream)
 
 
 def compile(text: str, **decls) -> Program:   # noqa: A001 - the natural name
@@ -960,6 +966,154 @@ class _Lowering:
         raise NotLowerable("dense term other than a copy or a dot product")
 
 
+# ------------------------------------------------ whole-program fusion
+
+
+def _only(terms):
+    return terms[0] if len(terms) == 1 else None
+
+
+def _facs_by_tensor(t):
+    out = {}
+    for f in t.facs:
+        out.setdefault(f.tensor, []).append(f.idx)
+    return out
+
+
+def _sparse_mask(p, t):
+    """(r, c) of the term's one full mask on the sparse matrix, else None."""
+    if len(t.masks) != 1 or t.masks[0].tensor != p.sparse:
+        return None
+    r, c = t.masks[0].idx
+    return None if r == c else (r, c)
+
+
+def _dense(p, name, shape):
+    info = p.tensors.get(name)
+    return info is not None and info.input and info.kind == "dense" and info.shape == shape
+
+
+def _fused_plan(p: Program, grads, value):
+    """The whole program as one fused loss kernel of the library, when it is
+    exactly one of them (the matrix's values entering linearly as written):
+      sum_{(i,j) in A} A_ij x_j                     -> nsd_loss_sum_spmv
+      0.5 * sum (C * C) with C = A B                -> nsd_loss_frob_spmm
+      sum_{(i,j) in A} A_ij <G_i, H_j>              -> nsd_loss_bilinear
+      sum_{(i,j) in A} R_ij R_ij, R = A - U V^T on A's keys -> nsd_loss_mf
+    Else None (the program is lowered term by term)."""
+    if p.sparse is None or p.value.order not in (0, None):
+        return None
+    t = _only(p.value.terms)
+    if t is None or t.keys:
+        return None
+    nr, nc = p.tensors[p.sparse].shape
+    A = p.sparse
+    facs = _facs_by_tensor(t)
+    mask = _sparse_mask(p, t)
+    plan = Plan(p)
+    for name, d in p.inputs.items():
+        plan.bufs[name] = Buf(name, "input", "pattern" if isinstance(d, Sparse) else "dense",
+                              d.shape)
+
+    def out(name, layout, shape, wanted):
+        """A result buffer, or a temporary when the kernel writes an output
+        nobody asked for."""
+        key = name if wanted else f"unused_{name}"
+        plan.bufs[key] = Buf(key, "out" if wanted else "temp", layout, shape)
+        if wanted:
+            plan.results[key] = key
+        return key
+
+    def want(x):
+        return x in grads
+
+    # SMVM
+    if mask and t.coef == 1.0 and len(t.facs) == 2 and A in facs and len(facs) == 2:
+        (x,) = [n for n in facs if n != A]
+        r, c = mask
+        if facs[A] == [(r, c)] and facs[x] == [(c,)] and _dense(p, x, (nc,)) \
+                and set(grads) <= {A, x}:
+            args = dict(x=x, loss=out("value", "scalar", (), value),
+                        dA=out("d" + A, "pattern", (nr, nc), want(A)),
+                        dx=out("d" + x, "dense", (nc,), want(x)))
+            plan.calls.append(Call("loss_sum_spmv", args, args["loss"]))
+            return plan
+    # bilinear
+    if mask and t.coef == 1.0 and len(t.facs) == 3 and len(facs) == 3 and A in facs:
+        r, c = mask
+        others = [n for n in facs if n != A]
+        H = [n for n in others if facs[n][0][0] == c]
+        G = [n for n in others if facs[n][0][0] == r]
+        if len(H) == 1 and len(G) == 1 and facs[A] == [(r, c)]:
+            H, G = H[0], G[0]
+            hz, gz = facs[H][0], facs[G][0]
+            if len(hz) == 2 and len(gz) == 2 and hz[1] == gz[1] and hz[1] in t.loops:
+                k = p.extent[hz[1]]
+                if _dense(p, H, (nc, k)) and _dense(p, G, (nr, k)) and set(grads) <= {A, H, G}:
+                    args = dict(H=H, G=G, k=k, loss=out("value", "scalar", (), value),
+                                dA=out("d" + A, "pattern", (nr, nc), want(A)),
+                                dH=out("d" + H, "dense", (nc, k), want(H)))
+                    plan.calls.append(Call("loss_bilinear", args, args["loss"]))
+                    if want(G):   # dG = A H, not part of the fused kernel
+                        dG = out("d" + G, "dense", (nr, k), True)
+                        plan.calls.append(Call("spmm", dict(vals=A, B=H, k=k), dG))
+                    return plan
+    # 1/2 ||A B||^2
+    if not t.masks and t.coef == 0.5 and len(t.facs) == 2 and len(facs) == 1:
+        (Cn,) = facs
+        info = p.tensors[Cn]
+        if not info.input and info.kind == "dense" and facs[Cn][0] == facs[Cn][1]:
+            d = _only(info.definition.terms)
+            dm = d and _sparse_mask(p, d)
+            if dm and d.coef == 1.0 and len(d.facs) == 2:
+                r, c = dm
+                df = _facs_by_tensor(d)
+                Bn = [n for n in df if n != A]
+                if A in df and len(Bn) == 1 and df[A] == [(r, c)]:
+                    Bn = Bn[0]
+                    bz = df[Bn][0]
+                    if len(bz) == 2 and bz[0] == c and d.keys == (r, bz[1]):
+                        k = p.extent[bz[1]]
+                        if _dense(p, Bn, (nc, k)) and set(grads) <= {A, Bn}:
+                            plan.bufs[Cn] = Buf(Cn, "inter", "dense", (nr, k))
+                            args = dict(B=Bn, k=k, C=Cn, loss=out("value", "scalar", (), value),
+                                        dA=out("d" + A, "pattern", (nr, nc), want(A)),
+                                        dB=out("d" + Bn, "dense", (nc, k), want(Bn)))
+                            plan.calls.append(Call("loss_frob_spmm", args, args["loss"]))
+                            return plan
+    # matrix factorisation
+    if mask and t.coef == 1.0 and len(t.facs) == 2 and len(facs) == 1:
+        (Rn,) = facs
+        info = p.tensors[Rn]
+        r, c = mask
+        if not info.input and info.kind == "patterned" and facs[Rn] == [(r, c), (r, c)] \
+                and len(info.definition.terms) == 2:
+            a_term = [u for u in info.definition.terms if len(u.facs) == 1]
+            uv_term = [u for u in info.definition.terms if len(u.facs) == 2]
+            if len(a_term) == 1 and len(uv_term) == 1:
+                at, ut = a_term[0], uv_term[0]
+                ok = at.coef == 1.0 and at.facs[0].tensor == A and at.facs[0].idx == at.keys
+                uf = _facs_by_tensor(ut)
+                ri, ci = ut.keys
+                Un = [n for n in uf if uf[n][0][0] == ri]
+                Vn = [n for n in uf if uf[n][0][0] == ci]
+                if ok and ut.coef == -1.0 and len(Un) == 1 and len(Vn) == 1:
+                    Un, Vn = Un[0], Vn[0]
+                    uz, vz = uf[Un][0], uf[Vn][0]
+                    if len(uz) == 2 and uz[1] == vz[1] and uz[1] in ut.loops:
+                        k = p.extent[uz[1]]
+                        # the fused kernel's widths: k <= 64, or k <= 256 in float4 rows
+                        fits = k <= 64 or (k <= 256 and k % 4 == 0)
+                        if fits and _dense(p, Un, (nr, k)) and _dense(p, Vn, (nc, k)) \
+                                and set(grads) <= {Un, Vn}:
+                            args = dict(U=Un, V=Vn, k=k, loss=out("value", "scalar", (), value),
+                                        dU=out("d" + Un, "dense", (nr, k), want(Un)),
+                                        dV=out("d" + Vn, "dense", (nc, k), want(Vn)))
+                            plan.calls.append(Call("loss_mf", args, args["loss"]))
+                            return plan
+    return None
+
+
 # ------------------------------------------------------------------ execution
 
 
@@ -1008,6 +1162,11 @@ def _execute(plan: Plan, inputs: dict, stream=None):
     def m(name):
         return None if name is None else mem[name]
 
+    def csc():
+        if A.csc is None:
+            A.build_csc(stream)
+        return A.csc
+
     for call in plan.calls:
         a, out = call.args, mem[call.out]
         if call.kernel == "axpby":
@@ -1029,6 +1188,18 @@ def _execute(plan: Plan, inputs: dict, stream=None):
                 A.build_csc(stream)
             nsd.nsd_spmm_t(desc(a["vals"]), A.csc, m(a["G"]), a["k"], a["alpha"], out, ws,
                            stream)
+        elif call.kernel == "loss_sum_spmv":
+            nsd.nsd_loss_sum_spmv(A.desc, csc(), m(a["x"]), 1.0, out, mem[a["dA"]],
+                                  mem[a["dx"]], ws, stream)
+        elif call.kernel == "loss_bilinear":
+            nsd.nsd_loss_bilinear(A.desc, csc(), m(a["H"]), m(a["G"]), a["k"], 1.0, out,
+                                  mem[a["dA"]], mem[a["dH"]], ws, stream)
+        elif call.kernel == "loss_frob_spmm":
+            nsd.nsd_loss_frob_spmm(A.desc, csc(), m(a["B"]), a["k"], 1.0, mem[a["C"]], out,
+                                   mem[a["dA"]], mem[a["dB"]], ws, stream)
+        elif call.kernel == "loss_mf":
+            nsd.nsd_loss_mf(A.desc, csc(), None, m(a["U"]), m(a["V"]), a["k"], 1.0, out,
+                            mem[a["dU"]], mem[a["dV"]], ws, stream)
         else:
             raise SdqlError(f"unknown kernel {call.kernel}")
     return {name: mem[name] for name in plan.results}

@@ -51,11 +51,12 @@ def mat(orc, S):
     return A, D, rows, colind
 
 
-def test_smvm(S, orc, mat):
+@pytest.mark.parametrize("fuse", [True, False])
+def test_smvm(S, orc, mat, fuse):
     A, D, rows, cols = mat
     x = np.random.default_rng(1).standard_normal(A.ncols).astype(np.float32)
     prog = S.compile(SMVM, A=S.Sparse(A.nrows, A.ncols), x=S.Dense(A.ncols))
-    out = prog.run({"A": A, "x": dev(x)}, grads=("A", "x"))
+    out = prog.run({"A": A, "x": dev(x)}, grads=("A", "x"), fuse=fuse)
     L, Lm = orc.loss_sum_spmv(D, x)
     assert_mag_close(host(out["value"])[0], L, Lm, what="value")
     dA, dAm = orc.sddmm(D, None, x.reshape(-1, 1), 1, rows, cols)
@@ -64,12 +65,13 @@ def test_smvm(S, orc, mat):
     assert_mag_close(host(out["dx"]), dx[:, 0], dxm[:, 0], what="dx")
 
 
+@pytest.mark.parametrize("fuse", [True, False])
 @pytest.mark.parametrize("k", [1, 12, 64])
-def test_frob(S, orc, mat, k):
+def test_frob(S, orc, mat, k, fuse):
     A, D, rows, cols = mat
     B = np.random.default_rng(k).standard_normal((A.ncols, k)).astype(np.float32)
     prog = S.compile(FROB, A=S.Sparse(A.nrows, A.ncols), B=S.Dense(A.ncols, k))
-    out = prog.run({"A": A, "B": dev(B)}, grads=("A", "B"))
+    out = prog.run({"A": A, "B": dev(B)}, grads=("A", "B"), fuse=fuse)
     C, Cm = orc.spmm(D, B, k)
     L, Lm = orc.loss_half_sq(C, Cm)
     assert_mag_close(host(out["value"])[0], L, Lm, what="value")
@@ -79,7 +81,8 @@ def test_frob(S, orc, mat, k):
     assert_mag_close(host(out["dB"]), dB, dBm, what="dB")
 
 
-def test_gnn(S, orc, mat):
+@pytest.mark.parametrize("fuse", [True, False])
+def test_gnn(S, orc, mat, fuse):
     A, D, rows, cols = mat
     k = 16
     rng = np.random.default_rng(2)
@@ -87,7 +90,7 @@ def test_gnn(S, orc, mat):
     G = rng.standard_normal((A.nrows, k)).astype(np.float32)
     prog = S.compile(GNN, A=S.Sparse(A.nrows, A.ncols), H=S.Dense(A.ncols, k),
                      G=S.Dense(A.nrows, k))
-    out = prog.run({"A": A, "H": dev(H), "G": dev(G)}, grads=("A", "H", "G"))
+    out = prog.run({"A": A, "H": dev(H), "G": dev(G)}, grads=("A", "H", "G"), fuse=fuse)
     L, Lm = orc.loss_bilinear(D, G, H, k)
     assert_mag_close(host(out["value"])[0], L, Lm, what="value")
     dA, dAm = orc.sddmm(D, G, H, k, rows, cols)
@@ -98,8 +101,9 @@ def test_gnn(S, orc, mat):
     assert_mag_close(host(out["dG"]), dG, dGm, what="dG")
 
 
+@pytest.mark.parametrize("grads", [("A", "U", "V"), ("U", "V")], ids=["with_dA", "fused"])
 @pytest.mark.parametrize("text", [MF, MF_INNER], ids=["let_outside", "let_inside"])
-def test_mf(S, orc, mat, text):
+def test_mf(S, orc, mat, text, grads):
     A, D, rows, cols = mat
     k = 12
     rng = np.random.default_rng(3)
@@ -107,15 +111,18 @@ def test_mf(S, orc, mat, text):
     V = (0.3 * rng.standard_normal((A.ncols, k))).astype(np.float32)
     prog = S.compile(text, A=S.Sparse(A.nrows, A.ncols), U=S.Dense(A.nrows, k),
                      V=S.Dense(A.ncols, k))
-    out = prog.run({"A": A, "U": dev(U), "V": dev(V)}, grads=("A", "U", "V"))
+    plan = prog.plan(grads)
+    assert (plan.kernels() == ["loss_mf"]) == ("A" not in grads)
+    out = prog.run({"A": A, "U": dev(U), "V": dev(V)}, grads=grads)
     L, Lm = orc.mf_loss(D, U, V, k)
     assert_mag_close(host(out["value"])[0], L, Lm, what="value")
     dU, dUm = orc.mf_grad(D, U, V, k, 0)
     assert_mag_close(host(out["dU"]), dU, dUm, what="dU")
     dV, dVm = orc.mf_grad(D, U, V, k, 1)
     assert_mag_close(host(out["dV"]), dV, dVm, what="dV")
-    r, rm = orc.mf_resid(D, U, V, k, rows, cols)
-    assert_mag_close(host(out["dA"]), 2 * r, 2 * rm, what="dA")
+    if "A" in grads:
+        r, rm = orc.mf_resid(D, U, V, k, rows, cols)
+        assert_mag_close(host(out["dA"]), 2 * r, 2 * rm, what="dA")
 
 
 def test_two_terms_accumulate(S, orc):

@@ -214,7 +214,7 @@ def test_zero_tangents_vanish():
 
 
 def plan_of(text, grads, **decls):
-    return S.compile(text, **decls).plan(grads)
+    return S.compile(text, **decls).plan(grads, fuse=False)
 
 
 def test_lowering_smvm():
@@ -273,7 +273,7 @@ def test_lowering_dense_dot_product():
 ])
 def test_outside_the_kernels_raises(text, decls, grads, msg):
     with pytest.raises(S.NotLowerable, match=msg):
-        S.compile(text, **decls).plan(grads)
+        S.compile(text, **decls).plan(grads, fuse=False)
 
 
 def test_errors():
@@ -294,3 +294,33 @@ def test_parser_binding():
     e = S.parse("a + b * c(i)(j)")
     assert isinstance(e, S.AddE) and isinstance(e.right, S.MulE)
     assert isinstance(e.right.right, S.Lookup) and isinstance(e.right.right.dict, S.Lookup)
+
+
+# ------------------------------------------------------- whole-program fusion
+
+
+@pytest.mark.parametrize("text,decls,grads,kernels", [
+    (SMVM, dict(A=S.Sparse(5, 4), x=S.Dense(4)), ("A", "x"), ["loss_sum_spmv"]),
+    (FROB, dict(A=S.Sparse(5, 4), B=S.Dense(4, 3)), ("A", "B"), ["loss_frob_spmm"]),
+    (GNN, dict(A=S.Sparse(5, 4), H=S.Dense(4, 3), G=S.Dense(5, 3)), ("A", "H"),
+     ["loss_bilinear"]),
+    (GNN, dict(A=S.Sparse(5, 4), H=S.Dense(4, 3), G=S.Dense(5, 3)), ("A", "H", "G"),
+     ["loss_bilinear", "spmm"]),
+    (MF, dict(A=S.Sparse(5, 4), U=S.Dense(5, 3), V=S.Dense(4, 3)), ("U", "V"), ["loss_mf"]),
+    (MF_INNER, dict(A=S.Sparse(5, 4), U=S.Dense(5, 3), V=S.Dense(4, 3)), ("U",), ["loss_mf"]),
+])
+def test_whole_programs_lower_to_fused_losses(text, decls, grads, kernels):
+    p = S.compile(text, **decls).plan(grads)
+    assert p.kernels() == kernels
+    assert set(p.results) == {"value"} | {"d" + x for x in grads}
+
+
+@pytest.mark.parametrize("text,decls,grads", [
+    (MF, dict(A=S.Sparse(5, 4), U=S.Dense(5, 3), V=S.Dense(4, 3)), ("A", "U")),  # no dA there
+    (MF, dict(A=S.Sparse(5, 4), U=S.Dense(5, 300), V=S.Dense(4, 300)), ("U",)),  # too wide
+    ("2 * " + SMVM, dict(A=S.Sparse(5, 4), x=S.Dense(4)), ("A",)),             # scaled
+    (QUAD, dict(A=S.Sparse(4, 4), x=S.Dense(4)), ("x",)),
+])
+def test_other_programs_stay_term_by_term(text, decls, grads):
+    p = S.compile(text, **decls).plan(grads)
+    assert not any(k.startswith("loss_") for k in p.kernels())
