@@ -221,7 +221,8 @@ nsd_status nsd_build_workspace_size(int32_t n, int32_t max_key, size_t *bytes);
 /* ------------------------------------------------------------- builders */
 
 /* Suggested item length L for a plan of an operand with nnz entries used at
- * dense width k (enough items to fill the GPU; 16 <= L <= 256). */
+ * dense width k (enough items to fill the GPU; 16 <= L <= 256, shorter, down
+ * to 2, for inputs too small to give every SIMD a wave of 16-entry items). */
 nsd_status nsd_plan_item_len(int32_t nnz, int32_t k, int32_t *item_len);
 
 /* Array sizes for nsd_plan_build: item_ptr needs *max_items + 1 entries,

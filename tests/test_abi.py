@@ -71,6 +71,12 @@ def test_workspace_queries(nsd):
     mi, ml, mc, wb = nsd.nsd_plan_bounds(100_000, 1_000_000, 32)
     assert mi >= 100_000 and ml >= 1 and mc >= 2 * 1_000_000 // 32 and wb > 0
     assert 16 <= nsd.nsd_plan_item_len(1_000_000, 64) <= 256
+    # shorter items only where 16-entry ones leave SIMDs without a wave
+    assert nsd.nsd_plan_item_len(10_000, 1) == 2
+    assert nsd.nsd_plan_item_len(0, 64) == 2
+    for k in (1, 12, 64, 300):
+        ls = [nsd.nsd_plan_item_len(n, k) for n in (0, 10**3, 10**4, 10**5, 10**6, 10**7, 10**8)]
+        assert ls == sorted(ls) and 2 <= ls[0] and ls[-1] <= 256, (k, ls)
     with pytest.raises(nsd.NsdError) as e:
         nsd.nsd_plan_bounds(10, 2**30, 16)
     assert e.value.status == nsd.NSD_ERR_TOO_LARGE
