@@ -13,8 +13,10 @@ indexes) is timed separately and is not part of a step.
 Prints one JSON line: the metric (gradient nonzeros per second), the roofline
 of the step's dominant kernel (its algorithmic bytes over its average launch
 duration, from HIP events recorded around every launch of that kernel during
-the timed steps, against 8 TB/s), and the fp64 oracle timed on this host on
-a bounded sample of the workload, as a reported baseline.
+the timed steps, against 8 TB/s), the same step replayed from a HIP graph
+(beside the eager value, for the paths that need no host round trip), and
+the fp64 oracle timed on this host on a bounded sample of the workload, as a
+reported baseline.
 """
 import argparse
 import hashlib
@@ -114,7 +116,10 @@ def committed_traffic(kernel, workload):
 
 class Setup:
     """Operands in HBM, one step function and the kernels worth a roofline:
-    name -> (kernel id, algorithmic bytes per launch)."""
+    name -> (kernel id, algorithmic bytes per launch).  `graphable`: the
+    step is launches only (no host synchronisation), so it can be captured
+    in a HIP graph."""
+    graphable = True
 
 
 def setup_spmm(d, dev, torch, nsd, ops):
@@ -258,6 +263,7 @@ def setup_build(d, dev, torch, nsd, ops):
 
     S = Setup()
     S.A, S.nnz, S.k, S.step = None, n, 0, step
+    S.graphable = False  # the builders read counts back to the host
     # scatter passes: by column (COO -> CSR), by row, by column (CSR -> CSC);
     # each reads and writes a key and a payload (16 B per entry), except the
     # first pass of a sort, whose payload is the entry's own index (12 B)
@@ -281,6 +287,7 @@ def setup_batax(d, dev, torch, nsd, ops):
     jcol = torch.empty(max(P, 1), dtype=torch.int32, device=dev)
     jval = torch.empty(max(P, 1), dtype=torch.float32, device=dev)
     S = Setup()
+    S.graphable = False  # the key count comes back to the host
     nk = nsd.nsd_batax_jacobian(A.desc, d["beta"], P, jrowptr, jcol, jval, ws)
     S.A, S.nnz, S.k = A, nk, 0
     S.step = lambda: nsd.nsd_batax_jacobian(A.desc, d["beta"], P, jrowptr, jcol, jval, ws)
@@ -451,6 +458,7 @@ def main():
                for n, v in per_kernel.items()}
 
     cold = cold_steps(torch, dev, S, args) if args.cold_steps else None
+    graph = graph_steps(torch, S, args.steps) if S.graphable else None
     stream = stream_copy(torch, dev)
     stream["frac"] = round(achieved / stream["copy_GBps"], 4)
 
@@ -479,11 +487,43 @@ def main():
         "kernels": kernels,
         "preprocess_ms": round(prep_ms, 2), "generate_s": round(gen_s, 1),
         "cold": cold,
+        "graph": graph,
         "achievable": stream,
         "cpu_baseline": cpu,
         "source_digest": source_digest(),
     }
     print(json.dumps(out))
+
+
+def graph_steps(torch, S, steps, per_graph=10):
+    """The step captured `per_graph` times in a row in one HIP graph, the
+    graph replayed until `steps` steps ran, between HIP events: the host's
+    per-call cost (argument marshalling, launch) leaves the step.  The
+    eager steps stay the reported value."""
+    per = per_graph if steps % per_graph == 0 else 1
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        S.step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        for _ in range(per):
+            S.step()
+    g.replay()
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(steps // per):
+        g.replay()
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / steps
+    return {"ms_per_step": round(ms, 5), "value": round(S.nnz / (ms * 1e-3), 1),
+            "steps": steps, "steps_per_graph": per,
+            "note": "consecutive steps captured in one HIP graph, replayed"}
 
 
 def stream_copy(torch, dev, nbytes=1 << 30, reps=10):
