@@ -28,8 +28,11 @@
  *   nsd_coo_to_csr.  A CSC is the stable column order of a CSR plus `perm`,
  *   the CSR slot of every CSC slot.
  * Streams.  `stream` is a hipStream_t passed as void* (NULL: the default
- *   stream).  Hot-path calls are asynchronous on it.  Builders and validators
- *   synchronise it before returning, because they report counts or errors.
+ *   stream).  Hot-path calls are asynchronous on it: they only enqueue
+ *   kernels (no copy, fill, allocation or synchronisation), so a sequence of
+ *   them can be captured in a HIP graph and replayed.  Builders, validators
+ *   and nsd_batax_jacobian synchronise it before returning, because they
+ *   report counts or errors.
  * Workspace.  Calls that need scratch take `ws` (device, 256-byte aligned) and
  *   `ws_bytes`; the size queries say how much.  Contents need no initial value.
  * Errors.  The status is the return value; nothing is thrown across the ABI.
