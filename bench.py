@@ -59,6 +59,9 @@ def parse():
                          "operand left in L2 or the 256 MB MALL); 0 to skip")
     ap.add_argument("--item-len", type=int, default=None,
                     help="work-plan item length (default: the library's choice)")
+    ap.add_argument("--replicate", type=int, default=0,
+                    help="input replicate (0: the headline inputs; 1, 2: same recipe, other "
+                         "seeds, for variance)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--profile-only", action="store_true",
                     help="warmup + steps only (for rocprofv3), no JSON line")
@@ -391,9 +394,10 @@ def main():
 
     synth.VERBOSE = True  # progress lines on stderr while the inputs are drawn
     t0 = time.perf_counter()
-    d = synth.make({"build": "mf", "jvp": "spmm"}.get(args.workload, args.workload), args.size)
+    d = synth.make({"build": "mf", "jvp": "spmm"}.get(args.workload, args.workload), args.size,
+                   replicate=args.replicate)
     if args.workload == "jvp":
-        g = synth.streams("spmm")[3]  # the fourth stream: the tangents
+        g = synth.streams("spmm", args.replicate)[3]  # the fourth stream: the tangents
         d["dval"] = g.standard_normal(len(d["val"]), dtype=np.float32)
         d["dB"] = g.standard_normal(d["B"].shape, dtype=np.float32)
     gen_s = time.perf_counter() - t0
@@ -457,6 +461,7 @@ def main():
                    "GBps": None if not v else round(S.kernels[n] / (v * 1e-3) / 1e9, 1)}
                for n, v in per_kernel.items()}
 
+    per_step = single_steps(torch, S, args.steps)
     cold = cold_steps(torch, dev, S, args) if args.cold_steps else None
     graph = graph_steps(torch, S, args.steps) if S.graphable else None
     stream = stream_copy(torch, dev)
@@ -481,11 +486,13 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f32", "data": "synthetic",
         "config": {"workload": WORKLOAD_NAMES[args.workload] if args.size == "full"
-                   else f"{args.workload}_{args.size}", "nnz": S.nnz, "k": S.k,
+                   else f"{args.workload}_{args.size}", "replicate": args.replicate,
+                   "nnz": S.nnz, "k": S.k,
                    "item_len": S.A.item_len if S.A is not None else None},
         "roofline": roofline,
         "kernels": kernels,
         "preprocess_ms": round(prep_ms, 2), "generate_s": round(gen_s, 1),
+        "per_step": per_step,
         "cold": cold,
         "graph": graph,
         "achievable": stream,
@@ -493,6 +500,22 @@ def main():
         "source_digest": source_digest(),
     }
     print(json.dumps(out))
+
+
+def single_steps(torch, S, steps):
+    """Each of `steps` warm steps between its own pair of HIP events (queued
+    back to back, one synchronisation at the end): median and minimum."""
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    torch.cuda.synchronize()
+    for a, b in ev:
+        a.record()
+        S.step()
+        b.record()
+    torch.cuda.synchronize()
+    t = [a.elapsed_time(b) for a, b in ev]
+    return {"median_ms": round(float(np.median(t)), 5), "min_ms": round(float(min(t)), 5),
+            "steps": steps}
 
 
 def graph_steps(torch, S, steps, per_graph=10):
@@ -635,50 +658,58 @@ def cpu_baseline(args, d):
     else:
         nnz = len(s["i"])
 
+    dok_s = [0.0]
+
+    def dok(*a):
+        t = time.perf_counter()
+        D = oracle.Dok(*a)
+        dok_s[0] += time.perf_counter() - t
+        return D
+
     def one_pass():
         if w == "spmm":
-            D = oracle.Dok((nrows, ncols), (rows, s["colind"]), s["val"])
+            D = dok((nrows, ncols), (rows, s["colind"]), s["val"])
             k = s["k"]
             Cr, Cm = oracle.spmm(D, s["B"], k)
             oracle.loss_half_sq(Cr, Cm)
             oracle.sddmm(D, Cr, s["B"], k, rows, s["colind"], Xmag=Cm)
             oracle.spmm_t(D, Cr, k, Gmag=Cm)
         elif w == "spmv":
-            D = oracle.Dok((nrows, ncols), (rows, s["colind"]), s["val"])
+            D = dok((nrows, ncols), (rows, s["colind"]), s["val"])
             oracle.loss_sum_spmv(D, s["x"])
             oracle.sddmm(D, None, s["x"].reshape(-1, 1), 1, rows, s["colind"])
             oracle.spmm_t(D, None, 1)
         elif w == "gnn":
-            D = oracle.Dok((nrows, ncols), (rows, s["colind"]), s["val"])
+            D = dok((nrows, ncols), (rows, s["colind"]), s["val"])
             k = s["k"]
             oracle.loss_bilinear(D, s["G"], s["H"], k)
             oracle.sddmm(D, s["G"], s["H"], k, rows, s["colind"])
             oracle.spmm_t(D, s["G"], k)
         elif w == "cp4":
-            D = oracle.Dok(s["dims"], s["coords"], s["val"])
+            D = dok(s["dims"], s["coords"], s["val"])
             oracle.cpn_loss(D, s["F"], s["rank"])
             oracle.cpn_resid(D, s["F"], s["rank"], s["coords"])
             for m in range(len(s["dims"])):
                 oracle.cpn_grad(D, s["F"], s["rank"], m)
         elif w == "jvp":
-            D = oracle.Dok((nrows, ncols), (rows, s["colind"]), s["val"])
-            dD = oracle.Dok((nrows, ncols), (rows, s["colind"]), s["dval"])
+            D = dok((nrows, ncols), (rows, s["colind"]), s["val"])
+            dD = dok((nrows, ncols), (rows, s["colind"]), s["dval"])
             oracle.spmm_jvp(D, dD, s["B"], s["dB"], s["k"])
         elif w == "batax":
-            D = oracle.Dok((nrows, ncols), (rows, s["colind"]), s["val"])
+            D = dok((nrows, ncols), (rows, s["colind"]), s["val"])
             one_pass.nk = len(oracle.batax_jacobian(D, s["beta"])[1])
         elif w == "build":
-            D = oracle.Dok((s["nrows"], s["ncols"]), (s["row"], s["col"]), s["val"])
+            D = dok((s["nrows"], s["ncols"]), (s["row"], s["col"]), s["val"])
             _, ci, _, _ = oracle.coo_to_csr(D)
             oracle.stable_sort_by_key(ci, s["ncols"])
         elif w == "mf":
-            D = oracle.Dok((s["nrows"], s["ncols"]), (s["row"], s["col"]), s["val"])
+            D = dok((s["nrows"], s["ncols"]), (s["row"], s["col"]), s["val"])
             k = s["k"]
             oracle.mf_loss(D, s["U"], s["V"], k)
             oracle.mf_grad(D, s["U"], s["V"], k, 0)
             oracle.mf_grad(D, s["U"], s["V"], k, 1)
         else:
-            D = oracle.Dok(s["dims"], (s["i"], s["j"], s["k"]), s["val"])
+            D = dok(s["dims"], (s["i"], s["j"], s["k"]), s["val"])
             F = (s["F1"], s["F2"], s["F3"])
             oracle.cp_loss(D, *F, s["rank"])
             oracle.cp_resid(D, *F, s["rank"], s["i"], s["j"], s["k"])
@@ -701,6 +732,7 @@ def cpu_baseline(args, d):
     return {"value": round(nnz * passes / el, 1), "unit": "entries/s" if w == "build" else "nnz/s",
             "cores": 1, "kind": "oracle",
             "sample": f"{what}: {passes} pass(es) of {done}, {el:.1f} s on one thread",
+            "dok_build_s": round(dok_s[0], 3), "compute_s": round(el - dok_s[0], 3),
             "host_cpus_visible": len(os.sched_getaffinity(0))}
 
 
