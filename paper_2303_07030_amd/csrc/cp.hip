@@ -31,6 +31,7 @@ struct CpSlot {
     bool on, first_mode;
     int row;
     bool carry;     // the open segment started before this item (a later chunk)
+    bool pend = false;  // acc is a chunk partial of segment `row`, not yet stored
     Vec<VEC> acc;   // sum of R * (fa o fb) over the open segment
     Vec<VEC> ownv;  // own[row]: the open segment's own factor row
     double &lsum;
@@ -51,10 +52,9 @@ struct CpSlot {
     }
 
     __device__ __forceinline__ void flush() {
-        if (!on) return;
         if (carry) {
-            acc.store(m.s.part + s * k + col);
-        } else {
+            pend = true;  // a chunk item holds one segment: this is its end
+        } else if (on) {
             Vec<VEC> t = acc;
             t.scale(m.s.alpha);
             t.store(m.s.out + (int64_t)row * k + col);
@@ -128,11 +128,8 @@ struct CpSlot {
 
     __device__ __forceinline__ void finish() {
         const SgrParams &a = m.s;
-        if (b0 == a.nnz || a.segidx[b0] != row) {
-            flush();
-        } else if (on) {
-            acc.store(a.part + s * k + col);  // the first chunk of a long segment
-        }
+        if (b0 == a.nnz || a.segidx[b0] != row) flush();
+        else pend = true;  // a chunk of a long segment that goes on
     }
 };
 
@@ -141,8 +138,8 @@ struct CpSlot {
 // batch takes its fields by broadcast); narrow slots load them per entry.
 // The next tile's (batch's) metadata is in flight under the current one.
 template <int VEC, int G, int U>
-__device__ __forceinline__ void cp_walk(const CpMode &m, int64_t s, int lane, bool first_mode,
-                                        double &lsum) {
+__device__ __forceinline__ int cp_walk(const CpMode &m, int64_t s, int lane, bool first_mode,
+                                       double &lsum, Vec<VEC> &part_acc) {
     const SgrParams &a = m.s;
     CpSlot<VEC, G, U> st(m, s, lane, first_mode, lsum);
     const int64_t a0 = a.plan.item_ptr[s], b0 = st.b0;
@@ -205,6 +202,8 @@ __device__ __forceinline__ void cp_walk(const CpMode &m, int64_t s, int lane, bo
         }
     }
     st.finish();
+    part_acc = st.acc;
+    return st.pend ? st.row : -1;  // a chunk partial, stored by store_chunk_partial
 }
 
 template <int VEC, int G, int U>
@@ -214,7 +213,11 @@ __device__ __forceinline__ void cp_block(const CpMode &m, int b, bool first_mode
     const int g = threadIdx.x % G;
     if (b < m.item_blocks) {
         const int64_t s = (int64_t)b * kSlots + threadIdx.x / G;
-        if (s < m.s.plan.nitems) cp_walk<VEC, G, U>(m, s, lane, first_mode, lsum);
+        Vec<VEC> pacc;
+        pacc.zero();
+        int pseg = -1;
+        if (s < m.s.plan.nitems) pseg = cp_walk<VEC, G, U>(m, s, lane, first_mode, lsum, pacc);
+        store_chunk_partial<VEC, G>(pseg, pacc, m.s.part, s, m.s.k, g * VEC, g * VEC < m.s.k);
     } else {
         zero_segment<VEC>(m.s, (int64_t)(b - m.item_blocks) * kSlots + threadIdx.x / G, g * VEC,
                           g * VEC < m.s.k);
@@ -265,6 +268,7 @@ static nsd_status launch_cp(CpParams f, double *loss, hipStream_t st) {
     for (int i = 0; i < 3; ++i) {
         f.m[i].item_blocks = (int32_t)ceil_div(f.m[i].s.plan.nitems, kSlots);
         f.m[i].empty_blocks = (int32_t)ceil_div(f.m[i].s.plan.nempty, kSlots);
+        f.m[i].s.chunk_stride = chunk_group<G>();
         grid += f.m[i].item_blocks + f.m[i].empty_blocks;
     }
     if (grid == 0) return loss_finalize(f.loss_part, 0, loss, st);

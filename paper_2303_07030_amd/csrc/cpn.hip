@@ -51,6 +51,7 @@ struct CpnSlot {
     bool on, first_mode;
     int row;
     bool carry;
+    bool pend = false;  // acc is a chunk partial of segment `row`, not yet stored
     Vec<VEC> acc, ownv;
     double &lsum;
 
@@ -70,10 +71,9 @@ struct CpnSlot {
     }
 
     __device__ __forceinline__ void flush() {
-        if (!on) return;
         if (carry) {
-            acc.store(m.s.part + s * k + col);
-        } else {
+            pend = true;  // a chunk item holds one segment: this is its end
+        } else if (on) {
             Vec<VEC> t = acc;
             t.scale(m.s.alpha);
             t.store(m.s.out + (int64_t)row * k + col);
@@ -148,19 +148,16 @@ struct CpnSlot {
 
     __device__ __forceinline__ void finish() {
         const SgrParams &a = m.s;
-        if (b0 == a.nnz || a.segidx[b0] != row) {
-            flush();
-        } else if (on) {
-            acc.store(a.part + s * k + col);
-        }
+        if (b0 == a.nnz || a.segidx[b0] != row) flush();
+        else pend = true;  // a chunk of a long segment that goes on
     }
 };
 
 // One slot's walk over item s of a mode pass; G >= 8 reads the metadata in
 // tiles of G entries, narrower slots per entry and lane.
 template <int N, int VEC, int G, int U>
-__device__ __forceinline__ void cpn_walk(const CpnMode<N> &m, int64_t s, int lane,
-                                         bool first_mode, double &lsum) {
+__device__ __forceinline__ int cpn_walk(const CpnMode<N> &m, int64_t s, int lane,
+                                        bool first_mode, double &lsum, Vec<VEC> &part_acc) {
     const SgrParams &a = m.s;
     CpnSlot<N, VEC, G, U> st(m, s, lane, first_mode, lsum);
     const int64_t a0 = a.plan.item_ptr[s], b0 = st.b0;
@@ -232,6 +229,8 @@ __device__ __forceinline__ void cpn_walk(const CpnMode<N> &m, int64_t s, int lan
         }
     }
     st.finish();
+    part_acc = st.acc;
+    return st.pend ? st.row : -1;  // a chunk partial, stored by store_chunk_partial
 }
 
 template <int N, int VEC, int G, int U>
@@ -242,7 +241,12 @@ __device__ __forceinline__ void cpn_block(const CpnMode<N> &m, int b, bool first
     const int g = threadIdx.x % G;
     if (b < m.item_blocks) {
         const int64_t s = (int64_t)b * kSlots + threadIdx.x / G;
-        if (s < m.s.plan.nitems) cpn_walk<N, VEC, G, U>(m, s, lane, first_mode, lsum);
+        Vec<VEC> pacc;
+        pacc.zero();
+        int pseg = -1;
+        if (s < m.s.plan.nitems)
+            pseg = cpn_walk<N, VEC, G, U>(m, s, lane, first_mode, lsum, pacc);
+        store_chunk_partial<VEC, G>(pseg, pacc, m.s.part, s, m.s.k, g * VEC, g * VEC < m.s.k);
     } else {
         zero_segment<VEC>(m.s, (int64_t)(b - m.item_blocks) * kSlots + threadIdx.x / G, g * VEC,
                           g * VEC < m.s.k);
@@ -282,6 +286,7 @@ static nsd_status launch_cpn(CpnParams<N> f, double *loss, hipStream_t st) {
     for (int i = 0; i < N; ++i) {
         f.m[i].item_blocks = (int32_t)ceil_div(f.m[i].s.plan.nitems, kSlots);
         f.m[i].empty_blocks = (int32_t)ceil_div(f.m[i].s.plan.nempty, kSlots);
+        f.m[i].s.chunk_stride = chunk_group<G>();
         grid += f.m[i].item_blocks + f.m[i].empty_blocks;
     }
     if (grid == 0) return loss_finalize(f.loss_part, 0, loss, st);

@@ -40,6 +40,7 @@ struct DualSlot {
     bool on;
     int row;
     bool carry;    // the open segment started before this item (a later chunk)
+    bool pend = false;  // acc is a chunk partial of segment `row`, not yet stored
     Vec<VEC> acc;
     Vec<VEC> ownv; // own[row] when kKeepOwn: the open segment's own dense row
     double &lsum;
@@ -69,10 +70,9 @@ struct DualSlot {
     }
 
     __device__ __forceinline__ void flush() {
-        if (!on) return;
         if (carry) {
-            acc.store(m.s.part + s * k + col);
-        } else {
+            pend = true;  // a chunk item holds one segment: this is its end
+        } else if (on) {
             Vec<VEC> t = acc;
             t.scale(m.s.alpha);
             t.store(m.s.out + (int64_t)row * k + col);
@@ -179,19 +179,21 @@ struct DualSlot {
 
     __device__ __forceinline__ void finish() {
         const SgrParams &a = m.s;
-        if (b0 == a.nnz || a.segidx[b0] != row) {
-            flush();
-        } else if (on) {
-            acc.store(a.part + s * k + col);  // the first chunk of a long segment
-        }
+        if (b0 == a.nnz || a.segidx[b0] != row) flush();
+        else pend = true;  // a chunk of a long segment that goes on
     }
 };
 
+// Walks item s; returns the segment of the chunk partial left in `part_acc`
+// (stored with store_chunk_partial), or -1.
 template <int KIND, int VEC, int G, int U>
-__device__ __forceinline__ void dual_walk(const DualPass &m, int64_t s, int lane, double &lsum) {
+__device__ __forceinline__ int dual_walk(const DualPass &m, int64_t s, int lane, double &lsum,
+                                         Vec<VEC> &part_acc) {
     DualSlot<KIND, VEC, G, U> st(m, s, lane, lsum);
     walk_item<G, U>(m.s, m.s.plan.item_ptr[s], st.b0, st.g, st);
     st.finish();
+    part_acc = st.acc;
+    return st.pend ? st.row : -1;
 }
 
 template <int KIND, int VEC, int G, int U>
@@ -201,7 +203,11 @@ __device__ __forceinline__ void dual_block(const DualPass &m, int b, double &lsu
     const int g = threadIdx.x % G;
     if (b < m.item_blocks) {
         const int64_t s = (int64_t)b * kSlots + threadIdx.x / G;
-        if (s < m.s.plan.nitems) dual_walk<KIND, VEC, G, U>(m, s, lane, lsum);
+        Vec<VEC> pacc;
+        pacc.zero();
+        int pseg = -1;
+        if (s < m.s.plan.nitems) pseg = dual_walk<KIND, VEC, G, U>(m, s, lane, lsum, pacc);
+        store_chunk_partial<VEC, G>(pseg, pacc, m.s.part, s, m.s.k, g * VEC, g * VEC < m.s.k);
     } else {
         zero_segment<VEC>(m.s, (int64_t)(b - m.item_blocks) * kSlots + threadIdx.x / G, g * VEC,
                           g * VEC < m.s.k);
@@ -264,6 +270,7 @@ static nsd_status launch_dual(DualParams f, int probe_id, LossJob job, hipStream
         }
         m.item_blocks = (int32_t)ceil_div(m.s.plan.nitems, kSlots);
         m.empty_blocks = (int32_t)ceil_div(m.s.plan.nempty, kSlots);
+        m.s.chunk_stride = chunk_group<G>();
         grid += m.item_blocks + m.empty_blocks;
     }
     if (job.loss && !job.p1) {

@@ -31,6 +31,7 @@ struct JvpSlot {
     bool on;
     int row;
     bool carry;
+    bool pend = false;  // acc, dacc are chunk partials of segment `row`, not yet stored
     Vec<VEC> acc, dacc;
 
     __device__ __forceinline__ JvpSlot(const JvpParams &f_, int64_t s_, int col_, bool on_,
@@ -43,11 +44,9 @@ struct JvpSlot {
     }
 
     __device__ __forceinline__ void flush() {
-        if (!on) return;
         if (carry) {
-            acc.store(f.c.part + s * k + col);
-            dacc.store(f.d.part + s * k + col);
-        } else {
+            pend = true;  // a chunk item holds one segment: this is its end
+        } else if (on) {
             acc.store(f.c.out + (int64_t)row * k + col);
             dacc.store(f.d.out + (int64_t)row * k + col);
         }
@@ -87,12 +86,8 @@ struct JvpSlot {
     }
 
     __device__ __forceinline__ void finish() {
-        if (b0 == f.c.nnz || f.c.segidx[b0] != row) {
-            flush();
-        } else if (on) {
-            acc.store(f.c.part + s * k + col);
-            dacc.store(f.d.part + s * k + col);
-        }
+        if (b0 == f.c.nnz || f.c.segidx[b0] != row) flush();
+        else pend = true;  // a chunk of a long segment that goes on
     }
 };
 
@@ -109,11 +104,23 @@ __global__ __launch_bounds__(kBlock) void jvp_kernel(JvpParams f) {
         return;
     }
     const int64_t s = (int64_t)blockIdx.x * kSlots + threadIdx.x / G;
-    if (s >= f.c.plan.nitems) return;
-    const int64_t a0 = f.c.plan.item_ptr[s], b0 = f.c.plan.item_ptr[s + 1];
-    JvpSlot<VEC, G, U> st(f, s, col, on, a0, b0);
-    walk_item<G, U>(f.c, a0, b0, g, st);
-    st.finish();
+    Vec<VEC> pc, pd;
+    pc.zero();
+    pd.zero();
+    int pseg = -1;
+    if (s < f.c.plan.nitems) {
+        const int64_t a0 = f.c.plan.item_ptr[s], b0 = f.c.plan.item_ptr[s + 1];
+        JvpSlot<VEC, G, U> st(f, s, col, on, a0, b0);
+        walk_item<G, U>(f.c, a0, b0, g, st);
+        st.finish();
+        if (st.pend) {
+            pseg = st.row;
+            pc = st.acc;
+            pd = st.dacc;
+        }
+    }
+    store_chunk_partial<VEC, G>(pseg, pc, f.c.part, s, f.c.k, col, on);
+    store_chunk_partial<VEC, G>(pseg, pd, f.d.part, s, f.c.k, col, on);
 }
 
 // Entries per batch (two rows are gathered per entry): four, measured on
@@ -131,6 +138,7 @@ template <int VEC, int G>
 static nsd_status launch_jvp(JvpParams f, hipStream_t st) {
     constexpr int kSlots = kBlock / G;
     f.c.item_blocks = (int32_t)ceil_div(f.c.plan.nitems, kSlots);
+    f.c.chunk_stride = f.d.chunk_stride = chunk_group<G>();
     const int64_t empty_blocks = ceil_div(f.c.plan.nempty, kSlots);
     dim3 grid((unsigned)(f.c.item_blocks + empty_blocks), (unsigned)ceil_div(f.c.k, G * VEC));
     probe_begin(NSD_KERNEL_JVP, st);

@@ -43,8 +43,11 @@ __global__ __launch_bounds__(kBlock) void sgr_main_kernel(SgrParams a) {
         return;
     }
     const int64_t s = (int64_t)blockIdx.x * kSlots + threadIdx.x / G;
-    if (s >= a.plan.nitems) return;
-    sgr_walk<VEC, G, U>(a, s, col, on, NoSegDone{});
+    Vec<VEC> pacc;
+    pacc.zero();
+    int pseg = -1;
+    if (s < a.plan.nitems) pseg = sgr_walk<VEC, G, U>(a, s, col, on, NoSegDone{}, pacc);
+    store_chunk_partial<VEC, G>(pseg, pacc, a.part, s, a.k, col, on);
 }
 
 // Zero-fill of a whole output when there is nothing to reduce.
@@ -61,6 +64,7 @@ template <int VEC, int G>
 static nsd_status launch_sgr_vg(SgrParams a, hipStream_t st) {
     constexpr int kSlots = kBlock / G;
     a.item_blocks = (int32_t)ceil_div(a.plan.nitems, kSlots);
+    a.chunk_stride = chunk_group<G>();
     const int64_t empty_blocks = ceil_div(a.plan.nempty, kSlots);
     dim3 grid((unsigned)(a.item_blocks + empty_blocks), (unsigned)ceil_div(a.k, G * VEC));
     probe_begin(NSD_KERNEL_SGR_MAIN, st);
@@ -310,13 +314,17 @@ __global__ __launch_bounds__(kBlock) NSD_FROB_OCCUPANCY void frob_row_kernel(Fro
                           on);
     } else {
         const int64_t s = (int64_t)blockIdx.x * kSlots + threadIdx.x / G;
+        Vec<VEC> pacc;
+        pacc.zero();
+        int pseg = -1;
         if (s < a.plan.nitems) {
-            sgr_walk<VEC, G, U>(a, s, col, on, [&](int, const Vec<VEC> &c) {
+            pseg = sgr_walk<VEC, G, U>(a, s, col, on, [&](int, const Vec<VEC> &c) {
                 if (on)
 #pragma unroll
                     for (int e = 0; e < VEC; ++e) lsq += (double)c.v[e] * c.v[e];
-            });
+            }, pacc);
         }
+        store_chunk_partial<VEC, G>(pseg, pacc, a.part, s, a.k, col, on);
     }
     const double t = block_sum(lsq);
     if (threadIdx.x == 0) f.loss_part[blockIdx.x] = 0.5 * t;
@@ -331,6 +339,7 @@ static nsd_status launch_frob(FrobParams f, hipStream_t st) {
     constexpr int kSlots = kBlock / G;
     constexpr int U = sgr_unroll<G>();
     f.rows.item_blocks = (int32_t)ceil_div(f.rows.plan.nitems, kSlots);
+    f.rows.chunk_stride = chunk_group<G>();
     const int row_blocks = f.rows.item_blocks + (int)ceil_div(f.rows.plan.nempty, kSlots);
     probe_begin(NSD_KERNEL_FROB_ROW, st);
     frob_row_kernel<VEC, G, U><<<row_blocks, kBlock, 0, st>>>(f);

@@ -17,6 +17,12 @@ struct SgrParams {
     float alpha = 1.f;
     float *out = nullptr;             // [nseg x k]
     float *part = nullptr;            // [plan.nitems x k] chunk partials
+    // Rows of `part` that hold a long segment's partials: its first chunk's
+    // and, past it, those of the chunks at item indexes divisible by
+    // chunk_stride (1: every chunk's; chunk_group<G>(): one per group of
+    // slots, the group's chunks of a segment added together first, see
+    // store_chunk_partial)
+    int32_t chunk_stride = 1;
     int32_t item_blocks = 0;          // set by the launcher
 };
 

@@ -144,6 +144,50 @@ __device__ __forceinline__ void walk_item(const SgrParams &a, int64_t a0, int64_
     }
 }
 
+// Chunk partials of a wave, added together before they are stored.  The
+// chunk items of a long segment are consecutive and hold no other segment,
+// so slots holding chunks of one segment are consecutive too.  Slots are
+// taken in groups of chunk_group<G>() (consecutive slots of one wave); in a
+// group, the first slot of every run of one segment adds the run's partials
+// in slot order (lane shuffles, no barrier) and stores the sum as its own
+// item's partial row.  A segment then has one partial row per group it
+// spans: its first chunk's and those of the chunks at item indexes
+// divisible by the group size, which the combine reads with chunk_stride =
+// chunk_group<G>().  Every lane of the wave calls this (seg < 0: the slot
+// holds no partial).
+template <int G>
+constexpr int chunk_group() {
+    return kWave / G < 8 ? kWave / G : 8;
+}
+
+template <int VEC, int G>
+__device__ __forceinline__ void store_chunk_partial(int seg, Vec<VEC> acc, float *part,
+                                                    int64_t s, int64_t k, int col, bool on) {
+    constexpr int CG = chunk_group<G>();
+    if constexpr (CG == 1) {
+        if (seg >= 0 && on) acc.store(part + s * k + col);
+    } else {
+        if (!__any(seg >= 0)) return;  // wave-uniform: no partial in this wave
+        const int lane = threadIdx.x % kWave;
+        const int q = (lane / G) % CG;  // slot within its group
+        const int prev = __shfl(seg, q > 0 ? lane - G : lane);
+        const bool leader = seg >= 0 && (q == 0 || prev != seg);
+        const Vec<VEC> own = acc;  // every lane reads the others' own partials
+        bool run = true;
+#pragma unroll
+        for (int d = 1; d < CG; ++d) {
+            const int src = q + d < CG ? lane + d * G : lane;
+            const int sseg = __shfl(seg, src);
+            Vec<VEC> x;
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) x.v[e] = __shfl(own.v[e], src);
+            run = run && q + d < CG && sseg == seg;
+            if (run) acc.add(x);
+        }
+        if (leader && on) acc.store(part + s * k + col);
+    }
+}
+
 // One slot's gather-reduce over item s (entries [a0, b0)).  Complete
 // segments are written as alpha * sum; a segment cut by the item's end or
 // start goes to part[s].  `seg_done(segment, unscaled sum)` is called for
@@ -156,6 +200,7 @@ struct SgrSlot {
     bool on;
     int row;
     bool carry;  // the open segment started before this item (a later chunk)
+    bool pend = false;  // acc is a chunk partial of segment `row`, not yet stored
     Vec<VEC> acc;
     SegDone &seg_done;
 
@@ -169,7 +214,7 @@ struct SgrSlot {
 
     __device__ __forceinline__ void flush() {
         if (carry) {
-            if (on) acc.store(a.part + s * k + col);
+            pend = true;  // a chunk item holds one segment: this is its end
         } else {
             seg_done(row, acc);
             if (on) {
@@ -201,22 +246,23 @@ struct SgrSlot {
     }
 
     __device__ __forceinline__ void finish(int64_t b0) {
-        if (b0 == a.nnz || a.segidx[b0] != row) {
-            flush();
-        } else if (on) {
-            acc.store(a.part + s * k + col);  // the first chunk of a long segment
-        }
+        if (b0 == a.nnz || a.segidx[b0] != row) flush();
+        else pend = true;  // a chunk of a long segment that goes on
     }
 };
 
+// Walks item s; returns the segment of the chunk partial left in `part_acc`
+// (to be stored with store_chunk_partial), or -1.
 template <int VEC, int G, int U, class SegDone>
-__device__ __forceinline__ void sgr_walk(const SgrParams &a, int64_t s, int col, bool on,
-                                         SegDone seg_done) {
+__device__ __forceinline__ int sgr_walk(const SgrParams &a, int64_t s, int col, bool on,
+                                        SegDone seg_done, Vec<VEC> &part_acc) {
     const int64_t a0 = a.plan.item_ptr[s];
     const int64_t b0 = a.plan.item_ptr[s + 1];
     SgrSlot<VEC, G, U, SegDone> st(a, s, col, on, a0, seg_done);
     walk_item<G, U>(a, a0, b0, (int)(threadIdx.x % G), st);
     st.finish(b0);
+    part_acc = st.acc;
+    return st.pend ? st.row : -1;
 }
 
 template <int VEC>
@@ -298,8 +344,14 @@ __device__ __forceinline__ void fix_block(const SgrParams &a, int b, int wave_bl
     }
     const int seg = a.plan.long_seg[i];
     const int64_t s0 = a.plan.long_first[i];
-    const int64_t n = ((int64_t)a.segptr[seg + 1] - a.segptr[seg] + L - 1) / L;
-    if (!huge && n > kHugeChunks) return;
+    const int64_t chunks = ((int64_t)a.segptr[seg + 1] - a.segptr[seg] + L - 1) / L;
+    // the segment's partial rows: s0, then s0 + fb + j * stride
+    const int64_t stride = a.chunk_stride;
+    const int64_t fb = stride - s0 % stride;
+    const int64_t n = fb < chunks ? 1 + (chunks - fb + stride - 1) / stride : 1;
+    auto prow = [&](int64_t t) { return s0 + (t == 0 ? 0 : fb + (t - 1) * stride); };
+    // one wave per segment of at most kHugeChunks partial rows, else a block
+    if (huge != (n > kHugeChunks)) return;
     double lsq = 0.0;
     for (int c0 = 0; c0 < a.k; c0 += G * VEC) {
         const int col = c0 + g * VEC;
@@ -314,7 +366,7 @@ __device__ __forceinline__ void fix_block(const SgrParams &a, int b, int wave_bl
                 Vec<VEC> x[kFixDepth];
 #pragma unroll
                 for (int j = 0; j < kFixDepth; ++j)
-                    x[j].load(a.part + (s0 + t + j * nsum) * k + col);
+                    x[j].load(a.part + prow(t + j * nsum) * k + col);
 #pragma unroll
                 for (int j = 0; j < kFixDepth; ++j) acc[j].add(x[j]);
             }
@@ -322,7 +374,7 @@ __device__ __forceinline__ void fix_block(const SgrParams &a, int b, int wave_bl
             for (int j = 0; j < kFixDepth - 1; ++j) {  // the ones left
                 if (t + j * nsum < n) {
                     Vec<VEC> x;
-                    x.load(a.part + (s0 + t + j * nsum) * k + col);
+                    x.load(a.part + prow(t + j * nsum) * k + col);
                     acc[j].add(x);
                 }
             }
