@@ -163,7 +163,8 @@ class DeviceCoo3:
         self.nnz = int(val.numel())
         # shorter items than the library's general choice: measured on
         # MI355X, 3/8 of it is best for the fused order-3 CP pass (24 entries
-        # at 20M entries, rank 32: 1.13 ms per step against 1.25 ms at 64)
+        # at 20M entries, rank 32: 1.05 ms per step against 1.08 at 16 and
+        # 1.10 at 32)
         self.item_len = item_len or max(8, nsd.nsd_plan_item_len(self.nnz, rank_hint) * 3 // 8)
         self.desc = nsd.nsd_coo3()
         self.desc.dims[:] = self.dims
@@ -219,9 +220,10 @@ class DeviceCooN:
         coords = [_dev(c, torch.int32, device) for c in coords]
         val = _dev(val, torch.float32, device)
         self.nnz = int(val.numel())
-        # half the library's general item length: measured best on MI355X
-        # for the order-4 CP pass (32 entries at 20M entries, rank 32)
-        self.item_len = item_len or max(8, nsd.nsd_plan_item_len(self.nnz, rank_hint) // 2)
+        # 3/8 of the library's general item length, as for order 3: measured
+        # best on MI355X for the order-4 CP pass (24 entries at 20M entries,
+        # rank 32: 1.46 ms per step against 1.51 at 16 and 1.48 at 32)
+        self.item_len = item_len or max(8, nsd.nsd_plan_item_len(self.nnz, rank_hint) * 3 // 8)
         self.desc = nsd.nsd_coon()
         self.desc.order = N
         for m in range(N):
