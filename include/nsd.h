@@ -81,7 +81,9 @@ typedef enum nsd_dup_policy { NSD_DUP_SUM = 0, NSD_DUP_ERROR = 1 } nsd_dup_polic
  * entries whose partial sums are added in chunk order afterwards, and empty
  * segments are listed for a zero fill.
  * It balances power-law segment lengths without atomics.  A long segment with
- * more than 64 chunks is "huge": its chunks are combined by a whole workgroup.
+ * more than 64 chunks is "huge" (listed in huge_idx): the combine gives a whole
+ * workgroup to each that still has more than 64 partial rows once the chunks
+ * computed by one wave have been added together.
  */
 typedef struct nsd_plan {
     int32_t item_len;          /* L: entries per chunk; segments above
@@ -93,6 +95,7 @@ typedef struct nsd_plan {
     const int32_t *huge_idx;   /* [nhuge] positions in the long lists of huge segments */
     const int32_t *chunk_item; /* [nchunks] every item that is a chunk of a long segment */
     const int32_t *empty_seg;  /* [nempty] segments without entries */
+    int32_t longest_chunks;    /* chunks of the longest segment (0: none is long) */
 } nsd_plan;
 
 /* Matrix CSR (Section 5.3, the matrix CSR storage `(len,pos,idx,val)`). */

@@ -63,7 +63,7 @@ __global__ void plan_window_kernel(int32_t nseg, const int32_t *segptr, int32_t 
 
 __global__ void plan_count_kernel(int32_t nseg, const int32_t *segptr, int32_t L,
                                   const int32_t *pos, const int32_t *prev_win, int32_t *nitem,
-                                  int32_t *nchunk, int32_t *is_huge) {
+                                  int32_t *nchunk, int32_t *is_huge, int32_t *longest) {
     const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (r >= nseg) return;
     const int32_t len = segptr[r + 1] - segptr[r];
@@ -77,6 +77,7 @@ __global__ void plan_count_kernel(int32_t nseg, const int32_t *segptr, int32_t L
     }
     nchunk[r] = lg ? nitem[r] : 0;
     is_huge[r] = lg && nitem[r] > kHugeChunks;
+    if (lg) atomicMax(longest, nitem[r]);  // integer max: order-independent
 }
 
 struct PlanScans {
@@ -211,8 +212,9 @@ nsd_status nsd_plan_build(int32_t nseg, int32_t nnz, const int32_t *segptr, int3
     plan_window_kernel<<<g, kPlanThreads, 0, st>>>(nseg, segptr, item_len, pos, win);
     NSD_TRY(check_launch("plan_window_kernel"));
     NSD_TRY(scan_exclusive_max(win, win, nseg, scan_ws, st));
+    NSD_HIP(hipMemsetAsync(tot + 5, 0, sizeof(int32_t), st));
     plan_count_kernel<<<g, kPlanThreads, 0, st>>>(nseg, segptr, item_len, pos, win, nitem, nchunk,
-                                                  is_huge);
+                                                  is_huge, tot + 5);
     NSD_TRY(check_launch("plan_count_kernel"));
     NSD_TRY(scan_exclusive(nitem, ipos, nseg, tot + 0, scan_ws, st));
     NSD_TRY(scan_exclusive(is_long, lpos, nseg, tot + 1, scan_ws, st));
@@ -223,7 +225,7 @@ nsd_status nsd_plan_build(int32_t nseg, int32_t nnz, const int32_t *segptr, int3
     plan_fill_kernel<<<g, kPlanThreads, 0, st>>>(nseg, nnz, segptr, item_len, sc, item_ptr, long_seg,
                                                  long_first, huge_idx, chunk_item, empty_seg);
     NSD_TRY(check_launch("plan_fill_kernel"));
-    int32_t h[5];
+    int32_t h[6];
     NSD_HIP(hipMemcpyAsync(h, tot, sizeof(h), hipMemcpyDeviceToHost, st));
     NSD_HIP(hipStreamSynchronize(st));
     plan->nitems = h[0];
@@ -231,6 +233,7 @@ nsd_status nsd_plan_build(int32_t nseg, int32_t nnz, const int32_t *segptr, int3
     plan->nempty = h[2];
     plan->nchunks = h[3];
     plan->nhuge = h[4];
+    plan->longest_chunks = h[5];
     return NSD_OK;
 }
 

@@ -491,7 +491,14 @@ inline void add_fix(FixJobs &f, const SgrParams &a, double *seg_loss = nullptr,
     j.seg_loss = seg_loss;
     j.beta = beta;
     j.wave_blocks = (int)ceil_div(a.plan.nlong, kBlockWaves);
-    j.blocks = a.plan.nlong > 0 ? j.wave_blocks + a.plan.nhuge : 0;
+    // a segment of c chunks has at most 1 + ceil((c - 1) / chunk_stride)
+    // partial rows; when the longest has no more than kHugeChunks, waves
+    // take every segment and no block per huge segment is launched (such
+    // blocks would each load their segment's bounds only to return)
+    const int64_t c = a.plan.longest_chunks;
+    const int64_t rows = c <= 1 ? c : 1 + (c - 1 + a.chunk_stride - 1) / a.chunk_stride;
+    const bool blocks_needed = a.plan.nhuge > 0 && (c == 0 || rows > kHugeChunks);
+    j.blocks = a.plan.nlong > 0 ? j.wave_blocks + (blocks_needed ? a.plan.nhuge : 0) : 0;
 }
 
 // Combines the long segments of every pass in f (those that have any) and

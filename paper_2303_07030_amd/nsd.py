@@ -40,7 +40,8 @@ class nsd_plan(C.Structure):
     _fields_ = [("item_len", C.c_int32), ("nitems", C.c_int32), ("nlong", C.c_int32),
                 ("nhuge", C.c_int32), ("nchunks", C.c_int32), ("nempty", C.c_int32),
                 ("item_ptr", C.c_void_p), ("long_seg", C.c_void_p), ("long_first", C.c_void_p),
-                ("huge_idx", C.c_void_p), ("chunk_item", C.c_void_p), ("empty_seg", C.c_void_p)]
+                ("huge_idx", C.c_void_p), ("chunk_item", C.c_void_p), ("empty_seg", C.c_void_p),
+                ("longest_chunks", C.c_int32)]
 
 
 class nsd_csr(C.Structure):

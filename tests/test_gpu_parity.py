@@ -223,6 +223,7 @@ def test_plan_invariants(nsd, L):
     nch_all = -(-lens[long_rows] // L)
     assert np.array_equal(huge, np.nonzero(nch_all > 64)[0])
     assert plan.nchunks == nch_all.sum()
+    assert plan.longest_chunks == (nch_all.max() if n_long else 0)
     assert np.array_equal(chunks, np.concatenate(
         [long_first[i] + np.arange(nch_all[i]) for i in range(n_long)]) if n_long else chunks)
     starts = set(item_ptr[:-1].tolist())
@@ -294,6 +295,40 @@ def test_spmm_t(nsd, orc, edge_A, k):
     nsd.nsd_spmm_t(A.desc, A.csc, dev(G), k, 1.5, out, A.workspace(k))
     ref, mag = orc.spmm_t(D, G, k, alpha=1.5)
     assert_mag_close(host(out), ref, mag, what=f"spmm_t k={k}")
+
+
+def chunk_offsets_pattern():
+    """Rows for item length 4: long rows whose first chunk falls at every
+    offset within a group of 8 slots (3 to 39 chunks, ragged last chunks),
+    a row of 75 chunks (a huge plan segment with few partial rows) and one of
+    750 chunks (more than 64 partial rows even after the in-wave sums),
+    between short and empty rows."""
+    rng = np.random.default_rng(41)
+    lengths = [1, 0, 2] + [4 * c - (c % 3) for c in range(3, 40)] + [1] * 5
+    lengths += [300, 0, 3000, 9, 17, 1, 0]
+    nrows, ncols = len(lengths), 4000
+    return nrows, ncols, *make_csr(rng, nrows, ncols, np.array(lengths), hot_col=7)
+
+
+@pytest.mark.parametrize("k", [1, 8, 12, 64, 256])
+def test_chunk_partials_at_every_group_offset(nsd, operand, orc, k):
+    nrows, ncols, rowptr, colind, val = chunk_offsets_pattern()
+    A = operand(nrows, ncols, rowptr, colind, val, item_len=4, k_hint=k)
+    D = oracle_dok(orc, nrows, ncols, rowptr, colind, val)
+    rng = np.random.default_rng(300 + k)
+    B = rng.standard_normal((ncols, k)).astype(np.float32)
+    G = rng.standard_normal((nrows, k)).astype(np.float32)
+    Cg = torch.full((nrows, k), np.nan, dtype=torch.float32, device="cuda")
+    nsd.nsd_spmm(A.desc, dev(B), k, Cg, A.workspace(k))
+    ref, mag = orc.spmm(D, B, k)
+    assert_mag_close(host(Cg), ref, mag, what=f"spmm k={k}")
+    out = torch.full((ncols, k), np.nan, dtype=torch.float32, device="cuda")
+    nsd.nsd_spmm_t(A.desc, A.csc, dev(G), k, 1.0, out, A.workspace(k))
+    ref, mag = orc.spmm_t(D, G, k)
+    assert_mag_close(host(out), ref, mag, what=f"spmm_t k={k}")
+    if k % 4 == 0 and k <= 256:
+        got = run_frob(nsd, A, B, k)
+        check_frob(orc, nrows, ncols, rowptr, colind, val, B, k, got)
 
 
 def test_spmm_t_ones_is_column_sums(nsd, orc, edge_A):
