@@ -224,7 +224,7 @@ __device__ __forceinline__ void dual_block(const DualPass &m, int b, double &lsu
 template <int KIND, int VEC, int G, int U>
 __global__ __launch_bounds__(kBlock) NSD_DUAL_OCCUPANCY void dual_kernel(DualParams f) {
     if (f.early.loss && blockIdx.x == gridDim.x - 1) {
-        loss_total_block(f.early);
+        loss_total_block<4>(f.early);  // a few thousand row partials; keeps VGPRs low
         return;
     }
     const int first = f.pass[0].item_blocks + f.pass[0].empty_blocks;

@@ -228,7 +228,7 @@ __global__ __launch_bounds__(kBlock) void loss_finalize_kernel(const double *par
     job.p2 = part2;
     job.n2 = n2;
     job.loss = loss;
-    loss_total_block(job);
+    loss_total_block<16>(job);
 }
 
 // Block partials of alpha * sum_i x_i * y_i (y NULL: ones) in fp64: block b

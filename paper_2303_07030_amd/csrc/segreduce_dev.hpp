@@ -281,23 +281,40 @@ struct NoSegDone {
 
 // ------------------------------------------------------------- loss total
 
-// Strided partial sums of one thread over p[0, n) (four independent chains so
-// the loads overlap).
+// Strided partial sums of one thread over p[0, n): C independent loads
+// issued before any is added, then the C chains added in a fixed pairwise
+// order.  One block summing ~10^5 block partials with few chains is a chain
+// of memory latencies; 16 chains take 32 more VGPRs, so kernels whose main
+// work needs the registers use 4.
+template <int C>
 __device__ __forceinline__ double strided_sum(const double *p, int64_t n) {
-    double s[4] = {0.0, 0.0, 0.0, 0.0};
-    int64_t i = threadIdx.x;
-    for (; i + 3 * kBlock < n; i += 4 * kBlock) {
+    double s[C];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) s[j] += p[i + j * kBlock];
+    for (int j = 0; j < C; ++j) s[j] = 0.0;
+    int64_t i = threadIdx.x;
+    for (; i + (C - 1) * kBlock < n; i += C * kBlock) {
+        double x[C];
+#pragma unroll
+        for (int j = 0; j < C; ++j) x[j] = p[i + j * kBlock];
+#pragma unroll
+        for (int j = 0; j < C; ++j) s[j] += x[j];
     }
-    for (int j = 0; i < n; i += kBlock, ++j) s[j & 3] += p[i];
-    return (s[0] + s[1]) + (s[2] + s[3]);
+#pragma unroll
+    for (int j = 0; j < C - 1; ++j)  // the ones left (static indexes)
+        if (i + j * kBlock < n) s[j] += p[i + j * kBlock];
+#pragma unroll
+    for (int w = C / 2; w >= 1; w >>= 1)
+#pragma unroll
+        for (int j = 0; j < w; ++j) s[j] += s[j + w];
+    return s[0];
 }
 
-// One whole block: the loss total of a job, in a fixed order.
+// One whole block: the loss total of a job, in a fixed order (C: loads in
+// flight per thread, see strided_sum).
+template <int C>
 __device__ __forceinline__ void loss_total_block(const LossJob &job) {
     __shared__ double sh[kBlock];
-    sh[threadIdx.x] = strided_sum(job.p1, job.n1) + strided_sum(job.p2, job.n2);
+    sh[threadIdx.x] = strided_sum<C>(job.p1, job.n1) + strided_sum<C>(job.p2, job.n2);
     __syncthreads();
     for (int w = kBlock / 2; w >= 1; w >>= 1) {
         if ((int)threadIdx.x < w) sh[threadIdx.x] += sh[threadIdx.x + w];
@@ -435,10 +452,18 @@ struct FixJobs {
 
 static_assert(sizeof(FixJobs) <= 4096, "combine jobs fit the kernel argument limit");
 
+// Loads in flight per thread for the loss total riding on the combine
+// launch (its partials are one per block of a main pass: ~10^5 for cfg4).
+#ifdef NSD_FIX_SUM_CHAINS
+constexpr int kFixSumChains = NSD_FIX_SUM_CHAINS;
+#else
+constexpr int kFixSumChains = 16;
+#endif
+
 template <int VEC, int G>
 __global__ __launch_bounds__(kBlock) void sgr_fix_kernel(FixJobs f) {
     if (f.loss.loss && blockIdx.x == gridDim.x - 1) {
-        loss_total_block(f.loss);
+        loss_total_block<kFixSumChains>(f.loss);
         return;
     }
     int b = blockIdx.x;
