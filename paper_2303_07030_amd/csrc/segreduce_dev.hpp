@@ -325,12 +325,13 @@ __device__ __forceinline__ void loss_total_block(const LossJob &job) {
 
 // ----------------------------------------------------------- long segments
 
-// out[seg] = alpha * sum of the segment's chunk partials, in chunk order per
-// row group, the groups then combined by a fixed butterfly.  Of a pass's
-// blocks, those below wave_blocks give one wave to each non-huge long
-// segment; the blocks after them give a whole block to each huge segment.
-// When seg_loss is given, beta * ||out[seg]||^2 is stored for every long
-// segment.  b is the block's index within the pass.
+// out[seg] = alpha * sum of the segment's partial rows (see chunk_stride), in
+// chunk order per row group, the groups then combined by a fixed butterfly.
+// Of a pass's blocks, those below wave_blocks give one wave to each long
+// segment of at most kHugeChunks partial rows; the blocks after them (when
+// launched) give a whole block to each huge segment with more.  When
+// seg_loss is given, beta * ||out[seg]||^2 is stored for every long segment.
+// b is the block's index within the pass.
 #ifdef NSD_FIX_DEPTH
 constexpr int kFixDepth = NSD_FIX_DEPTH;
 #else
@@ -453,7 +454,8 @@ struct FixJobs {
 static_assert(sizeof(FixJobs) <= 4096, "combine jobs fit the kernel argument limit");
 
 // Loads in flight per thread for the loss total riding on the combine
-// launch (its partials are one per block of a main pass: ~10^5 for cfg4).
+// launch (its partials are one per block of a main pass: ~10^5 for a CP
+// pass over 20M entries).
 #ifdef NSD_FIX_SUM_CHAINS
 constexpr int kFixSumChains = NSD_FIX_SUM_CHAINS;
 #else
