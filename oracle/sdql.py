@@ -450,6 +450,26 @@ def gradient(program, env, wrt):
     return out
 
 
+def jacobian(program, env, wrt):
+    """Jacobian of a program of any value (a real or a tensor) w.r.t. input
+    `wrt` on its stored keys, by one forward-mode evaluation per stored key
+    with that key's tangent seeded to 1 (Section 4.1): the column of the
+    Jacobian for that key.  Returns {output key path + wrt key path: value}
+    with the entries whose tangent is nonzero."""
+    e = parse(program) if isinstance(program, str) else program
+    out = {}
+    for target, _ in leaves(env[wrt]):
+        seeded = dict(env)
+        seeded[wrt] = _replace_leaves(
+            env[wrt], lambda key, v: Dual(v, 1.0 if key == target else 0.0))
+        r = evaluate(e, seeded)
+        for path, v in (leaves(r) if isinstance(r, dict) else [((), r)]):
+            t = v.t if isinstance(v, Dual) else 0.0
+            if t != 0.0:
+                out[path + target] = t
+    return out
+
+
 # ------------------------------------------- tensorized forward mode (literal)
 
 
@@ -542,3 +562,21 @@ def gradient_tensorized(program, env, wrt):
             raise KeyError(f"gradient key {p} is not a stored key of {wrt}")
         out[p] = 0.0 if v is ZERO else float(v)
     return out
+
+
+def jacobian_tensorized(program, env, wrt):
+    """`gradient e x` of a program of any value, evaluated literally as in
+    gradient_tensorized: the tangent's output keys come first and x's keys
+    after them (the tau levels of Section 4.2), so that for a tensor-valued
+    program the result is its Jacobian.  Returns {output key path + wrt key
+    path: value} for every entry the tangent stores (an output whose tangent
+    is the zero value, such as a key only another input stores, has none)."""
+    e = parse(program) if isinstance(program, str) else program
+    seeded = dict(env)
+    for name in env:
+        seeded[name + "'"] = onehot(env[name]) if name == wrt else ZERO
+    r = evaluate(tangent(e), seeded)
+    if r is ZERO:
+        return {}
+    return {p: float(v) for p, v in (leaves(r) if isinstance(r, dict) else [((), r)])
+            if v is not ZERO}

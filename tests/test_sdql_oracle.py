@@ -333,3 +333,88 @@ def test_tensorized_gradients_equal_the_c_oracle(orc):
     ref_dH, _ = orc.spmm_t(A, arr["G"], k)
     np.testing.assert_allclose(dense_grad(ref.gradient_tensorized(GNN, e, "H"), (nc, k)),
                                ref_dH, rtol=1e-11, atol=1e-12)
+
+
+# ------------------------- Jacobians of tensor-valued programs (vector kernels)
+
+VVA = "sum(<i,v> in V1) {i -> v} + sum(<i,v> in V2) {i -> v}"
+VSM = "sum(<i,v> in V) {i -> v * s * s}"
+MATVEC = "sum(<i,r> in M) {i -> sum(<j,a> in r) a * x(j)}"
+
+
+def sparse_vector(rng, n, nnz):
+    keys = np.sort(rng.choice(n, size=nnz, replace=False))
+    return {int(k): float(v) for k, v in zip(keys, rng.standard_normal(nnz))}
+
+
+def both_jacobians(text, env, wrt):
+    j1 = ref.jacobian(text, env, wrt)
+    j2 = ref.jacobian_tensorized(text, env, wrt)
+    assert set(j1) == {k for k, v in j2.items() if v != 0.0}
+    for key, v in j1.items():
+        assert j2[key] == pytest.approx(v, rel=1e-12, abs=1e-14), key
+    return j1
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_vector_addition_jacobian_is_the_identity_on_the_stored_keys(seed):
+    # the VVA kernel of the evaluation (Section 7.1): d(V1 + V2)/dV1 is 1 at
+    # (k, k) for every stored key k of V1 and nothing else, whatever V2 stores
+    rng = np.random.default_rng(seed)
+    env = {"V1": sparse_vector(rng, 40, 9), "V2": sparse_vector(rng, 40, 11)}
+    assert both_jacobians(VVA, env, "V1") == {(k, k): 1.0 for k in env["V1"]}
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_vector_scalar_product_jacobian_is_2sV(seed):
+    # the VSM kernel of the evaluation: f(i) = V(i) s s, df/ds = 2 s V on V's keys
+    rng = np.random.default_rng(10 + seed)
+    s = float(rng.standard_normal())
+    env = {"V": sparse_vector(rng, 50, 13), "s": s}
+    J = both_jacobians(VSM, env, "s")
+    assert J == pytest.approx({(k,): 2 * s * v for k, v in env["V"].items() if v != 0.0})
+    # and with respect to V: the diagonal s^2 on V's keys
+    J = both_jacobians(VSM, env, "V")
+    assert J == pytest.approx({(k, k): s * s for k in env["V"]})
+
+
+def test_matrix_vector_product_jacobian_is_the_matrix():
+    rng = np.random.default_rng(20)
+    M = {i: sparse_vector(rng, 7, int(rng.integers(1, 5))) for i in range(6) if i != 3}
+    env = {"M": M, "x": ref.dense_dict(rng.standard_normal(7))}
+    J = both_jacobians(MATVEC, env, "x")
+    assert J == pytest.approx({(i, j): a for i, r in M.items() for j, a in r.items()})
+
+
+def test_jacobian_of_a_real_valued_program_is_its_gradient():
+    rng = np.random.default_rng(21)
+    M = {i: sparse_vector(rng, 5, 3) for i in range(5)}
+    for i in (0, 2):
+        M[i][i] = float(rng.standard_normal())  # some stored diagonal keys
+    env = {"M": M}
+    trace = "sum(<i,r> in M) r(i)"
+    assert both_jacobians(trace, env, "M") == {(i, i): 1.0 for i in M if i in M[i]}
+    g = ref.gradient(trace, env, "M")
+    assert {k: v for k, v in g.items() if v != 0.0} == ref.jacobian(trace, env, "M")
+
+
+def test_jacobian_matches_central_differences():
+    # a nonlinear vector program: each column of the Jacobian against central
+    # differences of the output dictionary
+    text = "sum(<i,v> in V) {i -> sin(v * W(i)) + v * v * W(i)}"
+    rng = np.random.default_rng(22)
+    env = {"V": sparse_vector(rng, 12, 6), "W": ref.dense_dict(rng.standard_normal(12))}
+    h = 1e-5
+    for wrt in ("V", "W"):
+        J = both_jacobians(text, env, wrt)
+        for key, _ in ref.leaves(env[wrt]):
+            def shifted(dx):
+                e2 = dict(env)
+                e2[wrt] = ref._replace_leaves(env[wrt],
+                                              lambda kk, val: val + dx if kk == key else val)
+                return dict(ref.leaves(ref.value(text, e2)))
+
+            hi, lo = shifted(h), shifted(-h)
+            for out in hi:
+                fd = (hi[out] - lo[out]) / (2 * h)
+                assert J.get(out + key, 0.0) == pytest.approx(fd, rel=1e-6, abs=1e-8), (wrt, key)
