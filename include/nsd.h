@@ -488,6 +488,18 @@ nsd_status nsd_dot(int64_t n, const float *x, const float *y, double alpha, int 
 nsd_status nsd_axpby(int64_t n, float alpha, const float *x, float beta, float *y,
                      void *stream);
 
+/*
+ * out[p] = alpha where A's stored key p is diagonal (row = column), else 0,
+ * over A's nnz entries in its storage order: the gradient of the trace
+ * sum_i A(i, i) with respect to A on its stored keys, scaled by alpha.  It is
+ * the identity restricted to the stored diagonal keys (the trace example of
+ * Section 4.3, Example 3): a diagonal key that is not stored gets no
+ * gradient, and the value array is aligned 1:1 with A's keys like every
+ * sparse gradient.  Needs A's rowidx and colind (not its values or plan).
+ * Async.
+ */
+nsd_status nsd_diag_keys(const nsd_csr *A, float alpha, float *out, void *stream);
+
 /* ---------------------------------------------------------------------------
  * Order-N sparse tensors and the CP gradient for orders 3 to NSD_MAX_ORDER
  * (the order-N form of the nested-dictionary tensor of Section 3).

@@ -383,6 +383,12 @@ nsd_status nsd_axpby(int64_t n, float alpha, const float *x, float beta, float *
     return axpby(n, alpha, x, beta, y, as_stream(stream));
 }
 
+nsd_status nsd_diag_keys(const nsd_csr *A, float alpha, float *out, void *stream) {
+    NSD_TRY(check_csr(A, false, false));
+    NSD_REQUIRE(A->nnz == 0 || out != nullptr, "out is NULL");
+    return diag_keys(A->nnz, A->rowidx, A->colind, alpha, out, as_stream(stream));
+}
+
 nsd_status nsd_loss_mf(const nsd_csr *A, const nsd_csc *At, const float *valT, const float *U,
                        const float *V, int32_t k, float seed, double *loss, float *dU, float *dV,
                        void *ws, size_t ws_bytes, void *stream) {

@@ -281,6 +281,23 @@ nsd_status axpby(int64_t n, float alpha, const float *x, float beta, float *y, h
     return check_launch("axpby_kernel");
 }
 
+// out[p] = alpha * [rowidx[p] == colind[p]] over the stored entries.
+__global__ __launch_bounds__(kBlock) void diag_keys_kernel(int64_t n, const int32_t *rowidx,
+                                                           const int32_t *colind, float alpha,
+                                                           float *out) {
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    for (int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x; p < n; p += stride)
+        out[p] = rowidx[p] == colind[p] ? alpha : 0.f;
+}
+
+nsd_status diag_keys(int64_t n, const int32_t *rowidx, const int32_t *colind, float alpha,
+                     float *out, hipStream_t st) {
+    if (n == 0) return NSD_OK;
+    const int64_t nb = std::min<int64_t>(ceil_div(n, kBlock), 8192);
+    diag_keys_kernel<<<(unsigned)nb, kBlock, 0, st>>>(n, rowidx, colind, alpha, out);
+    return check_launch("diag_keys_kernel");
+}
+
 nsd_status loss_finalize(const double *part, int64_t n, double *loss, hipStream_t st) {
     probe_begin(NSD_KERNEL_LOSS, st);
     loss_finalize_kernel<<<1, kBlock, 0, st>>>(part, n, nullptr, 0, loss);

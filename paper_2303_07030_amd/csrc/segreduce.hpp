@@ -146,5 +146,8 @@ nsd_status dot(int64_t n, const float *x, const float *y, double alpha, bool acc
 
 // y = alpha x + beta y elementwise (x NULL: ones; beta 0: y is not read).
 nsd_status axpby(int64_t n, float alpha, const float *x, float beta, float *y, hipStream_t st);
+// out[p] = alpha where entry p's row equals its column, else 0.
+nsd_status diag_keys(int64_t n, const int32_t *rowidx, const int32_t *colind, float alpha,
+                     float *out, hipStream_t st);
 
 }  // namespace nsd

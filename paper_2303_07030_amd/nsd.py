@@ -148,6 +148,7 @@ _SIGS = {
     "nsd_validate_coo_workspace_size": (C.c_int, [_I, _P, _I, C.POINTER(_SZ)]),
     "nsd_validate_coo": (C.c_int, [_I, _P, _I, _P, C.c_int, _P, _SZ, _P]),
     "nsd_axpby": (C.c_int, [C.c_int64, C.c_float, _P, C.c_float, _P, _P]),
+    "nsd_diag_keys": (C.c_int, [_CSR, C.c_float, _P, _P]),
     "nsd_cpn_workspace_size": (C.c_int, [C.POINTER(nsd_coon), _I, C.POINTER(_SZ)]),
     "nsd_loss_cpn": (C.c_int, [C.POINTER(nsd_coon), C.POINTER(_P), _I, C.c_float, _P, _P,
                                C.POINTER(_P), _P, _SZ, _P]),
@@ -468,6 +469,10 @@ def nsd_dot(n, x, y, alpha, accumulate, out, ws, stream=None):
 
 def nsd_axpby(n, alpha, x, beta, y, stream=None):
     _check(_lib.nsd_axpby(n, alpha, _p(x), beta, _p(y), _stream(stream)), "nsd_axpby")
+
+
+def nsd_diag_keys(A: nsd_csr, alpha, out, stream=None):
+    _check(_lib.nsd_diag_keys(C.byref(A), alpha, _p(out), _stream(stream)), "nsd_diag_keys")
 
 
 def nsd_spmm_vjp(A: nsd_csr, At: nsd_csc, X, G, k, dA, dX, ws, stream=None):

@@ -823,7 +823,8 @@ class _Lowering:
         p = self.p
         r, c = mask.idx
         if r == c:
-            raise NotLowerable("diagonal keys of the sparse matrix (row index = column index)")
+            self._emit_diagonal(t, r, out, ob, accumulate)
+            return
         W = [f for f in t.facs if p.tensors[f.tensor].kind in ("sparse", "patterned")]
         D = [f for f in t.facs if p.tensors[f.tensor].kind == "dense"]
         for f in W:
@@ -907,6 +908,39 @@ class _Lowering:
             calls.append(Call("dot", dict(x=x, y=y, alpha=t.coef, acc=accumulate), out))
             return
         raise NotLowerable(f"result keys {keys} over the pattern ({r}, {c})")
+
+    # terms over the stored diagonal keys (i, i) of the sparse matrix: the
+    # trace and its gradient (Section 4.3, Example 3)
+    def _emit_diagonal(self, t, i, out, ob, accumulate):
+        p = self.p
+        calls = self.plan.calls
+        W = [f for f in t.facs if p.tensors[f.tensor].kind in ("sparse", "patterned")]
+        if len(W) != len(t.facs) or len(W) > 1 or any(f.idx != (i, i) for f in W):
+            raise NotLowerable("factors other than the matrix's values on its diagonal keys")
+        shape = p.tensors[p.sparse].shape
+        if t.keys == (i, i):
+            # a result on the matrix's keys: coef on the stored diagonal keys
+            if ob.layout != "pattern":
+                raise NotLowerable("a result on the matrix's keys must have its layout")
+            if W:
+                raise NotLowerable("values times the diagonal indicator on the pattern")
+            if not accumulate:
+                calls.append(Call("diag", dict(alpha=t.coef), out))
+            else:
+                tmp = self._temp(Buf("", "temp", "pattern", shape))
+                calls.append(Call("diag", dict(alpha=t.coef), tmp))
+                calls.append(Call("axpby", dict(alpha=1.0, x=tmp, beta=1.0), out))
+            return
+        if not t.keys:
+            # a real: coef * sum of the values (or ones) on the stored diagonal keys
+            if ob.layout != "scalar":
+                raise NotLowerable("a real result needs a scalar output")
+            tmp = self._temp(Buf("", "temp", "pattern", shape))
+            calls.append(Call("diag", dict(alpha=1.0), tmp))
+            calls.append(Call("dot", dict(x=tmp, y=self._vals(W[0].tensor) if W else None,
+                                          alpha=t.coef, acc=accumulate), out))
+            return
+        raise NotLowerable(f"result keys {t.keys} over the diagonal keys ({i}, {i})")
 
     def _sampled(self, D, r, c, loops):
         """X[r, z], Y[c, z] (or vectors X[r], Y[c]) of an SDDMM."""
@@ -1177,6 +1211,8 @@ def _execute(plan: Plan, inputs: dict, stream=None):
             nsd.nsd_dot(n, x, m(a["y"]), a["alpha"], a["acc"], out, ws, stream)
         elif call.kernel == "sddmm":
             nsd.nsd_sddmm(A.desc, m(a["X"]), m(a["Y"]), a["k"], a["alpha"], out, stream)
+        elif call.kernel == "diag":
+            nsd.nsd_diag_keys(A.desc, a["alpha"], out, stream)
         elif call.kernel == "spmm":
             D = desc(a["vals"])
             if a["k"] == 1:

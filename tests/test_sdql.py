@@ -256,6 +256,14 @@ def test_lowering_accumulates_terms_of_one_result():
     assert ks[-3:] == ["spmm_t", "spmm", "axpby"] and p.calls[-1].args["beta"] == 1.0
 
 
+def test_lowering_trace():
+    # Example 3: the value sums the values on the stored diagonal keys, the
+    # gradient is the indicator of those keys on the pattern
+    p = plan_of(TRACE, ("M",), M=S.Sparse(5, 5))
+    assert p.kernels() == ["diag", "dot", "diag"]
+    assert p.calls[1].args["y"] == "M" and p.calls[2].out == "dM"
+
+
 def test_lowering_dense_dot_product():
     p = plan_of(DOT1, ("V1", "V2"), V1=S.Dense(6), V2=S.Dense(6))
     assert p.kernels() == ["dot", "axpby", "axpby"]
@@ -263,7 +271,8 @@ def test_lowering_dense_dot_product():
 
 
 @pytest.mark.parametrize("text,decls,grads,msg", [
-    (TRACE, dict(M=S.Sparse(4, 4)), ("M",), "diagonal"),
+    ("sum(<i,r> in M) r(i) * x(i)", dict(M=S.Sparse(4, 4), x=S.Dense(4)), ("M",),
+     "diagonal"),
     ("sum(<i,r> in A) sum(<j,a> in r) a * a * x(j)", dict(A=S.Sparse(4, 3), x=S.Dense(3)),
      ("A",), "values on the pattern"),
     ("sum(<i,a> in x) exp(a)", dict(x=S.Dense(3)), (), "outside"),
