@@ -54,6 +54,8 @@ def _load():
         "orc_cp_grad": (None, [_p, _p, _p, _p, _i64, C.c_int, _i64, _p, _p, _p]),
         "orc_ttv": (_i64, [_p, _p, _p, _p, _p, _p]),
         "orc_ttv_vjp": (None, [_p, _p, _p, _i64, _p, _p, _p, _p, _p, _p, _p]),
+        "orc_ttm": (_i64, [_p, _p, C.c_int32, _p, _p, _p, _p]),
+        "orc_ttm_vjp": (None, [_p, _p, C.c_int32, _p, _i64, _p, _p, _p, _p, _p, _p, _p]),
         "orc_batax_jacobian": (_i64, [_p, _f64, _i64, _p, _p, _p, _p]),
         "orc_spmm_jvp": (None, [_p, _p, _p, _p, _i64, _p, _p, _p, _p]),
         "orc_dok_buildn": (_p, [C.c_int32, _p, _i64, _p, _p]),
@@ -293,6 +295,29 @@ def ttv_vjp(X: Dok, v, gY: Dok, qi, qj, ql):
     _load().orc_ttv_vjp(X.h, _ptr(v), gY.h, len(qi), _ptr(qi), _ptr(qj), _ptr(ql), _ptr(dX),
                         _ptr(dXm), _ptr(dv), _ptr(dvm))
     return dX, dXm, dv, dvm
+
+
+def ttm(X: Dok, U, R):
+    """Y = X x_3 U (U [dims[2] x R]) on the projected (i, j) keys:
+    (yi, yj, y [ny x R], ymag) in (i, j) order."""
+    U = _f64a(U)
+    cap = X.nkeys
+    yi, yj = np.empty(cap, dtype=np.int32), np.empty(cap, dtype=np.int32)
+    y, ym = np.empty(max(cap, 1) * R), np.empty(max(cap, 1) * R)
+    n = _load().orc_ttm(X.h, _ptr(U), R, _ptr(yi), _ptr(yj), _ptr(y), _ptr(ym))
+    return yi[:n], yj[:n], y[: n * R].reshape(n, R), ym[: n * R].reshape(n, R)
+
+
+def ttm_vjp(X: Dok, U, R, gY, qi, qj, ql):
+    """(dX at queries, dXmag, dU [dims[2] x R], dUmag) for the upstream gY
+    [ny x R] on Y's keys in (i, j) order."""
+    U, gY = _f64a(U), _f64a(gY)
+    qi, qj, ql = _i32(qi), _i32(qj), _i32(ql)
+    dX, dXm = np.empty(len(qi)), np.empty(len(qi))
+    dU, dUm = np.empty(X.dims[2] * R), np.empty(X.dims[2] * R)
+    _load().orc_ttm_vjp(X.h, _ptr(U), R, _ptr(gY), len(qi), _ptr(qi), _ptr(qj), _ptr(ql),
+                        _ptr(dX), _ptr(dXm), _ptr(dU), _ptr(dUm))
+    return dX, dXm, dU.reshape(X.dims[2], R), dUm.reshape(X.dims[2], R)
 
 
 def batax_jacobian(A: Dok, beta):

@@ -659,6 +659,106 @@ void orc_ttv_vjp(const orc_dok *X, const double *v, const orc_dok *gY, int64_t n
     }
 }
 
+/*
+ * Tensor-times-matrix along the third mode, the matrix form of TTV:
+ *   Y(i, j, r) = sum over stored (i, j, l) of X_ijl * U(l, r)
+ * on the projected keys {(i, j)}: a sum over X's keys inserting the row
+ * {(i, j) -> X_ijl U(l, :)} with "+=" (Section 3, Section 5.5).  U is row-major
+ * [dims[2] x R]; the keys come out sorted by (i, j), y row-major [ny x R]
+ * with mag on |terms|.  Returns ny.
+ */
+static orc_dok *ttm_keys(const orc_dok *X, int32_t *yi, int32_t *yj, int64_t *ny)
+{
+    int64_t dims[3] = {X->dims[0], X->dims[1], 1};
+    orc_dok *K = dok_new(2, dims, X->n);
+    for (int64_t s = 0; s < X->cap; ++s) {
+        if (X->key[s] == -1) continue;
+        int64_t i, j, l;
+        unpack3(X, X->key[s], &i, &j, &l);
+        dok_add(K, i * dims[1] + j, 1.0, 0);
+    }
+    int64_t n = K->n, m = 0;
+    kt_pair *kp = (kt_pair *)malloc(sizeof(kt_pair) * (n ? n : 1));
+    for (int64_t s = 0; s < K->cap; ++s)
+        if (K->key[s] != -1) { kp[m].key = K->key[s]; kp[m].tag = s; ++m; }
+    qsort(kp, (size_t)n, sizeof(kt_pair), cmp_kt);
+    for (int64_t q = 0; q < n; ++q) {  /* the value of key q becomes its row number */
+        int64_t i, j;
+        unpack2(K, kp[q].key, &i, &j);
+        if (yi) { yi[q] = (int32_t)i; yj[q] = (int32_t)j; }
+        K->val[kp[q].tag] = (double)q;
+    }
+    free(kp);
+    *ny = n;
+    return K;
+}
+
+int64_t orc_ttm(const orc_dok *X, const double *U, int32_t R, int32_t *yi, int32_t *yj, double *y,
+                double *ymag)
+{
+    int64_t ny;
+    orc_dok *K = ttm_keys(X, yi, yj, &ny);
+    memset(y, 0, sizeof(double) * ny * R);
+    memset(ymag, 0, sizeof(double) * ny * R);
+    for (int64_t s = 0; s < X->cap; ++s) {
+        if (X->key[s] == -1) continue;
+        int64_t i, j, l;
+        unpack3(X, X->key[s], &i, &j, &l);
+        int64_t q = (int64_t)dok_get(K, i * X->dims[1] + j, NULL);
+        for (int32_t r = 0; r < R; ++r) {
+            double t = X->val[s] * U[l * R + r];
+            y[q * R + r] += t;
+            ymag[q * R + r] += fabs(t);
+        }
+    }
+    orc_dok_free(K);
+    return ny;
+}
+
+/*
+ * Vector-Jacobian product of Y = X x_3 U given the upstream gY row-major
+ * [ny x R] on Y's keys in (i, j) order:
+ *   dX at queried (i, j, l) that are stored: sum_r gY(i, j, r) U(l, r)
+ *   dU(l, r) = sum over stored (i, j, l, x) of x * gY(i, j, r)
+ */
+void orc_ttm_vjp(const orc_dok *X, const double *U, int32_t R, const double *gY, int64_t nq,
+                 const int32_t *qi, const int32_t *qj, const int32_t *ql, double *dX,
+                 double *dXmag, double *dU, double *dUmag)
+{
+    int64_t ny;
+    orc_dok *K = ttm_keys(X, NULL, NULL, &ny);
+    for (int64_t q = 0; q < nq; ++q) {
+        int pr;
+        int64_t key = ((int64_t)qi[q] * X->dims[1] + qj[q]) * X->dims[2] + ql[q];
+        dok_get(X, key, &pr);
+        double d = 0.0, m = 0.0;
+        if (pr) {
+            int64_t row = (int64_t)dok_get(K, (int64_t)qi[q] * X->dims[1] + qj[q], NULL);
+            for (int32_t r = 0; r < R; ++r) {
+                double t = gY[row * R + r] * U[(int64_t)ql[q] * R + r];
+                d += t;
+                m += fabs(t);
+            }
+        }
+        dX[q] = d;
+        dXmag[q] = m;
+    }
+    memset(dU, 0, sizeof(double) * X->dims[2] * R);
+    memset(dUmag, 0, sizeof(double) * X->dims[2] * R);
+    for (int64_t s = 0; s < X->cap; ++s) {
+        if (X->key[s] == -1) continue;
+        int64_t i, j, l;
+        unpack3(X, X->key[s], &i, &j, &l);
+        int64_t row = (int64_t)dok_get(K, i * X->dims[1] + j, NULL);
+        for (int32_t r = 0; r < R; ++r) {
+            double t = X->val[s] * gY[row * R + r];
+            dU[l * R + r] += t;
+            dUmag[l * R + r] += fabs(t);
+        }
+    }
+    orc_dok_free(K);
+}
+
 /* ---------------------------------------------------- BATAX Jacobian */
 
 /*

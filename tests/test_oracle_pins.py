@@ -342,6 +342,40 @@ def test_ttv_and_vjp_match_autograd(orc):
     np.testing.assert_allclose(dv, vt.grad.numpy(), rtol=1e-12, atol=1e-12)
 
 
+@pytest.mark.parametrize("R", [1, 5])
+def test_ttm_and_vjp_match_autograd(orc, R):
+    # Y(i, j, :) = sum_l X(i, j, l) U(l, :) on the projected keys: autograd of
+    # the dense einsum, with the upstream placed on those keys
+    rng = np.random.default_rng(17 + R)
+    d0, d1, d2, nnz = 6, 5, 7, 90
+    keys = rng.choice(d0 * d1 * d2, size=nnz, replace=False)
+    i, j, l = keys // (d1 * d2), (keys // d2) % d1, keys % d2
+    x = rng.standard_normal(nnz).astype(np.float32)
+    U = rng.standard_normal((d2, R))
+    X = orc.Dok((d0, d1, d2), (i, j, l), x)
+    yi, yj, y, ym = orc.ttm(X, U, R)
+    proj = np.unique(i.astype(np.int64) * d1 + j)
+    assert np.array_equal(yi.astype(np.int64) * d1 + yj, proj)
+    Xd = torch.zeros(d0, d1, d2, dtype=torch.float64)
+    Xd[i, j, l] = torch.tensor(x.astype(np.float64))
+    Xd.requires_grad_(True)
+    Ut = torch.tensor(U, requires_grad=True)
+    Yd = torch.einsum("ijl,lr->ijr", Xd, Ut)
+    np.testing.assert_allclose(y, Yd.detach().numpy()[yi, yj], rtol=1e-12, atol=1e-12)
+    assert np.all(ym >= np.abs(y) - 1e-12)
+    gy = rng.standard_normal((len(yi), R))
+    Gd = torch.zeros(d0, d1, R, dtype=torch.float64)
+    Gd[yi, yj] = torch.tensor(gy)
+    (Yd * Gd).sum().backward()
+    dX, _, dU, _ = orc.ttm_vjp(X, U, R, gy, i, j, l)
+    np.testing.assert_allclose(dX, Xd.grad.numpy()[i, j, l], rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(dU, Ut.grad.numpy(), rtol=1e-12, atol=1e-12)
+    # R = 1 is TTV
+    if R == 1:
+        _, _, yv, _ = orc.ttv(X, U[:, 0])
+        np.testing.assert_allclose(y[:, 0], yv, rtol=1e-12, atol=1e-14)
+
+
 def test_mag_bounds_value_and_equals_it_for_nonnegative_terms(orc):
     rng = np.random.default_rng(17)
     row, col, val = rand_coo(rng, 25, 25, 100)
