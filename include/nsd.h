@@ -468,6 +468,30 @@ nsd_status nsd_ttv(const nsd_ttv_plan *T, const float *x, const float *v, float 
 nsd_status nsd_ttv_vjp(const nsd_ttv_plan *T, const float *x, const float *v, const float *gy,
                        float *dx, float *dv, void *ws, size_t ws_bytes, void *stream);
 
+/* Bytes of `ws` for nsd_ttm and nsd_ttm_vjp at width R (R >= 1).  Writes
+ * *bytes (host). */
+nsd_status nsd_ttm_workspace_size(const nsd_ttv_plan *T, int32_t R, size_t *bytes);
+
+/*
+ * Tensor-times-matrix along the third mode, the matrix form of nsd_ttv (an
+ * n-mode product of Section 3's tensor algebra, kept sparse on the projected
+ * keys): Y[s, :] = sum over stored (i, j, l) with key s = (yi[s], yj[s]) of
+ * x * U[l, :].  x [nnz] in X's input order, U row-major [dims[2] x R], Y
+ * row-major [ny x R], every row written.  T is X's TTV plan.  Async.
+ */
+nsd_status nsd_ttm(const nsd_ttv_plan *T, const float *x, const float *U, int32_t R, float *Y,
+                   void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Vector-Jacobian product of nsd_ttm for the upstream gY row-major [ny x R]:
+ * dx[p] = <gY[key(p), :], U[l_p, :]> on X's keys (input order, [nnz]);
+ * dU[l, :] = sum over stored (i, j, l) of x * gY[key, :]  (dU [dims[2] x R],
+ * every row written).  Async.
+ */
+nsd_status nsd_ttm_vjp(const nsd_ttv_plan *T, const float *x, const float *U, int32_t R,
+                       const float *gY, float *dx, float *dU, void *ws, size_t ws_bytes,
+                       void *stream);
+
 /*
  * *out = alpha * sum_{i < n} x[i] * y[i] (y NULL: ones), accumulated in fp64
  * in a fixed order, plus the previous *out when `accumulate` is nonzero: the

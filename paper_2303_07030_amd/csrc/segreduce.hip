@@ -136,7 +136,7 @@ __device__ __forceinline__ void sddmm_range(const SddmmParams &a, int64_t a0, in
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 if (p + u < b0) {
-                    a.out[p + u] = a.alpha * part[u];
+                    a.out[a.operm ? a.operm[p + u] : p + u] = a.alpha * part[u];
                     if (a.w) lsum += (double)a.w[p + u] * (double)part[u];
                 }
             }
@@ -145,7 +145,7 @@ __device__ __forceinline__ void sddmm_range(const SddmmParams &a, int64_t a0, in
             constexpr int kRep = G / U;
             const int64_t q = p + g / kRep;
             if (g % kRep == 0 && q < b0) {
-                a.out[q] = a.alpha * tot;
+                a.out[a.operm ? a.operm[q] : q] = a.alpha * tot;
                 if (a.w) lsum += (double)a.w[q] * (double)tot;
             }
         }

@@ -34,6 +34,7 @@ struct SddmmParams {
     const float *Y = nullptr;  // [ncols x k]
     float alpha = 1.f;
     float *out = nullptr;      // [nnz]
+    const int32_t *operm = nullptr;  // entry p goes to out[operm[p]] (NULL: out[p])
     const float *w = nullptr;  // fused loss weights (NULL: no loss)
     double beta = 1.0;         // loss += beta * sum_p w_p * <X_i, Y_j>
     double *part = nullptr;    // [nblocks] block partials of the loss

@@ -92,11 +92,12 @@ static size_t ttv_ws(const nsd_ttv_plan *T) {
 
 static SgrParams ttv_sgr(int32_t nseg, int32_t nnz, const nsd_plan &plan, const int32_t *segptr,
                          const int32_t *segidx, const int32_t *idx, const float *w,
-                         const int32_t *wperm, const float *X, float *out, void *ws) {
+                         const int32_t *wperm, const float *X, float *out, void *ws,
+                         int32_t k = 1) {
     SgrParams p;
     p.nseg = nseg;
     p.nnz = nnz;
-    p.k = 1;
+    p.k = k;
     p.plan = plan;
     p.segptr = segptr;
     p.segidx = segidx;
@@ -107,6 +108,11 @@ static SgrParams ttv_sgr(int32_t nseg, int32_t nnz, const nsd_plan &plan, const 
     p.out = out;
     p.part = static_cast<float *>(ws);
     return p;
+}
+
+static size_t ttm_ws(const nsd_ttv_plan *T, int32_t R) {
+    const size_t a = sgr_part_bytes(T->yplan, R), b = sgr_part_bytes(T->lplan, R);
+    return ((std::max(a, b) + 255) & ~size_t(255));
 }
 
 }  // namespace nsd
@@ -228,6 +234,64 @@ nsd_status nsd_ttv_vjp(const nsd_ttv_plan *T, const float *x, const float *v, co
     }
     return segreduce(ttv_sgr(T->dims[2], T->nnz, T->lplan, T->lptr, T->lseg, T->lpair, x, T->lperm,
                              gy, dv, ws),
+                     st);
+}
+
+nsd_status nsd_ttm_workspace_size(const nsd_ttv_plan *T, int32_t R, size_t *bytes) {
+    NSD_REQUIRE(bytes != nullptr, "bytes is NULL");
+    NSD_TRY(check_ttv(T));
+    NSD_REQUIRE(R >= 1, "R = %d < 1", R);
+    *bytes = ttm_ws(T, R);
+    return NSD_OK;
+}
+
+// Y = X x_3 U: the gather-reduce of TTV at width R (rows U[l] weighted by x).
+nsd_status nsd_ttm(const nsd_ttv_plan *T, const float *x, const float *U, int32_t R, float *Y,
+                   void *ws, size_t ws_bytes, void *stream) {
+    NSD_TRY(check_ttv(T));
+    NSD_REQUIRE(R >= 1, "R = %d < 1", R);
+    NSD_REQUIRE(T->nnz == 0 || (x && U && Y), "null pointer");
+    if (ws == nullptr || ws_bytes < ttm_ws(T, R))
+        return fail(NSD_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, ttm_ws(T, R));
+    if (T->ny == 0) return NSD_OK;
+    hipStream_t st = as_stream(stream);
+    probe_begin(NSD_KERNEL_TTV, st);
+    const nsd_status s = segreduce(ttv_sgr(T->ny, T->nnz, T->yplan, T->yptr, T->yseg, T->ykidx, x,
+                                           T->yperm, U, Y, ws, R),
+                                   st);
+    probe_end(NSD_KERNEL_TTV, st);
+    return s;
+}
+
+// dx = <gY[key], U[l]> per entry (an SDDMM in (i, j) order written to input
+// positions), dU = the gather-reduce over l of x * gY[key].
+nsd_status nsd_ttm_vjp(const nsd_ttv_plan *T, const float *x, const float *U, int32_t R,
+                       const float *gY, float *dx, float *dU, void *ws, size_t ws_bytes,
+                       void *stream) {
+    NSD_TRY(check_ttv(T));
+    NSD_REQUIRE(R >= 1, "R = %d < 1", R);
+    NSD_REQUIRE(dU != nullptr, "dU is NULL");
+    NSD_REQUIRE(T->nnz == 0 || (x && U && gY && dx), "null pointer");
+    if (ws == nullptr || ws_bytes < ttm_ws(T, R))
+        return fail(NSD_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, ttm_ws(T, R));
+    hipStream_t st = as_stream(stream);
+    if (T->nnz > 0) {
+        SddmmParams sp;
+        sp.nnz = T->nnz;
+        sp.k = R;
+        sp.rowidx = T->yseg;
+        sp.colind = T->ykidx;
+        sp.X = gY;
+        sp.Y = U;
+        sp.out = dx;
+        sp.operm = T->yperm;
+        probe_begin(NSD_KERNEL_TTV, st);
+        const nsd_status s = sddmm(sp, st);
+        probe_end(NSD_KERNEL_TTV, st);
+        NSD_TRY(s);
+    }
+    return segreduce(ttv_sgr(T->dims[2], T->nnz, T->lplan, T->lptr, T->lseg, T->lpair, x, T->lperm,
+                             gY, dU, ws, R),
                      st);
 }
 

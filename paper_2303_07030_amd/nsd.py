@@ -140,6 +140,9 @@ _SIGS = {
     "nsd_ttv_workspace_size": (C.c_int, [_TTV, C.POINTER(_SZ)]),
     "nsd_ttv": (C.c_int, [_TTV, _P, _P, _P, _P, _SZ, _P]),
     "nsd_ttv_vjp": (C.c_int, [_TTV, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "nsd_ttm_workspace_size": (C.c_int, [_TTV, _I, C.POINTER(_SZ)]),
+    "nsd_ttm": (C.c_int, [_TTV, _P, _P, _I, _P, _P, _SZ, _P]),
+    "nsd_ttm_vjp": (C.c_int, [_TTV, _P, _P, _I, _P, _P, _P, _P, _SZ, _P]),
     "nsd_dot": (C.c_int, [C.c_int64, _P, _P, C.c_double, C.c_int, _P, _P, _SZ, _P]),
     "nsd_spmm_vjp": (C.c_int, [C.POINTER(nsd_csr), C.POINTER(nsd_csc), _P, _P, _I, _P, _P, _P,
                                _SZ, _P]),
@@ -412,6 +415,22 @@ def nsd_ttv(T: nsd_ttv_plan, x, v, y, ws, stream=None):
 def nsd_ttv_vjp(T: nsd_ttv_plan, x, v, gy, dx, dv, ws, stream=None):
     _check(_lib.nsd_ttv_vjp(C.byref(T), _p(x), _p(v), _p(gy), _p(dx), _p(dv), _p(ws), _nbytes(ws),
                             _stream(stream)), "nsd_ttv_vjp")
+
+
+def nsd_ttm_workspace_size(T: nsd_ttv_plan, R: int) -> int:
+    b = _SZ(0)
+    _check(_lib.nsd_ttm_workspace_size(C.byref(T), R, C.byref(b)), "nsd_ttm_workspace_size")
+    return b.value
+
+
+def nsd_ttm(T: nsd_ttv_plan, x, U, R, Y, ws, stream=None):
+    _check(_lib.nsd_ttm(C.byref(T), _p(x), _p(U), R, _p(Y), _p(ws), _nbytes(ws), _stream(stream)),
+           "nsd_ttm")
+
+
+def nsd_ttm_vjp(T: nsd_ttv_plan, x, U, R, gY, dx, dU, ws, stream=None):
+    _check(_lib.nsd_ttm_vjp(C.byref(T), _p(x), _p(U), R, _p(gY), _p(dx), _p(dU), _p(ws),
+                            _nbytes(ws), _stream(stream)), "nsd_ttm_vjp")
 
 
 # ------------------------------------------------------------ BATAX Jacobian

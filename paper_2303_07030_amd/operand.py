@@ -300,3 +300,8 @@ class DeviceTtv:
     def workspace(self):
         n = nsd.nsd_ttv_workspace_size(self.desc)
         return torch.empty(max(n, 256), dtype=torch.uint8, device=self.yptr.device)
+
+    def ttm_workspace(self, R: int):
+        """Workspace of nsd_ttm / nsd_ttm_vjp at width R."""
+        n = nsd.nsd_ttm_workspace_size(self.desc, R)
+        return torch.empty(max(n, 256), dtype=torch.uint8, device=self.yptr.device)

@@ -583,6 +583,36 @@ def test_ttv_and_vjp(nsd, orc, dims, nnz):
     assert_mag_close(host(dv), rdv, rdvm, what="dv")
 
 
+@pytest.mark.parametrize("R", [1, 3, 8, 32, 64, 100])
+@pytest.mark.parametrize("dims,nnz", [((30, 40, 50), 6000), ((3, 4, 2000), 5000)])
+def test_ttm_and_vjp(nsd, orc, dims, nnz, R):
+    # TTM along mode 3 on the projected keys and its VJP; the second shape
+    # gives few projected keys holding long l-fibres (chunked segments)
+    from paper_2303_07030_amd.operand import DeviceTtv
+    rng = np.random.default_rng(nnz + R)
+    keys = rng.choice(dims[0] * dims[1] * dims[2], size=nnz, replace=False)
+    i = (keys // (dims[1] * dims[2])).astype(np.int32)
+    j = ((keys // dims[2]) % dims[1]).astype(np.int32)
+    l = (keys % dims[2]).astype(np.int32)
+    x = rng.standard_normal(nnz).astype(np.float32)
+    U = rng.standard_normal((dims[2], R)).astype(np.float32)
+    T = DeviceTtv(dims, i, j, l)
+    D = orc.Dok(dims, (i, j, l), x)
+    yi, yj, y, ym = orc.ttm(D, U, R)
+    assert T.ny == len(yi)
+    ws = T.ttm_workspace(R)
+    Y = torch.full((T.ny, R), np.nan, dtype=torch.float32, device="cuda")
+    nsd.nsd_ttm(T.desc, dev(x), dev(U), R, Y, ws)
+    assert_mag_close(host(Y), y, ym, what="Y")
+    gY = rng.standard_normal((T.ny, R)).astype(np.float32)
+    dx = torch.full((nnz,), np.nan, dtype=torch.float32, device="cuda")
+    dU = torch.full((dims[2], R), np.nan, dtype=torch.float32, device="cuda")
+    nsd.nsd_ttm_vjp(T.desc, dev(x), dev(U), R, dev(gY), dx, dU, ws)
+    rdx, rdxm, rdU, rdUm = orc.ttm_vjp(D, U, R, gY, i, j, l)
+    assert_mag_close(host(dx), rdx, rdxm, what="dX")
+    assert_mag_close(host(dU), rdU, rdUm, what="dU")
+
+
 # ------------------------------------------------------- edge cases
 
 def test_empty_matrix_writes_zeros(nsd, operand):
