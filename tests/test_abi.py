@@ -114,6 +114,21 @@ def test_host_argument_errors_before_launch(nsd):
         nsd.nsd_coo_mode_index(3, 0, 0x1000, 0x1000, 0x1000, 0x1000, None)   # dim < 1
     assert e.value.status == nsd.NSD_ERR_INVALID_ARG
     assert "dim" in nsd.nsd_last_error()
+    with pytest.raises(nsd.NsdError) as e:
+        nsd.nsd_diag_keys(A, 1.0, None)                     # no output for 3 entries
+    assert e.value.status == nsd.NSD_ERR_INVALID_ARG
+    T = nsd.nsd_ttv_plan()
+    T.dims[:] = (4, 4, 4)
+    with pytest.raises(nsd.NsdError) as e:
+        nsd.nsd_ttm_workspace_size(T, 0)                    # R < 1
+    assert e.value.status == nsd.NSD_ERR_INVALID_ARG
+    with pytest.raises(nsd.NsdError) as e:
+        nsd.nsd_ttm(T, None, None, 8, None, None)           # empty plan, no workspace
+    assert e.value.status == nsd.NSD_ERR_WORKSPACE
+    T.nnz = 5
+    with pytest.raises(nsd.NsdError) as e:
+        nsd.nsd_ttm_vjp(T, 0x1000, 0x1000, 8, 0x1000, 0x1000, 0x1000, None)  # plan not built
+    assert e.value.status == nsd.NSD_ERR_INVALID_ARG
 
 
 def test_binding_fails_loudly_without_library(tmp_path):
