@@ -520,9 +520,37 @@ def main():
         "graph": graph,
         "achievable": stream,
         "cpu_baseline": cpu,
+        "inputs": {"numpy": np.__version__, "index_sha256": index_digest(d),
+                   "seeds": f"PCG64 from SeedSequence(entropy={synth.ENTROPY}, "
+                            f"spawn_key=(workload, replicate={args.replicate}))"},
         "source_digest": source_digest(),
     }
     print(json.dumps(out))
+
+
+def index_digest(d):
+    """sha256 of the workload's index arrays (every integer array, in key
+    order), so that runs on different hosts can be checked for identical
+    patterns."""
+    h = hashlib.sha256()
+    for key in sorted(d):
+        v = d[key]
+        for a in (v if isinstance(v, (list, tuple)) else [v]):
+            if isinstance(a, np.ndarray) and a.dtype.kind in "iu":
+                h.update(key.encode())
+                h.update(memoryview(np.ascontiguousarray(a)).cast("B"))
+    return h.hexdigest()[:16]
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def single_steps(torch, S, steps):
@@ -756,7 +784,7 @@ def cpu_baseline(args, d):
             "cores": 1, "kind": "oracle",
             "sample": f"{what}: {passes} pass(es) of {done}, {el:.1f} s on one thread",
             "dok_build_s": round(dok_s[0], 3), "compute_s": round(el - dok_s[0], 3),
-            "host_cpus_visible": len(os.sched_getaffinity(0))}
+            "host_cpus_visible": len(os.sched_getaffinity(0)), "cpu_model": cpu_model()}
 
 
 if __name__ == "__main__":
