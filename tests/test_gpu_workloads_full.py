@@ -116,10 +116,16 @@ def test_bilinear_full_workload(nsd, orc):
 
 # ----------------------------------------------------- matrix factorisation
 
-def test_mf_full_workload(nsd, orc):
+@pytest.fixture(scope="module")
+def mf_data():
+    """The factorisation input (50M distinct COO entries), drawn once."""
     from paper_2303_07030_amd import synth
+    return synth.make("mf")
+
+
+def test_mf_full_workload(nsd, orc, mf_data):
     from paper_2303_07030_amd.operand import DeviceCsr
-    d = synth.make("mf")
+    d = mf_data
     nr, nc, k = d["nrows"], d["ncols"], d["k"]
     row, col, val, U, V = d["row"], d["col"], d["val"], d["U"], d["V"]
     A = DeviceCsr.from_coo(nr, nc, row, col, val, k_hint=k)
@@ -160,6 +166,68 @@ def test_mf_full_workload(nsd, orc):
 
     L, Lm = chunked_loss(orc, len(row), part)
     assert_mag_close(Lg, L, Lm, what="loss")
+
+
+# ---------------------------------------------------------------- builders
+
+def test_builders_full_workload(nsd, mf_data):
+    """COO -> CSR, CSR -> CSC and the value permute on the 50M unsorted
+    entries, the calls and arguments the builder bench times, bit for bit
+    against their definitions: a stable lexicographic (row, col) sort and a
+    stable sort of the CSR slots by column."""
+    d = mf_data
+    nr, nc = d["nrows"], d["ncols"]
+    row, col, val = d["row"], d["col"], d["val"]
+    n = len(row)
+
+    def i32(m):
+        return torch.full((max(m, 1),), -1, dtype=torch.int32, device="cuda")
+
+    rowptr, rowidx, colind, perm = i32(nr + 1), i32(n), i32(n), i32(n)
+    colptr, colidx, rowind, permc = i32(nc + 1), i32(n), i32(n), i32(n)
+    vout = torch.full((n,), np.nan, dtype=torch.float32, device="cuda")
+    valT = torch.full((n,), np.nan, dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(nsd.nsd_build_workspace_size(n, max(nr, nc)),
+                         nsd.nsd_build_workspace_size(n, nc)), dtype=torch.uint8, device="cuda")
+    m = nsd.nsd_coo_to_csr(nr, nc, n, dev(row), dev(col), dev(val), nsd.NSD_DUP_ERROR, rowptr,
+                           rowidx, colind, vout, perm, ws)
+    assert m == n  # the recipe keeps distinct coordinates only
+    A = nsd.csr_desc(nr, nc, rowptr, rowidx[:m], colind[:m], vout[:m])
+    nsd.nsd_csr_to_csc(A, colptr, colidx, rowind, permc, ws)
+    nsd.nsd_gather_f32(m, permc, vout, valT)
+
+    order = np.lexsort((col, row))  # by row, then column
+    assert np.array_equal(host(perm), order), "perm"
+    r_sorted, c_sorted = row[order], col[order]
+    assert np.array_equal(host(rowidx), r_sorted), "rowidx"
+    assert np.array_equal(host(colind), c_sorted), "colind"
+    assert np.array_equal(host(vout).view(np.uint32), val[order].view(np.uint32)), "values"
+    assert np.array_equal(host(rowptr), np.concatenate(
+        [[0], np.cumsum(np.bincount(row, minlength=nr))]).astype(np.int32)), "rowptr"
+    q = np.argsort(c_sorted, kind="stable")
+    assert np.array_equal(host(permc), q), "CSC perm"
+    assert np.array_equal(host(colidx), c_sorted[q]), "colidx"
+    assert np.array_equal(host(rowind), r_sorted[q]), "rowind"
+    assert np.array_equal(host(colptr), np.concatenate(
+        [[0], np.cumsum(np.bincount(col, minlength=nc))]).astype(np.int32)), "colptr"
+    assert np.array_equal(host(valT).view(np.uint32), val[order][q].view(np.uint32)), "valT"
+
+
+# ---------------------------------------------------------- BATAX Jacobian
+
+def test_batax_full_workload(nsd, orc):
+    """J = beta A^T A on the 100K x 100K, 1M-entry input of the BATAX bench
+    (10.1M Jacobian keys): pattern bit for bit, values to the 1e-4 bar, all
+    against the oracle's dictionary."""
+    from paper_2303_07030_amd import synth
+    from paper_2303_07030_amd.operand import DeviceCsr
+    from test_gpu_parity import check_batax, run_batax
+    d = synth.make("batax")
+    A = DeviceCsr(d["nrows"], d["ncols"], d["rowptr"], d["colind"], d["val"], build_csc=False)
+    got = run_batax(nsd, A, d["beta"])
+    assert len(got[1]) > 10_000_000
+    orc.set_threads(1)
+    check_batax(orc, d["nrows"], d["ncols"], d["rowptr"], d["colind"], d["val"], d["beta"], got)
 
 
 # --------------------------------------------------------- CP decomposition
