@@ -323,7 +323,8 @@ nsd_status nsd_validate_coo(int32_t order, const int32_t *dims, int32_t nnz,
 
 /* ------------------------------------------------------------- forward */
 
-/* y = A x (SpMV).  x [ncols], y [nrows].  Async. */
+/* y = A x (SpMV: the matrix-vector product of Logical SDQLite, Section 3,
+ * a sum over each row's stored entries).  x [ncols], y [nrows].  Async. */
 nsd_status nsd_spmv(const nsd_csr *A, const float *x, float *y, void *ws, size_t ws_bytes,
                     void *stream);
 
@@ -335,7 +336,9 @@ nsd_status nsd_spmm(const nsd_csr *A, const float *B, int32_t k, float *C, void 
 /* ---------------------------------------------------- VJP primitives */
 
 /*
- * SDDMM on A's pattern, the gradient w.r.t. a sparse operand:
+ * SDDMM on A's pattern, the gradient w.r.t. a sparse operand.  The gradient
+ * API seeds a sparse input with a one-hot over its own stored keys
+ * (Sections 4.2 and 4.3), so its gradient is keyed by those keys only:
  *   out[p] = alpha * <X[rowidx[p], :], Y[colind[p], :]>   for p < nnz,
  * aligned with A's CSR order (A's values are not read).  X [nrows x k]
  * (NULL: all ones), Y [ncols x k], out [nnz].  Async.
@@ -344,7 +347,10 @@ nsd_status nsd_sddmm(const nsd_csr *A, const float *X, const float *Y, int32_t k
                      float alpha, float *out, void *stream);
 
 /*
- * Transposed product, the gradient w.r.t. a dense right operand:
+ * Transposed product, the gradient w.r.t. a dense right operand of the
+ * matrix product (Sections 4.2 and 4.3; the "+=" of singletons inside a sum,
+ * Section 5.5, computed as a gather over the CSC so every output is written
+ * once):
  *   out[j, :] = alpha * sum over stored (i, j) of A(i, j) * G[i, :]
  * read through the CSC At of A (values taken from A->val via At->perm).
  * G [nrows x k] (NULL: all ones, e.g. column sums for k = 1), out [ncols x k].
@@ -375,7 +381,8 @@ nsd_status nsd_spmv_vjp(const nsd_csr *A, const nsd_csc *At, const float *x, con
  * every gradient and never the loss.  `loss` is one device double. */
 
 /*
- * L = sum(A x) (SMVM of the experiments section).
+ * L = sum(A x): the SMVM kernel of Section 7.1 (the sum of a matrix-vector
+ * product), differentiated with respect to both operands (Section 4.3).
  * dA[p] = seed * x[colind[p]] on A's pattern; dx = seed * A^T 1.
  * x [ncols]; dA [nnz]; dx [ncols].  Async.
  */
@@ -384,7 +391,9 @@ nsd_status nsd_loss_sum_spmv(const nsd_csr *A, const nsd_csc *At, const float *x
                              void *stream);
 
 /*
- * L = 1/2 ||A B||_F^2.  C = A B (written to C [nrows x k]);
+ * L = 1/2 ||A B||_F^2: a loss over the matrix product of Section 3, its
+ * gradients those of the gradient API (Section 4.3), the sparse one on A's
+ * keys (Section 4.2).  C = A B (written to C [nrows x k]);
  * dA[p] = seed * <C[i,:], B[j,:]> on A's pattern (SDDMM);
  * dB = seed * A^T C.  B, dB [ncols x k]; dA [nnz].  Async.
  */
@@ -393,7 +402,9 @@ nsd_status nsd_loss_frob_spmm(const nsd_csr *A, const nsd_csc *At, const float *
                               void *ws, size_t ws_bytes, void *stream);
 
 /*
- * GNN layer: L = sum((A H) o G) = sum over stored (i, j) of A(i,j) <G[i,:], H[j,:]>.
+ * GNN layer: L = sum((A H) o G) = sum over stored (i, j) of A(i,j) <G[i,:], H[j,:]>
+ * (the matrix product of Section 3 weighted by the upstream gradient G;
+ * gradients as in Sections 4.2 and 4.3).
  * dA[p] = seed * <G[i,:], H[j,:]> on A's pattern (SDDMM); dH = seed * A^T G.
  * H, dH [ncols x k]; G [nrows x k]; dA [nnz].  Async.
  */
@@ -402,7 +413,8 @@ nsd_status nsd_loss_bilinear(const nsd_csr *A, const nsd_csc *At, const float *H
                              float *dH, void *ws, size_t ws_bytes, void *stream);
 
 /*
- * Sparse matrix factorisation:
+ * Sparse matrix factorisation, a sum over A's stored keys (the dictionary
+ * iteration of Section 2.2; gradients by Sections 4.2 and 4.3):
  *   L = sum over stored (i, j) of r_ij^2,  r_ij = A(i,j) - <U[i,:], V[j,:]>
  *   dU[i,:] = -2 seed sum_j r_ij V[j,:];  dV[j,:] = -2 seed sum_i r_ij U[i,:]
  * A's CSR gives the row pass (values A->val), its CSC the column pass with
@@ -420,7 +432,9 @@ nsd_status nsd_loss_mf(const nsd_csr *A, const nsd_csc *At, const float *valT, c
 nsd_status nsd_cp_workspace_size(const nsd_coo3 *X, int32_t rank, size_t *bytes);
 
 /*
- * CP decomposition of a sparse 3-tensor X with factors F1 [dims[0] x rank],
+ * CP decomposition of a sparse 3-tensor X (an order-3 tensor of nested
+ * dictionaries, Section 3; its loss a sum over X's stored keys, gradients by
+ * Sections 4.2 and 4.3) with factors F1 [dims[0] x rank],
  * F2 [dims[1] x rank], F3 [dims[2] x rank]:
  *   R = X - m on X's keys, m_ijl = sum_r F1[i,r] F2[j,r] F3[l,r]
  *   L = 1/2 sum R^2
