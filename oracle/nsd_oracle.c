@@ -291,7 +291,8 @@ void orc_spmm(const orc_dok *A, const double *B, const double *Bmag, int64_t k,
 }
 
 /*
- * Transposed product, the gradient w.r.t. a dense right operand:
+ * Transposed product, the gradient w.r.t. a dense right operand (the reverse
+ * gradient that Sections 4.2-4.3 produce for the matrix product of Section 3):
  * out(j,:) = alpha * sum over stored (i, j, a) of a * G(i,:).
  * G == NULL means all ones (k must then be the output width, e.g. 1 for the
  * column sums of SMVM's gradient).  Only columns listed in sel are produced.
@@ -323,7 +324,8 @@ void orc_spmm_t(const orc_dok *A, const double *G, const double *Gmag, int64_t k
 }
 
 /*
- * SDDMM, the gradient w.r.t. the sparse operand: for every queried
+ * SDDMM, the gradient w.r.t. the sparse operand (keyed by its stored keys,
+ * since `onehot` iterates only those, Section 4.3): for every queried
  * coordinate (qi, qj) that is a stored key of A,
  *   out = alpha * sum_c X(qi, c) * Y(qj, c);
  * a coordinate that is not stored gets 0, because the one-hot seed of the
@@ -366,7 +368,7 @@ static void chunk_bounds(int64_t cap, int c, int64_t *lo, int64_t *hi)
     *hi = cap * (c + 1) / ORC_CHUNKS;
 }
 
-/* sum(A . x) with x dense (SMVM of the experiments): L = sum over stored
+/* sum(A . x) with x dense (the SMVM kernel of Section 7.1): L = sum over stored
  * (i, j, a) of a * x(j) */
 void orc_loss_sum_spmv(const orc_dok *A, const double *x, double *loss, double *mag)
 {
@@ -381,7 +383,8 @@ void orc_loss_sum_spmv(const orc_dok *A, const double *x, double *loss, double *
     *loss = L; *mag = M;
 }
 
-/* L = 1/2 * sum of C(i,c)^2 over a dense n x k array; mag uses Cmag */
+/* L = 1/2 * sum of C(i,c)^2 over a dense n x k array (a plain sum over a
+ * dense array, Section 3); mag uses Cmag */
 void orc_loss_half_sq(int64_t n, const double *C, const double *Cmag, double *loss,
                       double *mag)
 {
@@ -390,7 +393,8 @@ void orc_loss_half_sq(int64_t n, const double *C, const double *Cmag, double *lo
     *loss = 0.5 * L; *mag = 0.5 * M;
 }
 
-/* bilinear form of the GNN layer: L = sum over stored (i, j, a) of
+/* bilinear form of the GNN layer (a sum over A's stored keys, Section 2.2):
+ * L = sum over stored (i, j, a) of
  * a * <G(i,:), H(j,:)>  ( = sum of (A H) o G ) */
 void orc_loss_bilinear(const orc_dok *A, const double *G, const double *H, int64_t k,
                        double *loss, double *mag)
@@ -435,7 +439,8 @@ static double mf_resid(const double *U, const double *V, int64_t k, int64_t i, i
     return a - dot;
 }
 
-/* L = sum over stored (i, j, a) of (a - <U_i, V_j>)^2 */
+/* L = sum over stored (i, j, a) of (a - <U_i, V_j>)^2 (a sum over the stored
+ * keys, Section 2.2) */
 void orc_mf_loss(const orc_dok *A, const double *U, const double *V, int64_t k,
                  double *loss, double *mag)
 {
@@ -460,7 +465,8 @@ void orc_mf_loss(const orc_dok *A, const double *U, const double *V, int64_t k,
     *loss = L; *mag = M;
 }
 
-/* residual at queried coordinates (0 where not stored) */
+/* residual at queried coordinates (0 where not stored: the lookup of an
+ * absent key, Section 2.2) */
 void orc_mf_resid(const orc_dok *A, const double *U, const double *V, int64_t k,
                   int64_t nq, const int32_t *qi, const int32_t *qj, double *r,
                   double *rmag)
@@ -474,6 +480,7 @@ void orc_mf_resid(const orc_dok *A, const double *U, const double *V, int64_t k,
 }
 
 /*
+ * Reverse gradients of the factorisation loss (Sections 4.2-4.3):
  * mode 0: dU(i,:) = -2 * sum over stored (i, j) of r_ij * V(j,:)
  * mode 1: dV(j,:) = -2 * sum over stored (i, j) of r_ij * U(i,:)
  * for the selected rows of dU (mode 0) or of dV (mode 1).
@@ -518,7 +525,8 @@ static double cp_resid(const double *F1, const double *F2, const double *F3, int
     return x - m;
 }
 
-/* L = 1/2 * sum over stored (i, j, l, x) of (x - m_ijl)^2 */
+/* L = 1/2 * sum over stored (i, j, l, x) of (x - m_ijl)^2 (a sum over the
+ * stored keys of an order-3 tensor, Sections 2.2 and 3) */
 void orc_cp_loss(const orc_dok *X, const double *F1, const double *F2, const double *F3,
                  int64_t R, double *loss, double *mag)
 {
@@ -543,7 +551,8 @@ void orc_cp_loss(const orc_dok *X, const double *F1, const double *F2, const dou
     *loss = 0.5 * L; *mag = 0.5 * M;
 }
 
-/* residual (the gradient w.r.t. the stored values) at queried coordinates */
+/* residual (the gradient w.r.t. the stored values, keyed by X's keys,
+ * Section 4.3) at queried coordinates */
 void orc_cp_resid(const orc_dok *X, const double *F1, const double *F2, const double *F3,
                   int64_t R, int64_t nq, const int32_t *qi, const int32_t *qj,
                   const int32_t *ql, double *res, double *resmag)
@@ -558,7 +567,8 @@ void orc_cp_resid(const orc_dok *X, const double *F1, const double *F2, const do
 }
 
 /*
- * Factor gradients, the negated MTTKRPs of the residual:
+ * Factor gradients, the negated MTTKRPs of the residual (reverse gradients
+ * of the CP loss, Sections 4.2-4.3):
  *   mode 0: dF1(i,:) = -sum over stored (i, j, l) of R_ijl * (F2(j,:) o F3(l,:))
  *   mode 1: dF2(j,:) = -sum ... R_ijl * (F1(i,:) o F3(l,:))
  *   mode 2: dF3(l,:) = -sum ... R_ijl * (F1(i,:) o F2(j,:))
@@ -629,7 +639,8 @@ int64_t orc_ttv(const orc_dok *X, const double *v, int32_t *yi, int32_t *yj, dou
 }
 
 /*
- * Vector-Jacobian product of Y = X x_3 v given the upstream gY (a DOK on Y's
+ * Vector-Jacobian product (Sections 4.2-4.3) of Y = X x_3 v given the
+ * upstream gY (a DOK on Y's
  * keys, read by lookup so absent keys count as 0):
  *   dX at queried (i, j, l) that are stored: gY(i, j) * v(l)
  *   dv(l) = sum over stored (i, j, l, x) of x * gY(i, j)
@@ -716,7 +727,8 @@ int64_t orc_ttm(const orc_dok *X, const double *U, int32_t R, int32_t *yi, int32
 }
 
 /*
- * Vector-Jacobian product of Y = X x_3 U given the upstream gY row-major
+ * Vector-Jacobian product (Sections 4.2-4.3) of Y = X x_3 U given the
+ * upstream gY row-major
  * [ny x R] on Y's keys in (i, j) order:
  *   dX at queried (i, j, l) that are stored: sum_r gY(i, j, r) U(l, r)
  *   dU(l, r) = sum over stored (i, j, l, x) of x * gY(i, j, r)
@@ -912,7 +924,8 @@ void orc_cpn_loss(const orc_dok *X, const double *const *F, int64_t R, double *l
     *mag = 0.5 * M;
 }
 
-/* residual (the gradient w.r.t. the stored values) at queried keys;
+/* residual (the gradient w.r.t. the stored values, keyed by X's keys,
+ * Section 4.3) at queried keys;
  * q[n][p] is coordinate n of query p */
 void orc_cpn_resid(const orc_dok *X, const double *const *F, int64_t R, int64_t nq,
                    const int32_t *const *q, double *res, double *resmag)
@@ -932,7 +945,8 @@ void orc_cpn_resid(const orc_dok *X, const double *const *F, int64_t R, int64_t 
 }
 
 /*
- * Factor gradient of mode n, the negated mode-n MTTKRP of the residual:
+ * Factor gradient of mode n, the negated mode-n MTTKRP of the residual
+ * (reverse gradient of the CP loss, Sections 4.2-4.3):
  *   dF_n(c_n, :) = -sum over stored keys of R * (o_{m != n} F_m(c_m, :))
  */
 void orc_cpn_grad(const orc_dok *X, const double *const *F, int64_t R, int mode, int64_t nsel,
