@@ -243,9 +243,10 @@ constexpr int dual_unroll() {
     return reduce_unroll<G, NSD_DUAL_UNROLL>();
 #else
     // measured on MI355X: eight entries per batch for full-wave slots
-    // (k > 128), four for 32-lane slots, two for narrower ones, four for
-    // single-lane slots
-    return reduce_unroll<G, G >= 64 ? 8 : (G >= 32 || G == 1 ? 4 : 2)>();
+    // (k > 128), four for 32- and 16-lane slots (the SpMM column pass at
+    // k = 64: 54.8 us against 57.6 with two, 62.5 with eight), two for
+    // narrower ones, four for single-lane slots
+    return reduce_unroll<G, G >= 64 ? 8 : (G >= 16 || G == 1 ? 4 : 2)>();
 #endif
 }
 
