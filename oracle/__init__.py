@@ -56,6 +56,8 @@ def _load():
         "orc_ttv_vjp": (None, [_p, _p, _p, _i64, _p, _p, _p, _p, _p, _p, _p]),
         "orc_ttm": (_i64, [_p, _p, C.c_int32, _p, _p, _p, _p]),
         "orc_ttm_vjp": (None, [_p, _p, C.c_int32, _p, _i64, _p, _p, _p, _p, _p, _p, _p]),
+        "orc_ttmn": (_i64, [_p, C.c_int32, _p, C.c_int32, _p, _p, _p]),
+        "orc_ttmn_vjp": (None, [_p, C.c_int32, _p, C.c_int32, _p, _i64, _p, _p, _p, _p, _p]),
         "orc_batax_jacobian": (_i64, [_p, _f64, _i64, _p, _p, _p, _p]),
         "orc_spmm_jvp": (None, [_p, _p, _p, _p, _i64, _p, _p, _p, _p]),
         "orc_dok_buildn": (_p, [C.c_int32, _p, _i64, _p, _p]),
@@ -74,7 +76,9 @@ def _load():
 
 
 def set_threads(n: int):
-    """Threads for the oracle's OpenMP loss scans on the calling thread."""
+    """OpenMP threads of the oracle's loss scans and gradient loops, for
+    calls made from the calling thread.  The gradient loops split their
+    outputs by owner, so every thread count gives bitwise the same result."""
     _load().orc_set_threads(n)
 
 
@@ -318,6 +322,35 @@ def ttm_vjp(X: Dok, U, R, gY, qi, qj, ql):
     _load().orc_ttm_vjp(X.h, _ptr(U), R, _ptr(gY), len(qi), _ptr(qi), _ptr(qj), _ptr(ql),
                         _ptr(dX), _ptr(dXm), _ptr(dU), _ptr(dUm))
     return dX, dXm, dU.reshape(X.dims[2], R), dUm.reshape(X.dims[2], R)
+
+
+def ttmn(X: Dok, mode, U, R):
+    """Mode-`mode` product Y = X x_mode U (U [dims[mode] x R]) of an order-N
+    DOK on its projected keys: (keys, y [ny x R], ymag), keys a list of the
+    N - 1 coordinate arrays of the other modes, in lexicographic order."""
+    U = _f64a(U)
+    cap = max(X.nkeys, 1)
+    keys = [np.empty(cap, dtype=np.int32) for _ in range(len(X.dims) - 1)]
+    kp = (C.c_void_p * len(keys))(*[_ptr(k) for k in keys])
+    y, ym = np.empty(cap * R), np.empty(cap * R)
+    n = _load().orc_ttmn(X.h, int(mode), _ptr(U), R, kp, _ptr(y), _ptr(ym))
+    return [k[:n] for k in keys], y[: n * R].reshape(n, R), ym[: n * R].reshape(n, R)
+
+
+def ttmn_vjp(X: Dok, mode, U, R, gY, coords):
+    """(dX at the queried keys, dXmag, dU [dims[mode] x R], dUmag) of the
+    mode product for the upstream gY [ny x R] on Y's keys in lexicographic
+    order; coords: N arrays of query coordinates."""
+    U, gY = _f64a(U), _f64a(gY)
+    qs = [_i32(c) for c in coords]
+    qp = (C.c_void_p * len(qs))(*[_ptr(c) for c in qs])
+    n = len(qs[0])
+    dX, dXm = np.empty(n), np.empty(n)
+    nl = X.dims[mode]
+    dU, dUm = np.empty(nl * R), np.empty(nl * R)
+    _load().orc_ttmn_vjp(X.h, int(mode), _ptr(U), R, _ptr(gY), n, qp, _ptr(dX), _ptr(dXm),
+                         _ptr(dU), _ptr(dUm))
+    return dX, dXm, dU.reshape(nl, R), dUm.reshape(nl, R)
 
 
 def batax_jacobian(A: Dok, beta):

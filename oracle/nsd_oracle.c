@@ -38,7 +38,14 @@
 #include <omp.h>
 #endif
 
-/* threads used by the OpenMP loss scans (the rest is single-threaded) */
+/*
+ * Threads.  The loss scans sum fixed chunks of the hash table in chunk order;
+ * the gradient loops split their OUTPUTS by owner (output index modulo the
+ * thread count): every thread scans all stored keys and accumulates only into
+ * the outputs it owns.  Each output therefore receives its terms in the same
+ * slot order whatever the thread count, and the results are bitwise those of
+ * one thread.
+ */
 void orc_set_threads(int n)
 {
 #ifdef _OPENMP
@@ -54,6 +61,25 @@ int orc_max_threads(void)
     return omp_get_max_threads();
 #else
     return 1;
+#endif
+}
+
+/* number of threads of the enclosing parallel region and this one's index */
+static int orc_nthr(void)
+{
+#ifdef _OPENMP
+    return omp_get_num_threads();
+#else
+    return 1;
+#endif
+}
+
+static int orc_tid(void)
+{
+#ifdef _OPENMP
+    return omp_get_thread_num();
+#else
+    return 0;
 #endif
 }
 
@@ -133,6 +159,8 @@ static void unpack3(const orc_dok *d, int64_t k, int64_t *i, int64_t *j, int64_t
     *j = (k / d->dims[2]) % d->dims[1];
     *l = k % d->dims[2];
 }
+
+static void unpackn(const orc_dok *d, int64_t k, int64_t *c);
 
 orc_dok *orc_dok_build2(int64_t nr, int64_t nc, int64_t nnz, const int32_t *row,
                         const int32_t *col, const float *val)
@@ -273,12 +301,15 @@ void orc_spmm(const orc_dok *A, const double *B, const double *Bmag, int64_t k,
     int64_t rows = sel ? nsel : nr;
     memset(out, 0, sizeof(double) * rows * k);
     memset(outmag, 0, sizeof(double) * rows * k);
+#pragma omp parallel
+    {
+    const int nt = orc_nthr(), me = orc_tid();
     for (int64_t s = 0; s < A->cap; ++s) {
         if (A->key[s] == -1) continue;
         int64_t i, j;
         unpack2(A, A->key[s], &i, &j);
         int64_t o = map[i];
-        if (o < 0) continue;
+        if (o < 0 || o % nt != me) continue;
         double a = A->val[s];
         for (int64_t c = 0; c < k; ++c) {
             double b = B ? B[j * k + c] : 1.0;
@@ -286,6 +317,7 @@ void orc_spmm(const orc_dok *A, const double *B, const double *Bmag, int64_t k,
             out[o * k + c] += a * b;
             outmag[o * k + c] += fabs(a) * bm;
         }
+    }
     }
     free(map);
 }
@@ -306,12 +338,15 @@ void orc_spmm_t(const orc_dok *A, const double *G, const double *Gmag, int64_t k
     int64_t cols = sel ? nsel : nc;
     memset(out, 0, sizeof(double) * cols * k);
     memset(outmag, 0, sizeof(double) * cols * k);
+#pragma omp parallel
+    {
+    const int nt = orc_nthr(), me = orc_tid();
     for (int64_t s = 0; s < A->cap; ++s) {
         if (A->key[s] == -1) continue;
         int64_t i, j;
         unpack2(A, A->key[s], &i, &j);
         int64_t o = map[j];
-        if (o < 0) continue;
+        if (o < 0 || o % nt != me) continue;
         double a = A->val[s];
         for (int64_t c = 0; c < k; ++c) {
             double g = G ? G[i * k + c] : 1.0;
@@ -319,6 +354,7 @@ void orc_spmm_t(const orc_dok *A, const double *G, const double *Gmag, int64_t k
             out[o * k + c] += alpha * a * g;
             outmag[o * k + c] += fabs(alpha * a) * gm;
         }
+    }
     }
     free(map);
 }
@@ -336,6 +372,7 @@ void orc_sddmm(const orc_dok *A, const double *X, const double *Xmag, const doub
                const double *Ymag, int64_t k, double alpha, int64_t nq,
                const int32_t *qi, const int32_t *qj, double *out, double *outmag)
 {
+#pragma omp parallel for schedule(static)
     for (int64_t q = 0; q < nq; ++q) {
         int pr;
         int64_t i = qi[q], j = qj[q];
@@ -493,18 +530,22 @@ void orc_mf_grad(const orc_dok *A, const double *U, const double *V, int64_t k, 
     int64_t rows = sel ? nsel : n;
     memset(out, 0, sizeof(double) * rows * k);
     memset(outmag, 0, sizeof(double) * rows * k);
+#pragma omp parallel
+    {
+    const int nt = orc_nthr(), me = orc_tid();
     for (int64_t s = 0; s < A->cap; ++s) {
         if (A->key[s] == -1) continue;
         int64_t i, j;
         unpack2(A, A->key[s], &i, &j);
         int64_t o = map[mode == 0 ? i : j];
-        if (o < 0) continue;
+        if (o < 0 || o % nt != me) continue;
         double rm, r = mf_resid(U, V, k, i, j, A->val[s], &rm);
         const double *other = mode == 0 ? V + j * k : U + i * k;
         for (int64_t c = 0; c < k; ++c) {
             out[o * k + c] += -2.0 * r * other[c];
             outmag[o * k + c] += 2.0 * rm * fabs(other[c]);
         }
+    }
     }
     free(map);
 }
@@ -582,12 +623,15 @@ void orc_cp_grad(const orc_dok *X, const double *F1, const double *F2, const dou
     int64_t rows = sel ? nsel : n;
     memset(out, 0, sizeof(double) * rows * R);
     memset(outmag, 0, sizeof(double) * rows * R);
+#pragma omp parallel
+    {
+    const int nt = orc_nthr(), me = orc_tid();
     for (int64_t s = 0; s < X->cap; ++s) {
         if (X->key[s] == -1) continue;
         int64_t c[3];
         unpack3(X, X->key[s], &c[0], &c[1], &c[2]);
         int64_t o = map[c[mode]];
-        if (o < 0) continue;
+        if (o < 0 || o % nt != me) continue;
         double rm, r = cp_resid(F1, F2, F3, R, c[0], c[1], c[2], X->val[s], &rm);
         const double *Fs[3] = {F1, F2, F3};
         const double *P = Fs[(mode + 1) % 3] + c[(mode + 1) % 3] * R;
@@ -596,6 +640,7 @@ void orc_cp_grad(const orc_dok *X, const double *F1, const double *F2, const dou
             out[o * R + t] += -r * P[t] * Q[t];
             outmag[o * R + t] += rm * fabs(P[t] * Q[t]);
         }
+    }
     }
     free(map);
 }
@@ -766,6 +811,136 @@ void orc_ttm_vjp(const orc_dok *X, const double *U, int32_t R, const double *gY,
             double t = X->val[s] * gY[row * R + r];
             dU[l * R + r] += t;
             dUmag[l * R + r] += fabs(t);
+        }
+    }
+    orc_dok_free(K);
+}
+
+/* ------------------------------- tensor-times-matrix along any mode */
+
+/*
+ * Mode-n product of an order-N sparse tensor (3 <= N <= 6) with a matrix,
+ * kept sparse on the projected keys (the n-mode product of Section 3's
+ * tensor algebra; TTV is its R = 1 case):
+ *   Y(c_{-n}, r) = sum over stored keys c with those other coordinates of
+ *                  X(c) * U(c_n, r)
+ * where c_{-n} is the key with coordinate n dropped.  The result is a DOK of
+ * order N - 1 whose keys are the projections of X's keys, built by a sum over
+ * X's keys inserting the row {c_{-n} -> X(c) U(c_n, :)} with "+=" (Section 3,
+ * Section 5.5).  Keys come out in lexicographic order (mode 0 first) as
+ * N - 1 coordinate arrays ykey[o] (the modes other than n in increasing
+ * order), y row-major [ny x R] with its mag.  Returns ny.
+ */
+static void proj_dims(const orc_dok *X, int mode, int64_t *pd)
+{
+    int o = 0;
+    for (int m = 0; m < X->order; ++m)
+        if (m != mode) pd[o++] = X->dims[m];
+}
+
+static int64_t proj_pack(const orc_dok *X, int mode, const int64_t *c)
+{
+    int64_t key = 0;
+    for (int m = 0; m < X->order; ++m)
+        if (m != mode) key = key * X->dims[m] + c[m];
+    return key;
+}
+
+/* the projected keys of X, each DOK value set to the key's row number in
+ * lexicographic order; their coordinates written to ykey (when given) */
+static orc_dok *proj_keys(const orc_dok *X, int mode, int32_t *const *ykey, int64_t *ny)
+{
+    int64_t pd[ORC_MAX_ORDER], c[ORC_MAX_ORDER];
+    proj_dims(X, mode, pd);
+    orc_dok *K = dok_new(X->order - 1, pd, X->n);
+    for (int64_t s = 0; s < X->cap; ++s) {
+        if (X->key[s] == -1) continue;
+        unpackn(X, X->key[s], c);
+        dok_add(K, proj_pack(X, mode, c), 1.0, 0);
+    }
+    int64_t n = K->n, m = 0;
+    kt_pair *kp = (kt_pair *)malloc(sizeof(kt_pair) * (n ? n : 1));
+    for (int64_t s = 0; s < K->cap; ++s)
+        if (K->key[s] != -1) { kp[m].key = K->key[s]; kp[m].tag = s; ++m; }
+    qsort(kp, (size_t)n, sizeof(kt_pair), cmp_kt);
+    for (int64_t q = 0; q < n; ++q) {
+        if (ykey) {
+            int64_t pc[ORC_MAX_ORDER];
+            unpackn(K, kp[q].key, pc);
+            for (int o = 0; o < K->order; ++o) ykey[o][q] = (int32_t)pc[o];
+        }
+        K->val[kp[q].tag] = (double)q;
+    }
+    free(kp);
+    *ny = n;
+    return K;
+}
+
+int64_t orc_ttmn(const orc_dok *X, int32_t mode, const double *U, int32_t R,
+                 int32_t *const *ykey, double *y, double *ymag)
+{
+    int64_t ny, c[ORC_MAX_ORDER];
+    orc_dok *K = proj_keys(X, mode, ykey, &ny);
+    memset(y, 0, sizeof(double) * ny * R);
+    memset(ymag, 0, sizeof(double) * ny * R);
+    for (int64_t s = 0; s < X->cap; ++s) {
+        if (X->key[s] == -1) continue;
+        unpackn(X, X->key[s], c);
+        int64_t q = (int64_t)dok_get(K, proj_pack(X, mode, c), NULL);
+        for (int32_t r = 0; r < R; ++r) {
+            double t = X->val[s] * U[c[mode] * R + r];
+            y[q * R + r] += t;
+            ymag[q * R + r] += fabs(t);
+        }
+    }
+    orc_dok_free(K);
+    return ny;
+}
+
+/*
+ * Vector-Jacobian product (Sections 4.2-4.3) of the mode-n product for the
+ * upstream gY row-major [ny x R] on Y's keys in lexicographic order:
+ *   dX at the queried keys that are stored: sum_r gY(c_{-n}, r) U(c_n, r)
+ *   dU(l, r) = sum over stored keys c with c_n = l of X(c) gY(c_{-n}, r)
+ * q[m][p] is coordinate m of query p.
+ */
+void orc_ttmn_vjp(const orc_dok *X, int32_t mode, const double *U, int32_t R, const double *gY,
+                  int64_t nq, const int32_t *const *q, double *dX, double *dXmag, double *dU,
+                  double *dUmag)
+{
+    int64_t ny, c[ORC_MAX_ORDER];
+    orc_dok *K = proj_keys(X, mode, NULL, &ny);
+    for (int64_t p = 0; p < nq; ++p) {
+        int64_t key = 0;
+        for (int m = 0; m < X->order; ++m) {
+            c[m] = q[m][p];
+            key = key * X->dims[m] + c[m];
+        }
+        int pr;
+        dok_get(X, key, &pr);
+        double d = 0.0, mg = 0.0;
+        if (pr) {
+            int64_t row = (int64_t)dok_get(K, proj_pack(X, mode, c), NULL);
+            for (int32_t r = 0; r < R; ++r) {
+                double t = gY[row * R + r] * U[c[mode] * R + r];
+                d += t;
+                mg += fabs(t);
+            }
+        }
+        dX[p] = d;
+        dXmag[p] = mg;
+    }
+    int64_t nl = X->dims[mode];
+    memset(dU, 0, sizeof(double) * nl * R);
+    memset(dUmag, 0, sizeof(double) * nl * R);
+    for (int64_t s = 0; s < X->cap; ++s) {
+        if (X->key[s] == -1) continue;
+        unpackn(X, X->key[s], c);
+        int64_t row = (int64_t)dok_get(K, proj_pack(X, mode, c), NULL);
+        for (int32_t r = 0; r < R; ++r) {
+            double t = X->val[s] * gY[row * R + r];
+            dU[c[mode] * R + r] += t;
+            dUmag[c[mode] * R + r] += fabs(t);
         }
     }
     orc_dok_free(K);
@@ -957,12 +1132,15 @@ void orc_cpn_grad(const orc_dok *X, const double *const *F, int64_t R, int mode,
     int64_t rows = sel ? nsel : rows_all;
     memset(out, 0, sizeof(double) * rows * R);
     memset(outmag, 0, sizeof(double) * rows * R);
+#pragma omp parallel
+    {
+    const int nt = orc_nthr(), me = orc_tid();
     int64_t c[ORC_MAX_ORDER];
     for (int64_t s = 0; s < X->cap; ++s) {
         if (X->key[s] == -1) continue;
         unpackn(X, X->key[s], c);
         int64_t o = map[c[mode]];
-        if (o < 0) continue;
+        if (o < 0 || o % nt != me) continue;
         double rm, r = cpn_resid(X, F, R, c, X->val[s], &rm);
         for (int64_t t = 0; t < R; ++t) {
             double h = 1.0;
@@ -971,6 +1149,7 @@ void orc_cpn_grad(const orc_dok *X, const double *const *F, int64_t R, int mode,
             out[o * R + t] += -r * h;
             outmag[o * R + t] += rm * fabs(h);
         }
+    }
     }
     free(map);
 }

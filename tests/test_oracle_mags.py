@@ -305,3 +305,30 @@ def test_spmm_jvp_mags(orc):
     C2, Cm2, dC2, dCm2 = orc.spmm_jvp(Ap, dAp, np.abs(B), np.abs(dB), k)
     _close(Cm2, C2)
     _close(dCm2, dC2)
+
+
+@pytest.mark.parametrize("mode", [0, 1, 3])
+def test_ttmn_mags(orc, mode):
+    rng = np.random.default_rng(120 + mode)
+    dims, R = (4, 3, 5, 4), 3
+    c = _keys(rng, dims, 80)
+    x = rng.standard_normal(80).astype(np.float32)
+    X = orc.Dok(dims, c, x)
+    Xd = _dense(dims, c, x)
+    U = rng.standard_normal((dims[mode], R))
+    others = [m for m in range(4) if m != mode]
+    letters = "abcd"
+    out = "".join(letters[m] for m in others) + "r"
+    yk, y, ym = orc.ttmn(X, mode, U, R)
+    Ymag = np.einsum(f"{letters},{letters[mode]}r->{out}", np.abs(Xd), np.abs(U))
+    _close(ym, Ymag[tuple(yk)])
+    _bounds(y, ym)
+    gY = rng.standard_normal((len(yk[0]), R))
+    Gd = np.zeros([dims[m] for m in others] + [R])
+    Gd[tuple(yk)] = gY
+    dX, dXm, dU, dUm = orc.ttmn_vjp(X, mode, U, R, gY, c)
+    Gat = Gd[tuple(c[m] for m in others)]  # upstream row of every stored key
+    _close(dXm, np.einsum("pr,pr->p", np.abs(Gat), np.abs(U[c[mode]])))
+    _close(dUm, np.einsum(f"{letters},{out}->{letters[mode]}r", np.abs(Xd), np.abs(Gd)))
+    _bounds(dX, dXm)
+    _bounds(dU, dUm)

@@ -579,3 +579,104 @@ def test_cpn_order3_equals_the_order3_oracle(orc):
     for n in range(3):
         assert np.allclose(orc.cpn_grad(X3, F, R, n)[0], orc.cp_grad(X3, *F, R, n)[0],
                            rtol=1e-13, atol=1e-13)
+
+
+# ----------------------------------------------------- threads by owner
+
+def test_owner_parallel_loops_are_bitwise_single_threaded(orc):
+    """The gradient loops split their outputs by owner across threads; each
+    output keeps its single-threaded order of terms, so any thread count
+    gives bitwise the single-threaded result."""
+    rng = np.random.default_rng(51)
+    nr, nc, k = 60, 45, 6
+    row, col, val = rand_coo(rng, nr, nc, 900)
+    A = orc.Dok((nr, nc), (row, col), val)
+    B, G = rng.standard_normal((nc, k)), rng.standard_normal((nr, k))
+    U, V = rng.standard_normal((nr, k)), rng.standard_normal((nc, k))
+    d, R = 12, 4
+    keys = rng.choice(d ** 3, size=500, replace=False)
+    i, j, l = (c.astype(np.int32) for c in np.unravel_index(keys, (d, d, d)))
+    x = rng.standard_normal(500).astype(np.float32)
+    X = orc.Dok((d, d, d), (i, j, l), x)
+    F = [rng.standard_normal((d, R)) for _ in range(3)]
+
+    def run():
+        out = [orc.spmm(A, B, k), orc.spmm_t(A, G, k, alpha=0.5),
+               orc.sddmm(A, G, B, k, row, col), orc.mf_grad(A, U, V, k, 0),
+               orc.mf_grad(A, U, V, k, 1), orc.loss_bilinear(A, G, B, k)]
+        out += [orc.cp_grad(X, *F, R, m) for m in range(3)]
+        out += [orc.cpn_grad(X, F, R, m) for m in range(3)]
+        return out
+
+    try:
+        orc.set_threads(1)
+        one = run()
+        orc.set_threads(5)
+        many = run()
+    finally:
+        orc.set_threads(1)
+    for a, b in zip(one, many):
+        for x1, x2 in zip(a, b):
+            assert np.array_equal(np.asarray(x1), np.asarray(x2))
+
+
+# ------------------------------------------- mode products of any order
+
+@pytest.mark.parametrize("dims", [(5, 4, 6), (3, 4, 2, 5), (3, 2, 4, 2, 3)])
+def test_ttmn_matches_autograd_in_every_mode(orc, dims):
+    """Y = X x_n U on the projected keys and its VJP, every mode of orders
+    3 to 5: PyTorch fp64 autograd of the dense einsum, the upstream placed on
+    the projected keys; the keys are the distinct projections in
+    lexicographic order."""
+    N, R = len(dims), 3
+    rng = np.random.default_rng(sum(dims) + N)
+    size = int(np.prod(dims))
+    keys = rng.choice(size, size=size // 3, replace=False)
+    coords = [c.astype(np.int32) for c in np.unravel_index(keys, dims)]
+    x = rng.standard_normal(len(keys)).astype(np.float32)
+    X = orc.Dok(dims, coords, x)
+    letters = "abcdef"[:N]
+    for n in range(N):
+        U = rng.standard_normal((dims[n], R))
+        yk, y, ym = orc.ttmn(X, n, U, R)
+        others = [m for m in range(N) if m != n]
+        proj = np.unique(np.ravel_multi_index([coords[m] for m in others],
+                                              [dims[m] for m in others]))
+        want = np.unravel_index(proj, [dims[m] for m in others])
+        for o in range(N - 1):
+            assert np.array_equal(yk[o], want[o])
+        Xd = torch.zeros(dims, dtype=torch.float64)
+        Xd[tuple(torch.from_numpy(c.astype(np.int64)) for c in coords)] = \
+            torch.tensor(x.astype(np.float64))
+        Xd.requires_grad_(True)
+        Ut = torch.tensor(U, requires_grad=True)
+        out = "".join(letters[m] for m in others) + "r"
+        Yd = torch.einsum(f"{letters},{letters[n]}r->{out}", Xd, Ut)
+        idx = tuple(torch.from_numpy(k.astype(np.int64)) for k in yk)
+        np.testing.assert_allclose(y, Yd.detach().numpy()[idx], rtol=1e-12, atol=1e-12)
+        assert np.all(ym >= np.abs(y) - 1e-12)
+        gy = rng.standard_normal((len(yk[0]), R))
+        Gd = torch.zeros(Yd.shape, dtype=torch.float64)
+        Gd[idx] = torch.tensor(gy)
+        (Yd * Gd).sum().backward()
+        dX, _, dU, _ = orc.ttmn_vjp(X, n, U, R, gy, coords)
+        cidx = tuple(torch.from_numpy(c.astype(np.int64)) for c in coords)
+        np.testing.assert_allclose(dX, Xd.grad.numpy()[tuple(c.numpy() for c in cidx)],
+                                   rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(dU, Ut.grad.numpy(), rtol=1e-12, atol=1e-12)
+
+
+def test_ttmn_last_mode_of_order3_is_ttm_and_ttv(orc):
+    rng = np.random.default_rng(77)
+    dims, R = (6, 5, 7), 4
+    keys = rng.choice(210, size=90, replace=False)
+    i, j, l = (c.astype(np.int32) for c in np.unravel_index(keys, dims))
+    x = rng.standard_normal(90).astype(np.float32)
+    X = orc.Dok(dims, (i, j, l), x)
+    U = rng.standard_normal((dims[2], R))
+    yk, y, ym = orc.ttmn(X, 2, U, R)
+    yi, yj, y3, ym3 = orc.ttm(X, U, R)
+    assert np.array_equal(yk[0], yi) and np.array_equal(yk[1], yj)
+    assert np.array_equal(y, y3) and np.array_equal(ym, ym3)
+    _, _, yv, _ = orc.ttv(X, U[:, 0])
+    np.testing.assert_allclose(orc.ttmn(X, 2, U[:, :1], 1)[1][:, 0], yv, rtol=1e-14, atol=1e-15)
