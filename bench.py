@@ -2,11 +2,14 @@
 """Benchmark of the sparse-gradient hot path on one MI355X.
 
 A step is one pass of the whole path over one batch of inputs already
-resident in HBM.  The default workload is the SpMM gradient (CSR A 100,000 x
-100,000 with 1M power-law nnz, B 100,000 x 64): forward C = A B, the SDDMM
-gradient dA on A's pattern with the loss 1/2 ||C||^2, and dB = A^T C, through
-nsd_loss_frob_spmm.  --workload selects the other paths (gnn: bilinear GNN
-layer; mf: sparse factorisation; cp: CP decomposition; spmv: SMVM).
+resident in HBM.  The default workload is the largest one, the GNN-layer
+gradient (CSR adjacency of a 2.4M-node power-law graph with 60M weighted
+edges, node features H and upstream G of 2.4M x 256): the loss
+L = sum((A H) o G), the SDDMM gradient dA = <G_i, H_j> on A's pattern and
+dH = A^T G, through nsd_loss_bilinear.  --workload selects the others (spmm:
+the SpMM gradient 1/2 ||A B||^2; mf: sparse factorisation; cp: CP
+decomposition; spmv: SMVM; and the pattern builders, the BATAX Jacobian, the
+SpMM tangent and the order-4 CP).
 Pattern-only preprocessing (row expansion, CSR -> CSC, work plans, mode
 indexes) is timed separately and is not part of a step.
 
@@ -52,7 +55,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="spmm", choices=list(WORKLOAD_NAMES))
+    ap.add_argument("--workload", default="gnn", choices=list(WORKLOAD_NAMES))
     ap.add_argument("--size", default="full")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cold-steps", type=int, default=10,
@@ -473,10 +476,16 @@ def main():
 
     algo = S.kernels[dom]
     achieved = algo / (dom_ms * 1e-3) / 1e9
+    traffic = committed_traffic(dom, args.workload)
     roofline = {
         "bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
         "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-        "traffic": committed_traffic(dom, args.workload),
+        "traffic": traffic,
+        # the counters' bytes (FETCH_SIZE + WRITE_SIZE, scaled by a plain
+        # copy) over the same average launch duration
+        "traffic_GBps": None if traffic is None else round(traffic / (dom_ms * 1e-3) / 1e9, 1),
+        "traffic_frac": None if traffic is None else
+        round(traffic / (dom_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "algo_bytes_per_launch": int(algo), "avg_launch_ms": round(dom_ms, 5),
         "launches_timed": dom_launches,
     }
@@ -690,11 +699,25 @@ def _sample(args, d):
 
 
 def cpu_baseline(args, d):
-    """The fp64 oracle, unchanged, single-threaded, on a bounded sample of the
-    workload: whole passes (DOK build + every output) repeated for about
-    cpu_seconds."""
+    """The fp64 oracle, unchanged, on a bounded sample of the workload, on
+    every host CPU visible to the process (its gradient loops split their
+    outputs by owner, its loss scans by fixed chunks) and on one thread (the
+    paper's own protocol): whole passes (DOK build + every output) repeated
+    for about cpu_seconds each."""
     import oracle
-    oracle.set_threads(1)
+    ncpu = len(os.sched_getaffinity(0))
+    try:
+        oracle.set_threads(ncpu)
+        leg = _cpu_leg(args, d, ncpu)
+        oracle.set_threads(1)
+        leg["single_thread"] = _cpu_leg(args, d, 1)
+    finally:
+        oracle.set_threads(1)
+    return leg
+
+
+def _cpu_leg(args, d, threads):
+    import oracle
     s, what = _sample(args, d)
     w = args.workload
 
@@ -767,6 +790,8 @@ def cpu_baseline(args, d):
             for m in range(3):
                 oracle.cp_grad(D, *F, s["rank"], m)
 
+    one_pass()  # warm-up pass, untimed (first touch of the host arrays)
+    dok_s[0] = 0.0
     passes, t0 = 0, time.perf_counter()
     while True:
         one_pass()
@@ -780,9 +805,10 @@ def cpu_baseline(args, d):
                 w, "DOK build + loss + all gradients")
     if w == "batax":
         nnz = one_pass.nk  # the metric counts the Jacobian's keys
+    on = "one thread" if threads == 1 else f"{threads} threads"
     return {"value": round(nnz * passes / el, 1), "unit": "entries/s" if w == "build" else "nnz/s",
-            "cores": 1, "kind": "oracle",
-            "sample": f"{what}: {passes} pass(es) of {done}, {el:.1f} s on one thread",
+            "cores": threads, "kind": "oracle",
+            "sample": f"{what}: {passes} pass(es) of {done}, {el:.1f} s on {on}",
             "dok_build_s": round(dok_s[0], 3), "compute_s": round(el - dok_s[0], 3),
             "host_cpus_visible": len(os.sched_getaffinity(0)), "cpu_model": cpu_model()}
 
