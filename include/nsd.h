@@ -83,7 +83,9 @@ typedef enum nsd_dup_policy { NSD_DUP_SUM = 0, NSD_DUP_ERROR = 1 } nsd_dup_polic
  * It balances power-law segment lengths without atomics.  A long segment with
  * more than 64 chunks is "huge" (listed in huge_idx): the combine gives a whole
  * workgroup to each that still has more than 64 partial rows once the chunks
- * computed by one wave have been added together.
+ * computed by one wave have been added together.  Chunk partials are kept in
+ * a compact array with one row per chunk item (chunk_ord), so the scratch of
+ * a reduction grows with the entries of long segments only.
  */
 typedef struct nsd_plan {
     int32_t item_len;          /* L: entries per chunk; segments above
@@ -94,6 +96,8 @@ typedef struct nsd_plan {
     const int32_t *long_first; /* [nlong] first item of every long segment */
     const int32_t *huge_idx;   /* [nhuge] positions in the long lists of huge segments */
     const int32_t *chunk_item; /* [nchunks] every item that is a chunk of a long segment */
+    const int32_t *chunk_ord;  /* [nitems] position of a chunk item in chunk_item (the
+                                  row of its partial sum), -1 for other items */
     const int32_t *empty_seg;  /* [nempty] segments without entries */
     int32_t longest_chunks;    /* chunks of the longest segment (0: none is long) */
 } nsd_plan;
@@ -145,23 +149,33 @@ typedef struct nsd_coo3 {
     nsd_coo3_mode mode[3];
 } nsd_coo3;
 
+/* Highest tensor order of the order-N entry points. */
+#define NSD_MAX_ORDER 6
+
 /*
- * Tensor-times-vector along the third mode of a sparse 3-tensor X (see
- * nsd_ttv): X's entries in (i, j) order with the distinct projected keys
- * numbered, and in l order, each view with its work plan.  Built by
- * nsd_ttv_build; the two plans by nsd_plan_build on yptr and lptr.
+ * Projection of a sparse order-N tensor X (3 <= N <= NSD_MAX_ORDER) along
+ * one mode n, the layout of its mode-n products (nsd_ttv, nsd_ttm): X's
+ * entries in lexicographic order of their other coordinates with the
+ * distinct projected keys numbered (the keys of Y = X x_n U), and X's
+ * entries in mode-n order, each view with its work plan.  Built by
+ * nsd_ttv_build; the two plans by nsd_plan_build on yptr and lptr.  "l"
+ * below is the mode-n coordinate.
  */
 typedef struct nsd_ttv_plan {
-    int32_t dims[3];
-    int32_t nnz, ny;       /* entries of X; distinct (i, j) keys of Y */
-    const int32_t *yi;     /* [ny] key rows, (i, j) order */
-    const int32_t *yj;     /* [ny] key columns */
-    const int32_t *yptr;   /* [ny+1] entries of every key in the (i, j)-sorted order */
-    const int32_t *yseg;   /* [nnz] key of every (i, j)-sorted entry */
-    const int32_t *yperm;  /* [nnz] input position of every (i, j)-sorted entry */
-    const int32_t *ykidx;  /* [nnz] l of every (i, j)-sorted entry */
+    int32_t order;         /* N */
+    int32_t mode;          /* n, the contracted mode */
+    int32_t dims[NSD_MAX_ORDER];
+    int32_t nnz, ny;       /* entries of X; distinct projected keys of Y */
+    const int32_t *ykey[NSD_MAX_ORDER - 1];  /* [ny] coordinate of every key in
+                                                each other mode (modes in
+                                                increasing order), keys in
+                                                lexicographic order */
+    const int32_t *yptr;   /* [ny+1] entries of every key in the key-sorted order */
+    const int32_t *yseg;   /* [nnz] key of every key-sorted entry */
+    const int32_t *yperm;  /* [nnz] input position of every key-sorted entry */
+    const int32_t *ykidx;  /* [nnz] l of every key-sorted entry */
     nsd_plan yplan;        /* plan over the keys */
-    const int32_t *lptr;   /* [dims[2]+1] entries of every l in the l-sorted order */
+    const int32_t *lptr;   /* [dims[mode]+1] entries of every l in the l-sorted order */
     const int32_t *lseg;   /* [nnz] l of every l-sorted entry, non-decreasing */
     const int32_t *lperm;  /* [nnz] input position of every l-sorted entry */
     const int32_t *lpair;  /* [nnz] key of every l-sorted entry */
@@ -232,7 +246,8 @@ nsd_status nsd_build_workspace_size(int32_t n, int32_t max_key, size_t *bytes);
 nsd_status nsd_plan_item_len(int32_t nnz, int32_t k, int32_t *item_len);
 
 /* Array sizes for nsd_plan_build: item_ptr needs *max_items + 1 entries,
- * long_seg, long_first and huge_idx *max_long each, chunk_item *max_chunks,
+ * chunk_ord *max_items, long_seg, long_first and huge_idx *max_long each,
+ * chunk_item *max_chunks,
  * empty_seg nseg; *ws_bytes of workspace.  Host outputs.
  * NSD_ERR_TOO_LARGE when 2 nnz + nseg >= 2^31. */
 nsd_status nsd_plan_bounds(int32_t nseg, int32_t nnz, int32_t item_len, int32_t *max_items,
@@ -245,8 +260,9 @@ nsd_status nsd_plan_bounds(int32_t nseg, int32_t nnz, int32_t item_len, int32_t 
  */
 nsd_status nsd_plan_build(int32_t nseg, int32_t nnz, const int32_t *segptr, int32_t item_len,
                           int32_t *item_ptr, int32_t *long_seg, int32_t *long_first,
-                          int32_t *huge_idx, int32_t *chunk_item, int32_t *empty_seg,
-                          nsd_plan *plan, void *ws, size_t ws_bytes, void *stream);
+                          int32_t *huge_idx, int32_t *chunk_item, int32_t *chunk_ord,
+                          int32_t *empty_seg, nsd_plan *plan, void *ws, size_t ws_bytes,
+                          void *stream);
 
 /* rowidx[p] = the row r with rowptr[r] <= p < rowptr[r+1].  Async. */
 nsd_status nsd_csr_expand_rows(int32_t nrows, int32_t nnz, const int32_t *rowptr,
@@ -420,8 +436,11 @@ nsd_status nsd_loss_bilinear(const nsd_csr *A, const nsd_csc *At, const float *H
  * A's CSR gives the row pass (values A->val), its CSC the column pass with
  * the values in CSC order valT [nnz] (nsd_gather_f32 of A->val by At->perm,
  * made once when A is data; NULL: read A->val through At->perm each call).
- * U, dU [nrows x k]; V, dV [ncols x k].  k <= 256 (multiple of 4, 16-byte
- * aligned rows), otherwise k <= 64; larger k gives NSD_ERR_UNSUPPORTED.  Async.
+ * U, dU [nrows x k]; V, dV [ncols x k].  Any k >= 1: up to 256 (multiple of
+ * 4, 16-byte aligned rows) or up to 64 otherwise, both passes run fused in
+ * one launch; a wider k forms r once per stored entry in the workspace (its
+ * size query counts nnz floats for every k > 64) and runs the two
+ * gather-reduces with r as weights.  Async.
  */
 nsd_status nsd_loss_mf(const nsd_csr *A, const nsd_csc *At, const float *valT, const float *U,
                        const float *V, int32_t k, float seed, double *loss, float *dU, float *dV,
@@ -441,35 +460,48 @@ nsd_status nsd_cp_workspace_size(const nsd_coo3 *X, int32_t rank, size_t *bytes)
  *   dX [nnz] = seed * R, aligned with X's input order (X->mode[n].perm)
  *   dF1[i,:] = -seed sum R_ijl (F2[j,:] o F3[l,:]), cyclically dF2, dF3
  *   (the negated mode-n MTTKRPs of R).
- * rank <= 256 (multiple of 4, 16-byte aligned rows), otherwise <= 64.  Async.
+ * Any rank >= 1: up to 256 (multiple of 4, 16-byte aligned rows) or up to 64
+ * otherwise, the three mode passes run fused in one launch; a wider rank
+ * forms R once in the workspace (counted by nsd_cp_workspace_size for every
+ * rank > 64) and runs one gather-reduce per mode with R as weights.  Async.
  */
 nsd_status nsd_loss_cp(const nsd_coo3 *X, const float *F1, const float *F2, const float *F3,
                        int32_t rank, float seed, double *loss, float *dX, float *dF1,
                        float *dF2, float *dF3, void *ws, size_t ws_bytes, void *stream);
 
-/* Bytes of workspace nsd_ttv_build needs; dims is a host array of 3. */
-nsd_status nsd_ttv_build_workspace_size(int32_t nnz, const int32_t *dims, size_t *bytes);
+/* Bytes of workspace nsd_ttv_build needs; dims is a host array of `order`. */
+nsd_status nsd_ttv_build_workspace_size(int32_t order, const int32_t *dims, int32_t nnz,
+                                        size_t *bytes);
 
 /*
- * Projection of a COO 3-tensor (coordinates i, j, l [nnz], dims host[3]) onto
- * its (i, j) keys: stable sort by (i, j), distinct keys numbered in (i, j)
- * order (yi, yj [<= nnz]; yptr [nnz+1]), and the l-sorted view (lptr
- * [dims[2]+1]).  *ny (host) = number of distinct keys.  Arrays yseg, yperm,
- * ykidx, lseg, lperm, lpair are [nnz].  Bit-exact.  Synchronous.
+ * Projection of an order-N COO tensor along mode n (3 <= N <= NSD_MAX_ORDER,
+ * 0 <= n < N): coords is a HOST array of N device pointers to [nnz] int32
+ * coordinates (input order), dims a host array of N sizes.  The entries are
+ * stably sorted by their other coordinates in lexicographic order (mode 0
+ * most significant, ties in input order) and the distinct projected keys
+ * numbered in that order: ykey is a HOST array of N - 1 device pointers
+ * (capacity nnz each) receiving the keys' coordinates in the other modes,
+ * yptr [nnz+1] their entry ranges; yseg, yperm, ykidx [nnz] as in
+ * nsd_ttv_plan.  The mode-n view: lptr [dims[n]+1], lseg, lperm, lpair
+ * [nnz] (stable by the mode-n coordinate).  *ny (host) = number of keys.
+ * Coordinates out of range give NSD_ERR_BAD_FORMAT.  Bit-exact.
+ * Synchronous.
  */
-nsd_status nsd_ttv_build(int32_t nnz, const int32_t *dims, const int32_t *i, const int32_t *j,
-                         const int32_t *l, int32_t *yi, int32_t *yj, int32_t *yptr,
-                         int32_t *yseg, int32_t *yperm, int32_t *ykidx, int32_t *lptr,
-                         int32_t *lseg, int32_t *lperm, int32_t *lpair, int32_t *ny,
-                         void *ws, size_t ws_bytes, void *stream);
+nsd_status nsd_ttv_build(int32_t order, const int32_t *dims, int32_t nnz,
+                         const int32_t *const *coords, int32_t mode, int32_t *const *ykey,
+                         int32_t *yptr, int32_t *yseg, int32_t *yperm, int32_t *ykidx,
+                         int32_t *lptr, int32_t *lseg, int32_t *lperm, int32_t *lpair,
+                         int32_t *ny, void *ws, size_t ws_bytes, void *stream);
 
 /* Bytes of `ws` for nsd_ttv and nsd_ttv_vjp.  Writes *bytes (host). */
 nsd_status nsd_ttv_workspace_size(const nsd_ttv_plan *T, size_t *bytes);
 
 /*
- * y[s] = sum over stored (i, j, l) with key s = (yi[s], yj[s]) of x * v(l):
- * Y = X x_3 v on the projected keys.  x [nnz] in X's input order, v
- * [dims[2]], y [ny].  Async.
+ * Tensor-times-vector along the plan's mode n: y[s] = sum over the stored
+ * entries whose other coordinates form key s of x * v(l), Y = X x_n v on the
+ * projected keys (a sum over X's keys inserting singletons with "+=",
+ * Section 3 and Section 5.5).  x [nnz] in X's input order, v [dims[n]],
+ * y [ny].  Async.
  */
 nsd_status nsd_ttv(const nsd_ttv_plan *T, const float *x, const float *v, float *y, void *ws,
                    size_t ws_bytes, void *stream);
@@ -477,7 +509,8 @@ nsd_status nsd_ttv(const nsd_ttv_plan *T, const float *x, const float *v, float 
 /*
  * Vector-Jacobian product of nsd_ttv for the upstream gy [ny]:
  * dx[p] = gy[key(p)] * v(l_p) on X's keys (input order, [nnz]);
- * dv(l) = sum over stored (i, j, l) of x * gy[key]  (dv [dims[2]]).  Async.
+ * dv(l) = sum over the stored entries with mode-n coordinate l of
+ * x * gy[key]  (dv [dims[n]]).  Async.
  */
 nsd_status nsd_ttv_vjp(const nsd_ttv_plan *T, const float *x, const float *v, const float *gy,
                        float *dx, float *dv, void *ws, size_t ws_bytes, void *stream);
@@ -487,11 +520,12 @@ nsd_status nsd_ttv_vjp(const nsd_ttv_plan *T, const float *x, const float *v, co
 nsd_status nsd_ttm_workspace_size(const nsd_ttv_plan *T, int32_t R, size_t *bytes);
 
 /*
- * Tensor-times-matrix along the third mode, the matrix form of nsd_ttv (an
- * n-mode product of Section 3's tensor algebra, kept sparse on the projected
- * keys): Y[s, :] = sum over stored (i, j, l) with key s = (yi[s], yj[s]) of
- * x * U[l, :].  x [nnz] in X's input order, U row-major [dims[2] x R], Y
- * row-major [ny x R], every row written.  T is X's TTV plan.  Async.
+ * Tensor-times-matrix along the plan's mode n, the matrix form of nsd_ttv
+ * (the n-mode product of Section 3's tensor algebra, kept sparse on the
+ * projected keys): Y[s, :] = sum over the stored entries of key s of
+ * x * U[l, :].  x [nnz] in X's input order, U row-major [dims[n] x R], Y
+ * row-major [ny x R], every row written.  T is X's projection along n.
+ * Async.
  */
 nsd_status nsd_ttm(const nsd_ttv_plan *T, const float *x, const float *U, int32_t R, float *Y,
                    void *ws, size_t ws_bytes, void *stream);
@@ -499,8 +533,8 @@ nsd_status nsd_ttm(const nsd_ttv_plan *T, const float *x, const float *U, int32_
 /*
  * Vector-Jacobian product of nsd_ttm for the upstream gY row-major [ny x R]:
  * dx[p] = <gY[key(p), :], U[l_p, :]> on X's keys (input order, [nnz]);
- * dU[l, :] = sum over stored (i, j, l) of x * gY[key, :]  (dU [dims[2] x R],
- * every row written).  Async.
+ * dU[l, :] = sum over the stored entries with mode-n coordinate l of
+ * x * gY[key, :]  (dU [dims[n] x R], every row written).  Async.
  */
 nsd_status nsd_ttm_vjp(const nsd_ttv_plan *T, const float *x, const float *U, int32_t R,
                        const float *gY, float *dx, float *dU, void *ws, size_t ws_bytes,
@@ -548,8 +582,6 @@ nsd_status nsd_diag_keys(const nsd_csr *A, float alpha, float *out, void *stream
  * every entry in that order (o = 0 .. order - 2), val in that order, perm =
  * input position of every slot, and the slices' work plan.
  */
-#define NSD_MAX_ORDER 6
-
 typedef struct nsd_coon_mode {
     int32_t mode;
     const int32_t *segptr;                  /* [dims[mode] + 1] */
@@ -576,9 +608,10 @@ nsd_status nsd_cpn_workspace_size(const nsd_coon *X, int32_t rank, size_t *bytes
  *   dX = seed * R on X's keys (X's input order, [nnz]),
  *   dF_n(c_n, :) = -seed sum R * (o_{m != n} F_m(c_m, :))  (negated MTTKRPs).
  * F and dF are HOST arrays of `order` device pointers to [dims[n] x rank]
- * row-major factors.  *loss (device fp64) is not scaled by seed.  rank <= 256
- * (multiple of 4, 16-byte aligned rows) or <= 64 otherwise, else
- * NSD_ERR_UNSUPPORTED.  Async.
+ * row-major factors.  *loss (device fp64) is not scaled by seed.  Any
+ * rank >= 1; ranks above 256 (above 64 without 16-byte aligned rows of a
+ * multiple of 4) form R once in the workspace and run one gather-reduce per
+ * mode.  Async.
  */
 nsd_status nsd_loss_cpn(const nsd_coon *X, const float *const *F, int32_t rank, float seed,
                         double *loss, float *dX, float *const *dF, void *ws, size_t ws_bytes,

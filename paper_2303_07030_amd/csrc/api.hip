@@ -5,6 +5,7 @@
 
 #include "nsd_internal.hpp"
 #include "segreduce.hpp"
+#include "wide.hpp"
 
 namespace nsd {
 
@@ -67,9 +68,17 @@ static size_t loss_part_count(const nsd_csr *A, const nsd_csc *At, int k) {
     return (size_t)m;
 }
 
+// Widths that a fused factorisation pass may not hold (above 64 columns
+// without float4 rows, above 256 with them) form the residual once, one
+// float per stored entry.
+static size_t resid_buf_bytes(const nsd_csr *A, int k) {
+    return k > 64 ? round256((size_t)std::max(A->nnz, 1) * sizeof(float)) : 0;
+}
+
 static size_t compute_ws_bytes(const nsd_csr *A, const nsd_csc *At, int k) {
     return part_region_bytes(A, At, k) + round256(loss_part_count(A, At, k) * sizeof(double)) +
-           round256(std::max<size_t>(A->plan.nlong, 1) * sizeof(double));
+           round256(std::max<size_t>(A->plan.nlong, 1) * sizeof(double)) +
+           resid_buf_bytes(A, k);
 }
 
 struct ComputeWs {
@@ -77,6 +86,7 @@ struct ComputeWs {
     float *part_col;  // column-plan partials for passes sharing a launch
     double *loss_part;
     double *seg_loss;
+    float *rbuf;      // residual per stored entry (wide factorisation only)
 };
 
 static nsd_status carve_compute(void *ws, size_t ws_bytes, const nsd_csr *A, const nsd_csc *At,
@@ -91,6 +101,8 @@ static nsd_status carve_compute(void *ws, size_t ws_bytes, const nsd_csr *A, con
     out->loss_part = reinterpret_cast<double *>(b);
     b += round256(loss_part_count(A, At, k) * sizeof(double));
     out->seg_loss = reinterpret_cast<double *>(b);
+    b += round256(std::max<size_t>(A->plan.nlong, 1) * sizeof(double));
+    out->rbuf = resid_buf_bytes(A, k) ? reinterpret_cast<float *>(b) : nullptr;
     return NSD_OK;
 }
 
@@ -176,6 +188,44 @@ static bool col_dual_ok(const DualPass &pass) {
     DualParams f;
     f.pass[0] = pass;
     return dual_supported(pass.s.k, dual_vec_ok(f));
+}
+
+static nsd_status check_bilinear(const nsd_csr *A, const nsd_csc *At, const float *H,
+                                 const float *G, int k, const double *loss, const float *dA,
+                                 const float *dH) {
+    NSD_TRY(check_csr(A, true, false));
+    NSD_TRY(check_csc(At, A));
+    NSD_REQUIRE(k >= 1, "k = %d < 1", k);
+    NSD_REQUIRE(loss != nullptr, "loss is NULL");
+    NSD_REQUIRE(A->ncols == 0 || dH != nullptr, "dH is NULL");
+    NSD_REQUIRE(A->nnz == 0 || (H && G && dA), "H/G/dA is NULL");
+    return NSD_OK;
+}
+
+// The loss total of an unfused SDDMM's block partials; with nnz == 0 the
+// loss is 0.
+static nsd_status finish_loss(const SddmmParams &p, double *loss, hipStream_t st);
+
+// The bilinear layer L = sum (A H) o G with its gradients, given the chunk
+// partials of the column plan and the loss partials.
+static nsd_status bilinear_run(const nsd_csr *A, const nsd_csc *At, const float *H,
+                               const float *G, int k, float seed, double *loss, float *dA,
+                               float *dH, float *part_col, double *loss_part, hipStream_t st) {
+    if (A->nnz > 0) {
+        // one pass over the columns: own row H_j, gathered row G_i:
+        // dA[p] = seed <G_i, H_j>, loss = sum_p A_p <G_i, H_j>, dH = seed A^T G
+        const DualPass pass = col_dual(A, At, G, H, k, seed, dH, part_col, dA, seed, true);
+        if (col_dual_ok(pass)) return col_dual_loss(pass, loss_part, loss, st);
+    }
+    // dA = seed * <G_i, H_j>; loss = sum_p A_p <G_i, H_j>
+    SddmmParams sp = sddmm_params(A, G, H, k, seed, dA);
+    sp.w = A->val;
+    sp.beta = 1.0;
+    sp.part = loss_part;
+    NSD_TRY(sddmm(sp, st));
+    NSD_TRY(finish_loss(sp, loss, st));
+    // dH = seed * A^T G
+    return segreduce(cols_params(A, At, G, k, seed, dH, part_col), st);
 }
 
 // The loss partial count of a fused SDDMM; with nnz == 0 the loss is 0.
@@ -307,30 +357,11 @@ nsd_status nsd_loss_frob_spmm(const nsd_csr *A, const nsd_csc *At, const float *
 nsd_status nsd_loss_bilinear(const nsd_csr *A, const nsd_csc *At, const float *H,
                              const float *G, int32_t k, float seed, double *loss, float *dA,
                              float *dH, void *ws, size_t ws_bytes, void *stream) {
-    NSD_TRY(check_csr(A, true, false));
-    NSD_TRY(check_csc(At, A));
-    NSD_REQUIRE(k >= 1, "k = %d < 1", k);
-    NSD_REQUIRE(loss != nullptr, "loss is NULL");
-    NSD_REQUIRE(A->ncols == 0 || dH != nullptr, "dH is NULL");
-    NSD_REQUIRE(A->nnz == 0 || (H && G && dA), "H/G/dA is NULL");
+    NSD_TRY(check_bilinear(A, At, H, G, k, loss, dA, dH));
     ComputeWs w;
     NSD_TRY(carve_compute(ws, ws_bytes, A, At, k, &w));
-    hipStream_t st = as_stream(stream);
-    if (A->nnz > 0) {
-        // one pass over the columns: own row H_j, gathered row G_i:
-        // dA[p] = seed <G_i, H_j>, loss = sum_p A_p <G_i, H_j>, dH = seed A^T G
-        const DualPass pass = col_dual(A, At, G, H, k, seed, dH, w.part_col, dA, seed, true);
-        if (col_dual_ok(pass)) return col_dual_loss(pass, w.loss_part, loss, st);
-    }
-    // dA = seed * <G_i, H_j>; loss = sum_p A_p <G_i, H_j>
-    SddmmParams sp = sddmm_params(A, G, H, k, seed, dA);
-    sp.w = A->val;
-    sp.beta = 1.0;
-    sp.part = w.loss_part;
-    NSD_TRY(sddmm(sp, st));
-    NSD_TRY(finish_loss(sp, loss, st));
-    // dH = seed * A^T G
-    return segreduce(cols_params(A, At, G, k, seed, dH, w.part_col), st);
+    return bilinear_run(A, At, H, G, k, seed, loss, dA, dH, w.part_col, w.loss_part,
+                        as_stream(stream));
 }
 
 nsd_status nsd_spmm_vjp(const nsd_csr *A, const nsd_csc *At, const float *X, const float *G,
@@ -400,11 +431,32 @@ nsd_status nsd_loss_mf(const nsd_csr *A, const nsd_csc *At, const float *valT, c
     NSD_REQUIRE(A->ncols == 0 || dV != nullptr, "dV is NULL");
     NSD_REQUIRE(A->nnz == 0 || (U && V), "U/V is NULL");
     const bool vec = k % 4 == 0 && aligned16(U) && aligned16(V) && aligned16(dU) && aligned16(dV);
-    if (!dual_supported(k, vec))
-        return fail(NSD_ERR_UNSUPPORTED, "factor width k = %d (at most 256, multiple of 4 and "
-                                         "16-byte aligned rows; otherwise at most 64)", k);
     ComputeWs w;
     NSD_TRY(carve_compute(ws, ws_bytes, A, At, k, &w));
+    hipStream_t st = as_stream(stream);
+    if (!dual_supported(k, vec)) {
+        // wider than a fused slot: r_ij once (CSR order) with the loss,
+        // then dU over the rows and dV over the columns with r as weights
+        ResidParams r;
+        r.nnz = A->nnz;
+        r.k = k;
+        r.order = 2;
+        r.coord[0] = A->rowidx;
+        r.coord[1] = A->colind;
+        r.fac[0] = U;
+        r.fac[1] = V;
+        r.x = A->val;
+        r.rbuf = w.rbuf;
+        r.part = w.loss_part;
+        NSD_TRY(resid_pass(r, vec, st));
+        SgrParams rows = rows_params(A, V, k, -2.f * seed, dU, w.part);
+        rows.w = w.rbuf;
+        NSD_TRY(segreduce(rows, st));
+        SgrParams cols = cols_params(A, At, U, k, -2.f * seed, dV, w.part_col);
+        cols.w = w.rbuf;  // through At->perm
+        NSD_TRY(segreduce(cols, st));
+        return loss_finalize(w.loss_part, resid_blocks(A->nnz, k, vec), loss, st);
+    }
     // row pass: dU = -2 seed sum_j r_ij V_j with the loss; column pass:
     // dV = -2 seed sum_i r_ij U_i, r recomputed; both in one launch
     DualParams f;
@@ -419,7 +471,6 @@ nsd_status nsd_loss_mf(const nsd_csr *A, const nsd_csc *At, const float *valT, c
     }
     f.pass[1].own = V;
     f.loss_part = w.loss_part;
-    hipStream_t st = as_stream(stream);
     LossJob job;
     job.loss = loss;  // sums the dual kernel's own block partials
     return dual_fused(kDualMf, f, NSD_KERNEL_MF, job, st);
@@ -444,6 +495,8 @@ static nsd_status check_coo3(const nsd_coo3 *X) {
     return NSD_OK;
 }
 
+// Per-mode chunk partials, the loss partials, and (ranks above 64, which a
+// fused slot may not hold) the residual of every stored entry.
 static size_t cp_ws_bytes(const nsd_coo3 *X, int rank) {
     size_t b = 0;
     nsd_plan plans[3];
@@ -451,8 +504,72 @@ static size_t cp_ws_bytes(const nsd_coo3 *X, int rank) {
         b += round256(sgr_part_bytes(X->mode[n].plan, std::max(rank, 1)));
         plans[n] = X->mode[n].plan;
     }
-    const int64_t blocks = std::max(cp_blocks(plans, rank, true), cp_blocks(plans, rank, false));
-    return b + round256(std::max<int64_t>(blocks, 1) * sizeof(double));
+    int64_t blocks = std::max(cp_blocks(plans, rank, true), cp_blocks(plans, rank, false));
+    if (rank > 64)
+        blocks = std::max({blocks, resid_blocks(X->nnz, rank, true),
+                           resid_blocks(X->nnz, rank, false)});
+    b += round256(std::max<int64_t>(blocks, 1) * sizeof(double));
+    if (rank > 64) b += round256((size_t)std::max(X->nnz, 1) * sizeof(float));
+    return b;
+}
+
+// CP gradient of a rank wider than a fused slot: the residual once in mode
+// 0's order (written to dX and, unscaled, to a buffer in X's input order),
+// then one mode pass per mode reading it through the mode's permutation.
+static nsd_status cp_wide(const nsd_coo3 *X, const float *const *F, int rank, float seed,
+                          double *loss, float *dX, float *const *dF, bool vec, char *b,
+                          hipStream_t st) {
+    float *part[3];
+    for (int n = 0; n < 3; ++n) {
+        part[n] = reinterpret_cast<float *>(b);
+        b += round256(sgr_part_bytes(X->mode[n].plan, rank));
+    }
+    double *loss_part = reinterpret_cast<double *>(b);
+    nsd_plan plans[3] = {X->mode[0].plan, X->mode[1].plan, X->mode[2].plan};
+    const int64_t blocks = std::max({cp_blocks(plans, rank, true), cp_blocks(plans, rank, false),
+                                     resid_blocks(X->nnz, rank, true),
+                                     resid_blocks(X->nnz, rank, false)});
+    b += round256(std::max<int64_t>(blocks, 1) * sizeof(double));
+    float *rbuf = reinterpret_cast<float *>(b);
+    const nsd_coo3_mode &m0 = X->mode[0];
+    ResidParams r;
+    r.nnz = X->nnz;
+    r.k = rank;
+    r.order = 3;
+    r.coord[0] = m0.segidx;
+    r.coord[1] = m0.idx_a;
+    r.coord[2] = m0.idx_b;
+    for (int n = 0; n < 3; ++n) r.fac[n] = F[n];
+    r.x = m0.val;
+    r.perm = m0.perm;
+    r.rbuf = rbuf;
+    r.resid = dX;
+    r.seed = seed;
+    r.lscale = 0.5;
+    r.part = loss_part;
+    NSD_TRY(resid_pass(r, vec, st));
+    for (int n = 0; n < 3; ++n) {
+        const nsd_coo3_mode &md = X->mode[n];
+        MttkrpParams m;
+        m.s.nseg = X->dims[n];
+        m.s.nnz = X->nnz;
+        m.s.k = rank;
+        m.s.plan = md.plan;
+        m.s.segptr = md.segptr;
+        m.s.segidx = md.segidx;
+        m.s.idx = md.idx_a;
+        m.s.w = rbuf;
+        m.s.wperm = md.perm;
+        m.s.alpha = -seed;
+        m.s.out = dF[n];
+        m.s.part = part[n];
+        m.other[0] = md.idx_a;
+        m.other[1] = md.idx_b;
+        m.fac[0] = F[(n + 1) % 3];
+        m.fac[1] = F[(n + 2) % 3];
+        NSD_TRY(mttkrp_pass(m, 3, vec, st));
+    }
+    return loss_finalize(loss_part, resid_blocks(X->nnz, rank, vec), loss, st);
 }
 
 nsd_status nsd_cp_workspace_size(const nsd_coo3 *X, int32_t rank, size_t *bytes) {
@@ -478,13 +595,12 @@ nsd_status nsd_loss_cp(const nsd_coo3 *X, const float *F1, const float *F2, cons
     NSD_REQUIRE(X->nnz == 0 || dX != nullptr, "dX is NULL");
     bool vec = rank % 4 == 0;
     for (int n = 0; n < 3; ++n) vec = vec && aligned16(F[n]) && aligned16(dF[n]);
-    if (vec ? rank > 256 : rank > 64)
-        return fail(NSD_ERR_UNSUPPORTED, "rank %d (at most 256, multiple of 4 and 16-byte "
-                                         "aligned rows; otherwise at most 64)", rank);
     const size_t need = cp_ws_bytes(X, rank);
     if (ws == nullptr || ws_bytes < need)
         return fail(NSD_ERR_WORKSPACE, "workspace %zu bytes at %p, need %zu", ws_bytes, ws, need);
     char *b = static_cast<char *>(ws);
+    if (vec ? rank > 256 : rank > 64) return cp_wide(X, F, rank, seed, loss, dX, dF, vec, b,
+                                                     as_stream(stream));
     CpParams f;
     for (int n = 0; n < 3; ++n) {
         const nsd_coo3_mode &md = X->mode[n];

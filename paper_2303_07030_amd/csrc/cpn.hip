@@ -22,6 +22,7 @@
 #include "nsd_internal.hpp"
 #include "segreduce.hpp"
 #include "segreduce_dev.hpp"
+#include "wide.hpp"
 
 namespace nsd {
 
@@ -246,7 +247,8 @@ __device__ __forceinline__ void cpn_block(const CpnMode<N> &m, int b, bool first
         int pseg = -1;
         if (s < m.s.plan.nitems)
             pseg = cpn_walk<N, VEC, G, U>(m, s, lane, first_mode, lsum, pacc);
-        store_chunk_partial<VEC, G>(pseg, pacc, m.s.part, s, m.s.k, g * VEC, g * VEC < m.s.k);
+        store_chunk_partial<VEC, G>(pseg, pacc, m.s.part, m.s.plan.chunk_ord, s, m.s.k, g * VEC,
+                                    g * VEC < m.s.k);
     } else {
         zero_segment<VEC>(m.s, (int64_t)(b - m.item_blocks) * kSlots + threadIdx.x / G, g * VEC,
                           g * VEC < m.s.k);
@@ -324,11 +326,79 @@ static int64_t cpn_blocks(const nsd_coon *X, int rank, bool vec) {
 
 static size_t rnd256(size_t b) { return (b + 255) & ~size_t(255); }
 
+// Loss partials of either form (ranks above 64, which a fused slot may not
+// hold, form the residual once in its own pass).
+static int64_t cpn_loss_parts(const nsd_coon *X, int rank) {
+    int64_t blocks = std::max(cpn_blocks(X, rank, true), cpn_blocks(X, rank, false));
+    if (rank > 64)
+        blocks = std::max({blocks, resid_blocks(X->nnz, rank, true),
+                           resid_blocks(X->nnz, rank, false)});
+    return std::max<int64_t>(blocks, 1);
+}
+
+// Per-mode chunk partials, the loss partials and, for ranks above 64, the
+// residual of every stored entry.
 static size_t cpn_ws_bytes(const nsd_coon *X, int rank) {
     size_t b = 0;
     for (int n = 0; n < X->order; ++n) b += rnd256(sgr_part_bytes(X->mode[n].plan, rank));
-    const int64_t blocks = std::max(cpn_blocks(X, rank, true), cpn_blocks(X, rank, false));
-    return b + rnd256(std::max<int64_t>(blocks, 1) * sizeof(double));
+    b += rnd256(cpn_loss_parts(X, rank) * sizeof(double));
+    if (rank > 64) b += rnd256((size_t)std::max(X->nnz, 1) * sizeof(float));
+    return b;
+}
+
+// The gradient of a rank wider than a fused slot: the residual once in mode
+// 0's order (to dX and, unscaled, to a buffer in X's input order), then one
+// mode pass per mode reading it through the mode's permutation.
+static nsd_status cpn_wide(const nsd_coon *X, const float *const *F, int32_t rank, float seed,
+                           double *loss, float *dX, float *const *dF, bool vec, char *b,
+                           hipStream_t st) {
+    const int N = X->order;
+    float *part[NSD_MAX_ORDER];
+    for (int n = 0; n < N; ++n) {
+        part[n] = reinterpret_cast<float *>(b);
+        b += rnd256(sgr_part_bytes(X->mode[n].plan, rank));
+    }
+    double *loss_part = reinterpret_cast<double *>(b);
+    b += rnd256(cpn_loss_parts(X, rank) * sizeof(double));
+    float *rbuf = reinterpret_cast<float *>(b);
+    const nsd_coon_mode &m0 = X->mode[0];
+    ResidParams r;
+    r.nnz = X->nnz;
+    r.k = rank;
+    r.order = N;
+    r.coord[0] = m0.segidx;
+    for (int o = 0; o < N - 1; ++o) r.coord[o + 1] = m0.idx[o];  // mode o + 1
+    for (int n = 0; n < N; ++n) r.fac[n] = F[n];
+    r.x = m0.val;
+    r.perm = m0.perm;
+    r.rbuf = rbuf;
+    r.resid = dX;
+    r.seed = seed;
+    r.lscale = 0.5;
+    r.part = loss_part;
+    NSD_TRY(resid_pass(r, vec, st));
+    for (int n = 0; n < N; ++n) {
+        const nsd_coon_mode &md = X->mode[n];
+        MttkrpParams m;
+        m.s.nseg = X->dims[n];
+        m.s.nnz = X->nnz;
+        m.s.k = rank;
+        m.s.plan = md.plan;
+        m.s.segptr = md.segptr;
+        m.s.segidx = md.segidx;
+        m.s.idx = md.idx[0];
+        m.s.w = rbuf;
+        m.s.wperm = md.perm;
+        m.s.alpha = -seed;
+        m.s.out = dF[n];
+        m.s.part = part[n];
+        for (int o = 0; o < N - 1; ++o) {
+            m.other[o] = md.idx[o];
+            m.fac[o] = F[(n + 1 + o) % N];
+        }
+        NSD_TRY(mttkrp_pass(m, N, vec, st));
+    }
+    return loss_finalize(loss_part, resid_blocks(X->nnz, rank, vec), loss, st);
 }
 
 static nsd_status check_coon(const nsd_coon *X) {
@@ -415,14 +485,12 @@ nsd_status nsd_loss_cpn(const nsd_coon *X, const float *const *F, int32_t rank, 
         vec = vec && aligned16(F[n]) && aligned16(dF[n]);
     }
     NSD_REQUIRE(X->nnz == 0 || dX != nullptr, "dX is NULL");
-    if (vec ? rank > 256 : rank > 64)
-        return fail(NSD_ERR_UNSUPPORTED, "rank %d (at most 256, multiple of 4 and 16-byte "
-                                         "aligned rows; otherwise at most 64)", rank);
     const size_t need = cpn_ws_bytes(X, rank);
     if (ws == nullptr || ws_bytes < need)
         return fail(NSD_ERR_WORKSPACE, "workspace %zu bytes at %p, need %zu", ws_bytes, ws, need);
     char *b = static_cast<char *>(ws);
     hipStream_t st = as_stream(stream);
+    if (vec ? rank > 256 : rank > 64) return cpn_wide(X, F, rank, seed, loss, dX, dF, vec, b, st);
     switch (N) {
         case 3: return cpn_run<3>(X, F, rank, seed, loss, dX, dF, vec, b, st);
         case 4: return cpn_run<4>(X, F, rank, seed, loss, dX, dF, vec, b, st);

@@ -207,7 +207,8 @@ __device__ __forceinline__ void dual_block(const DualPass &m, int b, double &lsu
         pacc.zero();
         int pseg = -1;
         if (s < m.s.plan.nitems) pseg = dual_walk<KIND, VEC, G, U>(m, s, lane, lsum, pacc);
-        store_chunk_partial<VEC, G>(pseg, pacc, m.s.part, s, m.s.k, g * VEC, g * VEC < m.s.k);
+        store_chunk_partial<VEC, G>(pseg, pacc, m.s.part, m.s.plan.chunk_ord, s, m.s.k, g * VEC,
+                                    g * VEC < m.s.k);
     } else {
         zero_segment<VEC>(m.s, (int64_t)(b - m.item_blocks) * kSlots + threadIdx.x / G, g * VEC,
                           g * VEC < m.s.k);

@@ -119,8 +119,8 @@ __global__ __launch_bounds__(kBlock) void jvp_kernel(JvpParams f) {
             pd = st.dacc;
         }
     }
-    store_chunk_partial<VEC, G>(pseg, pc, f.c.part, s, f.c.k, col, on);
-    store_chunk_partial<VEC, G>(pseg, pd, f.d.part, s, f.c.k, col, on);
+    store_chunk_partial<VEC, G>(pseg, pc, f.c.part, f.c.plan.chunk_ord, s, f.c.k, col, on);
+    store_chunk_partial<VEC, G>(pseg, pd, f.d.part, f.c.plan.chunk_ord, s, f.c.k, col, on);
 }
 
 // Entries per batch (two rows are gathered per entry): four, measured on

@@ -87,7 +87,7 @@ struct PlanScans {
 __global__ void plan_fill_kernel(int32_t nseg, int32_t nnz, const int32_t *segptr, int32_t L,
                                  PlanScans sc, int32_t *item_ptr, int32_t *long_seg,
                                  int32_t *long_first, int32_t *huge_idx, int32_t *chunk_item,
-                                 int32_t *empty_seg) {
+                                 int32_t *chunk_ord, int32_t *empty_seg) {
     const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (r >= nseg) return;
     const int32_t *nitem = sc.nitem;
@@ -98,12 +98,16 @@ __global__ void plan_fill_kernel(int32_t nseg, int32_t nnz, const int32_t *segpt
         for (int32_t c = 0; c < nitem[r]; ++c) {
             item_ptr[first + c] = b + c * L;
             chunk_item[sc.cpos[r] + c] = first + c;
+            chunk_ord[first + c] = sc.cpos[r] + c;
         }
         long_seg[sc.lpos[r]] = (int32_t)r;
         long_first[sc.lpos[r]] = first;
         if (sc.is_huge[r]) huge_idx[sc.hpos[r]] = sc.lpos[r];
     } else if (len >= 1) {
-        if (nitem[r]) item_ptr[first] = b;
+        if (nitem[r]) {
+            item_ptr[first] = b;
+            chunk_ord[first] = -1;
+        }
     } else {
         empty_seg[sc.epos[r]] = (int32_t)r;
     }
@@ -163,12 +167,13 @@ nsd_status nsd_plan_bounds(int32_t nseg, int32_t nnz, int32_t item_len, int32_t 
 
 nsd_status nsd_plan_build(int32_t nseg, int32_t nnz, const int32_t *segptr, int32_t item_len,
                           int32_t *item_ptr, int32_t *long_seg, int32_t *long_first,
-                          int32_t *huge_idx, int32_t *chunk_item, int32_t *empty_seg,
-                          nsd_plan *plan, void *ws, size_t ws_bytes, void *stream) {
+                          int32_t *huge_idx, int32_t *chunk_item, int32_t *chunk_ord,
+                          int32_t *empty_seg, nsd_plan *plan, void *ws, size_t ws_bytes,
+                          void *stream) {
     NSD_REQUIRE(nseg >= 0 && nnz >= 0 && item_len >= 1, "need nseg, nnz >= 0, item_len >= 1");
     NSD_REQUIRE(plan && item_ptr, "null pointer");
     NSD_REQUIRE(nseg == 0 || (segptr && long_seg && long_first && huge_idx && chunk_item &&
-                              empty_seg && ws),
+                              chunk_ord && empty_seg && ws),
                 "null pointer");
     if (2LL * nnz + nseg >= (1LL << 31)) return fail(NSD_ERR_TOO_LARGE, "plan cost overflows int32");
     hipStream_t st = as_stream(stream);
@@ -179,6 +184,7 @@ nsd_status nsd_plan_build(int32_t nseg, int32_t nnz, const int32_t *segptr, int3
     plan->long_first = long_first;
     plan->huge_idx = huge_idx;
     plan->chunk_item = chunk_item;
+    plan->chunk_ord = chunk_ord;
     plan->empty_seg = empty_seg;
     if (nseg == 0) {
         plan_sentinel_kernel<<<1, 1, 0, st>>>(item_ptr, 0);
@@ -223,7 +229,8 @@ nsd_status nsd_plan_build(int32_t nseg, int32_t nnz, const int32_t *segptr, int3
     NSD_TRY(scan_exclusive(is_huge, hpos, nseg, tot + 4, scan_ws, st));
     PlanScans sc{nitem, ipos, lpos, hpos, cpos, epos, is_huge};
     plan_fill_kernel<<<g, kPlanThreads, 0, st>>>(nseg, nnz, segptr, item_len, sc, item_ptr, long_seg,
-                                                 long_first, huge_idx, chunk_item, empty_seg);
+                                                 long_first, huge_idx, chunk_item, chunk_ord,
+                                                 empty_seg);
     NSD_TRY(check_launch("plan_fill_kernel"));
     int32_t h[6];
     NSD_HIP(hipMemcpyAsync(h, tot, sizeof(h), hipMemcpyDeviceToHost, st));

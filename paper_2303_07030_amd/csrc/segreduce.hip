@@ -47,7 +47,7 @@ __global__ __launch_bounds__(kBlock) void sgr_main_kernel(SgrParams a) {
     pacc.zero();
     int pseg = -1;
     if (s < a.plan.nitems) pseg = sgr_walk<VEC, G, U>(a, s, col, on, NoSegDone{}, pacc);
-    store_chunk_partial<VEC, G>(pseg, pacc, a.part, s, a.k, col, on);
+    store_chunk_partial<VEC, G>(pseg, pacc, a.part, a.plan.chunk_ord, s, a.k, col, on);
 }
 
 // Zero-fill of a whole output when there is nothing to reduce.
@@ -56,8 +56,9 @@ __global__ void fill_zero_kernel(float *out, int64_t n) {
     if (i < n) out[i] = 0.f;
 }
 
+// One partial row per chunk item (compact, see store_chunk_partial).
 size_t sgr_part_bytes(const nsd_plan &plan, int k) {
-    return (size_t)std::max<int64_t>(plan.nitems, 1) * (size_t)k * sizeof(float);
+    return (size_t)std::max<int64_t>(plan.nchunks, 1) * (size_t)k * sizeof(float);
 }
 
 template <int VEC, int G>
@@ -341,7 +342,7 @@ __global__ __launch_bounds__(kBlock) NSD_FROB_OCCUPANCY void frob_row_kernel(Fro
                     for (int e = 0; e < VEC; ++e) lsq += (double)c.v[e] * c.v[e];
             }, pacc);
         }
-        store_chunk_partial<VEC, G>(pseg, pacc, a.part, s, a.k, col, on);
+        store_chunk_partial<VEC, G>(pseg, pacc, a.part, a.plan.chunk_ord, s, a.k, col, on);
     }
     const double t = block_sum(lsq);
     if (threadIdx.x == 0) f.loss_part[blockIdx.x] = 0.5 * t;

@@ -153,8 +153,9 @@ __device__ __forceinline__ void walk_item(const SgrParams &a, int64_t a0, int64_
 // item's partial row.  A segment then has one partial row per group it
 // spans: its first chunk's and those of the chunks at item indexes
 // divisible by the group size, which the combine reads with chunk_stride =
-// chunk_group<G>().  Every lane of the wave calls this (seg < 0: the slot
-// holds no partial).
+// chunk_group<G>().  Partial rows are compact: item s writes row
+// chunk_ord[s] (its position among the chunk items).  Every lane of the wave
+// calls this (seg < 0: the slot holds no partial).
 template <int G>
 constexpr int chunk_group() {
     return kWave / G < 8 ? kWave / G : 8;
@@ -162,10 +163,11 @@ constexpr int chunk_group() {
 
 template <int VEC, int G>
 __device__ __forceinline__ void store_chunk_partial(int seg, Vec<VEC> acc, float *part,
-                                                    int64_t s, int64_t k, int col, bool on) {
+                                                    const int32_t *chunk_ord, int64_t s,
+                                                    int64_t k, int col, bool on) {
     constexpr int CG = chunk_group<G>();
     if constexpr (CG == 1) {
-        if (seg >= 0 && on) acc.store(part + s * k + col);
+        if (seg >= 0 && on) acc.store(part + (int64_t)chunk_ord[s] * k + col);
     } else {
         if (!__any(seg >= 0)) return;  // wave-uniform: no partial in this wave
         const int lane = threadIdx.x % kWave;
@@ -184,7 +186,7 @@ __device__ __forceinline__ void store_chunk_partial(int seg, Vec<VEC> acc, float
             run = run && q + d < CG && sseg == seg;
             if (run) acc.add(x);
         }
-        if (leader && on) acc.store(part + s * k + col);
+        if (leader && on) acc.store(part + (int64_t)chunk_ord[s] * k + col);
     }
 }
 
@@ -363,11 +365,14 @@ __device__ __forceinline__ void fix_block(const SgrParams &a, int b, int wave_bl
     const int seg = a.plan.long_seg[i];
     const int64_t s0 = a.plan.long_first[i];
     const int64_t chunks = ((int64_t)a.segptr[seg + 1] - a.segptr[seg] + L - 1) / L;
-    // the segment's partial rows: s0, then s0 + fb + j * stride
+    // the segment's partial rows: items s0, then s0 + fb + j * stride, whose
+    // rows in the compact array follow the first chunk's (chunks are
+    // consecutive items and consecutive in chunk_item)
     const int64_t stride = a.chunk_stride;
     const int64_t fb = stride - s0 % stride;
     const int64_t n = fb < chunks ? 1 + (chunks - fb + stride - 1) / stride : 1;
-    auto prow = [&](int64_t t) { return s0 + (t == 0 ? 0 : fb + (t - 1) * stride); };
+    const int64_t r0 = a.plan.chunk_ord[s0];
+    auto prow = [&](int64_t t) { return r0 + (t == 0 ? 0 : fb + (t - 1) * stride); };
     // one wave per segment of at most kHugeChunks partial rows, else a block
     if (huge != (n > kHugeChunks)) return;
     double lsq = 0.0;

@@ -1,17 +1,19 @@
-// Tensor-times-vector of a sparse 3-tensor along its third mode and its
-// vector-Jacobian product:
-//   Y(i, j) = sum over stored (i, j, l) of X_ijl * v(l)
-// on the projected keys {(i, j) : some (i, j, l) is stored}; it is a sum over
-// X's stored keys with a singleton {(i, j) -> X_ijl v(l)} added by "+=", so Y
-// is itself sparse (Logical SDQLite, Section 3; code generation, Section 5.5).
-// Given the upstream gY on Y's keys:
-//   dX_ijl = gY(i, j) v(l)                 on X's keys (input order)
-//   dv(l)  = sum over stored (i, j, l) of X_ijl gY(i, j)
+// Mode-n products of a sparse order-N tensor and their vector-Jacobian
+// products:
+//   Y(c_{-n}) = sum over stored keys c of X(c) * v(c_n)        (TTV)
+//   Y(c_{-n}, :) = sum over stored keys c of X(c) * U(c_n, :)  (TTM)
+// on the projected keys {c_{-n} : some key c is stored}, c_{-n} being the key
+// with coordinate n dropped; Y is a sum over X's stored keys with a
+// singleton added by "+=", so it is itself sparse (Logical SDQLite,
+// Section 3; code generation, Section 5.5).  Given the upstream gY on Y's
+// keys:
+//   dX(c) = <gY(c_{-n}), U(c_n)>              on X's keys (input order)
+//   dU(l) = sum over stored keys with c_n = l of X(c) gY(c_{-n})
 //
-// The builder stably sorts X's entries by (i, j) (two counting-sort passes),
-// numbers the distinct keys, and also sorts by l (a mode index); both views
-// get a work plan, so the forward product and dv are k = 1 gather-reduces
-// and dX is one elementwise pass.
+// The builder stably sorts X's entries by their other coordinates (one
+// counting-sort pass per mode, last mode first), numbers the distinct keys,
+// and also sorts by the mode-n coordinate; both views get a work plan, so the
+// products and dU are gather-reduces and dX is one sampled product.
 #include <algorithm>
 
 #include "nsd_internal.hpp"
@@ -29,33 +31,40 @@ __global__ void ttv_gather_kernel(int64_t n, const int32_t *perm, const int32_t 
     if (q < n) dst[q] = src[perm[q]];
 }
 
-__global__ void ttv_heads_kernel(int64_t n, const int32_t *a, const int32_t *b, int32_t *head) {
+// The key-sorted coordinates of the modes other than n (up to 5 arrays).
+struct KeyCols {
+    const int32_t *c[NSD_MAX_ORDER - 1];
+    int32_t n;
+};
+
+__global__ void ttv_heads_kernel(int64_t n, KeyCols k, int32_t *head) {
     const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (q < n) head[q] = (q == 0 || a[q] != a[q - 1] || b[q] != b[q - 1]) ? 1 : 0;
+    if (q >= n) return;
+    bool h = q == 0;
+    for (int o = 0; o < k.n && !h; ++o) h = k.c[o][q] != k.c[o][q - 1];
+    head[q] = h ? 1 : 0;
 }
 
-// seg = inclusive count of heads - 1; the head of every key writes it out;
-// pair (input order) gets every entry's key index.
-__global__ void ttv_keys_kernel(int64_t n, const int32_t *head, const int32_t *pos,
-                                const int32_t *i_s, const int32_t *j_s, const int32_t *perm,
-                                int32_t *seg, int32_t *yi, int32_t *yj, int32_t *pair) {
+struct KeyOut {
+    int32_t *c[NSD_MAX_ORDER - 1];
+};
+
+// seg = inclusive count of heads - 1; the head of every key writes its
+// coordinates; pair (input order) gets every entry's key index.
+__global__ void ttv_keys_kernel(int64_t n, const int32_t *head, const int32_t *pos, KeyCols k,
+                                const int32_t *perm, int32_t *seg, KeyOut y, int32_t *pair) {
     const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (q >= n) return;
     const int32_t s = pos[q] + head[q] - 1;
     seg[q] = s;
     pair[perm[q]] = s;
-    if (head[q]) {
-        yi[s] = i_s[q];
-        yj[s] = j_s[q];
-    }
+    if (head[q])
+        for (int o = 0; o < k.n; ++o) y.c[o][s] = k.c[o][q];
 }
 
-__global__ void ttv_range_kernel(int64_t n, int32_t d0, int32_t d1, int32_t d2, const int32_t *i,
-                                 const int32_t *j, const int32_t *l, int32_t *flag) {
+__global__ void ttv_range_kernel(int64_t n, int32_t dim, const int32_t *c, int32_t *flag) {
     const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (p >= n) return;
-    if (i[p] < 0 || i[p] >= d0 || j[p] < 0 || j[p] >= d1 || l[p] < 0 || l[p] >= d2)
-        atomicOr(flag, 1);
+    if (p < n && (c[p] < 0 || c[p] >= dim)) atomicOr(flag, 1);
 }
 
 __global__ void ttv_dx_kernel(int64_t n, const int32_t *seg, const int32_t *perm,
@@ -64,16 +73,21 @@ __global__ void ttv_dx_kernel(int64_t n, const int32_t *seg, const int32_t *perm
     if (q < n) dx[perm[q]] = gy[seg[q]] * v[kidx[q]];
 }
 
-static size_t ttv_build_ws(int64_t nnz, int32_t maxdim) {
+// Scratch of the builder: the N - 1 key-sorted coordinate arrays, two
+// permutations, the head flags, the key of every entry and a flag word.
+static size_t ttv_build_ws(int32_t order, int64_t nnz, int32_t maxdim) {
     Carver c(nullptr);
-    for (int t = 0; t < 6; ++t) c.take<int32_t>(nnz > 0 ? nnz : 1);
+    for (int t = 0; t < order - 1 + 4; ++t) c.take<int32_t>(nnz > 0 ? nnz : 1);
     c.take<int32_t>(64);
     return c.bytes() + sort_ws_bytes(nnz, maxdim) + scan_ws_bytes(nnz);
 }
 
 static nsd_status check_ttv(const nsd_ttv_plan *T) {
     NSD_REQUIRE(T != nullptr, "TTV plan is NULL");
-    NSD_REQUIRE(T->nnz >= 0 && T->ny >= 0 && T->dims[2] >= 1, "bad TTV plan sizes");
+    NSD_REQUIRE(T->order >= 3 && T->order <= NSD_MAX_ORDER && T->mode >= 0 &&
+                    T->mode < T->order,
+                "TTV plan of order %d along mode %d", T->order, T->mode);
+    NSD_REQUIRE(T->nnz >= 0 && T->ny >= 0 && T->dims[T->mode] >= 1, "bad TTV plan sizes");
     if (T->nnz > 0) {
         NSD_REQUIRE(T->yptr && T->yseg && T->yperm && T->ykidx && T->lptr && T->lseg &&
                         T->lperm && T->lpair,
@@ -121,38 +135,60 @@ using namespace nsd;
 
 extern "C" {
 
-nsd_status nsd_ttv_build_workspace_size(int32_t nnz, const int32_t *dims, size_t *bytes) {
-    NSD_REQUIRE(dims && bytes, "null pointer");
-    NSD_REQUIRE(nnz >= 0 && dims[0] >= 1 && dims[1] >= 1 && dims[2] >= 1, "bad sizes");
-    *bytes = ttv_build_ws(nnz, std::max({dims[0], dims[1], dims[2]}));
+static nsd_status check_build_sizes(int32_t order, const int32_t *dims, int32_t nnz) {
+    NSD_REQUIRE(dims != nullptr, "dims is NULL");
+    NSD_REQUIRE(order >= 3 && order <= NSD_MAX_ORDER, "order %d outside [3, %d]", order,
+                NSD_MAX_ORDER);
+    NSD_REQUIRE(nnz >= 0, "negative nnz");
+    for (int m = 0; m < order; ++m) NSD_REQUIRE(dims[m] >= 1, "dims[%d] = %d < 1", m, dims[m]);
     return NSD_OK;
 }
 
-nsd_status nsd_ttv_build(int32_t nnz, const int32_t *dims, const int32_t *i, const int32_t *j,
-                         const int32_t *l, int32_t *yi, int32_t *yj, int32_t *yptr,
-                         int32_t *yseg, int32_t *yperm, int32_t *ykidx, int32_t *lptr,
-                         int32_t *lseg, int32_t *lperm, int32_t *lpair, int32_t *ny,
-                         void *ws, size_t ws_bytes, void *stream) {
-    NSD_REQUIRE(dims && ny && yptr && lptr, "null pointer");
-    NSD_REQUIRE(nnz >= 0 && dims[0] >= 1 && dims[1] >= 1 && dims[2] >= 1, "bad sizes");
+nsd_status nsd_ttv_build_workspace_size(int32_t order, const int32_t *dims, int32_t nnz,
+                                        size_t *bytes) {
+    NSD_REQUIRE(bytes != nullptr, "bytes is NULL");
+    NSD_TRY(check_build_sizes(order, dims, nnz));
+    *bytes = ttv_build_ws(order, nnz, *std::max_element(dims, dims + order));
+    return NSD_OK;
+}
+
+nsd_status nsd_ttv_build(int32_t order, const int32_t *dims, int32_t nnz,
+                         const int32_t *const *coords, int32_t mode, int32_t *const *ykey,
+                         int32_t *yptr, int32_t *yseg, int32_t *yperm, int32_t *ykidx,
+                         int32_t *lptr, int32_t *lseg, int32_t *lperm, int32_t *lpair,
+                         int32_t *ny, void *ws, size_t ws_bytes, void *stream) {
+    NSD_TRY(check_build_sizes(order, dims, nnz));
+    NSD_REQUIRE(mode >= 0 && mode < order, "mode %d of an order-%d tensor", mode, order);
+    NSD_REQUIRE(ny && yptr && lptr, "null pointer");
     hipStream_t st = as_stream(stream);
     if (nnz == 0) {
         NSD_TRY(segptr_from_sorted(0, 0, yseg, yptr, st));
-        NSD_TRY(segptr_from_sorted(0, dims[2], lseg, lptr, st));
+        NSD_TRY(segptr_from_sorted(0, dims[mode], lseg, lptr, st));
         NSD_HIP(hipStreamSynchronize(st));
         *ny = 0;
         return NSD_OK;
     }
-    NSD_REQUIRE(i && j && l && yi && yj && yseg && yperm && ykidx && lseg && lperm && lpair && ws,
+    NSD_REQUIRE(coords && ykey && yseg && yperm && ykidx && lseg && lperm && lpair && ws,
                 "null pointer");
-    const int32_t maxdim = std::max({dims[0], dims[1], dims[2]});
-    if (ws_bytes < ttv_build_ws(nnz, maxdim))
-        return fail(NSD_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, ttv_build_ws(nnz, maxdim));
+    int others[NSD_MAX_ORDER - 1];
+    for (int m = 0, o = 0; m < order; ++m) {
+        NSD_REQUIRE(coords[m] != nullptr, "coordinate array %d is NULL", m);
+        if (m != mode) {
+            NSD_REQUIRE(ykey[o] != nullptr, "key array %d is NULL", o);
+            others[o++] = m;
+        }
+    }
+    const int nk = order - 1;
+    const int32_t maxdim = *std::max_element(dims, dims + order);
+    const size_t need = ttv_build_ws(order, nnz, maxdim);
+    if (ws_bytes < need) return fail(NSD_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, need);
     Carver c(ws);
-    int32_t *t0 = c.take<int32_t>(nnz);
-    int32_t *t1 = c.take<int32_t>(nnz);
-    int32_t *t2 = c.take<int32_t>(nnz);
-    int32_t *t3 = c.take<int32_t>(nnz);
+    KeyCols kc;
+    kc.n = nk;
+    int32_t *sorted[NSD_MAX_ORDER - 1];
+    for (int o = 0; o < nk; ++o) kc.c[o] = sorted[o] = c.take<int32_t>(nnz);
+    int32_t *pa = c.take<int32_t>(nnz);
+    int32_t *pb = c.take<int32_t>(nnz);
     int32_t *head = c.take<int32_t>(nnz);
     int32_t *pair = c.take<int32_t>(nnz);
     int32_t *flag = c.take<int32_t>(64);
@@ -161,32 +197,52 @@ nsd_status nsd_ttv_build(int32_t nnz, const int32_t *dims, const int32_t *i, con
     const int64_t g = ttv_grid(nnz);
 
     NSD_HIP(hipMemsetAsync(flag, 0, sizeof(int32_t), st));
-    ttv_range_kernel<<<g, kTtvThreads, 0, st>>>(nnz, dims[0], dims[1], dims[2], i, j, l, flag);
-    NSD_TRY(check_launch("ttv_range_kernel"));
+    for (int m = 0; m < order; ++m) {
+        ttv_range_kernel<<<g, kTtvThreads, 0, st>>>(nnz, dims[m], coords[m], flag);
+        NSD_TRY(check_launch("ttv_range_kernel"));
+    }
     int32_t h = 0;
     NSD_HIP(hipMemcpyAsync(&h, flag, sizeof(int32_t), hipMemcpyDeviceToHost, st));
     NSD_HIP(hipStreamSynchronize(st));
     if (h) return fail(NSD_ERR_BAD_FORMAT, "coordinate out of range");
 
-    // (i, j) order: stable by j, then stable by i; ties keep input order
-    NSD_TRY(radix_sort_pairs(nnz, dims[1], j, nullptr, t0, t1, sort_ws, st));
-    ttv_gather_kernel<<<g, kTtvThreads, 0, st>>>(nnz, t1, i, t2);
+    // lexicographic order of the other coordinates: stable passes from the
+    // last other mode to the first; ties keep input order.  perm ends in
+    // yperm, each pass's sorted keys in a scratch array.
+    int32_t *perm = nullptr;  // identity before the first pass
+    for (int o = nk - 1; o >= 0; --o) {
+        const int m = others[o];
+        const int32_t *key = coords[m];
+        if (perm) {
+            ttv_gather_kernel<<<g, kTtvThreads, 0, st>>>(nnz, perm, coords[m], head);
+            NSD_TRY(check_launch("ttv_gather_kernel"));
+            key = head;
+        }
+        int32_t *out = o == 0 ? yperm : (perm == pa ? pb : pa);
+        NSD_TRY(radix_sort_pairs(nnz, dims[m], key, perm, sorted[o], out, sort_ws, st));
+        perm = out;
+    }
+    // the key-sorted coordinates of the other modes, and l
+    for (int o = 1; o < nk; ++o) {
+        ttv_gather_kernel<<<g, kTtvThreads, 0, st>>>(nnz, yperm, coords[others[o]], sorted[o]);
+        NSD_TRY(check_launch("ttv_gather_kernel"));
+    }
+    ttv_gather_kernel<<<g, kTtvThreads, 0, st>>>(nnz, yperm, coords[mode], ykidx);
     NSD_TRY(check_launch("ttv_gather_kernel"));
-    NSD_TRY(radix_sort_pairs(nnz, dims[0], t2, t1, t3, yperm, sort_ws, st));  // t3 = i sorted
-    ttv_gather_kernel<<<g, kTtvThreads, 0, st>>>(nnz, yperm, j, t0);          // t0 = j sorted
-    ttv_gather_kernel<<<g, kTtvThreads, 0, st>>>(nnz, yperm, l, ykidx);
-    ttv_heads_kernel<<<g, kTtvThreads, 0, st>>>(nnz, t3, t0, head);
+    ttv_heads_kernel<<<g, kTtvThreads, 0, st>>>(nnz, kc, head);
     NSD_TRY(check_launch("ttv_heads_kernel"));
-    NSD_TRY(scan_exclusive(head, t2, nnz, flag + 1, scan_ws, st));
-    ttv_keys_kernel<<<g, kTtvThreads, 0, st>>>(nnz, head, t2, t3, t0, yperm, yseg, yi, yj, pair);
+    NSD_TRY(scan_exclusive(head, pa, nnz, flag + 1, scan_ws, st));
+    KeyOut yo;
+    for (int o = 0; o < nk; ++o) yo.c[o] = ykey[o];
+    ttv_keys_kernel<<<g, kTtvThreads, 0, st>>>(nnz, head, pa, kc, yperm, yseg, yo, pair);
     NSD_TRY(check_launch("ttv_keys_kernel"));
     int32_t nkeys = 0;
     NSD_HIP(hipMemcpyAsync(&nkeys, flag + 1, sizeof(int32_t), hipMemcpyDeviceToHost, st));
     NSD_HIP(hipStreamSynchronize(st));
     NSD_TRY(segptr_from_sorted(nnz, nkeys, yseg, yptr, st));
-    // l order
-    NSD_TRY(radix_sort_pairs(nnz, dims[2], l, nullptr, lseg, lperm, sort_ws, st));
-    NSD_TRY(segptr_from_sorted(nnz, dims[2], lseg, lptr, st));
+    // mode-n order
+    NSD_TRY(radix_sort_pairs(nnz, dims[mode], coords[mode], nullptr, lseg, lperm, sort_ws, st));
+    NSD_TRY(segptr_from_sorted(nnz, dims[mode], lseg, lptr, st));
     ttv_gather_kernel<<<g, kTtvThreads, 0, st>>>(nnz, lperm, pair, lpair);
     NSD_TRY(check_launch("ttv_gather_kernel"));
     NSD_HIP(hipStreamSynchronize(st));
@@ -232,8 +288,8 @@ nsd_status nsd_ttv_vjp(const nsd_ttv_plan *T, const float *x, const float *v, co
         probe_end(NSD_KERNEL_TTV, st);
         NSD_TRY(check_launch("ttv_dx_kernel"));
     }
-    return segreduce(ttv_sgr(T->dims[2], T->nnz, T->lplan, T->lptr, T->lseg, T->lpair, x, T->lperm,
-                             gy, dv, ws),
+    return segreduce(ttv_sgr(T->dims[T->mode], T->nnz, T->lplan, T->lptr, T->lseg, T->lpair, x,
+                             T->lperm, gy, dv, ws),
                      st);
 }
 
@@ -245,7 +301,7 @@ nsd_status nsd_ttm_workspace_size(const nsd_ttv_plan *T, int32_t R, size_t *byte
     return NSD_OK;
 }
 
-// Y = X x_3 U: the gather-reduce of TTV at width R (rows U[l] weighted by x).
+// Y = X x_n U: the gather-reduce of TTV at width R (rows U[l] weighted by x).
 nsd_status nsd_ttm(const nsd_ttv_plan *T, const float *x, const float *U, int32_t R, float *Y,
                    void *ws, size_t ws_bytes, void *stream) {
     NSD_TRY(check_ttv(T));
@@ -263,7 +319,7 @@ nsd_status nsd_ttm(const nsd_ttv_plan *T, const float *x, const float *U, int32_
     return s;
 }
 
-// dx = <gY[key], U[l]> per entry (an SDDMM in (i, j) order written to input
+// dx = <gY[key], U[l]> per entry (an SDDMM in key order written to input
 // positions), dU = the gather-reduce over l of x * gY[key].
 nsd_status nsd_ttm_vjp(const nsd_ttv_plan *T, const float *x, const float *U, int32_t R,
                        const float *gY, float *dx, float *dU, void *ws, size_t ws_bytes,
@@ -290,8 +346,8 @@ nsd_status nsd_ttm_vjp(const nsd_ttv_plan *T, const float *x, const float *U, in
         probe_end(NSD_KERNEL_TTV, st);
         NSD_TRY(s);
     }
-    return segreduce(ttv_sgr(T->dims[2], T->nnz, T->lplan, T->lptr, T->lseg, T->lpair, x, T->lperm,
-                             gY, dU, ws, R),
+    return segreduce(ttv_sgr(T->dims[T->mode], T->nnz, T->lplan, T->lptr, T->lseg, T->lpair, x,
+                             T->lperm, gY, dU, ws, R),
                      st);
 }
 

@@ -40,7 +40,8 @@ class nsd_plan(C.Structure):
     _fields_ = [("item_len", C.c_int32), ("nitems", C.c_int32), ("nlong", C.c_int32),
                 ("nhuge", C.c_int32), ("nchunks", C.c_int32), ("nempty", C.c_int32),
                 ("item_ptr", C.c_void_p), ("long_seg", C.c_void_p), ("long_first", C.c_void_p),
-                ("huge_idx", C.c_void_p), ("chunk_item", C.c_void_p), ("empty_seg", C.c_void_p),
+                ("huge_idx", C.c_void_p), ("chunk_item", C.c_void_p), ("chunk_ord", C.c_void_p),
+                ("empty_seg", C.c_void_p),
                 ("longest_chunks", C.c_int32)]
 
 
@@ -81,8 +82,9 @@ class nsd_coon(C.Structure):
 
 
 class nsd_ttv_plan(C.Structure):
-    _fields_ = [("dims", C.c_int32 * 3), ("nnz", C.c_int32), ("ny", C.c_int32),
-                ("yi", C.c_void_p), ("yj", C.c_void_p), ("yptr", C.c_void_p),
+    _fields_ = [("order", C.c_int32), ("mode", C.c_int32), ("dims", C.c_int32 * MAX_ORDER),
+                ("nnz", C.c_int32), ("ny", C.c_int32),
+                ("ykey", C.c_void_p * (MAX_ORDER - 1)), ("yptr", C.c_void_p),
                 ("yseg", C.c_void_p), ("yperm", C.c_void_p), ("ykidx", C.c_void_p),
                 ("yplan", nsd_plan), ("lptr", C.c_void_p), ("lseg", C.c_void_p),
                 ("lperm", C.c_void_p), ("lpair", C.c_void_p), ("lplan", nsd_plan)]
@@ -112,8 +114,8 @@ _SIGS = {
     "nsd_plan_item_len": (C.c_int, [_I, _I, C.POINTER(_I)]),
     "nsd_plan_bounds": (C.c_int, [_I, _I, _I, C.POINTER(_I), C.POINTER(_I), C.POINTER(_I),
                                   C.POINTER(_SZ)]),
-    "nsd_plan_build": (C.c_int, [_I, _I, _P, _I, _P, _P, _P, _P, _P, _P, C.POINTER(nsd_plan), _P,
-                                 _SZ, _P]),
+    "nsd_plan_build": (C.c_int, [_I, _I, _P, _I, _P, _P, _P, _P, _P, _P, _P,
+                                 C.POINTER(nsd_plan), _P, _SZ, _P]),
     "nsd_build_workspace_size": (C.c_int, [_I, _I, C.POINTER(_SZ)]),
     "nsd_csr_expand_rows": (C.c_int, [_I, _I, _P, _P, _P]),
     "nsd_coo_to_csr": (C.c_int, [_I, _I, _I, _P, _P, _P, C.c_int, _P, _P, _P, _P, _P,
@@ -134,9 +136,10 @@ _SIGS = {
                                     _P]),
     "nsd_loss_mf": (C.c_int, [_CSR, _CSC, _P, _P, _P, _I, C.c_float, _P, _P, _P, _P, _SZ, _P]),
     "nsd_cp_workspace_size": (C.c_int, [_COO3, _I, C.POINTER(_SZ)]),
-    "nsd_ttv_build_workspace_size": (C.c_int, [_I, C.POINTER(_I), C.POINTER(_SZ)]),
-    "nsd_ttv_build": (C.c_int, [_I, C.POINTER(_I), _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
-                                _P, C.POINTER(_I), _P, _SZ, _P]),
+    "nsd_ttv_build_workspace_size": (C.c_int, [_I, C.POINTER(_I), _I, C.POINTER(_SZ)]),
+    "nsd_ttv_build": (C.c_int, [_I, C.POINTER(_I), _I, C.POINTER(_P), _I, C.POINTER(_P),
+                                _P, _P, _P, _P, _P, _P, _P, _P,
+                                C.POINTER(_I), _P, _SZ, _P]),
     "nsd_ttv_workspace_size": (C.c_int, [_TTV, C.POINTER(_SZ)]),
     "nsd_ttv": (C.c_int, [_TTV, _P, _P, _P, _P, _SZ, _P]),
     "nsd_ttv_vjp": (C.c_int, [_TTV, _P, _P, _P, _P, _P, _P, _SZ, _P]),
@@ -252,14 +255,16 @@ def nsd_plan_bounds(nseg: int, nnz: int, item_len: int):
 
 
 def nsd_plan_build(nseg, nnz, segptr, item_len, item_ptr, long_seg, long_first, huge_idx,
-                   chunk_item, empty_seg, ws, stream=None) -> nsd_plan:
+                   chunk_item, chunk_ord, empty_seg, ws, stream=None) -> nsd_plan:
     plan = nsd_plan()
     _check(_lib.nsd_plan_build(nseg, nnz, _p(segptr), item_len, _p(item_ptr), _p(long_seg),
-                               _p(long_first), _p(huge_idx), _p(chunk_item), _p(empty_seg),
-                               C.byref(plan), _p(ws), _nbytes(ws), _stream(stream)),
+                               _p(long_first), _p(huge_idx), _p(chunk_item), _p(chunk_ord),
+                               _p(empty_seg), C.byref(plan), _p(ws), _nbytes(ws),
+                               _stream(stream)),
            "nsd_plan_build")
     plan._keep = dict(item_ptr=item_ptr, long_seg=long_seg, long_first=long_first,
-                      huge_idx=huge_idx, chunk_item=chunk_item, empty_seg=empty_seg)
+                      huge_idx=huge_idx, chunk_item=chunk_item, chunk_ord=chunk_ord,
+                      empty_seg=empty_seg)
     return plan
 
 
@@ -384,19 +389,29 @@ def _dims3(dims):
     return (_I * 3)(*[int(x) for x in dims])
 
 
-def nsd_ttv_build_workspace_size(nnz, dims) -> int:
+def _dimsn(dims):
+    return (_I * len(dims))(*[int(x) for x in dims])
+
+
+def _ptr_array(ts):
+    return (_P * len(ts))(*[_p(t) for t in ts])
+
+
+def nsd_ttv_build_workspace_size(order, dims, nnz) -> int:
     b = _SZ(0)
-    _check(_lib.nsd_ttv_build_workspace_size(nnz, _dims3(dims), C.byref(b)),
+    _check(_lib.nsd_ttv_build_workspace_size(order, _dimsn(dims), nnz, C.byref(b)),
            "nsd_ttv_build_workspace_size")
     return b.value
 
 
-def nsd_ttv_build(nnz, dims, i, j, l, yi, yj, yptr, yseg, yperm, ykidx, lptr, lseg, lperm, lpair,
-                  ws, stream=None) -> int:
+def nsd_ttv_build(order, dims, nnz, coords, mode, ykey, yptr, yseg, yperm, ykidx, lptr, lseg,
+                  lperm, lpair, ws, stream=None) -> int:
+    """coords: `order` device tensors; ykey: order - 1 device tensors."""
     ny = _I(0)
-    _check(_lib.nsd_ttv_build(nnz, _dims3(dims), _p(i), _p(j), _p(l), _p(yi), _p(yj), _p(yptr),
-                              _p(yseg), _p(yperm), _p(ykidx), _p(lptr), _p(lseg), _p(lperm),
-                              _p(lpair), C.byref(ny), _p(ws), _nbytes(ws), _stream(stream)),
+    _check(_lib.nsd_ttv_build(order, _dimsn(dims), nnz, _ptr_array(coords), mode,
+                              _ptr_array(ykey), _p(yptr), _p(yseg), _p(yperm), _p(ykidx),
+                              _p(lptr), _p(lseg), _p(lperm), _p(lpair), C.byref(ny), _p(ws),
+                              _nbytes(ws), _stream(stream)),
            "nsd_ttv_build")
     return ny.value
 

@@ -29,7 +29,8 @@ def build_plan(nseg, nnz, segptr, item_len, device, stream=None):
 
     ws = torch.empty(max(wsb, 256), dtype=torch.uint8, device=device)
     return nsd.nsd_plan_build(nseg, nnz, segptr, item_len, arr(max_items + 1), arr(max_long),
-                              arr(max_long), arr(max_long), arr(max_chunks), arr(nseg), ws, stream)
+                              arr(max_long), arr(max_long), arr(max_chunks), arr(max_items),
+                              arr(nseg), ws, stream)
 
 
 class DeviceCsr:
@@ -265,34 +266,46 @@ class DeviceCooN:
 
 
 class DeviceTtv:
-    """The TTV projection of a COO 3-tensor onto its (i, j) keys, built by
-    nsd_ttv_build, with work plans over the keys and over l."""
+    """The projection of an order-N COO tensor (3 <= N <= 6) along one mode
+    n (default: the last), built by nsd_ttv_build: the distinct keys of the
+    other coordinates in lexicographic order (`ykey`, N - 1 arrays), work
+    plans over those keys and over the mode-n coordinate.  It is the layout
+    of the mode-n products nsd_ttv / nsd_ttm and their VJPs."""
 
-    def __init__(self, dims, i, j, l, device="cuda", item_len=16, stream=None):
+    def __init__(self, dims, coords, mode=-1, device="cuda", item_len=16, stream=None):
         self.dims = tuple(int(d) for d in dims)
-        i, j, l = (_dev(c, torch.int32, device) for c in (i, j, l))
-        nnz = int(i.numel())
+        N = len(self.dims)
+        self.order = N
+        self.mode = mode % N
+        coords = [_dev(c, torch.int32, device) for c in coords]
+        if len(coords) != N:
+            raise ValueError(f"{len(coords)} coordinate arrays for an order-{N} tensor")
+        nnz = int(coords[0].numel())
         n = max(nnz, 1)
 
         def arr(m):
             return torch.empty(max(m, 1), dtype=torch.int32, device=device)
 
-        self.yi, self.yj, self.yptr = arr(n), arr(n), arr(nnz + 1)
+        self.ykey = [arr(n) for _ in range(N - 1)]
+        self.yptr = arr(nnz + 1)
         self.yseg, self.yperm, self.ykidx = arr(n), arr(n), arr(n)
-        self.lptr, self.lseg, self.lperm, self.lpair = (arr(self.dims[2] + 1), arr(n), arr(n),
-                                                        arr(n))
-        ws = torch.empty(max(nsd.nsd_ttv_build_workspace_size(nnz, self.dims), 256),
+        self.lptr, self.lseg, self.lperm, self.lpair = (arr(self.dims[self.mode] + 1), arr(n),
+                                                        arr(n), arr(n))
+        ws = torch.empty(max(nsd.nsd_ttv_build_workspace_size(N, self.dims, nnz), 256),
                          dtype=torch.uint8, device=device)
-        self.ny = nsd.nsd_ttv_build(nnz, self.dims, i, j, l, self.yi, self.yj, self.yptr,
+        self.ny = nsd.nsd_ttv_build(N, self.dims, nnz, coords, self.mode, self.ykey, self.yptr,
                                     self.yseg, self.yperm, self.ykidx, self.lptr, self.lseg,
                                     self.lperm, self.lpair, ws, stream)
         self.nnz = nnz
         self.yplan = build_plan(self.ny, nnz, self.yptr, item_len, device, stream)
-        self.lplan = build_plan(self.dims[2], nnz, self.lptr, item_len, device, stream)
+        self.lplan = build_plan(self.dims[self.mode], nnz, self.lptr, item_len, device, stream)
         T = nsd.nsd_ttv_plan()
-        T.dims[:] = self.dims
+        T.order, T.mode = N, self.mode
+        T.dims[:N] = self.dims
         T.nnz, T.ny = nnz, self.ny
-        for f in ("yi", "yj", "yptr", "yseg", "yperm", "ykidx", "lptr", "lseg", "lperm", "lpair"):
+        for o in range(N - 1):
+            T.ykey[o] = self.ykey[o].data_ptr()
+        for f in ("yptr", "yseg", "yperm", "ykidx", "lptr", "lseg", "lperm", "lpair"):
             setattr(T, f, getattr(self, f).data_ptr())
         T.yplan, T.lplan = self.yplan, self.lplan
         self.desc = T

@@ -118,7 +118,11 @@ def test_host_argument_errors_before_launch(nsd):
         nsd.nsd_diag_keys(A, 1.0, None)                     # no output for 3 entries
     assert e.value.status == nsd.NSD_ERR_INVALID_ARG
     T = nsd.nsd_ttv_plan()
-    T.dims[:] = (4, 4, 4)
+    with pytest.raises(nsd.NsdError) as e:
+        nsd.nsd_ttm_workspace_size(T, 8)                    # order 0: not a built plan
+    assert e.value.status == nsd.NSD_ERR_INVALID_ARG
+    T.order, T.mode = 3, 2
+    T.dims[:3] = (4, 4, 4)
     with pytest.raises(nsd.NsdError) as e:
         nsd.nsd_ttm_workspace_size(T, 0)                    # R < 1
     assert e.value.status == nsd.NSD_ERR_INVALID_ARG
@@ -129,6 +133,13 @@ def test_host_argument_errors_before_launch(nsd):
     with pytest.raises(nsd.NsdError) as e:
         nsd.nsd_ttm_vjp(T, 0x1000, 0x1000, 8, 0x1000, 0x1000, 0x1000, None)  # plan not built
     assert e.value.status == nsd.NSD_ERR_INVALID_ARG
+    dims = (4, 4, 4, 4)
+    for order, mode in ((2, 0), (7, 0), (4, 4), (4, -1)):
+        with pytest.raises(nsd.NsdError) as e:              # order or mode out of range
+            nsd.nsd_ttv_build(order, dims[:max(min(order, 4), 1)] * 2, 3, [0x1000] * 4, mode,
+                              [0x1000] * 3, 0x1000, 0x1000, 0x1000, 0x1000, 0x1000, 0x1000,
+                              0x1000, 0x1000, None)
+        assert e.value.status == nsd.NSD_ERR_INVALID_ARG
 
 
 def test_binding_fails_loudly_without_library(tmp_path):

@@ -238,6 +238,11 @@ def test_plan_invariants(nsd, L):
         assert item_ptr[s0 + nch] == rowptr[r + 1]
     # bounded work: an item of short rows holds at most L + S entries
     assert np.diff(item_ptr).max() <= L + S
+    # compact partial rows: a chunk item's row is its position in chunk_item
+    ord_ = host(kp["chunk_ord"])[:n_it]
+    want = np.full(n_it, -1, np.int32)
+    want[chunks] = np.arange(plan.nchunks)
+    assert np.array_equal(ord_, want)
 
 
 # ---------------------------------------------------------------- primitives
@@ -467,14 +472,6 @@ def test_loss_mf_edge(nsd, operand, orc, k):
     check_mf(orc, D, U, V, k, got, seed=0.5)
 
 
-def test_loss_mf_rejects_wide_factors(nsd, operand):
-    nrows, ncols, rowptr, colind, val = edge_pattern(14)
-    A = operand(nrows, ncols, rowptr, colind, val)
-    with pytest.raises(nsd.NsdError) as e:
-        run_mf(nsd, A, np.zeros((nrows, 260), np.float32), np.zeros((ncols, 260), np.float32), 260)
-    assert e.value.status == nsd.NSD_ERR_UNSUPPORTED
-
-
 def run_cp(nsd, X, F, rank, seed=1.0):
     from paper_2303_07030_amd.operand import DeviceCoo3  # noqa: F401
     loss = torch.empty(1, dtype=torch.float64, device="cuda")
@@ -564,11 +561,12 @@ def test_ttv_and_vjp(nsd, orc, dims, nnz):
     l = (keys % dims[2]).astype(np.int32)
     x = rng.standard_normal(nnz).astype(np.float32)
     v = rng.standard_normal(dims[2]).astype(np.float32)
-    T = DeviceTtv(dims, i, j, l)
+    T = DeviceTtv(dims, [i, j, l])
     D = orc.Dok(dims, (i, j, l), x)
     yi, yj, y, ym = orc.ttv(D, v)
     assert T.ny == len(yi)
-    assert np.array_equal(host(T.yi)[:T.ny], yi) and np.array_equal(host(T.yj)[:T.ny], yj)
+    assert np.array_equal(host(T.ykey[0])[:T.ny], yi)
+    assert np.array_equal(host(T.ykey[1])[:T.ny], yj)
     ws = T.workspace()
     yg = torch.full((T.ny,), np.nan, dtype=torch.float32, device="cuda")
     nsd.nsd_ttv(T.desc, dev(x), dev(v), yg, ws)
@@ -596,7 +594,7 @@ def test_ttm_and_vjp(nsd, orc, dims, nnz, R):
     l = (keys % dims[2]).astype(np.int32)
     x = rng.standard_normal(nnz).astype(np.float32)
     U = rng.standard_normal((dims[2], R)).astype(np.float32)
-    T = DeviceTtv(dims, i, j, l)
+    T = DeviceTtv(dims, [i, j, l])
     D = orc.Dok(dims, (i, j, l), x)
     yi, yj, y, ym = orc.ttm(D, U, R)
     assert T.ny == len(yi)
@@ -611,6 +609,58 @@ def test_ttm_and_vjp(nsd, orc, dims, nnz, R):
     rdx, rdxm, rdU, rdUm = orc.ttm_vjp(D, U, R, gY, i, j, l)
     assert_mag_close(host(dx), rdx, rdxm, what="dX")
     assert_mag_close(host(dU), rdU, rdUm, what="dU")
+
+
+@pytest.mark.parametrize("dims,R", [((20, 30, 25), 7), ((6, 5, 4, 7), 16), ((4, 5, 3, 6, 2), 3),
+                                    ((3, 4, 2, 5, 2, 3), 64), ((2, 300, 3), 100)])
+def test_mode_products_every_mode(nsd, orc, dims, R):
+    """TTM (and TTV, its width-1 case) along every mode of orders 3 to 6,
+    with the VJPs: projected keys bit for bit, values against the oracle's
+    mode product (the 2 x 300 x 3 shape gives long fibres in mode 1)."""
+    from paper_2303_07030_amd.operand import DeviceTtv
+    N = len(dims)
+    rng = np.random.default_rng(sum(dims) * R)
+    size = int(np.prod(dims))
+    nnz = min(size // 2, 6000)
+    keys = rng.choice(size, size=nnz, replace=False)
+    coords = [c.astype(np.int32) for c in np.unravel_index(keys, dims)]
+    perm = rng.permutation(nnz)  # input order not sorted
+    coords = [c[perm] for c in coords]
+    x = rng.standard_normal(nnz).astype(np.float32)
+    D = orc.Dok(dims, coords, x)
+    for n in range(N):
+        T = DeviceTtv(dims, coords, mode=n)
+        U = rng.standard_normal((dims[n], R)).astype(np.float32)
+        yk, y, ym = orc.ttmn(D, n, U, R)
+        assert T.ny == len(yk[0])
+        for o in range(N - 1):
+            assert np.array_equal(host(T.ykey[o])[:T.ny], yk[o]), f"mode {n} key {o}"
+        ws = T.ttm_workspace(R)
+        Y = torch.full((T.ny, R), np.nan, dtype=torch.float32, device="cuda")
+        nsd.nsd_ttm(T.desc, dev(x), dev(U), R, Y, ws)
+        assert_mag_close(host(Y), y, ym, what=f"Y mode {n}")
+        gY = rng.standard_normal((T.ny, R)).astype(np.float32)
+        dx = torch.full((nnz,), np.nan, dtype=torch.float32, device="cuda")
+        dU = torch.full((dims[n], R), np.nan, dtype=torch.float32, device="cuda")
+        nsd.nsd_ttm_vjp(T.desc, dev(x), dev(U), R, dev(gY), dx, dU, ws)
+        rdx, rdxm, rdU, rdUm = orc.ttmn_vjp(D, n, U, R, gY, coords)
+        assert_mag_close(host(dx), rdx, rdxm, what=f"dX mode {n}")
+        assert_mag_close(host(dU), rdU, rdUm, what=f"dU mode {n}")
+        # TTV along the same mode: the first column of U
+        v = U[:, 0].copy()
+        yv = torch.full((max(T.ny, 1),), np.nan, dtype=torch.float32, device="cuda")
+        nsd.nsd_ttv(T.desc, dev(x), dev(v), yv, T.workspace())
+        _, y1, ym1 = orc.ttmn(D, n, v.reshape(-1, 1), 1)
+        assert_mag_close(host(yv)[:T.ny], y1[:, 0], ym1[:, 0], what=f"TTV mode {n}")
+
+
+def test_mode_product_builder_rejects_out_of_range(nsd):
+    from paper_2303_07030_amd.operand import DeviceTtv
+    c = [np.array([0, 1, 2], np.int32), np.array([0, 5, 1], np.int32),
+         np.array([1, 1, 1], np.int32), np.array([0, 0, 0], np.int32)]
+    with pytest.raises(nsd.NsdError) as e:
+        DeviceTtv((3, 4, 2, 1), c, mode=1)   # 5 >= dims[1]
+    assert e.value.status == nsd.NSD_ERR_BAD_FORMAT
 
 
 # ------------------------------------------------------- edge cases

@@ -5,12 +5,11 @@ The oracle cannot take whole passes over 20M-60M entries in test time, so:
   * sampled outputs are compared with the oracle run on a sub-problem that
     holds every stored entry the sampled outputs depend on (all entries of
     the sampled rows or columns), indices compacted;
-  * the global losses of the factorisation and CP workloads are the oracle's
-    losses summed over disjoint chunks of the stored entries (the loss is a
-    sum over stored entries, so the split is exact in fp64), chunks built in
-    parallel;
-  * the bilinear layer's loss is checked through identities that hold at any
-    size: L = sum_p A_p dA_p = <H, dH> (seed 1).
+  * the global losses are the oracle's losses summed over disjoint chunks of
+    the stored entries (the loss is a sum over stored entries, so the split
+    is exact in fp64), chunks built in parallel; the bilinear layer's loss
+    is also checked through identities that hold at any size:
+    L = sum_p A_p dA_p = <H, dH> (seed 1).
 Tolerance as everywhere: |got - ref| <= 1e-4 * mag, exact zero where mag = 0.
 """
 import concurrent.futures as cf
@@ -47,7 +46,7 @@ def compact(idx):
     return u, inv.astype(np.int32)
 
 
-def chunked_loss(orc, n, build_and_loss, nchunks=8):
+def chunked_loss(orc, n, build_and_loss, nchunks=8, workers=8):
     """Sum of (loss, mag) of the oracle over disjoint entry chunks, one
     single-threaded oracle per chunk, chunks in parallel threads."""
     bounds = np.linspace(0, n, nchunks + 1).astype(np.int64)
@@ -56,7 +55,7 @@ def chunked_loss(orc, n, build_and_loss, nchunks=8):
         orc.set_threads(1)  # OpenMP thread count is per calling thread
         return build_and_loss(bounds[c], bounds[c + 1])
 
-    with cf.ThreadPoolExecutor(max_workers=nchunks) as ex:
+    with cf.ThreadPoolExecutor(max_workers=min(workers, nchunks)) as ex:
         parts = list(ex.map(one, range(nchunks)))
     return sum(p[0] for p in parts), sum(p[1] for p in parts)
 
@@ -101,7 +100,17 @@ def test_bilinear_full_workload(nsd, orc):
     ref, mag = orc.spmm_t(D, G[ru], k)
     assert_mag_close(dHg[J], ref, mag, what="dH (sampled columns)")
 
-    # loss through identities of the exact values: sum_p A_p dA_p and <H, dH>
+    # the loss over all 60M entries, as a sum of per-chunk oracle losses
+    def part(b, e):
+        ru, ri = compact(rows[b:e])
+        cu, ci = compact(colind[b:e])
+        D = orc.Dok((len(ru), len(cu)), (ri, ci), val[b:e])
+        return orc.loss_bilinear(D, G[ru], H[cu], k)
+
+    L, Lm = chunked_loss(orc, len(colind), part, nchunks=32)
+    assert_mag_close(Lg, L, Lm, what="loss")
+
+    # and through identities of the exact values: sum_p A_p dA_p and <H, dH>
     a64 = val.astype(np.float64)
     s1 = float(np.dot(a64, dAg.astype(np.float64)))
     m1 = float(np.dot(np.abs(a64), np.abs(dAg.astype(np.float64))))
@@ -112,6 +121,83 @@ def test_bilinear_full_workload(nsd, orc):
         m2 += float(np.sum(np.abs(h) * np.abs(g)))
     assert abs(Lg - s1) <= TOL * m1, (Lg, s1, m1)
     assert abs(Lg - s2) <= TOL * m2, (Lg, s2, m2)
+
+
+# ------------------------------------- mode products of the CP tensor
+
+@pytest.mark.parametrize("mode", [2, 0])
+def test_mode_products_full_cp_tensor(nsd, orc, mode):
+    """TTV and TTM (width 32) with their VJPs on the CP workload's tensor
+    (10,000^3 with 20M uniform entries, about 18M distinct projected keys):
+    the projection's keys, entry order and key ranges bit for bit against a
+    stable lexicographic sort; values at sampled keys against the oracle on
+    the sub-problem of all entries of those keys; dX at sampled entries and
+    dU at sampled slices likewise."""
+    from paper_2303_07030_amd import synth
+    from paper_2303_07030_amd.operand import DeviceTtv
+    d = synth.make("cp")
+    dims, R = d["dims"], 32
+    coords = [d["i"], d["j"], d["k"]]
+    x = d["val"]
+    nnz = len(x)
+    others = [m for m in range(3) if m != mode]
+    T = DeviceTtv(dims, coords, mode=mode)
+    # definition: a stable sort by (other coordinates), keys = distinct runs
+    order = np.lexsort([coords[m] for m in others[::-1]])
+    assert np.array_equal(host(T.yperm)[:nnz], order), "entry order"
+    ka, kb = coords[others[0]][order], coords[others[1]][order]
+    head = np.ones(nnz, bool)
+    head[1:] = (ka[1:] != ka[:-1]) | (kb[1:] != kb[:-1])
+    starts = np.nonzero(head)[0]
+    ny = len(starts)
+    assert T.ny == ny and ny > 18_000_000
+    assert np.array_equal(host(T.ykey[0])[:ny], ka[starts]), "key coordinates"
+    assert np.array_equal(host(T.ykey[1])[:ny], kb[starts]), "key coordinates"
+    assert np.array_equal(host(T.yptr)[:ny + 1], np.append(starts, nnz).astype(np.int32))
+    seg = np.cumsum(head) - 1          # key of every sorted entry
+    key_of = np.empty(nnz, np.int64)
+    key_of[order] = seg                # key of every input entry
+    del ka, kb, head
+
+    rng = np.random.default_rng(9 + mode)
+    U = (0.5 * rng.standard_normal((dims[mode], R))).astype(np.float32)
+    xg, Ug = dev(x), dev(U)
+    Y = torch.empty((ny, R), dtype=torch.float32, device="cuda")
+    nsd.nsd_ttm(T.desc, xg, Ug, R, Y, T.ttm_workspace(R))
+    yv = torch.empty(ny, dtype=torch.float32, device="cuda")
+    nsd.nsd_ttv(T.desc, xg, dev(U[:, 0].copy()), yv, T.workspace())
+    gY = rng.standard_normal((ny, R)).astype(np.float32)
+    dx = torch.empty(nnz, dtype=torch.float32, device="cuda")
+    dU = torch.empty((dims[mode], R), dtype=torch.float32, device="cuda")
+    nsd.nsd_ttm_vjp(T.desc, xg, Ug, R, dev(gY), dx, dU, T.ttm_workspace(R))
+    Yh, yvh, dxh, dUh = host(Y), host(yv), host(dx), host(dU)
+    del Y, yv, dx, dU, xg
+
+    # sampled keys with all their entries
+    S = np.unique(np.concatenate([rng.choice(ny, 4096, replace=False), [0, ny - 1]]))
+    ent = order[np.concatenate([np.arange(starts[s], starts[s + 1] if s + 1 < ny else nnz)
+                                for s in S])]
+    D = orc.Dok(dims, [c[ent] for c in coords], x[ent])
+    yk, y, ym = orc.ttmn(D, mode, U, R)
+    assert len(yk[0]) == len(S)
+    assert_mag_close(Yh[S], y, ym, what="Y (sampled keys)")
+    _, y1, ym1 = orc.ttmn(D, mode, U[:, :1], 1)
+    assert_mag_close(yvh[S], y1[:, 0], ym1[:, 0], what="TTV (sampled keys)")
+
+    # dX at sampled entries: the upstream rows of their keys
+    P = rng.choice(nnz, 8192, replace=False)
+    D = orc.Dok(dims, [c[P] for c in coords], x[P])
+    kp = np.unique(key_of[P])          # the sub-problem's keys, in key order
+    rdx, rdxm, _, _ = orc.ttmn_vjp(D, mode, U, R, gY[kp], [c[P] for c in coords])
+    assert_mag_close(dxh[P], rdx, rdxm, what="dX (sampled entries)")
+
+    # dU at sampled slices, with every entry of those slices
+    L = np.unique(rng.choice(dims[mode], 4, replace=False))
+    sel = np.nonzero(np.isin(coords[mode], L))[0]
+    D = orc.Dok(dims, [c[sel] for c in coords], x[sel])
+    kp = np.unique(key_of[sel])
+    _, _, rdU, rdUm = orc.ttmn_vjp(D, mode, U, R, gY[kp], [c[sel] for c in coords])
+    assert_mag_close(dUh[L], rdU[L], rdUm[L], what="dU (sampled slices)")
 
 
 # ----------------------------------------------------- matrix factorisation
