@@ -429,6 +429,23 @@ nsd_status nsd_loss_bilinear(const nsd_csr *A, const nsd_csc *At, const float *H
                              float *dH, void *ws, size_t ws_bytes, void *stream);
 
 /*
+ * nsd_loss_bilinear without a workspace, for callers that cannot allocate
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same kernels and results, bit for bit, with the scratch
+ * (the column plan's chunk partials and the loss partials) taken from a
+ * static device array of 64 MiB that the library holds on every GPU it runs
+ * on until the process ends.  It calls no allocator.  Operands that need more
+ * scratch than that (about 64 MiB / (4 k) chunk items of long columns, or
+ * some 8M fused-pass blocks) give NSD_ERR_WORKSPACE before any launch; use
+ * nsd_loss_bilinear then.  Every call on a GPU uses that GPU's one array, so
+ * calls that overlap on one GPU (other streams, other threads) race: order
+ * them on one stream.  Arguments and results as nsd_loss_bilinear.  Async.
+ */
+nsd_status nsd_loss_bilinear_noalloc(const nsd_csr *A, const nsd_csc *At, const float *H,
+                                     const float *G, int32_t k, float seed, double *loss,
+                                     float *dA, float *dH, void *stream);
+
+/*
  * Sparse matrix factorisation, a sum over A's stored keys (the dictionary
  * iteration of Section 2.2; gradients by Sections 4.2 and 4.3):
  *   L = sum over stored (i, j) of r_ij^2,  r_ij = A(i,j) - <U[i,:], V[j,:]>

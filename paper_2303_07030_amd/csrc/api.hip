@@ -2,6 +2,7 @@
 // loss + gradient calls.  Each one validates its arguments on the host, then
 // enqueues kernels on the caller's stream and returns without waiting.
 #include <algorithm>
+#include <mutex>
 
 #include "nsd_internal.hpp"
 #include "segreduce.hpp"
@@ -202,6 +203,16 @@ static nsd_status check_bilinear(const nsd_csr *A, const nsd_csc *At, const floa
     return NSD_OK;
 }
 
+// Loss partials of the bilinear layer: one per block of its fused column
+// pass, or of the unfused SDDMM (widths a fused slot does not hold).
+static int64_t bilinear_loss_parts(const nsd_csr *A, const nsd_csc *At, int k) {
+    const nsd_plan *cols[1] = {&At->plan};
+    int64_t m = 1;
+    for (bool v : {true, false})
+        m = std::max({m, dual_blocks(cols, 1, k, v), sddmm_shape(A->nnz, k, v).nblocks});
+    return m;
+}
+
 // The loss total of an unfused SDDMM's block partials; with nnz == 0 the
 // loss is 0.
 static nsd_status finish_loss(const SddmmParams &p, double *loss, hipStream_t st);
@@ -226,6 +237,35 @@ static nsd_status bilinear_run(const nsd_csr *A, const nsd_csc *At, const float 
     NSD_TRY(finish_loss(sp, loss, st));
     // dH = seed * A^T G
     return segreduce(cols_params(A, At, G, k, seed, dH, part_col), st);
+}
+
+// ------------------------------------------------------ static scratch
+
+// Scratch of the entry points that allocate nothing (for callers that
+// cannot allocate: code under graph capture, serving loops): a file-scope
+// device array, one copy per GPU that the library runs on, held until the
+// process ends.  Host code never uses the array's name as an address: the
+// device address is looked up once per device (hipGetSymbolAddress, with that
+// device current, on the first call made there) and kept.
+constexpr size_t kScratchBytes = size_t(64) << 20;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static void *g_scratch[kMaxDevices];
+
+static nsd_status scratch_base(char **out) {
+    int dev = 0;
+    NSD_HIP(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices) return fail(NSD_ERR_UNSUPPORTED, "device %d", dev);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch[dev] == nullptr) {
+        void *p = nullptr;
+        NSD_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+        g_scratch[dev] = p;
+    }
+    *out = static_cast<char *>(g_scratch[dev]);
+    return NSD_OK;
 }
 
 // The loss partial count of a fused SDDMM; with nnz == 0 the loss is 0.
@@ -362,6 +402,24 @@ nsd_status nsd_loss_bilinear(const nsd_csr *A, const nsd_csc *At, const float *H
     NSD_TRY(carve_compute(ws, ws_bytes, A, At, k, &w));
     return bilinear_run(A, At, H, G, k, seed, loss, dA, dH, w.part_col, w.loss_part,
                         as_stream(stream));
+}
+
+nsd_status nsd_loss_bilinear_noalloc(const nsd_csr *A, const nsd_csc *At, const float *H,
+                                     const float *G, int32_t k, float seed, double *loss,
+                                     float *dA, float *dH, void *stream) {
+    NSD_TRY(check_bilinear(A, At, H, G, k, loss, dA, dH));
+    // the layout in the static scratch: the column plan's chunk partials,
+    // then the loss partials of the fused pass (or of the unfused SDDMM)
+    const size_t part = round256(sgr_part_bytes(At->plan, k));
+    const size_t need = part + round256(bilinear_loss_parts(A, At, k) * sizeof(double));
+    if (need > kScratchBytes)
+        return fail(NSD_ERR_WORKSPACE,
+                    "this operand needs %zu bytes of scratch; the static scratch holds %zu "
+                    "(use nsd_loss_bilinear with a workspace)", need, kScratchBytes);
+    char *b = nullptr;
+    NSD_TRY(scratch_base(&b));
+    return bilinear_run(A, At, H, G, k, seed, loss, dA, dH, reinterpret_cast<float *>(b),
+                        reinterpret_cast<double *>(b + part), as_stream(stream));
 }
 
 nsd_status nsd_spmm_vjp(const nsd_csr *A, const nsd_csc *At, const float *X, const float *G,

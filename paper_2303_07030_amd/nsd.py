@@ -134,6 +134,8 @@ _SIGS = {
                                      _P]),
     "nsd_loss_bilinear": (C.c_int, [_CSR, _CSC, _P, _P, _I, C.c_float, _P, _P, _P, _P, _SZ,
                                     _P]),
+    "nsd_loss_bilinear_noalloc": (C.c_int, [_CSR, _CSC, _P, _P, _I, C.c_float, _P, _P, _P,
+                                            _P]),
     "nsd_loss_mf": (C.c_int, [_CSR, _CSC, _P, _P, _P, _I, C.c_float, _P, _P, _P, _P, _SZ, _P]),
     "nsd_cp_workspace_size": (C.c_int, [_COO3, _I, C.POINTER(_SZ)]),
     "nsd_ttv_build_workspace_size": (C.c_int, [_I, C.POINTER(_I), _I, C.POINTER(_SZ)]),
@@ -366,6 +368,13 @@ def nsd_loss_bilinear(A: nsd_csr, At: nsd_csc, H, G, k, seed, loss, dA, dH, ws, 
     _check(_lib.nsd_loss_bilinear(C.byref(A), C.byref(At), _p(H), _p(G), k, seed, _p(loss),
                                   _p(dA), _p(dH), _p(ws), _nbytes(ws), _stream(stream)),
            "nsd_loss_bilinear")
+
+
+def nsd_loss_bilinear_noalloc(A: nsd_csr, At: nsd_csc, H, G, k, seed, loss, dA, dH,
+                              stream=None):
+    _check(_lib.nsd_loss_bilinear_noalloc(C.byref(A), C.byref(At), _p(H), _p(G), k, seed,
+                                          _p(loss), _p(dA), _p(dH), _stream(stream)),
+           "nsd_loss_bilinear_noalloc")
 
 
 def nsd_loss_mf(A: nsd_csr, At: nsd_csc, valT, U, V, k, seed, loss, dU, dV, ws, stream=None):
