@@ -80,7 +80,7 @@ def parse():
 KERNEL_SOURCE = {"frob_row": "segreduce.hip", "sgr_main": "segreduce.hip",
                  "sddmm": "segreduce.hip", "frob_col": "dual.hip", "dual": "dual.hip",
                  "mf": "dual.hip", "cp": "cp.hip", "sort": "build.hip", "jvp": "jvp.hip",
-                 "cpn": "cpn.hip"}
+                 "cpn": "cpn.hip", "perm": "perm.hip"}
 
 
 def source_digest(kernel=None):
@@ -165,11 +165,21 @@ def setup_gnn(d, dev, torch, nsd, ops):
     S = Setup()
     S.A, S.nnz, S.k = A, nnz, k
     S.step = lambda: nsd.nsd_loss_bilinear(A.desc, A.csc, H, G, k, 1.0, loss, dA, dH, ws)
-    S.kernels = {
-        # one column pass: colidx, rowind, perm, val (through perm) in, dA
-        # out; G and H read once, dH written once
-        "dual": 5 * 4 * nnz + 4 * k * (nr + 2 * nc),
-    }
+    if A.csc.to_csc.n:
+        S.kernels = {
+            # one column pass: colidx, rowind, the values in CSC order in and
+            # dA in CSC order out; G and H read once, dH written once
+            "dual": 4 * 4 * nnz + 4 * k * (nr + 2 * nc),
+            # each move of nnz values (before and after the pass): read once,
+            # written once
+            "perm": 2 * 4 * nnz,
+        }
+    else:
+        S.kernels = {
+            # one column pass: colidx, rowind, perm, val (through perm) in, dA
+            # out; G and H read once, dH written once
+            "dual": 5 * 4 * nnz + 4 * k * (nr + 2 * nc),
+        }
     return S
 
 

@@ -102,6 +102,19 @@ typedef struct nsd_plan {
     int32_t longest_chunks;    /* chunks of the longest segment (0: none is long) */
 } nsd_plan;
 
+/*
+ * A fixed permutation of n values split into two coalesced passes
+ * (nsd_permute_f32): dst[q] = src[perm[q]].  Built once per permutation by
+ * nsd_perm_plan_build into three caller arrays of n elements.
+ */
+typedef struct nsd_perm_plan {
+    int32_t n;                  /* elements */
+    int32_t tile;               /* span of either pass (source tile, destination bucket) */
+    const int32_t *stage;       /* [n] staging position of pass 1's output slot */
+    const uint16_t *src_local;  /* [n] source index within its tile of that slot */
+    const uint16_t *dst_local;  /* [n] destination offset within its bucket of staging slot */
+} nsd_perm_plan;
+
 /* Matrix CSR (Section 5.3, the matrix CSR storage `(len,pos,idx,val)`). */
 typedef struct nsd_csr {
     int32_t nrows, ncols, nnz;
@@ -120,6 +133,14 @@ typedef struct nsd_csc {
     const int32_t *rowind; /* [nnz], strictly increasing within a column */
     const int32_t *perm;   /* [nnz], CSR slot holding the same entry */
     nsd_plan plan;         /* plan over the columns (for reductions into columns) */
+    /* Optional (n = 0: absent) two-pass forms of perm, built once per pattern
+     * with nsd_perm_plan_build: to_csc moves values from CSR to CSC order
+     * (valT[q] = val[perm[q]], inverse = 0), to_csr moves them back
+     * (g[perm[q]] = gT[q], inverse = 1).  When both are present the column
+     * pass of nsd_loss_bilinear reads A's values and writes its sparse
+     * gradient in CSC order, moved by them, instead of one 4-byte access per
+     * entry through perm; its workspace then holds 3 nnz more floats. */
+    nsd_perm_plan to_csc, to_csr;
 } nsd_csc;
 
 /*
@@ -182,6 +203,7 @@ typedef struct nsd_ttv_plan {
     nsd_plan lplan;        /* plan over l */
 } nsd_ttv_plan;
 
+
 /* ----------------------------------------------------------------- info */
 
 /* Static string naming a status code. */
@@ -209,7 +231,8 @@ typedef enum nsd_kernel_id {
                                   (bilinear and SMVM losses) */
     NSD_KERNEL_SORT = 11,      /* radix-sort scatter pass of the builders */
     NSD_KERNEL_JVP = 12,       /* forward-mode tangent of the matrix product */
-    NSD_KERNEL_CPN = 13        /* order-N CP mode passes */
+    NSD_KERNEL_CPN = 13,       /* order-N CP mode passes */
+    NSD_KERNEL_PERM = 14       /* the two passes of a value permutation */
 } nsd_kernel_id;
 
 /*
@@ -306,6 +329,29 @@ nsd_status nsd_csr_to_csc(const nsd_csr *A, int32_t *colptr, int32_t *colidx,
 nsd_status nsd_coo_mode_index(int32_t nnz, int32_t dim, const int32_t *key,
                               int32_t *segptr, int32_t *segidx, int32_t *perm,
                               void *ws, size_t ws_bytes, void *stream);
+
+/* Bytes of `ws` nsd_perm_plan_build needs for n elements (host output). */
+nsd_status nsd_perm_plan_workspace_size(int32_t n, size_t *bytes);
+
+/*
+ * Plan of dst[q] = src[perm[q]] (inverse = 0) or of dst[perm[q]] = src[q]
+ * (inverse = 1), perm a permutation of [0, n) (device), for
+ * nsd_permute_f32: the permutation factored into two of bounded span (a
+ * two-digit radix permutation with digits of `tile` elements): pass 1 moves
+ * each source tile's values into the staging runs of their destination
+ * buckets, pass 2 places each bucket's values at their destinations.
+ * Outputs stage [n], src_local [n], dst_local [n] (caller arrays) and *plan
+ * (host).  NSD_ERR_BAD_FORMAT when perm is not a permutation.  Synchronous.
+ */
+nsd_status nsd_perm_plan_build(int32_t n, const int32_t *perm, int inverse, int32_t *stage,
+                               uint16_t *src_local, uint16_t *dst_local, nsd_perm_plan *plan,
+                               void *ws, size_t ws_bytes, void *stream);
+
+/* The plan's permutation applied to src: an exact fp32 copy in two
+ * coalesced passes; staging [n] is caller scratch; src and dst must not
+ * alias.  Async. */
+nsd_status nsd_permute_f32(const nsd_perm_plan *plan, const float *src, float *dst,
+                           float *staging, void *stream);
 
 /* dst[q] = src[perm[q]] for q < n: an exact fp32 copy (values into CSC or
  * mode order).  Async. */

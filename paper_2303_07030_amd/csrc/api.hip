@@ -76,10 +76,21 @@ static size_t resid_buf_bytes(const nsd_csr *A, int k) {
     return k > 64 ? round256((size_t)std::max(A->nnz, 1) * sizeof(float)) : 0;
 }
 
+// A CSC carrying both two-pass forms of its perm moves A's values to CSC
+// order and the sparse gradient back through them (three arrays of nnz
+// floats: the values, the gradient in CSC order, the staging of a move).
+static bool has_perm_plans(const nsd_csc *At) {
+    return At && At->nnz > 0 && At->to_csc.n == At->nnz && At->to_csr.n == At->nnz;
+}
+
+static size_t perm_bufs_bytes(const nsd_csr *A, const nsd_csc *At) {
+    return has_perm_plans(At) ? 3 * round256((size_t)A->nnz * sizeof(float)) : 0;
+}
+
 static size_t compute_ws_bytes(const nsd_csr *A, const nsd_csc *At, int k) {
     return part_region_bytes(A, At, k) + round256(loss_part_count(A, At, k) * sizeof(double)) +
            round256(std::max<size_t>(A->plan.nlong, 1) * sizeof(double)) +
-           resid_buf_bytes(A, k);
+           resid_buf_bytes(A, k) + perm_bufs_bytes(A, At);
 }
 
 struct ComputeWs {
@@ -88,6 +99,7 @@ struct ComputeWs {
     double *loss_part;
     double *seg_loss;
     float *rbuf;      // residual per stored entry (wide factorisation only)
+    float *valT, *gradT, *staging;  // with the CSC's perm plans only
 };
 
 static nsd_status carve_compute(void *ws, size_t ws_bytes, const nsd_csr *A, const nsd_csc *At,
@@ -104,6 +116,14 @@ static nsd_status carve_compute(void *ws, size_t ws_bytes, const nsd_csr *A, con
     out->seg_loss = reinterpret_cast<double *>(b);
     b += round256(std::max<size_t>(A->plan.nlong, 1) * sizeof(double));
     out->rbuf = resid_buf_bytes(A, k) ? reinterpret_cast<float *>(b) : nullptr;
+    b += resid_buf_bytes(A, k);
+    out->valT = out->gradT = out->staging = nullptr;
+    if (has_perm_plans(At)) {
+        const size_t one = round256((size_t)A->nnz * sizeof(float));
+        out->valT = reinterpret_cast<float *>(b);
+        out->gradT = reinterpret_cast<float *>(b + one);
+        out->staging = reinterpret_cast<float *>(b + 2 * one);
+    }
     return NSD_OK;
 }
 
@@ -218,15 +238,29 @@ static int64_t bilinear_loss_parts(const nsd_csr *A, const nsd_csc *At, int k) {
 static nsd_status finish_loss(const SddmmParams &p, double *loss, hipStream_t st);
 
 // The bilinear layer L = sum (A H) o G with its gradients, given the chunk
-// partials of the column plan and the loss partials.
+// partials of the column plan and the loss partials; with valT, gradT and
+// staging (nnz floats each) A's values are moved to CSC order and the sparse
+// gradient back by the CSC's two-pass permutations.
 static nsd_status bilinear_run(const nsd_csr *A, const nsd_csc *At, const float *H,
                                const float *G, int k, float seed, double *loss, float *dA,
-                               float *dH, float *part_col, double *loss_part, hipStream_t st) {
+                               float *dH, float *part_col, double *loss_part, hipStream_t st,
+                               float *valT = nullptr, float *gradT = nullptr,
+                               float *staging = nullptr) {
     if (A->nnz > 0) {
         // one pass over the columns: own row H_j, gathered row G_i:
         // dA[p] = seed <G_i, H_j>, loss = sum_p A_p <G_i, H_j>, dH = seed A^T G
-        const DualPass pass = col_dual(A, At, G, H, k, seed, dH, part_col, dA, seed, true);
-        if (col_dual_ok(pass)) return col_dual_loss(pass, loss_part, loss, st);
+        DualPass pass = col_dual(A, At, G, H, k, seed, dH, part_col, dA, seed, true);
+        if (col_dual_ok(pass)) {
+            if (!valT) return col_dual_loss(pass, loss_part, loss, st);
+            // values read and the gradient written in CSC order: the pass's
+            // entry positions are then its own slots
+            NSD_TRY(nsd_permute_f32(&At->to_csc, A->val, valT, staging, st));
+            pass.s.w = valT;
+            pass.s.wperm = nullptr;
+            pass.sdd = gradT;
+            NSD_TRY(col_dual_loss(pass, loss_part, loss, st));
+            return nsd_permute_f32(&At->to_csr, gradT, dA, staging, st);
+        }
     }
     // dA = seed * <G_i, H_j>; loss = sum_p A_p <G_i, H_j>
     SddmmParams sp = sddmm_params(A, G, H, k, seed, dA);
@@ -401,7 +435,7 @@ nsd_status nsd_loss_bilinear(const nsd_csr *A, const nsd_csc *At, const float *H
     ComputeWs w;
     NSD_TRY(carve_compute(ws, ws_bytes, A, At, k, &w));
     return bilinear_run(A, At, H, G, k, seed, loss, dA, dH, w.part_col, w.loss_part,
-                        as_stream(stream));
+                        as_stream(stream), w.valT, w.gradT, w.staging);
 }
 
 nsd_status nsd_loss_bilinear_noalloc(const nsd_csr *A, const nsd_csc *At, const float *H,

@@ -27,13 +27,19 @@ NSD_ERR_HIP = 7
 NSD_DUP_SUM = 0
 NSD_DUP_ERROR = 1
 KERNEL_IDS = {"sgr_main": 1, "sgr_fix": 2, "sddmm": 3, "frob_row": 4, "frob_col": 5, "mf": 6,
-              "cp": 7, "loss": 8, "ttv": 9, "dual": 10, "sort": 11, "jvp": 12, "cpn": 13}
+              "cp": 7, "loss": 8, "ttv": 9, "dual": 10, "sort": 11, "jvp": 12, "cpn": 13,
+              "perm": 14}
 
 
 class NsdError(RuntimeError):
     def __init__(self, status: int, func: str, msg: str):
         super().__init__(f"{func}: {status_name(status)}: {msg}")
         self.status = status
+
+
+class nsd_perm_plan(C.Structure):
+    _fields_ = [("n", C.c_int32), ("tile", C.c_int32), ("stage", C.c_void_p),
+                ("src_local", C.c_void_p), ("dst_local", C.c_void_p)]
 
 
 class nsd_plan(C.Structure):
@@ -54,7 +60,8 @@ class nsd_csr(C.Structure):
 class nsd_csc(C.Structure):
     _fields_ = [("nrows", C.c_int32), ("ncols", C.c_int32), ("nnz", C.c_int32),
                 ("colptr", C.c_void_p), ("colidx", C.c_void_p), ("rowind", C.c_void_p),
-                ("perm", C.c_void_p), ("plan", nsd_plan)]
+                ("perm", C.c_void_p), ("plan", nsd_plan), ("to_csc", nsd_perm_plan),
+                ("to_csr", nsd_perm_plan)]
 
 
 class nsd_coo3_mode(C.Structure):
@@ -117,6 +124,10 @@ _SIGS = {
     "nsd_plan_build": (C.c_int, [_I, _I, _P, _I, _P, _P, _P, _P, _P, _P, _P,
                                  C.POINTER(nsd_plan), _P, _SZ, _P]),
     "nsd_build_workspace_size": (C.c_int, [_I, _I, C.POINTER(_SZ)]),
+    "nsd_perm_plan_workspace_size": (C.c_int, [_I, C.POINTER(_SZ)]),
+    "nsd_perm_plan_build": (C.c_int, [_I, _P, C.c_int, _P, _P, _P, C.POINTER(nsd_perm_plan),
+                                      _P, _SZ, _P]),
+    "nsd_permute_f32": (C.c_int, [C.POINTER(nsd_perm_plan), _P, _P, _P, _P]),
     "nsd_csr_expand_rows": (C.c_int, [_I, _I, _P, _P, _P]),
     "nsd_coo_to_csr": (C.c_int, [_I, _I, _I, _P, _P, _P, C.c_int, _P, _P, _P, _P, _P,
                                  C.POINTER(_I), _P, _SZ, _P]),
@@ -268,6 +279,28 @@ def nsd_plan_build(nseg, nnz, segptr, item_len, item_ptr, long_seg, long_first, 
                       huge_idx=huge_idx, chunk_item=chunk_item, chunk_ord=chunk_ord,
                       empty_seg=empty_seg)
     return plan
+
+
+def nsd_perm_plan_workspace_size(n: int) -> int:
+    b = _SZ(0)
+    _check(_lib.nsd_perm_plan_workspace_size(n, C.byref(b)), "nsd_perm_plan_workspace_size")
+    return b.value
+
+
+def nsd_perm_plan_build(n, perm, inverse, stage, src_local, dst_local, ws,
+                        stream=None) -> nsd_perm_plan:
+    plan = nsd_perm_plan()
+    _check(_lib.nsd_perm_plan_build(n, _p(perm), int(inverse), _p(stage), _p(src_local),
+                                    _p(dst_local), C.byref(plan), _p(ws), _nbytes(ws),
+                                    _stream(stream)),
+           "nsd_perm_plan_build")
+    plan._keep = dict(stage=stage, src_local=src_local, dst_local=dst_local)
+    return plan
+
+
+def nsd_permute_f32(plan: nsd_perm_plan, src, dst, staging, stream=None):
+    _check(_lib.nsd_permute_f32(C.byref(plan), _p(src), _p(dst), _p(staging), _stream(stream)),
+           "nsd_permute_f32")
 
 
 def nsd_build_workspace_size(n: int, max_key: int) -> int:

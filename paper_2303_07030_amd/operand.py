@@ -33,10 +33,30 @@ def build_plan(nseg, nnz, segptr, item_len, device, stream=None):
                               arr(nseg), ws, stream)
 
 
+# Patterns with at least this many entries get the two-pass forms of their
+# CSC permutation (nsd_perm_plan_build) unless asked otherwise: below it the
+# two extra launches of a move cost more than the scattered 4-byte accesses
+# they replace.
+PERM_PLAN_MIN_NNZ = 4_000_000
+
+
+def build_perm_plan(n, perm, inverse, device, stream=None):
+    """Two-pass form of a permutation (device arrays kept alive on it)."""
+    stage = torch.empty(max(n, 1), dtype=torch.int32, device=device)
+    src_local = torch.empty(max(n, 1), dtype=torch.uint16, device=device)
+    dst_local = torch.empty(max(n, 1), dtype=torch.uint16, device=device)
+    ws = torch.empty(max(nsd.nsd_perm_plan_workspace_size(n), 256), dtype=torch.uint8,
+                     device=device)
+    return nsd.nsd_perm_plan_build(n, perm, inverse, stage, src_local, dst_local, ws, stream)
+
+
 class DeviceCsr:
     def __init__(self, nrows: int, ncols: int, rowptr, colind, val, device="cuda",
                  build_csc: bool = True, stream=None, k_hint: int = 64, item_len=None,
-                 rowidx=None):
+                 rowidx=None, perm_plans=None):
+        """perm_plans: build the two-pass forms of the CSC permutation (None:
+        when nnz >= PERM_PLAN_MIN_NNZ)."""
+        self.perm_plans = perm_plans
         self.nrows, self.ncols = int(nrows), int(ncols)
         self.rowptr = _dev(rowptr, torch.int32, device)
         self.colind = _dev(colind, torch.int32, device)
@@ -70,6 +90,14 @@ class DeviceCsr:
                                 self.perm)
         self.col_plan = build_plan(self.ncols, self.nnz, self.colptr, self.item_len, dev, stream)
         self.csc.plan = self.col_plan
+        plans = self.perm_plans
+        if plans is None:
+            plans = self.nnz >= PERM_PLAN_MIN_NNZ
+        if plans and self.nnz > 0:
+            # the descriptor holds copies of the plans; their arrays live here
+            self.to_csc = build_perm_plan(self.nnz, self.perm, 0, dev, stream)
+            self.to_csr = build_perm_plan(self.nnz, self.perm, 1, dev, stream)
+            self.csc.to_csc, self.csc.to_csr = self.to_csc, self.to_csr
         return self.csc
 
     def workspace(self, k: int):
