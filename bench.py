@@ -36,6 +36,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 ITEM_LEN = None  # work-plan item length; None = the library's choice
+CP_FIBERS = False  # order-N CP with its fiber level
 PROBE_EVERY = 4  # timed steps per step whose dominant-kernel launches are bracketed
 WORKLOAD_NAMES = {
     "spmm": "spmm_grad_100k_1M_zipf1.1_k64",
@@ -66,6 +67,9 @@ def parse():
     ap.add_argument("--replicate", type=int, default=0,
                     help="input replicate (0: the headline inputs; 1, 2: same recipe, other "
                          "seeds, for variance)")
+    ap.add_argument("--cp-fibers", action="store_true",
+                    help="order-N CP with its fiber level (the factor row of each run of equal "
+                         "coordinate gathered once)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--profile-only", action="store_true",
                     help="warmup + steps only (for rocprofv3), no JSON line")
@@ -340,7 +344,7 @@ def setup_jvp(d, dev, torch, nsd, ops):
 def setup_cp4(d, dev, torch, nsd, ops):
     """CP gradient of an order-4 tensor through the order-N entry point."""
     X = ops.DeviceCooN(d["dims"], d["coords"], d["val"], device=dev, rank_hint=d["rank"],
-                       item_len=ITEM_LEN)
+                       item_len=ITEM_LEN, fibers=CP_FIBERS)
     R, nnz, N = d["rank"], X.nnz, len(d["dims"])
     F = [torch.from_numpy(f).to(dev) for f in d["F"]]
     dF = [torch.empty((X.dims[m], R), dtype=torch.float32, device=dev) for m in range(N)]
@@ -397,8 +401,9 @@ def collect(torch, nsd, starts, stops):
 
 def main():
     args = parse()
-    global ITEM_LEN
+    global ITEM_LEN, CP_FIBERS
     ITEM_LEN = args.item_len
+    CP_FIBERS = args.cp_fibers
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): the library measures "
               "one GPU's share; a multi-GPU layout is described, not implemented",

@@ -653,6 +653,15 @@ typedef struct nsd_coon_mode {
     const float *val;                       /* [nnz] */
     const int32_t *perm;                    /* [nnz] */
     nsd_plan plan;
+    /* Second level of the compressed-fiber tree (0: none).  With 1, the
+     * slices' entries are taken as fibers: runs of equal coordinate of the
+     * fiber mode (mode 1 for mode 0, else mode 0), as lexicographic storage
+     * gives them.  The pass then gathers that mode's factor row once per
+     * fiber, keeps the fiber's partial product with the slice's own row and
+     * adds the fiber's sum once into the slice, instead of per entry.  Any
+     * order of entries gives the same values (up to rounding); long runs
+     * give the savings. */
+    int32_t fiber;
 } nsd_coon_mode;
 
 typedef struct nsd_coon {

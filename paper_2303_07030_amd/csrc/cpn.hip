@@ -35,6 +35,7 @@ struct CpnMode {
     const int32_t *perm = nullptr;   // input position of each slot (pass 0)
     float *resid = nullptr;          // dX (pass 0)
     float seed = 1.f;
+    int32_t fiber = 0;               // other[0] is the fiber coordinate (a run level)
     int32_t item_blocks = 0, empty_blocks = 0;
 };
 
@@ -154,13 +155,174 @@ struct CpnSlot {
     }
 };
 
+// The same pass with a fiber level (the second level of a compressed-fiber
+// tree): entries of a slice come in runs of equal coordinate other[0] (a
+// fiber), whose factor row fac[0] is gathered once per fiber.  With
+// t' = the product of the other N - 2 gathered rows,
+//   model = <own o fac0[fiber], t'>,  fiber sum += R t',
+// and at the fiber's end the slice's sum gets fac0[fiber] o (fiber sum),
+// which is sum R (fac0 o t') regrouped by fiber.  The open fiber keeps its
+// factor row fv and the partial product pv = own o fv, so an entry in it
+// needs N - 2 gathers and one dot product.
+template <int N, int VEC, int G, int U>
+struct CpnFiberSlot {
+    const CpnMode<N> &m;
+    int64_t s, k, b0;
+    int lane, g, col;
+    bool on, first_mode;
+    int row;
+    bool carry;
+    bool pend = false;
+    int fib = -1;          // coordinate of the open fiber (-1: none open)
+    Vec<VEC> acc, ownv, fv, pv, accf;
+    double &lsum;
+
+    __device__ __forceinline__ CpnFiberSlot(const CpnMode<N> &m_, int64_t s_, int lane_, bool fm,
+                                            double &ls)
+        : m(m_), s(s_), k(m_.s.k), lane(lane_), g(lane_ % G), col((lane_ % G) * VEC),
+          first_mode(fm), lsum(ls) {
+        const SgrParams &a = m.s;
+        on = col < a.k;
+        const int64_t a0 = a.plan.item_ptr[s];
+        b0 = a.plan.item_ptr[s + 1];
+        row = a.segidx[a0];
+        carry = a0 > 0 && a.segidx[a0 - 1] == row;
+        acc.zero();
+        accf.zero();
+        fv.zero();
+        pv.zero();
+        if (on) ownv.load(m.own + (int64_t)row * k + col);
+        else ownv.zero();
+    }
+
+    // the open fiber's sum into the slice's sum
+    __device__ __forceinline__ void close_fiber() {
+        if (fib >= 0) {
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) acc.v[e] = __builtin_fmaf(fv.v[e], accf.v[e], acc.v[e]);
+            accf.zero();
+            fib = -1;
+        }
+    }
+
+    __device__ __forceinline__ void flush() {
+        if (carry) {
+            pend = true;
+        } else if (on) {
+            Vec<VEC> t = acc;
+            t.scale(m.s.alpha);
+            t.store(m.s.out + (int64_t)row * k + col);
+        }
+    }
+
+    __device__ __forceinline__ void batch(int64_t p, const int (&r)[U], const int (&c)[N - 1][U],
+                                          const float (&x)[U], const int (&pp)[U]) {
+        bool same = true, samef = true;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            same = same && r[u] == row;
+            samef = samef && c[0][u] == fib;
+        }
+        samef = samef && same;
+        const int cl = on ? col : 0;
+        Vec<VEC> t[U], h[N - 2][U], ow[U], fr[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if constexpr (N >= 3) t[u].load(m.fac[1] + (int64_t)c[1][u] * k + cl);
+#pragma unroll
+            for (int f = 2; f < N - 1; ++f) h[f - 2][u].load(m.fac[f] + (int64_t)c[f][u] * k + cl);
+        }
+        if (!samef) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) fr[u].load(m.fac[0] + (int64_t)c[0][u] * k + cl);
+        }
+        if (!same) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) ow[u].load(m.own + (int64_t)r[u] * k + cl);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+#pragma unroll
+            for (int f = 0; f < N - 3; ++f) {
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) t[u].v[e] *= h[f][u].v[e];
+            }
+            if (!on) t[u].zero();
+        }
+        float d[U];
+        if (samef) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) d[u] = pv.dot(t[u]);
+        } else {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const Vec<VEC> &o = same ? ownv : ow[u];
+                Vec<VEC> q;
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) q.v[e] = o.v[e] * fr[u].v[e];
+                d[u] = q.dot(t[u]);
+            }
+        }
+        float res[U];
+        if constexpr (G == 1) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) res[u] = p + u < b0 ? x[u] - d[u] : 0.f;
+        } else {
+            float mv[U];
+            slot_totals<G, U>(transpose_reduce<G, U>(d, lane), lane, mv);
+#pragma unroll
+            for (int u = 0; u < U; ++u) res[u] = p + u < b0 ? x[u] - mv[u] : 0.f;
+        }
+        if (first_mode && g == 0) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                if (p + u < b0) {
+                    m.resid[pp[u]] = m.seed * res[u];
+                    lsum += 0.5 * (double)res[u] * res[u];
+                }
+            }
+        }
+        if (samef) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) accf.fma(res[u], t[u]);
+        } else {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                if (r[u] != row) {
+                    close_fiber();
+                    flush();
+                    row = r[u];
+                    carry = false;
+                    acc.zero();
+                }
+                if (c[0][u] != fib) {
+                    close_fiber();
+                    fib = c[0][u];
+                    fv = fr[u];
+                }
+                accf.fma(res[u], t[u]);
+            }
+            if (!same && on) ownv = ow[U - 1];
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) pv.v[e] = ownv.v[e] * fv.v[e];
+        }
+    }
+
+    __device__ __forceinline__ void finish() {
+        const SgrParams &a = m.s;
+        close_fiber();
+        if (b0 == a.nnz || a.segidx[b0] != row) flush();
+        else pend = true;
+    }
+};
+
 // One slot's walk over item s of a mode pass; G >= 8 reads the metadata in
 // tiles of G entries, narrower slots per entry and lane.
-template <int N, int VEC, int G, int U>
+template <int N, int VEC, int G, int U, class Slot>
 __device__ __forceinline__ int cpn_walk(const CpnMode<N> &m, int64_t s, int lane,
                                         bool first_mode, double &lsum, Vec<VEC> &part_acc) {
     const SgrParams &a = m.s;
-    CpnSlot<N, VEC, G, U> st(m, s, lane, first_mode, lsum);
+    Slot st(m, s, lane, first_mode, lsum);
     const int64_t a0 = a.plan.item_ptr[s], b0 = st.b0;
     // Fields of entry q, past the item those of its last entry (every load
     // unconditional, so none is consumed before its batch); the batch zeroes
@@ -245,8 +407,14 @@ __device__ __forceinline__ void cpn_block(const CpnMode<N> &m, int b, bool first
         Vec<VEC> pacc;
         pacc.zero();
         int pseg = -1;
-        if (s < m.s.plan.nitems)
-            pseg = cpn_walk<N, VEC, G, U>(m, s, lane, first_mode, lsum, pacc);
+        if (s < m.s.plan.nitems) {
+            if (m.fiber)
+                pseg = cpn_walk<N, VEC, G, U, CpnFiberSlot<N, VEC, G, U>>(m, s, lane, first_mode,
+                                                                          lsum, pacc);
+            else
+                pseg = cpn_walk<N, VEC, G, U, CpnSlot<N, VEC, G, U>>(m, s, lane, first_mode, lsum,
+                                                                     pacc);
+        }
         store_chunk_partial<VEC, G>(pseg, pacc, m.s.part, m.s.plan.chunk_ord, s, m.s.k, g * VEC,
                                     g * VEC < m.s.k);
     } else {
@@ -278,7 +446,11 @@ __global__ __launch_bounds__(kBlock) void cpn_kernel(CpnParams<N> f) {
 
 template <int G>
 constexpr int cpn_unroll() {
+#ifdef NSD_CPN_UNROLL
+    return reduce_unroll<G, NSD_CPN_UNROLL>();
+#else
     return reduce_unroll<G, (G >= 64 || G == 1) ? 4 : 2>();
+#endif
 }
 
 template <int N, int VEC, int G>
@@ -446,6 +618,15 @@ static nsd_status cpn_run(const nsd_coon *X, const float *const *F, int32_t rank
         for (int o = 0; o < N - 1; ++o) {
             m.other[o] = md.idx[o];
             m.fac[o] = F[(n + 1 + o) % N];
+        }
+        m.fiber = md.fiber ? 1 : 0;
+        if (m.fiber) {
+            // the fiber mode (mode 1 for mode 0, else mode 0) first: the
+            // product over the other rows does not depend on their order
+            const int fm = n == 0 ? 1 : 0;
+            const int of = (fm - n - 1 + N) % N;
+            std::swap(m.other[0], m.other[of]);
+            std::swap(m.fac[0], m.fac[of]);
         }
         m.own = F[n];
         m.perm = md.perm;

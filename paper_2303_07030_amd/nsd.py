@@ -80,7 +80,7 @@ MAX_ORDER = 6
 class nsd_coon_mode(C.Structure):
     _fields_ = [("mode", C.c_int32), ("segptr", C.c_void_p), ("segidx", C.c_void_p),
                 ("idx", C.c_void_p * (MAX_ORDER - 1)), ("val", C.c_void_p),
-                ("perm", C.c_void_p), ("plan", nsd_plan)]
+                ("perm", C.c_void_p), ("plan", nsd_plan), ("fiber", C.c_int32)]
 
 
 class nsd_coon(C.Structure):

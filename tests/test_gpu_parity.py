@@ -892,10 +892,11 @@ def test_loss_cpn_small_order4_workload(nsd, orc):
     check_cpn(orc, d["dims"], d["coords"], d["val"], d["F"], d["rank"], got)
 
 
+@pytest.mark.parametrize("fibers", [True, False])
 @pytest.mark.parametrize("dims,rank", [((9, 7, 5), 12), ((6, 5, 4, 7, 3), 8),
                                        ((4, 3, 5, 2, 3, 4), 5), ((40, 3, 2, 50), 64),
-                                       ((30, 2, 2, 2), 256)])
-def test_loss_cpn_orders_and_ranks(nsd, orc, dims, rank):
+                                       ((30, 2, 2, 2), 256), ((3, 4, 200, 5), 32)])
+def test_loss_cpn_orders_and_ranks(nsd, orc, dims, rank, fibers):
     # skewed and tiny modes (long slices, chunked), scalar ranks (5), wide
     # ranks (256: a full wave per slot), empty slices
     from paper_2303_07030_amd.operand import DeviceCooN
@@ -906,9 +907,40 @@ def test_loss_cpn_orders_and_ranks(nsd, orc, dims, rank):
     coords = [c.astype(np.int32) for c in np.unravel_index(keys, dims)]
     val = rng.standard_normal(nnz).astype(np.float32)
     F = [(0.3 * rng.standard_normal((dd, rank))).astype(np.float32) for dd in dims]
-    X = DeviceCooN(dims, coords, val, rank_hint=rank, item_len=16)
+    X = DeviceCooN(dims, coords, val, rank_hint=rank, item_len=16, fibers=fibers)
     got = run_cpn(nsd, X, F, rank, seed=0.5)
     check_cpn(orc, dims, coords, val, F, rank, got, seed=0.5)
+
+
+def test_loss_cpn_fibers_in_any_entry_order(nsd, orc):
+    """The fiber level regroups by runs of equal coordinate, so entries in an
+    order with short runs (mode indexes built over an unsorted input, not the
+    operand's lexicographic storage) give the same values to the bar."""
+    from paper_2303_07030_amd.operand import DeviceCooN
+    rng = np.random.default_rng(77)
+    dims, rank = (6, 5, 40, 7), 16
+    size = int(np.prod(dims))
+    keys = rng.choice(size, size=2500, replace=False)
+    coords = [c.astype(np.int32) for c in np.unravel_index(keys, dims)]
+    val = rng.standard_normal(2500).astype(np.float32)
+    F = [(0.3 * rng.standard_normal((d, rank))).astype(np.float32) for d in dims]
+    X = DeviceCooN(dims, coords, val, rank_hint=rank, item_len=8, fibers=True)
+    # scramble the entry order of every mode index within its slices: the
+    # per-entry arrays are permuted together, slices (and the plans) stay
+    keep = []
+    for m in range(len(dims)):
+        md, arrs = X.desc.mode[m], X.modes[m]
+        segptr = host(arrs["segptr"])
+        pi = np.concatenate([segptr[i] + rng.permutation(segptr[i + 1] - segptr[i])
+                             for i in range(dims[m])]).astype(np.int64)
+        new = {f: dev(host(arrs[f])[: X.nnz][pi]) for f in ("perm", "val")}
+        new["idx"] = [dev(host(t)[: X.nnz][pi]) for t in arrs["idx"]]
+        md.perm, md.val = new["perm"].data_ptr(), new["val"].data_ptr()
+        for o, t in enumerate(new["idx"]):
+            md.idx[o] = t.data_ptr()
+        keep.append(new)
+    got = run_cpn(nsd, X, F, rank)
+    check_cpn(orc, dims, coords, val, F, rank, got)
 
 
 def test_loss_cpn_order3_equals_cp(nsd, orc):
@@ -919,7 +951,7 @@ def test_loss_cpn_order3_equals_cp(nsd, orc):
     d = synth.make("cp", "small")
     F = [d["F1"], d["F2"], d["F3"]]
     X3 = DeviceCoo3(d["dims"], d["i"], d["j"], d["k"], d["val"], item_len=24)
-    XN = DeviceCooN(d["dims"], [d["i"], d["j"], d["k"]], d["val"], item_len=24)
+    XN = DeviceCooN(d["dims"], [d["i"], d["j"], d["k"]], d["val"], item_len=24, fibers=False)
     a = run_cp(nsd, X3, F, d["rank"])
     b = run_cpn(nsd, XN, F, d["rank"])
     check_cpn(orc, d["dims"], [d["i"], d["j"], d["k"]], d["val"], F, d["rank"], b)

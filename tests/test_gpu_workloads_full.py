@@ -361,12 +361,13 @@ def test_cp_full_workload(nsd, orc):
 
 # ------------------------------------------------ order-4 CP decomposition
 
-def test_cp4_full_workload(nsd, orc):
+@pytest.mark.parametrize("fibers", [False, True])
+def test_cp4_full_workload(nsd, orc, fibers):
     from paper_2303_07030_amd import synth
     from paper_2303_07030_amd.operand import DeviceCooN
     d = synth.make("cp4")
     dims, R, coords, val, F = d["dims"], d["rank"], d["coords"], d["val"], d["F"]
-    X = DeviceCooN(dims, coords, val, rank_hint=R)
+    X = DeviceCooN(dims, coords, val, rank_hint=R, fibers=fibers)
     loss = torch.empty(1, dtype=torch.float64, device="cuda")
     dX = torch.empty(X.nnz, dtype=torch.float32, device="cuda")
     dF = [torch.empty((dd, R), dtype=torch.float32, device="cuda") for dd in dims]
