@@ -70,6 +70,9 @@ def parse():
     ap.add_argument("--cp-fibers", action="store_true",
                     help="order-N CP with its fiber level (the factor row of each run of equal "
                          "coordinate gathered once)")
+    ap.add_argument("--tangents", type=int, default=1, metavar="M",
+                    help="jvp workload: M tangents per step, in one nsd_spmm_jvp_batch call "
+                         "(J V for a batch of M directions) when M > 1")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--profile-only", action="store_true",
                     help="warmup + steps only (for rocprofv3), no JSON line")
@@ -335,9 +338,23 @@ def setup_jvp(d, dev, torch, nsd, ops):
     ws = A.workspace(2 * k)
     S = Setup()
     S.A, S.nnz, S.k = A, nnz, k
-    S.step = lambda: nsd.nsd_spmm_jvp(A.desc, dA, B, dB, k, C, dC, ws)
-    # rowidx, colind, val, dA in; B and dB read once, C and dC written once
-    S.kernels = {"jvp": 4 * 4 * nnz + 2 * 4 * k * (nr + nc)}
+    M = d.get("tangents", 1)
+    if M == 1:
+        S.step = lambda: nsd.nsd_spmm_jvp(A.desc, dA, B, dB, k, C, dC, ws)
+        # rowidx, colind, val, dA in; B and dB read once, C and dC written once
+        S.kernels = {"jvp": 4 * 4 * nnz + 2 * 4 * k * (nr + nc)}
+        return S
+    # a batch of M tangents: groups of four per launch, each reading A's
+    # entries and B once and, per tangent, dA_t and dB_t once and writing
+    # dC_t once (C with the first group)
+    dC = torch.empty((M, nr, k), dtype=torch.float32, device=dev)
+    ws = torch.empty(nsd.nsd_spmm_jvp_batch_workspace_size(A.desc, k), dtype=torch.uint8,
+                     device=dev)
+    S.nnz = nnz * M
+    S.step = lambda: nsd.nsd_spmm_jvp_batch(A.desc, M, dA, B, dB, k, C, dC, ws)
+    groups = [min(4, M - g) for g in range(0, M, 4)]
+    per = [3 * 4 * nnz + 4 * k * nc + g * (4 * nnz + 4 * k * (nc + nr)) for g in groups]
+    S.kernels = {"jvp": (sum(per) + 4 * k * nr) / len(groups)}
     return S
 
 
@@ -424,8 +441,10 @@ def main():
                    replicate=args.replicate)
     if args.workload == "jvp":
         g = synth.streams("spmm", args.replicate)[3]  # the fourth stream: the tangents
-        d["dval"] = g.standard_normal(len(d["val"]), dtype=np.float32)
-        d["dB"] = g.standard_normal(d["B"].shape, dtype=np.float32)
+        M = d["tangents"] = args.tangents
+        lead = () if M == 1 else (M,)
+        d["dval"] = g.standard_normal(lead + (len(d["val"]),), dtype=np.float32)
+        d["dB"] = g.standard_normal(lead + d["B"].shape, dtype=np.float32)
     gen_s = time.perf_counter() - t0
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -524,6 +543,9 @@ def main():
                   args.workload, "gradient nonzeros/sec (forward+backward)")
     if args.workload == "jvp":
         metric = "tangent nonzeros/sec (forward-mode dC = dA B + A dB)"
+        if args.tangents > 1:
+            metric = (f"tangent nonzeros/sec (J V for a batch of {args.tangents} tangents "
+                      "dC_t = dA_t B + A dB_t; nnz x tangents per step)")
     out = {
         "metric": metric,
         "value": round(S.nnz / (ms_per_step * 1e-3), 1),
@@ -535,7 +557,8 @@ def main():
         "config": {"workload": WORKLOAD_NAMES[args.workload] if args.size == "full"
                    else f"{args.workload}_{args.size}", "replicate": args.replicate,
                    "nnz": S.nnz, "k": S.k,
-                   "item_len": S.A.item_len if S.A is not None else None},
+                   "item_len": S.A.item_len if S.A is not None else None,
+                   **({"tangents": args.tangents} if args.workload == "jvp" else {})},
         "roofline": roofline,
         "kernels": kernels,
         "preprocess_ms": round(prep_ms, 2), "generate_s": round(gen_s, 1),
@@ -739,7 +762,7 @@ def _cpu_leg(args, d, threads):
     if w in ("spmm", "spmv", "gnn", "batax", "jvp"):
         nrows, ncols = s["nrows"], s["ncols"]
         rows = np.repeat(np.arange(nrows, dtype=np.int32), np.diff(s["rowptr"]))
-        nnz = len(s["colind"])
+        nnz = len(s["colind"]) * s.get("tangents", 1)
     elif w in ("mf", "build"):
         nnz = len(s["row"])
     elif w == "cp4":
@@ -782,8 +805,11 @@ def _cpu_leg(args, d, threads):
                 oracle.cpn_grad(D, s["F"], s["rank"], m)
         elif w == "jvp":
             D = dok((nrows, ncols), (rows, s["colind"]), s["val"])
-            dD = dok((nrows, ncols), (rows, s["colind"]), s["dval"])
-            oracle.spmm_jvp(D, dD, s["B"], s["dB"], s["k"])
+            M = s.get("tangents", 1)
+            for t in range(M):
+                dv, dB = (s["dval"], s["dB"]) if M == 1 else (s["dval"][t], s["dB"][t])
+                dD = dok((nrows, ncols), (rows, s["colind"]), dv)
+                oracle.spmm_jvp(D, dD, s["B"], dB, s["k"])
         elif w == "batax":
             D = dok((nrows, ncols), (rows, s["colind"]), s["val"])
             one_pass.nk = len(oracle.batax_jacobian(D, s["beta"])[1])

@@ -635,6 +635,31 @@ nsd_status nsd_axpby(int64_t n, float alpha, const float *x, float beta, float *
  */
 nsd_status nsd_diag_keys(const nsd_csr *A, float alpha, float *out, void *stream);
 
+/*
+ * A product taken key by key (Section 5: what multiplication normalisation
+ * leaves of a term in which no index is summed): for i in [0, n)
+ *     y[yi] = alpha * s1 * s2 * x1[i] * x2[x2i] + beta * y[yi],
+ *     yi = y_idx ? y_idx[i] : i,   x2i = x2_idx ? x2_idx[i] : i.
+ * s1, s2: device doubles, reals of a program (inputs or results; NULL: 1).
+ * x1, x2: device floats (NULL: ones), x1 aligned with the n keys; x2_idx
+ * gathers x2 (a dense operand read at each key's row, column or index).
+ * y_idx scatters into a dense y and must hold n distinct indices (each
+ * output is written once).  beta == 0: y is not read.  The product is
+ * formed in double and rounded once.  The Jacobians of the vector kernels
+ * of Section 7.1 and of matrix-valued programs on a matrix's keys reduce to
+ * this.  Async.
+ */
+nsd_status nsd_scale(int64_t n, double alpha, const double *s1, const double *s2,
+                     const float *x1, const float *x2, const int32_t *x2_idx, float beta,
+                     float *y, const int32_t *y_idx, void *stream);
+
+/*
+ * The same for one real: y[0] = alpha * s1 * s2 * x + beta * y[0] on device
+ * doubles (s1, s2, x NULL: 1; beta == 0: y is not read).  Async.
+ */
+nsd_status nsd_scale_real(double alpha, const double *s1, const double *s2, const double *x,
+                          double beta, double *y, void *stream);
+
 /* ---------------------------------------------------------------------------
  * Order-N sparse tensors and the CP gradient for orders 3 to NSD_MAX_ORDER
  * (the order-N form of the nested-dictionary tensor of Section 3).
@@ -702,6 +727,24 @@ nsd_status nsd_loss_cpn(const nsd_coon *X, const float *const *F, int32_t rank, 
 nsd_status nsd_spmm_jvp(const nsd_csr *A, const float *dAval, const float *B, const float *dB,
                         int32_t k, float *C, float *dC, void *ws, size_t ws_bytes,
                         void *stream);
+
+/*
+ * A batch of m tangents of C = A B at once (Section 4.2: the tangent is a
+ * tensor with one more key, the batch index t; this is J V for the m
+ * columns of V):
+ *     dC_t = dA_t B + A dB_t,   t = 0 .. m - 1.
+ * Tangents are taken in groups of four: each group reads A and the rows of
+ * B once for all of its tangents.  dAval: [m x nnz], tangent t's values in
+ * A's storage order (NULL: every dA_t = 0).  dB: [m x ncols x k] (NULL:
+ * every dB_t = 0).  C: [nrows x k], computed when not NULL.  dC:
+ * [m x nrows x k], fully overwritten.  Any k >= 1, m >= 0.
+ * Workspace: nsd_spmm_jvp_batch_workspace_size bytes (independent of m).
+ * Async.
+ */
+nsd_status nsd_spmm_jvp_batch_workspace_size(const nsd_csr *A, int32_t k, size_t *bytes);
+nsd_status nsd_spmm_jvp_batch(const nsd_csr *A, int32_t m, const float *dAval, const float *B,
+                              const float *dB, int32_t k, float *C, float *dC, void *ws,
+                              size_t ws_bytes, void *stream);
 
 /* ---------------------------------------------------------------------------
  * Jacobian of the BATAX kernel f(j) = sum_{i,k} beta A(i,j) A(i,k) x(k) with

@@ -580,3 +580,22 @@ def jacobian_tensorized(program, env, wrt):
         return {}
     return {p: float(v) for p, v in (leaves(r) if isinstance(r, dict) else [((), r)])
             if v is not ZERO}
+
+
+def jvp_tensorized(program, env, tangents):
+    """The tensorized forward mode with a batch of tangents (Section 4.2: the
+    tangent of an input may carry tau levels after its own keys; with tau a
+    vector of m directions, one evaluation gives J V): every free variable v
+    gets v' = tangents[v] (v's key paths followed by the batch key t) when
+    given, else zero, and the tangent of the program is evaluated once.
+    Returns {output key path + (t,): value} for every entry the tangent
+    stores (t alone for a real-valued program)."""
+    e = parse(program) if isinstance(program, str) else program
+    seeded = dict(env)
+    for name in env:
+        seeded[name + "'"] = tangents.get(name, ZERO)
+    r = evaluate(tangent(e), seeded)
+    if r is ZERO:
+        return {}
+    return {p: float(v) for p, v in (leaves(r) if isinstance(r, dict) else [((), r)])
+            if v is not ZERO}

@@ -172,6 +172,10 @@ _SIGS = {
     "nsd_loss_cpn": (C.c_int, [C.POINTER(nsd_coon), C.POINTER(_P), _I, C.c_float, _P, _P,
                                C.POINTER(_P), _P, _SZ, _P]),
     "nsd_spmm_jvp": (C.c_int, [_CSR, _P, _P, _P, _I, _P, _P, _P, _SZ, _P]),
+    "nsd_spmm_jvp_batch_workspace_size": (C.c_int, [_CSR, _I, C.POINTER(_SZ)]),
+    "nsd_spmm_jvp_batch": (C.c_int, [_CSR, _I, _P, _P, _P, _I, _P, _P, _P, _SZ, _P]),
+    "nsd_scale": (C.c_int, [C.c_int64, C.c_double, _P, _P, _P, _P, _P, C.c_float, _P, _P, _P]),
+    "nsd_scale_real": (C.c_int, [C.c_double, _P, _P, _P, C.c_double, _P, _P]),
     "nsd_batax_pairs": (C.c_int, [_CSR, C.POINTER(C.c_int64), _P, _SZ, _P]),
     "nsd_batax_workspace_size": (C.c_int, [_CSR, C.c_int64, C.POINTER(_SZ)]),
     "nsd_batax_jacobian": (C.c_int, [_CSR, C.c_float, C.c_int64, _P, _P, _P, C.POINTER(_I), _P,
@@ -521,6 +525,19 @@ def nsd_spmm_jvp(A: nsd_csr, dAval, B, dB, k, C_out, dC, ws, stream=None):
                              _nbytes(ws), _stream(stream)), "nsd_spmm_jvp")
 
 
+def nsd_spmm_jvp_batch_workspace_size(A: nsd_csr, k: int) -> int:
+    b = _SZ(0)
+    _check(_lib.nsd_spmm_jvp_batch_workspace_size(C.byref(A), k, C.byref(b)),
+           "nsd_spmm_jvp_batch_workspace_size")
+    return b.value
+
+
+def nsd_spmm_jvp_batch(A: nsd_csr, m, dAval, B, dB, k, C_out, dC, ws, stream=None):
+    _check(_lib.nsd_spmm_jvp_batch(C.byref(A), m, _p(dAval), _p(B), _p(dB), k, _p(C_out),
+                                   _p(dC), _p(ws), _nbytes(ws), _stream(stream)),
+           "nsd_spmm_jvp_batch")
+
+
 # --------------------------------------------------- order-N CP gradient
 
 def nsd_cpn_workspace_size(X: nsd_coon, rank: int) -> int:
@@ -545,6 +562,16 @@ def nsd_dot(n, x, y, alpha, accumulate, out, ws, stream=None):
 
 def nsd_axpby(n, alpha, x, beta, y, stream=None):
     _check(_lib.nsd_axpby(n, alpha, _p(x), beta, _p(y), _stream(stream)), "nsd_axpby")
+
+
+def nsd_scale(n, alpha, s1, s2, x1, x2, x2_idx, beta, y, y_idx=None, stream=None):
+    _check(_lib.nsd_scale(n, alpha, _p(s1), _p(s2), _p(x1), _p(x2), _p(x2_idx), beta, _p(y),
+                          _p(y_idx), _stream(stream)), "nsd_scale")
+
+
+def nsd_scale_real(alpha, s1, s2, x, beta, y, stream=None):
+    _check(_lib.nsd_scale_real(alpha, _p(s1), _p(s2), _p(x), beta, _p(y), _stream(stream)),
+           "nsd_scale_real")
 
 
 def nsd_diag_keys(A: nsd_csr, alpha, out, stream=None):

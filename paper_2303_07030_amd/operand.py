@@ -133,6 +133,25 @@ class DeviceCsr:
         return valT[: self.nnz]
 
 
+class DeviceSparseVec:
+    """A sparse vector in HBM: its stored keys (int32, strictly increasing, in
+    [0, n)) and their values.  The keys are checked by nsd_validate_csr on
+    the 1 x n matrix they form (distinct keys are what lets a result be
+    scattered into a dense vector with one write per key)."""
+
+    def __init__(self, n: int, keys, val, device="cuda", stream=None):
+        self.n = int(n)
+        self.keys = _dev(keys, torch.int32, device).contiguous()
+        self.val = _dev(val, torch.float32, device).contiguous()
+        self.nnz = int(self.keys.numel())
+        if self.val.numel() != self.nnz:
+            raise ValueError(f"{self.nnz} keys and {self.val.numel()} values")
+        rowptr = torch.tensor([0, self.nnz], dtype=torch.int32, device=device)
+        ws = torch.empty(256, dtype=torch.uint8, device=device)
+        nsd.nsd_validate_csr(nsd.csr_desc(1, self.n, rowptr, None, self.keys, self.val), True,
+                             ws, stream)
+
+
 def lex_order(coords, dims, ws, stream=None):
     """Permutation q -> input position that sorts COO entries by (c0, c1, ...)
     lexicographically: stable sorts by the last coordinate first, each one the

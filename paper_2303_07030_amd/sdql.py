@@ -61,8 +61,19 @@ class Sparse:
 
 
 @dataclass(frozen=True)
+class SparseVec:
+    """A sparse vector input (its stored keys are its iteration domain)."""
+
+    n: int
+
+    @property
+    def shape(self):
+        return (self.n,)
+
+
+@dataclass(frozen=True)
 class Dense:
-    """A dense input of order 1 or 2 (row-major)."""
+    """A dense input: a real (no shape), a vector or a matrix (row-major)."""
 
     shape: tuple
 
@@ -383,14 +394,14 @@ class Program:
         if len(sparse) > 1:
             raise NotLowerable(f"one sparse matrix per program, got {sparse}")
         for name, d in decls.items():
-            if isinstance(d, Sparse):
+            if isinstance(d, (Sparse, SparseVec)):
                 self.tensors[name] = TensorInfo(name, "sparse", d.shape, pattern=name)
             elif isinstance(d, Dense):
-                if not 1 <= len(d.shape) <= 2:
-                    raise NotLowerable(f"dense input {name} must have order 1 or 2")
-                self.tensors[name] = TensorInfo(name, "dense", d.shape)
+                if len(d.shape) > 2:
+                    raise NotLowerable(f"dense input {name} must have order 0, 1 or 2")
+                self.tensors[name] = TensorInfo(name, "dense" if d.shape else "scalar", d.shape)
             else:
-                raise SdqlError(f"declaration of {name} must be Sparse or Dense")
+                raise SdqlError(f"declaration of {name} must be Sparse, SparseVec or Dense")
         self.sparse = sparse[0] if sparse else None
         self.inputs = dict(decls)
         env = {n: _Bind("access", Access(n, ())) for n in decls}
@@ -538,15 +549,19 @@ class Program:
         if bound.terms:
             shape = shape + tuple(self.extent[v] for v in bound.terms[0].keys)
         terms = _simplify(terms, self.tensors)
-        kind = "dense"
+        kind, pattern = "dense", None
         if keys_order == 0:
             kind = "scalar"
-        elif self.sparse is not None and keys_order == 2 and terms and all(
-                any(m.tensor == self.sparse and m.idx == t.keys for m in t.masks)
-                for t in terms):
-            kind = "patterned"
-        self.tensors[inter] = TensorInfo(inter, kind, shape,
-                                         pattern=self.sparse if kind == "patterned" else None,
+        else:
+            # on the stored keys of one sparse input: a value array aligned with them
+            for P in self.inputs:
+                pinfo = self.tensors[P]
+                if pinfo.kind == "sparse" and pinfo.order == keys_order and terms and all(
+                        any(m.tensor == P and m.idx == t.keys for m in t.masks)
+                        for t in terms):
+                    kind, pattern = "patterned", P
+                    break
+        self.tensors[inter] = TensorInfo(inter, kind, shape, pattern=pattern,
                                          definition=Terms(keys_order, terms), deps=deps)
         return Access(inter, deps)
 
@@ -559,15 +574,24 @@ class Program:
             return False
         return any(self.depends(f.tensor, x) for t in info.definition.terms for f in t.facs)
 
-    def tangent(self, T: Terms, x: str) -> Terms:
-        """Tangent of T when the input x is seeded with its one-hot tensor and
-        every other input with zero: a tensor of order T.order + order(x)."""
+    def tangent(self, T: Terms, x: str, seed: str | None = None) -> Terms:
+        """Tangent of T when the input x is seeded and every other input gets
+        the zero tangent.  With seed None, x's tangent is its one-hot tensor
+        (the gradient API of Section 4.3): the result has order T.order +
+        order(x), x's keys after T's, and for a tensor-valued T it is the
+        Jacobian.  With seed the name of a tangent input of x's layout (from
+        seed_of), the result is the directional derivative along it, of T's
+        order (the forward mode of Section 4.1)."""
         xinfo = self.tensors[x]
         out = []
         for t in T.terms:
             for p, f in enumerate(t.facs):
                 rest = t.facs[:p] + t.facs[p + 1:]
                 if f.tensor == x:
+                    if seed is not None:
+                        out.append(Term(t.coef, t.keys, t.loops, rest + (Fac(seed, f.idx),),
+                                        t.masks))
+                        continue
                     # x'(idx) is the one-hot tensor: 1 at the key idx, on x's
                     # stored keys only
                     masks = t.masks + ((Fac(xinfo.pattern, f.idx),)
@@ -575,7 +599,7 @@ class Program:
                     out.append(Term(t.coef, t.keys + f.idx, t.loops - set(f.idx), rest, masks))
                 elif not self.tensors[f.tensor].input and self.depends(f.tensor, x):
                     info = self.tensors[f.tensor]
-                    dT = self._tangent_of(f.tensor, x)
+                    dT = self._tangent_of(f.tensor, x, seed)
                     for s in dT.terms:
                         s = _fresh_all(s, self)
                         sub = {}
@@ -588,21 +612,43 @@ class Program:
                         out.append(Term(t.coef * s.coef, t.keys + gkeys,
                                         (t.loops | s.loops) - set(gkeys), rest + s.facs,
                                         t.masks + s.masks))
-        order = None if T.order is None else T.order + xinfo.order
+        order = None if T.order is None else T.order + (0 if seed else xinfo.order)
         return Terms(order, _simplify(out, self.tensors))
 
-    def _tangent_of(self, tensor, x):
-        key = (tensor, x)
+    def _tangent_of(self, tensor, x, seed=None):
+        key = (tensor, x, seed)
         if key not in self._tangents:
-            self._tangents[key] = self.tangent(self.tensors[tensor].definition, x)
+            self._tangents[key] = self.tangent(self.tensors[tensor].definition, x, seed)
         return self._tangents[key]
 
     def gradient(self, x: str) -> Terms:
         """`gradient e x` of the gradient API (Section 4.3): the program's
-        derivative w.r.t. input x, as terms over x's keys."""
+        derivative w.r.t. input x, as terms over x's keys; for a
+        tensor-valued program, its Jacobian (the output's keys, then x's)."""
         if x not in self.inputs:
             raise SdqlError(f"{x} is not an input")
         return self.tangent(self.value, x)
+
+    def seed_of(self, x: str) -> str:
+        """Name of the tangent input of x: a tensor of x's layout (a value
+        array on x's stored keys when x is sparse)."""
+        if x not in self.inputs:
+            raise SdqlError(f"{x} is not an input")
+        name = x + "'"
+        if name not in self.tensors:
+            info = self.tensors[x]
+            kind = {"sparse": "patterned"}.get(info.kind, info.kind)
+            self.tensors[name] = TensorInfo(name, kind, info.shape, pattern=info.pattern)
+        return name
+
+    def jvp_terms(self, wrt) -> Terms:
+        """The value's tangent along the tangents of the inputs in `wrt` (each
+        the input seed_of(x)), summed over them: the total derivative along
+        one direction, J v; a batch of directions is J V (Section 4.2)."""
+        out = []
+        for x in wrt:
+            out += self.tangent(self.value, x, self.seed_of(x)).terms
+        return Terms(self.value.order, _simplify(out, self.tensors))
 
     # -- step 5: lowering
     def plan(self, grads=(), value=True, fuse=True):
@@ -616,10 +662,38 @@ class Program:
         return _Lowering(self).run(value, tuple(grads))
 
     def run(self, inputs: dict, grads=(), value=True, stream=None, fuse=True):
-        """Executes the plan on device tensors: inputs maps each sparse name
-        to a DeviceCsr and each dense name to a float32 tensor of its shape.
-        Returns {"value": ..., "d<name>": ...}."""
+        """Executes the plan on device tensors: inputs maps a sparse matrix's
+        name to a DeviceCsr, a sparse vector's to a DeviceSparseVec, a
+        dense input's to a float32 tensor of its shape and a real's to a
+        one-element float64 tensor.  Returns {"value": ..., "d<name>": ...};
+        a result on an input's stored keys is a value array aligned with
+        them (Plan.layout tells which keys)."""
         return self.plan(grads, value, fuse).execute(inputs, stream)
+
+    def jvp_plan(self, wrt, fuse=True):
+        """Kernel calls for the tangent along the inputs in `wrt` (see
+        jvp_terms): one call for the whole batch when the program is a
+        matrix product the batched tangent kernel covers (and fuse is set),
+        else one pass of the term-by-term lowering per tangent."""
+        wrt = tuple(wrt)
+        for x in wrt:
+            if x not in self.inputs:
+                raise SdqlError(f"{x} is not an input")
+        if fuse:
+            fused = _fused_jvp_plan(self, wrt)
+            if fused is not None:
+                return fused
+        plan = _Lowering(self).run_tangent(wrt)
+        plan.per_tangent = True
+        return plan
+
+    def jvp(self, inputs: dict, tangents: dict, value=True, stream=None, fuse=True):
+        """J V for a batch of m tangents: tangents maps input names to device
+        tensors [m, *layout of the input] (a sparse input's tangent on its
+        stored keys: [m, nnz]; a real's: [m] float64).  Returns {"value": ...
+        (when asked), "tangent": [m, *layout of the value]}."""
+        return _execute_jvp(self.jvp_plan(tuple(tangents), fuse), inputs, tangents, value,
+                            stream)
 
 
 def compile(text: str, **decls) -> Program:   # noqa: A001 - the natural name
@@ -698,12 +772,17 @@ def _simplify(terms, tensors):
 
 @dataclass
 class Buf:
-    """A device buffer of the plan: "input" (caller's), "out", "inter" or "temp"."""
+    """A device buffer of the plan: "input" (caller's), "out", "inter" or "temp".
+    Layout "scalar" (one double), "pattern" (a float per stored key of the
+    sparse input `pattern`; output key position p is that key's coordinate
+    keymap[p]) or "dense" (float32 of `shape`)."""
 
     name: str
     role: str
-    layout: str          # "scalar" (one double), "pattern" (nnz floats), "dense"
+    layout: str
     shape: tuple = ()
+    pattern: str | None = None
+    keymap: tuple = ()
 
 
 @dataclass
@@ -719,12 +798,22 @@ class Plan:
     bufs: dict = field(default_factory=dict)
     calls: list = field(default_factory=list)
     results: dict = field(default_factory=dict)
+    per_tangent: bool = False   # a tangent plan run once per tangent of a batch
 
     def kernels(self):
         return [c.kernel for c in self.calls]
 
+    def layout(self, name):
+        """(layout, pattern, keymap, shape) of a result."""
+        b = self.bufs[name]
+        return b.layout, b.pattern, b.keymap, b.shape
+
     def execute(self, inputs: dict, stream=None):
         return _execute(self, inputs, stream)
+
+
+def _identity_map(n):
+    return tuple(range(n))
 
 
 class _Lowering:
@@ -734,34 +823,94 @@ class _Lowering:
         self.done = set()
         self.ntemp = itertools.count()
 
-    def run(self, value, grads):
+    def _inputs(self):
         p = self.p
         for name, d in p.inputs.items():
-            if isinstance(d, Sparse):
-                self.plan.bufs[name] = Buf(name, "input", "pattern", d.shape)
+            info = p.tensors[name]
+            if info.kind == "sparse":
+                self.plan.bufs[name] = Buf(name, "input", "pattern", d.shape, name,
+                                           _identity_map(info.order))
+            elif info.kind == "scalar":
+                self.plan.bufs[name] = Buf(name, "input", "scalar")
             else:
                 self.plan.bufs[name] = Buf(name, "input", "dense", d.shape)
+
+    def run(self, value, grads):
+        p = self.p
+        self._inputs()
         if value:
-            self._result("value", p.value, p.value.order or 0, self._value_shape())
+            self._result("value", p.value, self._layout(p.value))
         for x in grads:
             g = p.gradient(x)
             info = p.tensors[x]
-            layout = "pattern" if info.kind == "sparse" else "dense"
-            if p.value.order not in (0, None):
-                raise NotLowerable("gradients of tensor-valued programs")
-            self._result("d" + x, g, info.order, info.shape, layout)
+            if (p.value.order or 0) == 0:
+                # the gradient of a real has x's own layout
+                if info.kind == "sparse":
+                    b = Buf("", "out", "pattern", info.shape, info.pattern,
+                            _identity_map(info.order))
+                elif info.kind == "scalar":
+                    b = Buf("", "out", "scalar")
+                else:
+                    b = Buf("", "out", "dense", info.shape)
+            else:
+                b = self._layout(g, jacobian_of=x)
+            self._result("d" + x, g, b)
         return self.plan
 
-    def _value_shape(self):
-        ts = self.p.value.terms
-        if not ts or not ts[0].keys:
-            return ()
-        return tuple(self.p.extent[v] for v in ts[0].keys)
+    def run_tangent(self, wrt):
+        """The tangent along the inputs in wrt, for one tangent of each."""
+        p = self.p
+        self._inputs()
+        T = p.jvp_terms(wrt)
+        for x in wrt:
+            s = p.seed_of(x)
+            info = p.tensors[s]
+            layout = {"patterned": "pattern", "scalar": "scalar"}.get(info.kind, "dense")
+            self.plan.bufs[s] = Buf(s, "input", layout, info.shape, info.pattern,
+                                    _identity_map(info.order) if info.pattern else ())
+        # a tangent has the value's type, so the value's layout
+        self._result("tangent", T, self._layout(p.value))
+        return self.plan
 
-    def _result(self, name, T, order, shape, layout=None):
-        if layout is None:
-            layout = "scalar" if order == 0 else "dense"
-        self.plan.bufs[name] = Buf(name, "out", layout, tuple(shape))
+    # -- result layouts
+    def _layout(self, T, jacobian_of=None):
+        """Layout of a result: on the stored keys of one sparse input when
+        every term lies on them with the same key map (the Jacobians of the
+        vector kernels, matrix-valued programs on a matrix's keys), a real
+        for order 0, else dense."""
+        p = self.p
+        if not T.terms:
+            if (T.order or 0) == 0:
+                return Buf("", "out", "scalar")
+            raise NotLowerable("a tensor-valued result with no terms (an empty Jacobian)")
+        found = []
+        for t in T.terms:
+            full = [m for m in t.masks if len(m.idx) == p.tensors[m.tensor].order]
+            on = None
+            if len(full) == 1 and t.keys:
+                m = full[0]
+                if set(t.keys) == set(m.idx) and not set(t.keys) & set(t.loops):
+                    if len(set(m.idx)) == len(m.idx):
+                        on = (m.tensor, tuple(m.idx.index(v) for v in t.keys))
+                    elif t.keys == m.idx:
+                        # the diagonal keys (i, i) of a matrix, as its keys
+                        on = (m.tensor, _identity_map(len(m.idx)))
+            found.append(on)
+        if all(f is not None and f == found[0] for f in found):
+            P, keymap = found[0]
+            shape = tuple(p.tensors[P].shape[i] for i in keymap)
+            return Buf("", "out", "pattern", shape, P, keymap)
+        keys = T.terms[0].keys
+        if not keys:
+            return Buf("", "out", "scalar")
+        if len(keys) > 2:
+            what = f"the Jacobian w.r.t. {jacobian_of}" if jacobian_of else "a result"
+            raise NotLowerable(f"{what} has order {len(keys)} and is not on one input's "
+                               "stored keys (its products with tangents are: jvp)")
+        return Buf("", "out", "dense", tuple(p.extent[v] for v in keys))
+
+    def _result(self, name, T, b: Buf):
+        self.plan.bufs[name] = replace(b, name=name, role="out")
         self._emit_terms(T, name)
         self.plan.results[name] = name
 
@@ -770,17 +919,25 @@ class _Lowering:
         info = self.p.tensors[tensor]
         if info.input or tensor in self.done:
             return
-        if info.kind == "scalar":
-            raise NotLowerable(f"the real {tensor.split('%')[0]} is used as a factor")
         self.done.add(tensor)
-        layout = "pattern" if info.kind == "patterned" else "dense"
-        self.plan.bufs[tensor] = Buf(tensor, "inter", layout, info.shape)
+        if info.kind == "scalar":
+            self.plan.bufs[tensor] = Buf(tensor, "inter", "scalar")
+        elif info.kind == "patterned":
+            self.plan.bufs[tensor] = Buf(tensor, "inter", "pattern", info.shape, info.pattern,
+                                         _identity_map(info.order))
+        else:
+            self.plan.bufs[tensor] = Buf(tensor, "inter", "dense", info.shape)
         self._emit_terms(info.definition, tensor)
 
     def _temp(self, like: Buf):
         name = f"tmp{next(self.ntemp)}"
-        self.plan.bufs[name] = Buf(name, "temp", like.layout, like.shape)
+        self.plan.bufs[name] = Buf(name, "temp", like.layout, like.shape, like.pattern,
+                                   like.keymap)
         return name
+
+    def _pattern_temp(self, P):
+        info = self.p.tensors[P]
+        return self._temp(Buf("", "temp", "pattern", info.shape, P, _identity_map(info.order)))
 
     def _emit_terms(self, T: Terms, out):
         for t in T.terms:
@@ -802,7 +959,6 @@ class _Lowering:
 
     def _emit_term(self, t: Term, out, accumulate):
         p = self.p
-        ob = self.plan.bufs[out]
         masks = [m for m in t.masks]
         for m in masks:
             if len(m.idx) != p.tensors[m.tensor].order:
@@ -810,28 +966,129 @@ class _Lowering:
                                    "their entries")
         if len(set(masks)) > 1:
             raise NotLowerable("two sparse iterations in one term")
-        for f in t.facs:
-            if p.tensors[f.tensor].kind == "scalar":
-                raise NotLowerable(f"the real {f.tensor.split('%')[0]} is used as a factor")
-        if masks:
-            self._emit_sparse(t, masks[0], out, ob, accumulate)
-        else:
-            self._emit_dense(t, out, ob, accumulate)
+        # reals (inputs or computed) scale the rest of the term
+        reals = tuple(f.tensor for f in t.facs if p.tensors[f.tensor].kind == "scalar")
+        if len(reals) > 2:
+            raise NotLowerable("more than two real factors in one term")
+        t = replace(t, facs=tuple(f for f in t.facs if p.tensors[f.tensor].kind != "scalar"))
+        self._emit_plain(t, out, accumulate, reals)
 
-    # terms over the sparse matrix's stored keys (r, c)
-    def _emit_sparse(self, t, mask, out, ob, accumulate):
+    def _emit_plain(self, t, out, accumulate, reals):
         p = self.p
-        r, c = mask.idx
-        if r == c:
-            self._emit_diagonal(t, r, out, ob, accumulate)
+        ob = self.plan.bufs[out]
+        if not t.masks:
+            self._emit_dense(t, out, ob, accumulate, reals)
             return
+        m = t.masks[0]
+        if p.tensors[m.tensor].order == 1:
+            self._emit_vector(t, m, out, ob, accumulate, reals)
+        elif m.idx[0] == m.idx[1]:
+            self._emit_diagonal(t, m.idx[0], out, ob, accumulate, reals)
+        else:
+            self._emit_sparse(t, m, out, ob, accumulate, reals)
+
+    def _via_temp(self, t, out, ob, accumulate, reals):
+        """The term without its reals into a temporary, then scaled by them."""
+        tmp = self._temp(ob)
+        self._emit_plain(t, tmp, False, ())
+        self._scale_into(out, ob, tmp, reals, accumulate)
+
+    def _scale_into(self, out, ob, x, reals, accumulate, alpha=1.0):
+        s1, s2 = (tuple(reals) + (None, None))[:2]
+        beta = 1.0 if accumulate else 0.0
+        if ob.layout == "scalar":
+            self.plan.calls.append(Call("scale_real", dict(alpha=alpha, s1=s1, s2=s2, x=x,
+                                                           beta=beta), out))
+        else:
+            self.plan.calls.append(Call("scale", dict(n=None, alpha=alpha, s1=s1, s2=s2, x1=x,
+                                                      x2=None, x2_idx=None, beta=beta,
+                                                      y_idx=None), out))
+
+    def _product(self, ops, out, P, coef, reals, beta, y_idx=None):
+        """out = coef * reals * (product of ops) (+ beta * out) key by key over
+        the stored keys of P.  An op is ("v", name) for a value array aligned
+        with P's keys or ("g", name, index) for a dense vector read at each
+        key's row, column or index; one nsd_scale per pair beyond two."""
+        calls = self.plan.calls
+        ops = list(ops)
+
+        def pair(a, b):
+            if a is not None and a[0] == "g":
+                a, b = b, a
+            x1 = a[1] if a is not None else None
+            if a is not None and a[0] == "g":
+                raise AssertionError("two gathered operands in one call")
+            x2, idx = (b[1], b[2] if b[0] == "g" else None) if b is not None else (None, None)
+            return x1, x2, idx
+
+        while len(ops) > 2 or (len(ops) == 2 and ops[0][0] == "g" and ops[1][0] == "g"):
+            a, b = ops[0], ops[1]
+            if a[0] == "g" and b[0] == "g":
+                b = None   # materialise one gathered operand on its own
+            tmp = self._pattern_temp(P)
+            x1, x2, idx = pair(a, b)
+            calls.append(Call("scale", dict(n=("nnz", P), alpha=1.0, s1=None, s2=None, x1=x1,
+                                            x2=x2, x2_idx=idx, beta=0.0, y_idx=None), tmp))
+            ops = [("v", tmp)] + ops[1 if b is None else 2:]
+        a = ops[0] if ops else None
+        b = ops[1] if len(ops) > 1 else None
+        x1, x2, idx = pair(a, b)
+        s1, s2 = (tuple(reals) + (None, None))[:2]
+        calls.append(Call("scale", dict(n=("nnz", P), alpha=coef, s1=s1, s2=s2, x1=x1, x2=x2,
+                                        x2_idx=idx, beta=beta, y_idx=y_idx), out))
+
+    # terms over the stored keys (r, c) of the sparse matrix
+    def _emit_sparse(self, t, mask, out, ob, accumulate, reals):
+        p = self.p
+        P = mask.tensor
+        r, c = mask.idx
         W = [f for f in t.facs if p.tensors[f.tensor].kind in ("sparse", "patterned")]
         D = [f for f in t.facs if p.tensors[f.tensor].kind == "dense"]
         for f in W:
-            if f.idx != (r, c):
+            if f.idx != (r, c) or p.tensors[f.tensor].pattern != P:
                 raise NotLowerable(f"{f.tensor} is read off the iterated key")
         keys = t.keys
         calls = self.plan.calls
+        if set(keys) == {r, c} and r not in t.loops and c not in t.loops:
+            # a result on the matrix's keys
+            if ob.layout != "pattern" or ob.pattern != P:
+                raise NotLowerable("a result on the matrix's keys must have its layout")
+            if ob.keymap != tuple(0 if v == r else 1 for v in keys):
+                raise NotLowerable("terms of one result on different keys")
+            summed = [f for f in D if any(v in t.loops for v in f.idx)]
+            if not reals and not W and D and self._is_sampled(D, r, c, t.loops):
+                X, Y, k = self._sampled(D, r, c, t.loops)
+                dst = self._temp(ob) if accumulate else out
+                calls.append(Call("sddmm", dict(X=X, Y=Y, k=k, alpha=t.coef), dst))
+                if accumulate:
+                    calls.append(Call("axpby", dict(alpha=1.0, x=dst, beta=1.0), out))
+                return
+            if not reals and not D and len(W) <= 1:
+                x = self._vals(W[0].tensor) if W else None
+                calls.append(Call("axpby", dict(alpha=t.coef, x=x, beta=1.0
+                                                if accumulate else 0.0), out))
+                return
+            ops = [("v", self._vals(f.tensor)) for f in W]
+            if summed:
+                X, Y, k = self._sampled(summed, r, c, t.loops)
+                tmp = self._pattern_temp(P)
+                calls.append(Call("sddmm", dict(X=X, Y=Y, k=k, alpha=1.0), tmp))
+                ops.append(("v", tmp))
+            for f in D:
+                if f in summed:
+                    continue
+                if f.idx == (r,):
+                    ops.append(("g", f.tensor, ("rows", P)))
+                elif f.idx == (c,):
+                    ops.append(("g", f.tensor, ("cols", P)))
+                else:
+                    raise NotLowerable("a dense factor read at both coordinates of the "
+                                       "matrix's key (outside SDDMM)")
+            self._product(ops, out, P, t.coef, reals, 1.0 if accumulate else 0.0)
+            return
+        if reals:
+            self._via_temp(t, out, ob, accumulate, reals)
+            return
         # the product runs into a temporary when it must be added to `out`
         dst = self._temp(ob) if accumulate else out
 
@@ -842,22 +1099,6 @@ class _Lowering:
             elif not scale_done and t.coef != 1.0:
                 calls.append(Call("axpby", dict(alpha=t.coef, x=out, beta=0.0), out))
 
-        if keys == (r, c):
-            if ob.layout != "pattern":
-                raise NotLowerable("a result on the matrix's keys must have its layout")
-            if not D:
-                if len(W) > 1:
-                    raise NotLowerable("elementwise product of values on the pattern")
-                x = W[0].tensor if W else None
-                calls.append(Call("axpby", dict(alpha=t.coef, x=self._vals(x), beta=1.0
-                                                if accumulate else 0.0), out))
-                return
-            if W:
-                raise NotLowerable("sampled product times values on the pattern")
-            X, Y, k = self._sampled(D, r, c, t.loops)
-            calls.append(Call("sddmm", dict(X=X, Y=Y, k=k, alpha=t.coef), dst))
-            finish(True)
-            return
         if len(W) > 1 and keys:
             raise NotLowerable("elementwise product of values on the pattern")
         vals = self._vals(W[0].tensor) if W else None
@@ -896,7 +1137,7 @@ class _Lowering:
                 if len(W) > 1:
                     raise NotLowerable("elementwise product of values on the pattern")
                 X, Y, k = self._sampled(D, r, c, t.loops)
-                tmp = self._temp(Buf("", "temp", "pattern", p.tensors[p.sparse].shape))
+                tmp = self._pattern_temp(P)
                 calls.append(Call("sddmm", dict(X=X, Y=Y, k=k, alpha=1.0), tmp))
                 calls.append(Call("dot", dict(x=tmp, y=self._vals(W[0].tensor) if W else None,
                                               alpha=t.coef, acc=accumulate), out))
@@ -911,8 +1152,11 @@ class _Lowering:
 
     # terms over the stored diagonal keys (i, i) of the sparse matrix: the
     # trace and its gradient (Section 4.3, Example 3)
-    def _emit_diagonal(self, t, i, out, ob, accumulate):
+    def _emit_diagonal(self, t, i, out, ob, accumulate, reals):
         p = self.p
+        if reals:
+            self._via_temp(t, out, ob, accumulate, reals)
+            return
         calls = self.plan.calls
         W = [f for f in t.facs if p.tensors[f.tensor].kind in ("sparse", "patterned")]
         if len(W) != len(t.facs) or len(W) > 1 or any(f.idx != (i, i) for f in W):
@@ -920,14 +1164,14 @@ class _Lowering:
         shape = p.tensors[p.sparse].shape
         if t.keys == (i, i):
             # a result on the matrix's keys: coef on the stored diagonal keys
-            if ob.layout != "pattern":
+            if ob.layout != "pattern" or ob.pattern != p.sparse:
                 raise NotLowerable("a result on the matrix's keys must have its layout")
             if W:
                 raise NotLowerable("values times the diagonal indicator on the pattern")
             if not accumulate:
                 calls.append(Call("diag", dict(alpha=t.coef), out))
             else:
-                tmp = self._temp(Buf("", "temp", "pattern", shape))
+                tmp = self._pattern_temp(p.sparse)
                 calls.append(Call("diag", dict(alpha=t.coef), tmp))
                 calls.append(Call("axpby", dict(alpha=1.0, x=tmp, beta=1.0), out))
             return
@@ -935,12 +1179,69 @@ class _Lowering:
             # a real: coef * sum of the values (or ones) on the stored diagonal keys
             if ob.layout != "scalar":
                 raise NotLowerable("a real result needs a scalar output")
-            tmp = self._temp(Buf("", "temp", "pattern", shape))
+            tmp = self._temp(Buf("", "temp", "pattern", shape, p.sparse, (0, 1)))
             calls.append(Call("diag", dict(alpha=1.0), tmp))
             calls.append(Call("dot", dict(x=tmp, y=self._vals(W[0].tensor) if W else None,
                                           alpha=t.coef, acc=accumulate), out))
             return
         raise NotLowerable(f"result keys {t.keys} over the diagonal keys ({i}, {i})")
+
+    # terms over the stored keys k of a sparse vector (the vector kernels of
+    # Section 7.1)
+    def _emit_vector(self, t, mask, out, ob, accumulate, reals):
+        p = self.p
+        P = mask.tensor
+        (k,) = mask.idx
+        calls = self.plan.calls
+        ops = []
+        for f in t.facs:
+            info = p.tensors[f.tensor]
+            if info.kind in ("sparse", "patterned"):
+                if f.idx != (k,) or info.pattern != P:
+                    raise NotLowerable(f"{f.tensor} is read off the iterated key")
+                ops.append(("v", self._vals(f.tensor)))
+            elif f.idx == (k,):
+                ops.append(("g", f.tensor, ("keys", P)))
+            else:
+                raise NotLowerable(f"dense factor {f.tensor} of a sparse vector's term read "
+                                   "at other than its key")
+        keys = t.keys
+        if keys and all(v == k for v in keys) and k not in t.loops:
+            if ob.layout == "pattern" and ob.pattern == P:
+                if ob.keymap != (0,) * len(keys):
+                    raise NotLowerable("terms of one result on different keys")
+                self._product(ops, out, P, t.coef, reals, 1.0 if accumulate else 0.0)
+                return
+            if ob.layout == "dense" and len(keys) == 1:
+                # scattered into a dense vector (the keys are distinct)
+                if not accumulate:
+                    self._zero(out)
+                self._product(ops, out, P, t.coef, reals, 1.0, y_idx=("keys", P))
+                return
+            raise NotLowerable(f"result keys {keys} over the sparse vector {P}'s keys")
+        if not keys:
+            if ob.layout != "scalar":
+                raise NotLowerable("a real result needs a scalar output")
+            dst = self._temp(ob) if reals else out
+            if len(ops) <= 2 and all(o[0] == "v" for o in ops):
+                x = ops[0][1] if ops else None
+                y = ops[1][1] if len(ops) > 1 else None
+            else:
+                x, y = self._pattern_temp(P), None
+                self._product(ops, x, P, 1.0, (), 0.0)
+            calls.append(Call("dot", dict(x=x, y=y, n=("nnz", P), alpha=t.coef,
+                                          acc=accumulate and not reals), dst))
+            if reals:
+                self._scale_into(out, ob, dst, reals, accumulate)
+            return
+        raise NotLowerable(f"result keys {keys} over the sparse vector {P}'s keys")
+
+    def _is_sampled(self, D, r, c, loops):
+        try:
+            self._sampled(D, r, c, loops)
+            return True
+        except NotLowerable:
+            return False
 
     def _sampled(self, D, r, c, loops):
         """X[r, z], Y[c, z] (or vectors X[r], Y[c]) of an SDDMM."""
@@ -964,7 +1265,8 @@ class _Lowering:
     def _ones_pattern(self):
         name = "ones_nnz"
         if name not in self.plan.bufs:
-            self.plan.bufs[name] = Buf(name, "temp", "pattern", self.p.tensors[self.p.sparse].shape)
+            self.plan.bufs[name] = Buf(name, "temp", "pattern", self.p.tensors[self.p.sparse].shape,
+                                       self.p.sparse, (0, 1))
             self.plan.calls.append(Call("axpby", dict(alpha=1.0, x=None, beta=0.0), name))
         return name
 
@@ -976,9 +1278,23 @@ class _Lowering:
         return name
 
     # terms over dense tensors only
-    def _emit_dense(self, t, out, ob, accumulate):
+    def _emit_dense(self, t, out, ob, accumulate, reals):
         calls = self.plan.calls
+        if not t.facs and not t.keys:
+            # a constant: coef times the number of points of its loops
+            mult = 1
+            for v in t.loops:
+                mult *= self.p.extent[v]
+            if ob.layout != "scalar":
+                raise NotLowerable("a real result needs a scalar output")
+            calls.append(Call("scale_real", dict(alpha=t.coef * mult, s1=(reals + (None,))[0],
+                                                 s2=(reals + (None, None))[1], x=None,
+                                                 beta=1.0 if accumulate else 0.0), out))
+            return
         if not t.keys:
+            if reals:
+                self._via_temp(t, out, ob, accumulate, reals)
+                return
             if ob.layout != "scalar":
                 raise NotLowerable("a real result needs a scalar output")
             if not t.facs or len(t.facs) > 2 or any(f.idx != t.facs[0].idx for f in t.facs) \
@@ -992,10 +1308,18 @@ class _Lowering:
                                           y=t.facs[1].tensor if len(t.facs) > 1 else None,
                                           alpha=t.coef, acc=accumulate), out))
             return
-        if len(t.facs) == 1 and t.facs[0].idx == t.keys and not t.loops \
+        if len(t.facs) <= 1 and (not t.facs or t.facs[0].idx == t.keys) and not t.loops \
                 and len(set(t.keys)) == len(t.keys) and ob.layout == "dense":
-            calls.append(Call("axpby", dict(alpha=t.coef, x=t.facs[0].tensor,
-                                            beta=1.0 if accumulate else 0.0), out))
+            x = t.facs[0].tensor if t.facs else None
+            if reals:
+                s1, s2 = (reals + (None, None))[:2]
+                calls.append(Call("scale", dict(n=None, alpha=t.coef, s1=s1, s2=s2, x1=x,
+                                                x2=None, x2_idx=None,
+                                                beta=1.0 if accumulate else 0.0, y_idx=None),
+                                  out))
+            else:
+                calls.append(Call("axpby", dict(alpha=t.coef, x=x,
+                                                beta=1.0 if accumulate else 0.0), out))
             return
         raise NotLowerable("dense term other than a copy or a dot product")
 
@@ -1044,16 +1368,16 @@ def _fused_plan(p: Program, grads, value):
     A = p.sparse
     facs = _facs_by_tensor(t)
     mask = _sparse_mask(p, t)
-    plan = Plan(p)
-    for name, d in p.inputs.items():
-        plan.bufs[name] = Buf(name, "input", "pattern" if isinstance(d, Sparse) else "dense",
-                              d.shape)
+    low = _Lowering(p)
+    low._inputs()
+    plan = low.plan
 
     def out(name, layout, shape, wanted):
         """A result buffer, or a temporary when the kernel writes an output
         nobody asked for."""
         key = name if wanted else f"unused_{name}"
-        plan.bufs[key] = Buf(key, "out" if wanted else "temp", layout, shape)
+        on = (A, (0, 1)) if layout == "pattern" else (None, ())
+        plan.bufs[key] = Buf(key, "out" if wanted else "temp", layout, shape, *on)
         if wanted:
             plan.results[key] = key
         return key
@@ -1136,9 +1460,7 @@ def _fused_plan(p: Program, grads, value):
                     uz, vz = uf[Un][0], uf[Vn][0]
                     if len(uz) == 2 and uz[1] == vz[1] and uz[1] in ut.loops:
                         k = p.extent[uz[1]]
-                        # the fused kernel's widths: k <= 64, or k <= 256 in float4 rows
-                        fits = k <= 64 or (k <= 256 and k % 4 == 0)
-                        if fits and _dense(p, Un, (nr, k)) and _dense(p, Vn, (nc, k)) \
+                        if _dense(p, Un, (nr, k)) and _dense(p, Vn, (nc, k)) \
                                 and set(grads) <= {Un, Vn}:
                             args = dict(U=Un, V=Vn, k=k, loss=out("value", "scalar", (), value),
                                         dU=out("d" + Un, "dense", (nr, k), want(Un)),
@@ -1148,16 +1470,59 @@ def _fused_plan(p: Program, grads, value):
     return None
 
 
+def _fused_jvp_plan(p: Program, wrt):
+    """The tangent of C = A B (or y = A x) along tangents of A and/or B, for
+    a whole batch in one nsd_spmm_jvp_batch call; else None."""
+    if p.sparse is None or not set(wrt) <= set(p.inputs):
+        return None
+    t = _only(p.value.terms)
+    mask = t and _sparse_mask(p, t)
+    if not mask or t.coef != 1.0 or len(t.facs) != 2:
+        return None
+    A = p.sparse
+    r, c = mask
+    nr, nc = p.tensors[A].shape
+    facs = _facs_by_tensor(t)
+    Bn = [n for n in facs if n != A]
+    if facs.get(A) != [(r, c)] or len(Bn) != 1 or len(facs[Bn[0]]) != 1:
+        return None
+    Bn = Bn[0]
+    bz = facs[Bn][0]
+    if bz[0] != c or c not in t.loops or t.keys != (r,) + bz[1:] or len(bz) > 2:
+        return None
+    k = p.extent[bz[1]] if len(bz) == 2 else 1
+    if not _dense(p, Bn, (nc, k) if len(bz) == 2 else (nc,)) or not set(wrt) <= {A, Bn}:
+        return None
+    low = _Lowering(p)
+    low._inputs()
+    plan = low.plan
+    for x in wrt:
+        s = p.seed_of(x)
+        layout = "pattern" if x == A else "dense"
+        plan.bufs[s] = Buf(s, "input", layout, p.tensors[x].shape, A if x == A else None,
+                           (0, 1) if x == A else ())
+    shape = (nr, k) if len(bz) == 2 else (nr,)
+    plan.bufs["tangent"] = Buf("tangent", "out", "dense", shape)
+    plan.results["tangent"] = "tangent"
+    args = dict(B=Bn, k=k, dA=p.seed_of(A) if A in wrt else None,
+                dB=p.seed_of(Bn) if Bn in wrt else None)
+    plan.calls.append(Call("spmm_jvp_batch", args, "tangent"))
+    return plan
+
+
 # ------------------------------------------------------------------ execution
 
 
-def _execute(plan: Plan, inputs: dict, stream=None):
+def _execute(plan: Plan, inputs: dict, stream=None, outputs=None, m=1):
+    """Runs a plan's calls.  outputs: preallocated device tensors for some
+    results.  m: the batch of a fused tangent plan (its tangent inputs and
+    output carry a leading batch dimension)."""
     import torch
 
     from . import nsd
 
     prog = plan.prog
-    A = inputs.get(prog.sparse) if prog.sparse else None
+    pats = {}
     dev = None
     for name, d in prog.inputs.items():
         v = inputs.get(name)
@@ -1166,26 +1531,51 @@ def _execute(plan: Plan, inputs: dict, stream=None):
         if isinstance(d, Sparse):
             if (v.nrows, v.ncols) != d.shape:
                 raise SdqlError(f"{name} is {v.nrows}x{v.ncols}, declared {d.shape}")
+            pats[name] = v
             dev = v.val.device
+        elif isinstance(d, SparseVec):
+            if getattr(v, "n", None) != d.n or not hasattr(v, "keys"):
+                raise SdqlError(f"{name} must be a DeviceSparseVec of length {d.n}")
+            pats[name] = v
+            dev = v.val.device
+        elif not d.shape:
+            if v.dtype != torch.float64 or v.numel() != 1:
+                raise SdqlError(f"{name} must be a one-element float64 tensor (a real)")
+            dev = v.device
         else:
             if tuple(v.shape) != d.shape or v.dtype != torch.float32 or not v.is_contiguous():
                 raise SdqlError(f"{name} must be a contiguous float32 tensor of shape {d.shape}")
             dev = v.device
-    nnz = A.nnz if A is not None else 0
+    A = pats.get(prog.sparse) if prog.sparse else None
+
+    def nnz(P):
+        return pats[P].nnz
+
     mem = {}
     for name, b in plan.bufs.items():
-        if b.role == "input":
-            mem[name] = A.val if prog.tensors[name].kind == "sparse" else inputs[name]
+        if outputs and name in outputs:
+            mem[name] = outputs[name]
+        elif b.role == "input":
+            if name in pats:
+                mem[name] = pats[name].val
+            else:
+                v = inputs.get(name)
+                if v is None:
+                    raise SdqlError(f"missing input {name}")
+                mem[name] = v
         elif b.layout == "scalar":
             mem[name] = torch.empty(1, dtype=torch.float64, device=dev)
         elif b.layout == "pattern":
-            mem[name] = torch.empty(max(nnz, 1), dtype=torch.float32, device=dev)[:nnz]
+            n = nnz(b.pattern)
+            mem[name] = torch.empty(max(n, 1), dtype=torch.float32, device=dev)[:n]
         else:
             mem[name] = torch.empty(b.shape, dtype=torch.float32, device=dev)
     kmax = max([c.args.get("k", 1) for c in plan.calls] + [1])
     need = 16384
     if A is not None:
         need = max(need, nsd.nsd_workspace_size(A.desc, A.csc, kmax))
+        if any(c.kernel == "spmm_jvp_batch" for c in plan.calls):
+            need = max(need, nsd.nsd_spmm_jvp_batch_workspace_size(A.desc, kmax))
     ws = torch.empty(need, dtype=torch.uint8, device=dev)
 
     def desc(vals):
@@ -1193,8 +1583,20 @@ def _execute(plan: Plan, inputs: dict, stream=None):
         d.plan = A.row_plan
         return d
 
-    def m(name):
+    def m_(name):
         return None if name is None else mem[name]
+
+    def index(ix):
+        if ix is None:
+            return None
+        what, P = ix
+        return {"rows": lambda: pats[P].rowidx, "cols": lambda: pats[P].colind,
+                "keys": lambda: pats[P].keys}[what]()
+
+    def count(n, out):
+        if isinstance(n, tuple):
+            return nnz(n[1])
+        return out.numel() if n is None else n
 
     def csc():
         if A.csc is None:
@@ -1204,38 +1606,96 @@ def _execute(plan: Plan, inputs: dict, stream=None):
     for call in plan.calls:
         a, out = call.args, mem[call.out]
         if call.kernel == "axpby":
-            nsd.nsd_axpby(out.numel(), a["alpha"], m(a["x"]), a["beta"], out, stream)
+            nsd.nsd_axpby(out.numel(), a["alpha"], m_(a["x"]), a["beta"], out, stream)
+        elif call.kernel == "scale":
+            nsd.nsd_scale(count(a["n"], out), a["alpha"], m_(a["s1"]), m_(a["s2"]), m_(a["x1"]),
+                          m_(a["x2"]), index(a["x2_idx"]), a["beta"], out, index(a["y_idx"]),
+                          stream)
+        elif call.kernel == "scale_real":
+            nsd.nsd_scale_real(a["alpha"], m_(a["s1"]), m_(a["s2"]), m_(a["x"]), a["beta"], out,
+                               stream)
         elif call.kernel == "dot":
-            x = m(a["x"])
-            n = a.get("n", x.numel() if x is not None else 0)
-            nsd.nsd_dot(n, x, m(a["y"]), a["alpha"], a["acc"], out, ws, stream)
+            x = m_(a["x"])
+            n = a.get("n")
+            n = count(n, x) if n is not None else (x.numel() if x is not None else 0)
+            nsd.nsd_dot(n, x, m_(a["y"]), a["alpha"], a["acc"], out, ws, stream)
         elif call.kernel == "sddmm":
-            nsd.nsd_sddmm(A.desc, m(a["X"]), m(a["Y"]), a["k"], a["alpha"], out, stream)
+            nsd.nsd_sddmm(A.desc, m_(a["X"]), m_(a["Y"]), a["k"], a["alpha"], out, stream)
         elif call.kernel == "diag":
             nsd.nsd_diag_keys(A.desc, a["alpha"], out, stream)
         elif call.kernel == "spmm":
             D = desc(a["vals"])
             if a["k"] == 1:
-                nsd.nsd_spmv(D, m(a["B"]), out, ws, stream)
+                nsd.nsd_spmv(D, m_(a["B"]), out, ws, stream)
             else:
-                nsd.nsd_spmm(D, m(a["B"]), a["k"], out, ws, stream)
+                nsd.nsd_spmm(D, m_(a["B"]), a["k"], out, ws, stream)
         elif call.kernel == "spmm_t":
-            if A.csc is None:
-                A.build_csc(stream)
-            nsd.nsd_spmm_t(desc(a["vals"]), A.csc, m(a["G"]), a["k"], a["alpha"], out, ws,
+            nsd.nsd_spmm_t(desc(a["vals"]), csc(), m_(a["G"]), a["k"], a["alpha"], out, ws,
                            stream)
+        elif call.kernel == "spmm_jvp_batch":
+            nsd.nsd_spmm_jvp_batch(A.desc, m, m_(a["dA"]), m_(a["B"]), m_(a["dB"]), a["k"],
+                                   (outputs or {}).get("value"), out, ws, stream)
         elif call.kernel == "loss_sum_spmv":
-            nsd.nsd_loss_sum_spmv(A.desc, csc(), m(a["x"]), 1.0, out, mem[a["dA"]],
+            nsd.nsd_loss_sum_spmv(A.desc, csc(), m_(a["x"]), 1.0, out, mem[a["dA"]],
                                   mem[a["dx"]], ws, stream)
         elif call.kernel == "loss_bilinear":
-            nsd.nsd_loss_bilinear(A.desc, csc(), m(a["H"]), m(a["G"]), a["k"], 1.0, out,
+            nsd.nsd_loss_bilinear(A.desc, csc(), m_(a["H"]), m_(a["G"]), a["k"], 1.0, out,
                                   mem[a["dA"]], mem[a["dH"]], ws, stream)
         elif call.kernel == "loss_frob_spmm":
-            nsd.nsd_loss_frob_spmm(A.desc, csc(), m(a["B"]), a["k"], 1.0, mem[a["C"]], out,
+            nsd.nsd_loss_frob_spmm(A.desc, csc(), m_(a["B"]), a["k"], 1.0, mem[a["C"]], out,
                                    mem[a["dA"]], mem[a["dB"]], ws, stream)
         elif call.kernel == "loss_mf":
-            nsd.nsd_loss_mf(A.desc, csc(), None, m(a["U"]), m(a["V"]), a["k"], 1.0, out,
+            nsd.nsd_loss_mf(A.desc, csc(), None, m_(a["U"]), m_(a["V"]), a["k"], 1.0, out,
                             mem[a["dU"]], mem[a["dV"]], ws, stream)
         else:
             raise SdqlError(f"unknown kernel {call.kernel}")
     return {name: mem[name] for name in plan.results}
+
+
+def _execute_jvp(plan: Plan, inputs: dict, tangents: dict, value, stream):
+    import torch
+
+    prog = plan.prog
+    ms = {int(v.shape[0]) for v in tangents.values()}
+    if len(ms) != 1:
+        raise SdqlError(f"tangents of different batch sizes {sorted(ms)}")
+    (m,) = ms
+    seeded = dict(inputs)
+    for x, v in tangents.items():
+        b = plan.bufs[prog.seed_of(x)]
+        want = (m,) + ((inputs[x].nnz,) if b.layout == "pattern" else b.shape)
+        dtype = torch.float64 if b.layout == "scalar" else torch.float32
+        if b.layout == "scalar":
+            want = (m,)
+        if tuple(v.shape) != want or v.dtype != dtype or not v.is_contiguous():
+            raise SdqlError(f"the tangents of {x} must be a contiguous {dtype} tensor "
+                            f"of shape {want}")
+    ref = inputs[next(iter(tangents))] if tangents else None
+    dev = ref.val.device if hasattr(ref, "val") else ref.device
+    tb = plan.bufs["tangent"]
+    if tb.layout == "pattern":
+        rshape = (inputs[tb.pattern].nnz,)
+    elif tb.layout == "scalar":
+        rshape = ()
+    else:
+        rshape = tb.shape
+    out = {}
+    tan = torch.empty((m,) + rshape, dtype=torch.float64 if tb.layout == "scalar"
+                      else torch.float32, device=dev)
+    if not plan.per_tangent:
+        outputs = {"tangent": tan}
+        if value:
+            out["value"] = outputs["value"] = torch.empty(rshape, dtype=torch.float32,
+                                                          device=dev)
+        for x, v in tangents.items():
+            seeded[prog.seed_of(x)] = v
+        _execute(plan, seeded, stream, outputs=outputs, m=m)
+    else:
+        for t in range(m):
+            for x, v in tangents.items():
+                seeded[prog.seed_of(x)] = v[t]
+            _execute(plan, seeded, stream, outputs={"tangent": tan[t]})
+        if value:
+            out["value"] = prog.plan((), True).execute(inputs, stream)["value"]
+    out["tangent"] = tan
+    return out

@@ -861,6 +861,35 @@ def test_spmm_jvp_full_workload(nsd, operand, orc):
     assert_mag_close(dCg, dC, dCm, what="dC")
 
 
+def test_spmm_jvp_batch_full_workload(nsd, operand, orc):
+    # J V for five tangents on the full SpMM workload (a group of four and a
+    # group of one): each tangent bit for bit the one-tangent kernel's, and
+    # the last one against the oracle
+    from paper_2303_07030_amd import synth
+    d = synth.make("spmm")
+    k, m = d["k"], 5
+    A = operand(d["nrows"], d["ncols"], d["rowptr"], d["colind"], d["val"], build_csc=False,
+                k_hint=k)
+    rng = np.random.default_rng(8)
+    TA = rng.standard_normal((m, A.nnz), dtype=np.float32)
+    TB = rng.standard_normal((m,) + d["B"].shape, dtype=np.float32)
+    C = torch.full((A.nrows, k), np.nan, dtype=torch.float32, device="cuda")
+    dC = torch.full((m, A.nrows, k), np.nan, dtype=torch.float32, device="cuda")
+    ws = torch.empty(nsd.nsd_spmm_jvp_batch_workspace_size(A.desc, k), dtype=torch.uint8,
+                     device="cuda")
+    nsd.nsd_spmm_jvp_batch(A.desc, m, dev(TA), dev(d["B"]), dev(TB), k, C, dC, ws)
+    dC = host(dC)
+    for t in range(m):
+        Cg, dCg = run_spmm_jvp(nsd, A, TA[t], d["B"], TB[t], k)
+        assert np.array_equal(dCg, dC[t]), f"tangent {t}"
+    assert np.array_equal(Cg, host(C))
+    rows = np.repeat(np.arange(d["nrows"], dtype=np.int32), np.diff(d["rowptr"]))
+    D = orc.Dok((d["nrows"], d["ncols"]), (rows, d["colind"]), d["val"])
+    dD = orc.Dok((d["nrows"], d["ncols"]), (rows, d["colind"]), TA[m - 1])
+    _, _, dCo, dCm = orc.spmm_jvp(D, dD, d["B"], TB[m - 1], k)
+    assert_mag_close(dC[m - 1], dCo, dCm, what="dC[4]")
+
+
 # --------------------------------------------------- order-N CP gradient
 
 def run_cpn(nsd, X, F, rank, seed=1.0):

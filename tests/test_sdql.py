@@ -30,6 +30,15 @@ DOT1 = "sum(<i, a> in V1) a * V2(i)"
 DOT2 = "sum(<i, a> in V2) V1(i) * a"
 TRACE = "sum(<i,r> in M) r(i)"
 CUBIC = "sum(<i,r> in A) sum(<j,a> in r) 2 * a * a * a * x(j)"
+# Tensor-valued programs: the vector kernels of the evaluation (Section 7.1;
+# VVA parenthesised, since a sum's body runs to the end of the expression),
+# a sparse matrix-vector product, a matrix-valued program on a matrix's
+# keys and the matrix product.
+VVA = "(sum(<i,v> in V1) {i -> v}) + (sum(<i,v> in V2) {i -> v})"
+VSM = "sum(<i,v> in V) {i -> v * s * s}"
+MATVEC = "sum(<i,r> in M) {i -> sum(<j,a> in r) a * x(j)}"
+MATSQ = "sum(<i,r> in M) {i -> sum(<j,a> in r) {j -> a * a * x(j) * s}}"
+SPMM = "sum(<i,r> in A) {i -> sum(<j,a> in r) sum(<c,b> in B(j)) {c -> a * b}}"
 
 
 def rand_csr(rng, nr, nc, nnz):
@@ -119,7 +128,18 @@ def eval_terms(prog, T, arrays, cache=None):
 def setup_inputs(rng, decls, sparse_nnz):
     arrays, env, csr = {}, {}, {}
     for name, d in decls.items():
-        if isinstance(d, S.Sparse):
+        if isinstance(d, S.SparseVec):
+            keys = np.sort(rng.choice(d.n, size=min(sparse_nnz, d.n), replace=False))
+            val = rng.standard_normal(len(keys))
+            a, mask = np.zeros(d.n), np.zeros(d.n)
+            a[keys], mask[keys] = val, 1.0
+            arrays[name], arrays["#mask:" + name] = a, mask
+            env[name] = {int(k): float(v) for k, v in zip(keys, val)}
+            csr[name] = (keys, val)
+        elif isinstance(d, S.Dense) and not d.shape:
+            s = float(rng.standard_normal())
+            arrays[name], env[name] = np.asarray(s), s
+        elif isinstance(d, S.Sparse):
             rowptr, colind, val = rand_csr(rng, d.nrows, d.ncols, sparse_nnz)
             D = dense_of(d.nrows, d.ncols, rowptr, colind, val)
             arrays[name] = D
@@ -273,8 +293,12 @@ def test_lowering_dense_dot_product():
 @pytest.mark.parametrize("text,decls,grads,msg", [
     ("sum(<i,r> in M) r(i) * x(i)", dict(M=S.Sparse(4, 4), x=S.Dense(4)), ("M",),
      "diagonal"),
-    ("sum(<i,r> in A) sum(<j,a> in r) a * a * x(j)", dict(A=S.Sparse(4, 3), x=S.Dense(3)),
-     ("A",), "values on the pattern"),
+    ("sum(<i,v> in V) {i -> v * s * t * u}",
+     dict(V=S.SparseVec(5), s=S.Dense(), t=S.Dense(), u=S.Dense()), ("V",), "two real"),
+    # the Jacobian of C = A B w.r.t. B is of order 4 on no input's keys
+    (SPMM, dict(A=S.Sparse(4, 3), B=S.Dense(3, 2)), ("B",), "jvp"),
+    ("sum(<i,v> in V) {i -> v * W(i)(i)}", dict(V=S.SparseVec(3), W=S.Dense(3, 3)), (),
+     "other than its key"),
     ("sum(<i,a> in x) exp(a)", dict(x=S.Dense(3)), (), "outside"),
     ("sum(<i,a> in x) if a = 0 then 1", dict(x=S.Dense(3)), (), "outside"),
     ("sum(<i,r> in A) sum(<j,a> in r) a * B(i)(j)", dict(A=S.Sparse(4, 3), B=S.Dense(4, 3)),
@@ -317,6 +341,8 @@ def test_parser_binding():
      ["loss_bilinear", "spmm"]),
     (MF, dict(A=S.Sparse(5, 4), U=S.Dense(5, 3), V=S.Dense(4, 3)), ("U", "V"), ["loss_mf"]),
     (MF_INNER, dict(A=S.Sparse(5, 4), U=S.Dense(5, 3), V=S.Dense(4, 3)), ("U",), ["loss_mf"]),
+    # the fused factorisation takes any width
+    (MF, dict(A=S.Sparse(5, 4), U=S.Dense(5, 300), V=S.Dense(4, 300)), ("U",), ["loss_mf"]),
 ])
 def test_whole_programs_lower_to_fused_losses(text, decls, grads, kernels):
     p = S.compile(text, **decls).plan(grads)
@@ -326,10 +352,157 @@ def test_whole_programs_lower_to_fused_losses(text, decls, grads, kernels):
 
 @pytest.mark.parametrize("text,decls,grads", [
     (MF, dict(A=S.Sparse(5, 4), U=S.Dense(5, 3), V=S.Dense(4, 3)), ("A", "U")),  # no dA there
-    (MF, dict(A=S.Sparse(5, 4), U=S.Dense(5, 300), V=S.Dense(4, 300)), ("U",)),  # too wide
     ("2 * " + SMVM, dict(A=S.Sparse(5, 4), x=S.Dense(4)), ("A",)),             # scaled
     (QUAD, dict(A=S.Sparse(4, 4), x=S.Dense(4)), ("x",)),
 ])
 def test_other_programs_stay_term_by_term(text, decls, grads):
     p = S.compile(text, **decls).plan(grads)
     assert not any(k.startswith("loss_") for k in p.kernels())
+
+
+# ------------------------------- Jacobians of tensor-valued programs and J V
+
+JAC_CASES = [
+    ("vva", VVA, dict(V1=S.SparseVec(9), V2=S.SparseVec(9)), ("V1", "V2")),
+    ("vsm", VSM, dict(V=S.SparseVec(9), s=S.Dense()), ("s", "V")),
+    ("matvec", MATVEC, dict(M=S.Sparse(5, 6), x=S.Dense(6)), ("x", "M")),
+    ("matsq", MATSQ, dict(M=S.Sparse(5, 6), x=S.Dense(6), s=S.Dense()), ("M", "x", "s")),
+    ("trace", TRACE, dict(M=S.Sparse(5, 5)), ("M",)),
+]
+
+
+def dense_of_dict(d, shape):
+    out = np.zeros(shape)
+    for key, v in d.items():
+        out[key] += v
+    return out
+
+
+def value_shape(prog, decls):
+    ts = prog.value.terms
+    return tuple(prog.extent[v] for v in ts[0].keys) if ts else ()
+
+
+@pytest.mark.parametrize("name,text,decls,wrt", JAC_CASES, ids=[c[0] for c in JAC_CASES])
+@pytest.mark.parametrize("seed", [0, 1])
+def test_jacobians_match_interpreter(name, text, decls, wrt, seed):
+    # the gradient API on a tensor-valued program (the one-hot seed of
+    # Section 4.3) against the interpreter's one-key forward mode: the
+    # Jacobian, output keys first
+    rng = np.random.default_rng(40 + seed)
+    arrays, env, _ = setup_inputs(rng, decls, 6 if name != "trace" else 12)
+    prog = S.compile(text, **decls)
+    vshape = value_shape(prog, decls)
+    np.testing.assert_allclose(eval_terms(prog, prog.value, arrays),
+                               dense_of_dict(dict(ref.leaves(ref.value(text, env)))
+                                             if vshape else {(): ref.value(text, env)}, vshape),
+                               rtol=1e-12, atol=1e-12)
+    for x in wrt:
+        J = eval_terms(prog, prog.gradient(x), arrays)
+        want = dense_of_dict(ref.jacobian(text, env, x), vshape + decls[x].shape)
+        if J is None:
+            J = np.zeros(want.shape)
+        np.testing.assert_allclose(J, want, rtol=1e-11, atol=1e-12, err_msg=f"d/d{x}")
+
+
+def random_tangent(rng, d, arrays, name):
+    """A dense tangent of input `name` (zero off a sparse input's keys)."""
+    if isinstance(d, S.Dense) and not d.shape:
+        return np.asarray(float(rng.standard_normal()))
+    t = rng.standard_normal(d.shape)
+    if isinstance(d, (S.Sparse, S.SparseVec)):
+        t = t * arrays["#mask:" + name]
+    return t
+
+
+def tangent_dict(a, mask=None):
+    """A dense tangent batch [m, ...] as the interpreter's tangent: the
+    input's key paths followed by the batch key (stored keys only)."""
+    out = {}
+    for idx in np.ndindex(*a.shape[1:]):
+        if mask is not None and mask[idx] == 0:
+            continue
+        leaf = {t: float(a[(t,) + idx]) for t in range(a.shape[0])}
+        d = out
+        for k in idx[:-1]:
+            d = d.setdefault(int(k), {})
+        if idx:
+            d[int(idx[-1])] = leaf
+        else:
+            out = leaf
+    return out
+
+
+@pytest.mark.parametrize("name,text,decls,wrt", JAC_CASES, ids=[c[0] for c in JAC_CASES])
+def test_jvp_terms_match_the_batched_forward_mode(name, text, decls, wrt):
+    # J V for a batch of three tangents along all inputs at once: the
+    # directional-derivative terms (one tangent per evaluation) against the
+    # interpreter's tensorized forward mode with the whole batch as tau
+    # levels, and against the one-key Jacobians contracted with V
+    rng = np.random.default_rng(50)
+    arrays, env, _ = setup_inputs(rng, decls, 6 if name != "trace" else 12)
+    prog = S.compile(text, **decls)
+    vshape = value_shape(prog, decls)
+    m = 3
+    V = {x: np.stack([random_tangent(rng, decls[x], arrays, x) for _ in range(m)]) for x in wrt}
+    T = prog.jvp_terms(wrt)
+    got = []
+    for t in range(m):
+        a = dict(arrays)
+        for x in wrt:
+            a[prog.seed_of(x)] = V[x][t]
+        r = eval_terms(prog, T, a)
+        got.append(np.zeros(vshape) if r is None else r)
+    got = np.stack(got)
+    tangents = {x: tangent_dict(V[x], arrays.get("#mask:" + x)) for x in wrt}
+    lit = ref.jvp_tensorized(text, env, tangents)
+    want = np.zeros((m,) + vshape)
+    for key, v in lit.items():
+        want[(key[-1],) + key[:-1]] += v
+    np.testing.assert_allclose(got, want, rtol=1e-11, atol=1e-12)
+    contracted = np.zeros((m,) + vshape)
+    for x in wrt:
+        J = dense_of_dict(ref.jacobian(text, env, x), vshape + decls[x].shape)
+        nx = len(decls[x].shape)
+        for t in range(m):
+            contracted[t] += np.tensordot(J, V[x][t], axes=nx) if nx else J * V[x][t]
+    np.testing.assert_allclose(got, contracted, rtol=1e-11, atol=1e-12)
+
+
+def test_jacobian_layouts_are_the_stored_keys():
+    # each Jacobian is a value array on one input's stored keys; the key map
+    # says which coordinate of the stored key each output position takes
+    p = S.compile(VVA, V1=S.SparseVec(9), V2=S.SparseVec(9)).plan(("V1",), fuse=False)
+    assert p.layout("value")[:2] == ("dense", None)
+    assert p.layout("dV1")[:3] == ("pattern", "V1", (0, 0))
+    p = S.compile(MATVEC, M=S.Sparse(5, 6), x=S.Dense(6)).plan(("x", "M"), fuse=False)
+    assert p.layout("dx")[:3] == ("pattern", "M", (0, 1))
+    assert p.layout("dM")[:3] == ("pattern", "M", (0, 0, 1))
+    assert p.kernels() == ["spmm", "axpby", "sddmm"]
+    p = S.compile(MATSQ, M=S.Sparse(5, 6), x=S.Dense(6), s=S.Dense()).plan(("M", "x", "s"),
+                                                                           fuse=False)
+    assert p.layout("value")[:3] == ("pattern", "M", (0, 1))
+    assert p.layout("dM")[:3] == ("pattern", "M", (0, 1, 0, 1))
+    assert set(p.kernels()) == {"scale"}
+    dM = [c for c in p.calls if c.out == "dM"]
+    assert len(dM) == 1 and dM[0].args["alpha"] == 2.0 and dM[0].args["s1"] == "s" \
+        and dM[0].args["x2_idx"] == ("cols", "M")
+
+
+def test_vsm_jacobians_lower_to_one_scale_each():
+    p = S.compile(VSM, V=S.SparseVec(9), s=S.Dense()).plan(("s", "V"), fuse=False)
+    assert p.kernels() == ["scale", "scale", "scale"]
+    ds, dV = p.calls[1], p.calls[2]
+    assert (ds.args["alpha"], ds.args["s1"], ds.args["s2"], ds.args["x1"]) == (2.0, "s", None, "V")
+    assert (dV.args["s1"], dV.args["s2"], dV.args["x1"]) == ("s", "s", None)
+
+
+def test_matrix_product_jvp_is_one_batched_call():
+    prog = S.compile(SPMM, A=S.Sparse(5, 6), B=S.Dense(6, 3))
+    p = prog.jvp_plan(("A", "B"))
+    assert p.kernels() == ["spmm_jvp_batch"] and not p.per_tangent
+    assert p.calls[0].args["dA"] == "A'" and p.calls[0].args["dB"] == "B'"
+    p = prog.jvp_plan(("B",))
+    assert p.calls[0].args["dA"] is None
+    p = prog.jvp_plan(("A", "B"), fuse=False)
+    assert p.per_tangent and p.kernels() == ["spmm", "spmm", "axpby"]

@@ -418,3 +418,82 @@ def test_jacobian_matches_central_differences():
             for out in hi:
                 fd = (hi[out] - lo[out]) / (2 * h)
                 assert J.get(out + key, 0.0) == pytest.approx(fd, rel=1e-6, abs=1e-8), (wrt, key)
+
+
+# ------------------------------------- batched tangents (J V, Section 4.2)
+
+
+def _batch_tangent(rng, x, m):
+    """Random tangents of a dictionary x: its key paths, then the batch key."""
+    out = {}
+    for path, _ in ref.leaves(x):
+        leaf = {t: float(rng.standard_normal()) for t in range(m)}
+        d = out
+        for k in path[:-1]:
+            d = d.setdefault(k, {})
+        if path:
+            d[path[-1]] = leaf
+        else:
+            out = leaf
+    return out
+
+
+def test_batched_tangents_match_central_differences():
+    # the tangent along each direction of the batch against central
+    # differences of the output dictionary along that direction
+    text = "sum(<i,v> in V) {i -> sin(v * W(i)) + v * v * W(i)}"
+    rng = np.random.default_rng(60)
+    env = {"V": sparse_vector(rng, 12, 6), "W": ref.dense_dict(rng.standard_normal(12))}
+    m, h = 3, 1e-5
+    tans = {"V": _batch_tangent(rng, env["V"], m), "W": _batch_tangent(rng, env["W"], m)}
+    got = ref.jvp_tensorized(text, env, tans)
+    for t in range(m):
+        def moved(eps):
+            e2 = {n: ref._replace_leaves(env[n], lambda key, v, n=n: v + eps * _at(tans[n], key)[t])
+                  for n in env}
+            return dict(ref.leaves(ref.value(text, e2)))
+
+        hi, lo = moved(h), moved(-h)
+        for out in hi:
+            fd = (hi[out] - lo[out]) / (2 * h)
+            assert got.get(out + (t,), 0.0) == pytest.approx(fd, rel=1e-6, abs=1e-8), (out, t)
+
+
+def _at(d, key):
+    for k in key:
+        d = d[k]
+    return d
+
+
+def test_batched_tangents_equal_the_one_key_jacobian_times_V():
+    # J V from the per-key forward mode (one evaluation per stored key of
+    # each input, then contracted with the batch) for a matrix program
+    rng = np.random.default_rng(61)
+    M = {i: sparse_vector(rng, 7, int(rng.integers(1, 5))) for i in range(6) if i != 2}
+    env = {"M": M, "x": ref.dense_dict(rng.standard_normal(7)), "s": 0.75}
+    text = "sum(<i,r> in M) {i -> sum(<j,a> in r) {j -> a * a * x(j) * s}}"
+    m = 4
+    tans = {n: _batch_tangent(rng, env[n], m) for n in ("M", "x", "s")}
+    got = ref.jvp_tensorized(text, env, tans)
+    want = {}
+    for n in ("M", "x", "s"):
+        for key, v in ref.jacobian(text, env, n).items():
+            # the output keys (i, j), then n's key (none for the real s)
+            for t in range(m):
+                out = key[:2] + (t,)
+                want[out] = want.get(out, 0.0) + v * _at(tans[n], key[2:])[t]
+    assert set(want) == set(got)
+    for key, v in want.items():
+        assert got.get(key, 0.0) == pytest.approx(v, rel=1e-12, abs=1e-14), key
+
+
+def test_batched_tangents_are_linear_in_the_tangents():
+    rng = np.random.default_rng(62)
+    env = {"V": sparse_vector(rng, 20, 7), "s": -1.3}
+    text = "sum(<i,v> in V) {i -> v * s * s}"
+    a, b = _batch_tangent(rng, env["V"], 2), _batch_tangent(rng, env["V"], 2)
+    ab = {k: {t: a[k][t] + 2.0 * b[k][t] for t in range(2)} for k in a}
+    ga, gb = ref.jvp_tensorized(text, env, {"V": a}), ref.jvp_tensorized(text, env, {"V": b})
+    gab = ref.jvp_tensorized(text, env, {"V": ab})
+    for key in gab:
+        assert gab[key] == pytest.approx(ga[key] + 2.0 * gb[key], rel=1e-12, abs=1e-14)
