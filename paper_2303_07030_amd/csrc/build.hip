@@ -194,6 +194,18 @@ __global__ __launch_bounds__(kSortThreads) void radix_hist_kernel(const int32_t 
     hist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = cnt[threadIdx.x];
 }
 
+// Workgroups go to the eight XCDs round-robin (block b on XCD b mod 8), each
+// XCD with its own L2.  This renumbers the blocks so that every XCD takes one
+// contiguous range of the tiles: neighbouring tiles write adjacent runs of
+// one output region, and with the renumbering those runs meet in one L2 and
+// leave it as whole lines instead of partial ones from eight L2s.
+__device__ __forceinline__ int64_t xcd_contiguous_tile() {
+    const int nb = (int)gridDim.x, b = (int)blockIdx.x, x = b % 8;
+    int start = 0;
+    for (int y = 0; y < x; ++y) start += (nb - y + 7) / 8;  // blocks on XCDs before x
+    return start + b / 8;
+}
+
 // Stable scatter of one tile.  Wave w owns the tile's elements
 // [w * 1024, (w + 1) * 1024) and walks them in 16 rounds of 64 consecutive
 // elements, so (wave, round, lane) order is input order.  Inside a round the
@@ -212,11 +224,12 @@ __global__ __launch_bounds__(kSortThreads) void radix_scatter_kernel(
     __shared__ int sval[kSortTile];
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
+    const int64_t tile = xcd_contiguous_tile();
     for (int w = 0; w < kSortWaves; ++w) wcnt[w][threadIdx.x] = 0;
-    tile_off[threadIdx.x] = offs[(int64_t)threadIdx.x * ntiles + blockIdx.x];
+    tile_off[threadIdx.x] = offs[(int64_t)threadIdx.x * ntiles + tile];
     __syncthreads();
 
-    const int64_t tile0 = (int64_t)blockIdx.x * kSortTile;
+    const int64_t tile0 = tile * kSortTile;
     const int64_t base = tile0 + (int64_t)wave * (kSortRounds * kWave);
     int key[kSortRounds], val[kSortRounds], rank[kSortRounds], dig[kSortRounds];
 #pragma unroll

@@ -36,6 +36,19 @@ static int64_t perm_tiles(int64_t n) { return ceil_div(n, kPermTile); }
 
 // ------------------------------------------------------------- apply
 
+// Workgroups go to the eight XCDs round-robin (block b on XCD b mod 8), each
+// XCD with its own L2.  This renumbers the blocks so that every XCD takes one
+// contiguous range of the tiles: neighbouring tiles write adjacent runs of
+// one output region, and with the renumbering those runs meet in one L2 and
+// leave it as whole lines instead of partial ones from eight L2s.
+__device__ __forceinline__ int64_t xcd_contiguous_tile() {
+    const int nb = (int)gridDim.x, b = (int)blockIdx.x, x = b % 8;
+    int start = 0;
+    for (int y = 0; y < x; ++y) start += (nb - y + 7) / 8;  // blocks on XCDs before x
+    return start + b / 8;
+}
+
+
 // Each thread handles kPermPer elements of its tile, strided by the block
 // size, in batches of kPermBatch whose loads are all issued before any is
 // used (one memory round trip per batch, not per element).
@@ -48,7 +61,7 @@ __global__ __launch_bounds__(kPermThreads) void perm_pass1_kernel(int64_t n, con
                                                                   const uint16_t *src_local,
                                                                   float *staging) {
     __shared__ float tile[kPermTile];
-    const int64_t t0 = (int64_t)blockIdx.x * kPermTile;
+    const int64_t t0 = xcd_contiguous_tile() * kPermTile;
     const int len = (int)min((int64_t)kPermTile, n - t0);
     const int tid = threadIdx.x;
     for (int b = 0; b < kPermPer; b += kPermBatch) {
