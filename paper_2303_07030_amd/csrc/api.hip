@@ -241,6 +241,26 @@ static nsd_status finish_loss(const SddmmParams &p, double *loss, hipStream_t st
 // partials of the column plan and the loss partials; with valT, gradT and
 // staging (nnz floats each) A's values are moved to CSC order and the sparse
 // gradient back by the CSC's two-pass permutations.
+// With the CSC's two-pass permutations (large patterns), a column pass reads
+// A's values moved to CSC order and writes its sampled products there, so
+// its entry positions are its own slots; csc_order_after moves the products
+// back to A's order.  Without them the pass reads and writes through perm.
+static nsd_status csc_order_before(const nsd_csr *A, const nsd_csc *At, float *valT,
+                                   float *gradT, float *staging, DualPass &pass, hipStream_t st) {
+    if (!valT) return NSD_OK;
+    NSD_TRY(nsd_permute_f32(&At->to_csc, A->val, valT, staging, st));
+    pass.s.w = valT;
+    pass.s.wperm = nullptr;
+    pass.sdd = gradT;
+    return NSD_OK;
+}
+
+static nsd_status csc_order_after(const nsd_csc *At, float *valT, const float *gradT,
+                                  float *staging, float *dA, hipStream_t st) {
+    if (!valT) return NSD_OK;
+    return nsd_permute_f32(&At->to_csr, gradT, dA, staging, st);
+}
+
 static nsd_status bilinear_run(const nsd_csr *A, const nsd_csc *At, const float *H,
                                const float *G, int k, float seed, double *loss, float *dA,
                                float *dH, float *part_col, double *loss_part, hipStream_t st,
@@ -251,15 +271,9 @@ static nsd_status bilinear_run(const nsd_csr *A, const nsd_csc *At, const float 
         // dA[p] = seed <G_i, H_j>, loss = sum_p A_p <G_i, H_j>, dH = seed A^T G
         DualPass pass = col_dual(A, At, G, H, k, seed, dH, part_col, dA, seed, true);
         if (col_dual_ok(pass)) {
-            if (!valT) return col_dual_loss(pass, loss_part, loss, st);
-            // values read and the gradient written in CSC order: the pass's
-            // entry positions are then its own slots
-            NSD_TRY(nsd_permute_f32(&At->to_csc, A->val, valT, staging, st));
-            pass.s.w = valT;
-            pass.s.wperm = nullptr;
-            pass.sdd = gradT;
+            NSD_TRY(csc_order_before(A, At, valT, gradT, staging, pass, st));
             NSD_TRY(col_dual_loss(pass, loss_part, loss, st));
-            return nsd_permute_f32(&At->to_csr, gradT, dA, staging, st);
+            return csc_order_after(At, valT, gradT, staging, dA, st);
         }
     }
     // dA = seed * <G_i, H_j>; loss = sum_p A_p <G_i, H_j>
@@ -413,7 +427,9 @@ nsd_status nsd_loss_frob_spmm(const nsd_csr *A, const nsd_csc *At, const float *
         f.loss_part = w.loss_part;
         f.seg_loss = w.seg_loss;
         f.loss = loss;
-        return frob_fused(f, st);
+        NSD_TRY(csc_order_before(A, At, w.valT, w.gradT, w.staging, f.cols, st));
+        NSD_TRY(frob_fused(f, st));
+        return csc_order_after(At, w.valT, w.gradT, w.staging, dA, st);
     }
     // forward: C = A B
     NSD_TRY(segreduce(rows_params(A, B, k, 1.f, C, w.part), st));
@@ -469,13 +485,15 @@ nsd_status nsd_spmm_vjp(const nsd_csr *A, const nsd_csc *At, const float *X, con
     if (A->nnz > 0) {
         // one pass over the columns: own row X_j, gathered row G_i (NULL:
         // ones): dA[p] = <G_i, X_j>, dX = A^T G; no loss
-        const DualPass pass = col_dual(A, At, G, X, k, 1.f, dX, w.part_col, dA, 1.f, false);
+        DualPass pass = col_dual(A, At, G, X, k, 1.f, dX, w.part_col, dA, 1.f, false);
         if (col_dual_ok(pass)) {
+            NSD_TRY(csc_order_before(A, At, w.valT, w.gradT, w.staging, pass, st));
             DualParams f;
             f.pass[0] = pass;
             f.npass = 1;
             f.loss_part = w.loss_part;
-            return dual_fused(kDualLin, f, NSD_KERNEL_DUAL, LossJob{}, st);
+            NSD_TRY(dual_fused(kDualLin, f, NSD_KERNEL_DUAL, LossJob{}, st));
+            return csc_order_after(At, w.valT, w.gradT, w.staging, dA, st);
         }
         NSD_TRY(sddmm(sddmm_params(A, G, X, k, 1.f, dA), st));
     }

@@ -1,7 +1,8 @@
 """The two-pass value permutation (nsd_perm_plan_build / nsd_permute_f32)
 against its definition, dst[q] = src[perm[q]] (and the inverse form),
-bit for bit; and the bilinear layer through a CSC that carries the two-pass
-forms of its permutation against the same layer without them."""
+bit for bit; and the bilinear layer, the SpMM VJP and the Frobenius loss
+through a CSC that carries the two-pass forms of its permutation against
+the same calls without them."""
 import numpy as np
 import pytest
 import torch
@@ -104,3 +105,36 @@ def test_bilinear_with_perm_plans_equals_without(nsd, orc, k):
     rows = np.repeat(np.arange(nrows, dtype=np.int32), np.diff(rowptr))
     ref, mag = orc.sddmm(D, G.cpu().numpy(), H.cpu().numpy(), k, rows, colind, alpha=0.75)
     assert_mag_close(out[1][1], ref, mag, what="dA")
+
+
+@pytest.mark.parametrize("k", [1, 64])
+def test_vjp_and_frob_with_perm_plans_equal_without(nsd, k):
+    """The SpMM VJP and the Frobenius loss take the same moves around their
+    column pass: the same bits as through perm."""
+    from test_gpu_parity import make_csr
+    from paper_2303_07030_amd.operand import DeviceCsr
+    rng = np.random.default_rng(100 + k)
+    nrows, ncols = 2500, 3000
+    lengths = np.minimum((25 * rng.pareto(1.05, nrows)).astype(np.int64), ncols)
+    lengths[rng.random(nrows) < 0.1] = 0
+    rowptr, colind, val = make_csr(rng, nrows, ncols, lengths, hot_col=3)
+    X = torch.from_numpy(rng.standard_normal((ncols, k)).astype(np.float32)).cuda()
+    G = torch.from_numpy(rng.standard_normal((nrows, k)).astype(np.float32)).cuda()
+    out = []
+    for plans in (False, True):
+        A = DeviceCsr(nrows, ncols, rowptr, colind, val, k_hint=k, perm_plans=plans)
+        assert (A.csc.to_csc.n == A.nnz) == plans
+        dA = torch.full((A.nnz,), np.nan, dtype=torch.float32, device="cuda")
+        dX = torch.full((ncols, k), np.nan, dtype=torch.float32, device="cuda")
+        nsd.nsd_spmm_vjp(A.desc, A.csc, X, G, k, dA, dX, A.workspace(k))
+        loss = torch.empty(1, dtype=torch.float64, device="cuda")
+        C = torch.full((nrows, k), np.nan, dtype=torch.float32, device="cuda")
+        fA = torch.full((A.nnz,), np.nan, dtype=torch.float32, device="cuda")
+        fB = torch.full((ncols, k), np.nan, dtype=torch.float32, device="cuda")
+        nsd.nsd_loss_frob_spmm(A.desc, A.csc, X, k, 1.0, C, loss, fA, fB, A.workspace(k))
+        torch.cuda.synchronize()
+        out.append([t.cpu().numpy() for t in (dA, dX, loss, C, fA, fB)])
+    for a, b in zip(*out):
+        assert np.array_equal(a.view(np.uint8), b.view(np.uint8))
+    assert not np.isnan(out[1][0]).any() and not np.isnan(out[1][4]).any()
+
