@@ -30,6 +30,7 @@ MATVEC = "sum(<i,r> in M) {i -> sum(<j,a> in r) a * x(j)}"
 MATSQ = "sum(<i,r> in M) {i -> sum(<j,a> in r) {j -> a * a * x(j) * s}}"
 TRACE = "sum(<i,r> in M) r(i)"
 SPMM = "sum(<i,r> in A) {i -> sum(<j,a> in r) sum(<c,b> in B(j)) {c -> a * b}}"
+SAMPLED = ("sum(<i,r> in A) {i -> sum(<j,a> in r) {j -> a * sum(<c,x> in X(i)) x * Y(j)(c)}}")
 
 
 @pytest.fixture(scope="module")
@@ -311,6 +312,36 @@ def test_jvp_of_a_matrix_valued_program(S):
     compare(as_dict(lay, host(out["value"]), {"M": (rows, colind)}),
             dict(ref.leaves(ref.value(MATSQ, env))),
             dict(ref.leaves(ref.value(MATSQ, abs_env(env)))), "value")
+
+
+@pytest.mark.parametrize("k", [1, 8, 33])
+def test_jvp_of_a_sampled_product(S, k):
+    # J V over the SDDMM kernel: tangents of A(i,j) <X(i), Y(j)> on A's keys
+    # along A, X and Y at once, against the batched forward mode
+    A, rowptr, colind, val, rows = matrix(7)
+    rng = np.random.default_rng(70 + k)
+    X = rng.standard_normal((A.nrows, k)).astype(np.float32)
+    Y = rng.standard_normal((A.ncols, k)).astype(np.float32)
+    m = 3
+    prog = S.compile(SAMPLED, A=S.Sparse(A.nrows, A.ncols), X=S.Dense(A.nrows, k),
+                     Y=S.Dense(A.ncols, k))
+    TA = rng.standard_normal((m, A.nnz)).astype(np.float32)
+    TX = rng.standard_normal((m, A.nrows, k)).astype(np.float32)
+    TY = rng.standard_normal((m, A.ncols, k)).astype(np.float32)
+    out = prog.jvp({"A": A, "X": dev(X), "Y": dev(Y)},
+                   {"A": dev(TA), "X": dev(TX), "Y": dev(TY)})
+    env = {"A": ref.csr_dict(rowptr, colind, val.astype(np.float64)), "X": ref.dense_dict(X),
+           "Y": ref.dense_dict(Y)}
+    tans = {"A": batch_dict(TA, (rows, colind)), "X": batch_dict(TX), "Y": batch_dict(TY)}
+    want = ref.jvp_tensorized(SAMPLED, env, tans)
+    wmag = ref.jvp_tensorized(SAMPLED, abs_env(env),
+                              {x: ref._replace_leaves(v, lambda _, y: abs(y))
+                               for x, v in tans.items()})
+    lay = prog.jvp_plan(("A", "X", "Y")).layout("tangent")
+    coords = {"A": (rows, colind)}
+    compare(tangent_result(lay, host(out["tangent"]), coords), want, wmag, "tangent")
+    compare(as_dict(lay, host(out["value"]), coords), dict(ref.leaves(ref.value(SAMPLED, env))),
+            dict(ref.leaves(ref.value(SAMPLED, abs_env(env)))), "value")
 
 
 @pytest.mark.parametrize("wrt", [("A", "B"), ("A",), ("B",)])

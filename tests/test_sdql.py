@@ -39,6 +39,8 @@ VSM = "sum(<i,v> in V) {i -> v * s * s}"
 MATVEC = "sum(<i,r> in M) {i -> sum(<j,a> in r) a * x(j)}"
 MATSQ = "sum(<i,r> in M) {i -> sum(<j,a> in r) {j -> a * a * x(j) * s}}"
 SPMM = "sum(<i,r> in A) {i -> sum(<j,a> in r) sum(<c,b> in B(j)) {c -> a * b}}"
+# a matrix-valued sampled product on A's keys: A(i,j) <X(i), Y(j)>
+SAMPLED = ("sum(<i,r> in A) {i -> sum(<j,a> in r) {j -> a * sum(<c,x> in X(i)) x * Y(j)(c)}}")
 
 
 def rand_csr(rng, nr, nc, nnz):
@@ -368,6 +370,8 @@ JAC_CASES = [
     ("matvec", MATVEC, dict(M=S.Sparse(5, 6), x=S.Dense(6)), ("x", "M")),
     ("matsq", MATSQ, dict(M=S.Sparse(5, 6), x=S.Dense(6), s=S.Dense()), ("M", "x", "s")),
     ("trace", TRACE, dict(M=S.Sparse(5, 5)), ("M",)),
+    ("sampled", SAMPLED, dict(A=S.Sparse(5, 6), X=S.Dense(5, 3), Y=S.Dense(6, 3)),
+     ("A", "X", "Y")),
 ]
 
 
@@ -506,3 +510,16 @@ def test_matrix_product_jvp_is_one_batched_call():
     assert p.calls[0].args["dA"] is None
     p = prog.jvp_plan(("A", "B"), fuse=False)
     assert p.per_tangent and p.kernels() == ["spmm", "spmm", "axpby"]
+
+
+def test_sampled_product_tangents_lower_to_sddmm():
+    # J V of the matrix-valued sampled product: each tangent is an SDDMM on
+    # A's keys times A's values (or A's tangent times the SDDMM)
+    prog = S.compile(SAMPLED, A=S.Sparse(5, 6), X=S.Dense(5, 3), Y=S.Dense(6, 3))
+    p = prog.jvp_plan(("A", "X", "Y"))
+    assert p.per_tangent and p.layout("tangent")[:3] == ("pattern", "A", (0, 1))
+    assert p.kernels().count("sddmm") == 3 and set(p.kernels()) <= {"sddmm", "scale"}
+    # its Jacobian w.r.t. X has order 4 on no input's keys
+    with pytest.raises(S.NotLowerable, match="jvp"):
+        prog.plan(("X",), fuse=False)
+
