@@ -644,8 +644,10 @@ nsd_status nsd_diag_keys(const nsd_csr *A, float alpha, float *out, void *stream
  * x1, x2: device floats (NULL: ones), x1 aligned with the n keys; x2_idx
  * gathers x2 (a dense operand read at each key's row, column or index).
  * y_idx scatters into a dense y and must hold n distinct indices (each
- * output is written once).  beta == 0: y is not read.  The product is
- * formed in double and rounded once.  The Jacobians of the vector kernels
+ * output is written once); the indices are not checked (out of range or
+ * repeated ones are undefined, as a malformed operand of any hot-path call
+ * is).  beta == 0: y is not read.  The product is formed in double and
+ * rounded once.  The Jacobians of the vector kernels
  * of Section 7.1 and of matrix-valued programs on a matrix's keys reduce to
  * this.  Async.
  */
