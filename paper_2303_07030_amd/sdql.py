@@ -1656,6 +1656,8 @@ def _execute_jvp(plan: Plan, inputs: dict, tangents: dict, value, stream):
     import torch
 
     prog = plan.prog
+    if not tangents:
+        raise SdqlError("jvp needs the tangents of at least one input")
     ms = {int(v.shape[0]) for v in tangents.values()}
     if len(ms) != 1:
         raise SdqlError(f"tangents of different batch sizes {sorted(ms)}")
