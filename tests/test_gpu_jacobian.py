@@ -376,6 +376,47 @@ def test_jvp_of_the_matrix_product(S, orc, wrt, k):
             assert_mag_close(host(fused["value"]).reshape(A.nrows, k), C, Cm, what="C")
 
 
+def test_jvp_of_real_valued_losses_is_the_gradient_along_each_tangent(S, orc):
+    # forward mode against reverse mode: the tangent of a loss along v is
+    # <grad L, v> (Section 6, the differential), with the gradients from
+    # the C oracle; the magnitude is sum |terms of grad| * |v|
+    from test_sdql import FROB, GNN
+    A, rowptr, colind, val, rows = matrix(9, 700, 900)
+    rng = np.random.default_rng(9)
+    k, m = 16, 4
+    D = orc.Dok((A.nrows, A.ncols), (rows, colind), val)
+    TA = rng.standard_normal((m, A.nnz)).astype(np.float32)
+    # 1/2 ||A B||^2 along A and B
+    B = rng.standard_normal((A.ncols, k)).astype(np.float32)
+    TB = rng.standard_normal((m, A.ncols, k)).astype(np.float32)
+    prog = S.compile(FROB, A=S.Sparse(A.nrows, A.ncols), B=S.Dense(A.ncols, k))
+    got = host(prog.jvp({"A": A, "B": dev(B)}, {"A": dev(TA), "B": dev(TB)})["tangent"])
+    C, Cm = orc.spmm(D, B, k)
+    gA, gAm = orc.sddmm(D, C, B, k, rows, colind, Xmag=Cm)
+    gB, gBm = orc.spmm_t(D, C, k, Gmag=Cm)
+    for t in range(m):
+        want = gA @ TA[t].astype(np.float64) + np.sum(gB * TB[t])
+        mag = gAm @ np.abs(TA[t]).astype(np.float64) + np.sum(gBm * np.abs(TB[t]))
+        assert_mag_close(got[t], want, mag, what=f"frob tangent {t}")
+    # the GNN layer's loss along A, H and G
+    H = rng.standard_normal((A.ncols, k)).astype(np.float32)
+    G = rng.standard_normal((A.nrows, k)).astype(np.float32)
+    TH = rng.standard_normal((m, A.ncols, k)).astype(np.float32)
+    TG = rng.standard_normal((m, A.nrows, k)).astype(np.float32)
+    prog = S.compile(GNN, A=S.Sparse(A.nrows, A.ncols), H=S.Dense(A.ncols, k),
+                     G=S.Dense(A.nrows, k))
+    got = host(prog.jvp({"A": A, "H": dev(H), "G": dev(G)},
+                        {"A": dev(TA), "H": dev(TH), "G": dev(TG)})["tangent"])
+    gA, gAm = orc.sddmm(D, G, H, k, rows, colind)
+    gH, gHm = orc.spmm_t(D, G, k)
+    gG, gGm = orc.spmm(D, H, k)
+    for t in range(m):
+        want = (gA @ TA[t].astype(np.float64) + np.sum(gH * TH[t]) + np.sum(gG * TG[t]))
+        mag = (gAm @ np.abs(TA[t]).astype(np.float64) + np.sum(gHm * np.abs(TH[t]))
+               + np.sum(gGm * np.abs(TG[t])))
+        assert_mag_close(got[t], want, mag, what=f"gnn tangent {t}")
+
+
 # ------------------------------------------------ the C-ABI entry points
 
 
