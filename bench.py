@@ -87,7 +87,7 @@ def parse():
 KERNEL_SOURCE = {"frob_row": "segreduce.hip", "sgr_main": "segreduce.hip",
                  "sddmm": "segreduce.hip", "frob_col": "dual.hip", "dual": "dual.hip",
                  "mf": "dual.hip", "cp": "cp.hip", "sort": "build.hip", "jvp": "jvp.hip",
-                 "cpn": "cpn.hip", "perm": "perm.hip"}
+                 "cpn": "cpn.hip", "perm": "perm.hip", "batax_rows": "batax.hip"}
 
 
 def source_digest(kernel=None):
@@ -299,8 +299,9 @@ def setup_build(d, dev, torch, nsd, ops):
 
 def setup_batax(d, dev, torch, nsd, ops):
     """Jacobian of the BATAX kernel, J = beta A^T A (an output pattern that
-    is not an input's): expand the products of every row, two stable radix
-    sorts, runs, and fixed-order run sums."""
+    is not an input's): A's CSC, then each row of J gathered, sorted in LDS
+    and summed in fixed order (rows of at most 512 terms; else every product
+    expanded and sorted twice through HBM)."""
     A = ops.DeviceCsr(d["nrows"], d["ncols"], d["rowptr"], d["colind"], d["val"], device=dev,
                       build_csc=False)
     ws0 = torch.empty(256, dtype=torch.uint8, device=dev)
@@ -316,10 +317,15 @@ def setup_batax(d, dev, torch, nsd, ops):
     S.A, S.nnz, S.k = A, nk, 0
     S.step = lambda: nsd.nsd_batax_jacobian(A.desc, d["beta"], P, jrowptr, jcol, jval, ws)
     S.pairs = P
-    # scatter passes over the P products: by k, then by j (with payload)
+    nnz = A.nnz
+    # the CSC of A: a radix sort of the nnz column indices (index payload)
     p = _sort_passes(n)
-    launches = 2 * p
-    S.kernels = {"sort": (16 * P * launches - 4 * P) / launches}
+    S.kernels = {"sort": (16 * nnz * p - 4 * nnz) / p,
+                 # per stored entry: the CSC slot's row and CSR slot, the
+                 # row's bounds and a_ij (20 B); per product: k and a_ik
+                 # (8 B); per key of J: its column and value (8 B); per row
+                 # of J: its column bounds and key count
+                 "batax_rows": 20 * nnz + 8 * P + 8 * nk + 12 * n}
     return S
 
 

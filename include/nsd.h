@@ -232,7 +232,8 @@ typedef enum nsd_kernel_id {
     NSD_KERNEL_SORT = 11,      /* radix-sort scatter pass of the builders */
     NSD_KERNEL_JVP = 12,       /* forward-mode tangent of the matrix product */
     NSD_KERNEL_CPN = 13,       /* order-N CP mode passes */
-    NSD_KERNEL_PERM = 14       /* the two passes of a value permutation */
+    NSD_KERNEL_PERM = 14,      /* the two passes of a value permutation */
+    NSD_KERNEL_BATAX_ROWS = 15 /* rows of the BATAX Jacobian built in LDS */
 } nsd_kernel_id;
 
 /*
@@ -771,6 +772,11 @@ nsd_status nsd_spmm_jvp_batch(const nsd_csr *A, int32_t m, const float *dAval, c
  *                            the products in row order of A, accumulated in
  *                            fp64 and rounded once (reproducible).
  *                            Synchronous.
+ * Two ways give the same bits.  When every row of J has at most 512 terms,
+ * J is built row by row (row j gathers the rows of A storing column j, its
+ * terms sorted by column in LDS); otherwise every term is expanded and
+ * sorted twice through HBM.  The environment variable NSD_BATAX_ROW_CAP
+ * lowers the 512 (0: always the second way).
  * Errors: NSD_ERR_TOO_LARGE when npairs >= 2^30; NSD_ERR_INVALID_ARG when
  * npairs differs from A's (nothing is written then but workspace).
  */

@@ -19,7 +19,18 @@
 //      its diagonal run a serial tail, which the fixed order accepts.)
 // Keys are structural: a pair whose product is 0 keeps its key, as the
 // dictionary insert of the paper's program does.
+//
+// When every row of J has at most a few hundred terms (the common case), a
+// second path builds J row by row instead, the GPU form of the per-row
+// dictionary: row j gathers the rows i of A that store column j (A's CSC,
+// ascending i); one wave lays their terms (beta a_ij) a_ik out in LDS in
+// that order, sorts them stably by k (a bitonic sort of (k, position)
+// pairs), and sums each run of equal k in fp64 in order.  These are the
+// same terms, summed in the same order, as the sort path's, so both give
+// the same bits; the row path reads A and writes J a few times instead of
+// sorting every term twice through HBM.
 #include <algorithm>
+#include <cstdlib>
 
 #include "nsd_internal.hpp"
 
@@ -110,6 +121,294 @@ __global__ void run_sums_kernel(int32_t nruns, const int32_t *runptr, const int3
     jval[r] = (float)s;
 }
 
+// ------------------------------------------------------- row path
+
+constexpr int kRowCap = 512;     // terms of one row of J held in LDS (a power of two)
+constexpr int kRowThreads = 64;  // one wave per row of J
+// The row path takes rows of J with at most this many terms: kRowCap, or
+// less when the environment says so (NSD_BATAX_ROW_CAP; 0 keeps every call
+// on the sort path).
+static int row_cap() {
+    const char *e = std::getenv("NSD_BATAX_ROW_CAP");
+    if (!e) return kRowCap;
+    const int v = std::atoi(e);
+    return v < 0 ? 0 : std::min(v, kRowCap);
+}
+
+// row[c] = the row of A holding CSR slot slot[c]: the last r with
+// rowptr[r] <= slot[c] (an empty row shares its start with the next).
+__global__ void slot_rows_kernel(int64_t n, int32_t nrows, const int32_t *rowptr,
+                                 const int32_t *slot, int32_t *row) {
+    const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= n) return;
+    const int32_t p = slot[c];
+    int32_t lo = 0, hi = nrows - 1;
+    while (lo < hi) {
+        const int32_t mid = lo + (hi - lo + 1) / 2;
+        if (rowptr[mid] <= p) lo = mid;
+        else hi = mid - 1;
+    }
+    row[c] = lo;
+}
+
+// terms[j] = number of terms of row j of J: the summed lengths of the rows
+// of A storing column j; the largest goes to *mx (integer maximum: any order).
+__global__ void row_terms_kernel(int32_t ncols, const int32_t *colptr, const int32_t *crow,
+                                 const int32_t *rowptr, int32_t *terms, int32_t *mx) {
+    const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    int32_t t = 0;
+    if (j < ncols) {
+        for (int32_t c = colptr[j]; c < colptr[j + 1]; ++c) {
+            const int32_t i = crow[c];
+            t += rowptr[i + 1] - rowptr[i];
+        }
+        terms[j] = t;
+    }
+#pragma unroll
+    for (int m = kWave / 2; m >= 1; m >>= 1) t = max(t, __shfl_xor(t, m, kWave));
+    if ((threadIdx.x & (kWave - 1)) == 0 && t > 0) atomicMax(mx, t);
+}
+
+struct BataxRows {
+    int32_t ncols;
+    const int32_t *rowptr, *colind;
+    const float *val;
+    const int32_t *colptr, *cperm, *crow;  // A's CSC: column pointers, CSR slots, rows
+    float beta;
+    const int32_t *toff;  // first temporary slot of each row of J
+    int32_t *tkey;        // keys of each row, compact, at toff[j]
+    float *tval;
+    int32_t *cnt;         // keys of each row
+};
+
+// Inclusive scan of one value per lane over the wave.
+__device__ __forceinline__ int32_t wave_incl_scan(int32_t x, int lane) {
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        const int32_t y = __shfl_up(x, d, kWave);
+        if (lane >= d) x += y;
+    }
+    return x;
+}
+
+// Sort keys (k, position) packed in one word: 32 bits while k < 2^23 (the
+// position takes 9 bits), else 64.
+constexpr int kPosBits = 9;
+static_assert((1 << kPosBits) == kRowCap, "positions fill the low bits");
+
+template <class Key>
+struct RowKey;
+template <>
+struct RowKey<uint32_t> {
+    static constexpr uint32_t pad = ~0u;
+    __device__ static uint32_t make(int32_t k, int32_t s) {
+        return ((uint32_t)k << kPosBits) | (uint32_t)s;
+    }
+    __device__ static uint32_t k(uint32_t x) { return x >> kPosBits; }
+    __device__ static int32_t pos(uint32_t x) { return (int32_t)(x & (kRowCap - 1)); }
+};
+template <>
+struct RowKey<unsigned long long> {
+    static constexpr unsigned long long pad = ~0ull;
+    __device__ static unsigned long long make(int32_t k, int32_t s) {
+        return ((unsigned long long)(uint32_t)k << 32) | (uint32_t)s;
+    }
+    __device__ static uint32_t k(unsigned long long x) { return (uint32_t)(x >> 32); }
+    __device__ static int32_t pos(unsigned long long x) { return (int32_t)(uint32_t)x; }
+};
+
+// Row j of J by one wave (at most kRowCap terms, checked by the caller).
+template <class Key>
+__global__ __launch_bounds__(kRowThreads) void batax_rows_kernel(BataxRows a) {
+    using RK = RowKey<Key>;
+    __shared__ Key skey[kRowCap];                 // (k, position), sorted
+    __shared__ float sterm[kRowCap];              // terms by position
+    __shared__ int32_t spre[kRowCap + 1];         // first position of each gathered row
+    __shared__ int32_t sbeg[kRowCap];             // its first CSR slot
+    __shared__ float sa[kRowCap];                 // beta * a_ij
+    const int32_t j = blockIdx.x;
+    const int l = threadIdx.x;
+    const int32_t cb = a.colptr[j], nr = a.colptr[j + 1] - cb;  // nr <= terms <= kRowCap
+    // 1. the rows of A storing column j, in CSC (ascending) order
+    int32_t carry = 0;
+    for (int32_t base = 0; base < nr; base += kWave) {
+        const bool v = base + l < nr;
+        int32_t len = 0, b = 0;
+        float av = 0.f;
+        if (v) {
+            const int32_t c = cb + base + l;
+            const int32_t i = a.crow[c];
+            b = a.rowptr[i];
+            len = a.rowptr[i + 1] - b;
+            av = a.beta * a.val[a.cperm[c]];
+        }
+        const int32_t x = wave_incl_scan(len, l);
+        if (v) {
+            spre[base + l + 1] = carry + x;
+            sbeg[base + l] = b;
+            sa[base + l] = av;
+        }
+        carry += __shfl(x, kWave - 1, kWave);
+    }
+    const int32_t P = carry;
+    if (P == 0) {  // uniform over the wave
+        if (l == 0) a.cnt[j] = 0;
+        return;
+    }
+    if (l == 0) spre[0] = 0;
+    __syncthreads();
+    // 2. the terms, row by row: position s of gathered row r is its entry
+    //    sbeg[r] + s - spre[r]
+    int32_t np2 = kWave;
+    while (np2 < P) np2 <<= 1;
+    for (int32_t s = l; s < np2; s += kWave) {
+        if (s < P) {
+            int32_t lo = 0, hi = nr - 1;  // last r with spre[r] <= s
+            while (lo < hi) {
+                const int32_t mid = (lo + hi + 1) >> 1;
+                if (spre[mid] <= s) lo = mid;
+                else hi = mid - 1;
+            }
+            const int32_t q = sbeg[lo] + (s - spre[lo]);
+            skey[s] = RK::make(a.colind[q], s);
+            sterm[s] = sa[lo] * a.val[q];
+        } else {
+            skey[s] = RK::pad;
+        }
+    }
+    __syncthreads();
+    // 3. bitonic sort of the (k, position) pairs in LDS, ascending: equal
+    //    keys keep their positions' order (measured on MI355X against a
+    //    sort in registers with cross-lane shuffles, 634 us per call on the
+    //    uniform 1M-entry workload, and ranks by binary searches in the
+    //    other gathered rows, 685 us: this takes 407 us with 64-bit keys,
+    //    346 with 32-bit ones)
+    for (int32_t size = 2; size <= np2; size <<= 1) {
+        for (int32_t stride = size >> 1; stride > 0; stride >>= 1) {
+            for (int32_t t = l; t < np2 / 2; t += kWave) {
+                const int32_t i1 = 2 * t - (t & (stride - 1)), i2 = i1 + stride;
+                const Key x1 = skey[i1], x2 = skey[i2];
+                if ((x1 > x2) == ((i1 & size) == 0)) {
+                    skey[i1] = x2;
+                    skey[i2] = x1;
+                }
+            }
+            __syncthreads();
+        }
+    }
+    // 4. runs of equal k: each lane takes a contiguous chunk of the sorted
+    //    terms, numbers the runs that start there, and sums each of them in
+    //    order in fp64 (a run may continue into the next lanes' chunks)
+    const int32_t C = (P + kWave - 1) / kWave;
+    const int32_t s0 = min(l * C, P), s1 = min(s0 + C, P);
+    auto kof = [&](int32_t s) { return RK::k(skey[s]); };
+    int32_t h = 0;
+    for (int32_t s = s0; s < s1; ++s) h += (s == 0 || kof(s - 1) != kof(s)) ? 1 : 0;
+    const int32_t incl = wave_incl_scan(h, l);
+    int32_t r = incl - h;
+    const int32_t o = a.toff[j];
+    for (int32_t s = s0; s < s1; ++s) {
+        const uint32_t k = kof(s);
+        if (s == 0 || kof(s - 1) != k) {
+            double sum = 0.0;
+            for (int32_t t = s; t < P && kof(t) == k; ++t)
+                sum += (double)sterm[RK::pos(skey[t])];
+            a.tkey[o + r] = (int32_t)k;
+            a.tval[o + r] = (float)sum;
+            ++r;
+        }
+    }
+    if (l == kWave - 1) a.cnt[j] = incl;
+}
+
+// Rows of J moved from their temporary slots to the CSR.
+__global__ __launch_bounds__(kRowThreads) void batax_compact_kernel(
+    const int32_t *toff, const int32_t *cnt, const int32_t *jrowptr, const int32_t *tkey,
+    const float *tval, int32_t *jcolind, float *jval) {
+    const int32_t j = blockIdx.x;
+    const int32_t n = cnt[j], src = toff[j], dst = jrowptr[j];
+    for (int32_t t = threadIdx.x; t < n; t += kRowThreads) {
+        jcolind[dst + t] = tkey[src + t];
+        jval[dst + t] = tval[src + t];
+    }
+}
+
+struct BataxRowWs {
+    int32_t *csort, *cperm, *crow, *colptr, *terms, *toff, *cnt, *tkey, *mx;
+    float *tval;
+    void *sort_ws, *scan_ws;
+};
+
+static void batax_row_carve(Carver &c, int32_t ncols, int32_t nnz, int64_t P, BataxRowWs *w) {
+    const int64_t z = std::max<int32_t>(nnz, 1), n = std::max<int32_t>(ncols, 1);
+    w->csort = c.take<int32_t>(z);
+    w->cperm = c.take<int32_t>(z);
+    w->crow = c.take<int32_t>(z);
+    w->colptr = c.take<int32_t>(n + 1);
+    w->terms = c.take<int32_t>(n);
+    w->toff = c.take<int32_t>(n);
+    w->cnt = c.take<int32_t>(n);
+    w->mx = c.take<int32_t>(64);
+    w->tkey = c.take<int32_t>(std::max<int64_t>(P, 1));
+    w->tval = c.take<float>(std::max<int64_t>(P, 1));
+    const size_t sb = sort_ws_bytes(z, (int32_t)n), cb = scan_ws_bytes(std::max(z, n));
+    char *s = c.take<char>((int64_t)std::max(sb, cb));
+    w->sort_ws = w->scan_ws = s;
+}
+
+// J by rows when every row has at most `cap` terms; *done says whether it did.
+static nsd_status batax_by_rows(const nsd_csr *A, float beta, int64_t P, int cap,
+                                const BataxRowWs &w, int32_t *jrowptr, int32_t *jcolind,
+                                float *jval, int32_t *nnz_out, bool *done, hipStream_t st) {
+    *done = false;
+    const int32_t m = A->nrows, n = A->ncols, z = A->nnz;
+    // A's CSC: columns sorted stably (rows ascend within a column)
+    NSD_TRY(radix_sort_pairs(z, n, A->colind, nullptr, w.csort, w.cperm, w.sort_ws, st));
+    NSD_TRY(segptr_from_sorted(z, n, w.csort, w.colptr, st));
+    slot_rows_kernel<<<bgrid(z), kBataxThreads, 0, st>>>(z, m, A->rowptr, w.cperm, w.crow);
+    NSD_TRY(check_launch("slot_rows_kernel"));
+    NSD_HIP(hipMemsetAsync(w.mx, 0, sizeof(int32_t), st));
+    row_terms_kernel<<<bgrid(n), kBataxThreads, 0, st>>>(n, w.colptr, w.crow, A->rowptr,
+                                                         w.terms, w.mx);
+    NSD_TRY(check_launch("row_terms_kernel"));
+    int32_t mx = 0;
+    NSD_HIP(hipMemcpyAsync(&mx, w.mx, sizeof(mx), hipMemcpyDeviceToHost, st));
+    NSD_HIP(hipStreamSynchronize(st));
+    if (mx > cap) return NSD_OK;  // some row of J is too long: the sort path
+    NSD_TRY(scan_exclusive(w.terms, w.toff, n, w.mx + 1, w.scan_ws, st));
+    BataxRows a;
+    a.ncols = n;
+    a.rowptr = A->rowptr;
+    a.colind = A->colind;
+    a.val = A->val;
+    a.colptr = w.colptr;
+    a.cperm = w.cperm;
+    a.crow = w.crow;
+    a.beta = beta;
+    a.toff = w.toff;
+    a.tkey = w.tkey;
+    a.tval = w.tval;
+    a.cnt = w.cnt;
+    probe_begin(NSD_KERNEL_BATAX_ROWS, st);
+    if (n < (1 << (32 - kPosBits)))  // every real key below the padding
+        batax_rows_kernel<uint32_t><<<(unsigned)n, kRowThreads, 0, st>>>(a);
+    else
+        batax_rows_kernel<unsigned long long><<<(unsigned)n, kRowThreads, 0, st>>>(a);
+    probe_end(NSD_KERNEL_BATAX_ROWS, st);
+    NSD_TRY(check_launch("batax_rows_kernel"));
+    NSD_TRY(scan_exclusive(w.cnt, jrowptr, n, jrowptr + n, w.scan_ws, st));
+    batax_compact_kernel<<<(unsigned)n, kRowThreads, 0, st>>>(w.toff, w.cnt, jrowptr, w.tkey,
+                                                              w.tval, jcolind, jval);
+    NSD_TRY(check_launch("batax_compact_kernel"));
+    int32_t nk = 0;
+    NSD_HIP(hipMemcpyAsync(&nk, jrowptr + n, sizeof(nk), hipMemcpyDeviceToHost, st));
+    NSD_HIP(hipStreamSynchronize(st));
+    (void)P;
+    *nnz_out = nk;
+    *done = true;
+    return NSD_OK;
+}
+
 // Workspace layout shared by the size query and the call.
 struct BataxWs {
     int32_t *sq, *off, *tot;
@@ -120,8 +419,12 @@ struct BataxWs {
 };
 
 static nsd_status batax_carve(void *ws, int32_t nrows, int32_t n, int64_t P, BataxWs *w,
-                              size_t *total) {
+                              size_t *total, int32_t nnz = 0, BataxRowWs *rw = nullptr) {
     Carver c(ws);
+    // the row path's buffers first (it runs first; the sort path reuses
+    // nothing of it)
+    BataxRowWs rw_tmp;
+    batax_row_carve(c, n, nnz, P, rw ? rw : &rw_tmp);
     w->sq = c.take<int32_t>(std::max<int64_t>(nrows, 1));
     w->off = c.take<int32_t>(std::max<int64_t>(nrows, 1));
     w->tot = c.take<int32_t>(64);
@@ -191,7 +494,7 @@ nsd_status nsd_batax_workspace_size(const nsd_csr *A, int64_t npairs, size_t *by
     if (npairs >= kBataxMaxPairs)
         return fail(NSD_ERR_TOO_LARGE, "%lld row pairs (at most 2^30)", (long long)npairs);
     BataxWs w;
-    return batax_carve(nullptr, A->nrows, A->ncols, npairs, &w, bytes);
+    return batax_carve(nullptr, A->nrows, A->ncols, npairs, &w, bytes, A->nnz);
 }
 
 nsd_status nsd_batax_jacobian(const nsd_csr *A, float beta, int64_t npairs, int32_t *jrowptr,
@@ -205,10 +508,11 @@ nsd_status nsd_batax_jacobian(const nsd_csr *A, float beta, int64_t npairs, int3
     NSD_REQUIRE(npairs == 0 || (jcolind && jval), "jcolind/jval is NULL");
     size_t need = 0;
     BataxWs w;
-    NSD_TRY(batax_carve(nullptr, A->nrows, A->ncols, npairs, &w, &need));
+    BataxRowWs rw;
+    NSD_TRY(batax_carve(nullptr, A->nrows, A->ncols, npairs, &w, &need, A->nnz, &rw));
     if (ws == nullptr || ws_bytes < need)
         return fail(NSD_ERR_WORKSPACE, "workspace %zu bytes at %p, need %zu", ws_bytes, ws, need);
-    NSD_TRY(batax_carve(ws, A->nrows, A->ncols, npairs, &w, &need));
+    NSD_TRY(batax_carve(ws, A->nrows, A->ncols, npairs, &w, &need, A->nnz, &rw));
     hipStream_t st = as_stream(stream);
     const int32_t m = A->nrows, n = A->ncols;
     const int64_t P = npairs;
@@ -228,6 +532,12 @@ nsd_status nsd_batax_jacobian(const nsd_csr *A, float beta, int64_t npairs, int3
     if ((int64_t)hp != P)
         return fail(NSD_ERR_INVALID_ARG, "npairs = %lld, but A's rows give %d pairs",
                     (long long)P, hp);
+    const int cap = row_cap();
+    if (cap > 0) {
+        bool done = false;
+        NSD_TRY(batax_by_rows(A, beta, P, cap, rw, jrowptr, jcolind, jval, nnz_out, &done, st));
+        if (done) return NSD_OK;
+    }
     expand_pairs_kernel<<<bgrid(P), kBataxThreads, 0, st>>>(P, m, w.off, A->rowptr, A->colind,
                                                             A->val, beta, w.key_j, w.key_k,
                                                             w.term);

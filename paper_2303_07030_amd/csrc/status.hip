@@ -78,7 +78,7 @@ int nsd_version(void) { return 100; }
 
 nsd_status nsd_probe_set(int kernel_id, void *const *start_events, void *const *stop_events,
                          int32_t n) {
-    NSD_REQUIRE(kernel_id > 0 && kernel_id <= NSD_KERNEL_PERM, "unknown kernel id %d", kernel_id);
+    NSD_REQUIRE(kernel_id > 0 && kernel_id <= NSD_KERNEL_BATAX_ROWS, "unknown kernel id %d", kernel_id);
     NSD_REQUIRE(n >= 1 && start_events && stop_events, "need n >= 1 event pairs");
     nsd::Probe p;
     p.id = kernel_id;

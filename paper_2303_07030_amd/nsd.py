@@ -28,7 +28,7 @@ NSD_DUP_SUM = 0
 NSD_DUP_ERROR = 1
 KERNEL_IDS = {"sgr_main": 1, "sgr_fix": 2, "sddmm": 3, "frob_row": 4, "frob_col": 5, "mf": 6,
               "cp": 7, "loss": 8, "ttv": 9, "dual": 10, "sort": 11, "jvp": 12, "cpn": 13,
-              "perm": 14}
+              "perm": 14, "batax_rows": 15}
 
 
 class NsdError(RuntimeError):

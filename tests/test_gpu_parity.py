@@ -804,6 +804,100 @@ def test_batax_jacobian_degenerate(nsd, operand, orc, case):
     check_batax(orc, nrows, ncols, rowptr, colind, val, 2.0, got)
 
 
+def max_row_terms(ncols, rowptr, colind):
+    """Largest number of terms of a row of J = A^T A (the rows of A storing
+    column j, their lengths summed)."""
+    lens = np.diff(rowptr).astype(np.int64)
+    rows = np.repeat(np.arange(len(lens)), lens)
+    t = np.zeros(max(ncols, 1), np.int64)
+    np.add.at(t, colind, lens[rows])
+    return int(t.max()) if len(colind) else 0
+
+
+def boundary_pattern(rng, terms):
+    """Two rows of terms // 2 and terms - terms // 2 entries on columns
+    [0, 1000), both storing column 0, and 300 sparse rows on columns
+    [1000, 2000): the longest row of J (column 0's) has exactly `terms` terms."""
+    ncols = 2000
+    rows = []
+    for n in (terms // 2, terms - terms // 2):
+        c = rng.choice(np.arange(1, 1000), size=n - 1, replace=False)
+        rows.append(np.sort(np.concatenate([[0], c])))
+    for _ in range(300):
+        rows.append(np.sort(rng.choice(np.arange(1000, 2000), size=int(rng.integers(0, 6)),
+                                       replace=False)))
+    rowptr = np.concatenate([[0], np.cumsum([len(r) for r in rows])]).astype(np.int32)
+    colind = np.concatenate(rows).astype(np.int32)
+    val = rng.standard_normal(len(colind)).astype(np.float32)
+    return len(rows), ncols, rowptr, colind, val
+
+
+def many_rows_pattern(rng):
+    """40 rows of 12 entries sharing column 0 (column 0's row of J gathers 40
+    rows, 480 terms) and sparse rows elsewhere."""
+    rows = []
+    for _ in range(40):
+        rows.append(np.sort(np.concatenate([[0], rng.choice(np.arange(1, 2000), size=11,
+                                                             replace=False)])))
+    for _ in range(200):
+        rows.append(np.sort(rng.choice(np.arange(1, 2000), size=int(rng.integers(0, 4)),
+                                       replace=False)))
+    rowptr = np.concatenate([[0], np.cumsum([len(r) for r in rows])]).astype(np.int32)
+    colind = np.concatenate(rows).astype(np.int32)
+    return len(rows), 2000, rowptr, colind, rng.standard_normal(len(colind)).astype(np.float32)
+
+
+@pytest.mark.parametrize("case", ["small_workload", "edge", "dense_row", "cap", "cap_plus_one",
+                                  "many_rows", "wide"])
+def test_batax_row_path_equals_sort_path(nsd, operand, orc, case):
+    """J built row by row in LDS (when no row of J has more than 512 terms)
+    and by the two global sorts (forced with NSD_BATAX_ROW_CAP=0): the same
+    bits, and the oracle's keys."""
+    import os
+    from paper_2303_07030_amd import synth
+    rng = np.random.default_rng(31)
+    if case == "small_workload":
+        d = synth.make("batax", "small")
+        nrows, ncols, rowptr, colind, val = d["nrows"], d["ncols"], d["rowptr"], d["colind"], \
+            d["val"]
+    elif case == "edge":
+        nrows, ncols, rowptr, colind, val = edge_pattern(19)
+    elif case == "dense_row":
+        nrows, ncols = 4, 300
+        rowptr, colind, val = make_csr(rng, nrows, ncols, np.array([0, 300, 3, 0]))
+    elif case == "many_rows":
+        # a row of J gathering 40 rows of A
+        nrows, ncols, rowptr, colind, val = many_rows_pattern(rng)
+        assert np.bincount(colind).max() == 40
+    elif case == "wide":
+        # 2^23 + 5 columns: the row path's 64-bit sort keys
+        nrows, ncols = 300, (1 << 23) + 5
+        hot = rng.integers(0, ncols, 40)  # columns shared by several rows
+        rows = [np.unique(np.concatenate([rng.choice(hot, 3), rng.integers(0, ncols, 4)]))
+                for _ in range(nrows)]
+        rows[-1] = np.unique(np.concatenate([rows[-1], [ncols - 1]]))
+        rowptr = np.concatenate([[0], np.cumsum([len(r) for r in rows])]).astype(np.int32)
+        colind = np.concatenate(rows).astype(np.int32)
+        val = rng.standard_normal(len(colind)).astype(np.float32)
+    else:
+        nrows, ncols, rowptr, colind, val = boundary_pattern(rng, 512 if case == "cap" else 513)
+    mx = max_row_terms(ncols, rowptr, colind)
+    if case == "cap":
+        assert mx == 512
+    if case in ("edge", "cap_plus_one"):
+        assert mx > 512  # these take the sort path either way
+    A = operand(nrows, ncols, rowptr, colind, val, build_csc=False)
+    default = run_batax(nsd, A, 1.25)
+    os.environ["NSD_BATAX_ROW_CAP"] = "0"
+    try:
+        forced = run_batax(nsd, A, 1.25)
+    finally:
+        del os.environ["NSD_BATAX_ROW_CAP"]
+    for x, y in zip(default, forced):
+        assert np.array_equal(x.view(np.uint8), y.view(np.uint8))
+    check_batax(orc, nrows, ncols, rowptr, colind, val, 1.25, default)
+
+
 def test_batax_jacobian_rejects_wrong_pair_count(nsd, operand):
     nrows, ncols, rowptr, colind, val = edge_pattern(18)
     A = operand(nrows, ncols, rowptr, colind, val, build_csc=False)
