@@ -114,9 +114,58 @@ def case_cpn(nsd):
     return (lambda: nsd.nsd_loss_cpn(X.desc, F, R, 1.0, o[0], o[1], o[2:], ws)), o
 
 
+def case_bilinear_moves(nsd, k=64):
+    # the bilinear layer with the two-pass permutation moves (a pattern
+    # given the CSC's perm plans): two moves around the column pass
+    from paper_2303_07030_amd.operand import DeviceCsr
+    nrows, ncols, rowptr, colind, val = edge_pattern(32)
+    A = DeviceCsr(nrows, ncols, rowptr, colind, val, k_hint=k, perm_plans=True)
+    H, G, ws = rand(A.ncols, k, seed=12), rand(A.nrows, k, seed=13), A.workspace(k)
+    o = [out(1, dtype=torch.float64), out(A.nnz), out(A.ncols, k)]
+    return (lambda: nsd.nsd_loss_bilinear(A.desc, A.csc, H, G, k, 1.0, *o, ws)), o
+
+
+def case_bilinear_wide(nsd, k=300):
+    # a width beyond a fused slot: SDDMM and the gather-reduce
+    A = csr(k)
+    H, G, ws = rand(A.ncols, k, seed=14), rand(A.nrows, k, seed=15), A.workspace(k)
+    o = [out(1, dtype=torch.float64), out(A.nnz), out(A.ncols, k)]
+    return (lambda: nsd.nsd_loss_bilinear(A.desc, A.csc, H, G, k, 1.0, *o, ws)), o
+
+
+def case_mf_wide(nsd, k=300):
+    # the factorisation beyond a fused slot: residual once, two gather-reduces
+    A = csr(k)
+    U, V = rand(A.nrows, k, seed=16, scale=0.1), rand(A.ncols, k, seed=17, scale=0.1)
+    ws = A.workspace(k)
+    o = [out(1, dtype=torch.float64), out(A.nrows, k), out(A.ncols, k)]
+    return (lambda: nsd.nsd_loss_mf(A.desc, A.csc, None, U, V, k, 1.0, *o, ws)), o
+
+
+def case_jvp_batch(nsd, k=64, m=5):
+    A = csr(k)
+    dval, B = rand(m, A.nnz, seed=18), rand(A.ncols, k, seed=19)
+    dB = rand(m, A.ncols, k, seed=20)
+    ws = torch.empty(nsd.nsd_spmm_jvp_batch_workspace_size(A.desc, k), dtype=torch.uint8,
+                     device="cuda")
+    o = [out(A.nrows, k), out(m, A.nrows, k)]
+    return (lambda: nsd.nsd_spmm_jvp_batch(A.desc, m, dval, B, dB, k, o[0], o[1], ws)), o
+
+
+def case_scale(nsd, n=100_000):
+    g = np.random.default_rng(21)
+    x1, x2 = rand(n, seed=22), rand(3 * n, seed=23)
+    idx = dev(g.integers(0, 3 * n, n).astype(np.int32))
+    s1 = torch.tensor([1.5], dtype=torch.float64, device="cuda")
+    o = [out(n)]
+    return (lambda: nsd.nsd_scale(n, 2.0, s1, None, x1, x2, idx, 0.0, o[0])), o
+
+
 CASES = {
     "frob": case_frob, "bilinear": case_bilinear, "mf": case_mf, "sum_spmv": case_sum_spmv,
     "spmm_t": case_spmm_t, "jvp": case_jvp, "cp": case_cp, "cpn": case_cpn,
+    "bilinear_moves": case_bilinear_moves, "bilinear_wide": case_bilinear_wide,
+    "mf_wide": case_mf_wide, "jvp_batch": case_jvp_batch, "scale": case_scale,
 }
 
 
