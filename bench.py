@@ -288,12 +288,14 @@ def setup_build(d, dev, torch, nsd, ops):
     S = Setup()
     S.A, S.nnz, S.k, S.step = None, n, 0, step
     S.graphable = False  # the builders read counts back to the host
-    # scatter passes: by column (COO -> CSR), by row, by column (CSR -> CSC);
-    # each reads and writes a key and a payload (16 B per entry), except the
-    # first pass of a sort, whose payload is the entry's own index (12 B)
+    # scatter passes: by column, then by row (COO -> CSR), each carrying the
+    # input position, the other coordinate and the value (32 B per entry read
+    # and written); by column (CSR -> CSC) carrying the CSR slot and the row
+    # (24 B); a sort's first pass reads no position (its own index): 4 B less
     pc, pr = _sort_passes(nc), _sort_passes(nr)
     launches = 2 * pc + pr
-    S.kernels = {"sort": (16 * n * launches - 2 * 4 * n) / launches}
+    total = (32 * n * pc - 4 * n) + 32 * n * pr + (24 * n * pc - 4 * n)
+    S.kernels = {"sort": total / launches}
     return S
 
 

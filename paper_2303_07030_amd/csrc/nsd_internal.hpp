@@ -184,10 +184,15 @@ nsd_status scan_exclusive_max(const int32_t *in, int32_t *out, int64_t n, void *
 
 // Stable LSD radix sort of (key, payload) by key in [0, max_key); payload_in
 // NULL means the identity 0..n-1.  Results land in key_out / payload_out.
-size_t sort_ws_bytes(int64_t n, int32_t max_key);
+// radix_sort_multi carries np (1 to 3) payloads, the first of which may be
+// the identity; its workspace is sort_ws_bytes(n, max_key, np).
+size_t sort_ws_bytes(int64_t n, int32_t max_key, int np = 1);
 nsd_status radix_sort_pairs(int64_t n, int32_t max_key, const int32_t *key_in,
                             const int32_t *payload_in, int32_t *key_out, int32_t *payload_out,
                             void *ws, hipStream_t st);
+nsd_status radix_sort_multi(int64_t n, int32_t max_key, const int32_t *key_in, int np,
+                            const int32_t *const *payload_in, int32_t *key_out,
+                            int32_t *const *payload_out, void *ws, hipStream_t st);
 
 // segptr[r] = first position q with sorted_key[q] >= r, for r in [0, nseg].
 nsd_status segptr_from_sorted(int64_t n, int32_t nseg, const int32_t *sorted_key,
