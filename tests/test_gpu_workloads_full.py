@@ -1,10 +1,16 @@
 """Parity at the full workload sizes, in the launch configuration bench.py
 times (default work plans, the same entry points).
 
-The oracle cannot take whole passes over 20M-60M entries in test time, so:
-  * sampled outputs are compared with the oracle run on a sub-problem that
-    holds every stored entry the sampled outputs depend on (all entries of
-    the sampled rows or columns), indices compacted;
+The oracle cannot take every whole pass over 20M-60M entries in test time, so:
+  * the CP residuals (rank 16 and 32 per entry) are compared at every one of
+    the 20M entries, the oracle run on disjoint entry chunks in parallel;
+  * other sampled outputs are compared with the oracle run on a sub-problem
+    that holds every stored entry the sampled outputs depend on (all entries
+    of the sampled rows or columns), indices compacted;
+  * the bilinear layer's dH is also checked on all of its columns through
+    projections: dH v = A^T (G v) for random v, the right side in fp64 with
+    its own magnitude |A|^T (|G| |v|), which bounds the projected error of a
+    result that meets the bar element by element;
   * the global losses are the oracle's losses summed over disjoint chunks of
     the stored entries (the loss is a sum over stored entries, so the split
     is exact in fp64), chunks built in parallel; the bilinear layer's loss
@@ -60,6 +66,20 @@ def chunked_loss(orc, n, build_and_loss, nchunks=8, workers=8):
     return sum(p[0] for p in parts), sum(p[1] for p in parts)
 
 
+def chunked_map(orc, n, fn, nchunks=16, workers=8):
+    """fn(b, e) -> (values, mags) over disjoint entry chunks, one
+    single-threaded oracle per chunk, concatenated in entry order."""
+    bounds = np.linspace(0, n, nchunks + 1).astype(np.int64)
+
+    def one(c):
+        orc.set_threads(1)
+        return fn(bounds[c], bounds[c + 1])
+
+    with cf.ThreadPoolExecutor(max_workers=min(workers, nchunks)) as ex:
+        parts = list(ex.map(one, range(nchunks)))
+    return np.concatenate([p[0] for p in parts]), np.concatenate([p[1] for p in parts])
+
+
 # ------------------------------------------------------------ bilinear layer
 
 def test_bilinear_full_workload(nsd, orc):
@@ -100,6 +120,16 @@ def test_bilinear_full_workload(nsd, orc):
     ref, mag = orc.spmm_t(D, G[ru], k)
     assert_mag_close(dHg[J], ref, mag, what="dH (sampled columns)")
 
+    # dH on all columns, projected: dH v = A^T (G v) (seed 1)
+    a64 = val.astype(np.float64)
+    for t in range(2):
+        v = rng.standard_normal(k)
+        gv = G.astype(np.float64) @ v
+        gm = np.abs(G).astype(np.float64) @ np.abs(v)
+        ref = np.bincount(colind, weights=a64 * gv[rows], minlength=n)
+        mag = np.bincount(colind, weights=np.abs(a64) * gm[rows], minlength=n)
+        assert_mag_close(dHg.astype(np.float64) @ v, ref, mag, what=f"dH v (projection {t})")
+
     # the loss over all 60M entries, as a sum of per-chunk oracle losses
     def part(b, e):
         ru, ri = compact(rows[b:e])
@@ -111,7 +141,6 @@ def test_bilinear_full_workload(nsd, orc):
     assert_mag_close(Lg, L, Lm, what="loss")
 
     # and through identities of the exact values: sum_p A_p dA_p and <H, dH>
-    a64 = val.astype(np.float64)
     s1 = float(np.dot(a64, dAg.astype(np.float64)))
     m1 = float(np.dot(np.abs(a64), np.abs(dAg.astype(np.float64))))
     s2 = m2 = 0.0
@@ -337,11 +366,14 @@ def test_cp_full_workload(nsd, orc):
     rng = np.random.default_rng(7)
     coords = (i, j, l)
 
-    # residual at sampled entries (in the input order)
-    P = rng.choice(len(val), 8192, replace=False)
-    D = orc.Dok(dims, (i[P], j[P], l[P]), val[P])
-    ref, mag = orc.cp_resid(D, *F, R, i[P], j[P], l[P])
-    assert_mag_close(dXg[P], ref, mag, what="residual (sampled)")
+    # the residual at every entry (in the input order)
+    def resid(b, e):
+        D = orc.Dok(dims, (i[b:e], j[b:e], l[b:e]), val[b:e])
+        return orc.cp_resid(D, *F, R, i[b:e], j[b:e], l[b:e])
+
+    ref, mag = chunked_map(orc, len(val), resid)
+    assert_mag_close(dXg, ref, mag, what="residual (every entry)")
+    del ref, mag
 
     # every mode's gradient on sampled slices, with all their entries
     for m in range(3):
@@ -377,10 +409,14 @@ def test_cp4_full_workload(nsd, orc, fibers):
     dXg[host(X.coo_perm)] = host(dX)   # stored order -> input order
     del X, dX, dF
     rng = np.random.default_rng(8)
-    P = rng.choice(len(val), 8192, replace=False)
-    D = orc.Dok(dims, [c[P] for c in coords], val[P])
-    ref, mag = orc.cpn_resid(D, F, R, [c[P] for c in coords])
-    assert_mag_close(dXg[P], ref, mag, what="residual (sampled)")
+
+    def resid(b, e):
+        D = orc.Dok(dims, [c[b:e] for c in coords], val[b:e])
+        return orc.cpn_resid(D, F, R, [c[b:e] for c in coords])
+
+    ref, mag = chunked_map(orc, len(val), resid)
+    assert_mag_close(dXg, ref, mag, what="residual (every entry)")
+    del ref, mag
     for m in range(len(dims)):
         S = np.unique(rng.choice(dims[m], 3, replace=False))
         sel = np.isin(coords[m], S)
