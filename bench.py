@@ -320,14 +320,14 @@ def setup_batax(d, dev, torch, nsd, ops):
     S.step = lambda: nsd.nsd_batax_jacobian(A.desc, d["beta"], P, jrowptr, jcol, jval, ws)
     S.pairs = P
     nnz = A.nnz
-    # the CSC of A: a radix sort of the nnz column indices (index payload)
-    p = _sort_passes(n)
-    S.kernels = {"sort": (16 * nnz * p - 4 * nnz) / p,
-                 # per stored entry: the CSC slot's row and CSR slot, the
-                 # row's bounds and a_ij (20 B); per product: k and a_ik
-                 # (8 B); per key of J: its column and value (8 B); per row
-                 # of J: its column bounds and key count
-                 "batax_rows": 20 * nnz + 8 * P + 8 * nk + 12 * n}
+    # the CSC of A: a radix sort of the nnz column indices carrying each
+    # entry's row and value (key and two payloads read and written per pass)
+    S.kernels = {"sort": 24 * nnz,
+                 # per stored entry: the CSC slot's row and value and the
+                 # row's bounds (16 B); per product: k and a_ik (8 B); per
+                 # key of J: its column and value (8 B); per row of J: its
+                 # column bounds and key count
+                 "batax_rows": 16 * nnz + 8 * P + 8 * nk + 12 * n}
     return S
 
 

@@ -758,7 +758,7 @@ nsd_status nsd_spmm_jvp_batch(const nsd_csr *A, int32_t m, const float *dAval, c
  * normalised program of Example 5 inserts the outer product of every row
  * with itself).  Keys are structural: a pair whose product is 0 keeps its
  * key.  A is a CSR (rowptr, colind, val; sorted unique columns per row; no
- * plan or rowidx needed).
+ * plan needed; rowidx may be NULL, else it must be A's row index).
  *
  * Three calls:
  *   nsd_batax_pairs          *npairs (host) = sum over rows of length^2, the

@@ -124,7 +124,19 @@ __global__ void run_sums_kernel(int32_t nruns, const int32_t *runptr, const int3
 // ------------------------------------------------------- row path
 
 constexpr int kRowCap = 512;     // terms of one row of J held in LDS (a power of two)
-constexpr int kRowThreads = 64;  // one wave per row of J
+constexpr int kRowThreads = 64;  // one wave per row of J (the compaction's block)
+// Rows of J per block of the row kernel, one wave each (build-time knob
+// NSD_BATAX_ROW_WAVES).  The waves share nothing but the block: each has
+// its own LDS region and synchronises only itself.  Measured on MI355X on
+// the uniform 1M-entry input: 207 us with one wave per block, 218 / 220 /
+// 230 us with 2 / 4 / 8 (what raised the waves per CU was sizing the LDS
+// regions by the largest row instead of the row cap: 344 us before).
+#ifdef NSD_BATAX_ROW_WAVES
+constexpr int kRowWaves = NSD_BATAX_ROW_WAVES;
+#else
+constexpr int kRowWaves = 1;
+#endif
+constexpr int kRowBlock = kRowWaves * kWave;
 // The row path takes rows of J with at most this many terms: kRowCap, or
 // less when the environment says so (NSD_BATAX_ROW_CAP; 0 keeps every call
 // on the sort path).
@@ -135,13 +147,14 @@ static int row_cap() {
     return v < 0 ? 0 : std::min(v, kRowCap);
 }
 
-// row[c] = the row of A holding CSR slot slot[c]: the last r with
-// rowptr[r] <= slot[c] (an empty row shares its start with the next).
+// row[p] = the row of A holding CSR slot p: the last r with rowptr[r] <= p
+// (an empty row shares its start with the next); for a CSR given without
+// its row index.
 __global__ void slot_rows_kernel(int64_t n, int32_t nrows, const int32_t *rowptr,
-                                 const int32_t *slot, int32_t *row) {
+                                 int32_t *row) {
     const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (c >= n) return;
-    const int32_t p = slot[c];
+    const int32_t p = (int32_t)c;
     int32_t lo = 0, hi = nrows - 1;
     while (lo < hi) {
         const int32_t mid = lo + (hi - lo + 1) / 2;
@@ -152,12 +165,14 @@ __global__ void slot_rows_kernel(int64_t n, int32_t nrows, const int32_t *rowptr
 }
 
 // terms[j] = number of terms of row j of J: the summed lengths of the rows
-// of A storing column j; the largest goes to *mx (integer maximum: any order).
+// of A storing column j; the largest goes to mx[0], the largest number of
+// rows of A storing one column to mx[1] (integer maxima: any order).
 __global__ void row_terms_kernel(int32_t ncols, const int32_t *colptr, const int32_t *crow,
                                  const int32_t *rowptr, int32_t *terms, int32_t *mx) {
     const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    int32_t t = 0;
+    int32_t t = 0, nr = 0;
     if (j < ncols) {
+        nr = colptr[j + 1] - colptr[j];
         for (int32_t c = colptr[j]; c < colptr[j + 1]; ++c) {
             const int32_t i = crow[c];
             t += rowptr[i + 1] - rowptr[i];
@@ -165,20 +180,31 @@ __global__ void row_terms_kernel(int32_t ncols, const int32_t *colptr, const int
         terms[j] = t;
     }
 #pragma unroll
-    for (int m = kWave / 2; m >= 1; m >>= 1) t = max(t, __shfl_xor(t, m, kWave));
-    if ((threadIdx.x & (kWave - 1)) == 0 && t > 0) atomicMax(mx, t);
+    for (int m = kWave / 2; m >= 1; m >>= 1) {
+        t = max(t, __shfl_xor(t, m, kWave));
+        nr = max(nr, __shfl_xor(nr, m, kWave));
+    }
+    if ((threadIdx.x & (kWave - 1)) == 0) {
+        if (t > 0) atomicMax(mx, t);
+        if (nr > 0) atomicMax(mx + 1, nr);
+    }
 }
 
 struct BataxRows {
     int32_t ncols;
     const int32_t *rowptr, *colind;
     const float *val;
-    const int32_t *colptr, *cperm, *crow;  // A's CSC: column pointers, CSR slots, rows
+    const int32_t *colptr, *crow;  // A's CSC: column pointers, rows
+    const float *cval;             // and values
     float beta;
     const int32_t *toff;  // first temporary slot of each row of J
     int32_t *tkey;        // keys of each row, compact, at toff[j]
     float *tval;
     int32_t *cnt;         // keys of each row
+    // one wave's LDS region: the sort keys at its start, then the terms, the
+    // gathered rows' first positions, first CSR slots and beta * a_ij, each
+    // sized for the largest row of this J (byte offsets, 16-byte aligned)
+    int32_t lds_wave, off_term, off_pre, off_beg, off_a;
 };
 
 // Inclusive scan of one value per lane over the wave.
@@ -217,17 +243,23 @@ struct RowKey<unsigned long long> {
     __device__ static int32_t pos(unsigned long long x) { return (int32_t)(uint32_t)x; }
 };
 
-// Row j of J by one wave (at most kRowCap terms, checked by the caller).
+// Row j of J by one wave (at most kRowCap terms, checked by the caller); the
+// LDS regions are sized by the caller from the largest row's term count and
+// the longest column of A, so every index below stays inside its array.
 template <class Key>
-__global__ __launch_bounds__(kRowThreads) void batax_rows_kernel(BataxRows a) {
+__global__ __launch_bounds__(kRowBlock) void batax_rows_kernel(BataxRows a) {
     using RK = RowKey<Key>;
-    __shared__ Key skey[kRowCap];                 // (k, position), sorted
-    __shared__ float sterm[kRowCap];              // terms by position
-    __shared__ int32_t spre[kRowCap + 1];         // first position of each gathered row
-    __shared__ int32_t sbeg[kRowCap];             // its first CSR slot
-    __shared__ float sa[kRowCap];                 // beta * a_ij
-    const int32_t j = blockIdx.x;
-    const int l = threadIdx.x;
+    extern __shared__ __align__(16) unsigned char row_lds[];
+    const int wid = threadIdx.x / kWave;
+    const int l = threadIdx.x % kWave;
+    const int32_t j = blockIdx.x * kRowWaves + wid;
+    if (j >= a.ncols) return;  // the whole wave
+    unsigned char *base = row_lds + (size_t)wid * a.lds_wave;
+    Key *skey = reinterpret_cast<Key *>(base);                        // (k, position), sorted
+    float *sterm = reinterpret_cast<float *>(base + a.off_term);      // terms by position
+    int32_t *spre = reinterpret_cast<int32_t *>(base + a.off_pre);    // first position of each gathered row
+    int32_t *sbeg = reinterpret_cast<int32_t *>(base + a.off_beg);    // its first CSR slot
+    float *sa = reinterpret_cast<float *>(base + a.off_a);            // beta * a_ij
     const int32_t cb = a.colptr[j], nr = a.colptr[j + 1] - cb;  // nr <= terms <= kRowCap
     // 1. the rows of A storing column j, in CSC (ascending) order
     int32_t carry = 0;
@@ -240,7 +272,7 @@ __global__ __launch_bounds__(kRowThreads) void batax_rows_kernel(BataxRows a) {
             const int32_t i = a.crow[c];
             b = a.rowptr[i];
             len = a.rowptr[i + 1] - b;
-            av = a.beta * a.val[a.cperm[c]];
+            av = a.beta * a.cval[c];
         }
         const int32_t x = wave_incl_scan(len, l);
         if (v) {
@@ -256,7 +288,7 @@ __global__ __launch_bounds__(kRowThreads) void batax_rows_kernel(BataxRows a) {
         return;
     }
     if (l == 0) spre[0] = 0;
-    __syncthreads();
+    __syncwarp();  // this wave only
     // 2. the terms, row by row: position s of gathered row r is its entry
     //    sbeg[r] + s - spre[r]
     int32_t np2 = kWave;
@@ -276,7 +308,7 @@ __global__ __launch_bounds__(kRowThreads) void batax_rows_kernel(BataxRows a) {
             skey[s] = RK::pad;
         }
     }
-    __syncthreads();
+    __syncwarp();  // this wave only
     // 3. bitonic sort of the (k, position) pairs in LDS, ascending: equal
     //    keys keep their positions' order (measured on MI355X against a
     //    sort in registers with cross-lane shuffles, 634 us per call on the
@@ -293,7 +325,7 @@ __global__ __launch_bounds__(kRowThreads) void batax_rows_kernel(BataxRows a) {
                     skey[i2] = x1;
                 }
             }
-            __syncthreads();
+            __syncwarp();  // this wave only
         }
     }
     // 4. runs of equal k: each lane takes a contiguous chunk of the sorted
@@ -334,15 +366,16 @@ __global__ __launch_bounds__(kRowThreads) void batax_compact_kernel(
 }
 
 struct BataxRowWs {
-    int32_t *csort, *cperm, *crow, *colptr, *terms, *toff, *cnt, *tkey, *mx;
-    float *tval;
+    int32_t *csort, *ridx, *crow, *colptr, *terms, *toff, *cnt, *tkey, *mx;
+    float *cval, *tval;
     void *sort_ws, *scan_ws;
 };
 
 static void batax_row_carve(Carver &c, int32_t ncols, int32_t nnz, int64_t P, BataxRowWs *w) {
     const int64_t z = std::max<int32_t>(nnz, 1), n = std::max<int32_t>(ncols, 1);
     w->csort = c.take<int32_t>(z);
-    w->cperm = c.take<int32_t>(z);
+    w->ridx = c.take<int32_t>(z);
+    w->cval = c.take<float>(z);
     w->crow = c.take<int32_t>(z);
     w->colptr = c.take<int32_t>(n + 1);
     w->terms = c.take<int32_t>(n);
@@ -351,7 +384,7 @@ static void batax_row_carve(Carver &c, int32_t ncols, int32_t nnz, int64_t P, Ba
     w->mx = c.take<int32_t>(64);
     w->tkey = c.take<int32_t>(std::max<int64_t>(P, 1));
     w->tval = c.take<float>(std::max<int64_t>(P, 1));
-    const size_t sb = sort_ws_bytes(z, (int32_t)n), cb = scan_ws_bytes(std::max(z, n));
+    const size_t sb = sort_ws_bytes(z, (int32_t)n, 2), cb = scan_ws_bytes(std::max(z, n));
     char *s = c.take<char>((int64_t)std::max(sb, cb));
     w->sort_ws = w->scan_ws = s;
 }
@@ -362,38 +395,59 @@ static nsd_status batax_by_rows(const nsd_csr *A, float beta, int64_t P, int cap
                                 float *jval, int32_t *nnz_out, bool *done, hipStream_t st) {
     *done = false;
     const int32_t m = A->nrows, n = A->ncols, z = A->nnz;
-    // A's CSC: columns sorted stably (rows ascend within a column)
-    NSD_TRY(radix_sort_pairs(z, n, A->colind, nullptr, w.csort, w.cperm, w.sort_ws, st));
+    // A's CSC: columns sorted stably (rows ascend within a column), each
+    // entry's row and value travelling with its column
+    const int32_t *ridx = A->rowidx;
+    if (ridx == nullptr) {
+        slot_rows_kernel<<<bgrid(z), kBataxThreads, 0, st>>>(z, m, A->rowptr, w.ridx);
+        NSD_TRY(check_launch("slot_rows_kernel"));
+        ridx = w.ridx;
+    }
+    const int32_t *in[2] = {ridx, reinterpret_cast<const int32_t *>(A->val)};
+    int32_t *out[2] = {w.crow, reinterpret_cast<int32_t *>(w.cval)};
+    NSD_TRY(radix_sort_multi(z, n, A->colind, 2, in, w.csort, out, w.sort_ws, st));
     NSD_TRY(segptr_from_sorted(z, n, w.csort, w.colptr, st));
-    slot_rows_kernel<<<bgrid(z), kBataxThreads, 0, st>>>(z, m, A->rowptr, w.cperm, w.crow);
-    NSD_TRY(check_launch("slot_rows_kernel"));
-    NSD_HIP(hipMemsetAsync(w.mx, 0, sizeof(int32_t), st));
+    NSD_HIP(hipMemsetAsync(w.mx, 0, 2 * sizeof(int32_t), st));
     row_terms_kernel<<<bgrid(n), kBataxThreads, 0, st>>>(n, w.colptr, w.crow, A->rowptr,
                                                          w.terms, w.mx);
     NSD_TRY(check_launch("row_terms_kernel"));
-    int32_t mx = 0;
-    NSD_HIP(hipMemcpyAsync(&mx, w.mx, sizeof(mx), hipMemcpyDeviceToHost, st));
+    int32_t mx[2] = {0, 0};  // the most terms of a row of J; the longest column of A
+    NSD_HIP(hipMemcpyAsync(mx, w.mx, sizeof(mx), hipMemcpyDeviceToHost, st));
     NSD_HIP(hipStreamSynchronize(st));
-    if (mx > cap) return NSD_OK;  // some row of J is too long: the sort path
-    NSD_TRY(scan_exclusive(w.terms, w.toff, n, w.mx + 1, w.scan_ws, st));
+    if (mx[0] > cap) return NSD_OK;  // some row of J is too long: the sort path
+    NSD_TRY(scan_exclusive(w.terms, w.toff, n, w.mx + 2, w.scan_ws, st));
     BataxRows a;
     a.ncols = n;
     a.rowptr = A->rowptr;
     a.colind = A->colind;
     a.val = A->val;
     a.colptr = w.colptr;
-    a.cperm = w.cperm;
+    a.cval = w.cval;
     a.crow = w.crow;
     a.beta = beta;
     a.toff = w.toff;
     a.tkey = w.tkey;
     a.tval = w.tval;
     a.cnt = w.cnt;
+    // every gathered row stores column j, so a column's rows are at most its
+    // row's terms: mx[1] <= mx[0] <= kRowCap
+    const bool narrow = n < (1 << (32 - kPosBits));  // every real key below the padding
+    int32_t np2 = kWave;
+    while (np2 < mx[0]) np2 <<= 1;
+    auto r16 = [](int64_t b) { return (int32_t)((b + 15) / 16 * 16); };
+    const int32_t nrm = std::max(mx[1], 1);
+    a.off_term = r16((int64_t)np2 * (narrow ? 4 : 8));
+    a.off_pre = a.off_term + r16(4LL * std::max(mx[0], 1));
+    a.off_beg = a.off_pre + r16(4LL * (nrm + 1));
+    a.off_a = a.off_beg + r16(4LL * nrm);
+    a.lds_wave = a.off_a + r16(4LL * nrm);
+    const size_t lds = (size_t)kRowWaves * a.lds_wave;  // at most 12.3 KB per wave
+    const unsigned blocks = (unsigned)ceil_div(n, kRowWaves);
     probe_begin(NSD_KERNEL_BATAX_ROWS, st);
-    if (n < (1 << (32 - kPosBits)))  // every real key below the padding
-        batax_rows_kernel<uint32_t><<<(unsigned)n, kRowThreads, 0, st>>>(a);
+    if (narrow)
+        batax_rows_kernel<uint32_t><<<blocks, kRowBlock, lds, st>>>(a);
     else
-        batax_rows_kernel<unsigned long long><<<(unsigned)n, kRowThreads, 0, st>>>(a);
+        batax_rows_kernel<unsigned long long><<<blocks, kRowBlock, lds, st>>>(a);
     probe_end(NSD_KERNEL_BATAX_ROWS, st);
     NSD_TRY(check_launch("batax_rows_kernel"));
     NSD_TRY(scan_exclusive(w.cnt, jrowptr, n, jrowptr + n, w.scan_ws, st));

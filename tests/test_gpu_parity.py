@@ -852,7 +852,8 @@ def many_rows_pattern(rng):
 def test_batax_row_path_equals_sort_path(nsd, operand, orc, case):
     """J built row by row in LDS (when no row of J has more than 512 terms)
     and by the two global sorts (forced with NSD_BATAX_ROW_CAP=0): the same
-    bits, and the oracle's keys."""
+    bits, and the oracle's keys; likewise from a CSR descriptor without its
+    row index (the row path derives it from rowptr)."""
     import os
     from paper_2303_07030_amd import synth
     rng = np.random.default_rng(31)
@@ -894,6 +895,13 @@ def test_batax_row_path_equals_sort_path(nsd, operand, orc, case):
     finally:
         del os.environ["NSD_BATAX_ROW_CAP"]
     for x, y in zip(default, forced):
+        assert np.array_equal(x.view(np.uint8), y.view(np.uint8))
+
+    class Bare:  # rowptr, colind, val only
+        desc = nsd.csr_desc(A.nrows, A.ncols, A.rowptr, None, A.colind, A.val)
+    Bare.ncols = A.ncols
+    bare = run_batax(nsd, Bare, 1.25)
+    for x, y in zip(default, bare):
         assert np.array_equal(x.view(np.uint8), y.view(np.uint8))
     check_batax(orc, nrows, ncols, rowptr, colind, val, 1.25, default)
 
