@@ -243,6 +243,73 @@ struct RowKey<unsigned long long> {
     __device__ static int32_t pos(unsigned long long x) { return (int32_t)(uint32_t)x; }
 };
 
+// Compare-exchange of two keys of the bitonic network, a at the lower index:
+// afterwards a <= b when up, a >= b otherwise.
+template <class Key>
+__device__ __forceinline__ void row_ce(Key &a, Key &b, bool up) {
+    const bool sw = (a > b) == up;
+    const Key x = sw ? b : a, y = sw ? a : b;
+    a = x;
+    b = y;
+}
+
+// Substeps of bitonic stage `size` with strides 2^(lo + C - 1) down to 2^lo
+// in one pass over LDS: each lane holds the 2^C keys that those substeps
+// exchange among themselves (indices base + m 2^lo), so the C substeps
+// cost one LDS round trip.  The direction is that of the stage for all of
+// them (bit `size` of the index lies above the exchanged bits).
+template <class Key, int C>
+__device__ __forceinline__ void bitonic_group(Key *skey, int32_t np2, int32_t size, int lo,
+                                              int l) {
+    constexpr int E = 1 << C;
+    for (int32_t t = l; t < (np2 >> C); t += kWave) {
+        const int32_t base = ((t >> lo) << (lo + C)) | (t & ((1 << lo) - 1));
+        Key v[E];
+#pragma unroll
+        for (int m = 0; m < E; ++m) v[m] = skey[base + (m << lo)];
+        const bool up = (base & size) == 0;
+#pragma unroll
+        for (int b = C - 1; b >= 0; --b)
+#pragma unroll
+            for (int m = 0; m < E; ++m)
+                if (!(m & (1 << b))) row_ce(v[m], v[m | (1 << b)], up);
+#pragma unroll
+        for (int m = 0; m < E; ++m) skey[base + (m << lo)] = v[m];
+    }
+    __syncwarp();  // this wave only
+}
+
+// Stages 2, 4 and 8 of the bitonic network on every group of 8 consecutive
+// keys in one pass (the directions of stages 2 and 4 change inside a group:
+// bits 1 and 2 of the index).
+template <class Key>
+__device__ __forceinline__ void bitonic_first8(Key *skey, int32_t np2, int l) {
+    for (int32_t t = l; t < (np2 >> 3); t += kWave) {
+        const int32_t base = t << 3;
+        Key v[8];
+#pragma unroll
+        for (int m = 0; m < 8; ++m) v[m] = skey[base + m];
+#pragma unroll
+        for (int m = 0; m < 8; m += 2) row_ce(v[m], v[m + 1], (m & 2) == 0);
+#pragma unroll
+        for (int m = 0; m < 8; ++m)
+            if (!(m & 2)) row_ce(v[m], v[m + 2], (m & 4) == 0);
+#pragma unroll
+        for (int m = 0; m < 8; m += 2) row_ce(v[m], v[m + 1], (m & 4) == 0);
+        const bool up = (base & 8) == 0;
+#pragma unroll
+        for (int m = 0; m < 4; ++m) row_ce(v[m], v[m + 4], up);
+#pragma unroll
+        for (int m = 0; m < 8; ++m)
+            if (!(m & 2)) row_ce(v[m], v[m + 2], up);
+#pragma unroll
+        for (int m = 0; m < 8; m += 2) row_ce(v[m], v[m + 1], up);
+#pragma unroll
+        for (int m = 0; m < 8; ++m) skey[base + m] = v[m];
+    }
+    __syncwarp();  // this wave only
+}
+
 // Row j of J by one wave (at most kRowCap terms, checked by the caller); the
 // LDS regions are sized by the caller from the largest row's term count and
 // the longest column of A, so every index below stays inside its array.
@@ -310,11 +377,14 @@ __global__ __launch_bounds__(kRowBlock) void batax_rows_kernel(BataxRows a) {
     }
     __syncwarp();  // this wave only
     // 3. bitonic sort of the (k, position) pairs in LDS, ascending: equal
-    //    keys keep their positions' order (measured on MI355X against a
-    //    sort in registers with cross-lane shuffles, 634 us per call on the
-    //    uniform 1M-entry workload, and ranks by binary searches in the
-    //    other gathered rows, 685 us: this takes 407 us with 64-bit keys,
-    //    346 with 32-bit ones)
+    //    keys keep their positions' order (measured on MI355X with LDS
+    //    regions sized for 512 terms, against a sort in registers with
+    //    cross-lane shuffles, 634 us per call on the uniform 1M-entry
+    //    workload, and ranks by binary searches in the other gathered rows,
+    //    685 us: this took 407 us with 64-bit keys, 346 with 32-bit ones;
+    //    with regions sized for the largest row, one substep per round trip
+    //    200 us, up to three 187 us)
+#ifdef NSD_BATAX_SORT_PLAIN
     for (int32_t size = 2; size <= np2; size <<= 1) {
         for (int32_t stride = size >> 1; stride > 0; stride >>= 1) {
             for (int32_t t = l; t < np2 / 2; t += kWave) {
@@ -328,6 +398,20 @@ __global__ __launch_bounds__(kRowBlock) void batax_rows_kernel(BataxRows a) {
             __syncwarp();  // this wave only
         }
     }
+#else
+    // the same network, up to three substeps per LDS round trip: stages
+    // 2-8 in one pass, then each stage's strides from the top, the first
+    // pass taking log2(size) mod 3 of them and every later one three
+    bitonic_first8<Key>(skey, np2, l);
+    for (int32_t size = 16, n = 4; size <= np2; size <<= 1, ++n) {
+        int hi = n - 1;  // log2 of the largest stride left
+        const int first = n % 3;
+        if (first == 1) bitonic_group<Key, 1>(skey, np2, size, hi, l);
+        if (first == 2) bitonic_group<Key, 2>(skey, np2, size, hi - 1, l);
+        hi -= first;
+        for (; hi >= 2; hi -= 3) bitonic_group<Key, 3>(skey, np2, size, hi - 2, l);
+    }
+#endif
     // 4. runs of equal k: each lane takes a contiguous chunk of the sorted
     //    terms, numbers the runs that start there, and sums each of them in
     //    order in fp64 (a run may continue into the next lanes' chunks)
