@@ -164,20 +164,32 @@ __global__ void slot_rows_kernel(int64_t n, int32_t nrows, const int32_t *rowptr
     row[c] = lo;
 }
 
-// terms[j] = number of terms of row j of J: the summed lengths of the rows
-// of A storing column j; the largest goes to mx[0], the largest number of
-// rows of A storing one column to mx[1] (integer maxima: any order).
-__global__ void row_terms_kernel(int32_t ncols, const int32_t *colptr, const int32_t *crow,
-                                 const int32_t *rowptr, int32_t *terms, int32_t *mx) {
+// len[c] = the length of the row of A holding CSC slot c: the terms that
+// entry contributes to its column's row of J.
+__global__ void slot_len_kernel(int64_t n, const int32_t *crow, const int32_t *rowptr,
+                                int32_t *len) {
+    const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= n) return;
+    const int32_t i = crow[c];
+    len[c] = rowptr[i + 1] - rowptr[i];
+}
+
+// From the exclusive prefix sums `pre` of those lengths over the CSC slots
+// (nnz of them, their total at *total): toff[j] = the first term of row j of
+// J, and the largest row's term count to mx[0], the longest column of A to
+// mx[1] (integer maxima: any order).
+__global__ void row_terms_kernel(int32_t ncols, int32_t nnz, const int32_t *colptr,
+                                 const int32_t *pre, const int32_t *total, int32_t *toff,
+                                 int32_t *mx) {
     const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     int32_t t = 0, nr = 0;
     if (j < ncols) {
-        nr = colptr[j + 1] - colptr[j];
-        for (int32_t c = colptr[j]; c < colptr[j + 1]; ++c) {
-            const int32_t i = crow[c];
-            t += rowptr[i + 1] - rowptr[i];
-        }
-        terms[j] = t;
+        const int32_t c0 = colptr[j], c1 = colptr[j + 1];
+        const int32_t b = c0 < nnz ? pre[c0] : *total;
+        const int32_t e = c1 < nnz ? pre[c1] : *total;
+        toff[j] = b;
+        t = e - b;
+        nr = c1 - c0;
     }
 #pragma unroll
     for (int m = kWave / 2; m >= 1; m >>= 1) {
@@ -450,7 +462,7 @@ __global__ __launch_bounds__(kRowThreads) void batax_compact_kernel(
 }
 
 struct BataxRowWs {
-    int32_t *csort, *ridx, *crow, *colptr, *terms, *toff, *cnt, *tkey, *mx;
+    int32_t *csort, *ridx, *crow, *colptr, *toff, *cnt, *tkey, *mx;
     float *cval, *tval;
     void *sort_ws, *scan_ws;
 };
@@ -462,7 +474,6 @@ static void batax_row_carve(Carver &c, int32_t ncols, int32_t nnz, int64_t P, Ba
     w->cval = c.take<float>(z);
     w->crow = c.take<int32_t>(z);
     w->colptr = c.take<int32_t>(n + 1);
-    w->terms = c.take<int32_t>(n);
     w->toff = c.take<int32_t>(n);
     w->cnt = c.take<int32_t>(n);
     w->mx = c.take<int32_t>(64);
@@ -491,15 +502,24 @@ static nsd_status batax_by_rows(const nsd_csr *A, float beta, int64_t P, int cap
     int32_t *out[2] = {w.crow, reinterpret_cast<int32_t *>(w.cval)};
     NSD_TRY(radix_sort_multi(z, n, A->colind, 2, in, w.csort, out, w.sort_ws, st));
     NSD_TRY(segptr_from_sorted(z, n, w.csort, w.colptr, st));
+    // every row of J's first term: the prefix sums of the gathered row
+    // lengths over the CSC slots (their total is the number of products)
+    int32_t *len = w.ridx;  // free once the sort has read it
+    slot_len_kernel<<<bgrid(z), kBataxThreads, 0, st>>>(z, w.crow, A->rowptr, len);
+    NSD_TRY(check_launch("slot_len_kernel"));
     NSD_HIP(hipMemsetAsync(w.mx, 0, 2 * sizeof(int32_t), st));
-    row_terms_kernel<<<bgrid(n), kBataxThreads, 0, st>>>(n, w.colptr, w.crow, A->rowptr,
-                                                         w.terms, w.mx);
+    NSD_TRY(scan_exclusive(len, len, z, w.mx + 2, w.scan_ws, st));
+    row_terms_kernel<<<bgrid(n), kBataxThreads, 0, st>>>(n, z, w.colptr, len, w.mx + 2, w.toff,
+                                                         w.mx);
     NSD_TRY(check_launch("row_terms_kernel"));
-    int32_t mx[2] = {0, 0};  // the most terms of a row of J; the longest column of A
+    // the most terms of a row of J, the longest column of A, the products
+    int32_t mx[3] = {0, 0, 0};
     NSD_HIP(hipMemcpyAsync(mx, w.mx, sizeof(mx), hipMemcpyDeviceToHost, st));
     NSD_HIP(hipStreamSynchronize(st));
+    if ((int64_t)mx[2] != P)
+        return fail(NSD_ERR_INVALID_ARG, "npairs = %lld, but A's rows give %d pairs",
+                    (long long)P, mx[2]);
     if (mx[0] > cap) return NSD_OK;  // some row of J is too long: the sort path
-    NSD_TRY(scan_exclusive(w.terms, w.toff, n, w.mx + 2, w.scan_ws, st));
     BataxRows a;
     a.ncols = n;
     a.rowptr = A->rowptr;
@@ -661,20 +681,24 @@ nsd_status nsd_batax_jacobian(const nsd_csr *A, float beta, int64_t npairs, int3
         return NSD_OK;
     }
     // 1. term offsets per row and the terms
-    row_pairs_kernel<<<bgrid(m), kBataxThreads, 0, st>>>(m, A->rowptr, w.sq);
-    NSD_TRY(check_launch("row_pairs_kernel"));
-    NSD_TRY(scan_exclusive(w.sq, w.off, m, w.tot, w.scan_ws, st));
-    int32_t hp = 0;
-    NSD_HIP(hipMemcpyAsync(&hp, w.tot, sizeof(hp), hipMemcpyDeviceToHost, st));
-    NSD_HIP(hipStreamSynchronize(st));
-    if ((int64_t)hp != P)
-        return fail(NSD_ERR_INVALID_ARG, "npairs = %lld, but A's rows give %d pairs",
-                    (long long)P, hp);
+    // the row path checks npairs against A before it writes anything but
+    // workspace; the sort path checks it here when the row path is off
     const int cap = row_cap();
     if (cap > 0) {
         bool done = false;
         NSD_TRY(batax_by_rows(A, beta, P, cap, rw, jrowptr, jcolind, jval, nnz_out, &done, st));
         if (done) return NSD_OK;
+    }
+    row_pairs_kernel<<<bgrid(m), kBataxThreads, 0, st>>>(m, A->rowptr, w.sq);
+    NSD_TRY(check_launch("row_pairs_kernel"));
+    NSD_TRY(scan_exclusive(w.sq, w.off, m, w.tot, w.scan_ws, st));
+    if (cap == 0) {
+        int32_t hp = 0;
+        NSD_HIP(hipMemcpyAsync(&hp, w.tot, sizeof(hp), hipMemcpyDeviceToHost, st));
+        NSD_HIP(hipStreamSynchronize(st));
+        if ((int64_t)hp != P)
+            return fail(NSD_ERR_INVALID_ARG, "npairs = %lld, but A's rows give %d pairs",
+                        (long long)P, hp);
     }
     expand_pairs_kernel<<<bgrid(P), kBataxThreads, 0, st>>>(P, m, w.off, A->rowptr, A->colind,
                                                             A->val, beta, w.key_j, w.key_k,

@@ -906,7 +906,11 @@ def test_batax_row_path_equals_sort_path(nsd, operand, orc, case):
     check_batax(orc, nrows, ncols, rowptr, colind, val, 1.25, default)
 
 
-def test_batax_jacobian_rejects_wrong_pair_count(nsd, operand):
+@pytest.mark.parametrize("row_cap", [None, "0"])
+def test_batax_jacobian_rejects_wrong_pair_count(nsd, operand, row_cap, monkeypatch):
+    """A wrong npairs is refused on the row path and on the sort path."""
+    if row_cap is not None:
+        monkeypatch.setenv("NSD_BATAX_ROW_CAP", row_cap)
     nrows, ncols, rowptr, colind, val = edge_pattern(18)
     A = operand(nrows, ncols, rowptr, colind, val, build_csc=False)
     ws0 = torch.empty(256, dtype=torch.uint8, device="cuda")
