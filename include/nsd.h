@@ -302,8 +302,8 @@ nsd_status nsd_csr_expand_rows(int32_t nrows, int32_t nnz, const int32_t *rowptr
  * perm (input position of the first occurrence of each output entry).
  * *nnz_out is a host int32.  Index outputs are bit-exact; a merged value is
  * the fp32 sum of its duplicates in input order.  Coordinates out of range
- * give NSD_ERR_BAD_FORMAT (outputs untouched); on NSD_ERR_DUPLICATE rowidx,
- * colind, val_out and perm hold unspecified values and rowptr is untouched.
+ * give NSD_ERR_BAD_FORMAT (outputs untouched); on NSD_ERR_DUPLICATE the
+ * outputs hold unspecified values.
  * Synchronous.  ws: nsd_build_workspace_size(nnz, max(nrows, ncols)).
  */
 nsd_status nsd_coo_to_csr(int32_t nrows, int32_t ncols, int32_t nnz, const int32_t *row,

@@ -179,6 +179,17 @@ constexpr int kBins = 256;
 constexpr int kSortWaves = kSortThreads / kWave;
 constexpr int kMaxPayloads = 3;
 
+// The digit of a key at bit `shift`.  A composite key (lo_bits > 0) is the
+// pair (hi, lo) read as hi * 2^lo_bits + lo, with lo < 2^lo_bits: sorting by
+// it orders by hi, then by lo, in one sort.
+__device__ __forceinline__ int key_digit(int32_t lo, int32_t hi, int lo_bits, int shift) {
+    const uint32_t l = (uint32_t)lo, h = (uint32_t)hi;
+    // lo_bits and shift are the same for every thread: scalar branches
+    if (lo_bits == 0 || shift + 8 <= lo_bits) return (int)((l >> shift) & (kBins - 1));
+    if (shift >= lo_bits) return (int)((h >> (shift - lo_bits)) & (kBins - 1));
+    return (int)(((l >> shift) | (h << (lo_bits - shift))) & (kBins - 1));  // straddles both
+}
+
 // Digit counts of one tile.  Keys drawn from a skewed distribution share
 // their high digits, and same-address LDS atomics of one instruction are
 // serialised, so each round first peels off up to kHistPeel digit groups:
@@ -195,7 +206,10 @@ constexpr int kHistPeel = NSD_HIST_PEEL;
 constexpr int kHistPeel = 1;
 #endif
 
-__global__ __launch_bounds__(kSortThreads) void radix_hist_kernel(const int32_t *keys, int64_t n,
+template <bool PAIR>
+__global__ __launch_bounds__(kSortThreads) void radix_hist_kernel(const int32_t *keys,
+                                                                  const int32_t *khi,
+                                                                  int lo_bits, int64_t n,
                                                                   int shift, int64_t ntiles,
                                                                   int32_t *hist) {
     __shared__ int cnt[kBins];
@@ -203,17 +217,19 @@ __global__ __launch_bounds__(kSortThreads) void radix_hist_kernel(const int32_t 
     __syncthreads();
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t base = (int64_t)blockIdx.x * kSortTile;
-    int key[kSortRounds];
+    int key[kSortRounds], hi[kSortRounds];
 #pragma unroll
     for (int i = 0; i < kSortRounds; ++i) {
         const int64_t q = base + (int64_t)i * kSortThreads + threadIdx.x;
         key[i] = q < n ? keys[q] : 0;
+        if constexpr (PAIR) hi[i] = q < n ? khi[q] : 0;  // a composite key's high words
     }
 #pragma unroll
     for (int i = 0; i < kSortRounds; ++i) {
         const int64_t q = base + (int64_t)i * kSortThreads + threadIdx.x;
         const bool valid = q < n;
-        const int d = ((uint32_t)key[i] >> shift) & (kBins - 1);
+        const int d = PAIR ? key_digit(key[i], hi[i], lo_bits, shift)
+                           : (int)(((uint32_t)key[i] >> shift) & (kBins - 1));
         uint64_t rest = __ballot(valid);  // lanes not yet counted (wave-uniform)
 #pragma unroll
         for (int it = 0; it < kHistPeel; ++it) {
@@ -253,7 +269,8 @@ __device__ __forceinline__ int64_t xcd_contiguous_tile() {
 // Payloads carried with the keys: in[j] NULL is the element's own index.
 // Carrying what a caller would otherwise gather through the sort's
 // permutation (one random 4-byte read per element) costs 8 more bytes per
-// element and pass, read and written in runs.
+// element and pass, read and written in runs.  With a composite key
+// (lo_bits > 0) payload 0 is the key's high word.
 struct SortPayloads {
     const int32_t *in[kMaxPayloads];
     int32_t *out[kMaxPayloads];
@@ -261,8 +278,8 @@ struct SortPayloads {
 
 template <int NP>
 __global__ __launch_bounds__(kSortThreads) void radix_scatter_kernel(
-    const int32_t *kin, SortPayloads pl, int32_t *kout, int64_t n, int shift, int64_t ntiles,
-    const int32_t *offs) {
+    const int32_t *kin, SortPayloads pl, int32_t *kout, int64_t n, int lo_bits, int shift,
+    int64_t ntiles, const int32_t *offs) {
     __shared__ int wcnt[kSortWaves][kBins];
     __shared__ int tile_off[kBins];
     __shared__ int tile_start[kBins];
@@ -286,7 +303,7 @@ __global__ __launch_bounds__(kSortThreads) void radix_scatter_kernel(
 #pragma unroll
         for (int j = 0; j < NP; ++j)
             val[j][i] = valid ? (pl.in[j] ? pl.in[j][q] : (int32_t)q) : 0;
-        const int d = ((uint32_t)key[i] >> shift) & (kBins - 1);
+        const int d = key_digit(key[i], val[0][i], lo_bits, shift);
         dig[i] = d;
         uint64_t same = __ballot(valid);
 #pragma unroll
@@ -328,39 +345,53 @@ __global__ __launch_bounds__(kSortThreads) void radix_scatter_kernel(
     // same buffer (the staged keys give every position its output slot): one
     // buffer keeps four blocks per CU where a buffer per payload allowed two
     // (measured on MI355X: 0.52 against 0.62 ms per pass of 50M with three
-    // payloads, 0.37 against 0.53 with two)
+    // payloads, 0.37 against 0.53 with two).  The staged positions' digits,
+    // found with the first payload (a composite key's high word), serve the
+    // later payloads.
+    int lpos[kSortRounds];  // each element's staging slot (its digit run, its rank)
+#pragma unroll
+    for (int i = 0; i < kSortRounds; ++i) {
+        const int64_t q = base + (int64_t)i * kWave + lane;
+        lpos[i] = q < n ? tile_start[dig[i]] + wcnt[wave][dig[i]] + rank[i] : -1;
+    }
+    int odig[kSortRounds];
 #pragma unroll
     for (int j = 0; j < NP; ++j) {
         if (j > 0) __syncthreads();  // the previous payload is written out
 #pragma unroll
         for (int i = 0; i < kSortRounds; ++i) {
-            const int64_t q = base + (int64_t)i * kWave + lane;
-            if (q < n) {
-                const int lp = tile_start[dig[i]] + wcnt[wave][dig[i]] + rank[i];
-                if (j == 0) skey[lp] = key[i];
-                sval[lp] = val[j][i];
+            if (lpos[i] >= 0) {
+                if (j == 0) skey[lpos[i]] = key[i];
+                sval[lpos[i]] = val[j][i];
             }
         }
         __syncthreads();
-        for (int lp = threadIdx.x; lp < tile_n; lp += kSortThreads) {
-            const int k = skey[lp];
-            const int d = ((uint32_t)k >> shift) & (kBins - 1);
-            const int64_t pos = (int64_t)tile_off[d] + (lp - tile_start[d]);
-            if (j == 0) kout[pos] = k;
-            pl.out[j][pos] = sval[lp];
+#pragma unroll
+        for (int r = 0; r < kSortRounds; ++r) {
+            const int lp = threadIdx.x + r * kSortThreads;
+            if (lp < tile_n) {
+                if (j == 0) odig[r] = key_digit(skey[lp], sval[lp], lo_bits, shift);
+                const int d = odig[r];
+                const int64_t pos = (int64_t)tile_off[d] + (lp - tile_start[d]);
+                if (j == 0) kout[pos] = skey[lp];
+                pl.out[j][pos] = sval[lp];
+            }
         }
     }
 }
 
-static int key_passes(int32_t max_key) {
+// Bits of the largest key below max_key (0 for max_key <= 1).
+static int key_bits(int32_t max_key) {
     uint32_t top = max_key > 0 ? (uint32_t)(max_key - 1) : 0u;
     int bits = 0;
     while (top) {
         ++bits;
         top >>= 1;
     }
-    return bits == 0 ? 1 : (bits + 7) / 8;
+    return bits;
 }
+
+static int digit_passes(int bits) { return bits == 0 ? 1 : (bits + 7) / 8; }
 
 size_t sort_ws_bytes(int64_t n, int32_t max_key, int np) {
     Carver c(nullptr);
@@ -379,16 +410,18 @@ size_t sort_ws_bytes(int64_t n, int32_t max_key, int np) {
 
 template <int NP>
 static nsd_status launch_scatter(int64_t ntiles, const int32_t *ksrc, const SortPayloads &pl,
-                                 int32_t *kdst, int64_t n, int shift, const int32_t *hist,
-                                 hipStream_t st) {
-    radix_scatter_kernel<NP><<<ntiles, kSortThreads, 0, st>>>(ksrc, pl, kdst, n, shift, ntiles,
-                                                              hist);
+                                 int32_t *kdst, int64_t n, int lo_bits, int shift,
+                                 const int32_t *hist, hipStream_t st) {
+    radix_scatter_kernel<NP><<<ntiles, kSortThreads, 0, st>>>(ksrc, pl, kdst, n, lo_bits, shift,
+                                                              ntiles, hist);
     return check_launch("radix_scatter_kernel");
 }
 
-nsd_status radix_sort_multi(int64_t n, int32_t max_key, const int32_t *key_in, int np,
-                            const int32_t *const *payload_in, int32_t *key_out,
-                            int32_t *const *payload_out, void *ws, hipStream_t st) {
+// The passes of one sort: keys of `bits` bits, composite when lo_bits > 0
+// (then payload 0 is the key's high word).
+static nsd_status radix_sort_passes(int64_t n, int bits, int lo_bits, const int32_t *key_in,
+                                    int np, const int32_t *const *payload_in, int32_t *key_out,
+                                    int32_t *const *payload_out, void *ws, hipStream_t st) {
     if (n <= 0) return NSD_OK;
     if (np < 1 || np > kMaxPayloads) return fail(NSD_ERR_INVALID_ARG, "%d sort payloads", np);
     Carver c(ws);
@@ -401,7 +434,7 @@ nsd_status radix_sort_multi(int64_t n, int32_t max_key, const int32_t *key_in, i
     }
     int32_t *hist = c.take<int32_t>(ntiles * kBins);
     void *scan_ws = c.base + c.bytes();
-    const int passes = key_passes(max_key);
+    const int passes = digit_passes(bits);
     const int32_t *ksrc = key_in;
     SortPayloads pl{};
     for (int j = 0; j < np; ++j) pl.in[j] = payload_in[j];
@@ -409,20 +442,43 @@ nsd_status radix_sort_multi(int64_t n, int32_t max_key, const int32_t *key_in, i
         const bool last = p == passes - 1;
         int32_t *kdst = last ? key_out : kbuf[p & 1];
         for (int j = 0; j < np; ++j) pl.out[j] = last ? payload_out[j] : vbuf[j][p & 1];
-        radix_hist_kernel<<<ntiles, kSortThreads, 0, st>>>(ksrc, n, 8 * p, ntiles, hist);
+        if (lo_bits > 0)
+            radix_hist_kernel<true><<<ntiles, kSortThreads, 0, st>>>(ksrc, pl.in[0], lo_bits, n,
+                                                                     8 * p, ntiles, hist);
+        else
+            radix_hist_kernel<false><<<ntiles, kSortThreads, 0, st>>>(ksrc, nullptr, 0, n, 8 * p,
+                                                                      ntiles, hist);
         NSD_TRY(check_launch("radix_hist_kernel"));
         NSD_TRY(scan_exclusive(hist, hist, ntiles * kBins, nullptr, scan_ws, st));
         probe_begin(NSD_KERNEL_SORT, st);
+        const int sh = 8 * p;
         switch (np) {
-            case 1: NSD_TRY(launch_scatter<1>(ntiles, ksrc, pl, kdst, n, 8 * p, hist, st)); break;
-            case 2: NSD_TRY(launch_scatter<2>(ntiles, ksrc, pl, kdst, n, 8 * p, hist, st)); break;
-            default: NSD_TRY(launch_scatter<3>(ntiles, ksrc, pl, kdst, n, 8 * p, hist, st));
+            case 1: NSD_TRY(launch_scatter<1>(ntiles, ksrc, pl, kdst, n, lo_bits, sh, hist, st)); break;
+            case 2: NSD_TRY(launch_scatter<2>(ntiles, ksrc, pl, kdst, n, lo_bits, sh, hist, st)); break;
+            default: NSD_TRY(launch_scatter<3>(ntiles, ksrc, pl, kdst, n, lo_bits, sh, hist, st));
         }
         probe_end(NSD_KERNEL_SORT, st);
         ksrc = kdst;
         for (int j = 0; j < np; ++j) pl.in[j] = pl.out[j];
     }
     return NSD_OK;
+}
+
+nsd_status radix_sort_multi(int64_t n, int32_t max_key, const int32_t *key_in, int np,
+                            const int32_t *const *payload_in, int32_t *key_out,
+                            int32_t *const *payload_out, void *ws, hipStream_t st) {
+    return radix_sort_passes(n, key_bits(max_key), 0, key_in, np, payload_in, key_out,
+                             payload_out, ws, st);
+}
+
+nsd_status radix_sort_pair_key(int64_t n, int32_t max_hi, int32_t max_lo, const int32_t *lo_in,
+                               int np, const int32_t *const *payload_in, int32_t *lo_out,
+                               int32_t *const *payload_out, void *ws, hipStream_t st) {
+    if (np < 1 || payload_in[0] == nullptr)
+        return fail(NSD_ERR_INVALID_ARG, "a pair key needs its high word as payload 0");
+    const int lo_bits = std::max(key_bits(max_lo), 1);
+    return radix_sort_passes(n, lo_bits + key_bits(max_hi), lo_bits, lo_in, np, payload_in,
+                             lo_out, payload_out, ws, st);
 }
 
 nsd_status radix_sort_pairs(int64_t n, int32_t max_key, const int32_t *key_in,
@@ -459,6 +515,38 @@ __global__ void segptr_kernel(int64_t n, int32_t nseg, const int32_t *key, int32
         for (int32_t r = max(prev + 1, 0); r <= cur[u]; ++r) segptr[r] = (int32_t)q;
         prev = cur[u];
     }
+}
+
+// segptr_kernel over sorted (row, col) pairs that also adds to *ndup the
+// positions whose pair equals the previous one (coordinates given more than
+// once, beyond the first): one read of the sorted rows serves both.
+__global__ void segptr_dups_kernel(int64_t n, int32_t nseg, const int32_t *key,
+                                   const int32_t *col, int32_t *segptr, int32_t *ndup) {
+    const int64_t q0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * kSegPer;
+    int dups = 0;
+    if (q0 <= n) {
+        int32_t prev = q0 == 0 ? -1 : min(key[q0 - 1], nseg);
+        int32_t pcol = q0 == 0 ? -1 : col[q0 - 1];
+        int32_t cur[kSegPer], cc[kSegPer];
+#pragma unroll
+        for (int u = 0; u < kSegPer; ++u) {
+            const int64_t q = q0 + u;
+            cur[u] = q < n ? min(key[q], nseg) : nseg;
+            cc[u] = q < n ? col[q] : -1;
+        }
+#pragma unroll
+        for (int u = 0; u < kSegPer; ++u) {
+            const int64_t q = q0 + u;
+            if (q > n) break;
+            for (int32_t r = max(prev + 1, 0); r <= cur[u]; ++r) segptr[r] = (int32_t)q;
+            dups += (q < n && q > 0 && cur[u] == prev && cc[u] == pcol) ? 1 : 0;
+            prev = cur[u];
+            pcol = cc[u];
+        }
+    }
+#pragma unroll
+    for (int m = kWave / 2; m >= 1; m >>= 1) dups += __shfl_xor(dups, m, kWave);
+    if ((threadIdx.x & (kWave - 1)) == 0 && dups) atomicAdd(ndup, dups);
 }
 
 nsd_status segptr_from_sorted(int64_t n, int32_t nseg, const int32_t *sorted_key,
@@ -505,16 +593,6 @@ __global__ void run_heads_kernel(int64_t n, const int32_t *row_s, const int32_t 
     const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (q >= n) return;
     head[q] = (q == 0 || row_s[q] != row_s[q - 1] || col_s[q] != col_s[q - 1]) ? 1 : 0;
-}
-
-// *ndup += the positions q > 0 whose (row, col) equals that of q - 1 in the
-// sorted order: the coordinates given more than once, beyond the first.
-__global__ void dup_count_kernel(int64_t n, const int32_t *row_s, const int32_t *col_s,
-                                 int32_t *ndup) {
-    const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const bool dup = q > 0 && q < n && row_s[q] == row_s[q - 1] && col_s[q] == col_s[q - 1];
-    const uint64_t m = __ballot(dup);
-    if ((threadIdx.x & (kWave - 1)) == 0 && m) atomicAdd(ndup, __popcll(m));
 }
 
 // One thread per run of equal (row, col): the first occurrence names the
@@ -591,7 +669,7 @@ static nsd_status read_flag(int32_t *flag_dev, int32_t *flag_host, hipStream_t s
 static bool too_large(int64_t v) { return v < 0 || v >= (int64_t(1) << 31); }
 
 // n-element arrays a builder carves before the sort's own workspace
-constexpr int kBuildArrays = 10;
+constexpr int kBuildArrays = 6;
 
 }  // namespace nsd
 
@@ -662,17 +740,13 @@ nsd_status nsd_coo_to_csr(int32_t nrows, int32_t ncols, int32_t nnz, const int32
     }
     NSD_REQUIRE(nrows > 0 && ncols > 0, "nnz > 0 needs a non-empty shape");
     Carver c(ws);
-    int32_t *kcol = c.take<int32_t>(nnz);
-    int32_t *perm1 = c.take<int32_t>(nnz);
-    int32_t *rkey = c.take<int32_t>(nnz);
-    int32_t *vkey = c.take<int32_t>(nnz);
     int32_t *row_s = c.take<int32_t>(nnz);
     int32_t *pm = c.take<int32_t>(nnz);
     int32_t *col_s = c.take<int32_t>(nnz);
     int32_t *val_s = c.take<int32_t>(nnz);
     int32_t *head = c.take<int32_t>(nnz);
     int32_t *pos = c.take<int32_t>(nnz);
-    static_assert(kBuildArrays >= 10, "the arrays above");
+    static_assert(kBuildArrays >= 6, "the arrays above");
     int32_t *flag = c.take<int32_t>(64);
     void *sort_ws = c.base + c.bytes();
     void *scan_ws = static_cast<char *>(sort_ws) + sort_ws_bytes(nnz, max_key, kMaxPayloads);
@@ -684,25 +758,21 @@ nsd_status nsd_coo_to_csr(int32_t nrows, int32_t ncols, int32_t nnz, const int32
     NSD_TRY(read_flag(flag, &h, st));
     if (h) return fail(NSD_ERR_BAD_FORMAT, "COO coordinate out of range");
 
-    // stable sort by column, then stably by row: (row, col) order, ties in
-    // input order; the input position, the other coordinate and the value
-    // travel with the keys (the value's bits as a payload)
-    const int32_t *vin = reinterpret_cast<const int32_t *>(val);
+    // one stable sort by the pair (row, col), ties in input order, straight
+    // into the outputs: the row (the key's high word), the input position
+    // and the value's bits travel with the column.  With distinct
+    // coordinates (checked next) the sorted arrays are the CSR.
     {
-        const int32_t *in[3] = {nullptr, row, vin};
-        int32_t *out[3] = {perm1, rkey, vkey};
-        NSD_TRY(radix_sort_multi(nnz, ncols, col, 3, in, kcol, out, sort_ws, st));
+        const int32_t *in[3] = {row, nullptr, reinterpret_cast<const int32_t *>(val)};
+        int32_t *out[3] = {rowidx, perm, reinterpret_cast<int32_t *>(val_out)};
+        NSD_TRY(radix_sort_pair_key(nnz, nrows, ncols, col, 3, in, colind, out, sort_ws, st));
     }
-    // the second sort writes the outputs themselves: with distinct
-    // coordinates (checked next) the sorted arrays are the CSR
-    {
-        const int32_t *in[3] = {perm1, kcol, vkey};
-        int32_t *out[3] = {perm, colind, reinterpret_cast<int32_t *>(val_out)};
-        NSD_TRY(radix_sort_multi(nnz, nrows, rkey, 3, in, rowidx, out, sort_ws, st));
-    }
+    // the row pointers as if the coordinates were distinct, and how many
+    // are not
     NSD_HIP(hipMemsetAsync(flag + 1, 0, sizeof(int32_t), st));
-    dup_count_kernel<<<grid_for(nnz), kThreads, 0, st>>>(nnz, rowidx, colind, flag + 1);
-    NSD_TRY(check_launch("dup_count_kernel"));
+    segptr_dups_kernel<<<grid_for(ceil_div(nnz + 1, kSegPer)), kThreads, 0, st>>>(
+        nnz, nrows, rowidx, colind, rowptr, flag + 1);
+    NSD_TRY(check_launch("segptr_dups_kernel"));
     int32_t ndup = 0;
     NSD_TRY(read_flag(flag + 1, &ndup, st));
     if (ndup > 0 && policy == NSD_DUP_ERROR)
@@ -724,8 +794,8 @@ nsd_status nsd_coo_to_csr(int32_t nrows, int32_t ncols, int32_t nnz, const int32
             nnz, head, pos, row_s, col_s, pm, reinterpret_cast<const float *>(val_s), rowidx,
             colind, val_out, perm);
         NSD_TRY(check_launch("emit_runs_kernel"));
+        NSD_TRY(segptr_from_sorted(nuniq, nrows, rowidx, rowptr, st));
     }
-    NSD_TRY(segptr_from_sorted(nuniq, nrows, rowidx, rowptr, st));
     NSD_HIP(hipStreamSynchronize(st));
     *nnz_out = nuniq;
     return NSD_OK;
