@@ -302,8 +302,8 @@ nsd_status nsd_csr_expand_rows(int32_t nrows, int32_t nnz, const int32_t *rowptr
  * perm (input position of the first occurrence of each output entry).
  * *nnz_out is a host int32.  Index outputs are bit-exact; a merged value is
  * the fp32 sum of its duplicates in input order.  Coordinates out of range
- * give NSD_ERR_BAD_FORMAT (outputs untouched); on NSD_ERR_DUPLICATE the
- * outputs hold unspecified values.
+ * give NSD_ERR_BAD_FORMAT.  After NSD_ERR_BAD_FORMAT or NSD_ERR_DUPLICATE
+ * the outputs hold unspecified values.
  * Synchronous.  ws: nsd_build_workspace_size(nnz, max(nrows, ncols)).
  */
 nsd_status nsd_coo_to_csr(int32_t nrows, int32_t ncols, int32_t nnz, const int32_t *row,
@@ -316,7 +316,9 @@ nsd_status nsd_coo_to_csr(int32_t nrows, int32_t ncols, int32_t nnz, const int32
  * CSR -> CSC by a stable counting sort on the column index (Section 5.3, CSC
  * "expressed similarly" to CSR).  Outputs: colptr [ncols+1]; colidx, rowind,
  * perm [nnz] with perm[q] the CSR slot of CSC slot q; rows ascend within every
- * column.  Bit-exact.  Synchronous.  ws: nsd_build_workspace_size(nnz, ncols).
+ * column.  Bit-exact.  A column index outside [0, ncols) gives
+ * NSD_ERR_BAD_FORMAT (the outputs then hold unspecified values).
+ * Synchronous.  ws: nsd_build_workspace_size(nnz, ncols).
  */
 nsd_status nsd_csr_to_csc(const nsd_csr *A, int32_t *colptr, int32_t *colidx,
                           int32_t *rowind, int32_t *perm, void *ws, size_t ws_bytes,
@@ -326,7 +328,9 @@ nsd_status nsd_csr_to_csc(const nsd_csr *A, int32_t *colptr, int32_t *colidx,
  * Mode index of a COO 3-tensor (or any int32 key array): a stable counting
  * sort of positions 0..nnz-1 by key[p] in [0, dim).  Outputs: segptr [dim+1],
  * segidx [nnz] (sorted keys), perm [nnz] (input position of sorted slot q).
- * Bit-exact.  Synchronous.  ws: nsd_build_workspace_size(nnz, dim).
+ * Bit-exact.  A key outside [0, dim) gives NSD_ERR_BAD_FORMAT (the outputs
+ * then hold unspecified values).  Synchronous.  ws:
+ * nsd_build_workspace_size(nnz, dim).
  */
 nsd_status nsd_coo_mode_index(int32_t nnz, int32_t dim, const int32_t *key,
                               int32_t *segptr, int32_t *segidx, int32_t *perm,

@@ -206,12 +206,18 @@ constexpr int kHistPeel = NSD_HIST_PEEL;
 constexpr int kHistPeel = 1;
 #endif
 
+// With `bad` set (the first pass of a sort whose keys come from a caller),
+// a key outside [0, max_lo) (or a high word outside [0, max_hi)) sets *bad:
+// the range check of a builder rides on the read the sort makes anyway.
+// Digits are masked, so such keys stay within the sort's own arrays.
 template <bool PAIR>
 __global__ __launch_bounds__(kSortThreads) void radix_hist_kernel(const int32_t *keys,
                                                                   const int32_t *khi,
                                                                   int lo_bits, int64_t n,
                                                                   int shift, int64_t ntiles,
-                                                                  int32_t *hist) {
+                                                                  int32_t *hist, int32_t *bad,
+                                                                  int32_t max_lo,
+                                                                  int32_t max_hi) {
     __shared__ int cnt[kBins];
     cnt[threadIdx.x] = 0;
     __syncthreads();
@@ -223,6 +229,15 @@ __global__ __launch_bounds__(kSortThreads) void radix_hist_kernel(const int32_t 
         const int64_t q = base + (int64_t)i * kSortThreads + threadIdx.x;
         key[i] = q < n ? keys[q] : 0;
         if constexpr (PAIR) hi[i] = q < n ? khi[q] : 0;  // a composite key's high words
+    }
+    if (bad) {
+        bool out = false;
+#pragma unroll
+        for (int i = 0; i < kSortRounds; ++i) {
+            out = out || key[i] < 0 || key[i] >= max_lo;
+            if constexpr (PAIR) out = out || hi[i] < 0 || hi[i] >= max_hi;
+        }
+        if (__ballot(out) && lane == 0) atomicOr(bad, 1);
     }
 #pragma unroll
     for (int i = 0; i < kSortRounds; ++i) {
@@ -421,7 +436,9 @@ static nsd_status launch_scatter(int64_t ntiles, const int32_t *ksrc, const Sort
 // (then payload 0 is the key's high word).
 static nsd_status radix_sort_passes(int64_t n, int bits, int lo_bits, const int32_t *key_in,
                                     int np, const int32_t *const *payload_in, int32_t *key_out,
-                                    int32_t *const *payload_out, void *ws, hipStream_t st) {
+                                    int32_t *const *payload_out, void *ws, hipStream_t st,
+                                    int32_t *bad = nullptr, int32_t max_lo = 0,
+                                    int32_t max_hi = 0) {
     if (n <= 0) return NSD_OK;
     if (np < 1 || np > kMaxPayloads) return fail(NSD_ERR_INVALID_ARG, "%d sort payloads", np);
     Carver c(ws);
@@ -442,12 +459,13 @@ static nsd_status radix_sort_passes(int64_t n, int bits, int lo_bits, const int3
         const bool last = p == passes - 1;
         int32_t *kdst = last ? key_out : kbuf[p & 1];
         for (int j = 0; j < np; ++j) pl.out[j] = last ? payload_out[j] : vbuf[j][p & 1];
+        int32_t *chk = p == 0 ? bad : nullptr;  // the caller's keys: the first pass reads them
         if (lo_bits > 0)
-            radix_hist_kernel<true><<<ntiles, kSortThreads, 0, st>>>(ksrc, pl.in[0], lo_bits, n,
-                                                                     8 * p, ntiles, hist);
+            radix_hist_kernel<true><<<ntiles, kSortThreads, 0, st>>>(
+                ksrc, pl.in[0], lo_bits, n, 8 * p, ntiles, hist, chk, max_lo, max_hi);
         else
-            radix_hist_kernel<false><<<ntiles, kSortThreads, 0, st>>>(ksrc, nullptr, 0, n, 8 * p,
-                                                                      ntiles, hist);
+            radix_hist_kernel<false><<<ntiles, kSortThreads, 0, st>>>(
+                ksrc, nullptr, 0, n, 8 * p, ntiles, hist, chk, max_lo, max_hi);
         NSD_TRY(check_launch("radix_hist_kernel"));
         NSD_TRY(scan_exclusive(hist, hist, ntiles * kBins, nullptr, scan_ws, st));
         probe_begin(NSD_KERNEL_SORT, st);
@@ -471,14 +489,21 @@ nsd_status radix_sort_multi(int64_t n, int32_t max_key, const int32_t *key_in, i
                              payload_out, ws, st);
 }
 
-nsd_status radix_sort_pair_key(int64_t n, int32_t max_hi, int32_t max_lo, const int32_t *lo_in,
-                               int np, const int32_t *const *payload_in, int32_t *lo_out,
-                               int32_t *const *payload_out, void *ws, hipStream_t st) {
+// The same by the pair (hi, lo), hi in [0, max_hi) and lo in [0, max_lo):
+// ordered by hi, then by lo, stable, in one sort of the combined bits.  The
+// high words come in (and go out) as payload 0; lo is the key array.  The
+// workspace is sort_ws_bytes(n, any, np).  *bad is set when a key is out of
+// its range (the order is then unspecified).
+static nsd_status radix_sort_pair_key(int64_t n, int32_t max_hi, int32_t max_lo,
+                                      const int32_t *lo_in, int np,
+                                      const int32_t *const *payload_in, int32_t *lo_out,
+                                      int32_t *const *payload_out, void *ws, hipStream_t st,
+                                      int32_t *bad) {
     if (np < 1 || payload_in[0] == nullptr)
         return fail(NSD_ERR_INVALID_ARG, "a pair key needs its high word as payload 0");
     const int lo_bits = std::max(key_bits(max_lo), 1);
     return radix_sort_passes(n, lo_bits + key_bits(max_hi), lo_bits, lo_in, np, payload_in,
-                             lo_out, payload_out, ws, st);
+                             lo_out, payload_out, ws, st, bad, max_lo, max_hi);
 }
 
 nsd_status radix_sort_pairs(int64_t n, int32_t max_key, const int32_t *key_in,
@@ -574,13 +599,6 @@ template <class T>
 __global__ void gather_kernel(int64_t n, const int32_t *perm, const T *src, T *dst) {
     const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (q < n) dst[q] = src[perm[q]];
-}
-
-__global__ void coo_range_kernel(int64_t n, int32_t nrows, int32_t ncols, const int32_t *row,
-                                 const int32_t *col, int32_t *flag) {
-    const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (p >= n) return;
-    if (row[p] < 0 || row[p] >= nrows || col[p] < 0 || col[p] >= ncols) atomicOr(flag, 1);
 }
 
 __global__ void key_range_kernel(int64_t n, int32_t dim, const int32_t *key, int32_t *flag) {
@@ -751,30 +769,28 @@ nsd_status nsd_coo_to_csr(int32_t nrows, int32_t ncols, int32_t nnz, const int32
     void *sort_ws = c.base + c.bytes();
     void *scan_ws = static_cast<char *>(sort_ws) + sort_ws_bytes(nnz, max_key, kMaxPayloads);
 
-    int32_t h = 0;
-    NSD_HIP(hipMemsetAsync(flag, 0, sizeof(int32_t), st));
-    coo_range_kernel<<<grid_for(nnz), kThreads, 0, st>>>(nnz, nrows, ncols, row, col, flag);
-    NSD_TRY(check_launch("coo_range_kernel"));
-    NSD_TRY(read_flag(flag, &h, st));
-    if (h) return fail(NSD_ERR_BAD_FORMAT, "COO coordinate out of range");
-
     // one stable sort by the pair (row, col), ties in input order, straight
     // into the outputs: the row (the key's high word), the input position
-    // and the value's bits travel with the column.  With distinct
-    // coordinates (checked next) the sorted arrays are the CSR.
+    // and the value's bits travel with the column; its first pass checks
+    // the coordinates' ranges (flag[0]).  With coordinates in range and
+    // distinct (counted next, flag[1]) the sorted arrays are the CSR.
+    NSD_HIP(hipMemsetAsync(flag, 0, 2 * sizeof(int32_t), st));
     {
         const int32_t *in[3] = {row, nullptr, reinterpret_cast<const int32_t *>(val)};
         int32_t *out[3] = {rowidx, perm, reinterpret_cast<int32_t *>(val_out)};
-        NSD_TRY(radix_sort_pair_key(nnz, nrows, ncols, col, 3, in, colind, out, sort_ws, st));
+        NSD_TRY(radix_sort_pair_key(nnz, nrows, ncols, col, 3, in, colind, out, sort_ws, st,
+                                    flag));
     }
     // the row pointers as if the coordinates were distinct, and how many
     // are not
-    NSD_HIP(hipMemsetAsync(flag + 1, 0, sizeof(int32_t), st));
     segptr_dups_kernel<<<grid_for(ceil_div(nnz + 1, kSegPer)), kThreads, 0, st>>>(
         nnz, nrows, rowidx, colind, rowptr, flag + 1);
     NSD_TRY(check_launch("segptr_dups_kernel"));
-    int32_t ndup = 0;
-    NSD_TRY(read_flag(flag + 1, &ndup, st));
+    int32_t fl[2] = {0, 0};
+    NSD_HIP(hipMemcpyAsync(fl, flag, sizeof(fl), hipMemcpyDeviceToHost, st));
+    NSD_HIP(hipStreamSynchronize(st));
+    if (fl[0]) return fail(NSD_ERR_BAD_FORMAT, "COO coordinate out of range");
+    const int32_t ndup = fl[1];
     if (ndup > 0 && policy == NSD_DUP_ERROR)
         return fail(NSD_ERR_DUPLICATE, "%d duplicate coordinates", ndup);
     int32_t nuniq = nnz;
@@ -816,16 +832,18 @@ nsd_status nsd_csr_to_csc(const nsd_csr *A, int32_t *colptr, int32_t *colidx, in
         for (int i = 0; i < kBuildArrays; ++i) c.take<int32_t>(nnz);
         int32_t *flag = c.take<int32_t>(64);
         void *sort_ws = c.base + c.bytes();
-        int32_t h = 0;
+        // the CSR slot and its row travel with the column keys; the sort's
+        // first pass checks the columns' range
         NSD_HIP(hipMemsetAsync(flag, 0, sizeof(int32_t), st));
-        key_range_kernel<<<grid_for(nnz), kThreads, 0, st>>>(nnz, A->ncols, A->colind, flag);
-        NSD_TRY(check_launch("key_range_kernel"));
-        NSD_TRY(read_flag(flag, &h, st));
-        if (h) return fail(NSD_ERR_BAD_FORMAT, "column index out of range [0, %d)", A->ncols);
-        // the CSR slot and its row travel with the column keys
         const int32_t *in[2] = {nullptr, A->rowidx};
         int32_t *out[2] = {perm, rowind};
-        NSD_TRY(radix_sort_multi(nnz, A->ncols, A->colind, 2, in, colidx, out, sort_ws, st));
+        NSD_TRY(radix_sort_passes(nnz, key_bits(std::max(A->ncols, 1)), 0, A->colind, 2, in,
+                                  colidx, out, sort_ws, st, flag, A->ncols));
+        NSD_TRY(segptr_from_sorted(nnz, A->ncols, colidx, colptr, st));
+        int32_t h = 0;
+        NSD_TRY(read_flag(flag, &h, st));
+        if (h) return fail(NSD_ERR_BAD_FORMAT, "column index out of range [0, %d)", A->ncols);
+        return NSD_OK;
     }
     NSD_TRY(segptr_from_sorted(nnz, A->ncols, colidx, colptr, st));
     NSD_HIP(hipStreamSynchronize(st));
@@ -844,16 +862,20 @@ nsd_status nsd_coo_mode_index(int32_t nnz, int32_t dim, const int32_t *key, int3
         NSD_TRY(nsd_build_workspace_size(nnz, dim, &need));
         if (ws_bytes < need) return fail(NSD_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, need);
         Carver c(ws);
-        for (int i = 0; i < 8; ++i) c.take<int32_t>(nnz);
+        for (int i = 0; i < kBuildArrays; ++i) c.take<int32_t>(nnz);
         int32_t *flag = c.take<int32_t>(64);
         void *sort_ws = c.base + c.bytes();
-        int32_t h = 0;
+        // the sort's first pass checks the keys' range
         NSD_HIP(hipMemsetAsync(flag, 0, sizeof(int32_t), st));
-        key_range_kernel<<<grid_for(nnz), kThreads, 0, st>>>(nnz, dim, key, flag);
-        NSD_TRY(check_launch("key_range_kernel"));
+        const int32_t *in[1] = {nullptr};
+        int32_t *out[1] = {perm};
+        NSD_TRY(radix_sort_passes(nnz, key_bits(dim), 0, key, 1, in, segidx, out, sort_ws, st,
+                                  flag, dim));
+        NSD_TRY(segptr_from_sorted(nnz, dim, segidx, segptr, st));
+        int32_t h = 0;
         NSD_TRY(read_flag(flag, &h, st));
         if (h) return fail(NSD_ERR_BAD_FORMAT, "key out of range [0, %d)", dim);
-        NSD_TRY(radix_sort_pairs(nnz, dim, key, nullptr, segidx, perm, sort_ws, st));
+        return NSD_OK;
     }
     NSD_TRY(segptr_from_sorted(nnz, dim, segidx, segptr, st));
     NSD_HIP(hipStreamSynchronize(st));

@@ -193,13 +193,6 @@ nsd_status radix_sort_pairs(int64_t n, int32_t max_key, const int32_t *key_in,
 nsd_status radix_sort_multi(int64_t n, int32_t max_key, const int32_t *key_in, int np,
                             const int32_t *const *payload_in, int32_t *key_out,
                             int32_t *const *payload_out, void *ws, hipStream_t st);
-// The same by the pair (hi, lo), hi in [0, max_hi) and lo in [0, max_lo):
-// ordered by hi, then by lo, stable, in one sort of the combined bits.  The
-// high words come in (and go out) as payload 0; lo is the key array.  The
-// workspace is sort_ws_bytes(n, any, np).
-nsd_status radix_sort_pair_key(int64_t n, int32_t max_hi, int32_t max_lo, const int32_t *lo_in,
-                               int np, const int32_t *const *payload_in, int32_t *lo_out,
-                               int32_t *const *payload_out, void *ws, hipStream_t st);
 
 // segptr[r] = first position q with sorted_key[q] >= r, for r in [0, nseg].
 nsd_status segptr_from_sorted(int64_t n, int32_t nseg, const int32_t *sorted_key,

@@ -146,7 +146,41 @@ def test_coo_to_csr_errors(nsd):
     with pytest.raises(nsd.NsdError) as e:
         nsd.nsd_coo_to_csr(3, 3, 4, row, bad, val, nsd.NSD_DUP_SUM, *outs, ws)
     assert e.value.status == nsd.NSD_ERR_BAD_FORMAT
+    for r, c in (([0, 3, 1, 2], [0, 2, 2, 1]), ([0, 1, 1, 2], [0, -1, 2, 1]),
+                 ([-5, 1, 1, 2], [0, 2, 2, 1])):  # a row past the end, negative indices
+        with pytest.raises(nsd.NsdError) as e:
+            nsd.nsd_coo_to_csr(3, 3, 4, dev(np.array(r, np.int32)), dev(np.array(c, np.int32)),
+                               val, nsd.NSD_DUP_SUM, *outs, ws)
+        assert e.value.status == nsd.NSD_ERR_BAD_FORMAT
     assert nsd.nsd_coo_to_csr(3, 3, 4, row, col, val, nsd.NSD_DUP_SUM, *outs, ws) == 3
+
+
+def test_csc_and_mode_index_reject_out_of_range(nsd, operand):
+    """A column (or mode key) outside its range is refused, whichever
+    position holds it; the builders stay usable afterwards."""
+    n = 5000
+    ws = torch.empty(nsd.nsd_build_workspace_size(n, 64), dtype=torch.uint8, device="cuda")
+    i32 = lambda m: torch.empty(max(m, 1), dtype=torch.int32, device="cuda")  # noqa: E731
+    rng = np.random.default_rng(4)
+    for bad in (64, -1, 1 << 30):
+        for at in (0, 2047, n - 1):
+            key = rng.integers(0, 64, n).astype(np.int32)
+            key[at] = bad
+            with pytest.raises(nsd.NsdError) as e:
+                nsd.nsd_coo_mode_index(n, 64, dev(key), i32(65), i32(n), i32(n), ws)
+            assert e.value.status == nsd.NSD_ERR_BAD_FORMAT
+            rowptr = np.arange(0, n + 1, 5, dtype=np.int32)  # rows of 5 entries
+            colind = key.copy()
+            A = nsd.csr_desc(len(rowptr) - 1, 64, dev(rowptr),
+                             dev(np.repeat(np.arange(len(rowptr) - 1), 5).astype(np.int32)),
+                             dev(colind), dev(np.ones(n, np.float32)))
+            with pytest.raises(nsd.NsdError) as e:
+                nsd.nsd_csr_to_csc(A, i32(65), i32(n), i32(n), i32(n), ws)
+            assert e.value.status == nsd.NSD_ERR_BAD_FORMAT
+    key = rng.integers(0, 64, n).astype(np.int32)
+    segptr, segidx, perm = i32(65), i32(n), i32(n)
+    nsd.nsd_coo_mode_index(n, 64, dev(key), segptr, segidx, perm, ws)
+    assert np.array_equal(host(perm)[:n], np.argsort(key, kind="stable"))
 
 
 def test_mode_index_bit_exact(nsd, orc):
