@@ -131,6 +131,39 @@ def test_coo_to_csr_sums_duplicates(nsd, orc, seed):
     assert_mag_close(vout[:nuniq], val_r, mag, what="merged values")
 
 
+@pytest.mark.parametrize("nrows,ncols", [(1, 1), (3, 2), (1, 1 << 24), (1 << 21, 3),
+                                         (256, 256), (257, 255), (70_000, 65_536),
+                                         (1_000_003, 300_007), (1 << 20, (1 << 31) - 1)])
+def test_coo_to_csr_pair_key_widths(nsd, nrows, ncols):
+    """The sort by the pair (row, col) over the combined bits of both
+    coordinates (2 to 51 of them: digits straddling the two words, a last
+    pass of few bits) against a stable lexicographic sort, duplicates
+    merged."""
+    rng = np.random.default_rng(nrows ^ ncols)
+    n = 30_000
+    row = rng.integers(0, nrows, n).astype(np.int32)
+    col = rng.integers(0, ncols, n).astype(np.int32)
+    row[:50], col[:50] = nrows - 1, ncols - 1  # the largest coordinates, repeated
+    val = rng.standard_normal(n).astype(np.float32)
+    ws = torch.empty(nsd.nsd_build_workspace_size(n, max(nrows, ncols)), dtype=torch.uint8,
+                     device="cuda")
+    rowptr = torch.empty(nrows + 1, dtype=torch.int32, device="cuda")
+    out = [rowptr] + [torch.empty(n, dtype=t, device="cuda")
+                      for t in (torch.int32, torch.int32, torch.float32, torch.int32)]
+    m = nsd.nsd_coo_to_csr(nrows, ncols, n, dev(row), dev(col), dev(val), nsd.NSD_DUP_SUM, *out,
+                           ws)
+    order = np.lexsort((col, row))
+    r, c = row[order], col[order]
+    head = np.ones(n, bool)
+    head[1:] = (r[1:] != r[:-1]) | (c[1:] != c[:-1])
+    assert m == int(head.sum())
+    _, rowidx, colind, _, perm = [host(t) for t in out]
+    assert np.array_equal(rowidx[:m], r[head])
+    assert np.array_equal(colind[:m], c[head])
+    assert np.array_equal(perm[:m], order[head])
+    assert np.array_equal(host(rowptr), np.searchsorted(r[head], np.arange(nrows + 1)))
+
+
 def test_coo_to_csr_errors(nsd):
     row = dev(np.array([0, 1, 1, 2], np.int32))
     col = dev(np.array([0, 2, 2, 1], np.int32))
