@@ -31,6 +31,7 @@
 // sorting every term twice through HBM.
 #include <algorithm>
 #include <cstdlib>
+#include <cstring>
 
 #include "nsd_internal.hpp"
 
@@ -56,10 +57,18 @@ __global__ void pairs_total_kernel(int32_t nrows, const int32_t *rowptr,
         const unsigned long long len = (unsigned long long)(rowptr[i + 1] - rowptr[i]);
         v = len * len;
     }
-    // integer sums are exact in any order
+    // integer sums are exact in any order: the waves' sums, then one atomic
+    // per block
+    __shared__ unsigned long long part[kBataxThreads / kWave];
 #pragma unroll
     for (int m = kWave / 2; m >= 1; m >>= 1) v += __shfl_xor(v, m, kWave);
-    if ((threadIdx.x & (kWave - 1)) == 0 && v) atomicAdd(total, v);
+    if ((threadIdx.x & (kWave - 1)) == 0) part[threadIdx.x / kWave] = v;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned long long b = 0;
+        for (int w = 0; w < kBataxThreads / kWave; ++w) b += part[w];
+        if (b) atomicAdd(total, b);
+    }
 }
 
 // Term t of row i: the pair (p, q) = (u / len, u % len) of the row's
@@ -507,18 +516,24 @@ static nsd_status batax_by_rows(const nsd_csr *A, float beta, int64_t P, int cap
     int32_t *len = w.ridx;  // free once the sort has read it
     slot_len_kernel<<<bgrid(z), kBataxThreads, 0, st>>>(z, w.crow, A->rowptr, len);
     NSD_TRY(check_launch("slot_len_kernel"));
-    NSD_HIP(hipMemsetAsync(w.mx, 0, 2 * sizeof(int32_t), st));
+    // w.mx: [0] the most terms of a row of J, [1] the longest column of A,
+    // [2] the scan's (32-bit) total, [4..5] the products counted in 64 bits
+    auto *pairs = reinterpret_cast<unsigned long long *>(w.mx + 4);
+    NSD_HIP(hipMemsetAsync(w.mx, 0, 8 * sizeof(int32_t), st));
+    pairs_total_kernel<<<bgrid(m), kBataxThreads, 0, st>>>(m, A->rowptr, pairs);
+    NSD_TRY(check_launch("pairs_total_kernel"));
     NSD_TRY(scan_exclusive(len, len, z, w.mx + 2, w.scan_ws, st));
     row_terms_kernel<<<bgrid(n), kBataxThreads, 0, st>>>(n, z, w.colptr, len, w.mx + 2, w.toff,
                                                          w.mx);
     NSD_TRY(check_launch("row_terms_kernel"));
-    // the most terms of a row of J, the longest column of A, the products
-    int32_t mx[3] = {0, 0, 0};
+    int32_t mx[6] = {0, 0, 0, 0, 0, 0};
     NSD_HIP(hipMemcpyAsync(mx, w.mx, sizeof(mx), hipMemcpyDeviceToHost, st));
     NSD_HIP(hipStreamSynchronize(st));
-    if ((int64_t)mx[2] != P)
-        return fail(NSD_ERR_INVALID_ARG, "npairs = %lld, but A's rows give %d pairs",
-                    (long long)P, mx[2]);
+    unsigned long long np = 0;
+    std::memcpy(&np, mx + 4, sizeof(np));
+    if (np != (unsigned long long)P)
+        return fail(NSD_ERR_INVALID_ARG, "npairs = %lld, but A's rows give %llu pairs",
+                    (long long)P, np);
     if (mx[0] > cap) return NSD_OK;  // some row of J is too long: the sort path
     BataxRows a;
     a.ncols = n;
@@ -689,17 +704,22 @@ nsd_status nsd_batax_jacobian(const nsd_csr *A, float beta, int64_t npairs, int3
         NSD_TRY(batax_by_rows(A, beta, P, cap, rw, jrowptr, jcolind, jval, nnz_out, &done, st));
         if (done) return NSD_OK;
     }
+    if (cap == 0) {  // the products counted in 64 bits
+        auto *pairs = reinterpret_cast<unsigned long long *>(w.tot + 4);
+        NSD_HIP(hipMemsetAsync(pairs, 0, sizeof(*pairs), st));
+        pairs_total_kernel<<<bgrid(m), kBataxThreads, 0, st>>>(m, A->rowptr, pairs);
+        NSD_TRY(check_launch("pairs_total_kernel"));
+        unsigned long long np = 0;
+        NSD_HIP(hipMemcpyAsync(&np, pairs, sizeof(np), hipMemcpyDeviceToHost, st));
+        NSD_HIP(hipStreamSynchronize(st));
+        if (np != (unsigned long long)P)
+            return fail(NSD_ERR_INVALID_ARG, "npairs = %lld, but A's rows give %llu pairs",
+                        (long long)P, np);
+    }
+    // npairs is A's, below 2^30: every row's square and their sums fit int32
     row_pairs_kernel<<<bgrid(m), kBataxThreads, 0, st>>>(m, A->rowptr, w.sq);
     NSD_TRY(check_launch("row_pairs_kernel"));
     NSD_TRY(scan_exclusive(w.sq, w.off, m, w.tot, w.scan_ws, st));
-    if (cap == 0) {
-        int32_t hp = 0;
-        NSD_HIP(hipMemcpyAsync(&hp, w.tot, sizeof(hp), hipMemcpyDeviceToHost, st));
-        NSD_HIP(hipStreamSynchronize(st));
-        if ((int64_t)hp != P)
-            return fail(NSD_ERR_INVALID_ARG, "npairs = %lld, but A's rows give %d pairs",
-                        (long long)P, hp);
-    }
     expand_pairs_kernel<<<bgrid(P), kBataxThreads, 0, st>>>(P, m, w.off, A->rowptr, A->colind,
                                                             A->val, beta, w.key_j, w.key_k,
                                                             w.term);
