@@ -200,12 +200,25 @@ __global__ void row_terms_kernel(int32_t ncols, int32_t nnz, const int32_t *colp
         t = e - b;
         nr = c1 - c0;
     }
+    // the waves' maxima, then the block's, then one atomic each per block
+    // (atomics of every wave on the same two words serialise: 39 us for
+    // 100K columns)
+    __shared__ int32_t bt[kBataxThreads / kWave], bn[kBataxThreads / kWave];
 #pragma unroll
     for (int m = kWave / 2; m >= 1; m >>= 1) {
         t = max(t, __shfl_xor(t, m, kWave));
         nr = max(nr, __shfl_xor(nr, m, kWave));
     }
     if ((threadIdx.x & (kWave - 1)) == 0) {
+        bt[threadIdx.x / kWave] = t;
+        bn[threadIdx.x / kWave] = nr;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < kBataxThreads / kWave; ++w) {
+            t = max(t, bt[w]);
+            nr = max(nr, bn[w]);
+        }
         if (t > 0) atomicMax(mx, t);
         if (nr > 0) atomicMax(mx + 1, nr);
     }

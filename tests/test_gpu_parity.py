@@ -915,7 +915,7 @@ def many_rows_pattern(rng):
 
 
 @pytest.mark.parametrize("case", ["small_workload", "edge", "dense_row", "cap", "cap_plus_one",
-                                  "many_rows", "wide"])
+                                  "many_rows", "tall_column", "wide"])
 def test_batax_row_path_equals_sort_path(nsd, operand, orc, case):
     """J built row by row in LDS (when no row of J has more than 512 terms)
     and by the two global sorts (forced with NSD_BATAX_ROW_CAP=0): the same
@@ -937,6 +937,20 @@ def test_batax_row_path_equals_sort_path(nsd, operand, orc, case):
         # a row of J gathering 40 rows of A
         nrows, ncols, rowptr, colind, val = many_rows_pattern(rng)
         assert np.bincount(colind).max() == 40
+    elif case == "tall_column":
+        # column 5 stored by 150 short rows: a row of J gathering more rows
+        # of A than a wave has lanes (still at most 512 terms)
+        nrows, ncols = 300, 400
+        rows = []
+        for r in range(nrows):
+            c = rng.choice(np.arange(6, ncols), size=int(rng.integers(0, 3)), replace=False)
+            if r % 2 == 0:
+                c = np.concatenate([c, [5]])
+            rows.append(np.sort(c))
+        rowptr = np.concatenate([[0], np.cumsum([len(r) for r in rows])]).astype(np.int32)
+        colind = np.concatenate(rows).astype(np.int32)
+        val = rng.standard_normal(len(colind)).astype(np.float32)
+        assert np.bincount(colind)[5] == 150
     elif case == "wide":
         # 2^23 + 5 columns: the row path's 64-bit sort keys
         nrows, ncols = 300, (1 << 23) + 5
