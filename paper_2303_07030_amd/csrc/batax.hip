@@ -287,6 +287,37 @@ __device__ __forceinline__ void row_ce(Key &a, Key &b, bool up) {
     b = y;
 }
 
+// E consecutive keys at p (p aligned to E keys) in and out of LDS: whole
+// 16-byte words where the run holds some (one instruction per 16 bytes
+// instead of one per key).
+template <class Key, int E>
+__device__ __forceinline__ void load_run(const Key *p, Key (&v)[E]) {
+    if constexpr (E * sizeof(Key) % 16 == 0) {
+        constexpr int NV = E * (int)sizeof(Key) / 16;
+        uint4 w[NV];
+#pragma unroll
+        for (int i = 0; i < NV; ++i) w[i] = reinterpret_cast<const uint4 *>(p)[i];
+        __builtin_memcpy(v, w, sizeof(w));
+    } else {
+#pragma unroll
+        for (int m = 0; m < E; ++m) v[m] = p[m];
+    }
+}
+
+template <class Key, int E>
+__device__ __forceinline__ void store_run(Key *p, const Key (&v)[E]) {
+    if constexpr (E * sizeof(Key) % 16 == 0) {
+        constexpr int NV = E * (int)sizeof(Key) / 16;
+        uint4 w[NV];
+        __builtin_memcpy(w, v, sizeof(w));
+#pragma unroll
+        for (int i = 0; i < NV; ++i) reinterpret_cast<uint4 *>(p)[i] = w[i];
+    } else {
+#pragma unroll
+        for (int m = 0; m < E; ++m) p[m] = v[m];
+    }
+}
+
 // Substeps of bitonic stage `size` with strides 2^(lo + C - 1) down to 2^lo
 // in one pass over LDS: each lane holds the 2^C keys that those substeps
 // exchange among themselves (indices base + m 2^lo), so the C substeps
@@ -299,16 +330,24 @@ __device__ __forceinline__ void bitonic_group(Key *skey, int32_t np2, int32_t si
     for (int32_t t = l; t < (np2 >> C); t += kWave) {
         const int32_t base = ((t >> lo) << (lo + C)) | (t & ((1 << lo) - 1));
         Key v[E];
+        if (lo == 0) {  // the same for the whole wave: a contiguous run
+            load_run<Key, E>(skey + base, v);
+        } else {
 #pragma unroll
-        for (int m = 0; m < E; ++m) v[m] = skey[base + (m << lo)];
+            for (int m = 0; m < E; ++m) v[m] = skey[base + (m << lo)];
+        }
         const bool up = (base & size) == 0;
 #pragma unroll
         for (int b = C - 1; b >= 0; --b)
 #pragma unroll
             for (int m = 0; m < E; ++m)
                 if (!(m & (1 << b))) row_ce(v[m], v[m | (1 << b)], up);
+        if (lo == 0) {
+            store_run<Key, E>(skey + base, v);
+        } else {
 #pragma unroll
-        for (int m = 0; m < E; ++m) skey[base + (m << lo)] = v[m];
+            for (int m = 0; m < E; ++m) skey[base + (m << lo)] = v[m];
+        }
     }
     __syncwarp();  // this wave only
 }
@@ -321,8 +360,7 @@ __device__ __forceinline__ void bitonic_first8(Key *skey, int32_t np2, int l) {
     for (int32_t t = l; t < (np2 >> 3); t += kWave) {
         const int32_t base = t << 3;
         Key v[8];
-#pragma unroll
-        for (int m = 0; m < 8; ++m) v[m] = skey[base + m];
+        load_run<Key, 8>(skey + base, v);
 #pragma unroll
         for (int m = 0; m < 8; m += 2) row_ce(v[m], v[m + 1], (m & 2) == 0);
 #pragma unroll
@@ -338,8 +376,7 @@ __device__ __forceinline__ void bitonic_first8(Key *skey, int32_t np2, int l) {
             if (!(m & 2)) row_ce(v[m], v[m + 2], up);
 #pragma unroll
         for (int m = 0; m < 8; m += 2) row_ce(v[m], v[m + 1], up);
-#pragma unroll
-        for (int m = 0; m < 8; ++m) skey[base + m] = v[m];
+        store_run<Key, 8>(skey + base, v);
     }
     __syncwarp();  // this wave only
 }
