@@ -65,7 +65,7 @@ struct DualSlot {
         row = a.segidx[a0];
         carry = a0 > 0 && a.segidx[a0 - 1] == row;
         acc.zero();
-        if (kKeepOwn && on) ownv.load(m.own + (int64_t)row * k + col);
+        if (kKeepOwn && on) ownv.load_nt(m.own + (int64_t)row * k + col);
         else ownv.zero();
     }
 
@@ -75,7 +75,7 @@ struct DualSlot {
         } else if (on) {
             Vec<VEC> t = acc;
             t.scale(m.s.alpha);
-            t.store(m.s.out + (int64_t)row * k + col);
+            t.store_nt(m.s.out + (int64_t)row * k + col);  // written once
         }
     }
 
@@ -105,7 +105,7 @@ struct DualSlot {
             // segment that starts and ends inside the batch) loads its own
             const bool same = r[U - 1] == row;  // segments are sorted in an item
             Vec<VEC> ownn = ownv;
-            if (!same && on) ownn.load(m.own + (int64_t)r[U - 1] * k + col);
+            if (!same && on) ownn.load_nt(m.own + (int64_t)r[U - 1] * k + col);
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 if (!on) {

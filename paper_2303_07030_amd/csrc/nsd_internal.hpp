@@ -112,6 +112,22 @@ struct Vec<4> {
     __device__ __forceinline__ void store(float *p) const {
         *reinterpret_cast<float4 *>(p) = make_float4(v[0], v[1], v[2], v[3]);
     }
+    // Streamed data, read or written once (a segment's own row, its output
+    // row): non-temporal, so that it displaces less of what the L2 holds
+    // for reuse (the gathered rows).
+    __device__ __forceinline__ void load_nt(const float *p) {
+        typedef float f4 __attribute__((ext_vector_type(4)));
+        const f4 t = __builtin_nontemporal_load(reinterpret_cast<const f4 *>(p));
+        v[0] = t.x;
+        v[1] = t.y;
+        v[2] = t.z;
+        v[3] = t.w;
+    }
+    __device__ __forceinline__ void store_nt(float *p) const {
+        typedef float f4 __attribute__((ext_vector_type(4)));
+        const f4 t = {v[0], v[1], v[2], v[3]};
+        __builtin_nontemporal_store(t, reinterpret_cast<f4 *>(p));
+    }
     __device__ __forceinline__ void fma(float w, const Vec &x) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) v[i] = __builtin_fmaf(w, x.v[i], v[i]);
@@ -140,6 +156,8 @@ struct Vec<1> {
     __device__ __forceinline__ void ones() { v[0] = 1.f; }
     __device__ __forceinline__ void load(const float *p) { v[0] = *p; }
     __device__ __forceinline__ void store(float *p) const { *p = v[0]; }
+    __device__ __forceinline__ void load_nt(const float *p) { v[0] = __builtin_nontemporal_load(p); }
+    __device__ __forceinline__ void store_nt(float *p) const { __builtin_nontemporal_store(v[0], p); }
     __device__ __forceinline__ void fma(float w, const Vec &x) { v[0] = __builtin_fmaf(w, x.v[0], v[0]); }
     __device__ __forceinline__ void add(const Vec &x) { v[0] += x.v[0]; }
     __device__ __forceinline__ void scale(float a) { v[0] *= a; }
