@@ -518,7 +518,11 @@ def main():
 
     algo = S.kernels[dom]
     achieved = algo / (dom_ms * 1e-3) / 1e9
-    traffic = committed_traffic(dom, args.workload)
+    # the committed counters were taken on the workload's default inputs and
+    # arguments; any other configuration has none
+    default_config = (args.size == "full" and args.item_len is None and args.replicate == 0
+                      and args.tangents == 1 and not args.cp_fibers)
+    traffic = committed_traffic(dom, args.workload) if default_config else None
     roofline = {
         "bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
         "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
