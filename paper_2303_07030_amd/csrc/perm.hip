@@ -51,7 +51,12 @@ __device__ __forceinline__ int64_t xcd_contiguous_tile() {
 
 // Each thread handles kPermPer elements of its tile, strided by the block
 // size, in batches of kPermBatch whose loads are all issued before any is
-// used (one memory round trip per batch, not per element).
+// used (one memory round trip per batch, not per element).  Everything read
+// is read once and the result written once: those accesses are
+// non-temporal, leaving the L2 to the staging runs of pass 1, which meet
+// there with their neighbours' (measured on MI355X, a move of 60M values:
+// 0.310 ms with ordinary accesses, 0.266 ms so; the staging stores made
+// non-temporal as well, 0.433 ms).
 constexpr int kPermPer = kPermTile / kPermThreads;
 constexpr int kPermBatch = 8;
 static_assert(kPermPer % kPermBatch == 0, "whole batches per thread");
@@ -69,7 +74,7 @@ __global__ __launch_bounds__(kPermThreads) void perm_pass1_kernel(int64_t n, con
 #pragma unroll
         for (int u = 0; u < kPermBatch; ++u) {
             const int i = tid + (b + u) * kPermThreads;
-            v[u] = i < len ? src[t0 + i] : 0.f;
+            v[u] = i < len ? __builtin_nontemporal_load(src + t0 + i) : 0.f;
         }
 #pragma unroll
         for (int u = 0; u < kPermBatch; ++u) tile[tid + (b + u) * kPermThreads] = v[u];
@@ -81,8 +86,8 @@ __global__ __launch_bounds__(kPermThreads) void perm_pass1_kernel(int64_t n, con
 #pragma unroll
         for (int u = 0; u < kPermBatch; ++u) {
             const int o = tid + (b + u) * kPermThreads;
-            st[u] = o < len ? stage[t0 + o] : -1;
-            loc[u] = o < len ? src_local[t0 + o] : 0;
+            st[u] = o < len ? __builtin_nontemporal_load(stage + t0 + o) : -1;
+            loc[u] = o < len ? __builtin_nontemporal_load(src_local + t0 + o) : 0;
         }
 #pragma unroll
         for (int u = 0; u < kPermBatch; ++u)
@@ -104,8 +109,8 @@ __global__ __launch_bounds__(kPermThreads) void perm_pass2_kernel(int64_t n,
 #pragma unroll
         for (int u = 0; u < kPermBatch; ++u) {
             const int s = tid + (b + u) * kPermThreads;
-            v[u] = s < len ? staging[d0 + s] : 0.f;
-            loc[u] = s < len ? dst_local[d0 + s] : -1;
+            v[u] = s < len ? __builtin_nontemporal_load(staging + d0 + s) : 0.f;
+            loc[u] = s < len ? __builtin_nontemporal_load(dst_local + d0 + s) : -1;
         }
 #pragma unroll
         for (int u = 0; u < kPermBatch; ++u)
@@ -116,7 +121,7 @@ __global__ __launch_bounds__(kPermThreads) void perm_pass2_kernel(int64_t n,
 #pragma unroll
         for (int u = 0; u < kPermBatch; ++u) {
             const int i = tid + (b + u) * kPermThreads;
-            if (i < len) dst[d0 + i] = bucket[i];
+            if (i < len) __builtin_nontemporal_store(bucket[i], dst + d0 + i);
         }
     }
 }
